@@ -1,0 +1,383 @@
+"""Pins of the CPU oracle against things other than itself: hand-evaluated examples of the
+paper's definition, library routines (torch/scipy), brute force, closed forms, invariants,
+automatic differentiation and finite differences.  CPU only."""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import moe_oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _load(name):
+    with open(os.path.join(GOLDEN, name)) as fh:
+        return json.load(fh)
+
+
+# ---------------------------------------------------------------------------------------------
+# bf16 rounding
+# ---------------------------------------------------------------------------------------------
+def _torch_bf16(x32):
+    return torch.from_numpy(x32).to(torch.bfloat16).to(torch.float32).numpy().astype(np.float64)
+
+
+def test_bf16_round_matches_torch_random():
+    rng = np.random.default_rng(1)
+    x = (rng.standard_normal(200_000) * np.exp2(rng.integers(-140, 120, 200_000))).astype(np.float32)
+    np.testing.assert_array_equal(O.bf16_round(x.astype(np.float64)), _torch_bf16(x))
+
+
+def test_bf16_round_ties_and_edges():
+    # exact midpoints between neighbouring bf16 values, both parities, both signs, subnormals
+    base = np.array([1.0, 1.0 + 2**-7, 3.0, 1.5, 2.0**-126, 2.0**-130, 2.0**100], dtype=np.float64)
+    ulp = np.array([2**-7, 2**-7, 2**-6, 2**-7, 2**-133, 2**-133, 2.0**93])
+    mids = np.concatenate([base + ulp / 2, -(base + ulp / 2), base + ulp / 2 + ulp / 64])
+    x32 = mids.astype(np.float32)
+    assert np.array_equal(x32.astype(np.float64), mids)       # exact in fp32, so torch sees them
+    np.testing.assert_array_equal(O.bf16_round(mids), _torch_bf16(x32))
+    # closed forms: 1 + 2^-8 is a tie -> even neighbour 1.0; 1 + 3*2^-8 -> 1 + 2^-6
+    assert O.bf16_round(1 + 2**-8) == 1.0
+    assert O.bf16_round(1 + 3 * 2**-8) == 1 + 2**-6
+    assert O.bf16_round(1 + 2**-8 + 2**-30) == 1 + 2**-7
+    assert math.copysign(1.0, O.bf16_round(-0.0)) == -1.0
+    assert O.bf16_round(3.5e38) == np.inf and O.bf16_round(-3.5e38) == -np.inf
+    assert O.bf16_round(O.BF16_MAX) == O.BF16_MAX
+
+
+def test_bf16_bits_roundtrip():
+    rng = np.random.default_rng(2)
+    bits = rng.integers(0, 2**16, 5000, dtype=np.uint16)
+    bits = bits[(bits & 0x7F80) != 0x7F80]      # drop inf/nan patterns
+    vals = O.bf16_bits_to_f64(bits)
+    np.testing.assert_array_equal(O.f64_to_bf16_bits(vals), bits)
+    t = torch.from_numpy(bits.view(np.int16).copy()).view(torch.bfloat16).float().numpy()
+    np.testing.assert_array_equal(vals, t.astype(np.float64))
+
+
+# ---------------------------------------------------------------------------------------------
+# routing
+# ---------------------------------------------------------------------------------------------
+def test_route_permute_worked_example():
+    g = _load("route_permute_worked_example.json")
+    idx, w = O.route_topk(np.array(g["logits"], dtype=np.float32), g["k"])
+    np.testing.assert_array_equal(idx, g["topk_idx"])
+    np.testing.assert_allclose(w, g["topk_w"], rtol=1e-15, atol=0)
+    off, ros, tor = O.permute(idx, 4)
+    np.testing.assert_array_equal(off, g["offsets"])
+    np.testing.assert_array_equal(ros, g["row_of_slot"])
+    np.testing.assert_array_equal(tor, g["token_of_row"])
+
+
+@pytest.mark.parametrize("E,k", [(4, 1), (4, 2), (8, 3), (16, 16), (33, 5)])
+def test_route_brute_force_with_ties(E, k):
+    rng = np.random.default_rng(E * 100 + k)
+    T = 60
+    L = rng.integers(-3, 4, (T, E)).astype(np.float32)     # many exact ties
+    L[::7] = 0.0
+    L[1::11, 0] = -0.0                                      # -0 ties +0
+    idx, w = O.route_topk(L, k)
+    for t in range(T):
+        brute = sorted(range(E), key=lambda e: (-float(L[t, e]), e))[:k]
+        assert list(idx[t]) == brute
+    # softmax over the selected logits: weights sum to one, ratios follow exp of logit gaps,
+    # and equal logits share equal weight
+    np.testing.assert_allclose(w.sum(1), 1.0, rtol=1e-14)
+    sel = np.take_along_axis(L.astype(np.float64), idx, 1)
+    np.testing.assert_allclose(w[:, 1:] / w[:, :1], np.exp(sel[:, 1:] - sel[:, :1]), rtol=1e-13)
+
+
+def test_route_weights_library_softmax():
+    from scipy.special import softmax
+    rng = np.random.default_rng(3)
+    L = rng.standard_normal((50, 12)).astype(np.float32)
+    # k = E: the selected-k softmax is the full softmax, in descending-logit order
+    idx, w = O.route_topk(L, 12)
+    full = softmax(L.astype(np.float64), axis=1)
+    np.testing.assert_allclose(w, np.take_along_axis(full, idx, 1), rtol=1e-13)
+    # normalize=False: the full-softmax probability of each selected expert
+    idx3, w3 = O.route_topk(L, 3, normalize=False)
+    np.testing.assert_allclose(w3, np.take_along_axis(full, idx3, 1), rtol=1e-13)
+    # k = 1: weight exactly 1
+    _, w1 = O.route_topk(L, 1)
+    assert np.all(w1 == 1.0)
+
+
+# ---------------------------------------------------------------------------------------------
+# permutation
+# ---------------------------------------------------------------------------------------------
+def _check_permutation(idx, E, off, ros, tor):
+    T, k = idx.shape
+    R = T * k
+    counts = np.diff(off)
+    assert off[0] == 0 and off[-1] == R and np.all(counts >= 0)
+    assert np.array_equal(np.sort(ros), np.arange(R))                     # bijection
+    assert np.array_equal(tor[ros], np.arange(R) // k)                    # slot -> its token
+    for e in range(E):
+        rows = np.arange(off[e], off[e + 1])
+        slots = np.argsort(ros)[rows]
+        assert np.all(idx.reshape(-1)[slots] == e)                      # row in its expert's group
+        assert np.all(np.diff(tor[rows]) > 0)                            # ascending tokens
+        assert counts[e] == int((idx == e).sum())                        # count conservation
+
+
+@pytest.mark.parametrize("T,E,k", [(1, 1, 1), (5, 4, 4), (64, 8, 2), (300, 64, 6), (97, 256, 8)])
+def test_permute_invariants(T, E, k):
+    rng = np.random.default_rng(T + E + k)
+    L = rng.standard_normal((T, E)).astype(np.float32)
+    L[:, : E // 3] -= 1e4 if E > 3 else 0.0      # some experts never chosen (empty groups)
+    idx, _ = O.route_topk(L, k)
+    off, ros, tor = O.permute(idx, E)
+    _check_permutation(idx, E, off, ros, tor)
+
+
+def test_gather_combine_round_trip():
+    rng = np.random.default_rng(4)
+    T, d, E = 40, 16, 6
+    X = rng.integers(-8, 9, (T, d)).astype(np.float64)
+    for k in (1, 2, 3):
+        idx, _ = O.route_topk(rng.standard_normal((T, E)).astype(np.float32), k)
+        off, ros, tor = O.permute(idx, E)
+        xp = O.gather(X, tor)
+        back = O.combine(xp, None, ros, k)
+        np.testing.assert_array_equal(back, k * X)
+
+
+# ---------------------------------------------------------------------------------------------
+# grouped GEMMs
+# ---------------------------------------------------------------------------------------------
+def test_dw_worked_example():
+    g = _load("dw1_worked_example.json")
+    cum = np.array(g["cumsum_K"])
+    offsets = np.concatenate([[0], cum])
+    dw = O.grouped_gemm_dw(np.array(g["X"]), np.array(g["G"]), offsets)
+    np.testing.assert_array_equal(dw, np.array(g["dW1"]))
+
+
+def _small_int(rng, shape, lo=-2, hi=2):
+    return rng.integers(lo, hi + 1, shape).astype(np.float64)
+
+
+def test_grouped_gemms_exact_vs_torch():
+    """Small-integer operands make every product sum exact, so the oracle must equal torch's
+    per-group matmul bit for bit (non-square shapes catch transposed operands)."""
+    rng = np.random.default_rng(5)
+    counts = [3, 0, 7, 1, 12]
+    off = np.concatenate([[0], np.cumsum(counts)])
+    R, K, N, G = off[-1], 24, 40, len(counts)
+    A = _small_int(rng, (R, K))
+    B = _small_int(rng, (G, K, N))
+    B2 = _small_int(rng, (G, K, N))
+    dC = _small_int(rng, (R, N))
+    dC2 = _small_int(rng, (R, N))
+    tA, tB, tB2, tdC, tdC2 = (torch.from_numpy(v) for v in (A, B, B2, dC, dC2))
+    C = O.grouped_gemm(A, B, off)
+    dA = O.grouped_gemm_dx(dC, B, off, dC2, B2)
+    dB = O.grouped_gemm_dw(A, dC, off)
+    for g in range(G):
+        lo, hi = off[g], off[g + 1]
+        np.testing.assert_array_equal(C[lo:hi], torch.matmul(tA[lo:hi], tB[g]).numpy())
+        np.testing.assert_array_equal(
+            dA[lo:hi], (torch.matmul(tdC[lo:hi], tB[g].T) + torch.matmul(tdC2[lo:hi], tB2[g].T)).numpy())
+        np.testing.assert_array_equal(dB[g], torch.matmul(tA[lo:hi].T, tdC[lo:hi]).numpy())
+    assert np.all(dB[1] == 0)
+    # closed form: all-ones operands give K_g in every entry of dB[g]
+    ones = O.grouped_gemm_dw(np.ones((R, 3)), np.ones((R, 5)), off)
+    for g in range(G):
+        assert np.all(ones[g] == counts[g])
+
+
+def test_grouped_gemm_brute_force_loops():
+    rng = np.random.default_rng(6)
+    counts = [2, 3, 0, 1]
+    off = np.concatenate([[0], np.cumsum(counts)])
+    R, K, N = off[-1], 3, 5
+    A = rng.standard_normal((R, K))
+    B = rng.standard_normal((4, K, N))
+    C = O.grouped_gemm(A, B, off, rnd=None)
+    dB = O.grouped_gemm_dw(A, C, off)
+    for g in range(4):
+        for r in range(off[g], off[g + 1]):
+            for n in range(N):
+                assert abs(C[r, n] - sum(A[r, i] * B[g, i, n] for i in range(K))) < 1e-12
+        for i in range(K):
+            for n in range(N):
+                ref = sum(A[r, i] * C[r, n] for r in range(off[g], off[g + 1]))
+                assert abs(dB[g, i, n] - ref) < 1e-12
+
+
+# ---------------------------------------------------------------------------------------------
+# SwiGLU
+# ---------------------------------------------------------------------------------------------
+def test_swiglu_closed_forms_and_library():
+    g = np.array([0.0, 50.0, -50.0, 1.0, -1.0])
+    u = np.ones_like(g)
+    a = O.swiglu(g, u, rnd=None)
+    assert a[0] == 0.0 and abs(a[1] - 50.0) < 1e-12 and abs(a[2]) < 1e-12
+    rng = np.random.default_rng(7)
+    g = rng.standard_normal(1000) * 4
+    u = rng.standard_normal(1000)
+    ref = (torch.nn.functional.silu(torch.from_numpy(g)) * torch.from_numpy(u)).numpy()
+    np.testing.assert_allclose(O.swiglu(g, u, rnd=None), ref, rtol=1e-13, atol=1e-15)
+    # with bf16 storage the result is the bf16 rounding of the exact value
+    np.testing.assert_array_equal(O.swiglu(g, u), O.bf16_round(O.swiglu(g, u, rnd=None)))
+
+
+def test_swiglu_bwd_autograd():
+    rng = np.random.default_rng(8)
+    g = torch.from_numpy(rng.standard_normal(500) * 3).requires_grad_()
+    u = torch.from_numpy(rng.standard_normal(500)).requires_grad_()
+    da = torch.from_numpy(rng.standard_normal(500))
+    (torch.nn.functional.silu(g) * u).backward(da)
+    dhg, dhu = O.swiglu_bwd(g.detach().numpy(), u.detach().numpy(), da.numpy(), rnd=None)
+    np.testing.assert_allclose(dhg, g.grad.numpy(), rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(dhu, u.grad.numpy(), rtol=1e-12, atol=1e-14)
+    # closed form: sigmoid'(x) = s (1 - s) at 0 gives d/dg silu = 1/2
+    dg0, _ = O.swiglu_bwd(np.array([0.0]), np.array([1.0]), np.array([1.0]), rnd=None)
+    assert dg0[0] == 0.5
+
+
+# ---------------------------------------------------------------------------------------------
+# whole layer: dense special case, brute-force masked dense, autograd, finite differences
+# ---------------------------------------------------------------------------------------------
+def _tiny_layer(rng, T=24, d=16, f=20, E=5, k=2, shared_f=0, scale=0.3):
+    x = rng.standard_normal((T, d))
+    logits = rng.standard_normal((T, E)).astype(np.float32)
+    wg = rng.standard_normal((E, d, f)) * scale
+    wu = rng.standard_normal((E, d, f)) * scale
+    wd = rng.standard_normal((E, f, d)) * scale
+    dy = rng.standard_normal((T, d))
+    shared = None
+    if shared_f:
+        shared = (rng.standard_normal((d, shared_f)) * scale, rng.standard_normal((d, shared_f)) * scale,
+                  rng.standard_normal((shared_f, d)) * scale)
+    return x, logits, wg, wu, wd, dy, shared
+
+
+def _torch_masked_dense(x, logits, wg, wu, wd, k, shared):
+    """Every expert on every token, weighted by the routing weight (0 where not selected)."""
+    T, E = logits.shape
+    idx, w = O.route_topk(logits, k)      # routing is pinned separately; used as a fixed input
+    wfull = np.zeros((T, E))
+    np.put_along_axis(wfull, idx, w, 1)
+    y = 0
+    for e in range(E):
+        h = torch.nn.functional.silu(x @ wg[e]) * (x @ wu[e])
+        y = y + torch.from_numpy(wfull[:, e:e + 1]) * (h @ wd[e])
+    if shared is not None:
+        y = y + (torch.nn.functional.silu(x @ shared[0]) * (x @ shared[1])) @ shared[2]
+    return y
+
+
+@pytest.mark.parametrize("shared_f", [0, 12])
+def test_layer_forward_vs_brute_force(shared_f):
+    rng = np.random.default_rng(9 + shared_f)
+    x, logits, wg, wu, wd, dy, shared = _tiny_layer(rng, shared_f=shared_f)
+    fwd = O.layer_forward(x, logits, wg, wu, wd, 2, shared=shared, rnd=None)
+    tsh = None if shared is None else tuple(torch.from_numpy(s) for s in shared)
+    ref = _torch_masked_dense(torch.from_numpy(x), logits, torch.from_numpy(wg), torch.from_numpy(wu),
+                              torch.from_numpy(wd), 2, tsh)
+    np.testing.assert_allclose(fwd["y"], ref.numpy(), rtol=1e-11, atol=1e-12)
+    # with bf16 storage: within a few bf16 ulps of the exact layer output
+    fb = O.layer_forward(x, logits, wg, wu, wd, 2, shared=shared)
+    assert O.rel_fro(fb["y"], ref.numpy()) < 1e-2
+
+
+def test_layer_single_expert_is_dense_ffn():
+    rng = np.random.default_rng(10)
+    x, logits, wg, wu, wd, dy, _ = _tiny_layer(rng, E=1, k=1)
+    x = O.bf16_round(x)
+    wg, wu, wd = (O.bf16_round(w) for w in (wg, wu, wd))
+    fwd = O.layer_forward(x, logits, wg, wu, wd, 1)
+    # torch CPU fp32 dense FFN with bf16 rounding at the same stores
+    tb = lambda t: t.to(torch.bfloat16).to(torch.float32)
+    xt = torch.from_numpy(x).float()
+    hg = tb(xt @ torch.from_numpy(wg[0]).float())
+    hu = tb(xt @ torch.from_numpy(wu[0]).float())
+    a = tb(torch.nn.functional.silu(hg) * hu)
+    y = tb(a @ torch.from_numpy(wd[0]).float())
+    assert np.all(fwd["topk_w"] == 1.0) and np.all(fwd["topk_idx"] == 0)
+    assert O.rel_fro(fwd["y"], y.numpy()) < 1e-2
+    assert O.rel_fro(fwd["act"], a.numpy()) < 1e-2
+
+
+@pytest.mark.parametrize("shared_f", [0, 12])
+def test_layer_backward_vs_autograd(shared_f):
+    rng = np.random.default_rng(11 + shared_f)
+    k = 2
+    x, logits, wg, wu, wd, dy, shared = _tiny_layer(rng, shared_f=shared_f)
+    fwd = O.layer_forward(x, logits, wg, wu, wd, k, shared=shared, rnd=None)
+    bwd = O.layer_backward(fwd, x, dy, wg, wu, wd, shared=shared, rnd=None)
+
+    tx, twg, twu, twd = (torch.from_numpy(v).requires_grad_() for v in (x, wg, wu, wd))
+    tsh = None if shared is None else tuple(torch.from_numpy(s).requires_grad_() for s in shared)
+    # routing weights as a differentiable input to get d_topk_w
+    idx, w = O.route_topk(logits, k)
+    tw = torch.from_numpy(w).requires_grad_()
+    T, E = logits.shape
+    y = 0
+    for e in range(E):
+        h = torch.nn.functional.silu(tx @ twg[e]) * (tx @ twu[e])
+        sel = torch.from_numpy((idx == e).astype(np.float64))
+        y = y + (tw * sel).sum(1, keepdim=True) * (h @ twd[e])
+    if tsh is not None:
+        y = y + (torch.nn.functional.silu(tx @ tsh[0]) * (tx @ tsh[1])) @ tsh[2]
+    y.backward(torch.from_numpy(dy))
+    tol = dict(rtol=1e-10, atol=1e-11)
+    np.testing.assert_allclose(bwd["dx"], tx.grad.numpy(), **tol)
+    np.testing.assert_allclose(bwd["dw_gate"], twg.grad.numpy(), **tol)
+    np.testing.assert_allclose(bwd["dw_up"], twu.grad.numpy(), **tol)
+    np.testing.assert_allclose(bwd["dw_down"], twd.grad.numpy(), **tol)
+    np.testing.assert_allclose(bwd["d_topk_w"], tw.grad.numpy(), **tol)
+    if tsh is not None:
+        for key, t in zip(("dw_gate", "dw_up", "dw_down"), tsh):
+            np.testing.assert_allclose(bwd["shared"][key], t.grad.numpy(), **tol)
+
+
+def test_layer_backward_finite_differences():
+    rng = np.random.default_rng(12)
+    k = 2
+    x, logits, wg, wu, wd, dy, shared = _tiny_layer(rng, T=10, d=8, f=6, E=3, shared_f=4)
+    loss = lambda x_, wg_, wd_: float((O.layer_forward(x_, logits, wg_, wu, wd_, k, shared=shared,
+                                                       rnd=None)["y"] * dy).sum())
+    fwd = O.layer_forward(x, logits, wg, wu, wd, k, shared=shared, rnd=None)
+    bwd = O.layer_backward(fwd, x, dy, wg, wu, wd, shared=shared, rnd=None)
+    h = 1e-6
+    for (arr, grad, pos) in ((x, bwd["dx"], (3, 5)), (wg, bwd["dw_gate"], (fwd["topk_idx"][0, 0], 2, 4)),
+                             (wd, bwd["dw_down"], (fwd["topk_idx"][1, 1], 1, 7))):
+        p, m = arr.copy(), arr.copy()
+        p[pos] += h
+        m[pos] -= h
+        args_p = [x, wg, wd]
+        args_m = [x, wg, wd]
+        which = 0 if arr is x else (1 if arr is wg else 2)
+        args_p[which], args_m[which] = p, m
+        fd = (loss(*args_p) - loss(*args_m)) / (2 * h)
+        assert abs(fd - grad[pos]) < 1e-6 * max(1.0, abs(fd))
+
+
+def test_sampled_helpers_match_full_oracle():
+    rng = np.random.default_rng(13)
+    k = 2
+    x, logits, wg, wu, wd, dy, _ = _tiny_layer(rng, T=40, d=16, f=24, E=4)
+    x, wg, wu, wd, dy = (O.bf16_round(v) for v in (x, wg, wu, wd, dy))
+    fwd = O.layer_forward(x, logits, wg, wu, wd, k)
+    bwd = O.layer_backward(fwd, x, dy, wg, wu, wd)
+    off = fwd["offsets"]
+    e = int(np.argmax(np.diff(off)))
+    lo, hi = off[e], off[e + 1]
+    rows = np.arange(lo, hi)[::3]
+    hg, hu, a, yp = O.expert_rows_forward(fwd["x_perm"][rows], wg[e], wu[e], wd[e])
+    np.testing.assert_array_equal(yp, fwd["y_perm"][rows])
+    da, dhg, dhu, dxp = O.expert_rows_backward(hg, hu, bwd["dy_perm"][rows], wg[e], wu[e], wd[e])
+    np.testing.assert_array_equal(dxp, bwd["dx_perm"][rows])
+    cols = np.array([0, 5, 23])
+    np.testing.assert_allclose(O.dw_down_rows(fwd["x_perm"][lo:hi], bwd["dy_perm"][lo:hi], wg[e], wu[e], cols),
+                               bwd["dw_down"][e][cols], rtol=1e-12)
+    dwg, dwu = O.dw_gate_up_cols(fwd["x_perm"][lo:hi], bwd["dy_perm"][lo:hi], wg[e], wu[e], wd[e], cols)
+    np.testing.assert_allclose(dwg, bwd["dw_gate"][e][:, cols], rtol=1e-12)
+    np.testing.assert_allclose(dwu, bwd["dw_up"][e][:, cols], rtol=1e-12)

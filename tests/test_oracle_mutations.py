@@ -1,0 +1,136 @@
+"""Planted mistakes in the oracle (on the CPU only): each plausible mistake must make at least one
+of the oracle's pins fail, which shows the pins constrain every part of it."""
+import numpy as np
+import pytest
+
+from oracle import moe_oracle as O
+from tests import test_oracle as P
+
+PINS = [
+    P.test_bf16_round_matches_torch_random,
+    P.test_bf16_round_ties_and_edges,
+    P.test_route_permute_worked_example,
+    lambda: P.test_route_brute_force_with_ties(8, 3),
+    P.test_route_weights_library_softmax,
+    lambda: P.test_permute_invariants(64, 8, 2),
+    P.test_gather_combine_round_trip,
+    P.test_dw_worked_example,
+    P.test_grouped_gemms_exact_vs_torch,
+    P.test_grouped_gemm_brute_force_loops,
+    P.test_swiglu_closed_forms_and_library,
+    P.test_swiglu_bwd_autograd,
+    lambda: P.test_layer_forward_vs_brute_force(12),
+    P.test_layer_single_expert_is_dense_ffn,
+    lambda: P.test_layer_backward_vs_autograd(12),
+    P.test_layer_backward_finite_differences,
+]
+
+
+def _gg(A, B, offsets, rnd=O.bf16_round):                      # wrong expert's weights
+    A = np.asarray(A, dtype=np.float64)
+    G = B.shape[0]
+    C = np.zeros((A.shape[0], B.shape[2]))
+    for g in range(G):
+        lo, hi = int(offsets[g]), int(offsets[g + 1])
+        C[lo:hi] = A[lo:hi] @ B[(g + 1) % G]
+    return O._r(rnd, C)
+
+
+def _dw_drop_last(A, dC, offsets, G=None):                      # ragged bound off by one
+    G = len(offsets) - 1 if G is None else G
+    out = np.zeros((G, A.shape[1], dC.shape[1]))
+    for g in range(G):
+        lo, hi = int(offsets[g]), int(offsets[g + 1])
+        if hi - 1 > lo:
+            out[g] = np.asarray(A[lo:hi - 1]).T @ np.asarray(dC[lo:hi - 1])
+    return out
+
+
+def _dx_b_twice(dC, B, offsets, dC2=None, B2=None, rnd=O.bf16_round):   # second pair uses B
+    return O.__dict__["_orig_dx"](dC, B, offsets, dC2, B if B2 is not None else None, rnd)
+
+
+def _swiglu_bwd_dropped(h_gate, h_up, d_act, rnd=O.bf16_round):         # dropped term
+    s = O.sigmoid(h_gate)
+    return O._r(rnd, d_act * h_up * s), O._r(rnd, d_act * h_gate * s)
+
+
+def _swiglu_bwd_sign(h_gate, h_up, d_act, rnd=O.bf16_round):            # wrong sign
+    g, u, da = (np.asarray(v, dtype=np.float64) for v in (h_gate, h_up, d_act))
+    s = O.sigmoid(g)
+    return O._r(rnd, da * u * s * (1.0 - g * (1.0 - s))), O._r(rnd, da * g * s)
+
+
+def _combine_bwd_unweighted(dy, topk_w, row_of_slot, y_perm, k, rnd=O.bf16_round):
+    return O.__dict__["_orig_cb"](dy, None, row_of_slot, y_perm, k, rnd)
+
+
+def _route_ties_high(logits, k, normalize=True):                        # ties -> higher id
+    L = np.asarray(logits, dtype=np.float64)
+    T, E = L.shape
+    ids = np.broadcast_to(np.arange(E), (T, E))
+    idx = np.lexsort((-ids, -L), axis=-1)[:, :k]
+    sel = np.take_along_axis(L, idx, 1)
+    ex = np.exp(sel - sel[:, :1])
+    return idx, ex / ex.sum(1, keepdims=True)
+
+
+def _permute_desc(topk_idx, E):                                          # wrong in-group order
+    off, ros, tor = O.__dict__["_orig_perm"](topk_idx, E)
+    ros2 = ros.copy()
+    for e in range(E):
+        lo, hi = off[e], off[e + 1]
+        sel = (ros >= lo) & (ros < hi)
+        ros2[sel] = lo + hi - 1 - ros[sel]
+    tor2 = np.empty_like(tor)
+    tor2[ros2] = np.arange(len(ros2)) // topk_idx.shape[1]
+    return off, ros2, tor2
+
+
+def _bf16_truncate(x):                                                   # truncation, not RNE
+    x = np.asarray(x, dtype=np.float64)
+    b = x.astype(np.float32).view(np.uint32) & np.uint32(0xFFFF0000)
+    return b.view(np.float32).astype(np.float64)
+
+
+def _combine_weighted_add(y_perm, topk_w, row_of_slot, k, add=None, rnd=O.bf16_round):
+    out = O.__dict__["_orig_comb"](y_perm, topk_w, row_of_slot, k, None, None)
+    if add is not None:
+        out = out + 0.5 * np.asarray(add)
+    return O._r(rnd, out)
+
+
+MUTANTS = {
+    "grouped_gemm wrong expert": ("grouped_gemm", _gg),
+    "dw ragged bound off by one": ("grouped_gemm_dw", _dw_drop_last),
+    "dx second pair uses first weights": ("grouped_gemm_dx", _dx_b_twice),
+    "swiglu_bwd dropped term": ("swiglu_bwd", _swiglu_bwd_dropped),
+    "swiglu_bwd sign": ("swiglu_bwd", _swiglu_bwd_sign),
+    "combine_bwd unweighted": ("combine_bwd", _combine_bwd_unweighted),
+    "route ties to higher id": ("route_topk", _route_ties_high),
+    "permute descending tokens": ("permute", _permute_desc),
+    "bf16 truncation": ("bf16_round", _bf16_truncate),
+    "combine weights the shared add": ("combine", _combine_weighted_add),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_planted_mistake_is_caught(name, monkeypatch):
+    attr, fn = MUTANTS[name]
+    monkeypatch.setitem(O.__dict__, "_orig_dx", O.grouped_gemm_dx)
+    monkeypatch.setitem(O.__dict__, "_orig_cb", O.combine_bwd)
+    monkeypatch.setitem(O.__dict__, "_orig_perm", O.permute)
+    monkeypatch.setitem(O.__dict__, "_orig_comb", O.combine)
+    monkeypatch.setattr(O, attr, fn)
+    if attr == "bf16_round":
+        # default arguments captured the original function; patch the module-level users too
+        monkeypatch.setattr(O, "_r", lambda rnd, x: x if rnd is None else _bf16_truncate(x))
+    failures = 0
+    for pin in PINS:
+        try:
+            pin()
+        except AssertionError:
+            failures += 1
+        except (ValueError, IndexError):
+            failures += 1
+    assert failures > 0, f"no pin caught the planted mistake '{name}'"
