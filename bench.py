@@ -1,0 +1,174 @@
+"""Benchmark of the MoE expert-FFN training layer (forward + backward) on one MI355X.
+
+python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1] [--no-cpu-baseline]
+
+A step is one forward and one backward pass of the whole layer (routing, permutation, gather,
+gate/up grouped GEMM with fused SwiGLU, down grouped GEMM, combine, and the backward dX/dW grouped
+GEMMs, SwiGLU backward, combine backward and dX unpermute) over one batch of synthetic tokens
+whose inputs already sit in HBM.  Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+METRIC = "MoE layer fwd+bwd tokens/sec + grouped-GEMM TFLOP/s (% of bf16 MFMA peak), 1 GPU"
+
+
+def _args():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=1)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-tokens", type=int, default=0)
+    ap.add_argument("--no-trace", action="store_true", help="no per-call events inside the timed region")
+    return ap.parse_args()
+
+
+def cpu_baseline(cfg, inp, sample_tokens):
+    """The CPU oracle (float64 numpy, as it stands) on a bounded sample of the same workload: the
+    full layer forward+backward over the first `sample_tokens` tokens with all experts."""
+    import numpy as np
+
+    from oracle import moe_oracle as O
+    f = lambda t: t.float().cpu().numpy().astype(np.float64)
+    Ts = sample_tokens
+    x, dy = f(inp["x"][:Ts]), f(inp["dy"][:Ts])
+    logits = inp["logits"][:Ts].cpu().numpy()
+    wg, wu, wd = f(inp["w_gate"]), f(inp["w_up"]), f(inp["w_down"])
+    shared = None
+    if cfg.f_shared:
+        shared = (f(inp["w_gate_sh"]), f(inp["w_up_sh"]), f(inp["w_down_sh"]))
+    try:
+        import threadpoolctl
+        info = threadpoolctl.threadpool_info()
+        cores = max((i.get("num_threads", 1) for i in info), default=1)
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    t0 = time.perf_counter()
+    fwd = O.layer_forward(x, logits, wg, wu, wd, cfg.k, shared=shared)
+    O.layer_backward(fwd, x, dy, wg, wu, wd, shared=shared)
+    dt = time.perf_counter() - t0
+    return {"value": Ts / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"full layer fwd+bwd (float64 numpy oracle) on the first {Ts} of {cfg.T} tokens, "
+                      f"all {cfg.E} experts, {dt:.1f} s"}
+
+
+def main():
+    a = _args()
+    if a.gpus != 1:
+        print(f"bench.py measures one GPU only (--gpus {a.gpus} requested): this build has no "
+              f"multi-GPU path; run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2606_26453_amd import layer as L
+    from paper_2606_26453_amd import workloads as W
+
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    cfg = W.CONFIGS[a.config]
+    t_gen = time.perf_counter()
+    if cfg.dw_only:
+        inp = W.make_dw_inputs(cfg, a.seed, dev)
+        lay = L.DWOnly(cfg, inp)
+    else:
+        inp = W.make_inputs(cfg, a.seed, dev)
+        lay = L.MoELayer(cfg, inp)
+    torch.cuda.synchronize()
+    t_gen = time.perf_counter() - t_gen
+
+    stream = torch.cuda.current_stream()
+    for _ in range(a.warmup):
+        lay.step()
+    torch.cuda.synchronize()
+
+    lay.trace = None if a.no_trace else []
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for _ in range(a.steps):
+        lay.step()
+    end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    ms_per_step = total_ms / a.steps
+
+    # per-call averages over the timed region
+    per = {}
+    for name, e0, e1 in (lay.trace or []):
+        per.setdefault(name, []).append(e0.elapsed_time(e1))
+    work = lay.work()
+    calls = {}
+    gemm_ms = gemm_flops = 0.0
+    for name, ts in per.items():
+        avg = sum(ts) / len(ts)
+        kind, amount = work[name]
+        rec = {"ms": round(avg, 4)}
+        if kind == "flops":
+            rec["tflops"] = round(amount / avg / 1e9, 1)
+            rec["frac_peak"] = round(amount / avg / 1e9 / PEAK_BF16_TFLOPS, 4)
+            gemm_ms += avg
+            gemm_flops += amount
+        else:
+            rec["gbs"] = round(amount / avg / 1e6, 1)
+            rec["frac_peak"] = round(amount / avg / 1e6 / PEAK_HBM_GBS, 4)
+        calls[name] = rec
+
+    roofline = None
+    if per:
+        dom = max(per, key=lambda n: sum(per[n]))
+        kind, amount = work[dom]
+        avg = sum(per[dom]) / len(per[dom])
+        if kind == "flops":
+            ach = amount / avg / 1e9
+            roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 1), "peak": PEAK_BF16_TFLOPS,
+                        "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                        "work_per_launch": amount, "avg_launch_ms": round(avg, 4)}
+        else:
+            ach = amount / avg / 1e6
+            roofline = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
+                        "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None,
+                        "work_per_launch": amount, "avg_launch_ms": round(avg, 4)}
+
+    tokens = cfg.T
+    value = tokens * a.steps / (total_ms / 1e3)
+    offs = (inp["offsets"] if cfg.dw_only else lay.buf["offsets"]).cpu().tolist()
+    counts = [offs[i + 1] - offs[i] for i in range(len(offs) - 1)]
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) activations, N(0,0.02) weights, router logits X.Wr)",
+        "config": {"workload": f"config {a.config}: {cfg.name} MoE FFN layer fwd+bwd" if not cfg.dw_only
+                   else f"config {a.config}: {cfg.name} dW grouped GEMMs",
+                   "T": cfg.T, "d": cfg.d, "f": cfg.f, "E": cfg.E, "k": cfg.k, "f_shared": cfg.f_shared,
+                   "parallelism": "single GPU"},
+        "gemm_tflops": round(gemm_flops / gemm_ms / 1e9, 1) if gemm_ms else None,
+        "gemm_frac_peak": round(gemm_flops / gemm_ms / 1e9 / PEAK_BF16_TFLOPS, 4) if gemm_ms else None,
+        "gemm_tflops_step": round(cfg.gemm_flops() / (ms_per_step / 1e3) / 1e12, 1),
+        "calls": calls,
+        "roofline": roofline,
+        "groups": W.group_stats(counts),
+        "input_gen_s": round(t_gen, 1),
+    }
+    if not a.no_cpu_baseline and not cfg.dw_only:
+        ts = a.cpu_sample_tokens or max(8, min(cfg.T, int(2e11 // (18 * cfg.k * cfg.d * cfg.f))))
+        out["cpu_baseline"] = cpu_baseline(cfg, inp, ts)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,190 @@
+/*
+ * moe.h - C ABI of the MI355X (gfx950) MoE expert-FFN training layer library (libmoe_mi355x.so).
+ *
+ * The layer: top-k routing of T tokens over E experts, packing of the T*k routed rows into one
+ * buffer ordered by expert, bf16 grouped GEMMs over the ragged per-expert row groups (gate/up
+ * with a fused SwiGLU, then down), a weighted combine back to token order, and the backward
+ * dX/dW grouped GEMMs.  The paper (section 5.4; Appendix H, "What the kernel computes") defines
+ * the packed expert-ordered buffer, the cumulative per-expert row counts and the ragged weight
+ * gradient dW1_e = X_e^T G_e; the other steps follow the standard MoE layer, with the readings
+ * stated at each function below.
+ *
+ * Conventions shared by every entry point
+ *  - All tensor pointers are DEVICE pointers, owned and allocated by the caller; the library
+ *    allocates nothing and keeps no state between calls apart from cached device properties.
+ *  - Tensors are dense row-major (C order) with the shapes given in brackets.
+ *  - bf16 tensors are passed as moe_bf16 (the IEEE bfloat16 bit pattern in a uint16_t).
+ *  - Floating-point results are computed with fp32 arithmetic (MFMA fp32 accumulation for the
+ *    GEMMs) and rounded to bf16 with round-to-nearest-even where a bf16 tensor is stored.
+ *  - Row groups are given by exclusive offsets: int32 offsets[G+1], offsets[0] = 0,
+ *    offsets[G] = R, group g = rows offsets[g] <= r < offsets[g+1] (offsets[g+1] is the paper's
+ *    inclusive cumulative sum cumsum_K[g]).  offsets must be non-decreasing; this is NOT checked
+ *    (it lives in device memory and the calls never synchronize).
+ *  - Every call is asynchronous on `stream` (NULL = the default stream), performs no host/device
+ *    synchronization and no allocation.  Arguments are validated on the host before anything is
+ *    launched; an invalid call returns an error status and launches nothing.  Faults inside a
+ *    kernel surface at the caller's next synchronization.
+ *  - Shape limits: 1 <= k <= E <= 256; hidden and FFN widths (d, f, and the GEMMs' K and N) are
+ *    positive multiples of 64; R = T*k < 2^31; device pointers 16-byte aligned.  T = 0 / R = 0
+ *    is a successful no-op, except that moe_grouped_gemm_dw still writes its zero output.
+ *  - Outputs must not alias inputs.
+ */
+#ifndef MOE_MI355X_H
+#define MOE_MI355X_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef uint16_t moe_bf16;
+
+typedef enum {
+  MOE_SUCCESS = 0,
+  MOE_ERROR_INVALID_VALUE = 1, /* null or misaligned pointer, negative size, k > E, ...      */
+  MOE_ERROR_NOT_SUPPORTED = 2, /* a size outside the limits above (E > 256, d % 64 != 0, ...) */
+  MOE_ERROR_WORKSPACE = 3,     /* workspace missing or smaller than the query says            */
+  MOE_ERROR_HIP = 4            /* a HIP runtime call (launch, device query) failed             */
+} moe_status;
+
+/* Static description of a status code. */
+const char* moe_status_string(moe_status s);
+
+/* Detail of the last error returned on the calling host thread ("" if none). */
+const char* moe_last_error(void);
+
+/* ------------------------------------------------------------------------------------------ */
+/* A1-A4: routing, grouping, permutation and gather                                           */
+/* ------------------------------------------------------------------------------------------ */
+
+/* Bytes of device workspace moe_route_permute needs for these sizes (0 if none). */
+size_t moe_route_permute_workspace_bytes(int64_t T, int32_t E, int32_t k);
+
+/*
+ * Top-k routing and packing of the routed rows by expert (section 5.4: top-k routing;
+ * Appendix H: routed tokens packed into one contiguous buffer ordered by expert, groups given by
+ * cumulative per-expert counts).  The paper fixes neither the routing rule nor the order inside a
+ * group; this library reads them as:
+ *   - topk_idx[t, 0..k-1]: the k experts with the largest logits[t, :], by descending logit,
+ *     equal logits ordered by ascending expert id (exact: selection compares the fp32 logits);
+ *   - topk_w[t, j] = exp(l_j - l_0) / sum_{j'<k} exp(l_j' - l_0) over the selected logits
+ *     (normalize_topk = 1), or the softmax probability over all E experts (normalize_topk = 0);
+ *   - slot s = t*k + j; offsets = exclusive prefix sum of per-expert slot counts;
+ *     row_of_slot[s] = offsets[e] + (number of slots s' < s routed to the same expert e), so
+ *     each group keeps ascending token order (a stable counting sort);
+ *     token_of_row[row_of_slot[s]] = s / k;
+ *   - x_perm[r, :] = x[token_of_row[r], :] (bit copy) when x and x_perm are non-NULL.
+ * logits [T,E] fp32; x [T,d] bf16 or NULL; topk_idx [T,k] int32; topk_w [T,k] fp32;
+ * offsets [E+1] int32; row_of_slot [T*k] int32; token_of_row [T*k] int32; x_perm [T*k,d] bf16 or
+ * NULL.  workspace: device scratch of at least moe_route_permute_workspace_bytes(T, E, k) bytes,
+ * contents on entry ignored.  Results are deterministic and bit-exact (no order-dependent
+ * atomics).  NaN logits are not supported.
+ */
+moe_status moe_route_permute(const float* logits, const moe_bf16* x, int64_t T, int64_t d,
+                             int32_t E, int32_t k, int32_t normalize_topk, int32_t* topk_idx,
+                             float* topk_w, int32_t* offsets, int32_t* row_of_slot,
+                             int32_t* token_of_row, moe_bf16* x_perm, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------------------------ */
+/* B, D: forward grouped GEMM (+ fused SwiGLU)                                                 */
+/* ------------------------------------------------------------------------------------------ */
+
+/*
+ * Grouped GEMM over ragged row groups: C[r, :] = bf16(A[r, :] . B[g]) for rows r of group g.
+ * With B2 != NULL (gate/up in one pass sharing the A tiles): C2[r, :] = bf16(A[r, :] . B2[g]),
+ * and if act != NULL also act[r, c] = bf16(silu(C[r,c]) * C2[r,c]) computed in fp32 from the
+ * bf16-rounded C and C2 (silu(g) = g / (1 + exp(-g)); plain SwiGLU, the paper leaves the
+ * activation open).
+ * A [R,K] bf16; B, B2 [G,K,N] bf16; offsets [G+1]; C, C2, act [R,N] bf16.  K, N multiples of 64.
+ * C is required; C2 is required iff B2 is given; act requires B2.
+ */
+moe_status moe_grouped_gemm_fwd(const moe_bf16* A, const moe_bf16* B, const moe_bf16* B2,
+                                const int32_t* offsets, int32_t G, int64_t R, int64_t K,
+                                int64_t N, moe_bf16* C, moe_bf16* C2, moe_bf16* act,
+                                hipStream_t stream);
+
+/* ------------------------------------------------------------------------------------------ */
+/* C, I: SwiGLU and its backward (standalone elementwise kernels)                               */
+/* ------------------------------------------------------------------------------------------ */
+
+/* act = bf16(silu(h_gate) * h_up), elementwise over [rows, f] bf16 (the same arithmetic as the
+ * fused epilogue of moe_grouped_gemm_fwd). */
+moe_status moe_swiglu(const moe_bf16* h_gate, const moe_bf16* h_up, moe_bf16* act,
+                      int64_t rows, int64_t f, hipStream_t stream);
+
+/* Backward of moe_swiglu, elementwise over [rows, f] bf16, s = sigmoid(h_gate):
+ *   dh_up   = bf16(d_act * h_gate * s)
+ *   dh_gate = bf16(d_act * h_up * s * (1 + h_gate * (1 - s))). */
+moe_status moe_swiglu_bwd(const moe_bf16* h_gate, const moe_bf16* h_up, const moe_bf16* d_act,
+                          moe_bf16* dh_gate, moe_bf16* dh_up, int64_t rows, int64_t f,
+                          hipStream_t stream);
+
+/* ------------------------------------------------------------------------------------------ */
+/* E, L: weighted unpermute-combine;  F: its backward                                           */
+/* ------------------------------------------------------------------------------------------ */
+
+/*
+ * y[t, :] = bf16( sum_{j=0..k-1} w[t,j] * y_perm[row_of_slot[t*k+j], :] + add[t, :] ), fp32 sum
+ * in j order then the add, one rounding.  topk_w == NULL means every weight is 1 (the
+ * unpermute-sum of dX_perm in the backward); add == NULL means no add (the shared-FFN output is
+ * added here in the forward, its dX in the backward).  The paper does not describe the combine;
+ * this is the standard weighted MoE combine.
+ * y_perm [T*k,d] bf16; topk_w [T,k] fp32 or NULL; row_of_slot [T*k] int32; add [T,d] bf16 or
+ * NULL; y [T,d] bf16.
+ */
+moe_status moe_unpermute_combine(const moe_bf16* y_perm, const float* topk_w,
+                                 const int32_t* row_of_slot, const moe_bf16* add, int64_t T,
+                                 int64_t d, int32_t k, moe_bf16* y, hipStream_t stream);
+
+/*
+ * Backward of the weighted combine (the routing weight is applied while permuting dY):
+ *   dy_perm[row_of_slot[t*k+j], :] = bf16(w[t,j] * dy[t, :])
+ *   d_topk_w[t, j] = sum_c dy[t,c] * y_perm[row_of_slot[t*k+j], c]   (fp32; skipped if y_perm or
+ *                                                                     d_topk_w is NULL)
+ * dy [T,d] bf16; topk_w [T,k] fp32; row_of_slot [T*k]; y_perm [T*k,d] bf16 or NULL;
+ * dy_perm [T*k,d] bf16; d_topk_w [T,k] fp32 or NULL.
+ */
+moe_status moe_unpermute_combine_bwd(const moe_bf16* dy, const float* topk_w,
+                                     const int32_t* row_of_slot, const moe_bf16* y_perm,
+                                     int64_t T, int64_t d, int32_t k, moe_bf16* dy_perm,
+                                     float* d_topk_w, hipStream_t stream);
+
+/* ------------------------------------------------------------------------------------------ */
+/* G, J: backward data-gradient grouped GEMM                                                    */
+/* ------------------------------------------------------------------------------------------ */
+
+/*
+ * dA[r, :] = bf16( dC[r, :] . B[g]^T (+ dC2[r, :] . B2[g]^T) ) for rows r of group g, one fp32
+ * accumulation over the whole (N or 2N long) contraction.  This is the gradient of
+ * moe_grouped_gemm_fwd with respect to A (dX_perm takes the gate and up pairs together).
+ * dC, dC2 [R,N] bf16; B, B2 [G,K,N] bf16; dA [R,K] bf16.  dC2 and B2 both NULL or both set.
+ */
+moe_status moe_grouped_gemm_dx(const moe_bf16* dC, const moe_bf16* B, const moe_bf16* dC2,
+                               const moe_bf16* B2, const int32_t* offsets, int32_t G, int64_t R,
+                               int64_t K, int64_t N, moe_bf16* dA, hipStream_t stream);
+
+/* ------------------------------------------------------------------------------------------ */
+/* H, K: backward weight-gradient grouped GEMM (the paper's dW1 kernel class)                   */
+/* ------------------------------------------------------------------------------------------ */
+
+/*
+ * dB[g] = A_g^T . dC_g over the rows of group g, in fp32 (section 5.4 and Appendix H:
+ * dW1_e = X_e^T G_e, a contraction over the expert's ragged row count K_e).  dB is overwritten,
+ * not accumulated into; an empty group (K_g = 0) gets exact zeros.  With dC2 != NULL the same A
+ * tiles also give dB2[g] = A_g^T . dC2_g (gate and up weight gradients in one pass).
+ * A [R,K] bf16; dC, dC2 [R,N] bf16; dB, dB2 [G,K,N] fp32.  dC2 and dB2 both NULL or both set.
+ * Deterministic: each output element is reduced in one fixed order (no atomics).
+ */
+moe_status moe_grouped_gemm_dw(const moe_bf16* A, const moe_bf16* dC, const moe_bf16* dC2,
+                               const int32_t* offsets, int32_t G, int64_t R, int64_t K,
+                               int64_t N, float* dB, float* dB2, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOE_MI355X_H */

@@ -1,0 +1,229 @@
+// HBM-bound kernels of the layer: SwiGLU forward/backward (elementwise over [rows, f]) and the
+// weighted unpermute-combine with its backward (one wavefront per token; each token's rows of
+// the permuted buffer are whole 16-byte-vector rows, so every access is a coalesced row copy).
+#include "common.h"
+
+namespace moe {
+namespace {
+
+__global__ __launch_bounds__(256) void swiglu_kernel(const u32x4* __restrict__ hg,
+                                                     const u32x4* __restrict__ hu,
+                                                     u32x4* __restrict__ act, int64_t n8) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n8; i += (int64_t)gridDim.x * 256) {
+    float g[8], u[8], a[8];
+    unpack8(hg[i], g);
+    unpack8(hu[i], u);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) a[j] = silu_f32(g[j]) * u[j];
+    act[i] = pack8(a);
+  }
+}
+
+__global__ __launch_bounds__(256) void swiglu_bwd_kernel(const u32x4* __restrict__ hg,
+                                                         const u32x4* __restrict__ hu,
+                                                         const u32x4* __restrict__ da,
+                                                         u32x4* __restrict__ dhg,
+                                                         u32x4* __restrict__ dhu, int64_t n8) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n8; i += (int64_t)gridDim.x * 256) {
+    float g[8], u[8], d[8], og[8], ou[8];
+    unpack8(hg[i], g);
+    unpack8(hu[i], u);
+    unpack8(da[i], d);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float s = sigmoid_f32(g[j]);
+      ou[j] = d[j] * g[j] * s;
+      og[j] = d[j] * u[j] * s * (1.0f + g[j] * (1.0f - s));
+    }
+    dhg[i] = pack8(og);
+    dhu[i] = pack8(ou);
+  }
+}
+
+// y[t] = bf16(sum_j w[t,j] * y_perm[row_of_slot[t*k+j]] + add[t])
+template <int U>
+__global__ __launch_bounds__(256) void combine_kernel(const u32x4* __restrict__ y_perm,
+                                                      const float* __restrict__ w,
+                                                      const int32_t* __restrict__ row_of_slot,
+                                                      const u32x4* __restrict__ add, int64_t T,
+                                                      int64_t chunks, int k,
+                                                      u32x4* __restrict__ y) {
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  for (int64_t c0 = 0; c0 < chunks; c0 += 64 * U) {
+    float acc[U][8];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc[u][i] = 0.f;
+    for (int j = 0; j < k; ++j) {
+      const int64_t r = row_of_slot[t * k + j];
+      const float wj = w ? w[t * k + j] : 1.0f;
+      const u32x4* src = y_perm + r * chunks;
+      u32x4 v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t c = c0 + u * 64 + lane;
+        if (c < chunks) v[u] = src[c];
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        float f[8];
+        unpack8(v[u], f);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[u][i] += wj * f[i];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t c = c0 + u * 64 + lane;
+      if (c < chunks) {
+        if (add) {
+          float f[8];
+          unpack8(add[t * chunks + c], f);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) acc[u][i] += f[i];
+        }
+        y[t * chunks + c] = pack8(acc[u]);
+      }
+    }
+  }
+}
+
+// dy_perm[row] = bf16(w * dy[t]); d_w[t,j] = <dy[t], y_perm[row]>
+template <int U>
+__global__ __launch_bounds__(256) void combine_bwd_kernel(const u32x4* __restrict__ dy,
+                                                          const float* __restrict__ w,
+                                                          const int32_t* __restrict__ row_of_slot,
+                                                          const u32x4* __restrict__ y_perm,
+                                                          int64_t T, int64_t chunks, int k,
+                                                          u32x4* __restrict__ dy_perm,
+                                                          float* __restrict__ d_w) {
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  const u32x4* src = dy + t * chunks;
+  for (int j = 0; j < k; ++j) {
+    const int64_t r = row_of_slot[t * k + j];
+    const float wj = w[t * k + j];
+    float dot = 0.f;
+    for (int64_t c0 = 0; c0 < chunks; c0 += 64 * U) {
+      u32x4 v[U], yv[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t c = c0 + u * 64 + lane;
+        if (c < chunks) {
+          v[u] = src[c];
+          if (y_perm) yv[u] = y_perm[r * chunks + c];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t c = c0 + u * 64 + lane;
+        if (c < chunks) {
+          float f[8], o[8];
+          unpack8(v[u], f);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) o[i] = wj * f[i];
+          dy_perm[r * chunks + c] = pack8(o);
+          if (y_perm) {
+            float yf[8];
+            unpack8(yv[u], yf);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) dot += f[i] * yf[i];
+          }
+        }
+      }
+    }
+    if (y_perm && d_w) {
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) dot += __shfl_xor(dot, off);
+      if (lane == 0) d_w[t * k + j] = dot;
+    }
+  }
+}
+
+unsigned elementwise_grid(int64_t n8) {
+  const int64_t want = (n8 + 255) / 256;
+  const int64_t cap = (int64_t)device_cu_count() * 16;
+  return (unsigned)(want < cap ? (want > 0 ? want : 1) : cap);
+}
+
+}  // namespace
+}  // namespace moe
+
+using namespace moe;
+
+extern "C" moe_status moe_swiglu(const moe_bf16* h_gate, const moe_bf16* h_up, moe_bf16* act,
+                                 int64_t rows, int64_t f, hipStream_t stream) {
+  if (rows < 0 || f < 0) return fail(MOE_ERROR_INVALID_VALUE, "moe_swiglu: negative size");
+  if (f % 64 != 0) return fail(MOE_ERROR_NOT_SUPPORTED, "moe_swiglu: f must be a multiple of 64");
+  if (rows == 0 || f == 0) return MOE_SUCCESS;
+  if (!h_gate || !h_up || !act) return fail(MOE_ERROR_INVALID_VALUE, "moe_swiglu: NULL pointer");
+  if (!aligned16(h_gate) || !aligned16(h_up) || !aligned16(act))
+    return fail(MOE_ERROR_INVALID_VALUE, "moe_swiglu: pointers must be 16-byte aligned");
+  const int64_t n8 = rows * f / 8;
+  swiglu_kernel<<<elementwise_grid(n8), 256, 0, stream>>>(
+      reinterpret_cast<const u32x4*>(h_gate), reinterpret_cast<const u32x4*>(h_up),
+      reinterpret_cast<u32x4*>(act), n8);
+  return check_launch("swiglu_kernel");
+}
+
+extern "C" moe_status moe_swiglu_bwd(const moe_bf16* h_gate, const moe_bf16* h_up,
+                                     const moe_bf16* d_act, moe_bf16* dh_gate, moe_bf16* dh_up,
+                                     int64_t rows, int64_t f, hipStream_t stream) {
+  if (rows < 0 || f < 0) return fail(MOE_ERROR_INVALID_VALUE, "moe_swiglu_bwd: negative size");
+  if (f % 64 != 0) return fail(MOE_ERROR_NOT_SUPPORTED, "moe_swiglu_bwd: f must be a multiple of 64");
+  if (rows == 0 || f == 0) return MOE_SUCCESS;
+  if (!h_gate || !h_up || !d_act || !dh_gate || !dh_up)
+    return fail(MOE_ERROR_INVALID_VALUE, "moe_swiglu_bwd: NULL pointer");
+  if (!aligned16(h_gate) || !aligned16(h_up) || !aligned16(d_act) || !aligned16(dh_gate) ||
+      !aligned16(dh_up))
+    return fail(MOE_ERROR_INVALID_VALUE, "moe_swiglu_bwd: pointers must be 16-byte aligned");
+  const int64_t n8 = rows * f / 8;
+  swiglu_bwd_kernel<<<elementwise_grid(n8), 256, 0, stream>>>(
+      reinterpret_cast<const u32x4*>(h_gate), reinterpret_cast<const u32x4*>(h_up),
+      reinterpret_cast<const u32x4*>(d_act), reinterpret_cast<u32x4*>(dh_gate),
+      reinterpret_cast<u32x4*>(dh_up), n8);
+  return check_launch("swiglu_bwd_kernel");
+}
+
+extern "C" moe_status moe_unpermute_combine(const moe_bf16* y_perm, const float* topk_w,
+                                            const int32_t* row_of_slot, const moe_bf16* add,
+                                            int64_t T, int64_t d, int32_t k, moe_bf16* y,
+                                            hipStream_t stream) {
+  if (T < 0 || d < 0) return fail(MOE_ERROR_INVALID_VALUE, "moe_unpermute_combine: negative size");
+  if (k < 1 || k > 256) return fail(MOE_ERROR_INVALID_VALUE, "moe_unpermute_combine: need 1 <= k <= 256");
+  if (d % 64 != 0) return fail(MOE_ERROR_NOT_SUPPORTED, "moe_unpermute_combine: d must be a multiple of 64");
+  if (T == 0 || d == 0) return MOE_SUCCESS;
+  if (!y_perm || !row_of_slot || !y)
+    return fail(MOE_ERROR_INVALID_VALUE, "moe_unpermute_combine: NULL pointer");
+  if (!aligned16(y_perm) || !aligned16(y) || (add && !aligned16(add)))
+    return fail(MOE_ERROR_INVALID_VALUE, "moe_unpermute_combine: pointers must be 16-byte aligned");
+  const int64_t chunks = d / 8;
+  combine_kernel<4><<<(unsigned)((T + 3) / 4), 256, 0, stream>>>(
+      reinterpret_cast<const u32x4*>(y_perm), topk_w, row_of_slot,
+      reinterpret_cast<const u32x4*>(add), T, chunks, k, reinterpret_cast<u32x4*>(y));
+  return check_launch("combine_kernel");
+}
+
+extern "C" moe_status moe_unpermute_combine_bwd(const moe_bf16* dy, const float* topk_w,
+                                                const int32_t* row_of_slot, const moe_bf16* y_perm,
+                                                int64_t T, int64_t d, int32_t k, moe_bf16* dy_perm,
+                                                float* d_topk_w, hipStream_t stream) {
+  if (T < 0 || d < 0) return fail(MOE_ERROR_INVALID_VALUE, "moe_unpermute_combine_bwd: negative size");
+  if (k < 1 || k > 256) return fail(MOE_ERROR_INVALID_VALUE, "moe_unpermute_combine_bwd: need 1 <= k <= 256");
+  if (d % 64 != 0) return fail(MOE_ERROR_NOT_SUPPORTED, "moe_unpermute_combine_bwd: d must be a multiple of 64");
+  if (T == 0 || d == 0) return MOE_SUCCESS;
+  if (!dy || !topk_w || !row_of_slot || !dy_perm)
+    return fail(MOE_ERROR_INVALID_VALUE, "moe_unpermute_combine_bwd: NULL pointer");
+  if (!aligned16(dy) || !aligned16(dy_perm) || (y_perm && !aligned16(y_perm)))
+    return fail(MOE_ERROR_INVALID_VALUE, "moe_unpermute_combine_bwd: pointers must be 16-byte aligned");
+  const int64_t chunks = d / 8;
+  combine_bwd_kernel<4><<<(unsigned)((T + 3) / 4), 256, 0, stream>>>(
+      reinterpret_cast<const u32x4*>(dy), topk_w, row_of_slot,
+      reinterpret_cast<const u32x4*>(y_perm), T, chunks, k, reinterpret_cast<u32x4*>(dy_perm),
+      d_topk_w);
+  return check_launch("combine_bwd_kernel");
+}

@@ -1,0 +1,175 @@
+"""The MoE expert-FFN training layer as a fixed sequence of library calls on one stream.
+
+Forward:  route_permute -> grouped_gemm_fwd (gate/up + fused SwiGLU) -> grouped_gemm_fwd (down)
+          [-> shared FFN as one-group calls] -> unpermute_combine.
+Backward: unpermute_combine_bwd (weighted dY permute + d_topk_w) -> grouped_gemm_dx (down)
+          -> grouped_gemm_dw (down) -> swiglu_bwd -> grouped_gemm_dx (gate+up in one contraction)
+          -> grouped_gemm_dw (gate+up in one pass) [-> shared FFN backward]
+          -> unpermute_combine (unweighted sum of dX_perm + shared dX).
+
+All buffers are allocated once (torch owns device memory); a step only enqueues kernels, with no
+host synchronization.
+"""
+from __future__ import annotations
+
+import torch
+
+from . import moe
+
+
+class _Traced:
+    """Optional per-call timing: when `trace` is a list, each library call is bracketed by two
+    events recorded on the stream the call is enqueued on, and (name, start, end) is appended."""
+
+    trace = None
+
+    def _run(self, name, fn, *args, stream=None, **kw):
+        if self.trace is None:
+            return fn(*args, stream=stream, **kw)
+        st = torch.cuda.current_stream() if stream is None else stream
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        out = fn(*args, stream=stream, **kw)
+        e1.record(st)
+        self.trace.append((name, e0, e1))
+        return out
+
+
+class MoELayer(_Traced):
+    def __init__(self, cfg, inputs: dict, normalize_topk: bool = True):
+        self.cfg = cfg
+        self.inp = inputs
+        self.normalize = normalize_topk
+        dev = inputs["x"].device
+        T, d, f, E, k = cfg.T, cfg.d, cfg.f, cfg.E, cfg.k
+        R = T * k
+        bf, f32, i32 = torch.bfloat16, torch.float32, torch.int32
+        e = lambda shape, dt=bf: torch.empty(shape, dtype=dt, device=dev)
+        self.buf = b = {
+            "topk_idx": e((T, k), i32), "topk_w": e((T, k), f32), "offsets": e(E + 1, i32),
+            "row_of_slot": e(R, i32), "token_of_row": e(R, i32), "x_perm": e((R, d)),
+            "h_gate": e((R, f)), "h_up": e((R, f)), "act": e((R, f)), "y_perm": e((R, d)), "y": e((T, d)),
+            "dy_perm": e((R, d)), "d_topk_w": e((T, k), f32), "d_act": e((R, f)),
+            "dh_gate": e((R, f)), "dh_up": e((R, f)), "dx_perm": e((R, d)), "dx": e((T, d)),
+            "dw_gate": e((E, d, f), f32), "dw_up": e((E, d, f), f32), "dw_down": e((E, f, d), f32),
+            "workspace": e(max(16, moe.moe_route_permute_workspace_bytes(T, E, k)), torch.uint8),
+        }
+        self.shared = cfg.f_shared > 0
+        if self.shared:
+            fs = cfg.f_shared
+            self.offsets_sh = torch.tensor([0, T], dtype=i32, device=dev)
+            b.update({
+                "h_gate_sh": e((T, fs)), "h_up_sh": e((T, fs)), "act_sh": e((T, fs)), "y_sh": e((T, d)),
+                "d_act_sh": e((T, fs)), "dh_gate_sh": e((T, fs)), "dh_up_sh": e((T, fs)), "dx_sh": e((T, d)),
+                "dw_gate_sh": e((1, d, fs), f32), "dw_up_sh": e((1, d, fs), f32), "dw_down_sh": e((1, fs, d), f32),
+            })
+            self.w_sh = (inputs["w_gate_sh"].unsqueeze(0), inputs["w_up_sh"].unsqueeze(0),
+                         inputs["w_down_sh"].unsqueeze(0))
+
+    # ------------------------------------------------------------------------------------------
+    def forward(self, stream=None):
+        b, i, k, run = self.buf, self.inp, self.cfg.k, self._run
+        run("route_permute", moe.moe_route_permute, i["logits"], i["x"], k, self.normalize, b["topk_idx"],
+            b["topk_w"], b["offsets"], b["row_of_slot"], b["token_of_row"], b["x_perm"], b["workspace"],
+            stream=stream)
+        run("fwd_gate_up", moe.moe_grouped_gemm_fwd, b["x_perm"], i["w_gate"], b["offsets"], i["w_up"],
+            b["h_gate"], b["h_up"], b["act"], want_act=True, stream=stream)
+        run("fwd_down", moe.moe_grouped_gemm_fwd, b["act"], i["w_down"], b["offsets"], C=b["y_perm"],
+            stream=stream)
+        add = None
+        if self.shared:
+            wg, wu, wd = self.w_sh
+            run("fwd_gate_up_sh", moe.moe_grouped_gemm_fwd, i["x"], wg, self.offsets_sh, wu, b["h_gate_sh"],
+                b["h_up_sh"], b["act_sh"], want_act=True, stream=stream)
+            run("fwd_down_sh", moe.moe_grouped_gemm_fwd, b["act_sh"], wd, self.offsets_sh, C=b["y_sh"],
+                stream=stream)
+            add = b["y_sh"]
+        run("combine", moe.moe_unpermute_combine, b["y_perm"], b["topk_w"], b["row_of_slot"], k, add=add,
+            y=b["y"], stream=stream)
+        return b["y"]
+
+    def backward(self, stream=None):
+        b, i, k, run = self.buf, self.inp, self.cfg.k, self._run
+        run("combine_bwd", moe.moe_unpermute_combine_bwd, i["dy"], b["topk_w"], b["row_of_slot"], k,
+            y_perm=b["y_perm"], dy_perm=b["dy_perm"], d_topk_w=b["d_topk_w"], stream=stream)
+        run("dx_down", moe.moe_grouped_gemm_dx, b["dy_perm"], i["w_down"], b["offsets"], dA=b["d_act"],
+            stream=stream)
+        run("dw_down", moe.moe_grouped_gemm_dw, b["act"], b["dy_perm"], b["offsets"], dB=b["dw_down"],
+            stream=stream)
+        run("swiglu_bwd", moe.moe_swiglu_bwd, b["h_gate"], b["h_up"], b["d_act"], b["dh_gate"], b["dh_up"],
+            stream=stream)
+        run("dx_gate_up", moe.moe_grouped_gemm_dx, b["dh_gate"], i["w_gate"], b["offsets"], b["dh_up"],
+            i["w_up"], dA=b["dx_perm"], stream=stream)
+        run("dw_gate_up", moe.moe_grouped_gemm_dw, b["x_perm"], b["dh_gate"], b["offsets"], b["dh_up"],
+            dB=b["dw_gate"], dB2=b["dw_up"], stream=stream)
+        add = None
+        if self.shared:
+            wg, wu, wd = self.w_sh
+            run("dx_down_sh", moe.moe_grouped_gemm_dx, i["dy"], wd, self.offsets_sh, dA=b["d_act_sh"],
+                stream=stream)
+            run("dw_down_sh", moe.moe_grouped_gemm_dw, b["act_sh"], i["dy"], self.offsets_sh,
+                dB=b["dw_down_sh"], stream=stream)
+            run("swiglu_bwd_sh", moe.moe_swiglu_bwd, b["h_gate_sh"], b["h_up_sh"], b["d_act_sh"],
+                b["dh_gate_sh"], b["dh_up_sh"], stream=stream)
+            run("dx_gate_up_sh", moe.moe_grouped_gemm_dx, b["dh_gate_sh"], wg, self.offsets_sh, b["dh_up_sh"],
+                wu, dA=b["dx_sh"], stream=stream)
+            run("dw_gate_up_sh", moe.moe_grouped_gemm_dw, i["x"], b["dh_gate_sh"], self.offsets_sh,
+                b["dh_up_sh"], dB=b["dw_gate_sh"], dB2=b["dw_up_sh"], stream=stream)
+            add = b["dx_sh"]
+        run("unpermute_dx", moe.moe_unpermute_combine, b["dx_perm"], None, b["row_of_slot"], k, add=add,
+            y=b["dx"], stream=stream)
+        return b["dx"]
+
+    def step(self, stream=None):
+        self.forward(stream)
+        self.backward(stream)
+
+    # algorithmic work of each call (FLOPs for GEMMs, unique HBM bytes for the rest)
+    def work(self):
+        c = self.cfg
+        T, d, f, k, E = c.T, c.d, c.f, c.k, c.E
+        R = T * k
+        w = {
+            "route_permute": ("bytes", T * E * 4 + T * k * 8 + R * 8 + T * d * 2 + R * d * 2),
+            "fwd_gate_up": ("flops", 4 * R * d * f), "fwd_down": ("flops", 2 * R * f * d),
+            "combine": ("bytes", R * d * 2 + T * d * 2 + T * k * 8 + (T * d * 2 if self.shared else 0)),
+            "combine_bwd": ("bytes", T * d * 2 + 2 * R * d * 2 + T * k * 12),
+            "dx_down": ("flops", 2 * R * d * f), "dw_down": ("flops", 2 * R * f * d),
+            "swiglu_bwd": ("bytes", 5 * R * f * 2),
+            "dx_gate_up": ("flops", 4 * R * d * f), "dw_gate_up": ("flops", 4 * R * d * f),
+            "unpermute_dx": ("bytes", R * d * 2 + T * d * 2 + R * 4 + (T * d * 2 if self.shared else 0)),
+        }
+        if self.shared:
+            fs = c.f_shared
+            w.update({"fwd_gate_up_sh": ("flops", 4 * T * d * fs), "fwd_down_sh": ("flops", 2 * T * fs * d),
+                      "dx_down_sh": ("flops", 2 * T * d * fs), "dw_down_sh": ("flops", 2 * T * fs * d),
+                      "swiglu_bwd_sh": ("bytes", 5 * T * fs * 2),
+                      "dx_gate_up_sh": ("flops", 4 * T * d * fs), "dw_gate_up_sh": ("flops", 4 * T * d * fs)})
+        return w
+
+
+class DWOnly(_Traced):
+    """The weight-gradient-only workload: dW_gate and dW_up in one pass, then dW_down."""
+
+    def __init__(self, cfg, inputs: dict):
+        self.cfg = cfg
+        self.inp = inputs
+        dev = inputs["x_perm"].device
+        E, d, f = cfg.E, cfg.d, cfg.f
+        self.buf = {
+            "dw_gate": torch.empty((E, d, f), dtype=torch.float32, device=dev),
+            "dw_up": torch.empty((E, d, f), dtype=torch.float32, device=dev),
+            "dw_down": torch.empty((E, f, d), dtype=torch.float32, device=dev),
+        }
+
+    def step(self, stream=None):
+        i, b = self.inp, self.buf
+        self._run("dw_gate_up", moe.moe_grouped_gemm_dw, i["x_perm"], i["dh_gate"], i["offsets"], i["dh_up"],
+                  dB=b["dw_gate"], dB2=b["dw_up"], stream=stream)
+        self._run("dw_down", moe.moe_grouped_gemm_dw, i["act"], i["dy_perm"], i["offsets"], dB=b["dw_down"],
+                  stream=stream)
+
+    def work(self):
+        c = self.cfg
+        return {"dw_gate_up": ("flops", 4 * c.R * c.d * c.f), "dw_down": ("flops", 2 * c.R * c.f * c.d)}

@@ -1,0 +1,248 @@
+"""Python binding of libmoe_mi355x.so: one function per C entry point, same names.
+
+Argument marshalling only: tensors become device pointers, the stream defaults to torch's
+current stream, and missing outputs are allocated with torch (device memory is torch's job).
+Every computation runs in the library's HIP kernels; if the library is missing this module
+raises instead of falling back to anything else.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+from .build import LIB_PATH
+
+_lib = None
+
+MOE_SUCCESS = 0
+STATUS_NAMES = {0: "MOE_SUCCESS", 1: "MOE_ERROR_INVALID_VALUE", 2: "MOE_ERROR_NOT_SUPPORTED",
+                3: "MOE_ERROR_WORKSPACE", 4: "MOE_ERROR_HIP"}
+
+
+class MoEError(RuntimeError):
+    def __init__(self, fn, status, detail):
+        super().__init__(f"{fn}: {STATUS_NAMES.get(status, status)}: {detail}")
+        self.status = status
+
+
+_P = ctypes.c_void_p
+_I64 = ctypes.c_int64
+_I32 = ctypes.c_int32
+_SIG = {
+    "moe_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "moe_last_error": (ctypes.c_char_p, []),
+    "moe_route_permute_workspace_bytes": (ctypes.c_size_t, [_I64, _I32, _I32]),
+    "moe_route_permute": (ctypes.c_int, [_P, _P, _I64, _I64, _I32, _I32, _I32, _P, _P, _P, _P, _P,
+                                         _P, _P, ctypes.c_size_t, _P]),
+    "moe_grouped_gemm_fwd": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P, _P]),
+    "moe_swiglu": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _P]),
+    "moe_swiglu_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _I64, _I64, _P]),
+    "moe_unpermute_combine": (ctypes.c_int, [_P, _P, _P, _P, _I64, _I64, _I32, _P, _P]),
+    "moe_unpermute_combine_bwd": (ctypes.c_int, [_P, _P, _P, _P, _I64, _I64, _I32, _P, _P, _P]),
+    "moe_grouped_gemm_dx": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P]),
+    "moe_grouped_gemm_dw": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P]),
+}
+
+
+def lib():
+    """The loaded library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2606_26453_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIG.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _check(fn, status):
+    if status != MOE_SUCCESS:
+        raise MoEError(fn, status, lib().moe_last_error().decode())
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if not t.is_cuda:
+        raise ValueError("tensors passed to the MoE library must be on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to the MoE library must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _need(t, dtype, shape, name):
+    if t is None:
+        return
+    if t.dtype != dtype or tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: expected {dtype} {tuple(shape)}, got {t.dtype} {tuple(t.shape)}")
+
+
+def moe_route_permute_workspace_bytes(T, E, k):
+    return lib().moe_route_permute_workspace_bytes(T, E, k)
+
+
+def moe_route_permute(logits, x, k, normalize_topk=True, topk_idx=None, topk_w=None, offsets=None,
+                      row_of_slot=None, token_of_row=None, x_perm=None, workspace=None, stream=None):
+    T, E = logits.shape
+    dev = logits.device
+    _need(logits, torch.float32, (T, E), "logits")
+    d = x.shape[1] if x is not None else 0
+    if x is not None:
+        _need(x, torch.bfloat16, (T, d), "x")
+    R = T * k
+    topk_idx = torch.empty((T, k), dtype=torch.int32, device=dev) if topk_idx is None else topk_idx
+    topk_w = torch.empty((T, k), dtype=torch.float32, device=dev) if topk_w is None else topk_w
+    offsets = torch.empty(E + 1, dtype=torch.int32, device=dev) if offsets is None else offsets
+    row_of_slot = torch.empty(R, dtype=torch.int32, device=dev) if row_of_slot is None else row_of_slot
+    token_of_row = torch.empty(R, dtype=torch.int32, device=dev) if token_of_row is None else token_of_row
+    if x is not None and x_perm is None:
+        x_perm = torch.empty((R, d), dtype=torch.bfloat16, device=dev)
+    _need(topk_idx, torch.int32, (T, k), "topk_idx")
+    _need(topk_w, torch.float32, (T, k), "topk_w")
+    _need(offsets, torch.int32, (E + 1,), "offsets")
+    _need(row_of_slot, torch.int32, (R,), "row_of_slot")
+    _need(token_of_row, torch.int32, (R,), "token_of_row")
+    _need(x_perm, torch.bfloat16, (R, d), "x_perm")
+    ws_bytes = moe_route_permute_workspace_bytes(T, E, k)
+    if workspace is None:
+        workspace = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device=dev)
+    st = lib().moe_route_permute(_ptr(logits), _ptr(x), T, d, E, k, int(bool(normalize_topk)),
+                                 _ptr(topk_idx), _ptr(topk_w), _ptr(offsets), _ptr(row_of_slot),
+                                 _ptr(token_of_row), _ptr(x_perm), _ptr(workspace),
+                                 workspace.numel() * workspace.element_size(), _stream(stream))
+    _check("moe_route_permute", st)
+    return {"topk_idx": topk_idx, "topk_w": topk_w, "offsets": offsets, "row_of_slot": row_of_slot,
+            "token_of_row": token_of_row, "x_perm": x_perm}
+
+
+def moe_grouped_gemm_fwd(A, B, offsets, B2=None, C=None, C2=None, act=None, want_act=False,
+                         stream=None):
+    R, K = A.shape
+    G, K2, N = B.shape
+    if K2 != K:
+        raise ValueError("A and B disagree on K")
+    _need(A, torch.bfloat16, (R, K), "A")
+    _need(B, torch.bfloat16, (G, K, N), "B")
+    _need(B2, torch.bfloat16, (G, K, N), "B2")
+    _need(offsets, torch.int32, (G + 1,), "offsets")
+    dev = A.device
+    C = torch.empty((R, N), dtype=torch.bfloat16, device=dev) if C is None else C
+    if B2 is not None and C2 is None:
+        C2 = torch.empty((R, N), dtype=torch.bfloat16, device=dev)
+    if want_act and act is None:
+        act = torch.empty((R, N), dtype=torch.bfloat16, device=dev)
+    for t, n in ((C, "C"), (C2, "C2"), (act, "act")):
+        _need(t, torch.bfloat16, (R, N), n)
+    st = lib().moe_grouped_gemm_fwd(_ptr(A), _ptr(B), _ptr(B2), _ptr(offsets), G, R, K, N, _ptr(C),
+                                    _ptr(C2), _ptr(act), _stream(stream))
+    _check("moe_grouped_gemm_fwd", st)
+    return C, C2, act
+
+
+def moe_swiglu(h_gate, h_up, act=None, stream=None):
+    rows, f = h_gate.shape
+    _need(h_gate, torch.bfloat16, (rows, f), "h_gate")
+    _need(h_up, torch.bfloat16, (rows, f), "h_up")
+    act = torch.empty_like(h_gate) if act is None else act
+    _need(act, torch.bfloat16, (rows, f), "act")
+    _check("moe_swiglu", lib().moe_swiglu(_ptr(h_gate), _ptr(h_up), _ptr(act), rows, f, _stream(stream)))
+    return act
+
+
+def moe_swiglu_bwd(h_gate, h_up, d_act, dh_gate=None, dh_up=None, stream=None):
+    rows, f = h_gate.shape
+    for t, n in ((h_gate, "h_gate"), (h_up, "h_up"), (d_act, "d_act")):
+        _need(t, torch.bfloat16, (rows, f), n)
+    dh_gate = torch.empty_like(h_gate) if dh_gate is None else dh_gate
+    dh_up = torch.empty_like(h_gate) if dh_up is None else dh_up
+    _need(dh_gate, torch.bfloat16, (rows, f), "dh_gate")
+    _need(dh_up, torch.bfloat16, (rows, f), "dh_up")
+    _check("moe_swiglu_bwd", lib().moe_swiglu_bwd(_ptr(h_gate), _ptr(h_up), _ptr(d_act), _ptr(dh_gate),
+                                                  _ptr(dh_up), rows, f, _stream(stream)))
+    return dh_gate, dh_up
+
+
+def moe_unpermute_combine(y_perm, topk_w, row_of_slot, k, add=None, y=None, stream=None):
+    R, d = y_perm.shape
+    T = R // k
+    _need(y_perm, torch.bfloat16, (T * k, d), "y_perm")
+    _need(topk_w, torch.float32, (T, k), "topk_w")
+    _need(row_of_slot, torch.int32, (R,), "row_of_slot")
+    _need(add, torch.bfloat16, (T, d), "add")
+    y = torch.empty((T, d), dtype=torch.bfloat16, device=y_perm.device) if y is None else y
+    _need(y, torch.bfloat16, (T, d), "y")
+    _check("moe_unpermute_combine",
+           lib().moe_unpermute_combine(_ptr(y_perm), _ptr(topk_w), _ptr(row_of_slot), _ptr(add), T, d, k,
+                                       _ptr(y), _stream(stream)))
+    return y
+
+
+def moe_unpermute_combine_bwd(dy, topk_w, row_of_slot, k, y_perm=None, dy_perm=None, d_topk_w=None,
+                              stream=None):
+    T, d = dy.shape
+    _need(dy, torch.bfloat16, (T, d), "dy")
+    _need(topk_w, torch.float32, (T, k), "topk_w")
+    _need(row_of_slot, torch.int32, (T * k,), "row_of_slot")
+    _need(y_perm, torch.bfloat16, (T * k, d), "y_perm")
+    dy_perm = torch.empty((T * k, d), dtype=torch.bfloat16, device=dy.device) if dy_perm is None else dy_perm
+    if y_perm is not None and d_topk_w is None:
+        d_topk_w = torch.empty((T, k), dtype=torch.float32, device=dy.device)
+    _need(dy_perm, torch.bfloat16, (T * k, d), "dy_perm")
+    _need(d_topk_w, torch.float32, (T, k), "d_topk_w")
+    _check("moe_unpermute_combine_bwd",
+           lib().moe_unpermute_combine_bwd(_ptr(dy), _ptr(topk_w), _ptr(row_of_slot), _ptr(y_perm), T, d, k,
+                                           _ptr(dy_perm), _ptr(d_topk_w), _stream(stream)))
+    return dy_perm, d_topk_w
+
+
+def moe_grouped_gemm_dx(dC, B, offsets, dC2=None, B2=None, dA=None, stream=None):
+    R, N = dC.shape
+    G, K, N2 = B.shape
+    if N2 != N:
+        raise ValueError("dC and B disagree on N")
+    _need(dC, torch.bfloat16, (R, N), "dC")
+    _need(dC2, torch.bfloat16, (R, N), "dC2")
+    _need(B, torch.bfloat16, (G, K, N), "B")
+    _need(B2, torch.bfloat16, (G, K, N), "B2")
+    _need(offsets, torch.int32, (G + 1,), "offsets")
+    dA = torch.empty((R, K), dtype=torch.bfloat16, device=dC.device) if dA is None else dA
+    _need(dA, torch.bfloat16, (R, K), "dA")
+    _check("moe_grouped_gemm_dx",
+           lib().moe_grouped_gemm_dx(_ptr(dC), _ptr(B), _ptr(dC2), _ptr(B2), _ptr(offsets), G, R, K, N,
+                                     _ptr(dA), _stream(stream)))
+    return dA
+
+
+def moe_grouped_gemm_dw(A, dC, offsets, dC2=None, dB=None, dB2=None, stream=None):
+    R, K = A.shape
+    N = dC.shape[1]
+    G = offsets.numel() - 1
+    _need(A, torch.bfloat16, (R, K), "A")
+    _need(dC, torch.bfloat16, (R, N), "dC")
+    _need(dC2, torch.bfloat16, (R, N), "dC2")
+    _need(offsets, torch.int32, (G + 1,), "offsets")
+    dB = torch.empty((G, K, N), dtype=torch.float32, device=A.device) if dB is None else dB
+    if dC2 is not None and dB2 is None:
+        dB2 = torch.empty((G, K, N), dtype=torch.float32, device=A.device)
+    _need(dB, torch.float32, (G, K, N), "dB")
+    _need(dB2, torch.float32, (G, K, N), "dB2")
+    _check("moe_grouped_gemm_dw",
+           lib().moe_grouped_gemm_dw(_ptr(A), _ptr(dC), _ptr(dC2), _ptr(offsets), G, R, K, N, _ptr(dB),
+                                     _ptr(dB2), _stream(stream)))
+    return dB, dB2

@@ -1,0 +1,96 @@
+"""The C-ABI library loads, exports every entry point include/moe.h declares, and rejects invalid
+arguments on the host before launching anything (no GPU needed: no compute call reaches HIP)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_26453_amd import moe
+from paper_2606_26453_amd.build import LIB_PATH
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "moe.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(LIB_PATH), reason="library not built")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(moe_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_exports_every_declared_symbol():
+    names = _declared()
+    assert len(names) >= 11
+    L = ctypes.CDLL(LIB_PATH)
+    for n in names:
+        assert hasattr(L, n), f"{n} declared in moe.h but not exported"
+    assert set(names) == set(moe._SIG), "binding and header disagree"
+
+
+def test_status_strings():
+    L = moe.lib()
+    for code in range(5):
+        assert L.moe_status_string(code)
+    assert L.moe_status_string(99) == b"unknown status"
+
+
+FAKE = 1 << 20        # a 16-byte-aligned non-NULL address that is never dereferenced
+BAD = FAKE + 2        # misaligned
+
+
+def test_route_permute_rejects():
+    L = moe.lib()
+    args = lambda T=10, d=64, E=4, k=2, norm=1, x=FAKE, ws=FAKE, wsb=1 << 20: (
+        FAKE, x, T, d, E, k, norm, FAKE, FAKE, FAKE, FAKE, FAKE, x, ws, wsb, None)
+    assert L.moe_route_permute(*args(k=5)) == 1            # k > E
+    assert L.moe_route_permute(*args(k=0)) == 1
+    assert L.moe_route_permute(*args(E=300, k=2)) == 2     # E > 256
+    assert L.moe_route_permute(*args(d=100)) == 2          # d % 64
+    assert L.moe_route_permute(*args(T=-1)) == 1
+    assert L.moe_route_permute(*args(norm=2)) == 1
+    assert L.moe_route_permute(*args(x=BAD)) == 1          # misaligned
+    assert L.moe_route_permute(*args(wsb=0)) == 3          # workspace too small
+    assert b"workspace" in L.moe_last_error()
+    assert L.moe_route_permute(*args(T=1 << 30, k=4)) == 2  # R >= 2^31
+    assert L.moe_route_permute_workspace_bytes(0, 4, 2) == 0
+    assert L.moe_route_permute_workspace_bytes(1000, 64, 6) > 0
+
+
+def test_gemm_rejects():
+    L = moe.lib()
+    fwd = lambda G=4, R=100, K=128, N=128, A=FAKE, B2=None, C2=None, act=None: L.moe_grouped_gemm_fwd(
+        A, FAKE, B2, FAKE, G, R, K, N, FAKE, C2, act, None)
+    assert fwd(G=0) == 2 and fwd(G=257) == 2
+    assert fwd(K=100) == 2 and fwd(N=96) == 2
+    assert fwd(R=-1) == 1
+    assert fwd(A=BAD) == 1
+    assert fwd(B2=FAKE) == 1                 # B2 without C2
+    assert fwd(act=FAKE) == 1                # act without B2
+    assert fwd(A=None) == 1
+    assert fwd(R=0) == 0                     # empty: successful no-op
+    dx = lambda G=4, R=100, K=128, N=128, dC2=None, B2=None: L.moe_grouped_gemm_dx(
+        FAKE, FAKE, dC2, B2, FAKE, G, R, K, N, FAKE, None)
+    assert dx(K=65) == 2 and dx(dC2=FAKE) == 1 and dx(R=0) == 0
+    dw = lambda G=4, R=100, K=128, N=128, dC2=None, dB2=None, dB=FAKE: L.moe_grouped_gemm_dw(
+        FAKE, FAKE, dC2, FAKE, G, R, K, N, dB, dB2, None)
+    assert dw(N=32) == 2 and dw(dC2=FAKE) == 1 and dw(dB=None) == 1 and dw(dB=BAD) == 1
+
+
+def test_elementwise_rejects():
+    L = moe.lib()
+    assert L.moe_swiglu(FAKE, FAKE, FAKE, 10, 100, None) == 2
+    assert L.moe_swiglu(FAKE, FAKE, None, 10, 128, None) == 1
+    assert L.moe_swiglu(FAKE, FAKE, FAKE, 0, 128, None) == 0
+    assert L.moe_swiglu_bwd(FAKE, FAKE, FAKE, FAKE, BAD, 10, 128, None) == 1
+    assert L.moe_unpermute_combine(FAKE, FAKE, FAKE, None, 10, 128, 0, FAKE, None) == 1
+    assert L.moe_unpermute_combine(FAKE, FAKE, FAKE, None, 10, 96, 2, FAKE, None) == 2
+    assert L.moe_unpermute_combine(FAKE, FAKE, FAKE, None, 0, 128, 2, FAKE, None) == 0
+    assert L.moe_unpermute_combine_bwd(FAKE, None, FAKE, None, 10, 128, 2, FAKE, None, None) == 1
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    with pytest.raises(ValueError):
+        moe._ptr(torch.zeros(4))
