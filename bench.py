@@ -165,7 +165,7 @@ def main():
         "input_gen_s": round(t_gen, 1),
     }
     if not a.no_cpu_baseline and not cfg.dw_only:
-        ts = a.cpu_sample_tokens or max(8, min(cfg.T, int(2e11 // (18 * cfg.k * cfg.d * cfg.f))))
+        ts = a.cpu_sample_tokens or max(8, min(cfg.T, int(2e12 // (18 * cfg.k * cfg.d * cfg.f))))
         out["cpu_baseline"] = cpu_baseline(cfg, inp, ts)
     print(json.dumps(out), flush=True)
 
