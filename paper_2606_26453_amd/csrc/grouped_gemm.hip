@@ -31,8 +31,22 @@
 namespace moe {
 namespace {
 
-constexpr int NT = 256;
-constexpr int BK = 64;
+constexpr int TILE = 256;    // output tile edge (rows and N-side columns)
+constexpr int BK = 32;       // contraction elements per pipeline stage
+constexpr int NSTAGE = 4;    // LDS ring depth
+constexpr int OPND = TILE * BK * 2;      // bytes of one operand tile in one stage (16 KiB)
+constexpr int STAGE = 2 * OPND;          // M side at +0, N side at +OPND
+
+// Two LDS tile layouts, chosen so that DMA stores are plain 1 KiB runs and every fragment read
+// of 8 (ds_read_b128) or 16 (ds_read_b64_tr_b16) lanes touches distinct banks:
+//  - direct operand (contraction contiguous in memory, e.g. the routed rows): [256 rows][4 chunks
+//    of 8 elements], chunk c of row r at r*64 + 16*(c ^ ((r >> 2) & 3)) (16 consecutive rows of one
+//    chunk fill all 64 banks);
+//  - mn operand (contraction is the memory row, e.g. a [K,N] weight): 4 groups of 64 columns,
+//    each [32 contraction rows][8 chunks], chunk c of row k at group*4096 + k*128 +
+//    16*(c ^ 2*(k & 3)).
+__device__ __forceinline__ int swz_d(int r) { return (r >> 2) & 3; }
+__device__ __forceinline__ int swz_t(int k) { return (k & 3) << 1; }
 
 enum { KIND_FWD = 0, KIND_DX = 1, KIND_DW = 2 };
 
@@ -47,142 +61,241 @@ struct GemmParams {
   uint16_t* act;       // FWD SwiGLU output
   int G;
   int64_t R, K, N;
-  int mt_bound;        // FWD/DX: upper bound on the number of row tiles (grid extent)
+  int mt_bound;        // FWD/DX: upper bound on the number of row tiles
   int m_tiles;         // DW: tiles over K
   int n_tiles;         // tiles over the output columns
 };
 
-// LDS element offset of (row, 16-byte chunk) in a [rows][64] bf16 tile.
-__device__ __forceinline__ int lds_off(int row, int ch) {
-  return row * BK + ((ch ^ (row & 7) ^ ((row >> 3) & 7)) << 3);
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+
+// Raw buffer resource (four scalar dwords) over [base, base + bytes): reads at offsets >= bytes
+// return zero, which zero-fills the rows past a ragged group's end.
+__device__ __forceinline__ i32x4 make_rsrc(const void* base, int64_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  const int n = bytes <= 0 ? 0 : (bytes > 0x7fffffff ? 0x7fffffff : (int)bytes);
+  i32x4 r;
+  r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  r[1] = __builtin_amdgcn_readfirstlane((int)((a >> 32) & 0xffffu));
+  r[2] = __builtin_amdgcn_readfirstlane(n);
+  r[3] = 0x00020000;
+  return r;
 }
 
-__device__ __forceinline__ u32x4 ld16(const uint16_t* p) {
-  return *reinterpret_cast<const u32x4*>(p);
+// One 16-byte-per-lane buffer load written straight to LDS at lds_addr + 16*lane.  Issued as
+// inline assembly so the compiler does not serialise later LDS reads behind it; completion is
+// tracked explicitly with vmcnt waits (loads retire in order).
+__device__ __forceinline__ void dma16(i32x4 rsrc, int voff, int lds_addr) {
+  asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+               :
+               : "v"(voff), "s"(rsrc), "s"(lds_addr)
+               : "memory", "m0");
 }
 
-// 8x8 bf16 transpose: in[i] holds 8 elements of row i; out[j] gets element j of rows 0..7.
-__device__ __forceinline__ void transpose8x8(const u32x4* in, u32x4* out) {
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      const uint32_t x = in[2 * p][j >> 1];
-      const uint32_t y = in[2 * p + 1][j >> 1];
-      out[j][p] = (j & 1) ? ((x >> 16) | (y & 0xffff0000u)) : ((x & 0xffffu) | (y << 16));
-    }
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  // s_waitcnt vmcnt(N) with the other counters left unconstrained
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+__device__ __forceinline__ bf16x8 lds_read16(const char* p) { return *reinterpret_cast<const bf16x8*>(p); }
+
+// Two transposing 8-byte LDS reads -> one MFMA operand (see the mn layout above).
+__device__ __forceinline__ bf16x8 lds_read_tr(const char* p) {
+  typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+  const lds_i16x4* q = (const lds_i16x4*)(const __attribute__((address_space(3))) char*)p;
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(const_cast<lds_i16x4*>(q));
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(const_cast<lds_i16x4*>(
+      (const lds_i16x4*)((const __attribute__((address_space(3))) char*)p + 4 * 128)));
+  typedef short i16x8 __attribute__((ext_vector_type(8)));
+  const i16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+// Logical tile index of block `bid` (< n): blocks go round-robin to the 8 XCDs, so give XCD x
+// the contiguous logical range it would otherwise see interleaved with the other seven.
+__device__ __forceinline__ int xcd_remap(int bid, int n) {
+  const int q = n >> 3, r = n & 7, x = bid & 7, l = bid >> 3;
+  return x * q + (x < r ? x : r) + l;
+}
+
+// Logical index within an (mt x nt) grid -> (m, n), walking bands of 8 column tiles so that 32
+// consecutive tiles form a 4 x 8 block (A rows reused 8x, B columns 4x in the XCD's L2).
+__device__ __forceinline__ void band_order(int id, int mtiles, int ntiles, int& m, int& n) {
+  const int full = ntiles >> 3;
+  const int span = mtiles * 8;
+  if (id < full * span) {
+    const int band = id / span, rem = id - band * span;
+    m = rem >> 3;
+    n = band * 8 + (rem & 7);
+  } else {
+    const int rem = id - full * span, w = ntiles - full * 8;
+    m = rem / w;
+    n = full * 8 + rem % w;
   }
 }
 
-template <int KIND, int BM, int BN, bool DUAL, bool ACT>
-__global__ __launch_bounds__(NT, 1) void grouped_gemm_kernel(GemmParams p) {
-  constexpr int WM = BM / 2, WN = BN / 2;     // per-wave tile
-  constexpr int MB = WM / 32, NB = WN / 32;   // 32x32 MFMA blocks per wave
+// WAVES_M x WAVES_N wavefronts share the 256x256 tile (4 = one per SIMD, 8 = two per SIMD).
+template <int KIND, bool DUAL, bool ACT, int WAVES_M, int WAVES_N>
+__global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void grouped_gemm_kernel(GemmParams p) {
+  constexpr int NWAVE = WAVES_M * WAVES_N;
+  constexpr int DPW = 16 / NWAVE;             // DMA loads per wave per operand per stage
+  constexpr int WTM = TILE / WAVES_M;         // per-wave tile rows (64)
+  constexpr int WTN = TILE / WAVES_N;         // per-wave tile columns (128)
+  constexpr int MB = WTM / 32;                // 32x32 MFMA blocks per wave along rows
+  constexpr int NB = WTN / 32;                // ... and along columns
   constexpr bool M_T = (KIND == KIND_DW);     // M-side operand stored contraction-major
   constexpr bool N_T = (KIND != KIND_DX);     // N-side operand stored contraction-major
-  static_assert(BM % 64 == 0 && BN % 64 == 0 && BM <= 256 && BN <= 256, "tile");
 
-  __shared__ __attribute__((aligned(16))) uint16_t lds[2][(BM + BN) * BK];
+  __shared__ __attribute__((aligned(16))) char lds[NSTAGE * STAGE];
   __shared__ int s_scan[256];
-  __shared__ int s_tile[2];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
 
-  // ---------------- tile -> (group, row range, column range, contraction range) ------------
+  // ---------------- tile -> (group, output rows, output columns, contraction range) ----------
   int g, mt, nt;
-  int64_t row_lo = 0, row_hi = 0;    // FWD/DX: output rows; DW: contraction rows
+  int64_t row_lo, row_hi;   // FWD/DX: output rows of the tile's group; DW: contraction rows
   if constexpr (KIND == KIND_DW) {
+    // Largest groups first (their tiles run longest).  When a group's tile count divides by 8,
+    // each XCD takes one contiguous eighth of every group (in band order), so the long tiles of a
+    // hot group spread over all XCDs while each XCD's L2 still sees neighbouring tiles.
     const int per_g = p.m_tiles * p.n_tiles;
-    g = blockIdx.x / per_g;
-    const int rem = blockIdx.x - g * per_g;
-    mt = rem % p.m_tiles;
-    nt = rem / p.m_tiles;
+    int slot, within;
+    if ((per_g & 7) == 0) {
+      const int c = per_g >> 3, x = blockIdx.x & 7, l = blockIdx.x >> 3;
+      slot = l / c;
+      within = x * c + (l - slot * c);
+    } else {
+      slot = blockIdx.x / per_g;
+      within = blockIdx.x - slot * per_g;
+    }
+    int kg = 0;
+    if (tid < p.G) kg = p.offsets[tid + 1] - p.offsets[tid];
+    if (tid < 256) s_scan[tid] = kg;
+    __syncthreads();
+    int rank = 0;
+    if (tid < p.G)
+      for (int h = 0; h < p.G; ++h) {
+        const int kh = s_scan[h];
+        rank += (kh > kg) || (kh == kg && h < tid);
+      }
+    __syncthreads();
+    if (tid < p.G) s_scan[rank] = tid;
+    __syncthreads();
+    g = s_scan[slot];
+    band_order(within, p.m_tiles, p.n_tiles, mt, nt);
     row_lo = p.offsets[g];
     row_hi = p.offsets[g + 1];
   } else {
-    const int mt_glob = blockIdx.x % p.mt_bound;
-    nt = blockIdx.x / p.mt_bound;
-    // inclusive scan of per-group row-tile counts (G <= 256)
     int cnt = 0;
-    if (tid < p.G) {
-      const int lo = p.offsets[tid], hi = p.offsets[tid + 1];
-      cnt = (hi - lo + BM - 1) / BM;
-    }
-    s_scan[tid] = cnt;
+    if (tid < p.G) cnt = (p.offsets[tid + 1] - p.offsets[tid] + TILE - 1) / TILE;
+    if (tid < 256) s_scan[tid] = cnt;
     __syncthreads();
     for (int off = 1; off < 256; off <<= 1) {
-      const int add = tid >= off ? s_scan[tid - off] : 0;
+      const int add = (tid < 256 && tid >= off) ? s_scan[tid - off] : 0;
       __syncthreads();
-      s_scan[tid] += add;
+      if (tid < 256) s_scan[tid] += add;
       __syncthreads();
     }
-    const int total = s_scan[255];
-    if (mt_glob >= total) return;  // uniform over the workgroup
-    const int ng = __syncthreads_count(tid < p.G && s_scan[tid] <= mt_glob);
-    g = ng;
+    const int mtotal = s_scan[255];
+    const int ntiles_all = mtotal * p.n_tiles;
+    if ((int)blockIdx.x >= ntiles_all) return;   // uniform over the workgroup
+    int mt_glob;
+    band_order(xcd_remap(blockIdx.x, ntiles_all), mtotal, p.n_tiles, mt_glob, nt);
+    g = __syncthreads_count(tid < p.G && s_scan[tid] <= mt_glob);
     mt = mt_glob - (g > 0 ? s_scan[g - 1] : 0);
-    row_lo = (int64_t)p.offsets[g] + (int64_t)mt * BM;
+    row_lo = (int64_t)p.offsets[g] + (int64_t)mt * TILE;
     row_hi = p.offsets[g + 1];
   }
 
-  // ---------------- per-thread load descriptors ----------------------------------------------
+  // values derived through LDS are uniform by construction; say so to the compiler so that buffer
+  // resources and LDS DMA addresses stay in scalar registers
+  g = __builtin_amdgcn_readfirstlane(g);
+  mt = __builtin_amdgcn_readfirstlane(mt);
+  nt = __builtin_amdgcn_readfirstlane(nt);
+  row_lo = __builtin_amdgcn_readfirstlane((int)row_lo);
+  row_hi = __builtin_amdgcn_readfirstlane((int)row_hi);
+
+  // ---------------- DMA descriptors ------------------------------------------------------------
+  // Each stage stages 256 x 32 of both operands in 16 DMA loads of 1 KiB per operand; wave w
+  // issues loads I = DPW*w .. DPW*w + DPW-1.  Direct side: load I covers rows 16I .. 16I+15 (lane
+  // -> row 16I + lane/4, chunk (lane&3) ^ swz_d(row) = (lane&3) ^ swz_d(lane/4)).  mn side: load I
+  // covers column group I/4, contraction rows 8(I%4) .. +7 (lane -> row 8(I%4) + lane/8, chunk
+  // (lane&7) ^ swz_t(row)).
+  const int lds0 = (int)(size_t)(const __attribute__((address_space(3))) char*)lds;
+
   // M side
-  constexpr int M_DIRECT_LOADS = BM / 32;     // direct: 16-byte chunks per thread
-  int64_t m_off[M_T ? 1 : M_DIRECT_LOADS];    // element offset of each loaded row
-  const uint16_t* mt_ptr = nullptr;           // transposed: column base
-  bool mt_live = false;
-  int m_kb = 0, m_mb = 0;
+  const char* m_src = nullptr;    // base of the contraction window at c = 0
+  const char* m_src2 = nullptr;   // DX dual: second half of the contraction
+  int64_t m_ld;                   // elements per memory row
+  int m_voff[DPW];
   if constexpr (!M_T) {
-    const int64_t ld = (KIND == KIND_FWD) ? p.K : p.N;
+    m_ld = (KIND == KIND_FWD) ? p.K : p.N;
+    const int64_t rows_valid = row_hi - row_lo;   // > 0
+    m_src = reinterpret_cast<const char*>(p.a + row_lo * m_ld);
+    if constexpr (KIND == KIND_DX && DUAL) m_src2 = reinterpret_cast<const char*>(p.a2 + row_lo * m_ld);
 #pragma unroll
-    for (int i = 0; i < M_DIRECT_LOADS; ++i) {
-      int64_t r = row_lo + tid / 8 + 32 * i;
-      if (r > row_hi - 1) r = row_hi - 1;
-      m_off[i] = r * ld + 8 * (tid & 7);
+    for (int i = 0; i < DPW; ++i) {
+      int64_t r = 16 * (DPW * wave + i) + (lane >> 2);
+      if (r > rows_valid - 1) r = rows_valid - 1;
+      const int c = (lane & 3) ^ swz_d(lane >> 2);
+      m_voff[i] = (int)((r * m_ld + 8 * c) * 2);
     }
   } else {
-    // DW: A[r, m], columns m in [mt*BM, mt*BM+BM)
-    mt_live = tid < BM;
-    m_mb = tid % (BM / 8);
-    m_kb = tid / (BM / 8);
-    int64_t col = (int64_t)mt * BM + 8 * m_mb;
-    if (col > p.K - 8) col = p.K - 8;
-    mt_ptr = p.a + col;
+    m_ld = p.K;
+    const int grp = (DPW * wave) / 4;
+    int64_t col0 = (int64_t)mt * TILE + 64 * grp;
+    if (col0 > p.K - 64) col0 = p.K - 64;
+    m_src = reinterpret_cast<const char*>(p.a + row_lo * m_ld + col0);
+#pragma unroll
+    for (int i = 0; i < DPW; ++i) {
+      const int k = 8 * ((DPW * wave + i) & 3) + (lane >> 3);
+      const int c = (lane & 7) ^ swz_t(k);
+      m_voff[i] = (int)((k * m_ld + 8 * c) * 2);
+    }
   }
   // N side
-  constexpr int N_DIRECT_LOADS = BN / 32;
-  int64_t n_off[N_T ? 1 : N_DIRECT_LOADS];
-  const uint16_t* nt_ptr = nullptr;
-  bool nt_live = false;
-  int n_kb = 0, n_mb = 0;
+  const char* n_src = nullptr;
+  const char* n_src2 = nullptr;
+  int64_t n_ld;
+  int n_voff[DPW];
   if constexpr (!N_T) {
-    // DX: B[g][kk, c], kk = output column
+    // DX: B[g][kk, c]; the tile's output columns kk = nt*TILE + row, clamped
+    n_ld = p.N;
+    n_src = reinterpret_cast<const char*>(p.b + (int64_t)g * p.K * p.N);
+    if constexpr (DUAL) n_src2 = reinterpret_cast<const char*>(p.b2 + (int64_t)g * p.K * p.N);
 #pragma unroll
-    for (int i = 0; i < N_DIRECT_LOADS; ++i) {
-      int64_t kk = (int64_t)nt * BN + tid / 8 + 32 * i;
+    for (int i = 0; i < DPW; ++i) {
+      int64_t kk = (int64_t)nt * TILE + 16 * (DPW * wave + i) + (lane >> 2);
       if (kk > p.K - 1) kk = p.K - 1;
-      n_off[i] = (int64_t)g * p.K * p.N + kk * p.N + 8 * (tid & 7);
+      const int c = (lane & 3) ^ swz_d(lane >> 2);
+      n_voff[i] = (int)((kk * p.N + 8 * c) * 2);
     }
   } else {
-    nt_live = tid < BN;
-    n_mb = tid % (BN / 8);
-    n_kb = tid / (BN / 8);
-    const int v0 = 8 * n_mb;  // virtual column of this thread's block
-    const int64_t ncols = (KIND == KIND_FWD) ? p.N : p.N;
-    int64_t col;
+    // this wave's column group: in dual mode groups 0,2 come from the first source and 1,3 from
+    // the second, at the same output columns
+    n_ld = p.N;
+    const int grp = (DPW * wave) / 4;
+    int64_t col0;
     const uint16_t* src = p.b;
     if constexpr (DUAL) {
-      const int w = v0 / WN, u = v0 % WN;
-      col = (int64_t)nt * (BN / 2) + w * (WN / 2) + (u % (WN / 2));
-      if (u >= WN / 2) src = p.b2;
+      col0 = (int64_t)nt * (TILE / 2) + 64 * (grp >> 1);
+      if (grp & 1) src = p.b2;
     } else {
-      col = (int64_t)nt * BN + v0;
+      col0 = (int64_t)nt * TILE + 64 * grp;
     }
-    if (col > ncols - 8) col = ncols - 8;
-    nt_ptr = src + col + ((KIND == KIND_FWD) ? (int64_t)g * p.K * p.N : 0);
+    if (col0 > p.N - 64) col0 = p.N - 64;
+    const int64_t rowbase = (KIND == KIND_FWD) ? (int64_t)g * p.K : row_lo;
+    n_src = reinterpret_cast<const char*>(src + rowbase * p.N + col0);
+#pragma unroll
+    for (int i = 0; i < DPW; ++i) {
+      const int k = 8 * ((DPW * wave + i) & 3) + (lane >> 3);
+      const int c = (lane & 7) ^ swz_t(k);
+      n_voff[i] = (int)((k * n_ld + 8 * c) * 2);
+    }
   }
 
   // contraction extent
@@ -192,86 +305,67 @@ __global__ __launch_bounds__(NT, 1) void grouped_gemm_kernel(GemmParams p) {
   else c_len = row_hi - row_lo;
   const int nsteps = (int)((c_len + BK - 1) / BK);
 
-  // ---------------- global -> register loads for one k-step ----------------------------------
-  u32x4 mreg[M_T ? 8 : M_DIRECT_LOADS];
-  u32x4 nreg[N_T ? 8 : N_DIRECT_LOADS];
-
-  auto load_step = [&](int s) {
+  // buffer resources of step s for the M and N operands
+  auto rsrc_m = [&](int s) {
     const int64_t c0 = (int64_t)s * BK;
+    if (s >= nsteps) return make_rsrc(m_src, 0);   // past the end: every load is out of range
     if constexpr (!M_T) {
-      const uint16_t* base = p.a;
+      const char* base = m_src;
       int64_t cc = c0;
       if constexpr (KIND == KIND_DX && DUAL) {
-        if (c0 >= p.N) { base = p.a2; cc = c0 - p.N; }
+        if (c0 >= p.N) { base = m_src2; cc = c0 - p.N; }
       }
-#pragma unroll
-      for (int i = 0; i < M_DIRECT_LOADS; ++i) mreg[i] = ld16(base + m_off[i] + cc);
+      return make_rsrc(base + cc * 2, (int64_t)0x7fffffff);
     } else {
-      if (mt_live) {
-        const int64_t r0 = row_lo + c0 + 8 * m_kb;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const int64_t r = r0 + i;
-          mreg[i] = (r < row_hi) ? ld16(mt_ptr + r * p.K) : u32x4{0u, 0u, 0u, 0u};
-        }
-      }
+      const int64_t left = c_len - c0;
+      return make_rsrc(m_src + c0 * m_ld * 2, (left < BK ? left : BK) * m_ld * 2);
     }
+  };
+  auto rsrc_n = [&](int s) {
+    const int64_t c0 = (int64_t)s * BK;
+    if (s >= nsteps) return make_rsrc(n_src, 0);
     if constexpr (!N_T) {
-      const uint16_t* base = p.b;
+      const char* base = n_src;
       int64_t cc = c0;
       if constexpr (DUAL) {
-        if (c0 >= p.N) { base = p.b2; cc = c0 - p.N; }
+        if (c0 >= p.N) { base = n_src2; cc = c0 - p.N; }
       }
-#pragma unroll
-      for (int i = 0; i < N_DIRECT_LOADS; ++i) nreg[i] = ld16(base + n_off[i] + cc);
+      return make_rsrc(base + cc * 2, (int64_t)0x7fffffff);
     } else {
-      if (nt_live) {
-        if constexpr (KIND == KIND_FWD) {
-          const int64_t r0 = c0 + 8 * n_kb;
-#pragma unroll
-          for (int i = 0; i < 8; ++i) nreg[i] = ld16(nt_ptr + (r0 + i) * p.N);
-        } else {
-          const int64_t r0 = row_lo + c0 + 8 * n_kb;
-#pragma unroll
-          for (int i = 0; i < 8; ++i) {
-            const int64_t r = r0 + i;
-            nreg[i] = (r < row_hi) ? ld16(nt_ptr + r * p.N) : u32x4{0u, 0u, 0u, 0u};
-          }
-        }
-      }
+      const int64_t left = c_len - c0;
+      return make_rsrc(n_src + c0 * n_ld * 2, (left < BK ? left : BK) * n_ld * 2);
     }
+  };
+  // load d (0 .. 2*DPW-1) of this wave for a step whose slot starts at LDS byte slot_lds
+  auto dma_one = [&](int d, const i32x4& rm, const i32x4& rn, int slot_lds) {
+    if (d < DPW) dma16(rm, m_voff[d], slot_lds + (DPW * wave + d) * 1024);
+    else dma16(rn, n_voff[d - DPW], slot_lds + OPND + (DPW * wave + d - DPW) * 1024);
+  };
+  auto issue = [&](int s) {
+    const int slot_lds = lds0 + (s & (NSTAGE - 1)) * STAGE;
+    const i32x4 rm = rsrc_m(s), rn = rsrc_n(s);
+#pragma unroll
+    for (int d = 0; d < 2 * DPW; ++d) dma_one(d, rm, rn, slot_lds);
   };
 
-  auto store_step = [&](int buf) {
-    uint16_t* ms = &lds[buf][0];
-    uint16_t* ns = &lds[buf][BM * BK];
-    if constexpr (!M_T) {
-#pragma unroll
-      for (int i = 0; i < M_DIRECT_LOADS; ++i)
-        *reinterpret_cast<u32x4*>(ms + lds_off(tid / 8 + 32 * i, tid & 7)) = mreg[i];
-    } else {
-      if (mt_live) {
-        u32x4 t[8];
-        transpose8x8(mreg, t);
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-          *reinterpret_cast<u32x4*>(ms + lds_off(8 * m_mb + j, m_kb)) = t[j];
-      }
-    }
-    if constexpr (!N_T) {
-#pragma unroll
-      for (int i = 0; i < N_DIRECT_LOADS; ++i)
-        *reinterpret_cast<u32x4*>(ns + lds_off(tid / 8 + 32 * i, tid & 7)) = nreg[i];
-    } else {
-      if (nt_live) {
-        u32x4 t[8];
-        transpose8x8(nreg, t);
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-          *reinterpret_cast<u32x4*>(ns + lds_off(8 * n_mb + j, n_kb)) = t[j];
-      }
-    }
+  // ---------------- fragment reads ---------------------------------------------------------------
+  // direct side: rows R0 + 32j + lane%32, chunk 2ks + lane/32
+  // mn side (transposing reads): lane group G = lane/16, j16 = lane%16 reads contraction row
+  //   16ks + 8(G>>1) + j16/4 (+4 for the second read), columns 32j + 16(G&1) + 4(j16&3) .. +3
+  const int l32 = lane & 31, fh = lane >> 5;
+  const int G16 = lane >> 4, j16 = lane & 15, kq = j16 >> 2, cq = j16 & 3;
+  auto d_addr = [&](int R0, int ks) {
+    return (R0 + l32) * 64 + (((2 * ks + fh) ^ swz_d(l32)) << 4);
   };
+  auto t_addr = [&](int grp0, int jodd) {
+    return grp0 * 4096 + (8 * (G16 >> 1) + kq) * 128 +
+           (((4 * jodd + 2 * (G16 & 1) + (cq >> 1)) ^ (2 * kq)) << 4) + (cq & 1) * 8;
+  };
+  // byte offsets within a stage (M side at 0, N side at OPND), per ks (direct) or j parity (mn)
+  const int m_a0 = M_T ? t_addr(wm * WTM / 64, 0) : d_addr(wm * WTM, 0);
+  const int m_a1 = M_T ? t_addr(wm * WTM / 64, 1) : d_addr(wm * WTM, 1);
+  const int n_a0 = OPND + (N_T ? t_addr(wn * WTN / 64, 0) : d_addr(wn * WTN, 0));
+  const int n_a1 = OPND + (N_T ? t_addr(wn * WTN / 64, 1) : d_addr(wn * WTN, 1));
 
   f32x16 acc[MB][NB];
 #pragma unroll
@@ -279,58 +373,94 @@ __global__ __launch_bounds__(NT, 1) void grouped_gemm_kernel(GemmParams p) {
 #pragma unroll
     for (int j = 0; j < NB; ++j) acc[i][j] = f32x16{};
 
-  const int frag_row = lane & 31;
-  const int frag_ch = lane >> 5;
-
-  if (nsteps > 0) {
-    load_step(0);
-    store_step(0);
-    __syncthreads();
-  }
-  for (int s = 0; s < nsteps; ++s) {
-    const int buf = s & 1;
-    if (s + 1 < nsteps) load_step(s + 1);
-    const uint16_t* ms = &lds[buf][0];
-    const uint16_t* ns = &lds[buf][BM * BK];
+  bf16x8 fa[2][NB], fb[2][MB];   // N-side (MFMA A) and M-side (MFMA B) fragments, two sets
+  auto load_frags = [&](int set, int slot, int ks) {
+    const char* st = lds + slot * STAGE;
 #pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      const int ch = 2 * ks + frag_ch;
-      bf16x8 af[NB], bfr[MB];
+    for (int j = 0; j < NB; ++j) {
+      if constexpr (N_T)
+        fa[set][j] = lds_read_tr(st + ((j & 1) ? n_a1 : n_a0) + (j >> 1) * 4096 + ks * 2048);
+      else
+        fa[set][j] = lds_read16(st + (ks ? n_a1 : n_a0) + j * 2048);
+    }
+#pragma unroll
+    for (int i = 0; i < MB; ++i) {
+      if constexpr (M_T)
+        fb[set][i] = lds_read_tr(st + ((i & 1) ? m_a1 : m_a0) + (i >> 1) * 4096 + ks * 2048);
+      else
+        fb[set][i] = lds_read16(st + (ks ? m_a1 : m_a0) + i * 2048);
+    }
+  };
+  auto mfmas = [&](int set) {
+#pragma unroll
+    for (int i = 0; i < MB; ++i)
 #pragma unroll
       for (int j = 0; j < NB; ++j)
-        af[j] = *reinterpret_cast<const bf16x8*>(ns + lds_off(wn * WN + 32 * j + frag_row, ch));
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[set][j], fb[set][i], acc[i][j], 0, 0, 0);
+  };
+  // the same, with the 2*DPW refill loads of step `s` spread one after every second MFMA so the
+  // vector-memory and LDS-write work of the refill overlaps the matrix cores
+  static_assert(MB * NB >= 4 * DPW, "need two MFMAs per refill load");
+  auto mfmas_refill = [&](int set, int s) {
+    const int slot_lds = lds0 + (s & (NSTAGE - 1)) * STAGE;
+    const i32x4 rm = rsrc_m(s), rn = rsrc_n(s);
 #pragma unroll
-      for (int i = 0; i < MB; ++i)
-        bfr[i] = *reinterpret_cast<const bf16x8*>(ms + lds_off(wm * WM + 32 * i + frag_row, ch));
+    for (int i = 0; i < MB; ++i)
 #pragma unroll
-      for (int i = 0; i < MB; ++i)
+      for (int j = 0; j < NB; ++j) {
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[set][j], fb[set][i], acc[i][j], 0, 0, 0);
+        const int m = i * NB + j;
+        if ((m & 1) && (m >> 1) < 2 * DPW) {
+          dma_one(m >> 1, rm, rn, slot_lds);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+  };
+
+  // ---------------- pipelined main loop ---------------------------------------------------------
+  // Stage s is read in two halves (ks = 0, 1).  Between them every wave waits for its own loads
+  // of stage s+1 (at most two later stages may stay in flight), then one barrier makes all of
+  // stage s+1 visible and frees stage s's slot (its reads have completed); the slot is refilled
+  // with stage s+4 during the second half.  Refills past the last stage use an empty buffer
+  // resource (no memory access), which keeps the wait counts the same on every iteration.
+  if (nsteps > 0) {
 #pragma unroll
-        for (int j = 0; j < NB; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[j], bfr[i], acc[i][j], 0, 0, 0);
-    }
-    if (s + 1 < nsteps) store_step(buf ^ 1);
+    for (int s = 0; s < NSTAGE; ++s) issue(s);
+    wait_vm<(NSTAGE - 1) * 2 * DPW>();
     __syncthreads();
+    load_frags(0, 0, 0);
   }
+  for (int s = 0; s < nsteps; ++s) {
+    const int slot = s & (NSTAGE - 1);
+    load_frags(1, slot, 1);
+    mfmas(0);
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vm<(NSTAGE - 2) * 2 * DPW>();
+    __syncthreads();
+    load_frags(0, (s + 1) & (NSTAGE - 1), 0);   // unused after the last stage
+    __builtin_amdgcn_sched_barrier(0);
+    mfmas_refill(1, s + NSTAGE);
+  }
+  wait_vm<0>();
 
   // ---------------- epilogue ------------------------------------------------------------------
-  // lane holds output row (wm*WM + 32*i + lane%32) and columns wn*WN + 32*j + 8*q + 4*(lane/32) + 0..3
-  const int col_in = 4 * (lane >> 5);
+  // lane holds output row (wm*WTM + 32*i + lane%32) and columns wn*WTN + 32*j + 8*q + 4*(lane/32) + 0..3
+  const int col_in = 4 * fh;
 #pragma unroll
   for (int i = 0; i < MB; ++i) {
-    const int mrow = wm * WM + 32 * i + frag_row;
+    const int mrow = wm * WTM + 32 * i + l32;
     if constexpr (KIND == KIND_DW) {
-      const int64_t m = (int64_t)mt * BM + mrow;
+      const int64_t m = (int64_t)mt * TILE + mrow;
       if (m >= p.K) continue;
 #pragma unroll
       for (int j = 0; j < NB; ++j) {
         float* dst;
         int64_t col;
         if constexpr (DUAL) {
-          const int half = (j >= NB / 2);
-          col = (int64_t)nt * (BN / 2) + wn * (WN / 2) + 32 * (j % (NB / 2));
-          dst = static_cast<float*>(half ? p.out2 : p.out);
+          col = (int64_t)nt * (TILE / 2) + wn * (WTN / 2) + 32 * (j % (NB / 2));
+          dst = static_cast<float*>(j >= NB / 2 ? p.out2 : p.out);
         } else {
-          col = (int64_t)nt * BN + wn * WN + 32 * j;
+          col = (int64_t)nt * TILE + wn * WTN + 32 * j;
           dst = static_cast<float*>(p.out);
         }
         dst += (int64_t)g * p.K * p.N + m * p.N;
@@ -352,7 +482,7 @@ __global__ __launch_bounds__(NT, 1) void grouped_gemm_kernel(GemmParams p) {
         for (int j = 0; j < NB; ++j)
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            const int64_t n = (int64_t)nt * BN + wn * WN + 32 * j + 8 * q + col_in;
+            const int64_t n = (int64_t)nt * TILE + wn * WTN + 32 * j + 8 * q + col_in;
             if (n < p.K) {
               uint2 v;
               v.x = pack_bf16(acc[i][j][4 * q], acc[i][j][4 * q + 1]);
@@ -368,7 +498,7 @@ __global__ __launch_bounds__(NT, 1) void grouped_gemm_kernel(GemmParams p) {
         for (int j = 0; j < NB / 2; ++j)
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            const int64_t n = (int64_t)nt * (BN / 2) + wn * (WN / 2) + 32 * j + 8 * q + col_in;
+            const int64_t n = (int64_t)nt * (TILE / 2) + wn * (WTN / 2) + 32 * j + 8 * q + col_in;
             if (n < p.N) {
               uint2 vg, vu;
               vg.x = pack_bf16(acc[i][j][4 * q], acc[i][j][4 * q + 1]);
@@ -393,7 +523,7 @@ __global__ __launch_bounds__(NT, 1) void grouped_gemm_kernel(GemmParams p) {
         for (int j = 0; j < NB; ++j)
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            const int64_t n = (int64_t)nt * BN + wn * WN + 32 * j + 8 * q + col_in;
+            const int64_t n = (int64_t)nt * TILE + wn * WTN + 32 * j + 8 * q + col_in;
             if (n < p.N) {
               uint2 v;
               v.x = pack_bf16(acc[i][j][4 * q], acc[i][j][4 * q + 1]);
@@ -406,13 +536,18 @@ __global__ __launch_bounds__(NT, 1) void grouped_gemm_kernel(GemmParams p) {
   }
 }
 
-constexpr int kBM = 256;
-constexpr int kBN = 256;
+constexpr int kBM = TILE;
+constexpr int kBN = TILE;
+
+// wave layout per product: 4 wavefronts (128x128 each) where the transposing LDS reads dominate,
+// 8 (64x128 each, two per SIMD) for dX whose operands are both read 16 bytes per lane
+template <int KIND> struct Waves { static constexpr int M = (KIND == KIND_DX) ? 4 : 2, N = 2; };
 
 template <int KIND, bool DUAL, bool ACT>
 moe_status launch(const GemmParams& p, unsigned grid, hipStream_t stream, const char* name) {
   if (grid == 0) return MOE_SUCCESS;
-  grouped_gemm_kernel<KIND, kBM, kBN, DUAL, ACT><<<grid, NT, 0, stream>>>(p);
+  constexpr int WM = Waves<KIND>::M, WN = Waves<KIND>::N;
+  grouped_gemm_kernel<KIND, DUAL, ACT, WM, WN><<<grid, 64 * WM * WN, 0, stream>>>(p);
   return check_launch(name);
 }
 
