@@ -19,25 +19,34 @@ __global__ __launch_bounds__(256) void swiglu_kernel(const u32x4* __restrict__ h
   }
 }
 
+__device__ __forceinline__ void swiglu_bwd8(const u32x4& hg, const u32x4& hu, const u32x4& da,
+                                            u32x4& dhg, u32x4& dhu) {
+  float g[8], u[8], d[8], og[8], ou[8];
+  unpack8(hg, g);
+  unpack8(hu, u);
+  unpack8(da, d);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const float s = sigmoid_f32(g[j]);
+    ou[j] = d[j] * g[j] * s;
+    og[j] = d[j] * u[j] * s * (1.0f + g[j] * (1.0f - s));
+  }
+  dhg = pack8(og);
+  dhu = pack8(ou);
+}
+
+// one 16-byte vector (8 elements) per thread, no grid-stride loop
 __global__ __launch_bounds__(256) void swiglu_bwd_kernel(const u32x4* __restrict__ hg,
                                                          const u32x4* __restrict__ hu,
                                                          const u32x4* __restrict__ da,
                                                          u32x4* __restrict__ dhg,
                                                          u32x4* __restrict__ dhu, int64_t n8) {
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n8; i += (int64_t)gridDim.x * 256) {
-    float g[8], u[8], d[8], og[8], ou[8];
-    unpack8(hg[i], g);
-    unpack8(hu[i], u);
-    unpack8(da[i], d);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const float s = sigmoid_f32(g[j]);
-      ou[j] = d[j] * g[j] * s;
-      og[j] = d[j] * u[j] * s * (1.0f + g[j] * (1.0f - s));
-    }
-    dhg[i] = pack8(og);
-    dhu[i] = pack8(ou);
-  }
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n8) return;
+  u32x4 a, b;
+  swiglu_bwd8(hg[i], hu[i], da[i], a, b);
+  dhg[i] = a;
+  dhu[i] = b;
 }
 
 // y[t] = bf16(sum_j w[t,j] * y_perm[row_of_slot[t*k+j]] + add[t])
@@ -91,8 +100,9 @@ __global__ __launch_bounds__(256) void combine_kernel(const u32x4* __restrict__ 
   }
 }
 
-// dy_perm[row] = bf16(w * dy[t]); d_w[t,j] = <dy[t], y_perm[row]>
-template <int U>
+// dy_perm[row] = bf16(w * dy[t]); d_w[t,j] = <dy[t], y_perm[row]>.  The token's choices are taken
+// eight at a time; for each group the dY row is read once per chunk and the partial dot products
+// stay in registers until one wavefront reduction per choice at the end.
 __global__ __launch_bounds__(256) void combine_bwd_kernel(const u32x4* __restrict__ dy,
                                                           const float* __restrict__ w,
                                                           const int32_t* __restrict__ row_of_slot,
@@ -100,46 +110,50 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(const u32x4* __restric
                                                           int64_t T, int64_t chunks, int k,
                                                           u32x4* __restrict__ dy_perm,
                                                           float* __restrict__ d_w) {
+  constexpr int J = 8;
   const int lane = threadIdx.x & 63;
   const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;
   const u32x4* src = dy + t * chunks;
-  for (int j = 0; j < k; ++j) {
-    const int64_t r = row_of_slot[t * k + j];
-    const float wj = w[t * k + j];
-    float dot = 0.f;
-    for (int64_t c0 = 0; c0 < chunks; c0 += 64 * U) {
-      u32x4 v[U], yv[U];
+  for (int j0 = 0; j0 < k; j0 += J) {
+    const int nj = k - j0 < J ? k - j0 : J;
+    int64_t row[J];
+    float wj[J], dot[J];
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int64_t c = c0 + u * 64 + lane;
-        if (c < chunks) {
-          v[u] = src[c];
-          if (y_perm) yv[u] = y_perm[r * chunks + c];
-        }
-      }
+    for (int j = 0; j < J; ++j) {
+      row[j] = j < nj ? row_of_slot[t * k + j0 + j] : 0;
+      wj[j] = j < nj ? w[t * k + j0 + j] : 0.f;
+      dot[j] = 0.f;
+    }
+    for (int64_t c = lane; c < chunks; c += 64) {
+      float f[8];
+      unpack8(src[c], f);
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int64_t c = c0 + u * 64 + lane;
-        if (c < chunks) {
-          float f[8], o[8];
-          unpack8(v[u], f);
+      for (int j = 0; j < J; ++j) {
+        if (j < nj) {
+          float o[8];
 #pragma unroll
-          for (int i = 0; i < 8; ++i) o[i] = wj * f[i];
-          dy_perm[r * chunks + c] = pack8(o);
+          for (int i = 0; i < 8; ++i) o[i] = wj[j] * f[i];
+          dy_perm[row[j] * chunks + c] = pack8(o);
           if (y_perm) {
             float yf[8];
-            unpack8(yv[u], yf);
+            unpack8(y_perm[row[j] * chunks + c], yf);
 #pragma unroll
-            for (int i = 0; i < 8; ++i) dot += f[i] * yf[i];
+            for (int i = 0; i < 8; ++i) dot[j] += f[i] * yf[i];
           }
         }
       }
     }
     if (y_perm && d_w) {
 #pragma unroll
-      for (int off = 32; off > 0; off >>= 1) dot += __shfl_xor(dot, off);
-      if (lane == 0) d_w[t * k + j] = dot;
+      for (int j = 0; j < J; ++j) {
+        if (j < nj) {
+          float v = dot[j];
+#pragma unroll
+          for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+          if (lane == 0) d_w[t * k + j0 + j] = v;
+        }
+      }
     }
   }
 }
@@ -182,7 +196,9 @@ extern "C" moe_status moe_swiglu_bwd(const moe_bf16* h_gate, const moe_bf16* h_u
       !aligned16(dh_up))
     return fail(MOE_ERROR_INVALID_VALUE, "moe_swiglu_bwd: pointers must be 16-byte aligned");
   const int64_t n8 = rows * f / 8;
-  swiglu_bwd_kernel<<<elementwise_grid(n8), 256, 0, stream>>>(
+  if ((n8 + 255) / 256 > 0x7fffffff)
+    return fail(MOE_ERROR_NOT_SUPPORTED, "moe_swiglu_bwd: rows*f too large");
+  swiglu_bwd_kernel<<<(unsigned)((n8 + 255) / 256), 256, 0, stream>>>(
       reinterpret_cast<const u32x4*>(h_gate), reinterpret_cast<const u32x4*>(h_up),
       reinterpret_cast<const u32x4*>(d_act), reinterpret_cast<u32x4*>(dh_gate),
       reinterpret_cast<u32x4*>(dh_up), n8);
@@ -221,7 +237,7 @@ extern "C" moe_status moe_unpermute_combine_bwd(const moe_bf16* dy, const float*
   if (!aligned16(dy) || !aligned16(dy_perm) || (y_perm && !aligned16(y_perm)))
     return fail(MOE_ERROR_INVALID_VALUE, "moe_unpermute_combine_bwd: pointers must be 16-byte aligned");
   const int64_t chunks = d / 8;
-  combine_bwd_kernel<4><<<(unsigned)((T + 3) / 4), 256, 0, stream>>>(
+  combine_bwd_kernel<<<(unsigned)((T + 3) / 4), 256, 0, stream>>>(
       reinterpret_cast<const u32x4*>(dy), topk_w, row_of_slot,
       reinterpret_cast<const u32x4*>(y_perm), T, chunks, k, reinterpret_cast<u32x4*>(dy_perm),
       d_topk_w);

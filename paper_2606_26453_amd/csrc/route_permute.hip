@@ -188,9 +188,10 @@ struct RangePlan {
 };
 
 RangePlan plan_ranges(int64_t R) {
-  // ranges of S slots, at most 1024 of them
-  int64_t S = 1024 * ((R + (1024 * 1024) - 1) / (1024 * 1024));
-  if (S < 1024) S = 1024;
+  // ranges of S slots (a multiple of 256), at most 4096 of them: short ranges keep the
+  // sequential part of the ballot ranking short and give the scatter many wavefronts
+  int64_t S = 256 * ((R + 256 * 4096 - 1) / (256 * 4096));
+  if (S < 256) S = 256;
   return {S, (int)((R + S - 1) / S)};
 }
 
