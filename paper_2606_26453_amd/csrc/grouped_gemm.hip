@@ -136,7 +136,7 @@ __device__ __forceinline__ void band_order(int id, int mtiles, int ntiles, int& 
 }
 
 // WAVES_M x WAVES_N wavefronts share the 256x256 tile (4 = one per SIMD, 8 = two per SIMD).
-template <int KIND, bool DUAL, bool ACT, int WAVES_M, int WAVES_N>
+template <int KIND, bool DUAL, bool ACT, int WAVES_M, int WAVES_N, bool PINGPONG>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void grouped_gemm_kernel(GemmParams p) {
   constexpr int NWAVE = WAVES_M * WAVES_N;
   constexpr int DPW = 16 / NWAVE;             // DMA loads per wave per operand per stage
@@ -373,7 +373,8 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void grouped_gemm_kernel
 #pragma unroll
     for (int j = 0; j < NB; ++j) acc[i][j] = f32x16{};
 
-  bf16x8 fa[2][NB], fb[2][MB];   // N-side (MFMA A) and M-side (MFMA B) fragments, two sets
+  // fragment sets: 0/1 hold the first K-half of alternating stages, 2 the second K-half
+  bf16x8 fa[3][NB], fb[3][MB];   // N-side (MFMA A) and M-side (MFMA B) fragments
   auto load_frags = [&](int set, int slot, int ks) {
     const char* st = lds + slot * STAGE;
 #pragma unroll
@@ -391,12 +392,12 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void grouped_gemm_kernel
         fb[set][i] = lds_read16(st + (ks ? m_a1 : m_a0) + i * 2048);
     }
   };
-  auto mfmas = [&](int set) {
+  // MFMAs m0 .. m1-1 of the MB x NB block grid (row-major order) with fragment set `set`
+  auto mfmas = [&](int set, int m0, int m1) {
 #pragma unroll
-    for (int i = 0; i < MB; ++i)
-#pragma unroll
-      for (int j = 0; j < NB; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[set][j], fb[set][i], acc[i][j], 0, 0, 0);
+    for (int m = m0; m < m1; ++m)
+      acc[m / NB][m % NB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[set][m % NB], fb[set][m / NB],
+                                                                   acc[m / NB][m % NB], 0, 0, 0);
   };
   // the same, with the 2*DPW refill loads of step `s` spread one after every second MFMA so the
   // vector-memory and LDS-write work of the refill overlaps the matrix cores
@@ -418,30 +419,90 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void grouped_gemm_kernel
   };
 
   // ---------------- pipelined main loop ---------------------------------------------------------
-  // Stage s is read in two halves (ks = 0, 1).  Between them every wave waits for its own loads
-  // of stage s+1 (at most two later stages may stay in flight), then one barrier makes all of
-  // stage s+1 visible and frees stage s's slot (its reads have completed); the slot is refilled
-  // with stage s+4 during the second half.  Refills past the last stage use an empty buffer
-  // resource (no memory access), which keeps the wait counts the same on every iteration.
-  if (nsteps > 0) {
+  // Per stage s (two K-halves of 16):
+  //   a. read the second half of stage s into set 2
+  //   b. first MFMAs of the first half (set s&1)
+  //   c. wait for this wave's loads of stage s+1 (two later stages may stay in flight); barrier:
+  //      stage s+1 is now visible to all, and every read of stage s has completed
+  //   d. read the first half of stage s+1 into set (s+1)&1
+  //   e. remaining MFMAs of the first half, then the second half (set 2) with the refill of stage
+  //      s's slot by stage s+4 spread between them
+  // so the reads issued in (d) have ~3/4 of a stage of MFMAs to land before they are used.  Refills
+  // past the last stage use an empty buffer resource (no memory access; the slot fills with
+  // zeros), which keeps the wait counts the same on every iteration; the loop runs an even number
+  // of stages, a trailing all-zero stage adding nothing.
+  constexpr int MFMA_HALF = MB * NB;
+  if constexpr (!PINGPONG) {
+    constexpr int MFMA_HALF = MB * NB;
+    constexpr int SPLIT = MFMA_HALF / 2;
+    auto stage_body = [&](int s, int cur) {
+      const int slot = s & (NSTAGE - 1);
+      load_frags(2, slot, 1);
+      mfmas(cur, 0, SPLIT);
+      __builtin_amdgcn_sched_barrier(0);
+      wait_vm<(NSTAGE - 2) * 2 * DPW>();
+      __syncthreads();
+      load_frags(cur ^ 1, (s + 1) & (NSTAGE - 1), 0);   // unused after the last stage
+      __builtin_amdgcn_sched_barrier(0);
+      mfmas(cur, SPLIT, MFMA_HALF);
+      mfmas_refill(2, s + NSTAGE);
+    };
+    if (nsteps > 0) {
+  #pragma unroll
+      for (int s = 0; s < NSTAGE; ++s) issue(s);
+      wait_vm<(NSTAGE - 1) * 2 * DPW>();
+      __syncthreads();
+      load_frags(0, 0, 0);
+    }
+    for (int s = 0; s < nsteps; s += 2) {
+      stage_body(s, 0);
+      stage_body(s + 1, 1);
+    }
+    wait_vm<0>();
+  } else {
+    // Ping-pong (8 wavefronts, two per SIMD): wave group 0 (tile rows 0..127) and group 1 (rows
+    // 128..255) alternate every half stage between a compute phase (all MFMAs of one stage) and a
+    // memory phase (all fragment reads of the next stage + this group's DMA of stage s+3), so one
+    // wavefront of each SIMD feeds the matrix core while the other waits on LDS and memory.  Every
+    // half stage ends with one barrier; group 1 runs half a stage behind (one extra barrier at the
+    // start, one for group 0 at the end).  Before each barrier every wave waits until at most two
+    // of its DMA stages are in flight: stage t is read (group 0 first) only after the barrier that
+    // follows both groups' waits for t, and stage s+3 refills the slot of stage s-1, whose reads
+    // both groups completed before the previous barrier.
+    static_assert(NWAVE == 8 && WAVES_N == 2, "ping-pong needs the 4x2 wave layout");
+    const int grp = wave >> 2;
+    auto memory_phase = [&](int s) {
+      const int slot = s & (NSTAGE - 1);
+      load_frags(0, slot, 0);
+      load_frags(1, slot, 1);
+      const int slot_lds = lds0 + ((s + 3) & (NSTAGE - 1)) * STAGE;
+      const i32x4 rm = rsrc_m(s + 3), rn = rsrc_n(s + 3);
 #pragma unroll
-    for (int s = 0; s < NSTAGE; ++s) issue(s);
-    wait_vm<(NSTAGE - 1) * 2 * DPW>();
-    __syncthreads();
-    load_frags(0, 0, 0);
+      for (int d = 0; d < 2 * DPW; ++d) dma_one(d, rm, rn, slot_lds);
+    };
+    auto half_end = [&]() {
+      __builtin_amdgcn_sched_barrier(0);
+      wait_vm<(NSTAGE - 2) * 2 * DPW>();
+      __syncthreads();
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    if (nsteps > 0) {
+#pragma unroll
+      for (int s = 0; s < NSTAGE - 1; ++s) issue(s);
+      wait_vm<(NSTAGE - 2) * 2 * DPW>();
+      __syncthreads();
+      if (grp == 1) half_end();
+      for (int s = 0; s < nsteps; ++s) {
+        memory_phase(s);
+        half_end();
+        mfmas(0, 0, MFMA_HALF);
+        mfmas(1, 0, MFMA_HALF);
+        half_end();
+      }
+      if (grp == 0) half_end();
+    }
+    wait_vm<0>();
   }
-  for (int s = 0; s < nsteps; ++s) {
-    const int slot = s & (NSTAGE - 1);
-    load_frags(1, slot, 1);
-    mfmas(0);
-    __builtin_amdgcn_sched_barrier(0);
-    wait_vm<(NSTAGE - 2) * 2 * DPW>();
-    __syncthreads();
-    load_frags(0, (s + 1) & (NSTAGE - 1), 0);   // unused after the last stage
-    __builtin_amdgcn_sched_barrier(0);
-    mfmas_refill(1, s + NSTAGE);
-  }
-  wait_vm<0>();
 
   // ---------------- epilogue ------------------------------------------------------------------
   // lane holds output row (wm*WTM + 32*i + lane%32) and columns wn*WTN + 32*j + 8*q + 4*(lane/32) + 0..3
@@ -539,15 +600,20 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void grouped_gemm_kernel
 constexpr int kBM = TILE;
 constexpr int kBN = TILE;
 
-// wave layout per product: 4 wavefronts (128x128 each) where the transposing LDS reads dominate,
-// 8 (64x128 each, two per SIMD) for dX whose operands are both read 16 bytes per lane
-template <int KIND> struct Waves { static constexpr int M = (KIND == KIND_DX) ? 4 : 2, N = 2; };
+// Wave layout and schedule per product, chosen by measurement on the Mixtral-shaped layer: dX
+// (both operands read 16 bytes per lane) runs 8 wavefronts in the ping-pong schedule; fwd and dW,
+// whose transposing LDS reads make the memory phase longer than a compute phase, run 4 wavefronts
+// (one per SIMD, 128x128 each) in the single-group schedule.
+template <int KIND> struct Waves {
+  static constexpr bool PINGPONG = (KIND == KIND_DX);
+  static constexpr int M = PINGPONG ? 4 : 2, N = 2;
+};
 
 template <int KIND, bool DUAL, bool ACT>
 moe_status launch(const GemmParams& p, unsigned grid, hipStream_t stream, const char* name) {
   if (grid == 0) return MOE_SUCCESS;
   constexpr int WM = Waves<KIND>::M, WN = Waves<KIND>::N;
-  grouped_gemm_kernel<KIND, DUAL, ACT, WM, WN><<<grid, 64 * WM * WN, 0, stream>>>(p);
+  grouped_gemm_kernel<KIND, DUAL, ACT, WM, WN, Waves<KIND>::PINGPONG><<<grid, 64 * WM * WN, 0, stream>>>(p);
   return check_launch(name);
 }
 
