@@ -31,11 +31,8 @@
 namespace moe {
 namespace {
 
-constexpr int TILE = 256;    // output tile edge (rows and N-side columns)
+constexpr int TN = 256;      // output tile columns (N side)
 constexpr int BK = 32;       // contraction elements per pipeline stage
-constexpr int NSTAGE = 4;    // LDS ring depth
-constexpr int OPND = TILE * BK * 2;      // bytes of one operand tile in one stage (16 KiB)
-constexpr int STAGE = 2 * OPND;          // M side at +0, N side at +OPND
 
 // Two LDS tile layouts, chosen so that DMA stores are plain 1 KiB runs and every fragment read
 // of 8 (ds_read_b128) or 16 (ds_read_b64_tr_b16) lanes touches distinct banks:
@@ -135,13 +132,20 @@ __device__ __forceinline__ void band_order(int id, int mtiles, int ntiles, int& 
   }
 }
 
-// WAVES_M x WAVES_N wavefronts share the 256x256 tile (4 = one per SIMD, 8 = two per SIMD).
-template <int KIND, bool DUAL, bool ACT, int WAVES_M, int WAVES_N, bool PINGPONG>
-__global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void grouped_gemm_kernel(GemmParams p) {
+// One workgroup computes a TM x 256 output tile with WAVES_M x WAVES_N wavefronts through an
+// NSTAGE-deep LDS ring; WPE workgroups share a CU (2 when the ring is small enough).
+template <int KIND, bool DUAL, bool ACT, int TM, int WAVES_M, int WAVES_N, int NSTAGE, bool PINGPONG, int WPE>
+__global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kernel(GemmParams p) {
   constexpr int NWAVE = WAVES_M * WAVES_N;
-  constexpr int DPW = 16 / NWAVE;             // DMA loads per wave per operand per stage
-  constexpr int WTM = TILE / WAVES_M;         // per-wave tile rows (64)
-  constexpr int WTN = TILE / WAVES_N;         // per-wave tile columns (128)
+  constexpr int OPND_M = TM * BK * 2;         // bytes of the M-side tile of one stage
+  constexpr int OPND_N = TN * BK * 2;         // bytes of the N-side tile of one stage (16 KiB)
+  constexpr int STAGE = OPND_M + OPND_N;      // M side at +0, N side at +OPND_M
+  constexpr int DPW_M = TM / 16 / NWAVE;      // 1 KiB DMA loads per wave per stage, M side
+  constexpr int DPW_N = TN / 16 / NWAVE;      // ... N side
+  constexpr int DPW_T = DPW_M + DPW_N;
+  static_assert(DPW_M * NWAVE * 16 == TM && DPW_N * NWAVE * 16 == TN, "DMA split");
+  constexpr int WTM = TM / WAVES_M;           // per-wave tile rows
+  constexpr int WTN = TN / WAVES_N;           // per-wave tile columns
   constexpr int MB = WTM / 32;                // 32x32 MFMA blocks per wave along rows
   constexpr int NB = WTN / 32;                // ... and along columns
   constexpr bool M_T = (KIND == KIND_DW);     // M-side operand stored contraction-major
@@ -191,7 +195,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void grouped_gemm_kernel
     row_hi = p.offsets[g + 1];
   } else {
     int cnt = 0;
-    if (tid < p.G) cnt = (p.offsets[tid + 1] - p.offsets[tid] + TILE - 1) / TILE;
+    if (tid < p.G) cnt = (p.offsets[tid + 1] - p.offsets[tid] + TM - 1) / TM;
     if (tid < 256) s_scan[tid] = cnt;
     __syncthreads();
     for (int off = 1; off < 256; off <<= 1) {
@@ -207,7 +211,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void grouped_gemm_kernel
     band_order(xcd_remap(blockIdx.x, ntiles_all), mtotal, p.n_tiles, mt_glob, nt);
     g = __syncthreads_count(tid < p.G && s_scan[tid] <= mt_glob);
     mt = mt_glob - (g > 0 ? s_scan[g - 1] : 0);
-    row_lo = (int64_t)p.offsets[g] + (int64_t)mt * TILE;
+    row_lo = (int64_t)p.offsets[g] + (int64_t)mt * TM;
     row_hi = p.offsets[g + 1];
   }
 
@@ -231,28 +235,28 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void grouped_gemm_kernel
   const char* m_src = nullptr;    // base of the contraction window at c = 0
   const char* m_src2 = nullptr;   // DX dual: second half of the contraction
   int64_t m_ld;                   // elements per memory row
-  int m_voff[DPW];
+  int m_voff[DPW_M];
   if constexpr (!M_T) {
     m_ld = (KIND == KIND_FWD) ? p.K : p.N;
     const int64_t rows_valid = row_hi - row_lo;   // > 0
     m_src = reinterpret_cast<const char*>(p.a + row_lo * m_ld);
     if constexpr (KIND == KIND_DX && DUAL) m_src2 = reinterpret_cast<const char*>(p.a2 + row_lo * m_ld);
 #pragma unroll
-    for (int i = 0; i < DPW; ++i) {
-      int64_t r = 16 * (DPW * wave + i) + (lane >> 2);
+    for (int i = 0; i < DPW_M; ++i) {
+      int64_t r = 16 * (DPW_M * wave + i) + (lane >> 2);
       if (r > rows_valid - 1) r = rows_valid - 1;
       const int c = (lane & 3) ^ swz_d(lane >> 2);
       m_voff[i] = (int)((r * m_ld + 8 * c) * 2);
     }
   } else {
     m_ld = p.K;
-    const int grp = (DPW * wave) / 4;
-    int64_t col0 = (int64_t)mt * TILE + 64 * grp;
+    const int grp = (DPW_M * wave) / 4;
+    int64_t col0 = (int64_t)mt * TM + 64 * grp;
     if (col0 > p.K - 64) col0 = p.K - 64;
     m_src = reinterpret_cast<const char*>(p.a + row_lo * m_ld + col0);
 #pragma unroll
-    for (int i = 0; i < DPW; ++i) {
-      const int k = 8 * ((DPW * wave + i) & 3) + (lane >> 3);
+    for (int i = 0; i < DPW_M; ++i) {
+      const int k = 8 * ((DPW_M * wave + i) & 3) + (lane >> 3);
       const int c = (lane & 7) ^ swz_t(k);
       m_voff[i] = (int)((k * m_ld + 8 * c) * 2);
     }
@@ -261,15 +265,15 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void grouped_gemm_kernel
   const char* n_src = nullptr;
   const char* n_src2 = nullptr;
   int64_t n_ld;
-  int n_voff[DPW];
+  int n_voff[DPW_N];
   if constexpr (!N_T) {
-    // DX: B[g][kk, c]; the tile's output columns kk = nt*TILE + row, clamped
+    // DX: B[g][kk, c]; the tile's output columns kk = nt*TN + row, clamped
     n_ld = p.N;
     n_src = reinterpret_cast<const char*>(p.b + (int64_t)g * p.K * p.N);
     if constexpr (DUAL) n_src2 = reinterpret_cast<const char*>(p.b2 + (int64_t)g * p.K * p.N);
 #pragma unroll
-    for (int i = 0; i < DPW; ++i) {
-      int64_t kk = (int64_t)nt * TILE + 16 * (DPW * wave + i) + (lane >> 2);
+    for (int i = 0; i < DPW_N; ++i) {
+      int64_t kk = (int64_t)nt * TN + 16 * (DPW_N * wave + i) + (lane >> 2);
       if (kk > p.K - 1) kk = p.K - 1;
       const int c = (lane & 3) ^ swz_d(lane >> 2);
       n_voff[i] = (int)((kk * p.N + 8 * c) * 2);
@@ -278,21 +282,21 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void grouped_gemm_kernel
     // this wave's column group: in dual mode groups 0,2 come from the first source and 1,3 from
     // the second, at the same output columns
     n_ld = p.N;
-    const int grp = (DPW * wave) / 4;
+    const int grp = (DPW_N * wave) / 4;
     int64_t col0;
     const uint16_t* src = p.b;
     if constexpr (DUAL) {
-      col0 = (int64_t)nt * (TILE / 2) + 64 * (grp >> 1);
+      col0 = (int64_t)nt * (TN / 2) + 64 * (grp >> 1);
       if (grp & 1) src = p.b2;
     } else {
-      col0 = (int64_t)nt * TILE + 64 * grp;
+      col0 = (int64_t)nt * TN + 64 * grp;
     }
     if (col0 > p.N - 64) col0 = p.N - 64;
     const int64_t rowbase = (KIND == KIND_FWD) ? (int64_t)g * p.K : row_lo;
     n_src = reinterpret_cast<const char*>(src + rowbase * p.N + col0);
 #pragma unroll
-    for (int i = 0; i < DPW; ++i) {
-      const int k = 8 * ((DPW * wave + i) & 3) + (lane >> 3);
+    for (int i = 0; i < DPW_N; ++i) {
+      const int k = 8 * ((DPW_N * wave + i) & 3) + (lane >> 3);
       const int c = (lane & 7) ^ swz_t(k);
       n_voff[i] = (int)((k * n_ld + 8 * c) * 2);
     }
@@ -336,16 +340,17 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void grouped_gemm_kernel
       return make_rsrc(n_src + c0 * n_ld * 2, (left < BK ? left : BK) * n_ld * 2);
     }
   };
-  // load d (0 .. 2*DPW-1) of this wave for a step whose slot starts at LDS byte slot_lds
+  // load d (0 .. DPW_T-1) of this wave for a step whose slot starts at LDS byte slot_lds
   auto dma_one = [&](int d, const i32x4& rm, const i32x4& rn, int slot_lds) {
-    if (d < DPW) dma16(rm, m_voff[d], slot_lds + (DPW * wave + d) * 1024);
-    else dma16(rn, n_voff[d - DPW], slot_lds + OPND + (DPW * wave + d - DPW) * 1024);
+    if (d < DPW_M) dma16(rm, m_voff[d], slot_lds + (DPW_M * wave + d) * 1024);
+    else dma16(rn, n_voff[d - DPW_M], slot_lds + OPND_M + (DPW_N * wave + d - DPW_M) * 1024);
   };
+  auto slot_of = [&](int s) { return s % NSTAGE; };
   auto issue = [&](int s) {
-    const int slot_lds = lds0 + (s & (NSTAGE - 1)) * STAGE;
+    const int slot_lds = lds0 + slot_of(s) * STAGE;
     const i32x4 rm = rsrc_m(s), rn = rsrc_n(s);
 #pragma unroll
-    for (int d = 0; d < 2 * DPW; ++d) dma_one(d, rm, rn, slot_lds);
+    for (int d = 0; d < DPW_T; ++d) dma_one(d, rm, rn, slot_lds);
   };
 
   // ---------------- fragment reads ---------------------------------------------------------------
@@ -361,11 +366,11 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void grouped_gemm_kernel
     return grp0 * 4096 + (8 * (G16 >> 1) + kq) * 128 +
            (((4 * jodd + 2 * (G16 & 1) + (cq >> 1)) ^ (2 * kq)) << 4) + (cq & 1) * 8;
   };
-  // byte offsets within a stage (M side at 0, N side at OPND), per ks (direct) or j parity (mn)
+  // byte offsets within a stage (M side at 0, N side at OPND_M), per ks (direct) or j parity (mn)
   const int m_a0 = M_T ? t_addr(wm * WTM / 64, 0) : d_addr(wm * WTM, 0);
   const int m_a1 = M_T ? t_addr(wm * WTM / 64, 1) : d_addr(wm * WTM, 1);
-  const int n_a0 = OPND + (N_T ? t_addr(wn * WTN / 64, 0) : d_addr(wn * WTN, 0));
-  const int n_a1 = OPND + (N_T ? t_addr(wn * WTN / 64, 1) : d_addr(wn * WTN, 1));
+  const int n_a0 = OPND_M + (N_T ? t_addr(wn * WTN / 64, 0) : d_addr(wn * WTN, 0));
+  const int n_a1 = OPND_M + (N_T ? t_addr(wn * WTN / 64, 1) : d_addr(wn * WTN, 1));
 
   f32x16 acc[MB][NB];
 #pragma unroll
@@ -399,23 +404,20 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void grouped_gemm_kernel
       acc[m / NB][m % NB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[set][m % NB], fb[set][m / NB],
                                                                    acc[m / NB][m % NB], 0, 0, 0);
   };
-  // the same, with the 2*DPW refill loads of step `s` spread one after every second MFMA so the
+  // the same, with the DPW_T refill loads of step `s` spread evenly between the MFMAs so the
   // vector-memory and LDS-write work of the refill overlaps the matrix cores
-  static_assert(MB * NB >= 4 * DPW, "need two MFMAs per refill load");
   auto mfmas_refill = [&](int set, int s) {
-    const int slot_lds = lds0 + (s & (NSTAGE - 1)) * STAGE;
+    const int slot_lds = lds0 + slot_of(s) * STAGE;
     const i32x4 rm = rsrc_m(s), rn = rsrc_n(s);
+    constexpr int NM = MB * NB;
 #pragma unroll
-    for (int i = 0; i < MB; ++i)
+    for (int m = 0; m < NM; ++m) {
+      acc[m / NB][m % NB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[set][m % NB], fb[set][m / NB],
+                                                                   acc[m / NB][m % NB], 0, 0, 0);
 #pragma unroll
-      for (int j = 0; j < NB; ++j) {
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[set][j], fb[set][i], acc[i][j], 0, 0, 0);
-        const int m = i * NB + j;
-        if ((m & 1) && (m >> 1) < 2 * DPW) {
-          dma_one(m >> 1, rm, rn, slot_lds);
-          __builtin_amdgcn_sched_barrier(0);
-        }
-      }
+      for (int d = (m * DPW_T) / NM; d < ((m + 1) * DPW_T) / NM; ++d) dma_one(d, rm, rn, slot_lds);
+      if (((m + 1) * DPW_T) / NM > (m * DPW_T) / NM) __builtin_amdgcn_sched_barrier(0);
+    }
   };
 
   // ---------------- pipelined main loop ---------------------------------------------------------
@@ -436,13 +438,13 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void grouped_gemm_kernel
     constexpr int MFMA_HALF = MB * NB;
     constexpr int SPLIT = MFMA_HALF / 2;
     auto stage_body = [&](int s, int cur) {
-      const int slot = s & (NSTAGE - 1);
+      const int slot = slot_of(s);
       load_frags(2, slot, 1);
       mfmas(cur, 0, SPLIT);
       __builtin_amdgcn_sched_barrier(0);
-      wait_vm<(NSTAGE - 2) * 2 * DPW>();
+      wait_vm<(NSTAGE - 2) * DPW_T>();
       __syncthreads();
-      load_frags(cur ^ 1, (s + 1) & (NSTAGE - 1), 0);   // unused after the last stage
+      load_frags(cur ^ 1, slot_of(s + 1), 0);   // unused after the last stage
       __builtin_amdgcn_sched_barrier(0);
       mfmas(cur, SPLIT, MFMA_HALF);
       mfmas_refill(2, s + NSTAGE);
@@ -450,7 +452,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void grouped_gemm_kernel
     if (nsteps > 0) {
   #pragma unroll
       for (int s = 0; s < NSTAGE; ++s) issue(s);
-      wait_vm<(NSTAGE - 1) * 2 * DPW>();
+      wait_vm<(NSTAGE - 1) * DPW_T>();
       __syncthreads();
       load_frags(0, 0, 0);
     }
@@ -469,27 +471,28 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void grouped_gemm_kernel
     // of its DMA stages are in flight: stage t is read (group 0 first) only after the barrier that
     // follows both groups' waits for t, and stage s+3 refills the slot of stage s-1, whose reads
     // both groups completed before the previous barrier.
-    static_assert(NWAVE == 8 && WAVES_N == 2, "ping-pong needs the 4x2 wave layout");
+    static_assert(NWAVE == 8 && WAVES_N == 2 && TM == 256, "ping-pong needs the 4x2 wave layout");
     const int grp = wave >> 2;
+    static_assert(NSTAGE == 4, "ping-pong refill distance assumes a 4-slot ring");
     auto memory_phase = [&](int s) {
-      const int slot = s & (NSTAGE - 1);
+      const int slot = slot_of(s);
       load_frags(0, slot, 0);
       load_frags(1, slot, 1);
-      const int slot_lds = lds0 + ((s + 3) & (NSTAGE - 1)) * STAGE;
+      const int slot_lds = lds0 + slot_of(s + 3) * STAGE;
       const i32x4 rm = rsrc_m(s + 3), rn = rsrc_n(s + 3);
 #pragma unroll
-      for (int d = 0; d < 2 * DPW; ++d) dma_one(d, rm, rn, slot_lds);
+      for (int d = 0; d < DPW_T; ++d) dma_one(d, rm, rn, slot_lds);
     };
     auto half_end = [&]() {
       __builtin_amdgcn_sched_barrier(0);
-      wait_vm<(NSTAGE - 2) * 2 * DPW>();
+      wait_vm<(NSTAGE - 2) * DPW_T>();
       __syncthreads();
       __builtin_amdgcn_sched_barrier(0);
     };
     if (nsteps > 0) {
 #pragma unroll
       for (int s = 0; s < NSTAGE - 1; ++s) issue(s);
-      wait_vm<(NSTAGE - 2) * 2 * DPW>();
+      wait_vm<(NSTAGE - 2) * DPW_T>();
       __syncthreads();
       if (grp == 1) half_end();
       for (int s = 0; s < nsteps; ++s) {
@@ -511,17 +514,17 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void grouped_gemm_kernel
   for (int i = 0; i < MB; ++i) {
     const int mrow = wm * WTM + 32 * i + l32;
     if constexpr (KIND == KIND_DW) {
-      const int64_t m = (int64_t)mt * TILE + mrow;
+      const int64_t m = (int64_t)mt * TM + mrow;
       if (m >= p.K) continue;
 #pragma unroll
       for (int j = 0; j < NB; ++j) {
         float* dst;
         int64_t col;
         if constexpr (DUAL) {
-          col = (int64_t)nt * (TILE / 2) + wn * (WTN / 2) + 32 * (j % (NB / 2));
+          col = (int64_t)nt * (TN / 2) + wn * (WTN / 2) + 32 * (j % (NB / 2));
           dst = static_cast<float*>(j >= NB / 2 ? p.out2 : p.out);
         } else {
-          col = (int64_t)nt * TILE + wn * WTN + 32 * j;
+          col = (int64_t)nt * TN + wn * WTN + 32 * j;
           dst = static_cast<float*>(p.out);
         }
         dst += (int64_t)g * p.K * p.N + m * p.N;
@@ -543,7 +546,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void grouped_gemm_kernel
         for (int j = 0; j < NB; ++j)
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            const int64_t n = (int64_t)nt * TILE + wn * WTN + 32 * j + 8 * q + col_in;
+            const int64_t n = (int64_t)nt * TN + wn * WTN + 32 * j + 8 * q + col_in;
             if (n < p.K) {
               uint2 v;
               v.x = pack_bf16(acc[i][j][4 * q], acc[i][j][4 * q + 1]);
@@ -559,7 +562,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void grouped_gemm_kernel
         for (int j = 0; j < NB / 2; ++j)
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            const int64_t n = (int64_t)nt * (TILE / 2) + wn * (WTN / 2) + 32 * j + 8 * q + col_in;
+            const int64_t n = (int64_t)nt * (TN / 2) + wn * (WTN / 2) + 32 * j + 8 * q + col_in;
             if (n < p.N) {
               uint2 vg, vu;
               vg.x = pack_bf16(acc[i][j][4 * q], acc[i][j][4 * q + 1]);
@@ -584,7 +587,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void grouped_gemm_kernel
         for (int j = 0; j < NB; ++j)
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            const int64_t n = (int64_t)nt * TILE + wn * WTN + 32 * j + 8 * q + col_in;
+            const int64_t n = (int64_t)nt * TN + wn * WTN + 32 * j + 8 * q + col_in;
             if (n < p.N) {
               uint2 v;
               v.x = pack_bf16(acc[i][j][4 * q], acc[i][j][4 * q + 1]);
@@ -597,23 +600,26 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void grouped_gemm_kernel
   }
 }
 
-constexpr int kBM = TILE;
-constexpr int kBN = TILE;
-
-// Wave layout and schedule per product, chosen by measurement on the Mixtral-shaped layer: dX
-// (both operands read 16 bytes per lane) runs 8 wavefronts in the ping-pong schedule; fwd and dW,
-// whose transposing LDS reads make the memory phase longer than a compute phase, run 4 wavefronts
-// (one per SIMD, 128x128 each) in the single-group schedule.
-template <int KIND> struct Waves {
-  static constexpr bool PINGPONG = (KIND == KIND_DX);
-  static constexpr int M = PINGPONG ? 4 : 2, N = 2;
+// Tile shape and schedule per product, chosen by measurement on the Mixtral-shaped layer: every
+// product uses 256x256 tiles with a 4-slot ring (128-row tiles, which would pad ragged groups
+// less, measured 10-20% slower: they need 1.5x the LDS and DMA traffic per MFMA).  dX (both
+// operands read 16 bytes per lane) runs 8 wavefronts in the ping-pong schedule; fwd and dW, whose
+// transposing LDS reads make a memory phase longer than a compute phase, run 4 wavefronts (one
+// per SIMD, 128x128 each) in the single-group schedule.
+template <int KIND> struct Cfg {
+  static constexpr bool PP = (KIND == KIND_DX);
+  static constexpr int TM = 256;
+  static constexpr int WM = PP ? 4 : 2, WN = 2;
+  static constexpr int NS = 4;
+  static constexpr int WPE = 1;
 };
 
 template <int KIND, bool DUAL, bool ACT>
 moe_status launch(const GemmParams& p, unsigned grid, hipStream_t stream, const char* name) {
   if (grid == 0) return MOE_SUCCESS;
-  constexpr int WM = Waves<KIND>::M, WN = Waves<KIND>::N;
-  grouped_gemm_kernel<KIND, DUAL, ACT, WM, WN, Waves<KIND>::PINGPONG><<<grid, 64 * WM * WN, 0, stream>>>(p);
+  using C = Cfg<KIND>;
+  grouped_gemm_kernel<KIND, DUAL, ACT, C::TM, C::WM, C::WN, C::NS, C::PP, C::WPE>
+      <<<grid, 64 * C::WM * C::WN, 0, stream>>>(p);
   return check_launch(name);
 }
 
@@ -643,8 +649,9 @@ extern "C" moe_status moe_grouped_gemm_fwd(const moe_bf16* A, const moe_bf16* B,
   GemmParams p{};
   p.a = A; p.b = B; p.b2 = B2; p.offsets = offsets; p.out = C; p.out2 = C2; p.act = act;
   p.G = G; p.R = R; p.K = K; p.N = N;
-  p.mt_bound = (int)((R + kBM - 1) / kBM + G);
-  const int cols_per_tile = B2 ? kBN / 2 : kBN;
+  constexpr int TM = Cfg<KIND_FWD>::TM;
+  p.mt_bound = (int)((R + TM - 1) / TM + G);
+  const int cols_per_tile = B2 ? TN / 2 : TN;
   p.n_tiles = (int)((N + cols_per_tile - 1) / cols_per_tile);
   const unsigned grid = (unsigned)((int64_t)p.mt_bound * p.n_tiles);
   if (B2 && act) return launch<KIND_FWD, true, true>(p, grid, stream, "grouped_gemm_fwd(dual,swiglu)");
@@ -663,6 +670,8 @@ extern "C" moe_status moe_grouped_gemm_dx(const moe_bf16* dC, const moe_bf16* B,
   if (!offsets) return fail(MOE_ERROR_INVALID_VALUE, "moe_grouped_gemm_dx: offsets is NULL");
   if ((dC2 == nullptr) != (B2 == nullptr))
     return fail(MOE_ERROR_INVALID_VALUE, "moe_grouped_gemm_dx: dC2 and B2 must both be set or both NULL");
+  if (K * N * 2 >= ((int64_t)1 << 31))
+    return fail(MOE_ERROR_NOT_SUPPORTED, "moe_grouped_gemm_dx: one group's B must be < 2 GiB");
   if (R == 0) return MOE_SUCCESS;
   if (!dC || !B || !dA) return fail(MOE_ERROR_INVALID_VALUE, "moe_grouped_gemm_dx: NULL pointer");
   if (bad_ptr(dC) || bad_ptr(B) || bad_ptr(dC2) || bad_ptr(B2) || bad_ptr(dA))
@@ -670,8 +679,9 @@ extern "C" moe_status moe_grouped_gemm_dx(const moe_bf16* dC, const moe_bf16* B,
   GemmParams p{};
   p.a = dC; p.a2 = dC2; p.b = B; p.b2 = B2; p.offsets = offsets; p.out = dA;
   p.G = G; p.R = R; p.K = K; p.N = N;
-  p.mt_bound = (int)((R + kBM - 1) / kBM + G);
-  p.n_tiles = (int)((K + kBN - 1) / kBN);
+  constexpr int TM = Cfg<KIND_DX>::TM;
+  p.mt_bound = (int)((R + TM - 1) / TM + G);
+  p.n_tiles = (int)((K + TN - 1) / TN);
   const unsigned grid = (unsigned)((int64_t)p.mt_bound * p.n_tiles);
   if (dC2) return launch<KIND_DX, true, false>(p, grid, stream, "grouped_gemm_dx(dual)");
   return launch<KIND_DX, false, false>(p, grid, stream, "grouped_gemm_dx");
@@ -694,8 +704,8 @@ extern "C" moe_status moe_grouped_gemm_dw(const moe_bf16* A, const moe_bf16* dC,
   GemmParams p{};
   p.a = A; p.b = dC; p.b2 = dC2; p.offsets = offsets; p.out = dB; p.out2 = dB2;
   p.G = G; p.R = R; p.K = K; p.N = N;
-  p.m_tiles = (int)((K + kBM - 1) / kBM);
-  const int cols_per_tile = dC2 ? kBN / 2 : kBN;
+  p.m_tiles = (int)((K + Cfg<KIND_DW>::TM - 1) / Cfg<KIND_DW>::TM);
+  const int cols_per_tile = dC2 ? TN / 2 : TN;
   p.n_tiles = (int)((N + cols_per_tile - 1) / cols_per_tile);
   const unsigned grid = (unsigned)((int64_t)G * p.m_tiles * p.n_tiles);
   if (dC2) return launch<KIND_DW, true, false>(p, grid, stream, "grouped_gemm_dw(dual)");
