@@ -23,6 +23,31 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 METRIC = "MoE layer fwd+bwd tokens/sec + grouped-GEMM TFLOP/s (% of bf16 MFMA peak), 1 GPU"
 
+# HBM bytes per launch of each grouped GEMM on the Mixtral-shaped layer, from rocprofv3 FETCH_SIZE /
+# WRITE_SIZE runs scaled by a plain copy of known size (profiles/grouped_gemm_hbm_traffic_*.md).
+# Valid only for the kernel source they were measured on (sha256 prefix); otherwise reported null.
+TRAFFIC_SOURCE = ("paper_2606_26453_amd/csrc/grouped_gemm.hip", "654fe6b73bc3ddcd")
+TRAFFIC_CONFIG = 1
+FETCH_SCALE, WRITE_SCALE = 2.0 * 1024, 1.0 * 1024
+TRAFFIC_KIB = {  # call: (FETCH_SIZE KiB, WRITE_SIZE KiB) per dispatch
+    "fwd_gate_up": (4547755, 1743197), "fwd_down": (2104631, 131072),
+    "dx_down": (2458416, 472511), "dx_gate_up": (4270704, 139449),
+    "dw_down": (1526221, 1835136), "dw_gate_up": (2758872, 3671823),
+}
+
+
+def measured_traffic(call, config):
+    import hashlib
+    path = os.path.join(ROOT, TRAFFIC_SOURCE[0])
+    try:
+        sha = hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+    except OSError:
+        return None
+    if sha != TRAFFIC_SOURCE[1] or config != TRAFFIC_CONFIG or call not in TRAFFIC_KIB:
+        return None
+    f, w = TRAFFIC_KIB[call]
+    return int(f * FETCH_SCALE + w * WRITE_SCALE)
+
 
 def _args():
     ap = argparse.ArgumentParser()
@@ -34,7 +59,20 @@ def _args():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tokens", type=int, default=0)
     ap.add_argument("--no-trace", action="store_true", help="no per-call events inside the timed region")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device copy of BYTES bytes 3 times (counter calibration)")
     return ap.parse_args()
+
+
+def copy_probe(nbytes):
+    """A plain copy of known size: the reference that scales the HBM byte counters."""
+    import torch
+    a = torch.ones(nbytes // 2, dtype=torch.bfloat16, device="cuda:0")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": nbytes, "copies": 3}), flush=True)
 
 
 def cpu_baseline(cfg, inp, sample_tokens):
@@ -72,6 +110,9 @@ def main():
         print(f"bench.py measures one GPU only (--gpus {a.gpus} requested): this build has no "
               f"multi-GPU path; run with --gpus 1", file=sys.stderr)
         sys.exit(2)
+    if a.copy_probe:
+        copy_probe(a.copy_probe)
+        return
     import torch
 
     from paper_2606_26453_amd import layer as L
@@ -135,7 +176,8 @@ def main():
         if kind == "flops":
             ach = amount / avg / 1e9
             roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 1), "peak": PEAK_BF16_TFLOPS,
-                        "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                        "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
+                        "traffic": measured_traffic(dom, a.config),
                         "work_per_launch": amount, "avg_launch_ms": round(avg, 4)}
         else:
             ach = amount / avg / 1e6
