@@ -25,8 +25,9 @@ METRIC = "MoE layer fwd+bwd tokens/sec + grouped-GEMM TFLOP/s (% of bf16 MFMA pe
 
 # HBM bytes per launch of each grouped GEMM on the Mixtral-shaped layer, from rocprofv3 FETCH_SIZE /
 # WRITE_SIZE runs scaled by a plain copy of known size (profiles/grouped_gemm_hbm_traffic_*.md).
-# Valid only for the kernel source they were measured on (sha256 prefix); otherwise reported null.
-TRAFFIC_SOURCE = ("paper_2606_26453_amd/csrc/grouped_gemm.hip", "654fe6b73bc3ddcd")
+# Valid only for the kernel code they were measured on (sha256 prefix of the source with comments
+# and blank lines removed); otherwise reported null.
+TRAFFIC_SOURCE = ("paper_2606_26453_amd/csrc/grouped_gemm.hip", "da47f9ac83763902")
 TRAFFIC_CONFIG = 1
 FETCH_SCALE, WRITE_SCALE = 2.0 * 1024, 1.0 * 1024
 TRAFFIC_KIB = {  # call: (FETCH_SIZE KiB, WRITE_SIZE KiB) per dispatch
@@ -36,11 +37,17 @@ TRAFFIC_KIB = {  # call: (FETCH_SIZE KiB, WRITE_SIZE KiB) per dispatch
 }
 
 
-def measured_traffic(call, config):
+def code_hash(text):
     import hashlib
+    import re
+    lines = [re.sub(r"//.*$", "", ln).rstrip() for ln in text.splitlines()]
+    return hashlib.sha256("\n".join(ln for ln in lines if ln.strip()).encode()).hexdigest()[:16]
+
+
+def measured_traffic(call, config):
     path = os.path.join(ROOT, TRAFFIC_SOURCE[0])
     try:
-        sha = hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+        sha = code_hash(open(path).read())
     except OSError:
         return None
     if sha != TRAFFIC_SOURCE[1] or config != TRAFFIC_CONFIG or call not in TRAFFIC_KIB:

@@ -6,24 +6,21 @@
 //   DW   dB[g][m, n]  = sum_r A[r, m]  * dC[r, n]        r over group g (ragged contraction)
 // DW is the paper's dW1_e = X_e^T G_e (section 5.4, Appendix H).
 //
-// Work decomposition.  A 256-thread workgroup (4 wavefronts in a 2x2 grid) owns a BM x BN output
-// tile and walks the contraction in steps of BK = 64.  Both operand tiles are staged in LDS in
-// one layout, [row][64 contraction elements] with the contraction contiguous, which is what a
-// lane of v_mfma_f32_32x32x16_bf16 consumes (8 consecutive contraction elements of one row, one
-// ds_read_b128).  An operand whose contraction index is its memory row (B in FWD, both operands
-// in DW) is loaded as 8x8 bf16 blocks (eight 16-byte row segments per thread, coalesced along
-// the memory row) and transposed in registers before the LDS store; the other operands are
-// copied 16 bytes per thread.  16-byte LDS chunks are XOR-swizzled by row so that both the
-// MFMA reads (8 consecutive rows, same chunk) and the transposed stores (rows 8 apart, same
-// chunk) hit distinct banks.  LDS is double buffered: global loads for step s+1 are in flight
-// while step s runs on the matrix cores, with one barrier per step.
+// Work decomposition.  A workgroup owns a 256 x 256 output tile and walks the contraction 32 at a
+// time through a ring of LDS slots.  Both operand tiles reach LDS through buffer loads that write
+// LDS directly (16 bytes per lane, no register staging); ragged contraction rows beyond a group
+// fall outside the buffer resource and read as zero.  An operand whose contraction is contiguous in
+// memory (the routed rows, dX's weights) is read into MFMA layout with ds_read_b128; an operand
+// whose contraction index is its memory row (the weights in FWD, both operands in DW) is kept in
+// LDS with its rows intact and read with the transposing ds_read_b64_tr_b16, since the matrix
+// cores take both operands contraction-contiguous per lane.
 //
 // MFMA operand roles: the N-side operand is the MFMA "A" (32 MFMA rows = 32 output columns) and
 // the M-side operand the MFMA "B", so each lane's accumulator holds one output row and runs of
 // 4 consecutive output columns, stored as 8-byte (bf16) or 16-byte (fp32) vectors.
 //
-// Dual mode (FWD gate/up, DW gate/up): the N side of a tile is split into two halves fed from two
-// sources at the same output columns; each wave's 128 N-columns are 64 from each source, so the
+// Dual mode (FWD gate/up, DW gate/up): the N side of a tile is split into column groups fed from
+// two sources at the same output columns; each wave's 128 N-columns are 64 from each source, so the
 // accumulators for the same (row, column) of both products sit in the same lane, which is what
 // the fused SwiGLU epilogue needs.  DX dual mode appends the second pair to the contraction.
 #include "common.h"
