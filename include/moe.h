@@ -167,6 +167,21 @@ moe_status moe_grouped_gemm_dx(const moe_bf16* dC, const moe_bf16* B, const moe_
                                const moe_bf16* B2, const int32_t* offsets, int32_t G, int64_t R,
                                int64_t K, int64_t N, moe_bf16* dA, hipStream_t stream);
 
+/*
+ * G + I fused: the down projection's data gradient followed by the SwiGLU backward, without
+ * storing dA.  For rows r of group g, dA[r, :] = bf16(dC[r, :] . B[g]^T) is formed in registers
+ * (rounded exactly as the stored tensor would be) and the epilogue writes
+ *   dh_up   = bf16(dA * h_gate * s),  dh_gate = bf16(dA * h_up * s * (1 + h_gate * (1 - s))),
+ *   s = sigmoid(h_gate),
+ * i.e. the result is bitwise identical to moe_grouped_gemm_dx (single pair) followed by
+ * moe_swiglu_bwd.  Saves the dA store and reload and the separate elementwise pass.
+ * dC [R,N]; B [G,K,N]; h_gate, h_up, dh_gate, dh_up [R,K] bf16.
+ */
+moe_status moe_grouped_gemm_dx_swiglu_bwd(const moe_bf16* dC, const moe_bf16* B,
+                                          const int32_t* offsets, int32_t G, int64_t R, int64_t K,
+                                          int64_t N, const moe_bf16* h_gate, const moe_bf16* h_up,
+                                          moe_bf16* dh_gate, moe_bf16* dh_up, hipStream_t stream);
+
 /* ------------------------------------------------------------------------------------------ */
 /* H, K: backward weight-gradient grouped GEMM (the paper's dW1 kernel class)                   */
 /* ------------------------------------------------------------------------------------------ */

@@ -44,6 +44,14 @@ __device__ __forceinline__ u32x4 pack8(const float* f) {
 __device__ __forceinline__ float silu_f32(float g) { return g / (1.0f + expf(-g)); }
 __device__ __forceinline__ float sigmoid_f32(float g) { return 1.0f / (1.0f + expf(-g)); }
 
+// SwiGLU backward for one element (the same arithmetic everywhere it is computed):
+// dh_up = d * g * s, dh_gate = d * u * s * (1 + g * (1 - s)), s = sigmoid(g).
+__device__ __forceinline__ void swiglu_bwd1(float g, float u, float d, float& dh_gate, float& dh_up) {
+  const float s = sigmoid_f32(g);
+  dh_up = d * g * s;
+  dh_gate = d * u * s * (1.0f + g * (1.0f - s));
+}
+
 }  // namespace moe
 
 // ---- host-side status plumbing (defined in status.hip) ----

@@ -26,11 +26,7 @@ __device__ __forceinline__ void swiglu_bwd8(const u32x4& hg, const u32x4& hu, co
   unpack8(hu, u);
   unpack8(da, d);
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const float s = sigmoid_f32(g[j]);
-    ou[j] = d[j] * g[j] * s;
-    og[j] = d[j] * u[j] * s * (1.0f + g[j] * (1.0f - s));
-  }
+  for (int j = 0; j < 8; ++j) swiglu_bwd1(g[j], u[j], d[j], og[j], ou[j]);
   dhg = pack8(og);
   dhu = pack8(ou);
 }

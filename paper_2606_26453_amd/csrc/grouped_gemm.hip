@@ -50,9 +50,11 @@ struct GemmParams {
   const uint16_t* b;   // N side: FWD B [G,K,N]; DX B [G,K,N]; DW dC [R,N]
   const uint16_t* b2;  // FWD B2; DX B2; DW dC2
   const int32_t* offsets;
-  void* out;           // FWD C; DX dA; DW dB
-  void* out2;          // FWD C2; DW dB2
+  void* out;           // FWD C; DX dA (dH_gate with the SwiGLU-backward epilogue); DW dB
+  void* out2;          // FWD C2; DX dH_up with the SwiGLU-backward epilogue; DW dB2
   uint16_t* act;       // FWD SwiGLU output
+  const uint16_t* hg;  // DX SwiGLU-backward epilogue: H_gate [R,K]
+  const uint16_t* hu;  //                               H_up [R,K]
   int G;
   int64_t R, K, N;
   int mt_bound;        // FWD/DX: upper bound on the number of row tiles
@@ -507,10 +509,10 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
   // ---------------- epilogue ------------------------------------------------------------------
   // lane holds output row (wm*WTM + 32*i + lane%32) and columns wn*WTN + 32*j + 8*q + 4*(lane/32) + 0..3
   const int col_in = 4 * fh;
+  if constexpr (KIND == KIND_DW) {
 #pragma unroll
-  for (int i = 0; i < MB; ++i) {
-    const int mrow = wm * WTM + 32 * i + l32;
-    if constexpr (KIND == KIND_DW) {
+    for (int i = 0; i < MB; ++i) {
+      const int mrow = wm * WTM + 32 * i + l32;
       const int64_t m = (int64_t)mt * TM + mrow;
       if (m >= p.K) continue;
 #pragma unroll
@@ -534,64 +536,109 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
           }
         }
       }
-    } else {
-      const int64_t r = row_lo + mrow;
-      if (r >= row_hi) continue;
-      if constexpr (KIND == KIND_DX) {
-        uint16_t* dst = static_cast<uint16_t*>(p.out) + r * p.K;
+    }
+  } else {
+    // bf16 results leave through LDS.  The accumulators, rounded to bf16, go to an LDS copy of the
+    // tile (tile row t, 16-byte chunk c = 8 columns, at t*512 + 16*(c ^ (t & 31))); then each thread
+    // moves whole chunks, so a wavefront's global accesses cover two (dual: four) contiguous row
+    // segments instead of 16 bytes in each of 32 rows.  Dual mode keeps the gate columns of a row in
+    // chunks 0..15 and the up columns in chunks 16..31.
+    static_assert(TM * TN * 2 <= NSTAGE * STAGE, "the bf16 tile fits in the ring");
+    // only the forward dual product has two outputs side by side in its tile; the dual dX product
+    // sums both contractions into one output
+    constexpr bool SPLIT = (KIND == KIND_FWD) && DUAL;
+    __syncthreads();   // every wave is done with the ring
 #pragma unroll
-        for (int j = 0; j < NB; ++j)
+    for (int i = 0; i < MB; ++i) {
+      char* trow = lds + (wm * WTM + 32 * i + l32) * 512;   // (t & 31) == l32
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int64_t n = (int64_t)nt * TN + wn * WTN + 32 * j + 8 * q + col_in;
-            if (n < p.K) {
-              uint2 v;
-              v.x = pack_bf16(acc[i][j][4 * q], acc[i][j][4 * q + 1]);
-              v.y = pack_bf16(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
-              *reinterpret_cast<uint2*>(dst + n) = v;
-            }
+      for (int j = 0; j < NB; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          int c;
+          if constexpr (SPLIT) c = (j >= NB / 2 ? 16 : 0) + (wn * (WTN / 2) + 32 * (j % (NB / 2)) + 8 * q) / 8;
+          else c = (wn * WTN + 32 * j + 8 * q) / 8;
+          uint2 v;
+          v.x = pack_bf16(acc[i][j][4 * q], acc[i][j][4 * q + 1]);
+          v.y = pack_bf16(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+          *reinterpret_cast<uint2*>(trow + 16 * (c ^ l32) + 8 * fh) = v;
+        }
+    }
+    __syncthreads();
+    constexpr int NT = 64 * NWAVE;
+    auto chunk = [&](int t, int c) { return *reinterpret_cast<const u32x4*>(lds + t * 512 + 16 * (c ^ (t & 31))); };
+    if constexpr (SPLIT) {
+      // FWD gate/up (+ SwiGLU): thread -> gate chunk c and up chunk 16 + c of rows t, t + NT/16, ...
+      const int c = tid & 15;
+      const int64_t n = (int64_t)nt * (TN / 2) + 8 * c;
+      if (n < p.N) {
+        uint16_t* c1 = static_cast<uint16_t*>(p.out) + n;
+        uint16_t* c2 = static_cast<uint16_t*>(p.out2) + n;
+        for (int t = tid >> 4; t < TM; t += NT / 16) {
+          const int64_t r = row_lo + t;
+          if (r >= row_hi) break;
+          const u32x4 vg = chunk(t, c), vu = chunk(t, 16 + c);
+          *reinterpret_cast<u32x4*>(c1 + r * p.N) = vg;
+          *reinterpret_cast<u32x4*>(c2 + r * p.N) = vu;
+          if constexpr (ACT) {
+            u32x4 va;
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              va[e] = pack_bf16(silu_f32(bf16_lo(vg[e])) * bf16_lo(vu[e]), silu_f32(bf16_hi(vg[e])) * bf16_hi(vu[e]));
+            *reinterpret_cast<u32x4*>(p.act + r * p.N + n) = va;
           }
-      } else if constexpr (DUAL) {
-        uint16_t* c1 = static_cast<uint16_t*>(p.out) + r * p.N;
-        uint16_t* c2 = static_cast<uint16_t*>(p.out2) + r * p.N;
-        uint16_t* ca = p.act + r * p.N;
+        }
+      }
+    } else {
+      // thread -> chunk c of rows t, t + NT/32, ...
+      const int64_t W = (KIND == KIND_DX) ? p.K : p.N;   // output row length
+      const int c = tid & 31;
+      const int64_t n = (int64_t)nt * TN + 8 * c;
+      if (n < W) {
+        if constexpr (KIND == KIND_DX && ACT) {
+          // SwiGLU backward on the bf16-rounded dA (what moe_swiglu_bwd would read back); the
+          // H_gate/H_up chunks of U rows are loaded ahead of their use (rows clamped in range)
+          constexpr int RPP = NT / 32, U = (TM / RPP) < 8 ? (TM / RPP) : 8;
+          uint16_t* og = static_cast<uint16_t*>(p.out) + n;
+          uint16_t* ou = static_cast<uint16_t*>(p.out2) + n;
+          for (int t0 = tid >> 5; t0 < TM; t0 += U * RPP) {
+            if (row_lo + t0 >= row_hi) break;
+            u32x4 gv[U], uv[U];
 #pragma unroll
-        for (int j = 0; j < NB / 2; ++j)
+            for (int u = 0; u < U; ++u) {
+              int64_t r = row_lo + t0 + u * RPP;
+              if (r > row_hi - 1) r = row_hi - 1;
+              gv[u] = *reinterpret_cast<const u32x4*>(p.hg + r * W + n);
+              uv[u] = *reinterpret_cast<const u32x4*>(p.hu + r * W + n);
+            }
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int64_t n = (int64_t)nt * (TN / 2) + wn * (WTN / 2) + 32 * j + 8 * q + col_in;
-            if (n < p.N) {
-              uint2 vg, vu;
-              vg.x = pack_bf16(acc[i][j][4 * q], acc[i][j][4 * q + 1]);
-              vg.y = pack_bf16(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
-              vu.x = pack_bf16(acc[i][j + NB / 2][4 * q], acc[i][j + NB / 2][4 * q + 1]);
-              vu.y = pack_bf16(acc[i][j + NB / 2][4 * q + 2], acc[i][j + NB / 2][4 * q + 3]);
-              *reinterpret_cast<uint2*>(c1 + n) = vg;
-              *reinterpret_cast<uint2*>(c2 + n) = vu;
-              if constexpr (ACT) {
-                uint2 va;
-                va.x = pack_bf16(silu_f32(bf16_lo(vg.x)) * bf16_lo(vu.x),
-                                 silu_f32(bf16_hi(vg.x)) * bf16_hi(vu.x));
-                va.y = pack_bf16(silu_f32(bf16_lo(vg.y)) * bf16_lo(vu.y),
-                                 silu_f32(bf16_hi(vg.y)) * bf16_hi(vu.y));
-                *reinterpret_cast<uint2*>(ca + n) = va;
+            for (int u = 0; u < U; ++u) {
+              const int t = t0 + u * RPP;
+              const int64_t r = row_lo + t;
+              if (r < row_hi) {
+                const u32x4 dv = chunk(t, c);
+                u32x4 vg, vu;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                  float a0, a1, b0, b1;
+                  swiglu_bwd1(bf16_lo(gv[u][e]), bf16_lo(uv[u][e]), bf16_lo(dv[e]), a0, b0);
+                  swiglu_bwd1(bf16_hi(gv[u][e]), bf16_hi(uv[u][e]), bf16_hi(dv[e]), a1, b1);
+                  vg[e] = pack_bf16(a0, a1);
+                  vu[e] = pack_bf16(b0, b1);
+                }
+                *reinterpret_cast<u32x4*>(og + r * W) = vg;
+                *reinterpret_cast<u32x4*>(ou + r * W) = vu;
               }
             }
           }
-      } else {
-        uint16_t* dst = static_cast<uint16_t*>(p.out) + r * p.N;
-#pragma unroll
-        for (int j = 0; j < NB; ++j)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int64_t n = (int64_t)nt * TN + wn * WTN + 32 * j + 8 * q + col_in;
-            if (n < p.N) {
-              uint2 v;
-              v.x = pack_bf16(acc[i][j][4 * q], acc[i][j][4 * q + 1]);
-              v.y = pack_bf16(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
-              *reinterpret_cast<uint2*>(dst + n) = v;
-            }
+        } else {
+          uint16_t* dst = static_cast<uint16_t*>(p.out) + n;
+          for (int t = tid >> 5; t < TM; t += NT / 32) {
+            const int64_t r = row_lo + t;
+            if (r >= row_hi) break;
+            *reinterpret_cast<u32x4*>(dst + r * W) = chunk(t, c);
           }
+        }
       }
     }
   }
@@ -682,6 +729,34 @@ extern "C" moe_status moe_grouped_gemm_dx(const moe_bf16* dC, const moe_bf16* B,
   const unsigned grid = (unsigned)((int64_t)p.mt_bound * p.n_tiles);
   if (dC2) return launch<KIND_DX, true, false>(p, grid, stream, "grouped_gemm_dx(dual)");
   return launch<KIND_DX, false, false>(p, grid, stream, "grouped_gemm_dx");
+}
+
+extern "C" moe_status moe_grouped_gemm_dx_swiglu_bwd(const moe_bf16* dC, const moe_bf16* B,
+                                                      const int32_t* offsets, int32_t G, int64_t R,
+                                                      int64_t K, int64_t N, const moe_bf16* h_gate,
+                                                      const moe_bf16* h_up, moe_bf16* dh_gate,
+                                                      moe_bf16* dh_up, hipStream_t stream) {
+  const char* fn = "moe_grouped_gemm_dx_swiglu_bwd";
+  if (G < 1 || G > 256) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: need 1 <= G <= 256", fn);
+  if (R < 0 || K <= 0 || N <= 0) return fail(MOE_ERROR_INVALID_VALUE, "%s: bad size", fn);
+  if (K % 64 || N % 64) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: K and N must be multiples of 64", fn);
+  if (R >= ((int64_t)1 << 31)) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: R >= 2^31", fn);
+  if (!offsets) return fail(MOE_ERROR_INVALID_VALUE, "%s: offsets is NULL", fn);
+  if (K * N * 2 >= ((int64_t)1 << 31))
+    return fail(MOE_ERROR_NOT_SUPPORTED, "%s: one group's B must be < 2 GiB", fn);
+  if (R == 0) return MOE_SUCCESS;
+  if (!dC || !B || !h_gate || !h_up || !dh_gate || !dh_up)
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: NULL pointer", fn);
+  if (bad_ptr(dC) || bad_ptr(B) || bad_ptr(h_gate) || bad_ptr(h_up) || bad_ptr(dh_gate) || bad_ptr(dh_up))
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: pointers must be 16-byte aligned", fn);
+  GemmParams p{};
+  p.a = dC; p.b = B; p.offsets = offsets; p.out = dh_gate; p.out2 = dh_up; p.hg = h_gate; p.hu = h_up;
+  p.G = G; p.R = R; p.K = K; p.N = N;
+  constexpr int TM = Cfg<KIND_DX>::TM;
+  p.mt_bound = (int)((R + TM - 1) / TM + G);
+  p.n_tiles = (int)((K + TN - 1) / TN);
+  const unsigned grid = (unsigned)((int64_t)p.mt_bound * p.n_tiles);
+  return launch<KIND_DX, false, true>(p, grid, stream, "grouped_gemm_dx(swiglu_bwd)");
 }
 
 extern "C" moe_status moe_grouped_gemm_dw(const moe_bf16* A, const moe_bf16* dC, const moe_bf16* dC2,

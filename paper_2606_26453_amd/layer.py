@@ -37,8 +37,13 @@ class _Traced:
 
 
 class MoELayer(_Traced):
-    def __init__(self, cfg, inputs: dict, normalize_topk: bool = True):
+    """fuse_swiglu_bwd: the down projection's dX GEMM computes the SwiGLU backward in its epilogue
+    (moe_grouped_gemm_dx_swiglu_bwd) instead of storing dA for a separate moe_swiglu_bwd pass;
+    dA is then not materialised (buf["d_act"] / buf["d_act_sh"] stay unwritten)."""
+
+    def __init__(self, cfg, inputs: dict, normalize_topk: bool = True, fuse_swiglu_bwd: bool = True):
         self.cfg = cfg
+        self.fuse = fuse_swiglu_bwd
         self.inp = inputs
         self.normalize = normalize_topk
         dev = inputs["x"].device
@@ -93,12 +98,17 @@ class MoELayer(_Traced):
         b, i, k, run = self.buf, self.inp, self.cfg.k, self._run
         run("combine_bwd", moe.moe_unpermute_combine_bwd, i["dy"], b["topk_w"], b["row_of_slot"], k,
             y_perm=b["y_perm"], dy_perm=b["dy_perm"], d_topk_w=b["d_topk_w"], stream=stream)
-        run("dx_down", moe.moe_grouped_gemm_dx, b["dy_perm"], i["w_down"], b["offsets"], dA=b["d_act"],
-            stream=stream)
+        if self.fuse:
+            run("dx_down_swiglu_bwd", moe.moe_grouped_gemm_dx_swiglu_bwd, b["dy_perm"], i["w_down"],
+                b["offsets"], b["h_gate"], b["h_up"], b["dh_gate"], b["dh_up"], stream=stream)
+        else:
+            run("dx_down", moe.moe_grouped_gemm_dx, b["dy_perm"], i["w_down"], b["offsets"], dA=b["d_act"],
+                stream=stream)
         run("dw_down", moe.moe_grouped_gemm_dw, b["act"], b["dy_perm"], b["offsets"], dB=b["dw_down"],
             stream=stream)
-        run("swiglu_bwd", moe.moe_swiglu_bwd, b["h_gate"], b["h_up"], b["d_act"], b["dh_gate"], b["dh_up"],
-            stream=stream)
+        if not self.fuse:
+            run("swiglu_bwd", moe.moe_swiglu_bwd, b["h_gate"], b["h_up"], b["d_act"], b["dh_gate"],
+                b["dh_up"], stream=stream)
         run("dx_gate_up", moe.moe_grouped_gemm_dx, b["dh_gate"], i["w_gate"], b["offsets"], b["dh_up"],
             i["w_up"], dA=b["dx_perm"], stream=stream)
         run("dw_gate_up", moe.moe_grouped_gemm_dw, b["x_perm"], b["dh_gate"], b["offsets"], b["dh_up"],
@@ -106,12 +116,17 @@ class MoELayer(_Traced):
         add = None
         if self.shared:
             wg, wu, wd = self.w_sh
-            run("dx_down_sh", moe.moe_grouped_gemm_dx, i["dy"], wd, self.offsets_sh, dA=b["d_act_sh"],
-                stream=stream)
+            if self.fuse:
+                run("dx_down_swiglu_bwd_sh", moe.moe_grouped_gemm_dx_swiglu_bwd, i["dy"], wd, self.offsets_sh,
+                    b["h_gate_sh"], b["h_up_sh"], b["dh_gate_sh"], b["dh_up_sh"], stream=stream)
+            else:
+                run("dx_down_sh", moe.moe_grouped_gemm_dx, i["dy"], wd, self.offsets_sh, dA=b["d_act_sh"],
+                    stream=stream)
             run("dw_down_sh", moe.moe_grouped_gemm_dw, b["act_sh"], i["dy"], self.offsets_sh,
                 dB=b["dw_down_sh"], stream=stream)
-            run("swiglu_bwd_sh", moe.moe_swiglu_bwd, b["h_gate_sh"], b["h_up_sh"], b["d_act_sh"],
-                b["dh_gate_sh"], b["dh_up_sh"], stream=stream)
+            if not self.fuse:
+                run("swiglu_bwd_sh", moe.moe_swiglu_bwd, b["h_gate_sh"], b["h_up_sh"], b["d_act_sh"],
+                    b["dh_gate_sh"], b["dh_up_sh"], stream=stream)
             run("dx_gate_up_sh", moe.moe_grouped_gemm_dx, b["dh_gate_sh"], wg, self.offsets_sh, b["dh_up_sh"],
                 wu, dA=b["dx_sh"], stream=stream)
             run("dw_gate_up_sh", moe.moe_grouped_gemm_dw, i["x"], b["dh_gate_sh"], self.offsets_sh,
@@ -136,6 +151,7 @@ class MoELayer(_Traced):
             "combine": ("bytes", R * d * 2 + T * d * 2 + T * k * 8 + (T * d * 2 if self.shared else 0)),
             "combine_bwd": ("bytes", T * d * 2 + 2 * R * d * 2 + T * k * 12),
             "dx_down": ("flops", 2 * R * d * f), "dw_down": ("flops", 2 * R * f * d),
+            "dx_down_swiglu_bwd": ("flops", 2 * R * d * f),
             "swiglu_bwd": ("bytes", 5 * R * f * 2),
             "dx_gate_up": ("flops", 4 * R * d * f), "dw_gate_up": ("flops", 4 * R * d * f),
             "unpermute_dx": ("bytes", R * d * 2 + T * d * 2 + R * 4 + (T * d * 2 if self.shared else 0)),
@@ -144,6 +160,7 @@ class MoELayer(_Traced):
             fs = c.f_shared
             w.update({"fwd_gate_up_sh": ("flops", 4 * T * d * fs), "fwd_down_sh": ("flops", 2 * T * fs * d),
                       "dx_down_sh": ("flops", 2 * T * d * fs), "dw_down_sh": ("flops", 2 * T * fs * d),
+                      "dx_down_swiglu_bwd_sh": ("flops", 2 * T * d * fs),
                       "swiglu_bwd_sh": ("bytes", 5 * T * fs * 2),
                       "dx_gate_up_sh": ("flops", 4 * T * d * fs), "dw_gate_up_sh": ("flops", 4 * T * d * fs)})
         return w

@@ -43,6 +43,7 @@ _SIG = {
     "moe_unpermute_combine_bwd": (ctypes.c_int, [_P, _P, _P, _P, _I64, _I64, _I32, _P, _P, _P]),
     "moe_grouped_gemm_dx": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P]),
     "moe_grouped_gemm_dw": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P]),
+    "moe_grouped_gemm_dx_swiglu_bwd": (ctypes.c_int, [_P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P, _P, _P]),
 }
 
 
@@ -246,3 +247,23 @@ def moe_grouped_gemm_dw(A, dC, offsets, dC2=None, dB=None, dB2=None, stream=None
            lib().moe_grouped_gemm_dw(_ptr(A), _ptr(dC), _ptr(dC2), _ptr(offsets), G, R, K, N, _ptr(dB),
                                      _ptr(dB2), _stream(stream)))
     return dB, dB2
+
+
+def moe_grouped_gemm_dx_swiglu_bwd(dC, B, offsets, h_gate, h_up, dh_gate=None, dh_up=None, stream=None):
+    R, N = dC.shape
+    G, K, N2 = B.shape
+    if N2 != N:
+        raise ValueError("dC and B disagree on N")
+    _need(dC, torch.bfloat16, (R, N), "dC")
+    _need(B, torch.bfloat16, (G, K, N), "B")
+    _need(offsets, torch.int32, (G + 1,), "offsets")
+    _need(h_gate, torch.bfloat16, (R, K), "h_gate")
+    _need(h_up, torch.bfloat16, (R, K), "h_up")
+    dh_gate = torch.empty((R, K), dtype=torch.bfloat16, device=dC.device) if dh_gate is None else dh_gate
+    dh_up = torch.empty((R, K), dtype=torch.bfloat16, device=dC.device) if dh_up is None else dh_up
+    _need(dh_gate, torch.bfloat16, (R, K), "dh_gate")
+    _need(dh_up, torch.bfloat16, (R, K), "dh_up")
+    _check("moe_grouped_gemm_dx_swiglu_bwd",
+           lib().moe_grouped_gemm_dx_swiglu_bwd(_ptr(dC), _ptr(B), _ptr(offsets), G, R, K, N, _ptr(h_gate),
+                                                _ptr(h_up), _ptr(dh_gate), _ptr(dh_up), _stream(stream)))
+    return dh_gate, dh_up

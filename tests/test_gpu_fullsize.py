@@ -68,6 +68,7 @@ def test_layer_fullsize_sampled(cfg_id, ntok):
 
     ref = {key: {} for key in ("h_gate", "h_up", "act", "y_perm", "dy_perm", "d_act", "dh_gate", "dh_up",
                                "dx_perm")}
+    fused = lay.fuse   # dA is not materialised when the SwiGLU backward is fused into the dX GEMM
     dw_cols = rng.choice(cfg.f, 4, replace=False)
     dw_rows_f = rng.choice(cfg.f, 3, replace=False)
     dy_all = None
@@ -107,6 +108,8 @@ def test_layer_fullsize_sampled(cfg_id, ntok):
 
     all_rows = sorted(ref["h_gate"])
     for key in ref:
+        if key == "d_act" and fused:
+            continue
         got = _rows(b[key], all_rows)
         want = np.stack([ref[key][r] for r in all_rows])
         check_float(key, got, want)
@@ -120,6 +123,8 @@ def test_layer_fullsize_sampled(cfg_id, ntok):
         tok_t = torch.as_tensor(toks, dtype=torch.long, device=DEV)
         for key, val in (("h_gate_sh", hgs), ("h_up_sh", hus), ("act_sh", as_), ("y_sh", ys),
                          ("d_act_sh", das), ("dh_gate_sh", dhgs), ("dh_up_sh", dhus), ("dx_sh", dxs)):
+            if key == "d_act_sh" and fused:
+                continue
             check_float(key, f64(b[key][tok_t]), val)
         y_sh_t, dx_sh_t = ys, dxs
         xs = f64(inp["x"])

@@ -192,10 +192,10 @@ def test_swiglu_fwd_bwd():
 # ---------------------------------------------------------------------------------------------
 # whole layer, small configs: every tensor vs the oracle
 # ---------------------------------------------------------------------------------------------
-def _layer_parity(cfg, seed=0, expert_bias=None, log=None):
+def _layer_parity(cfg, seed=0, expert_bias=None, log=None, fuse=True):
     inp = W.make_inputs(cfg, seed, "cpu", expert_bias=expert_bias)
     dinp = {k_: v.to(DEV) for k_, v in inp.items()}
-    lay = L.MoELayer(cfg, dinp)
+    lay = L.MoELayer(cfg, dinp, fuse_swiglu_bwd=fuse)
     for t in lay.buf.values():
         if t.dtype != torch.uint8:
             poison_(t)
@@ -215,22 +215,51 @@ def _layer_parity(cfg, seed=0, expert_bias=None, log=None):
     check_float("topk_w", f64(b["topk_w"]), fwd["topk_w"], 1e-5, log)
     for key in ("h_gate", "h_up", "act", "y_perm", "y"):
         check_float(key, f64(b[key]), fwd[key], log=log)
-    for key in ("dy_perm", "d_topk_w", "d_act", "dw_down", "dh_gate", "dh_up", "dx_perm", "dw_gate", "dw_up", "dx"):
+    for key in ("dy_perm", "d_topk_w", "dw_down", "dh_gate", "dh_up", "dx_perm", "dw_gate", "dw_up", "dx"):
         check_float(key, f64(b[key]), bwd[key], log=log)
+    if not fuse:
+        check_float("d_act", f64(b["d_act"]), bwd["d_act"], log=log)
     if cfg.f_shared:
         for key in ("h_gate", "h_up", "act", "y"):
             check_float(key + "_sh", f64(b[key + "_sh" if key != "y" else "y_sh"]), fwd["shared"][key], log=log)
         for key in ("dw_gate", "dw_up", "dw_down"):
             check_float(key + "_sh", f64(b[key + "_sh"])[0], bwd["shared"][key], log=log)
         check_float("dx_sh", f64(b["dx_sh"]), bwd["shared"]["dx"], log=log)
+        for key in ("dh_gate", "dh_up"):
+            check_float(key + "_sh", f64(b[key + "_sh"]), bwd["shared"][key], log=log)
     return lay
 
 
-def test_layer_config0_parity():
-    _say("layer parity cfg0")
+@pytest.mark.parametrize("fuse", [True, False], ids=["fused_swiglu_bwd", "unfused"])
+def test_layer_config0_parity(fuse):
+    _say("layer parity cfg0", "fused" if fuse else "unfused")
     log = {}
-    _layer_parity(W.CONFIGS[0], log=log)
+    _layer_parity(W.CONFIGS[0], log=log, fuse=fuse)
     _say({k_: f"{v:.2e}" for k_, v in log.items()})
+
+
+def test_dx_swiglu_bwd_fusion_bitwise():
+    """The fused dX+SwiGLU-backward epilogue equals moe_grouped_gemm_dx then moe_swiglu_bwd bit for
+    bit (same rounding of dA, same elementwise arithmetic), on ragged groups spanning tiles."""
+    g = torch.Generator().manual_seed(21)
+    counts = GROUPS
+    G, R = len(counts), sum(counts)
+    K, N = 320, 192
+    off = torch.tensor(np.concatenate([[0], np.cumsum(counts)]), dtype=torch.int32).to(DEV)
+    dC = torch.randn((R, N), generator=g).to(torch.bfloat16).to(DEV)
+    B = (torch.randn((G, K, N), generator=g) * 0.1).to(torch.bfloat16).to(DEV)
+    hg = (torch.randn((R, K), generator=g) * 2).to(torch.bfloat16).to(DEV)
+    hu = torch.randn((R, K), generator=g).to(torch.bfloat16).to(DEV)
+    dA = moe.moe_grouped_gemm_dx(dC, B, off)
+    ref_g, ref_u = moe.moe_swiglu_bwd(hg, hu, dA)
+    fg, fu = (poison_(torch.empty((R, K), dtype=torch.bfloat16, device=DEV)) for _ in range(2))
+    moe.moe_grouped_gemm_dx_swiglu_bwd(dC, B, off, hg, hu, fg, fu)
+    torch.cuda.synchronize()
+    assert torch.equal(fg.view(torch.int16), ref_g.view(torch.int16))
+    assert torch.equal(fu.view(torch.int16), ref_u.view(torch.int16))
+    og, ou = O.swiglu_bwd(f64(hg), f64(hu), O.grouped_gemm_dx(f64(dC), f64(B), off.cpu().numpy()))
+    check_float("dh_gate", f64(fg), og)
+    check_float("dh_up", f64(fu), ou)
 
 
 @pytest.mark.parametrize("name,cfg,bias", [
