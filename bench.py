@@ -27,13 +27,13 @@ METRIC = "MoE layer fwd+bwd tokens/sec + grouped-GEMM TFLOP/s (% of bf16 MFMA pe
 # WRITE_SIZE runs scaled by a plain copy of known size (profiles/grouped_gemm_hbm_traffic_*.md).
 # Valid only for the kernel code they were measured on (sha256 prefix of the source with comments
 # and blank lines removed); otherwise reported null.
-TRAFFIC_SOURCE = ("paper_2606_26453_amd/csrc/grouped_gemm.hip", "ca34d45e38d0caa6")
+TRAFFIC_SOURCE = ("paper_2606_26453_amd/csrc/grouped_gemm.hip", "0565df3d83ed8e93")
 TRAFFIC_CONFIG = 1
 FETCH_SCALE, WRITE_SCALE = 2.0 * 1024, 1.0 * 1024
 TRAFFIC_KIB = {  # call: (FETCH_SIZE KiB, WRITE_SIZE KiB) per dispatch
-    "fwd_gate_up": (4602359, 1376256), "fwd_down": (2015935, 131072),
-    "dx_down_swiglu_bwd": (2937298, 917504), "dx_gate_up": (4257400, 131072),
-    "dw_down": (1525793, 1835008), "dw_gate_up": (2761579, 3671781),
+    "fwd_gate_up": (4609741, 1376256), "fwd_down": (2044464, 131072),
+    "dx_down_swiglu_bwd": (3036474, 917504), "dx_gate_up": (4296027, 131072),
+    "dw_down": (1545215, 1835017), "dw_gate_up": (2756682, 3671501),
 }
 
 

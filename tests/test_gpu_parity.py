@@ -153,6 +153,52 @@ def test_grouped_gemm_dw_exact(K, N):
     assert torch.count_nonzero(dB[5]) == 0 and torch.count_nonzero(dB[10]) == 0   # empty groups
 
 
+def test_grouped_gemm_256_groups_exact():
+    """The maximum group count (G = 256, empty groups included) with more row tiles than CUs, so
+    the persistent dX kernel walks several tiles per workgroup: every product exact on
+    small-integer operands, and the fused dX + SwiGLU backward bitwise equal to the two calls."""
+    _say("gemm 256 groups exact")
+    rng = np.random.default_rng(256)
+    counts = rng.integers(0, 400, 256)
+    counts[rng.choice(256, 20, replace=False)] = 0
+    G, R = 256, int(counts.sum())
+    off = torch.tensor(np.concatenate([[0], np.cumsum(counts)]), dtype=torch.int32)
+    offd = off.to(DEV)
+    g = torch.Generator().manual_seed(256)
+    # fwd: C = A B[g] (K = 64, N = 512), dual with SwiGLU
+    A = _int_tensor(g, (R, 64))
+    B, B2 = _int_tensor(g, (G, 64, 512)), _int_tensor(g, (G, 64, 512))
+    C, C2, act = moe.moe_grouped_gemm_fwd(A.to(DEV), B.to(DEV), offd, B2.to(DEV), want_act=True)
+    C1 = moe.moe_grouped_gemm_fwd(A.to(DEV), B.to(DEV), offd)[0]
+    torch.cuda.synchronize()
+    refC = O.grouped_gemm(f64(A), f64(B), off.numpy())
+    np.testing.assert_array_equal(f64(C), refC)
+    np.testing.assert_array_equal(f64(C1), refC)
+    np.testing.assert_array_equal(f64(C2), O.grouped_gemm(f64(A), f64(B2), off.numpy()))
+    # dX: dA = dC B[g]^T (K = 512 output columns, N = 64 contraction), single and dual
+    dC, dC2 = _int_tensor(g, (R, 64)), _int_tensor(g, (R, 64))
+    Bx, Bx2 = _int_tensor(g, (G, 512, 64)), _int_tensor(g, (G, 512, 64))
+    dA = moe.moe_grouped_gemm_dx(dC.to(DEV), Bx.to(DEV), offd)
+    dA2 = moe.moe_grouped_gemm_dx(dC.to(DEV), Bx.to(DEV), offd, dC2.to(DEV), Bx2.to(DEV))
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(f64(dA), O.grouped_gemm_dx(f64(dC), f64(Bx), off.numpy()))
+    np.testing.assert_array_equal(f64(dA2), O.grouped_gemm_dx(f64(dC), f64(Bx), off.numpy(), f64(dC2), f64(Bx2)))
+    hg = (torch.randn((R, 512), generator=g) * 2).to(torch.bfloat16).to(DEV)
+    hu = torch.randn((R, 512), generator=g).to(torch.bfloat16).to(DEV)
+    ref_g, ref_u = moe.moe_swiglu_bwd(hg, hu, dA)
+    fg, fu = moe.moe_grouped_gemm_dx_swiglu_bwd(dC.to(DEV), Bx.to(DEV), offd, hg, hu)
+    torch.cuda.synchronize()
+    assert torch.equal(fg.view(torch.int16), ref_g.view(torch.int16))
+    assert torch.equal(fu.view(torch.int16), ref_u.view(torch.int16))
+    # dW: dB[g] = A_g^T dC_g (64 x 128 per group), empty groups exactly zero
+    dCw = _int_tensor(g, (R, 128), -2, 2)
+    dB = moe.moe_grouped_gemm_dw(A.to(DEV), dCw.to(DEV), offd)[0]
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(f64(dB), O.grouped_gemm_dw(f64(A), f64(dCw), off.numpy()))
+    for e in np.flatnonzero(counts == 0):
+        assert torch.count_nonzero(dB[int(e)]) == 0
+
+
 def test_grouped_gemm_dw_worked_example():
     """The hand-evaluated dW1 example of Appendix H's definition, zero-padded to 64-multiples."""
     import json, os
