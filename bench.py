@@ -2,6 +2,10 @@
 
 python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1] [--no-cpu-baseline]
 
+--config 0..4 are the layer configurations (1, the Mixtral-shaped layer, is the default and the
+headline); --config 5 times the paper's own kernel alone, the gate/up weight gradient dW1 at its
+GPT-OSS-120B shape with bf16 output.
+
 A step is one forward and one backward pass of the whole layer (routing, permutation, gather,
 gate/up grouped GEMM with fused SwiGLU, down grouped GEMM, combine, and the backward dX/dW grouped
 GEMMs, SwiGLU backward, combine backward and dX unpermute) over one batch of synthetic tokens
@@ -111,6 +115,17 @@ def cpu_baseline(cfg, inp, sample_tokens):
                       f"all {cfg.E} experts, {dt:.1f} s"}
 
 
+def workload_name(i, cfg):
+    if not cfg.dw_only:
+        return f"config {i}: {cfg.name} MoE FFN layer fwd+bwd"
+    what = "dW1 (gate/up weight gradient) grouped GEMM" if cfg.dw1_only else "dW grouped GEMMs"
+    extra = []
+    if cfg.dirmult_alpha:
+        extra.append(f"Dirichlet-Multinomial loads alpha={cfg.dirmult_alpha}")
+    extra.append("bf16 output" if cfg.dw_bf16 else "fp32 output")
+    return f"config {i}: {cfg.name} {what}, " + ", ".join(extra)
+
+
 def main():
     a = _args()
     if a.gpus != 1:
@@ -201,8 +216,7 @@ def main():
         "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded N(0,1) activations, N(0,0.02) weights, router logits X.Wr)",
-        "config": {"workload": f"config {a.config}: {cfg.name} MoE FFN layer fwd+bwd" if not cfg.dw_only
-                   else f"config {a.config}: {cfg.name} dW grouped GEMMs",
+        "config": {"workload": workload_name(a.config, cfg),
                    "T": cfg.T, "d": cfg.d, "f": cfg.f, "E": cfg.E, "k": cfg.k, "f_shared": cfg.f_shared,
                    "parallelism": "single GPU"},
         "gemm_tflops": round(gemm_flops / gemm_ms / 1e9, 1) if gemm_ms else None,

@@ -198,6 +198,18 @@ moe_status moe_grouped_gemm_dw(const moe_bf16* A, const moe_bf16* dC, const moe_
                                const int32_t* offsets, int32_t G, int64_t R, int64_t K,
                                int64_t N, float* dB, float* dB2, hipStream_t stream);
 
+/*
+ * The same weight gradient with each result rounded once to bf16 (round-to-nearest-even of the
+ * fp32 sum): the output dtype of the paper's kernel, which stores dW1 in the input precision
+ * (Appendix H, kernel epilogue and host launcher).  Halves the output bytes, which matters at the
+ * paper's GPT-OSS shape (K = 2880, N = 2 x 2880, 128 experts), whose dW output is as large as its
+ * operands.  Arguments, layout, empty-group zeros and errors as moe_grouped_gemm_dw; dB, dB2
+ * [G,K,N] bf16.
+ */
+moe_status moe_grouped_gemm_dw_bf16(const moe_bf16* A, const moe_bf16* dC, const moe_bf16* dC2,
+                                    const int32_t* offsets, int32_t G, int64_t R, int64_t K,
+                                    int64_t N, moe_bf16* dB, moe_bf16* dB2, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -133,9 +133,10 @@ __device__ __forceinline__ void band_order(int id, int mtiles, int ntiles, int& 
 
 // One workgroup computes a TM x 256 output tile with WAVES_M x WAVES_N wavefronts through an
 // NSTAGE-deep LDS ring; WPE workgroups share a CU (2 when the ring is small enough).  PERSIST: the
-// workgroup loops over tiles (grid = CU slots) instead of computing one tile (grid = tiles).
+// workgroup loops over tiles (grid = CU slots) instead of computing one tile (grid = tiles).  OUT16:
+// dW results are rounded to bf16 (as the paper's kernel stores them) instead of stored as fp32.
 template <int KIND, bool DUAL, bool ACT, int TM, int WAVES_M, int WAVES_N, int NSTAGE, bool PINGPONG, int WPE,
-          bool PERSIST>
+          bool PERSIST, bool OUT16>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kernel(GemmParams p) {
   constexpr int NWAVE = WAVES_M * WAVES_N;
   constexpr int OPND_M = TM * BK * 2;         // bytes of the M-side tile of one stage
@@ -544,7 +545,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
   if constexpr (PERSIST) asm volatile("" : "+v"(tid));
   const int lane = tid & 63, l32 = lane & 31, fh = lane >> 5;
   const int col_in = 4 * fh;
-  if constexpr (KIND == KIND_DW) {
+  if constexpr (KIND == KIND_DW && !OUT16) {
 #pragma unroll
     for (int i = 0; i < MB; ++i) {
       const int mrow = wm * WTM + 32 * i + l32;
@@ -579,9 +580,17 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
     // segments instead of 16 bytes in each of 32 rows.  Dual mode keeps the gate columns of a row in
     // chunks 0..15 and the up columns in chunks 16..31.
     static_assert(TM * TN * 2 <= NSTAGE * STAGE, "the bf16 tile fits in the ring");
-    // only the forward dual product has two outputs side by side in its tile; the dual dX product
-    // sums both contractions into one output
-    constexpr bool SPLIT = (KIND == KIND_FWD) && DUAL;
+    // the dual fwd and dW products have two outputs side by side in their tile; the dual dX
+    // product sums both contractions into one output
+    constexpr bool SPLIT = (KIND != KIND_DX) && DUAL;
+    // output rows of the tile: fwd/dX the permuted rows row_lo .. row_hi-1; dW rows mt*TM .. of
+    // dB[g] (at most K)
+    int64_t obase = 0;
+    if constexpr (KIND == KIND_DW) {
+      obase = (int64_t)g * p.K * p.N;
+      row_lo = (int64_t)mt * TM;
+      row_hi = p.K;
+    }
     __syncthreads();   // every wave is done with the ring
 #pragma unroll
     for (int i = 0; i < MB; ++i) {
@@ -607,8 +616,8 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
       const int c = tid & 15;
       const int64_t n = (int64_t)nt * (TN / 2) + 8 * c;
       if (n < p.N) {
-        uint16_t* c1 = static_cast<uint16_t*>(p.out) + n;
-        uint16_t* c2 = static_cast<uint16_t*>(p.out2) + n;
+        uint16_t* c1 = static_cast<uint16_t*>(p.out) + obase + n;
+        uint16_t* c2 = static_cast<uint16_t*>(p.out2) + obase + n;
         for (int t = tid >> 4; t < TM; t += NT / 16) {
           const int64_t r = row_lo + t;
           if (r >= row_hi) break;
@@ -667,7 +676,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
             }
           }
         } else {
-          uint16_t* dst = static_cast<uint16_t*>(p.out) + n;
+          uint16_t* dst = static_cast<uint16_t*>(p.out) + obase + n;
           for (int t = tid >> 5; t < TM; t += NT / 32) {
             const int64_t r = row_lo + t;
             if (r >= row_hi) break;
@@ -698,7 +707,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
     const int next = it + (int)gridDim.x;
     const bool more = next < ntiles_all;   // uniform
     int g2 = 0, mt2 = 0, nt2 = 0, lo2 = 0, hi2 = 0;
-    if constexpr (KIND == KIND_DW) {
+    if constexpr (KIND == KIND_DW && !OUT16) {
       // fp32 results leave from registers: once every wave is done with the ring, start filling
       // it with the next tile's first stages, then store this tile
       __syncthreads();
@@ -743,7 +752,7 @@ template <int KIND> struct Cfg {
   static constexpr bool PERSIST = (KIND == KIND_DX);
 };
 
-template <int KIND, bool DUAL, bool ACT>
+template <int KIND, bool DUAL, bool ACT, bool OUT16 = false>
 moe_status launch(const GemmParams& p, int64_t tiles_bound, hipStream_t stream, const char* name) {
   if (tiles_bound == 0) return MOE_SUCCESS;
   if (tiles_bound >= ((int64_t)1 << 31)) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: too many tiles", name);
@@ -756,7 +765,7 @@ moe_status launch(const GemmParams& p, int64_t tiles_bound, hipStream_t stream, 
     if (slots > 8) slots &= ~7u;
     if (grid > slots) grid = slots;
   }
-  grouped_gemm_kernel<KIND, DUAL, ACT, C::TM, C::WM, C::WN, C::NS, C::PP, C::WPE, C::PERSIST>
+  grouped_gemm_kernel<KIND, DUAL, ACT, C::TM, C::WM, C::WN, C::NS, C::PP, C::WPE, C::PERSIST, OUT16>
       <<<grid, 64 * C::WM * C::WN, 0, stream>>>(p);
   return check_launch(name);
 }
@@ -853,20 +862,21 @@ extern "C" moe_status moe_grouped_gemm_dx_swiglu_bwd(const moe_bf16* dC, const m
   return launch<KIND_DX, false, true>(p, tiles, stream, "grouped_gemm_dx(swiglu_bwd)");
 }
 
-extern "C" moe_status moe_grouped_gemm_dw(const moe_bf16* A, const moe_bf16* dC, const moe_bf16* dC2,
-                                          const int32_t* offsets, int32_t G, int64_t R, int64_t K,
-                                          int64_t N, float* dB, float* dB2, hipStream_t stream) {
-  if (G < 1 || G > 256) return fail(MOE_ERROR_NOT_SUPPORTED, "moe_grouped_gemm_dw: need 1 <= G <= 256");
-  if (R < 0 || K <= 0 || N <= 0) return fail(MOE_ERROR_INVALID_VALUE, "moe_grouped_gemm_dw: bad size");
-  if (K % 64 || N % 64) return fail(MOE_ERROR_NOT_SUPPORTED, "moe_grouped_gemm_dw: K and N must be multiples of 64");
-  if (R >= ((int64_t)1 << 31)) return fail(MOE_ERROR_NOT_SUPPORTED, "moe_grouped_gemm_dw: R >= 2^31");
-  if (!offsets) return fail(MOE_ERROR_INVALID_VALUE, "moe_grouped_gemm_dw: offsets is NULL");
+namespace moe {
+namespace {
+moe_status grouped_gemm_dw_impl(const char* fn, bool out16, const moe_bf16* A, const moe_bf16* dC,
+                                const moe_bf16* dC2, const int32_t* offsets, int32_t G, int64_t R,
+                                int64_t K, int64_t N, void* dB, void* dB2, hipStream_t stream) {
+  if (G < 1 || G > 256) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: need 1 <= G <= 256", fn);
+  if (R < 0 || K <= 0 || N <= 0) return fail(MOE_ERROR_INVALID_VALUE, "%s: bad size", fn);
+  if (K % 64 || N % 64) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: K and N must be multiples of 64", fn);
+  if (R >= ((int64_t)1 << 31)) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: R >= 2^31", fn);
+  if (!offsets) return fail(MOE_ERROR_INVALID_VALUE, "%s: offsets is NULL", fn);
   if ((dC2 == nullptr) != (dB2 == nullptr))
-    return fail(MOE_ERROR_INVALID_VALUE, "moe_grouped_gemm_dw: dC2 and dB2 must both be set or both NULL");
-  if (!dB || (R > 0 && (!A || !dC)))
-    return fail(MOE_ERROR_INVALID_VALUE, "moe_grouped_gemm_dw: NULL pointer");
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: dC2 and dB2 must both be set or both NULL", fn);
+  if (!dB || (R > 0 && (!A || !dC))) return fail(MOE_ERROR_INVALID_VALUE, "%s: NULL pointer", fn);
   if (bad_ptr(A) || bad_ptr(dC) || bad_ptr(dC2) || bad_ptr(dB) || bad_ptr(dB2))
-    return fail(MOE_ERROR_INVALID_VALUE, "moe_grouped_gemm_dw: pointers must be 16-byte aligned");
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: pointers must be 16-byte aligned", fn);
   GemmParams p{};
   p.a = A; p.b = dC; p.b2 = dC2; p.offsets = offsets; p.out = dB; p.out2 = dB2;
   p.G = G; p.R = R; p.K = K; p.N = N;
@@ -874,6 +884,25 @@ extern "C" moe_status moe_grouped_gemm_dw(const moe_bf16* A, const moe_bf16* dC,
   const int cols_per_tile = dC2 ? TN / 2 : TN;
   p.n_tiles = (int)((N + cols_per_tile - 1) / cols_per_tile);
   const int64_t tiles = (int64_t)G * p.m_tiles * p.n_tiles;
+  if (out16) {
+    if (dC2) return launch<KIND_DW, true, false, true>(p, tiles, stream, "grouped_gemm_dw_bf16(dual)");
+    return launch<KIND_DW, false, false, true>(p, tiles, stream, "grouped_gemm_dw_bf16");
+  }
   if (dC2) return launch<KIND_DW, true, false>(p, tiles, stream, "grouped_gemm_dw(dual)");
   return launch<KIND_DW, false, false>(p, tiles, stream, "grouped_gemm_dw");
+}
+}  // namespace
+}  // namespace moe
+
+extern "C" moe_status moe_grouped_gemm_dw(const moe_bf16* A, const moe_bf16* dC, const moe_bf16* dC2,
+                                          const int32_t* offsets, int32_t G, int64_t R, int64_t K,
+                                          int64_t N, float* dB, float* dB2, hipStream_t stream) {
+  return grouped_gemm_dw_impl("moe_grouped_gemm_dw", false, A, dC, dC2, offsets, G, R, K, N, dB, dB2, stream);
+}
+
+extern "C" moe_status moe_grouped_gemm_dw_bf16(const moe_bf16* A, const moe_bf16* dC, const moe_bf16* dC2,
+                                               const int32_t* offsets, int32_t G, int64_t R, int64_t K,
+                                               int64_t N, moe_bf16* dB, moe_bf16* dB2, hipStream_t stream) {
+  return grouped_gemm_dw_impl("moe_grouped_gemm_dw_bf16", true, A, dC, dC2, offsets, G, R, K, N, dB, dB2,
+                              stream);
 }

@@ -167,26 +167,33 @@ class MoELayer(_Traced):
 
 
 class DWOnly(_Traced):
-    """The weight-gradient-only workload: dW_gate and dW_up in one pass, then dW_down."""
+    """The weight-gradient-only workload: dW_gate and dW_up in one pass, then dW_down (unless
+    cfg.dw1_only: the paper's dW1 alone); fp32 results, or bf16 when cfg.dw_bf16."""
 
     def __init__(self, cfg, inputs: dict):
         self.cfg = cfg
         self.inp = inputs
         dev = inputs["x_perm"].device
         E, d, f = cfg.E, cfg.d, cfg.f
+        dt = torch.bfloat16 if cfg.dw_bf16 else torch.float32
         self.buf = {
-            "dw_gate": torch.empty((E, d, f), dtype=torch.float32, device=dev),
-            "dw_up": torch.empty((E, d, f), dtype=torch.float32, device=dev),
-            "dw_down": torch.empty((E, f, d), dtype=torch.float32, device=dev),
+            "dw_gate": torch.empty((E, d, f), dtype=dt, device=dev),
+            "dw_up": torch.empty((E, d, f), dtype=dt, device=dev),
         }
+        if not cfg.dw1_only:
+            self.buf["dw_down"] = torch.empty((E, f, d), dtype=dt, device=dev)
 
     def step(self, stream=None):
         i, b = self.inp, self.buf
-        self._run("dw_gate_up", moe.moe_grouped_gemm_dw, i["x_perm"], i["dh_gate"], i["offsets"], i["dh_up"],
+        dw = moe.moe_grouped_gemm_dw_bf16 if self.cfg.dw_bf16 else moe.moe_grouped_gemm_dw
+        self._run("dw_gate_up", dw, i["x_perm"], i["dh_gate"], i["offsets"], i["dh_up"],
                   dB=b["dw_gate"], dB2=b["dw_up"], stream=stream)
-        self._run("dw_down", moe.moe_grouped_gemm_dw, i["act"], i["dy_perm"], i["offsets"], dB=b["dw_down"],
-                  stream=stream)
+        if not self.cfg.dw1_only:
+            self._run("dw_down", dw, i["act"], i["dy_perm"], i["offsets"], dB=b["dw_down"], stream=stream)
 
     def work(self):
         c = self.cfg
-        return {"dw_gate_up": ("flops", 4 * c.R * c.d * c.f), "dw_down": ("flops", 2 * c.R * c.f * c.d)}
+        w = {"dw_gate_up": ("flops", 4 * c.R * c.d * c.f)}
+        if not c.dw1_only:
+            w["dw_down"] = ("flops", 2 * c.R * c.f * c.d)
+        return w

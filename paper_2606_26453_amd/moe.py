@@ -43,6 +43,7 @@ _SIG = {
     "moe_unpermute_combine_bwd": (ctypes.c_int, [_P, _P, _P, _P, _I64, _I64, _I32, _P, _P, _P]),
     "moe_grouped_gemm_dx": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P]),
     "moe_grouped_gemm_dw": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P]),
+    "moe_grouped_gemm_dw_bf16": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P]),
     "moe_grouped_gemm_dx_swiglu_bwd": (ctypes.c_int, [_P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P, _P, _P]),
 }
 
@@ -246,6 +247,26 @@ def moe_grouped_gemm_dw(A, dC, offsets, dC2=None, dB=None, dB2=None, stream=None
     _check("moe_grouped_gemm_dw",
            lib().moe_grouped_gemm_dw(_ptr(A), _ptr(dC), _ptr(dC2), _ptr(offsets), G, R, K, N, _ptr(dB),
                                      _ptr(dB2), _stream(stream)))
+    return dB, dB2
+
+
+def moe_grouped_gemm_dw_bf16(A, dC, offsets, dC2=None, dB=None, dB2=None, stream=None):
+    """moe_grouped_gemm_dw with bf16 results (one rounding of the fp32 sum)."""
+    R, K = A.shape
+    N = dC.shape[1]
+    G = offsets.numel() - 1
+    _need(A, torch.bfloat16, (R, K), "A")
+    _need(dC, torch.bfloat16, (R, N), "dC")
+    _need(dC2, torch.bfloat16, (R, N), "dC2")
+    _need(offsets, torch.int32, (G + 1,), "offsets")
+    dB = torch.empty((G, K, N), dtype=torch.bfloat16, device=A.device) if dB is None else dB
+    if dC2 is not None and dB2 is None:
+        dB2 = torch.empty((G, K, N), dtype=torch.bfloat16, device=A.device)
+    _need(dB, torch.bfloat16, (G, K, N), "dB")
+    _need(dB2, torch.bfloat16, (G, K, N), "dB2")
+    _check("moe_grouped_gemm_dw_bf16",
+           lib().moe_grouped_gemm_dw_bf16(_ptr(A), _ptr(dC), _ptr(dC2), _ptr(offsets), G, R, K, N, _ptr(dB),
+                                          _ptr(dB2), _stream(stream)))
     return dB, dB2
 
 

@@ -34,6 +34,9 @@ class MoEConfig:
     zipf_s: float = 0.0      # Zipf exponent of the per-expert logit bias profile (0 = no bias)
     zipf_beta: float = 0.0   # bias scale: bias_e = beta * ln(z_rank(e))
     dw_only: bool = False    # weight-gradient path only, exactly uniform groups
+    dirmult_alpha: float = 0.0   # dw_only: group sizes ~ Dirichlet(alpha)-Multinomial(R) instead
+    dw1_only: bool = False   # dw_only: only the gate/up weight gradient (the paper's dW1)
+    dw_bf16: bool = False    # dw_only: weight gradients stored in bf16 (the paper's output dtype)
 
     @property
     def R(self) -> int:
@@ -42,7 +45,7 @@ class MoEConfig:
     def gemm_flops(self) -> int:
         """Algorithmic FLOPs of all grouped GEMMs of one step (only real rows, no padding)."""
         if self.dw_only:
-            return 6 * self.R * self.d * self.f
+            return (4 if self.dw1_only else 6) * self.R * self.d * self.f
         fl = 18 * self.R * self.d * self.f
         if self.f_shared:
             fl += 18 * self.T * self.d * self.f_shared
@@ -55,6 +58,12 @@ CONFIGS = {
     2: MoEConfig("fine_grained_shared", T=16384, d=2048, f=1408, E=64, k=6, f_shared=2 * 1408),
     3: MoEConfig("zipf_skew", T=16384, d=4096, f=2048, E=32, k=4, zipf_s=1.2, zipf_beta=1.5),
     4: MoEConfig("dw_long_batch", T=65536, d=4096, f=4096, E=16, k=2, dw_only=True),
+    # The paper's own measurement shape (section 5.4, Appendix H): GPT-OSS-120B's gate_up_proj
+    # weight gradient dW1 (hidden 2880, gate and up 2880 each), 128 experts, top-4, 57,768 routed
+    # rows, expert loads from the paper's Dirichlet-Multinomial fit (alpha = 0.24, empty experts
+    # possible), bf16 output.  Synthetic operands stand in for the model's activations.
+    5: MoEConfig("paper_dw1_gptoss", T=14442, d=2880, f=2880, E=128, k=4, dw_only=True,
+                 dirmult_alpha=0.24, dw1_only=True, dw_bf16=True),
 }
 
 ACT_STD = 1.0
@@ -121,11 +130,25 @@ def make_inputs(cfg: MoEConfig, seed: int = 0, device="cpu", expert_bias=None,
     return out
 
 
+def dirmult_counts(E: int, R: int, alpha: float, seed: int = 0):
+    """Rows per expert drawn as p ~ Dirichlet(alpha, ..., alpha) over E experts, then
+    counts ~ Multinomial(R, p) (the load model fitted in Appendix H, "Estimating the token-to-expert
+    distribution").  numpy's seeded generator; small alpha leaves some experts empty."""
+    import numpy as np
+    rng = np.random.default_rng(seed)
+    p = rng.dirichlet([alpha] * E)
+    return [int(v) for v in rng.multinomial(R, p)]
+
+
 def make_dw_inputs(cfg: MoEConfig, seed: int = 0, device="cpu", counts=None) -> dict:
-    """Operands of the weight-gradient-only workload: exactly uniform groups (R/E rows each unless
-    `counts` is given), x_perm [R,d], act [R,f], dh_gate/dh_up [R,f], dy_perm [R,d] ~ N(0,1) bf16."""
+    """Operands of the weight-gradient-only workload: exactly uniform groups (R/E rows each), or
+    Dirichlet-Multinomial group sizes when cfg.dirmult_alpha > 0, unless `counts` is given;
+    x_perm [R,d], dh_gate/dh_up [R,f] and (unless cfg.dw1_only) act [R,f], dy_perm [R,d] ~ N(0,1)
+    bf16."""
     gen = torch.Generator(device=device).manual_seed(seed)
     R, d, f, E = cfg.R, cfg.d, cfg.f, cfg.E
+    if counts is None and cfg.dirmult_alpha > 0:
+        counts = dirmult_counts(E, R, cfg.dirmult_alpha, seed)
     if counts is None:
         assert R % E == 0
         counts = [R // E] * E
@@ -133,14 +156,14 @@ def make_dw_inputs(cfg: MoEConfig, seed: int = 0, device="cpu", counts=None) -> 
     assert int(counts.sum()) == R and counts.numel() == E
     offsets = torch.zeros(E + 1, dtype=torch.int32)
     offsets[1:] = torch.cumsum(counts, 0).to(torch.int32)
-    return {
-        "offsets": offsets.to(device),
-        "x_perm": _normal((R, d), ACT_STD, gen, device),
-        "act": _normal((R, f), ACT_STD, gen, device),
-        "dh_gate": _normal((R, f), ACT_STD, gen, device),
-        "dh_up": _normal((R, f), ACT_STD, gen, device),
-        "dy_perm": _normal((R, d), ACT_STD, gen, device),
-    }
+    out = {"offsets": offsets.to(device), "x_perm": _normal((R, d), ACT_STD, gen, device)}
+    if not cfg.dw1_only:
+        out["act"] = _normal((R, f), ACT_STD, gen, device)
+    out["dh_gate"] = _normal((R, f), ACT_STD, gen, device)
+    out["dh_up"] = _normal((R, f), ACT_STD, gen, device)
+    if not cfg.dw1_only:
+        out["dy_perm"] = _normal((R, d), ACT_STD, gen, device)
+    return out
 
 
 def small_int_(t: torch.Tensor, gen: torch.Generator, lo=-1, hi=1, density=1.0) -> torch.Tensor:

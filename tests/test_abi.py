@@ -76,6 +76,13 @@ def test_gemm_rejects():
     dw = lambda G=4, R=100, K=128, N=128, dC2=None, dB2=None, dB=FAKE: L.moe_grouped_gemm_dw(
         FAKE, FAKE, dC2, FAKE, G, R, K, N, dB, dB2, None)
     assert dw(N=32) == 2 and dw(dC2=FAKE) == 1 and dw(dB=None) == 1 and dw(dB=BAD) == 1
+    dw16 = lambda G=4, R=100, K=128, N=128, dC2=None, dB2=None, dB=FAKE: L.moe_grouped_gemm_dw_bf16(
+        FAKE, FAKE, dC2, FAKE, G, R, K, N, dB, dB2, None)
+    assert dw16(G=257) == 2 and dw16(K=2880 + 32) == 2 and dw16(dC2=FAKE) == 1 and dw16(dB=None) == 1
+    assert dw16(dB=BAD) == 1 and dw16(R=-1) == 1
+    dxs = lambda G=4, R=100, K=128, N=128, hg=FAKE: L.moe_grouped_gemm_dx_swiglu_bwd(
+        FAKE, FAKE, FAKE, G, R, K, N, hg, FAKE, FAKE, FAKE, None)
+    assert dxs(N=100) == 2 and dxs(hg=None) == 1 and dxs(hg=BAD) == 1 and dxs(R=0) == 0
 
 
 def test_elementwise_rejects():

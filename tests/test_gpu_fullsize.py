@@ -1,5 +1,5 @@
 """Full-size parity of the layer in the launch configuration the benchmark times (MoELayer.step on
-the five layer configurations), against the CPU oracle.
+the five layer configurations and the paper's own dW1 shape), against the CPU oracle.
 
 Routing indices, expert offsets, the permutation and the gathered rows are compared in full and
 bit-exactly.  Floating outputs are compared on samples the oracle computes one by one with the
@@ -173,3 +173,36 @@ def test_dw_only_fullsize_sampled():
         rws_t = torch.as_tensor(rws, dtype=torch.long, device=DEV)
         check_float(f"dw_down[{e}] rows", f64(b["dw_down"][e][rws_t]),
                     O.grouped_gemm_dw(f64(inp["act"][sl][:, rws_t]), f64(inp["dy_perm"][sl]), loc)[0])
+
+
+def test_paper_dw1_fullsize_sampled():
+    """The paper's GPT-OSS dW1 shape (K = 2880, gate and up 2880 each, 128 experts, 57,768 rows,
+    Dirichlet-Multinomial loads with empty experts), bf16 output: sampled columns of the largest,
+    a small and the first nonempty expert against the oracle's bf16-rounded sums; every empty
+    expert's gradient exactly zero."""
+    cfg = W.CONFIGS[5]
+    _say(f"full-size dW1 parity: config 5 {cfg}")
+    inp = W.make_dw_inputs(cfg, 0, DEV)
+    lay = L.DWOnly(cfg, inp)
+    lay.step()
+    torch.cuda.synchronize()
+    b = lay.buf
+    assert b["dw_gate"].dtype == torch.bfloat16 and "dw_down" not in b
+    off = i64(inp["offsets"])
+    counts = np.diff(off)
+    _say("groups:", W.group_stats(counts))
+    assert (counts == 0).any()
+    rng = np.random.default_rng(5)
+    nz = np.flatnonzero(counts)
+    small = nz[np.argmin(counts[nz])]
+    for e in sorted({int(np.argmax(counts)), int(small), int(nz[0])}):
+        lo, hi = int(off[e]), int(off[e + 1])
+        cols = np.concatenate([rng.choice(cfg.f, 3, replace=False), [cfg.f - 1]])   # incl. the ragged last tile
+        cols_t = torch.as_tensor(cols, dtype=torch.long, device=DEV)
+        xp = f64(inp["x_perm"][lo:hi])
+        loc = np.array([0, hi - lo])
+        for name, src in (("dw_gate", "dh_gate"), ("dw_up", "dh_up")):
+            want = O.bf16_round(O.grouped_gemm_dw(xp, f64(inp[src][lo:hi][:, cols_t]), loc)[0])
+            check_float(f"{name}[{e}] cols", f64(b[name][e][:, cols_t]), want)
+    for e in np.flatnonzero(counts == 0):
+        assert torch.count_nonzero(b["dw_gate"][int(e)]) == 0 and torch.count_nonzero(b["dw_up"][int(e)]) == 0

@@ -199,6 +199,28 @@ def test_grouped_gemm_256_groups_exact():
         assert torch.count_nonzero(dB[int(e)]) == 0
 
 
+@pytest.mark.parametrize("K,N", [(320, 192), (256, 256)])
+def test_grouped_gemm_dw_bf16_exact(K, N):
+    """bf16-output dW: the fp32 sum of small integers is exact, so every output equals the
+    round-to-nearest-even of the exact sum (group sums above 256 do round); empty groups zero."""
+    _say("gemm_dw_bf16 exact", K, N)
+    g = torch.Generator().manual_seed(7 * K + N)
+    counts = GROUPS
+    G, R = len(counts), sum(counts)
+    off = torch.tensor(np.concatenate([[0], np.cumsum(counts)]), dtype=torch.int32)
+    A = _int_tensor(g, (R, K), -2, 2)
+    dC, dC2 = _int_tensor(g, (R, N), -2, 2), _int_tensor(g, (R, N), -2, 2)
+    dB, dB2, dB1 = (poison_(torch.empty((G, K, N), dtype=torch.bfloat16, device=DEV)) for _ in range(3))
+    moe.moe_grouped_gemm_dw_bf16(A.to(DEV), dC.to(DEV), off.to(DEV), dC2.to(DEV), dB, dB2)
+    moe.moe_grouped_gemm_dw_bf16(A.to(DEV), dC.to(DEV), off.to(DEV), dB=dB1)
+    torch.cuda.synchronize()
+    ref = O.bf16_round(O.grouped_gemm_dw(f64(A), f64(dC), off.numpy()))
+    np.testing.assert_array_equal(f64(dB), ref)
+    np.testing.assert_array_equal(f64(dB1), ref)
+    np.testing.assert_array_equal(f64(dB2), O.bf16_round(O.grouped_gemm_dw(f64(A), f64(dC2), off.numpy())))
+    assert torch.count_nonzero(dB[5]) == 0 and torch.count_nonzero(dB2[10]) == 0
+
+
 def test_grouped_gemm_dw_worked_example():
     """The hand-evaluated dW1 example of Appendix H's definition, zero-padded to 64-multiples."""
     import json, os
