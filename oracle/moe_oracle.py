@@ -16,8 +16,9 @@ defines one step of this layer: routed tokens are packed into one buffer ordered
 per-expert row counts are given as a cumulative sum, and for every expert the weight gradient of
 the first FFN projection is dW1_e = X_e^T G_e, a contraction over that expert's K_e rows (K_e may
 be zero).  `grouped_gemm_dw` is that definition.  The paper states no routing rule, row order,
-activation, combine or other backward formula; the readings used for those are the standard MoE
-layer and are named at each function.
+activation, combine, router or other backward formula; the readings used for those are the
+standard MoE layer (and, for the router's load-balancing loss, the Switch-style auxiliary loss) and
+are named at each function.
 
 Parity: every function here is pinned by the CPU test suite against closed forms, library
 routines, brute force or automatic differentiation; no function is "parity unpinned".
@@ -241,6 +242,74 @@ def combine_bwd(dy, topk_w, row_of_slot, y_perm, k, rnd=bf16_round):
         if y_perm is not None:
             d_w[:, j] = (dy * np.asarray(y_perm, dtype=np.float64)[rows[:, j]]).sum(axis=1)
     return _r(rnd, dy_perm), d_w
+
+
+# --------------------------------------------------------------------------------------------
+# Router: logits, the backward through the routing weights, the load-balancing loss
+# --------------------------------------------------------------------------------------------
+def router_logits(x, wr, bias=None):
+    """Router logits [T, E] = x [T, d] . Wr [d, E] (+ a per-expert bias).  The paper names top-k
+    routing (section 5.4) but not the router; reading: one linear map of the token, computed in
+    float32 by the layer (exactly here)."""
+    L = np.asarray(x, dtype=np.float64) @ np.asarray(wr, dtype=np.float64)
+    if bias is not None:
+        L = L + np.asarray(bias, dtype=np.float64)
+    return L
+
+
+def route_topk_bwd(logits, topk_idx, d_topk_w, normalize=True):
+    """Gradient of the routing weights with respect to the logits (the selection itself is
+    piecewise constant and passes no gradient).  With p the probabilities the weights are read
+    from (the softmax over the k selected logits when normalize, zero elsewhere; else the softmax
+    over all E) and G[t, e] = d_topk_w[t, j] where e = topk_idx[t, j] (0 for unselected e):
+        dlogits[t, e] = p[t, e] * (G[t, e] - sum_j d_topk_w[t, j] * p[t, topk_idx[t, j]]).
+    Returns dlogits [T, E] float64."""
+    L = np.asarray(logits, dtype=np.float64)
+    idx = np.asarray(topk_idx)
+    g = np.asarray(d_topk_w, dtype=np.float64)
+    T, E = L.shape
+    if normalize:
+        sel = np.take_along_axis(L, idx, axis=1)
+        ex = np.exp(sel - sel.max(axis=1, keepdims=True))
+        p = np.zeros((T, E))
+        np.put_along_axis(p, idx, ex / ex.sum(axis=1, keepdims=True), axis=1)
+    else:
+        ex = np.exp(L - L.max(axis=1, keepdims=True))
+        p = ex / ex.sum(axis=1, keepdims=True)
+    G = np.zeros((T, E))
+    np.put_along_axis(G, idx, g, axis=1)
+    s = (g * np.take_along_axis(p, idx, axis=1)).sum(axis=1, keepdims=True)
+    return p * (G - s)
+
+
+def aux_loss(logits, counts, k, alpha):
+    """Load-balancing loss of Switch-style MoE training (not in the paper; a standard companion
+    of top-k routing): L = alpha * E * sum_e f_e * P_e with f_e = counts[e] / (T * k), the share
+    of routed slots expert e received (held constant: counts are not differentiable), and P_e the
+    mean over tokens of the full softmax probability of e.  Returns (L, dL/dlogits [T, E]):
+        dL/dlogits[t, e] = alpha * E / T * p[t, e] * (f_e - sum_e' f_e' * p[t, e'])."""
+    L = np.asarray(logits, dtype=np.float64)
+    T, E = L.shape
+    ex = np.exp(L - L.max(axis=1, keepdims=True))
+    p = ex / ex.sum(axis=1, keepdims=True)
+    f = np.asarray(counts, dtype=np.float64) / (T * k)
+    loss = alpha * E * float((f * p.mean(axis=0)).sum())
+    grad = alpha * E / T * p * (f[None, :] - (p * f[None, :]).sum(axis=1, keepdims=True))
+    return loss, grad
+
+
+def router_bwd(x, wr, dlogits, dx=None, rnd=bf16_round):
+    """Backward of the router map: dWr [d, E] = x^T . dlogits (float64), and the router's share
+    of the token gradient, dlogits . Wr^T [T, d].  Reading: the router runs after the experts'
+    unpermute-sum has stored dX in bf16, so its share is added to that stored value and rounded
+    once more: returns (dWr, rnd(dx + dlogits . Wr^T)) (dx = None: the share alone, rounded)."""
+    x = np.asarray(x, dtype=np.float64)
+    g = np.asarray(dlogits, dtype=np.float64)
+    wr = np.asarray(wr, dtype=np.float64)
+    share = g @ wr.T
+    if dx is not None:
+        share = np.asarray(dx, dtype=np.float64) + share
+    return x.T @ g, _r(rnd, share)
 
 
 # --------------------------------------------------------------------------------------------

@@ -381,3 +381,100 @@ def test_sampled_helpers_match_full_oracle():
     dwg, dwu = O.dw_gate_up_cols(fwd["x_perm"][lo:hi], bwd["dy_perm"][lo:hi], wg[e], wu[e], wd[e], cols)
     np.testing.assert_allclose(dwg, bwd["dw_gate"][e][:, cols], rtol=1e-12)
     np.testing.assert_allclose(dwu, bwd["dw_up"][e][:, cols], rtol=1e-12)
+
+
+# ---------------------------------------------------------------------------------------------
+# Router: logits, routing-weight backward, load-balancing loss, router-map backward
+# ---------------------------------------------------------------------------------------------
+def test_router_logits_one_hot_and_integers():
+    """One-hot tokens read rows of Wr exactly; small-integer operands give exact dot products
+    checked by explicit loops (no matrix routine)."""
+    rng = np.random.default_rng(1)
+    d, E = 12, 5
+    wr = rng.normal(0, 0.02, (d, E))
+    x = np.eye(d)[[3, 0, 11]]
+    np.testing.assert_array_equal(O.router_logits(x, wr), wr[[3, 0, 11]])
+    bias = rng.normal(size=E)
+    np.testing.assert_array_equal(O.router_logits(x, wr, bias), wr[[3, 0, 11]] + bias)
+    xi = rng.integers(-3, 4, (7, d)).astype(float)
+    wi = rng.integers(-3, 4, (d, E)).astype(float)
+    want = [[sum(xi[t, i] * wi[i, e] for i in range(d)) for e in range(E)] for t in range(7)]
+    np.testing.assert_array_equal(O.router_logits(xi, wi), np.array(want))
+
+
+@pytest.mark.parametrize("normalize", [True, False])
+def test_route_topk_bwd_autograd(normalize):
+    """dlogits against torch autograd of the routing weights (softmax over the selected logits,
+    or the full softmax read at the selected experts), selection held fixed."""
+    rng = np.random.default_rng(2)
+    T, E, k = 9, 7, 3
+    L = rng.normal(size=(T, E)) * 2
+    idx, w = O.route_topk(L, k, normalize)
+    g = rng.normal(size=(T, k))
+    Lt = torch.tensor(L, dtype=torch.float64, requires_grad=True)
+    it = torch.tensor(idx)
+    if normalize:
+        wt = torch.softmax(torch.gather(Lt, 1, it), dim=1)
+    else:
+        wt = torch.gather(torch.softmax(Lt, dim=1), 1, it)
+    np.testing.assert_allclose(wt.detach().numpy(), w, rtol=1e-12)
+    (wt * torch.tensor(g)).sum().backward()
+    np.testing.assert_allclose(O.route_topk_bwd(L, idx, g, normalize), Lt.grad.numpy(), rtol=1e-10, atol=1e-14)
+
+
+def test_route_topk_bwd_properties_and_fd():
+    """Rows of the normalized-weight gradient sum to zero (the k weights sum to one) and vanish
+    outside the selection; one central finite difference of sum(g * w)."""
+    rng = np.random.default_rng(3)
+    T, E, k = 6, 8, 2
+    L = rng.normal(size=(T, E))
+    idx, _ = O.route_topk(L, k)
+    g = rng.normal(size=(T, k))
+    dl = O.route_topk_bwd(L, idx, g)
+    np.testing.assert_allclose(dl.sum(axis=1), 0, atol=1e-14)
+    mask = np.zeros((T, E), bool)
+    np.put_along_axis(mask, idx, True, axis=1)
+    assert (dl[~mask] == 0).all()
+    t, e = 4, int(idx[4, 1])
+    h = 1e-6
+    f = lambda LL: (g * O.route_topk(LL, k)[1]).sum()
+    Lp, Lm = L.copy(), L.copy()
+    Lp[t, e] += h
+    Lm[t, e] -= h
+    assert abs((f(Lp) - f(Lm)) / (2 * h) - dl[t, e]) < 1e-8
+
+
+def test_aux_loss_closed_form_and_autograd():
+    """Uniform logits give P_e = 1/E, so L = alpha * E * sum_e f_e / E = alpha whatever the counts;
+    the gradient against torch autograd with the counts held constant."""
+    T, E, k, alpha = 10, 6, 2, 0.01
+    counts = np.array([7, 0, 3, 5, 4, 1])
+    loss, grad = O.aux_loss(np.zeros((T, E)), counts, k, alpha)
+    assert abs(loss - alpha) < 1e-15
+    np.testing.assert_allclose(grad.sum(axis=1), 0, atol=1e-16)
+    rng = np.random.default_rng(4)
+    L = rng.normal(size=(T, E))
+    loss, grad = O.aux_loss(L, counts, k, alpha)
+    Lt = torch.tensor(L, requires_grad=True)
+    f = torch.tensor(counts / (T * k))
+    lt = alpha * E * (f * torch.softmax(Lt, dim=1).mean(dim=0)).sum()
+    lt.backward()
+    assert abs(lt.item() - loss) < 1e-14
+    np.testing.assert_allclose(grad, Lt.grad.numpy(), rtol=1e-10, atol=1e-16)
+
+
+def test_router_bwd_autograd():
+    """dWr and the token gradient against torch autograd of logits = x . Wr; the stored-dX sum
+    rounds once."""
+    rng = np.random.default_rng(5)
+    T, d, E = 5, 8, 4
+    x, wr, g = rng.normal(size=(T, d)), rng.normal(size=(d, E)), rng.normal(size=(T, E))
+    xt = torch.tensor(x, requires_grad=True)
+    wt = torch.tensor(wr, requires_grad=True)
+    (xt @ wt * torch.tensor(g)).sum().backward()
+    dwr, dxr = O.router_bwd(x, wr, g, rnd=None)
+    np.testing.assert_allclose(dwr, wt.grad.numpy(), rtol=1e-12)
+    np.testing.assert_allclose(dxr, xt.grad.numpy(), rtol=1e-12)
+    dx0 = O.bf16_round(rng.normal(size=(T, d)))
+    _, dxs = O.router_bwd(x, wr, g, dx=dx0)
+    np.testing.assert_array_equal(dxs, O.bf16_round(dx0 + xt.grad.numpy()))

@@ -23,6 +23,12 @@ PINS = [
     P.test_layer_single_expert_is_dense_ffn,
     lambda: P.test_layer_backward_vs_autograd(12),
     P.test_layer_backward_finite_differences,
+    P.test_router_logits_one_hot_and_integers,
+    lambda: P.test_route_topk_bwd_autograd(True),
+    lambda: P.test_route_topk_bwd_autograd(False),
+    P.test_route_topk_bwd_properties_and_fd,
+    P.test_aux_loss_closed_form_and_autograd,
+    P.test_router_bwd_autograd,
 ]
 
 
@@ -100,7 +106,47 @@ def _combine_weighted_add(y_perm, topk_w, row_of_slot, k, add=None, rnd=O.bf16_r
     return O._r(rnd, out)
 
 
+def _logits_no_bias(x, wr, bias=None):                                   # bias dropped
+    return np.asarray(x, dtype=np.float64) @ np.asarray(wr, dtype=np.float64)
+
+
+def _topk_bwd_no_mean(logits, topk_idx, d_topk_w, normalize=True):       # dropped subtraction
+    L = np.asarray(logits, dtype=np.float64)
+    idx = np.asarray(topk_idx)
+    sel = np.take_along_axis(L, idx, axis=1)
+    ex = np.exp(sel - sel.max(axis=1, keepdims=True))
+    p = np.zeros(L.shape)
+    np.put_along_axis(p, idx, ex / ex.sum(axis=1, keepdims=True), axis=1)
+    G = np.zeros(L.shape)
+    np.put_along_axis(G, idx, np.asarray(d_topk_w, dtype=np.float64), axis=1)
+    return p * G
+
+
+def _topk_bwd_full_softmax(logits, topk_idx, d_topk_w, normalize=True):  # wrong probabilities
+    return O.__dict__["_orig_tkb"](logits, topk_idx, d_topk_w, False)
+
+
+def _aux_no_E(logits, counts, k, alpha):                                   # missing factor E
+    loss, grad = O.__dict__["_orig_aux"](logits, counts, k, alpha)
+    E = np.asarray(logits).shape[1]
+    return loss / E, grad / E
+
+
+def _router_bwd_misaligned(x, wr, dlogits, dx=None, rnd=O.bf16_round):     # token rows misaligned
+    x = np.asarray(x, dtype=np.float64)
+    g = np.asarray(dlogits, dtype=np.float64)
+    share = g @ np.asarray(wr, dtype=np.float64).T
+    if dx is not None:
+        share = np.asarray(dx, dtype=np.float64) + share
+    return x.T @ np.roll(g, 1, axis=0), O._r(rnd, share)
+
+
 MUTANTS = {
+    "router logits drop the bias": ("router_logits", _logits_no_bias),
+    "route_topk_bwd drops the weighted mean": ("route_topk_bwd", _topk_bwd_no_mean),
+    "route_topk_bwd uses the full softmax": ("route_topk_bwd", _topk_bwd_full_softmax),
+    "aux loss without the factor E": ("aux_loss", _aux_no_E),
+    "router_bwd pairs x and dlogits of different tokens": ("router_bwd", _router_bwd_misaligned),
     "grouped_gemm wrong expert": ("grouped_gemm", _gg),
     "dw ragged bound off by one": ("grouped_gemm_dw", _dw_drop_last),
     "dx second pair uses first weights": ("grouped_gemm_dx", _dx_b_twice),
@@ -121,6 +167,8 @@ def test_planted_mistake_is_caught(name, monkeypatch):
     monkeypatch.setitem(O.__dict__, "_orig_cb", O.combine_bwd)
     monkeypatch.setitem(O.__dict__, "_orig_perm", O.permute)
     monkeypatch.setitem(O.__dict__, "_orig_comb", O.combine)
+    monkeypatch.setitem(O.__dict__, "_orig_tkb", O.route_topk_bwd)
+    monkeypatch.setitem(O.__dict__, "_orig_aux", O.aux_loss)
     monkeypatch.setattr(O, attr, fn)
     if attr == "bf16_round":
         # default arguments captured the original function; patch the module-level users too
