@@ -25,6 +25,7 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+PEAK_FP32_VALU_TFLOPS = 157.3   # MI355X fp32 vector
 METRIC = "MoE layer fwd+bwd tokens/sec + grouped-GEMM TFLOP/s (% of bf16 MFMA peak), 1 GPU"
 
 # HBM bytes per launch of each grouped GEMM on the Mixtral-shaped layer, from rocprofv3 FETCH_SIZE /
@@ -66,6 +67,10 @@ def _args():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=1)
+    ap.add_argument("--router", action="store_true",
+                    help="also run the router on the GPU (logits, load-balancing loss, router backward); "
+                         "the default step starts from given logits")
+    ap.add_argument("--aux-alpha", type=float, default=0.01, help="load-balancing loss weight with --router")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tokens", type=int, default=0)
@@ -115,9 +120,9 @@ def cpu_baseline(cfg, inp, sample_tokens):
                       f"all {cfg.E} experts, {dt:.1f} s"}
 
 
-def workload_name(i, cfg):
+def workload_name(i, cfg, router=False):
     if not cfg.dw_only:
-        return f"config {i}: {cfg.name} MoE FFN layer fwd+bwd"
+        return f"config {i}: {cfg.name} MoE FFN layer fwd+bwd" + (" incl. router" if router else "")
     what = "dW1 (gate/up weight gradient) grouped GEMM" if cfg.dw1_only else "dW grouped GEMMs"
     extra = []
     if cfg.dirmult_alpha:
@@ -149,7 +154,7 @@ def main():
         lay = L.DWOnly(cfg, inp)
     else:
         inp = W.make_inputs(cfg, a.seed, dev)
-        lay = L.MoELayer(cfg, inp)
+        lay = L.MoELayer(cfg, inp, router=a.router, aux_alpha=a.aux_alpha if a.router else 0.0)
     torch.cuda.synchronize()
     t_gen = time.perf_counter() - t_gen
 
@@ -185,6 +190,9 @@ def main():
             rec["frac_peak"] = round(amount / avg / 1e9 / PEAK_BF16_TFLOPS, 4)
             gemm_ms += avg
             gemm_flops += amount
+        elif kind == "valu":
+            rec["tflops_fp32"] = round(amount / avg / 1e9, 1)
+            rec["frac_peak"] = round(amount / avg / 1e9 / PEAK_FP32_VALU_TFLOPS, 4)
         else:
             rec["gbs"] = round(amount / avg / 1e6, 1)
             rec["frac_peak"] = round(amount / avg / 1e6 / PEAK_HBM_GBS, 4)
@@ -192,7 +200,7 @@ def main():
 
     roofline = None
     if per:
-        dom = max(per, key=lambda n: sum(per[n]))
+        dom = max((n for n in per if work[n][0] != "valu"), key=lambda n: sum(per[n]))
         kind, amount = work[dom]
         avg = sum(per[dom]) / len(per[dom])
         if kind == "flops":
@@ -216,7 +224,7 @@ def main():
         "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded N(0,1) activations, N(0,0.02) weights, router logits X.Wr)",
-        "config": {"workload": workload_name(a.config, cfg),
+        "config": {"workload": workload_name(a.config, cfg, a.router and not cfg.dw_only),
                    "T": cfg.T, "d": cfg.d, "f": cfg.f, "E": cfg.E, "k": cfg.k, "f_shared": cfg.f_shared,
                    "parallelism": "single GPU"},
         "gemm_tflops": round(gemm_flops / gemm_ms / 1e9, 1) if gemm_ms else None,

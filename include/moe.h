@@ -210,6 +210,59 @@ moe_status moe_grouped_gemm_dw_bf16(const moe_bf16* A, const moe_bf16* dC, const
                                     const int32_t* offsets, int32_t G, int64_t R, int64_t K,
                                     int64_t N, moe_bf16* dB, moe_bf16* dB2, hipStream_t stream);
 
+/* ------------------------------------------------------------------------------------------ */
+/* Router: logits, backward through the routing weights, load-balancing loss                   */
+/* ------------------------------------------------------------------------------------------ */
+
+/*
+ * logits[t, e] = sum_i x[t, i] * wr[i, e] (+ bias[e]) in fp32: the router ahead of the top-k
+ * selection (section 5.4 names top-k routing; the router itself is not described: one linear
+ * map, the usual MoE router).  x [T,d] bf16 (16-byte aligned); wr [d,E] fp32; bias [E] fp32 or
+ * NULL; logits [T,E] fp32.  1 <= E <= 256, d a multiple of 64.  The sum runs over eight slices
+ * of the hidden dimension added in a fixed order: deterministic, but not bitwise equal to a CPU
+ * fp32 dot product, so decisions at near-tied logits may differ from one computed elsewhere.
+ */
+moe_status moe_router_logits(const moe_bf16* x, const float* wr, const float* bias, int64_t T,
+                             int64_t d, int32_t E, float* logits, hipStream_t stream);
+
+/* Bytes of device workspace moe_router_bwd needs (partial sums of dWr over token chunks). */
+size_t moe_router_bwd_workspace_bytes(int64_t T, int64_t d, int32_t E);
+
+/*
+ * Backward of the router, given the routing of moe_route_permute and d_topk_w [T,k] from
+ * moe_unpermute_combine_bwd:
+ *   dlogits[t, e] = p[t, e] * (G[t, e] - sum_j d_topk_w[t, j] * topk_w[t, j])
+ *                   + aux_alpha * E / T * q[t, e] * (f[e] - sum_e' f[e'] * q[t, e'])
+ * where p are the probabilities the weights were read from (the k normalized weights at the
+ * selected experts and 0 elsewhere when normalize_topk, else the full softmax q of the logits),
+ * G[t, e] = d_topk_w[t, j] for e = topk_idx[t, j] (0 for unselected experts: the selection
+ * passes no gradient), and f[e] = (offsets[e+1] - offsets[e]) / (T*k) the share of slots expert e
+ * received (the Switch-style load-balancing loss alpha*E*sum_e f_e*mean_t(q_e), counts held
+ * constant; aux_alpha = 0 leaves it out and offsets may then be NULL).  Then
+ *   dwr[i, e] = sum_t x[t, i] * dlogits[t, e]                               (fp32, overwritten)
+ *   dx[t, i]  = bf16(dx[t, i] + sum_e dlogits[t, e] * wr[i, e])              (if dx != NULL)
+ * i.e. the router's share of the token gradient is added to the stored bf16 dX of the experts
+ * (one more rounding).  logits [T,E], topk_w, d_topk_w [T,k] fp32; topk_idx [T,k] int32;
+ * dlogits [T,E] fp32 (output); workspace of moe_router_bwd_workspace_bytes; deterministic.
+ */
+moe_status moe_router_bwd(const moe_bf16* x, const float* wr, const float* logits,
+                          const int32_t* topk_idx, const float* topk_w, const float* d_topk_w,
+                          const int32_t* offsets, int64_t T, int64_t d, int32_t E, int32_t k,
+                          int32_t normalize_topk, float aux_alpha, void* workspace,
+                          size_t workspace_bytes, float* dlogits, float* dwr, moe_bf16* dx,
+                          hipStream_t stream);
+
+/* Bytes of device workspace moe_router_aux_loss needs. */
+size_t moe_router_aux_loss_workspace_bytes(int64_t T, int32_t E);
+
+/*
+ * The load-balancing loss itself: loss[0] = alpha * E * sum_e f[e] * P[e], f as above and P[e]
+ * the mean over tokens of the full softmax of the logits (fp32; fixed reduction order).
+ */
+moe_status moe_router_aux_loss(const float* logits, const int32_t* offsets, int64_t T, int32_t E,
+                               int32_t k, float alpha, void* workspace, size_t workspace_bytes,
+                               float* loss, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

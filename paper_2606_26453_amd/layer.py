@@ -1,11 +1,14 @@
 """The MoE expert-FFN training layer as a fixed sequence of library calls on one stream.
 
-Forward:  route_permute -> grouped_gemm_fwd (gate/up + fused SwiGLU) -> grouped_gemm_fwd (down)
-          [-> shared FFN as one-group calls] -> unpermute_combine.
+Forward:  [router_logits ->] route_permute [-> router_aux_loss] -> grouped_gemm_fwd (gate/up +
+          fused SwiGLU) -> grouped_gemm_fwd (down) [-> shared FFN as one-group calls]
+          -> unpermute_combine.
 Backward: unpermute_combine_bwd (weighted dY permute + d_topk_w) -> grouped_gemm_dx (down)
           -> grouped_gemm_dw (down) -> swiglu_bwd -> grouped_gemm_dx (gate+up in one contraction)
           -> grouped_gemm_dw (gate+up in one pass) [-> shared FFN backward]
-          -> unpermute_combine (unweighted sum of dX_perm + shared dX).
+          -> unpermute_combine (unweighted sum of dX_perm + shared dX) [-> router_bwd: dlogits, dWr,
+          and the router's share added into dX].  The bracketed router calls run with router=True;
+          otherwise the layer starts from the given logits, as the measured hot path does.
 
 All buffers are allocated once (torch owns device memory); a step only enqueues kernels, with no
 host synchronization.
@@ -41,9 +44,12 @@ class MoELayer(_Traced):
     (moe_grouped_gemm_dx_swiglu_bwd) instead of storing dA for a separate moe_swiglu_bwd pass;
     dA is then not materialised (buf["d_act"] / buf["d_act_sh"] stay unwritten)."""
 
-    def __init__(self, cfg, inputs: dict, normalize_topk: bool = True, fuse_swiglu_bwd: bool = True):
+    def __init__(self, cfg, inputs: dict, normalize_topk: bool = True, fuse_swiglu_bwd: bool = True,
+                 router: bool = False, aux_alpha: float = 0.0):
         self.cfg = cfg
         self.fuse = fuse_swiglu_bwd
+        self.router = router
+        self.aux_alpha = float(aux_alpha)
         self.inp = inputs
         self.normalize = normalize_topk
         dev = inputs["x"].device
@@ -60,6 +66,13 @@ class MoELayer(_Traced):
             "dw_gate": e((E, d, f), f32), "dw_up": e((E, d, f), f32), "dw_down": e((E, f, d), f32),
             "workspace": e(max(16, moe.moe_route_permute_workspace_bytes(T, E, k)), torch.uint8),
         }
+        if router:
+            b.update({
+                "logits": e((T, E), f32), "dlogits": e((T, E), f32), "dwr": e((d, E), f32),
+                "aux_loss": e(1, f32),
+                "router_ws": e(max(16, moe.lib().moe_router_bwd_workspace_bytes(T, d, E)), torch.uint8),
+                "aux_ws": e(max(16, moe.lib().moe_router_aux_loss_workspace_bytes(T, E)), torch.uint8),
+            })
         self.shared = cfg.f_shared > 0
         if self.shared:
             fs = cfg.f_shared
@@ -75,9 +88,17 @@ class MoELayer(_Traced):
     # ------------------------------------------------------------------------------------------
     def forward(self, stream=None):
         b, i, k, run = self.buf, self.inp, self.cfg.k, self._run
-        run("route_permute", moe.moe_route_permute, i["logits"], i["x"], k, self.normalize, b["topk_idx"],
+        logits = i["logits"]
+        if self.router:
+            logits = b["logits"]
+            run("router_logits", moe.moe_router_logits, i["x"], i["wr"], i.get("router_bias"), logits=logits,
+                stream=stream)
+        run("route_permute", moe.moe_route_permute, logits, i["x"], k, self.normalize, b["topk_idx"],
             b["topk_w"], b["offsets"], b["row_of_slot"], b["token_of_row"], b["x_perm"], b["workspace"],
             stream=stream)
+        if self.router and self.aux_alpha:
+            run("router_aux_loss", moe.moe_router_aux_loss, logits, b["offsets"], k, self.aux_alpha,
+                loss=b["aux_loss"], workspace=b["aux_ws"], stream=stream)
         run("fwd_gate_up", moe.moe_grouped_gemm_fwd, b["x_perm"], i["w_gate"], b["offsets"], i["w_up"],
             b["h_gate"], b["h_up"], b["act"], want_act=True, stream=stream)
         run("fwd_down", moe.moe_grouped_gemm_fwd, b["act"], i["w_down"], b["offsets"], C=b["y_perm"],
@@ -134,6 +155,10 @@ class MoELayer(_Traced):
             add = b["dx_sh"]
         run("unpermute_dx", moe.moe_unpermute_combine, b["dx_perm"], None, b["row_of_slot"], k, add=add,
             y=b["dx"], stream=stream)
+        if self.router:
+            run("router_bwd", moe.moe_router_bwd, i["x"], i["wr"], b["logits"], b["topk_idx"], b["topk_w"],
+                b["d_topk_w"], b["offsets"], self.normalize, self.aux_alpha, dx=b["dx"], workspace=b["router_ws"],
+                dlogits=b["dlogits"], dwr=b["dwr"], stream=stream)
         return b["dx"]
 
     def step(self, stream=None):
@@ -155,6 +180,9 @@ class MoELayer(_Traced):
             "swiglu_bwd": ("bytes", 5 * R * f * 2),
             "dx_gate_up": ("flops", 4 * R * d * f), "dw_gate_up": ("flops", 4 * R * d * f),
             "unpermute_dx": ("bytes", R * d * 2 + T * d * 2 + R * 4 + (T * d * 2 if self.shared else 0)),
+            # router: fp32 vector-ALU work (multiply-adds x2) of the two contractions with Wr
+            "router_logits": ("valu", 2 * T * d * E), "router_bwd": ("valu", 4 * T * d * E),
+            "router_aux_loss": ("bytes", T * E * 4),
         }
         if self.shared:
             fs = c.f_shared

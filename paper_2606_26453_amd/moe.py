@@ -44,6 +44,12 @@ _SIG = {
     "moe_grouped_gemm_dx": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P]),
     "moe_grouped_gemm_dw": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P]),
     "moe_grouped_gemm_dw_bf16": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P]),
+    "moe_router_logits": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _I32, _P, _P]),
+    "moe_router_bwd_workspace_bytes": (ctypes.c_size_t, [_I64, _I64, _I32]),
+    "moe_router_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I32, _I32, _I32, ctypes.c_float,
+                                      _P, ctypes.c_size_t, _P, _P, _P, _P]),
+    "moe_router_aux_loss_workspace_bytes": (ctypes.c_size_t, [_I64, _I32]),
+    "moe_router_aux_loss": (ctypes.c_int, [_P, _P, _I64, _I32, _I32, ctypes.c_float, _P, ctypes.c_size_t, _P, _P]),
     "moe_grouped_gemm_dx_swiglu_bwd": (ctypes.c_int, [_P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P, _P, _P]),
 }
 
@@ -288,3 +294,64 @@ def moe_grouped_gemm_dx_swiglu_bwd(dC, B, offsets, h_gate, h_up, dh_gate=None, d
            lib().moe_grouped_gemm_dx_swiglu_bwd(_ptr(dC), _ptr(B), _ptr(offsets), G, R, K, N, _ptr(h_gate),
                                                 _ptr(h_up), _ptr(dh_gate), _ptr(dh_up), _stream(stream)))
     return dh_gate, dh_up
+
+
+def moe_router_logits(x, wr, bias=None, logits=None, stream=None):
+    """logits [T, E] fp32 = x [T, d] bf16 . wr [d, E] fp32 (+ bias [E])."""
+    T, d = x.shape
+    E = wr.shape[1]
+    _need(x, torch.bfloat16, (T, d), "x")
+    _need(wr, torch.float32, (d, E), "wr")
+    _need(bias, torch.float32, (E,), "bias")
+    logits = torch.empty((T, E), dtype=torch.float32, device=x.device) if logits is None else logits
+    _need(logits, torch.float32, (T, E), "logits")
+    _check("moe_router_logits", lib().moe_router_logits(_ptr(x), _ptr(wr), _ptr(bias), T, d, E, _ptr(logits),
+                                                        _stream(stream)))
+    return logits
+
+
+def moe_router_bwd(x, wr, logits, topk_idx, topk_w, d_topk_w, offsets=None, normalize_topk=True,
+                   aux_alpha=0.0, dx=None, workspace=None, dlogits=None, dwr=None, stream=None):
+    """Router backward: returns (dlogits [T, E], dwr [d, E]); adds the router's share into dx
+    [T, d] bf16 in place when dx is given."""
+    T, d = x.shape
+    E = wr.shape[1]
+    k = topk_idx.shape[1]
+    _need(x, torch.bfloat16, (T, d), "x")
+    _need(wr, torch.float32, (d, E), "wr")
+    _need(logits, torch.float32, (T, E), "logits")
+    _need(topk_idx, torch.int32, (T, k), "topk_idx")
+    _need(topk_w, torch.float32, (T, k), "topk_w")
+    _need(d_topk_w, torch.float32, (T, k), "d_topk_w")
+    _need(offsets, torch.int32, (E + 1,), "offsets")
+    _need(dx, torch.bfloat16, (T, d), "dx")
+    dev = x.device
+    dlogits = torch.empty((T, E), dtype=torch.float32, device=dev) if dlogits is None else dlogits
+    dwr = torch.empty((d, E), dtype=torch.float32, device=dev) if dwr is None else dwr
+    _need(dlogits, torch.float32, (T, E), "dlogits")
+    _need(dwr, torch.float32, (d, E), "dwr")
+    nbytes = lib().moe_router_bwd_workspace_bytes(T, d, E)
+    if workspace is None:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    _check("moe_router_bwd",
+           lib().moe_router_bwd(_ptr(x), _ptr(wr), _ptr(logits), _ptr(topk_idx), _ptr(topk_w), _ptr(d_topk_w),
+                                _ptr(offsets), T, d, E, k, 1 if normalize_topk else 0, float(aux_alpha),
+                                _ptr(workspace), workspace.numel(), _ptr(dlogits), _ptr(dwr), _ptr(dx),
+                                _stream(stream)))
+    return dlogits, dwr
+
+
+def moe_router_aux_loss(logits, offsets, k, alpha, loss=None, workspace=None, stream=None):
+    """Load-balancing loss alpha * E * sum_e f_e * P_e as a one-element fp32 tensor."""
+    T, E = logits.shape
+    _need(logits, torch.float32, (T, E), "logits")
+    _need(offsets, torch.int32, (E + 1,), "offsets")
+    dev = logits.device
+    loss = torch.empty(1, dtype=torch.float32, device=dev) if loss is None else loss
+    nbytes = lib().moe_router_aux_loss_workspace_bytes(T, E)
+    if workspace is None:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    _check("moe_router_aux_loss",
+           lib().moe_router_aux_loss(_ptr(logits), _ptr(offsets), T, E, k, float(alpha), _ptr(workspace),
+                                     workspace.numel(), _ptr(loss), _stream(stream)))
+    return loss

@@ -98,9 +98,10 @@ def make_inputs(cfg: MoEConfig, seed: int = 0, device="cpu", expert_bias=None,
                 want_dy: bool = True) -> dict:
     """Draw one seeded input set for `cfg` on `device`.
 
-    Returns bf16 tensors x [T,d], w_gate/w_up [E,d,f], w_down [E,f,d], dy [T,d], float32 router
-    logits [T,E] (= x.float() @ wr, plus the Zipf bias / `expert_bias`), and for a shared-FFN
-    config w_gate_sh/w_up_sh [d,f_sh], w_down_sh [f_sh,d].  The logits are computed once here and
+    Returns bf16 tensors x [T,d], w_gate/w_up [E,d,f], w_down [E,f,d], dy [T,d], the float32
+    router weight wr [d,E] and logits [T,E] (= x.float() @ wr, plus the Zipf bias / `expert_bias`,
+    which is also returned as router_bias [E] when present), and for a shared-FFN config
+    w_gate_sh/w_up_sh [d,f_sh], w_down_sh [f_sh,d].  The logits are computed once here and
     handed bit-identically to the oracle and to the GPU path.
     """
     if cfg.dw_only:
@@ -122,10 +123,15 @@ def make_inputs(cfg: MoEConfig, seed: int = 0, device="cpu", expert_bias=None,
     if want_dy:
         out["dy"] = _normal((T, d), ACT_STD, gen, device)
     logits = out["x"].float() @ wr
+    bias = None
     if cfg.zipf_s:
-        logits += zipf_bias(cfg, gen, device).to(device)
+        bias = zipf_bias(cfg, gen, device).to(device)
     if expert_bias is not None:
-        logits += torch.as_tensor(expert_bias, dtype=torch.float32, device=device)
+        eb = torch.as_tensor(expert_bias, dtype=torch.float32, device=device)
+        bias = eb if bias is None else bias + eb
+    if bias is not None:
+        logits += bias
+        out["router_bias"] = bias        # [E] fp32: the per-expert logit bias (absent: none)
     out["logits"] = logits.contiguous()
     return out
 

@@ -85,6 +85,23 @@ def test_gemm_rejects():
     assert dxs(N=100) == 2 and dxs(hg=None) == 1 and dxs(hg=BAD) == 1 and dxs(R=0) == 0
 
 
+def test_router_rejects():
+    L = moe.lib()
+    assert L.moe_router_logits(FAKE, FAKE, None, 10, 100, 8, FAKE, None) == 2     # d % 64
+    assert L.moe_router_logits(FAKE, FAKE, None, 10, 128, 257, FAKE, None) == 1   # E > 256
+    assert L.moe_router_logits(FAKE, FAKE, None, 10, 128, 8, None, None) == 1
+    assert L.moe_router_logits(BAD, FAKE, None, 10, 128, 8, FAKE, None) == 1
+    assert L.moe_router_logits(FAKE, FAKE, None, 0, 128, 8, FAKE, None) == 0       # empty: no-op
+    assert L.moe_router_bwd_workspace_bytes(1000, 128, 8) == 4 * 128 * 8 * 4      # 4 token chunks
+    bwd = lambda ws=FAKE, nbytes=1 << 20, k=2, offsets=None, alpha=0.0, dx=None: L.moe_router_bwd(
+        FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, offsets, 1000, 128, 8, k, 1, alpha, ws, nbytes, FAKE, FAKE, dx, None)
+    assert bwd(ws=None) == 3 and bwd(nbytes=100) == 3                            # workspace
+    assert bwd(k=9) == 1 and bwd(alpha=0.01) == 1                                 # k > E; aux without offsets
+    assert bwd(dx=BAD) == 1
+    assert L.moe_router_aux_loss(FAKE, FAKE, 100, 8, 2, 0.01, None, 0, FAKE, None) == 3
+    assert L.moe_router_aux_loss(FAKE, None, 100, 8, 2, 0.01, FAKE, 1 << 20, FAKE, None) == 1
+
+
 def test_elementwise_rejects():
     L = moe.lib()
     assert L.moe_swiglu(FAKE, FAKE, FAKE, 10, 100, None) == 2
