@@ -225,7 +225,8 @@ moe_status moe_grouped_gemm_dw_bf16(const moe_bf16* A, const moe_bf16* dC, const
 moe_status moe_router_logits(const moe_bf16* x, const float* wr, const float* bias, int64_t T,
                              int64_t d, int32_t E, float* logits, hipStream_t stream);
 
-/* Bytes of device workspace moe_router_bwd needs (partial sums of dWr over token chunks). */
+/* Bytes of device workspace moe_router_bwd needs (partial sums of dWr over token chunks and a
+   transposed copy of Wr). */
 size_t moe_router_bwd_workspace_bytes(int64_t T, int64_t d, int32_t E);
 
 /*

@@ -99,51 +99,96 @@ __global__ __launch_bounds__(64 * RL_WAVES) void router_logits_kernel(
   }
 }
 
-// dlogits of one token: the routing weights' backward (with p the probabilities the weights were
+constexpr int RD_TPW = 4;       // dlogits: tokens per wavefront
+constexpr int RA_TPW = 16;      // load-balancing loss: tokens per wavefront
+constexpr int RD_EPL = 4;       // experts per lane (E <= 64 * RD_EPL = 256)
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// Full softmax of one token's logits across the wavefront: lane l holds experts l, l+64, ...
+// (q = 0 past E).
+__device__ __forceinline__ void wave_softmax(const float* __restrict__ L, int E, int lane, float* q) {
+  float v[RD_EPL];
+  float m = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < RD_EPL; ++j) {
+    const int e = lane + 64 * j;
+    v[j] = e < E ? L[e] : -INFINITY;
+    m = fmaxf(m, v[j]);
+  }
+  m = wave_max(m);
+  float z = 0.0f;
+#pragma unroll
+  for (int j = 0; j < RD_EPL; ++j) {
+    q[j] = lane + 64 * j < E ? expf(v[j] - m) : 0.0f;
+    z += q[j];
+  }
+  z = wave_sum(z);
+#pragma unroll
+  for (int j = 0; j < RD_EPL; ++j) q[j] = q[j] / z;
+}
+
+// dlogits of a token: the routing weights' backward (with p the probabilities the weights were
 // read from: the k weights themselves when normalized, the full softmax otherwise), plus the
 // load-balancing loss's gradient when alpha != 0:
 //   dl[e] = p[e] * (G[e] - sum_j g_j w_j)  +  alpha*E/T * q[e] * (f[e] - sum_e' f[e'] q[e'])
 // with G[e] = g_j if e = topk_idx[j] (else 0), q the full softmax, f[e] = counts[e] / (T*k).
+// One wavefront per RD_TPW tokens, lane l owning experts l, l+64, ... (coalesced rows; the
+// softmax reductions are wavefront reductions).
 __global__ __launch_bounds__(256) void router_dlogits_kernel(
     const float* __restrict__ logits, const int32_t* __restrict__ topk_idx,
     const float* __restrict__ topk_w, const float* __restrict__ d_topk_w,
     const int32_t* __restrict__ offsets, int64_t T, int E, int k, int normalize, float alpha,
     float* __restrict__ dlogits) {
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= T) return;
-  const float* L = logits + t * E;
-  float* out = dlogits + t * E;
+  const int lane = threadIdx.x & 63;
+  const int64_t wv = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const bool full = !normalize || alpha != 0.0f;
-  float m = 0.0f, z = 1.0f;
-  if (full) {
-    m = L[0];
-    for (int e = 1; e < E; ++e) m = fmaxf(m, L[e]);
-    z = 0.0f;
-    for (int e = 0; e < E; ++e) z += expf(L[e] - m);
-  }
-  float gw = 0.0f;                     // sum_j g_j w_j
-  for (int j = 0; j < k; ++j) gw += d_topk_w[t * k + j] * topk_w[t * k + j];
-  float fq = 0.0f;                     // sum_e f_e q_e
   const float inv_slots = 1.0f / (float)(T * k);
-  if (alpha != 0.0f)
-    for (int e = 0; e < E; ++e) fq += (float)(offsets[e + 1] - offsets[e]) * inv_slots * (expf(L[e] - m) / z);
   const float aux = alpha * (float)E / (float)T;
-  for (int e = 0; e < E; ++e) {
-    float v = 0.0f;
-    if (!normalize) v = -(expf(L[e] - m) / z) * gw;   // the unselected part of p_e (G_e - gw)
-    if (alpha != 0.0f) {
-      const float q = expf(L[e] - m) / z;
-      v += aux * q * ((float)(offsets[e + 1] - offsets[e]) * inv_slots - fq);
-    }
-    out[e] = v;
+  float f[RD_EPL];
+#pragma unroll
+  for (int j = 0; j < RD_EPL; ++j) {
+    const int e = lane + 64 * j;
+    f[j] = (alpha != 0.0f && e < E) ? (float)(offsets[e + 1] - offsets[e]) * inv_slots : 0.0f;
   }
-  // selected experts: p_e * G_e (and, normalized, the -p_e * gw term that lives only there)
-  for (int j = 0; j < k; ++j) {
-    const int e = topk_idx[t * k + j];
-    if ((unsigned)e >= (unsigned)E) continue;   // not a routing of E experts: nothing to add
-    const float g = d_topk_w[t * k + j];
-    if (normalize) out[e] += topk_w[t * k + j] * (g - gw);
-    else out[e] += (expf(L[e] - m) / z) * g;
+  for (int64_t t = wv * RD_TPW; t < (wv + 1) * RD_TPW && t < T; ++t) {
+    const float* L = logits + t * E;
+    float q[RD_EPL] = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (full) wave_softmax(L, E, lane, q);
+    float gw = 0.0f;                       // sum_j g_j w_j (the same in every lane)
+    for (int j = 0; j < k; ++j) gw += d_topk_w[t * k + j] * topk_w[t * k + j];
+    float fq = 0.0f;
+    if (alpha != 0.0f) {
+#pragma unroll
+      for (int j = 0; j < RD_EPL; ++j) fq += f[j] * q[j];
+      fq = wave_sum(fq);
+    }
+    float out[RD_EPL];
+#pragma unroll
+    for (int j = 0; j < RD_EPL; ++j) {
+      out[j] = normalize ? 0.0f : -q[j] * gw;          // the G = 0 part of p * (G - gw)
+      if (alpha != 0.0f) out[j] += aux * q[j] * (f[j] - fq);
+    }
+    // selected experts: + p_e * G_e (normalized: p_e = w_j, and the -p_e * gw term lives there)
+    for (int j = 0; j < k; ++j) {
+      const int e = topk_idx[t * k + j];
+      const float g = d_topk_w[t * k + j];
+#pragma unroll
+      for (int jj = 0; jj < RD_EPL; ++jj)
+        if (e == lane + 64 * jj) out[jj] += normalize ? topk_w[t * k + j] * (g - gw) : q[jj] * g;
+    }
+#pragma unroll
+    for (int j = 0; j < RD_EPL; ++j)
+      if (lane + 64 * j < E) dlogits[t * E + lane + 64 * j] = out[j];
   }
 }
 
@@ -169,6 +214,16 @@ struct DlBlock {
   }
 };
 
+// Wr^T [E, d] from Wr [d, E] (so that a wavefront reads a row of experts' weights for 128
+// consecutive hidden columns in one access).
+__global__ __launch_bounds__(256) void router_transpose_kernel(const float* __restrict__ wr, int64_t d, int E,
+                                                             float* __restrict__ wrt) {
+  const int64_t o = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (o >= d * E) return;
+  const int64_t e = o / d, i = o - e * d;
+  wrt[o] = wr[i * E + e];
+}
+
 // dX[t, i] = bf16(dX[t, i] + sum_e dl[t, e] * wr[i, e]) for the 2 hidden columns i, i+1 of each
 // lane (a one-wavefront workgroup covers 128 columns) and RB_TOK tokens, in blocks of RB_SUB
 // tokens whose sums stay in registers; Wr's columns stay in registers for RB_DXE experts at
@@ -176,7 +231,7 @@ struct DlBlock {
 // fetched.
 constexpr int RB_DXE = 32;
 __global__ __launch_bounds__(64) void router_dx_kernel(
-    const float* __restrict__ dl, const float* __restrict__ wr, int64_t T, int64_t d, int E,
+    const float* __restrict__ dl, const float* __restrict__ wrt, int64_t T, int64_t d, int E,
     uint16_t* __restrict__ dx) {
   __shared__ __attribute__((aligned(16))) float s_dl[RB_SUB][RB_DXE];
   const int lane = threadIdx.x;
@@ -187,12 +242,13 @@ __global__ __launch_bounds__(64) void router_dx_kernel(
   const int64_t t_end = t_beg + RB_TOK < T ? t_beg + RB_TOK : T;
   const int nch = (E + RB_DXE - 1) / RB_DXE;
   float w0[RB_DXE], w1[RB_DXE];
-  auto load_w = [&](int ec) {
+  auto load_w = [&](int ec) {                    // Wr^T rows: 64 lanes read 512 contiguous bytes
 #pragma unroll
     for (int e = 0; e < RB_DXE; ++e) {
       const bool ok = ec + e < E;
-      w0[e] = ok ? wr[ic * E + ec + e] : 0.0f;
-      w1[e] = ok ? wr[(ic + 1) * E + ec + e] : 0.0f;
+      const f32x2 v = ok ? *reinterpret_cast<const f32x2*>(wrt + (int64_t)(ec + e) * d + ic) : f32x2{0.0f, 0.0f};
+      w0[e] = v[0];
+      w1[e] = v[1];
     }
   };
   load_w(0);
@@ -311,50 +367,59 @@ __global__ __launch_bounds__(256) void router_dwr_reduce_kernel(const float* __r
   dwr[o] = s;
 }
 
-// Load-balancing loss, first stage: per block of 256 tokens, sum_t softmax(logits[t])_e.
+// Load-balancing loss, first stage: each wavefront sums the full softmax of its RA_TPW tokens per
+// expert (lane l owning experts l, l+64, ...) in token order; the workgroup's four sums are added
+// in wavefront order and stored as one row of partials.
 __global__ __launch_bounds__(256) void router_aux_partial_kernel(const float* __restrict__ logits, int64_t T,
                                                                  int E, float* __restrict__ part) {
-  __shared__ float s_p[256];
-  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  float m = 0.0f, z = 1.0f;
-  const float* L = logits + (t < T ? t : 0) * E;
-  if (t < T) {
-    m = L[0];
-    for (int e = 1; e < E; ++e) m = fmaxf(m, L[e]);
-    z = 0.0f;
-    for (int e = 0; e < E; ++e) z += expf(L[e] - m);
+  __shared__ float s_acc[4][64 * RD_EPL];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t wv = (int64_t)blockIdx.x * 4 + w;
+  float acc[RD_EPL] = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int64_t t = wv * RA_TPW; t < (wv + 1) * RA_TPW && t < T; ++t) {
+    float q[RD_EPL];
+    wave_softmax(logits + t * E, E, lane, q);
+#pragma unroll
+    for (int j = 0; j < RD_EPL; ++j) acc[j] += q[j];
   }
-  for (int e = 0; e < E; ++e) {
-    s_p[threadIdx.x] = t < T ? expf(L[e] - m) / z : 0.0f;
-    __syncthreads();
-    for (int h = 128; h > 0; h >>= 1) {
-      if ((int)threadIdx.x < h) s_p[threadIdx.x] += s_p[threadIdx.x + h];
-      __syncthreads();
-    }
-    if (threadIdx.x == 0) part[(int64_t)blockIdx.x * E + e] = s_p[0];
-    __syncthreads();
-  }
+#pragma unroll
+  for (int j = 0; j < RD_EPL; ++j) s_acc[w][lane + 64 * j] = acc[j];
+  __syncthreads();
+  for (int e = threadIdx.x; e < E; e += 256)
+    part[(int64_t)blockIdx.x * E + e] = ((s_acc[0][e] + s_acc[1][e]) + s_acc[2][e]) + s_acc[3][e];
 }
 
-// Second stage: loss = alpha * E * sum_e f_e * P_e, P_e = (sum over blocks) / T.
-__global__ __launch_bounds__(256) void router_aux_final_kernel(const float* __restrict__ part, int nblk,
+// Second stage: loss = alpha * E * sum_e f_e * P_e, P_e = (sum of the partial rows) / T.  Thread
+// (e, h) of 4 per expert sums rows h, h+4, ... (eight independent running sums, added in a fixed
+// order), then the four are added in order.
+__global__ __launch_bounds__(256) void router_aux_final_kernel(const float* __restrict__ part, int nrow,
                                                                const int32_t* __restrict__ offsets,
                                                                int64_t T, int E, int k, float alpha,
                                                                float* __restrict__ loss) {
-  __shared__ float s_v[256];
-  float v = 0.0f;
-  for (int e = threadIdx.x; e < E; e += 256) {
-    float P = 0.0f;
-    for (int b = 0; b < nblk; ++b) P += part[(int64_t)b * E + e];
-    v += (float)(offsets[e + 1] - offsets[e]) / (float)(T * k) * (P / (float)T);
-  }
-  s_v[threadIdx.x] = v;
-  __syncthreads();
-  for (int h = 128; h > 0; h >>= 1) {
-    if ((int)threadIdx.x < h) s_v[threadIdx.x] += s_v[threadIdx.x + h];
+  __shared__ float s_p[4][64];
+  __shared__ float s_v[64];
+  float total = 0.0f;
+  for (int eb = 0; eb < E; eb += 64) {
+    const int e = eb + (threadIdx.x & 63), h = threadIdx.x >> 6;
+    float r[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (e < E)
+      for (int b = h; b < nrow; b += 32) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (b + 4 * u < nrow) r[u] += part[(int64_t)(b + 4 * u) * E + e];
+      }
+    s_p[h][threadIdx.x & 63] = ((r[0] + r[1]) + (r[2] + r[3])) + ((r[4] + r[5]) + (r[6] + r[7]));
+    __syncthreads();
+    if (threadIdx.x < 64) {
+      const float P = (((s_p[0][threadIdx.x] + s_p[1][threadIdx.x]) + s_p[2][threadIdx.x]) + s_p[3][threadIdx.x]) / (float)T;
+      s_v[threadIdx.x] = e < E ? (float)(offsets[e + 1] - offsets[e]) / (float)(T * k) * P : 0.0f;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0)
+      for (int j = 0; j < 64; ++j) total += s_v[j];
     __syncthreads();
   }
-  if (threadIdx.x == 0) loss[0] = alpha * (float)E * s_v[0];
+  if (threadIdx.x == 0) loss[0] = alpha * (float)E * total;
 }
 
 int64_t dwr_chunks(int64_t T) {
@@ -384,7 +449,7 @@ extern "C" moe_status moe_router_logits(const moe_bf16* x, const float* wr, cons
 
 extern "C" size_t moe_router_bwd_workspace_bytes(int64_t T, int64_t d, int32_t E) {
   if (T <= 0 || d <= 0 || E <= 0) return 0;
-  return (size_t)(dwr_chunks(T) * d * E * (int64_t)sizeof(float));
+  return (size_t)((dwr_chunks(T) + 1) * d * E * (int64_t)sizeof(float));   // dWr partials, then Wr^T
 }
 
 extern "C" moe_status moe_router_bwd(const moe_bf16* x, const float* wr, const float* logits,
@@ -405,7 +470,8 @@ extern "C" moe_status moe_router_bwd(const moe_bf16* x, const float* wr, const f
   const size_t need = moe_router_bwd_workspace_bytes(T, d, E);
   if (!workspace || workspace_bytes < need)
     return fail(MOE_ERROR_WORKSPACE, "%s: workspace of %zu bytes needed", fn, need);
-  router_dlogits_kernel<<<(unsigned)((T + 255) / 256), 256, 0, stream>>>(
+  const int64_t waves = (T + RD_TPW - 1) / RD_TPW;
+  router_dlogits_kernel<<<(unsigned)((waves + 3) / 4), 256, 0, stream>>>(
       logits, topk_idx, topk_w, d_topk_w, offsets, T, E, k, normalize_topk, aux_alpha, dlogits);
   moe_status st = check_launch("router_dlogits");
   if (st != MOE_SUCCESS) return st;
@@ -419,8 +485,11 @@ extern "C" moe_status moe_router_bwd(const moe_bf16* x, const float* wr, const f
   router_dwr_reduce_kernel<<<(unsigned)((n + 255) / 256), 256, 0, stream>>>(part, (int)chunks, n, dwr);
   if ((st = check_launch("router_dwr_reduce")) != MOE_SUCCESS) return st;
   if (dx) {
+    float* wrt = part + chunks * n;
+    router_transpose_kernel<<<(unsigned)((n + 255) / 256), 256, 0, stream>>>(wr, d, E, wrt);
+    if ((st = check_launch("router_transpose")) != MOE_SUCCESS) return st;
     router_dx_kernel<<<dim3((unsigned)((d + 127) / 128), (unsigned)((T + RB_TOK - 1) / RB_TOK)), 64, 0, stream>>>(
-        dlogits, wr, T, d, E, dx);
+        dlogits, wrt, T, d, E, dx);
     if ((st = check_launch("router_dx")) != MOE_SUCCESS) return st;
   }
   return MOE_SUCCESS;
@@ -428,7 +497,8 @@ extern "C" moe_status moe_router_bwd(const moe_bf16* x, const float* wr, const f
 
 extern "C" size_t moe_router_aux_loss_workspace_bytes(int64_t T, int32_t E) {
   if (T <= 0 || E <= 0) return 0;
-  return (size_t)((T + 255) / 256) * (size_t)E * sizeof(float);
+  const int64_t waves = (T + RA_TPW - 1) / RA_TPW;
+  return (size_t)((waves + 3) / 4) * (size_t)E * sizeof(float);
 }
 
 extern "C" moe_status moe_router_aux_loss(const float* logits, const int32_t* offsets, int64_t T, int32_t E,
@@ -440,8 +510,9 @@ extern "C" moe_status moe_router_aux_loss(const float* logits, const int32_t* of
   const size_t need = moe_router_aux_loss_workspace_bytes(T, E);
   if (!workspace || workspace_bytes < need)
     return fail(MOE_ERROR_WORKSPACE, "%s: workspace of %zu bytes needed", fn, need);
-  const int64_t nblk = (T + 255) / 256;
-  if (nblk > ((int64_t)1 << 31) - 1) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: T too large", fn);
+  const int64_t waves = (T + RA_TPW - 1) / RA_TPW;
+  const int64_t nblk = (waves + 3) / 4;
+  if (nblk > ((int64_t)1 << 30)) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: T too large", fn);
   float* part = static_cast<float*>(workspace);
   router_aux_partial_kernel<<<(unsigned)nblk, 256, 0, stream>>>(logits, T, E, part);
   moe_status st = check_launch("router_aux_partial");

@@ -92,7 +92,7 @@ def test_router_rejects():
     assert L.moe_router_logits(FAKE, FAKE, None, 10, 128, 8, None, None) == 1
     assert L.moe_router_logits(BAD, FAKE, None, 10, 128, 8, FAKE, None) == 1
     assert L.moe_router_logits(FAKE, FAKE, None, 0, 128, 8, FAKE, None) == 0       # empty: no-op
-    assert L.moe_router_bwd_workspace_bytes(1000, 128, 8) == 4 * 128 * 8 * 4      # 4 token chunks
+    assert L.moe_router_bwd_workspace_bytes(1000, 128, 8) == (4 + 1) * 128 * 8 * 4   # 4 token chunks + Wr^T
     bwd = lambda ws=FAKE, nbytes=1 << 20, k=2, offsets=None, alpha=0.0, dx=None: L.moe_router_bwd(
         FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, offsets, 1000, 128, 8, k, 1, alpha, ws, nbytes, FAKE, FAKE, dx, None)
     assert bwd(ws=None) == 3 and bwd(nbytes=100) == 3                            # workspace
