@@ -71,6 +71,8 @@ def _args():
                     help="also run the router on the GPU (logits, load-balancing loss, router backward); "
                          "the default step starts from given logits")
     ap.add_argument("--aux-alpha", type=float, default=0.01, help="load-balancing loss weight with --router")
+    ap.add_argument("--dw-transposed", action="store_true",
+                    help="weight gradients from contraction-major copies of their operands")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tokens", type=int, default=0)
@@ -154,7 +156,8 @@ def main():
         lay = L.DWOnly(cfg, inp)
     else:
         inp = W.make_inputs(cfg, a.seed, dev)
-        lay = L.MoELayer(cfg, inp, router=a.router, aux_alpha=a.aux_alpha if a.router else 0.0)
+        lay = L.MoELayer(cfg, inp, router=a.router, aux_alpha=a.aux_alpha if a.router else 0.0,
+                         dw_transposed=a.dw_transposed)
     torch.cuda.synchronize()
     t_gen = time.perf_counter() - t_gen
 

@@ -210,6 +210,35 @@ moe_status moe_grouped_gemm_dw_bf16(const moe_bf16* A, const moe_bf16* dC, const
                                     const int32_t* offsets, int32_t G, int64_t R, int64_t K,
                                     int64_t N, moe_bf16* dB, moe_bf16* dB2, hipStream_t stream);
 
+/*
+ * The weight gradient of moe_grouped_gemm_dw from contraction-major copies of its operands
+ * (the layout moe_transpose_grouped writes): At [K, ld] and dCt, dC2t [N, ld] bf16, in which
+ * group g's rows occupy columns pstart[g] .. pstart[g] + K_g - 1, pstart[g] = sum over h < g of
+ * K_h rounded up to a multiple of 32, and the padding columns hold zeros.  Same definition,
+ * outputs, empty-group zeros, ordering and errors as moe_grouped_gemm_dw (out_bf16 = 0: fp32
+ * dB, dB2 [G,K,N]; 1: bf16, as moe_grouped_gemm_dw_bf16); the contraction of every group is
+ * contiguous, so both operands are read without transposition, and the results are bitwise
+ * identical to moe_grouped_gemm_dw's.  ld: a multiple of 64, at least
+ * moe_transposed_cols_bound(R, G); max(K, N) * ld * 2 < 2^31.
+ */
+moe_status moe_grouped_gemm_dw_t(const moe_bf16* At, const moe_bf16* dCt, const moe_bf16* dC2t,
+                                 const int32_t* offsets, int32_t G, int64_t R, int64_t K, int64_t N,
+                                 int64_t ld, void* dB, void* dB2, int32_t out_bf16,
+                                 hipStream_t stream);
+
+/* Columns the contraction-major layout needs at most: round32(R) + 32 * G. */
+int64_t moe_transposed_cols_bound(int64_t R, int32_t G);
+
+/*
+ * dst[c, pstart[g] + i] = src[offsets[g] + i, c] for 0 <= i < K_g, zeros in each group's padding
+ * up to the next multiple of 32 (and up to the end of the last 64-column block): the
+ * contraction-major copy that moe_grouped_gemm_dw_t reads.  src [R, C] bf16 row-major (the rows
+ * of the routed buffer, grouped by offsets); dst [C, ld_dst] bf16; C a multiple of 64; ld_dst a
+ * multiple of 64 and >= moe_transposed_cols_bound(R, G).
+ */
+moe_status moe_transpose_grouped(const moe_bf16* src, const int32_t* offsets, int32_t G, int64_t R,
+                                 int64_t C, moe_bf16* dst, int64_t ld_dst, hipStream_t stream);
+
 /* ------------------------------------------------------------------------------------------ */
 /* Router: logits, backward through the routing weights, load-balancing loss                   */
 /* ------------------------------------------------------------------------------------------ */

@@ -42,7 +42,11 @@ constexpr int BK = 32;       // contraction elements per pipeline stage
 __device__ __forceinline__ int swz_d(int r) { return (r >> 2) & 3; }
 __device__ __forceinline__ int swz_t(int k) { return (k & 3) << 1; }
 
-enum { KIND_FWD = 0, KIND_DX = 1, KIND_DW = 2 };
+// FWD: C = A.B per group; DX: dA = dC.B^T per group; DW: dB[g] = A_g^T.dC_g from row-major
+// operands (contraction = rows, read with transposing LDS reads); DWT: the same dB[g] from
+// contraction-major copies A^T [K, ld], dC^T [N, ld] in which each group's rows form a contiguous
+// segment zero-padded to 32 (both operands then read directly).
+enum { KIND_FWD = 0, KIND_DX = 1, KIND_DW = 2, KIND_DWT = 3 };
 
 struct GemmParams {
   const uint16_t* a;   // M side: FWD A [R,K]; DX dC [R,N]; DW A [R,K]
@@ -60,6 +64,7 @@ struct GemmParams {
   int mt_bound;        // FWD/DX: upper bound on the number of row tiles
   int m_tiles;         // DW: tiles over K
   int n_tiles;         // tiles over the output columns
+  int64_t ld_t;        // DWT: row length of the contraction-major operands
 };
 
 typedef int i32x4 __attribute__((ext_vector_type(4)));
@@ -151,7 +156,9 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
   constexpr int MB = WTM / 32;                // 32x32 MFMA blocks per wave along rows
   constexpr int NB = WTN / 32;                // ... and along columns
   constexpr bool M_T = (KIND == KIND_DW);     // M-side operand stored contraction-major
-  constexpr bool N_T = (KIND != KIND_DX);     // N-side operand stored contraction-major
+  constexpr bool N_T = (KIND == KIND_FWD || KIND == KIND_DW);   // N side stored contraction-major
+  constexpr bool IS_DW = (KIND == KIND_DW || KIND == KIND_DWT); // weight gradient: groups own the
+                                                                // contraction, outputs are dB[g]
 
   __shared__ __attribute__((aligned(16))) char lds[NSTAGE * STAGE];
   __shared__ int s_scan[256];
@@ -168,9 +175,22 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
   // offsets, the tile prefix over groups (fwd/dX) and the group order (dW) are built once per
   // workgroup in LDS.
   __shared__ int s_off[257];
+  __shared__ int s_pp[257];   // DWT: padded segment starts (exclusive prefix of ceil32(rows_g))
   for (int i = tid; i <= p.G; i += 64 * NWAVE) s_off[i] = p.offsets[i];   // G + 1 may exceed the threads
   int ntiles_all, mtotal = 0;
-  if constexpr (KIND == KIND_DW) {
+  if constexpr (KIND == KIND_DWT) {
+    __syncthreads();
+    if (tid < 256) s_pp[tid + 1] = tid < p.G ? ((s_off[tid + 1] - s_off[tid] + 31) & ~31) : 0;
+    if (tid == 0) s_pp[0] = 0;
+    __syncthreads();
+    for (int off = 1; off < 256; off <<= 1) {
+      const int add = (tid < 256 && tid >= off) ? s_pp[tid + 1 - off] : 0;
+      __syncthreads();
+      if (tid < 256) s_pp[tid + 1] += add;
+      __syncthreads();
+    }
+  }
+  if constexpr (IS_DW) {
     // Largest groups first (their tiles run longest).
     int kg = 0;
     if (tid < p.G) kg = p.offsets[tid + 1] - p.offsets[tid];
@@ -203,7 +223,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
   // dispatch index -> (group, row tile, column tile, row range).  FWD/DX: output rows of the
   // tile; DW: the group's contraction rows.  Uniform over the workgroup (FWD/DX use a barrier).
   auto map_tile = [&](int it, int& g, int& mt, int& nt, int& row_lo, int& row_hi) {
-    if constexpr (KIND == KIND_DW) {
+    if constexpr (IS_DW) {
       // When a group's tile count divides by 8, each XCD takes one contiguous eighth of every
       // group (in band order), so the long tiles of a hot group spread over all XCDs while each
       // XCD's L2 still sees neighbouring tiles.
@@ -219,8 +239,13 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
       }
       g = s_scan[slot];
       band_order(within, p.m_tiles, p.n_tiles, mt, nt);
-      row_lo = s_off[g];
-      row_hi = s_off[g + 1];
+      if constexpr (KIND == KIND_DWT) {   // the group's padded segment of the contraction-major copies
+        row_lo = s_pp[g];
+        row_hi = s_pp[g + 1];
+      } else {
+        row_lo = s_off[g];
+        row_hi = s_off[g + 1];
+      }
     } else {
       int mt_glob;
       band_order(xcd_remap(it, ntiles_all), mtotal, p.n_tiles, mt_glob, nt);
@@ -262,7 +287,20 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
     int lane = threadIdx.x & 63;
     if constexpr (PERSIST) asm volatile("" : "+v"(lane));
     // M side
-    if constexpr (!M_T) {
+    if constexpr (KIND == KIND_DWT) {
+      // A^T [K, ld_t]: tile rows = dB rows mt*TM .. (clamped to K), contraction = the group's
+      // padded segment starting at column row_lo
+      m_ld = p.ld_t;
+      const int64_t rows_valid = p.K - (int64_t)mt * TM;   // > 0
+      m_src = reinterpret_cast<const char*>(p.a + (int64_t)mt * TM * m_ld + row_lo);
+#pragma unroll
+      for (int i = 0; i < DPW_M; ++i) {
+        int64_t r = 16 * (DPW_M * wave + i) + (lane >> 2);
+        if (r > rows_valid - 1) r = rows_valid - 1;
+        const int c = (lane & 3) ^ swz_d(lane >> 2);
+        m_voff[i] = (int)((r * m_ld + 8 * c) * 2);
+      }
+    } else if constexpr (!M_T) {
       m_ld = (KIND == KIND_FWD) ? p.K : p.N;
       const int64_t rows_valid = row_hi - row_lo;   // > 0
       m_src = reinterpret_cast<const char*>(p.a + row_lo * m_ld);
@@ -288,7 +326,27 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
       }
     }
     // N side
-    if constexpr (!N_T) {
+    if constexpr (KIND == KIND_DWT) {
+      // dC^T [N, ld_t]: tile row r is output column nt*TN + r, or in dual mode column
+      // nt*TN/2 + 64*(r/128) + r%64 of dC^T (r%128 < 64) or of dC2^T (r%128 >= 64), so that each
+      // wave's accumulator halves hold the two outputs at the same columns; this wave's 16*DPW_N
+      // rows lie in one 64-row half (one source)
+      n_ld = p.ld_t;
+      const int r0w = 16 * DPW_N * wave;
+      const uint16_t* src = p.b;
+      if constexpr (DUAL) {
+        if ((r0w & 127) >= 64) src = p.b2;
+      }
+      n_src = reinterpret_cast<const char*>(src + row_lo);
+#pragma unroll
+      for (int i = 0; i < DPW_N; ++i) {
+        const int r = 16 * (DPW_N * wave + i) + (lane >> 2);
+        int64_t col = DUAL ? (int64_t)nt * (TN / 2) + 64 * (r >> 7) + (r & 63) : (int64_t)nt * TN + r;
+        if (col > p.N - 1) col = p.N - 1;
+        const int c = (lane & 3) ^ swz_d(lane >> 2);
+        n_voff[i] = (int)((col * n_ld + 8 * c) * 2);
+      }
+    } else if constexpr (!N_T) {
       // DX: B[g][kk, c]; the tile's output columns kk = nt*TN + row, clamped
       n_ld = p.N;
       n_src = reinterpret_cast<const char*>(p.b + (int64_t)g * p.K * p.N);
@@ -353,7 +411,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
     if constexpr (!N_T) {
       const char* base = n_src;
       int64_t cc = c0;
-      if constexpr (DUAL) {
+      if constexpr (DUAL && KIND == KIND_DX) {
         if (c0 >= p.N) { base = n_src2; cc = c0 - p.N; }
       }
       return make_rsrc(base + cc * 2, (int64_t)0x7fffffff);
@@ -545,7 +603,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
   if constexpr (PERSIST) asm volatile("" : "+v"(tid));
   const int lane = tid & 63, l32 = lane & 31, fh = lane >> 5;
   const int col_in = 4 * fh;
-  if constexpr (KIND == KIND_DW && !OUT16) {
+  if constexpr (IS_DW && !OUT16) {
 #pragma unroll
     for (int i = 0; i < MB; ++i) {
       const int mrow = wm * WTM + 32 * i + l32;
@@ -586,7 +644,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
     // output rows of the tile: fwd/dX the permuted rows row_lo .. row_hi-1; dW rows mt*TM .. of
     // dB[g] (at most K)
     int64_t obase = 0;
-    if constexpr (KIND == KIND_DW) {
+    if constexpr (IS_DW) {
       obase = (int64_t)g * p.K * p.N;
       row_lo = (int64_t)mt * TM;
       row_hi = p.K;
@@ -707,7 +765,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
     const int next = it + (int)gridDim.x;
     const bool more = next < ntiles_all;   // uniform
     int g2 = 0, mt2 = 0, nt2 = 0, lo2 = 0, hi2 = 0;
-    if constexpr (KIND == KIND_DW && !OUT16) {
+    if constexpr (IS_DW && !OUT16) {
       // fp32 results leave from registers: once every wave is done with the ring, start filling
       // it with the next tile's first stages, then store this tile
       __syncthreads();
@@ -744,7 +802,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
 // group sizes: the hardware dispatcher then balances them dynamically, where a static walk of the
 // largest-first order measured 7% slower on the Zipf-skewed layer.
 template <int KIND> struct Cfg {
-  static constexpr bool PP = (KIND == KIND_DX);
+  static constexpr bool PP = (KIND == KIND_DX || KIND == KIND_DWT);   // both operands read directly
   static constexpr int TM = 256;
   static constexpr int WM = PP ? 4 : 2, WN = 2;
   static constexpr int NS = 4;
@@ -893,6 +951,41 @@ moe_status grouped_gemm_dw_impl(const char* fn, bool out16, const moe_bf16* A, c
 }
 }  // namespace
 }  // namespace moe
+
+extern "C" moe_status moe_grouped_gemm_dw_t(const moe_bf16* At, const moe_bf16* dCt, const moe_bf16* dC2t,
+                                            const int32_t* offsets, int32_t G, int64_t R, int64_t K, int64_t N,
+                                            int64_t ld, void* dB, void* dB2, int32_t out_bf16,
+                                            hipStream_t stream) {
+  const char* fn = "moe_grouped_gemm_dw_t";
+  if (G < 1 || G > 256) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: need 1 <= G <= 256", fn);
+  if (R < 0 || K <= 0 || N <= 0) return fail(MOE_ERROR_INVALID_VALUE, "%s: bad size", fn);
+  if (K % 64 || N % 64) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: K and N must be multiples of 64", fn);
+  if (R >= ((int64_t)1 << 31)) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: R >= 2^31", fn);
+  const int64_t bound = ((R + 31) & ~(int64_t)31) + 32 * (int64_t)G;
+  if (ld < bound || ld % 64)
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: ld must be a multiple of 64 and >= %lld", fn, (long long)bound);
+  if ((K > N ? K : N) * ld * 2 >= ((int64_t)1 << 31))
+    return fail(MOE_ERROR_NOT_SUPPORTED, "%s: operands of 2 GiB or more", fn);
+  if (!offsets) return fail(MOE_ERROR_INVALID_VALUE, "%s: offsets is NULL", fn);
+  if ((dC2t == nullptr) != (dB2 == nullptr))
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: dC2t and dB2 must both be set or both NULL", fn);
+  if (!dB || !At || !dCt) return fail(MOE_ERROR_INVALID_VALUE, "%s: NULL pointer", fn);
+  if (bad_ptr(At) || bad_ptr(dCt) || bad_ptr(dC2t) || bad_ptr(dB) || bad_ptr(dB2))
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: pointers must be 16-byte aligned", fn);
+  GemmParams p{};
+  p.a = At; p.b = dCt; p.b2 = dC2t; p.offsets = offsets; p.out = dB; p.out2 = dB2;
+  p.G = G; p.R = R; p.K = K; p.N = N; p.ld_t = ld;
+  p.m_tiles = (int)((K + Cfg<KIND_DWT>::TM - 1) / Cfg<KIND_DWT>::TM);
+  const int cols_per_tile = dC2t ? TN / 2 : TN;
+  p.n_tiles = (int)((N + cols_per_tile - 1) / cols_per_tile);
+  const int64_t tiles = (int64_t)G * p.m_tiles * p.n_tiles;
+  if (out_bf16) {
+    if (dC2t) return launch<KIND_DWT, true, false, true>(p, tiles, stream, "grouped_gemm_dw_t_bf16(dual)");
+    return launch<KIND_DWT, false, false, true>(p, tiles, stream, "grouped_gemm_dw_t_bf16");
+  }
+  if (dC2t) return launch<KIND_DWT, true, false>(p, tiles, stream, "grouped_gemm_dw_t(dual)");
+  return launch<KIND_DWT, false, false>(p, tiles, stream, "grouped_gemm_dw_t");
+}
 
 extern "C" moe_status moe_grouped_gemm_dw(const moe_bf16* A, const moe_bf16* dC, const moe_bf16* dC2,
                                           const int32_t* offsets, int32_t G, int64_t R, int64_t K,

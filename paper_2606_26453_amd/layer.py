@@ -45,9 +45,10 @@ class MoELayer(_Traced):
     dA is then not materialised (buf["d_act"] / buf["d_act_sh"] stay unwritten)."""
 
     def __init__(self, cfg, inputs: dict, normalize_topk: bool = True, fuse_swiglu_bwd: bool = True,
-                 router: bool = False, aux_alpha: float = 0.0):
+                 router: bool = False, aux_alpha: float = 0.0, dw_transposed: bool = False):
         self.cfg = cfg
         self.fuse = fuse_swiglu_bwd
+        self.dw_t = dw_transposed
         self.router = router
         self.aux_alpha = float(aux_alpha)
         self.inp = inputs
@@ -66,6 +67,11 @@ class MoELayer(_Traced):
             "dw_gate": e((E, d, f), f32), "dw_up": e((E, d, f), f32), "dw_down": e((E, f, d), f32),
             "workspace": e(max(16, moe.moe_route_permute_workspace_bytes(T, E, k)), torch.uint8),
         }
+        if dw_transposed:
+            # contraction-major copies of the dW operands (moe_transpose_grouped layout)
+            ld = moe.transposed_cols(R, E)
+            b.update({"x_perm_t": e((d, ld)), "dy_perm_t": e((d, ld)), "act_t": e((f, ld)),
+                      "dh_gate_t": e((f, ld)), "dh_up_t": e((f, ld))})
         if router:
             b.update({
                 "logits": e((T, E), f32), "dlogits": e((T, E), f32), "dwr": e((d, E), f32),
@@ -125,15 +131,29 @@ class MoELayer(_Traced):
         else:
             run("dx_down", moe.moe_grouped_gemm_dx, b["dy_perm"], i["w_down"], b["offsets"], dA=b["d_act"],
                 stream=stream)
-        run("dw_down", moe.moe_grouped_gemm_dw, b["act"], b["dy_perm"], b["offsets"], dB=b["dw_down"],
-            stream=stream)
+        if self.dw_t:
+            run("transpose_act", moe.moe_transpose_grouped, b["act"], b["offsets"], dst=b["act_t"], stream=stream)
+            run("transpose_dy_perm", moe.moe_transpose_grouped, b["dy_perm"], b["offsets"], dst=b["dy_perm_t"],
+                stream=stream)
+            run("dw_down", moe.moe_grouped_gemm_dw_t, b["act_t"], b["dy_perm_t"], b["offsets"], self.R,
+                dB=b["dw_down"], stream=stream)
+        else:
+            run("dw_down", moe.moe_grouped_gemm_dw, b["act"], b["dy_perm"], b["offsets"], dB=b["dw_down"],
+                stream=stream)
         if not self.fuse:
             run("swiglu_bwd", moe.moe_swiglu_bwd, b["h_gate"], b["h_up"], b["d_act"], b["dh_gate"],
                 b["dh_up"], stream=stream)
         run("dx_gate_up", moe.moe_grouped_gemm_dx, b["dh_gate"], i["w_gate"], b["offsets"], b["dh_up"],
             i["w_up"], dA=b["dx_perm"], stream=stream)
-        run("dw_gate_up", moe.moe_grouped_gemm_dw, b["x_perm"], b["dh_gate"], b["offsets"], b["dh_up"],
-            dB=b["dw_gate"], dB2=b["dw_up"], stream=stream)
+        if self.dw_t:
+            run("transpose_x_perm", moe.moe_transpose_grouped, b["x_perm"], b["offsets"], dst=b["x_perm_t"],
+                stream=stream)
+            run("transpose_dh", self._transpose_dh, stream=stream)
+            run("dw_gate_up", moe.moe_grouped_gemm_dw_t, b["x_perm_t"], b["dh_gate_t"], b["offsets"], self.R,
+                b["dh_up_t"], dB=b["dw_gate"], dB2=b["dw_up"], stream=stream)
+        else:
+            run("dw_gate_up", moe.moe_grouped_gemm_dw, b["x_perm"], b["dh_gate"], b["offsets"], b["dh_up"],
+                dB=b["dw_gate"], dB2=b["dw_up"], stream=stream)
         add = None
         if self.shared:
             wg, wu, wd = self.w_sh
@@ -161,6 +181,15 @@ class MoELayer(_Traced):
                 dlogits=b["dlogits"], dwr=b["dwr"], stream=stream)
         return b["dx"]
 
+    @property
+    def R(self):
+        return self.cfg.T * self.cfg.k
+
+    def _transpose_dh(self, stream=None):
+        b = self.buf
+        moe.moe_transpose_grouped(b["dh_gate"], b["offsets"], dst=b["dh_gate_t"], stream=stream)
+        moe.moe_transpose_grouped(b["dh_up"], b["offsets"], dst=b["dh_up_t"], stream=stream)
+
     def step(self, stream=None):
         self.forward(stream)
         self.backward(stream)
@@ -183,6 +212,9 @@ class MoELayer(_Traced):
             # router: fp32 vector-ALU work (multiply-adds x2) of the two contractions with Wr
             "router_logits": ("valu", 2 * T * d * E), "router_bwd": ("valu", 4 * T * d * E),
             "router_aux_loss": ("bytes", T * E * 4),
+            # contraction-major copies for the dW products (read + write)
+            "transpose_act": ("bytes", 2 * R * f * 2), "transpose_dy_perm": ("bytes", 2 * R * d * 2),
+            "transpose_x_perm": ("bytes", 2 * R * d * 2), "transpose_dh": ("bytes", 4 * R * f * 2),
         }
         if self.shared:
             fs = c.f_shared

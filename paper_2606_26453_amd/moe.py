@@ -44,6 +44,9 @@ _SIG = {
     "moe_grouped_gemm_dx": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P]),
     "moe_grouped_gemm_dw": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P]),
     "moe_grouped_gemm_dw_bf16": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P]),
+    "moe_grouped_gemm_dw_t": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _I64, _P, _P, _I32, _P]),
+    "moe_transposed_cols_bound": (ctypes.c_int64, [_I64, _I32]),
+    "moe_transpose_grouped": (ctypes.c_int, [_P, _P, _I32, _I64, _I64, _P, _I64, _P]),
     "moe_router_logits": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _I32, _P, _P]),
     "moe_router_bwd_workspace_bytes": (ctypes.c_size_t, [_I64, _I64, _I32]),
     "moe_router_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I32, _I32, _I32, ctypes.c_float,
@@ -355,3 +358,44 @@ def moe_router_aux_loss(logits, offsets, k, alpha, loss=None, workspace=None, st
            lib().moe_router_aux_loss(_ptr(logits), _ptr(offsets), T, E, k, float(alpha), _ptr(workspace),
                                      workspace.numel(), _ptr(loss), _stream(stream)))
     return loss
+
+
+def transposed_cols(R, G):
+    """Row length (a multiple of 64) of a contraction-major copy of R grouped rows in G groups."""
+    b = lib().moe_transposed_cols_bound(R, G)
+    return (b + 63) // 64 * 64
+
+
+def moe_transpose_grouped(src, offsets, dst=None, stream=None):
+    """dst [C, ld] bf16: the contraction-major, group-padded copy of src [R, C]."""
+    R, C = src.shape
+    G = offsets.numel() - 1
+    _need(src, torch.bfloat16, (R, C), "src")
+    _need(offsets, torch.int32, (G + 1,), "offsets")
+    ld = transposed_cols(R, G)
+    dst = torch.empty((C, ld), dtype=torch.bfloat16, device=src.device) if dst is None else dst
+    _need(dst, torch.bfloat16, (C, ld), "dst")
+    _check("moe_transpose_grouped", lib().moe_transpose_grouped(_ptr(src), _ptr(offsets), G, R, C, _ptr(dst), ld,
+                                                                _stream(stream)))
+    return dst
+
+
+def moe_grouped_gemm_dw_t(At, dCt, offsets, R, dC2t=None, dB=None, dB2=None, out_bf16=False, stream=None):
+    """moe_grouped_gemm_dw from contraction-major copies At [K, ld], dCt (dC2t) [N, ld]."""
+    K, ld = At.shape
+    N = dCt.shape[0]
+    G = offsets.numel() - 1
+    _need(At, torch.bfloat16, (K, ld), "At")
+    _need(dCt, torch.bfloat16, (N, ld), "dCt")
+    _need(dC2t, torch.bfloat16, (N, ld), "dC2t")
+    _need(offsets, torch.int32, (G + 1,), "offsets")
+    dt = torch.bfloat16 if out_bf16 else torch.float32
+    dB = torch.empty((G, K, N), dtype=dt, device=At.device) if dB is None else dB
+    if dC2t is not None and dB2 is None:
+        dB2 = torch.empty((G, K, N), dtype=dt, device=At.device)
+    _need(dB, dt, (G, K, N), "dB")
+    _need(dB2, dt, (G, K, N), "dB2")
+    _check("moe_grouped_gemm_dw_t",
+           lib().moe_grouped_gemm_dw_t(_ptr(At), _ptr(dCt), _ptr(dC2t), _ptr(offsets), G, R, K, N, ld, _ptr(dB),
+                                       _ptr(dB2), 1 if out_bf16 else 0, _stream(stream)))
+    return dB, dB2

@@ -85,6 +85,19 @@ def test_gemm_rejects():
     assert dxs(N=100) == 2 and dxs(hg=None) == 1 and dxs(hg=BAD) == 1 and dxs(R=0) == 0
 
 
+def test_dw_t_and_transpose_rejects():
+    L = moe.lib()
+    assert L.moe_transposed_cols_bound(100, 4) == 128 + 128
+    ld = 256
+    dwt = lambda G=4, R=100, K=128, N=128, ld=ld, dC2t=None, dB2=None: L.moe_grouped_gemm_dw_t(
+        FAKE, FAKE, dC2t, FAKE, G, R, K, N, ld, FAKE, dB2, 0, None)
+    assert dwt(ld=192) == 1 and dwt(ld=300) == 1          # below the bound / not a multiple of 64
+    assert dwt(K=100) == 2 and dwt(G=0) == 2 and dwt(dC2t=FAKE) == 1
+    assert dwt(K=1 << 20, ld=1 << 12) == 2                # operand of 2 GiB or more
+    tr = lambda C=128, ld=ld, src=FAKE: L.moe_transpose_grouped(src, FAKE, 4, 100, C, FAKE, ld, None)
+    assert tr(C=100) == 2 and tr(ld=128) == 1 and tr(src=BAD) == 1
+
+
 def test_router_rejects():
     L = moe.lib()
     assert L.moe_router_logits(FAKE, FAKE, None, 10, 100, 8, FAKE, None) == 2     # d % 64

@@ -193,10 +193,14 @@ def test_grouped_gemm_256_groups_exact():
     # dW: dB[g] = A_g^T dC_g (64 x 128 per group), empty groups exactly zero
     dCw = _int_tensor(g, (R, 128), -2, 2)
     dB = moe.moe_grouped_gemm_dw(A.to(DEV), dCw.to(DEV), offd)[0]
+    dBt = moe.moe_grouped_gemm_dw_t(moe.moe_transpose_grouped(A.to(DEV), offd),
+                                    moe.moe_transpose_grouped(dCw.to(DEV), offd), offd, R)[0]
     torch.cuda.synchronize()
-    np.testing.assert_array_equal(f64(dB), O.grouped_gemm_dw(f64(A), f64(dCw), off.numpy()))
+    refw = O.grouped_gemm_dw(f64(A), f64(dCw), off.numpy())
+    np.testing.assert_array_equal(f64(dB), refw)
+    np.testing.assert_array_equal(f64(dBt), refw)
     for e in np.flatnonzero(counts == 0):
-        assert torch.count_nonzero(dB[int(e)]) == 0
+        assert torch.count_nonzero(dB[int(e)]) == 0 and torch.count_nonzero(dBt[int(e)]) == 0
 
 
 @pytest.mark.parametrize("K,N", [(320, 192), (256, 256)])
@@ -219,6 +223,72 @@ def test_grouped_gemm_dw_bf16_exact(K, N):
     np.testing.assert_array_equal(f64(dB1), ref)
     np.testing.assert_array_equal(f64(dB2), O.bf16_round(O.grouped_gemm_dw(f64(A), f64(dC2), off.numpy())))
     assert torch.count_nonzero(dB[5]) == 0 and torch.count_nonzero(dB2[10]) == 0
+
+
+def _padded_starts(counts):
+    pad = [(c + 31) // 32 * 32 for c in counts]
+    return np.concatenate([[0], np.cumsum(pad)]).astype(np.int64)
+
+
+@pytest.mark.parametrize("C", [64, 320])
+def test_transpose_grouped_exact(C):
+    """The contraction-major copy: a bit copy of every row into its group's padded segment, zero
+    padding up to the next multiple of 32 (and to the end of the last 64-column block)."""
+    _say("transpose_grouped", C)
+    g = torch.Generator().manual_seed(C)
+    counts = GROUPS
+    G, R = len(counts), sum(counts)
+    off = torch.tensor(np.concatenate([[0], np.cumsum(counts)]), dtype=torch.int32)
+    src = torch.randn((R, C), generator=g).to(torch.bfloat16)
+    ld = moe.transposed_cols(R, G)
+    dst = poison_(torch.empty((C, ld), dtype=torch.bfloat16, device=DEV))
+    moe.moe_transpose_grouped(src.to(DEV), off.to(DEV), dst=dst)
+    torch.cuda.synchronize()
+    ps = _padded_starts(counts)
+    want = np.zeros((C, int(ps[-1])), dtype=np.int16)
+    sb = src.view(torch.int16).numpy()
+    o = off.numpy()
+    for gi in range(G):
+        want[:, ps[gi]:ps[gi] + counts[gi]] = sb[o[gi]:o[gi + 1]].T
+    got = dst.view(torch.int16).cpu().numpy()
+    np.testing.assert_array_equal(got[:, :ps[-1]], want)
+    end = (int(ps[-1]) + 63) // 64 * 64
+    assert (got[:, ps[-1]:end] == 0).all()
+
+
+@pytest.mark.parametrize("K,N", [(192, 320), (256, 256), (576, 64)])
+def test_grouped_gemm_dw_t_exact(K, N):
+    """dW from contraction-major copies: exact on small-integer operands (fp32 and bf16 outputs,
+    single and dual), empty groups zero, and bitwise equal to moe_grouped_gemm_dw on Gaussian
+    operands (same per-element reduction order; padding adds exact zeros)."""
+    _say("gemm_dw_t exact", K, N)
+    g = torch.Generator().manual_seed(100 * K + N + 1)
+    counts = GROUPS
+    G, R = len(counts), sum(counts)
+    off = torch.tensor(np.concatenate([[0], np.cumsum(counts)]), dtype=torch.int32).to(DEV)
+    A = _int_tensor(g, (R, K), -2, 2).to(DEV)
+    dC, dC2 = _int_tensor(g, (R, N), -2, 2).to(DEV), _int_tensor(g, (R, N), -2, 2).to(DEV)
+    At, dCt, dC2t = (moe.moe_transpose_grouped(t, off) for t in (A, dC, dC2))
+    dB, dB2 = moe.moe_grouped_gemm_dw_t(At, dCt, off, R, dC2t)
+    dB1 = moe.moe_grouped_gemm_dw_t(At, dCt, off, R)[0]
+    hB, hB2 = moe.moe_grouped_gemm_dw_t(At, dCt, off, R, dC2t, out_bf16=True)
+    torch.cuda.synchronize()
+    offn = off.cpu().numpy()
+    ref = O.grouped_gemm_dw(f64(A), f64(dC), offn)
+    ref2 = O.grouped_gemm_dw(f64(A), f64(dC2), offn)
+    np.testing.assert_array_equal(f64(dB), ref)
+    np.testing.assert_array_equal(f64(dB1), ref)
+    np.testing.assert_array_equal(f64(dB2), ref2)
+    np.testing.assert_array_equal(f64(hB), O.bf16_round(ref))
+    np.testing.assert_array_equal(f64(hB2), O.bf16_round(ref2))
+    assert torch.count_nonzero(dB[5]) == 0 and torch.count_nonzero(dB2[10]) == 0
+    # Gaussian operands: bitwise equal to the row-major dW kernel
+    Ag = torch.randn((R, K), generator=g).to(torch.bfloat16).to(DEV)
+    dCg = torch.randn((R, N), generator=g).to(torch.bfloat16).to(DEV)
+    d_rm = moe.moe_grouped_gemm_dw(Ag, dCg, off)[0]
+    d_t = moe.moe_grouped_gemm_dw_t(moe.moe_transpose_grouped(Ag, off), moe.moe_transpose_grouped(dCg, off), off, R)[0]
+    torch.cuda.synchronize()
+    assert torch.equal(d_rm.view(torch.int32), d_t.view(torch.int32))
 
 
 def test_grouped_gemm_dw_worked_example():
@@ -260,10 +330,10 @@ def test_swiglu_fwd_bwd():
 # ---------------------------------------------------------------------------------------------
 # whole layer, small configs: every tensor vs the oracle
 # ---------------------------------------------------------------------------------------------
-def _layer_parity(cfg, seed=0, expert_bias=None, log=None, fuse=True):
+def _layer_parity(cfg, seed=0, expert_bias=None, log=None, fuse=True, dw_t=False):
     inp = W.make_inputs(cfg, seed, "cpu", expert_bias=expert_bias)
     dinp = {k_: v.to(DEV) for k_, v in inp.items()}
-    lay = L.MoELayer(cfg, dinp, fuse_swiglu_bwd=fuse)
+    lay = L.MoELayer(cfg, dinp, fuse_swiglu_bwd=fuse, dw_transposed=dw_t)
     for t in lay.buf.values():
         if t.dtype != torch.uint8:
             poison_(t)
@@ -304,6 +374,25 @@ def test_layer_config0_parity(fuse):
     log = {}
     _layer_parity(W.CONFIGS[0], log=log, fuse=fuse)
     _say({k_: f"{v:.2e}" for k_, v in log.items()})
+
+
+@pytest.mark.parametrize("cfg_id", [0, 2, 3])
+def test_layer_dw_transposed(cfg_id):
+    """The layer with its weight gradients computed from contraction-major copies: oracle parity,
+    and every dW bitwise equal to the row-major path's on the same inputs.  Configs 2 and 3 run
+    at 512 tokens (their shapes otherwise)."""
+    import dataclasses
+    cfg = W.CONFIGS[cfg_id]
+    if cfg_id:
+        cfg = dataclasses.replace(cfg, T=512)
+    _say("layer dw transposed", cfg)
+    lay_t = _layer_parity(cfg, dw_t=True)
+    inp = W.make_inputs(cfg, 0, "cpu")
+    lay = L.MoELayer(cfg, {k_: v.to(DEV) for k_, v in inp.items()})
+    lay.step()
+    torch.cuda.synchronize()
+    for key in ("dw_gate", "dw_up", "dw_down"):
+        assert torch.equal(lay.buf[key].view(torch.int32), lay_t.buf[key].view(torch.int32)), key
 
 
 def test_dx_swiglu_bwd_fusion_bitwise():
