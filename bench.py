@@ -73,6 +73,9 @@ def _args():
     ap.add_argument("--aux-alpha", type=float, default=0.01, help="load-balancing loss weight with --router")
     ap.add_argument("--dw-transposed", action="store_true",
                     help="weight gradients from contraction-major copies of their operands")
+    ap.add_argument("--concurrent", action="store_true",
+                    help="weight gradients and the shared FFN on a second stream beside the main chain "
+                         "(per-call times then include the sharing of the CUs)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tokens", type=int, default=0)
@@ -157,7 +160,7 @@ def main():
     else:
         inp = W.make_inputs(cfg, a.seed, dev)
         lay = L.MoELayer(cfg, inp, router=a.router, aux_alpha=a.aux_alpha if a.router else 0.0,
-                         dw_transposed=a.dw_transposed)
+                         dw_transposed=a.dw_transposed, concurrent=a.concurrent)
     torch.cuda.synchronize()
     t_gen = time.perf_counter() - t_gen
 

@@ -45,10 +45,16 @@ class MoELayer(_Traced):
     dA is then not materialised (buf["d_act"] / buf["d_act_sh"] stay unwritten)."""
 
     def __init__(self, cfg, inputs: dict, normalize_topk: bool = True, fuse_swiglu_bwd: bool = True,
-                 router: bool = False, aux_alpha: float = 0.0, dw_transposed: bool = False):
+                 router: bool = False, aux_alpha: float = 0.0, dw_transposed: bool = False,
+                 concurrent: bool = False):
         self.cfg = cfg
         self.fuse = fuse_swiglu_bwd
         self.dw_t = dw_transposed
+        # concurrent: independent products run on a second stream (default priority): the weight
+        # gradients beside the data gradients, the shared FFN beside the routed experts, so each
+        # kernel's last partial round of tiles fills with the other's tiles
+        self.concurrent = concurrent
+        self.side = torch.cuda.Stream(device=inputs["x"].device) if concurrent else None
         self.router = router
         self.aux_alpha = float(aux_alpha)
         self.inp = inputs
@@ -92,8 +98,31 @@ class MoELayer(_Traced):
                          inputs["w_down_sh"].unsqueeze(0))
 
     # ------------------------------------------------------------------------------------------
+    def _streams(self, stream):
+        main = torch.cuda.current_stream() if stream is None else stream
+        return main, (self.side if self.concurrent else main)
+
+    @staticmethod
+    def _join(waiter, signaller):
+        """waiter waits for everything enqueued on signaller so far (no-op on the same stream)."""
+        if waiter is not signaller:
+            ev = torch.cuda.Event()
+            ev.record(signaller)
+            waiter.wait_event(ev)
+
     def forward(self, stream=None):
         b, i, k, run = self.buf, self.inp, self.cfg.k, self._run
+        main, side = self._streams(stream)
+        stream = main
+        self._join(side, main)            # the side stream starts after the main stream's prior work
+        add = None
+        if self.shared:                   # the shared FFN needs only x: beside the routed experts
+            wg, wu, wd = self.w_sh
+            run("fwd_gate_up_sh", moe.moe_grouped_gemm_fwd, i["x"], wg, self.offsets_sh, wu, b["h_gate_sh"],
+                b["h_up_sh"], b["act_sh"], want_act=True, stream=side)
+            run("fwd_down_sh", moe.moe_grouped_gemm_fwd, b["act_sh"], wd, self.offsets_sh, C=b["y_sh"],
+                stream=side)
+            add = b["y_sh"]
         logits = i["logits"]
         if self.router:
             logits = b["logits"]
@@ -109,71 +138,69 @@ class MoELayer(_Traced):
             b["h_gate"], b["h_up"], b["act"], want_act=True, stream=stream)
         run("fwd_down", moe.moe_grouped_gemm_fwd, b["act"], i["w_down"], b["offsets"], C=b["y_perm"],
             stream=stream)
-        add = None
-        if self.shared:
-            wg, wu, wd = self.w_sh
-            run("fwd_gate_up_sh", moe.moe_grouped_gemm_fwd, i["x"], wg, self.offsets_sh, wu, b["h_gate_sh"],
-                b["h_up_sh"], b["act_sh"], want_act=True, stream=stream)
-            run("fwd_down_sh", moe.moe_grouped_gemm_fwd, b["act_sh"], wd, self.offsets_sh, C=b["y_sh"],
-                stream=stream)
-            add = b["y_sh"]
+        self._join(main, side)
         run("combine", moe.moe_unpermute_combine, b["y_perm"], b["topk_w"], b["row_of_slot"], k, add=add,
             y=b["y"], stream=stream)
         return b["y"]
 
     def backward(self, stream=None):
         b, i, k, run = self.buf, self.inp, self.cfg.k, self._run
+        main, side = self._streams(stream)
+        stream = main
+        self._join(side, main)
+        dx_add = None
+        if self.shared:                   # needs dY and the shared forward only
+            wg, wu, wd = self.w_sh
+            if self.fuse:
+                run("dx_down_swiglu_bwd_sh", moe.moe_grouped_gemm_dx_swiglu_bwd, i["dy"], wd, self.offsets_sh,
+                    b["h_gate_sh"], b["h_up_sh"], b["dh_gate_sh"], b["dh_up_sh"], stream=side)
+            else:
+                run("dx_down_sh", moe.moe_grouped_gemm_dx, i["dy"], wd, self.offsets_sh, dA=b["d_act_sh"],
+                    stream=side)
+            run("dw_down_sh", moe.moe_grouped_gemm_dw, b["act_sh"], i["dy"], self.offsets_sh,
+                dB=b["dw_down_sh"], stream=side)
+            if not self.fuse:
+                run("swiglu_bwd_sh", moe.moe_swiglu_bwd, b["h_gate_sh"], b["h_up_sh"], b["d_act_sh"],
+                    b["dh_gate_sh"], b["dh_up_sh"], stream=side)
+            run("dx_gate_up_sh", moe.moe_grouped_gemm_dx, b["dh_gate_sh"], wg, self.offsets_sh, b["dh_up_sh"],
+                wu, dA=b["dx_sh"], stream=side)
+            run("dw_gate_up_sh", moe.moe_grouped_gemm_dw, i["x"], b["dh_gate_sh"], self.offsets_sh,
+                b["dh_up_sh"], dB=b["dw_gate_sh"], dB2=b["dw_up_sh"], stream=side)
+            dx_add = b["dx_sh"]
         run("combine_bwd", moe.moe_unpermute_combine_bwd, i["dy"], b["topk_w"], b["row_of_slot"], k,
             y_perm=b["y_perm"], dy_perm=b["dy_perm"], d_topk_w=b["d_topk_w"], stream=stream)
+        self._join(side, main)            # dW_down needs dY_perm
+        if self.dw_t:
+            run("transpose_act", moe.moe_transpose_grouped, b["act"], b["offsets"], dst=b["act_t"], stream=side)
+            run("transpose_dy_perm", moe.moe_transpose_grouped, b["dy_perm"], b["offsets"], dst=b["dy_perm_t"],
+                stream=side)
+            run("dw_down", moe.moe_grouped_gemm_dw_t, b["act_t"], b["dy_perm_t"], b["offsets"], self.R,
+                dB=b["dw_down"], stream=side)
+        else:
+            run("dw_down", moe.moe_grouped_gemm_dw, b["act"], b["dy_perm"], b["offsets"], dB=b["dw_down"],
+                stream=side)
         if self.fuse:
             run("dx_down_swiglu_bwd", moe.moe_grouped_gemm_dx_swiglu_bwd, b["dy_perm"], i["w_down"],
                 b["offsets"], b["h_gate"], b["h_up"], b["dh_gate"], b["dh_up"], stream=stream)
         else:
             run("dx_down", moe.moe_grouped_gemm_dx, b["dy_perm"], i["w_down"], b["offsets"], dA=b["d_act"],
                 stream=stream)
-        if self.dw_t:
-            run("transpose_act", moe.moe_transpose_grouped, b["act"], b["offsets"], dst=b["act_t"], stream=stream)
-            run("transpose_dy_perm", moe.moe_transpose_grouped, b["dy_perm"], b["offsets"], dst=b["dy_perm_t"],
-                stream=stream)
-            run("dw_down", moe.moe_grouped_gemm_dw_t, b["act_t"], b["dy_perm_t"], b["offsets"], self.R,
-                dB=b["dw_down"], stream=stream)
-        else:
-            run("dw_down", moe.moe_grouped_gemm_dw, b["act"], b["dy_perm"], b["offsets"], dB=b["dw_down"],
-                stream=stream)
-        if not self.fuse:
             run("swiglu_bwd", moe.moe_swiglu_bwd, b["h_gate"], b["h_up"], b["d_act"], b["dh_gate"],
                 b["dh_up"], stream=stream)
+        self._join(side, main)            # dW_gate/dW_up need dH
         run("dx_gate_up", moe.moe_grouped_gemm_dx, b["dh_gate"], i["w_gate"], b["offsets"], b["dh_up"],
             i["w_up"], dA=b["dx_perm"], stream=stream)
         if self.dw_t:
             run("transpose_x_perm", moe.moe_transpose_grouped, b["x_perm"], b["offsets"], dst=b["x_perm_t"],
-                stream=stream)
-            run("transpose_dh", self._transpose_dh, stream=stream)
+                stream=side)
+            run("transpose_dh", self._transpose_dh, stream=side)
             run("dw_gate_up", moe.moe_grouped_gemm_dw_t, b["x_perm_t"], b["dh_gate_t"], b["offsets"], self.R,
-                b["dh_up_t"], dB=b["dw_gate"], dB2=b["dw_up"], stream=stream)
+                b["dh_up_t"], dB=b["dw_gate"], dB2=b["dw_up"], stream=side)
         else:
             run("dw_gate_up", moe.moe_grouped_gemm_dw, b["x_perm"], b["dh_gate"], b["offsets"], b["dh_up"],
-                dB=b["dw_gate"], dB2=b["dw_up"], stream=stream)
-        add = None
-        if self.shared:
-            wg, wu, wd = self.w_sh
-            if self.fuse:
-                run("dx_down_swiglu_bwd_sh", moe.moe_grouped_gemm_dx_swiglu_bwd, i["dy"], wd, self.offsets_sh,
-                    b["h_gate_sh"], b["h_up_sh"], b["dh_gate_sh"], b["dh_up_sh"], stream=stream)
-            else:
-                run("dx_down_sh", moe.moe_grouped_gemm_dx, i["dy"], wd, self.offsets_sh, dA=b["d_act_sh"],
-                    stream=stream)
-            run("dw_down_sh", moe.moe_grouped_gemm_dw, b["act_sh"], i["dy"], self.offsets_sh,
-                dB=b["dw_down_sh"], stream=stream)
-            if not self.fuse:
-                run("swiglu_bwd_sh", moe.moe_swiglu_bwd, b["h_gate_sh"], b["h_up_sh"], b["d_act_sh"],
-                    b["dh_gate_sh"], b["dh_up_sh"], stream=stream)
-            run("dx_gate_up_sh", moe.moe_grouped_gemm_dx, b["dh_gate_sh"], wg, self.offsets_sh, b["dh_up_sh"],
-                wu, dA=b["dx_sh"], stream=stream)
-            run("dw_gate_up_sh", moe.moe_grouped_gemm_dw, i["x"], b["dh_gate_sh"], self.offsets_sh,
-                b["dh_up_sh"], dB=b["dw_gate_sh"], dB2=b["dw_up_sh"], stream=stream)
-            add = b["dx_sh"]
-        run("unpermute_dx", moe.moe_unpermute_combine, b["dx_perm"], None, b["row_of_slot"], k, add=add,
+                dB=b["dw_gate"], dB2=b["dw_up"], stream=side)
+        self._join(main, side)            # the shared dX, and every weight gradient, are complete
+        run("unpermute_dx", moe.moe_unpermute_combine, b["dx_perm"], None, b["row_of_slot"], k, add=dx_add,
             y=b["dx"], stream=stream)
         if self.router:
             run("router_bwd", moe.moe_router_bwd, i["x"], i["wr"], b["logits"], b["topk_idx"], b["topk_w"],

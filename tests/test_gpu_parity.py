@@ -395,6 +395,33 @@ def test_layer_dw_transposed(cfg_id):
         assert torch.equal(lay.buf[key].view(torch.int32), lay_t.buf[key].view(torch.int32)), key
 
 
+@pytest.mark.parametrize("cfg_id", [0, 2])
+def test_layer_concurrent_bitwise(cfg_id):
+    """The two-stream schedule (weight gradients and the shared FFN beside the main chain) gives
+    bitwise the same outputs as one stream: every kernel is deterministic and the joins order
+    every dependency.  Two steps in a row (the second reuses every buffer)."""
+    import dataclasses
+    cfg = W.CONFIGS[cfg_id]
+    if cfg_id:
+        cfg = dataclasses.replace(cfg, T=1024)
+    _say("layer concurrent", cfg)
+    inp = W.make_inputs(cfg, 0, "cpu")
+    dinp = {k_: v.to(DEV) for k_, v in inp.items()}
+    seq = L.MoELayer(cfg, dinp)
+    con = L.MoELayer(cfg, dinp, concurrent=True)
+    seq.step()
+    for _ in range(2):
+        for t in con.buf.values():
+            poison_(t)
+        con.step()
+    torch.cuda.synchronize()
+    for key, t in seq.buf.items():
+        if key in ("workspace", "d_act", "d_act_sh"):
+            continue
+        u = con.buf[key]
+        assert torch.equal(t.view(torch.uint8), u.view(torch.uint8)), key
+
+
 def test_dx_swiglu_bwd_fusion_bitwise():
     """The fused dX+SwiGLU-backward epilogue equals moe_grouped_gemm_dx then moe_swiglu_bwd bit for
     bit (same rounding of dA, same elementwise arithmetic), on ragged groups spanning tiles."""
