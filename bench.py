@@ -73,6 +73,8 @@ def _args():
     ap.add_argument("--aux-alpha", type=float, default=0.01, help="load-balancing loss weight with --router")
     ap.add_argument("--dw-transposed", action="store_true",
                     help="weight gradients from contraction-major copies of their operands")
+    ap.add_argument("--no-split-tail", action="store_true",
+                    help="persistent dX products do not split their last partial round of tiles")
     ap.add_argument("--concurrent", action="store_true",
                     help="weight gradients and the shared FFN on a second stream beside the main chain "
                          "(per-call times then include the sharing of the CUs)")
@@ -160,7 +162,7 @@ def main():
     else:
         inp = W.make_inputs(cfg, a.seed, dev)
         lay = L.MoELayer(cfg, inp, router=a.router, aux_alpha=a.aux_alpha if a.router else 0.0,
-                         dw_transposed=a.dw_transposed, concurrent=a.concurrent)
+                         dw_transposed=a.dw_transposed, concurrent=a.concurrent, split_tail=not a.no_split_tail)
     torch.cuda.synchronize()
     t_gen = time.perf_counter() - t_gen
 

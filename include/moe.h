@@ -182,6 +182,27 @@ moe_status moe_grouped_gemm_dx_swiglu_bwd(const moe_bf16* dC, const moe_bf16* B,
                                           int64_t N, const moe_bf16* h_gate, const moe_bf16* h_up,
                                           moe_bf16* dh_gate, moe_bf16* dh_up, hipStream_t stream);
 
+/*
+ * The same products as moe_grouped_gemm_dx / moe_grouped_gemm_dx_swiglu_bwd (same arguments,
+ * definitions and errors) with a workspace that lets the persistent kernel split the tiles of its
+ * last, partial round of tiles along the contraction over the otherwise idle CUs: each piece
+ * stores an fp32 partial tile, and the last piece to finish adds the pieces in a fixed order
+ * before the usual epilogue.  Deterministic; a split tile's fp32 sum is grouped differently from
+ * the unsplit kernel's, so bf16 results may differ from it in the last place.  workspace: device
+ * memory of moe_grouped_gemm_split_workspace_bytes() bytes, 16-byte aligned, owned by the caller;
+ * calls that overlap in time (on different streams) need separate workspaces.
+ */
+size_t moe_grouped_gemm_split_workspace_bytes(void);
+moe_status moe_grouped_gemm_dx_split(const moe_bf16* dC, const moe_bf16* B, const moe_bf16* dC2,
+                                     const moe_bf16* B2, const int32_t* offsets, int32_t G, int64_t R,
+                                     int64_t K, int64_t N, moe_bf16* dA, void* workspace,
+                                     size_t workspace_bytes, hipStream_t stream);
+moe_status moe_grouped_gemm_dx_swiglu_bwd_split(const moe_bf16* dC, const moe_bf16* B,
+                                                const int32_t* offsets, int32_t G, int64_t R, int64_t K,
+                                                int64_t N, const moe_bf16* h_gate, const moe_bf16* h_up,
+                                                moe_bf16* dh_gate, moe_bf16* dh_up, void* workspace,
+                                                size_t workspace_bytes, hipStream_t stream);
+
 /* ------------------------------------------------------------------------------------------ */
 /* H, K: backward weight-gradient grouped GEMM (the paper's dW1 kernel class)                   */
 /* ------------------------------------------------------------------------------------------ */

@@ -65,6 +65,9 @@ struct GemmParams {
   int m_tiles;         // DW: tiles over K
   int n_tiles;         // tiles over the output columns
   int64_t ld_t;        // DWT: row length of the contraction-major operands
+  int* split_cnt;      // persistent kernels: split the last partial round's tiles (NULL: no split);
+  float* split_part;   //   arrival counters (zero at launch) and fp32 partial tiles, one per unit
+  int split_max;       //   at most this many contraction pieces per tail tile
 };
 
 typedef int i32x4 __attribute__((ext_vector_type(4)));
@@ -390,8 +393,9 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
   };
 
   // buffer resources of step s for the M and N operands
+  int s_base = 0;   // first contraction step of the tile's range (a piece of a split tile)
   auto rsrc_m = [&](int s) {
-    const int64_t c0 = (int64_t)s * BK;
+    const int64_t c0 = (int64_t)(s + s_base) * BK;
     if (s >= nsteps) return make_rsrc(m_src, 0);   // past the end: every load is out of range
     if constexpr (!M_T) {
       const char* base = m_src;
@@ -406,7 +410,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
     }
   };
   auto rsrc_n = [&](int s) {
-    const int64_t c0 = (int64_t)s * BK;
+    const int64_t c0 = (int64_t)(s + s_base) * BK;
     if (s >= nsteps) return make_rsrc(n_src, 0);
     if constexpr (!N_T) {
       const char* base = n_src;
@@ -747,47 +751,139 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
   };
 
   // ---------------- tile loop -----------------------------------------------------------------
-  int it = blockIdx.x;
-  if (it >= ntiles_all) return;   // uniform over the workgroup
-  int g, mt, nt, row_lo, row_hi;
-  map_tile(it, g, mt, nt, row_lo, row_hi);
-  setup(g, mt, nt, row_lo, row_hi);
-  zero_acc();
-  prefill();
-  if constexpr (!PERSIST) {
-    // one tile per workgroup; the hardware dispatcher hands the next tile to whichever CU frees
-    main_loop();
-    epilogue(g, mt, nt, row_lo, row_hi);
-    return;
-  }
-  for (;;) {
-    main_loop();
-    const int next = it + (int)gridDim.x;
-    const bool more = next < ntiles_all;   // uniform
-    int g2 = 0, mt2 = 0, nt2 = 0, lo2 = 0, hi2 = 0;
-    if constexpr (IS_DW && !OUT16) {
-      // fp32 results leave from registers: once every wave is done with the ring, start filling
-      // it with the next tile's first stages, then store this tile
-      __syncthreads();
-      if (more) {
-        map_tile(next, g2, mt2, nt2, lo2, hi2);
-        setup(g2, mt2, nt2, lo2, hi2);
-        prefill();
-      }
-      epilogue(g, mt, nt, row_lo, row_hi);
-    } else {
-      epilogue(g, mt, nt, row_lo, row_hi);   // stages the tile through the ring
-      if (more) {
-        __syncthreads();   // every staged chunk has been read
-        map_tile(next, g2, mt2, nt2, lo2, hi2);
-        setup(g2, mt2, nt2, lo2, hi2);
-        prefill();
+  // A persistent kernel given a split workspace runs only the full rounds of tiles this way; the
+  // tiles of the last, partial round are split along the contraction (below).
+  int normal_end = ntiles_all, tail_first = ntiles_all, S = 1;
+  if constexpr (PERSIST) {
+    if (p.split_part != nullptr) {
+      const int slots = (int)gridDim.x;
+      const int full = (ntiles_all / slots) * slots;
+      const int tail = ntiles_all - full;
+      if (tail > 0) {
+        int sp = slots / tail;
+        if (sp > p.split_max) sp = p.split_max;
+        if (sp > 1) {
+          S = sp;
+          normal_end = full;
+          tail_first = full;
+        }
       }
     }
-    if (!more) break;
-    it = next;
-    g = g2; mt = mt2; nt = nt2; row_lo = lo2; row_hi = hi2;
+  }
+  int it = blockIdx.x;
+  int g, mt, nt, row_lo, row_hi;
+  if (it < normal_end) {   // uniform over the workgroup
+    map_tile(it, g, mt, nt, row_lo, row_hi);
+    setup(g, mt, nt, row_lo, row_hi);
     zero_acc();
+    prefill();
+    if constexpr (!PERSIST) {
+      // one tile per workgroup; the hardware dispatcher hands the next tile to whichever CU frees
+      main_loop();
+      epilogue(g, mt, nt, row_lo, row_hi);
+      return;
+    }
+    for (;;) {
+      main_loop();
+      const int next = it + (int)gridDim.x;
+      const bool more = next < normal_end;   // uniform
+      int g2 = 0, mt2 = 0, nt2 = 0, lo2 = 0, hi2 = 0;
+      if constexpr (IS_DW && !OUT16) {
+        // fp32 results leave from registers: once every wave is done with the ring, start filling
+        // it with the next tile's first stages, then store this tile
+        __syncthreads();
+        if (more) {
+          map_tile(next, g2, mt2, nt2, lo2, hi2);
+          setup(g2, mt2, nt2, lo2, hi2);
+          prefill();
+        }
+        epilogue(g, mt, nt, row_lo, row_hi);
+      } else {
+        epilogue(g, mt, nt, row_lo, row_hi);   // stages the tile through the ring
+        if (more) {
+          __syncthreads();   // every staged chunk has been read
+          map_tile(next, g2, mt2, nt2, lo2, hi2);
+          setup(g2, mt2, nt2, lo2, hi2);
+          prefill();
+        }
+      }
+      if (!more) break;
+      it = next;
+      g = g2; mt = mt2; nt = nt2; row_lo = lo2; row_hi = hi2;
+      zero_acc();
+    }
+  }
+
+  // ---------------- split tail ------------------------------------------------------------------
+  // Unit u (one per workgroup) computes piece q = u % S of tail tile u / S: contraction steps
+  // [q*n/S, (q+1)*n/S).  It stores its fp32 partial tile to the workspace and counts itself in; the
+  // last of the S pieces to arrive adds the S partials in piece order (a fixed order: the result
+  // does not depend on which piece arrives last) and runs the tile's epilogue.
+  if constexpr (PERSIST) {
+    __shared__ int s_arrived;
+    const int units = (ntiles_all - tail_first) * S;
+    if (S > 1 && (int)blockIdx.x < units) {
+      const int u = blockIdx.x, tl = u / S, q = u - tl * S;
+      __syncthreads();   // the ring and the staging area are free (the last normal tile is done)
+      map_tile(tail_first + tl, g, mt, nt, row_lo, row_hi);
+      setup(g, mt, nt, row_lo, row_hi);
+      const int total = nsteps;
+      const int sb = (int)((int64_t)total * q / S), se = (int)((int64_t)total * (q + 1) / S);
+      s_base = sb;
+      nsteps = se - sb;
+      zero_acc();
+      prefill();
+      main_loop();
+      constexpr int NT = 64 * NWAVE;
+      constexpr int SLOT = NT * 4;   // floats per float4 slot across the workgroup
+      auto part_of = [&](int unit) { return p.split_part + (int64_t)unit * (TM * TN); };
+      // The partials cross XCDs (separate L2s).  They are written and read with agent-coherent
+      // (sc1) buffer accesses, which write through / bypass the non-coherent caches, so the only
+      // ordering needed is: every store of the piece has completed (vmcnt 0, then the barrier)
+      // before the piece is counted, and the reads start after the count was seen.  A device-scope
+      // fence would do the same by writing back and invalidating the whole L2 of the XCD, which
+      // measured 3-4% slower on the whole product.
+      constexpr int SC1 = 16;   // cache-policy bit: agent-scope coherent
+      auto off_of = [&](int i, int j, int q4) { return (((i * NB + j) * 4 + q4) * SLOT + tid * 4) * 4; };
+      {
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(part_of(u), 0, TM * TN * 4, 0x00020000);
+#pragma unroll
+        for (int i = 0; i < MB; ++i)
+#pragma unroll
+          for (int j = 0; j < NB; ++j)
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+              const f32x4 v = {acc[i][j][4 * q4], acc[i][j][4 * q4 + 1], acc[i][j][4 * q4 + 2], acc[i][j][4 * q4 + 3]};
+              __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), rs, off_of(i, j, q4), 0, SC1);
+            }
+      }
+      wait_vm<0>();
+      __syncthreads();
+      if (tid == 0)
+        s_arrived = __hip_atomic_fetch_add(p.split_cnt + tl, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __syncthreads();
+      if (s_arrived == S - 1) {   // uniform: this workgroup completes the tile
+        zero_acc();
+        for (int r = 0; r < S; ++r) {
+          const __amdgpu_buffer_rsrc_t rs =
+              __builtin_amdgcn_make_buffer_rsrc(part_of(tl * S + r), 0, TM * TN * 4, 0x00020000);
+#pragma unroll
+          for (int i = 0; i < MB; ++i)
+#pragma unroll
+            for (int j = 0; j < NB; ++j)
+#pragma unroll
+              for (int q4 = 0; q4 < 4; ++q4) {
+                const f32x4 v =
+                    __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, off_of(i, j, q4), 0, SC1));
+                acc[i][j][4 * q4] += v[0];
+                acc[i][j][4 * q4 + 1] += v[1];
+                acc[i][j][4 * q4 + 2] += v[2];
+                acc[i][j][4 * q4 + 3] += v[3];
+              }
+        }
+        epilogue(g, mt, nt, row_lo, row_hi);
+      }
+    }
   }
 }
 
@@ -830,6 +926,30 @@ moe_status launch(const GemmParams& p, int64_t tiles_bound, hipStream_t stream, 
 
 bool bad_ptr(const void* q) { return q != nullptr && !aligned16(q); }
 
+// Split-tail workspace: 256 arrival counters, then one fp32 256x256 partial tile per unit (at most
+// one unit per persistent workgroup, i.e. per CU slot, which device_cu_count bounds by 256 here).
+constexpr int SPLIT_UNITS = 256, SPLIT_MAX = 8;
+constexpr size_t SPLIT_CNT_BYTES = SPLIT_UNITS * sizeof(int);
+constexpr size_t SPLIT_BYTES = SPLIT_CNT_BYTES + (size_t)SPLIT_UNITS * 256 * TN * sizeof(float);
+
+__global__ void zero_i32_kernel(int* p, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
+
+// Attach a split workspace to p (zeroing its counters on `stream`); NULL leaves p unsplit.
+moe_status attach_split(GemmParams& p, void* ws, size_t ws_bytes, const char* fn, hipStream_t stream) {
+  if (ws == nullptr) return MOE_SUCCESS;
+  if (ws_bytes < SPLIT_BYTES || !aligned16(ws))
+    return fail(MOE_ERROR_WORKSPACE, "%s: a 16-byte aligned workspace of %zu bytes is needed", fn, SPLIT_BYTES);
+  if (device_cu_count() > SPLIT_UNITS) return MOE_SUCCESS;   // more slots than partial tiles: no split
+  p.split_cnt = static_cast<int*>(ws);
+  p.split_part = reinterpret_cast<float*>(static_cast<char*>(ws) + SPLIT_CNT_BYTES);
+  p.split_max = SPLIT_MAX;
+  zero_i32_kernel<<<1, SPLIT_UNITS, 0, stream>>>(p.split_cnt, SPLIT_UNITS);
+  return check_launch(fn);
+}
+
 }  // namespace
 }  // namespace moe
 
@@ -864,10 +984,11 @@ extern "C" moe_status moe_grouped_gemm_fwd(const moe_bf16* A, const moe_bf16* B,
   return launch<KIND_FWD, false, false>(p, tiles, stream, "grouped_gemm_fwd");
 }
 
-extern "C" moe_status moe_grouped_gemm_dx(const moe_bf16* dC, const moe_bf16* B, const moe_bf16* dC2,
-                                          const moe_bf16* B2, const int32_t* offsets, int32_t G,
-                                          int64_t R, int64_t K, int64_t N, moe_bf16* dA,
-                                          hipStream_t stream) {
+namespace moe {
+namespace {
+moe_status grouped_gemm_dx_impl(const moe_bf16* dC, const moe_bf16* B, const moe_bf16* dC2, const moe_bf16* B2,
+                                const int32_t* offsets, int32_t G, int64_t R, int64_t K, int64_t N, moe_bf16* dA,
+                                void* ws, size_t ws_bytes, hipStream_t stream) {
   if (G < 1 || G > 256) return fail(MOE_ERROR_NOT_SUPPORTED, "moe_grouped_gemm_dx: need 1 <= G <= 256");
   if (R < 0 || K <= 0 || N <= 0) return fail(MOE_ERROR_INVALID_VALUE, "moe_grouped_gemm_dx: bad size");
   if (K % 64 || N % 64) return fail(MOE_ERROR_NOT_SUPPORTED, "moe_grouped_gemm_dx: K and N must be multiples of 64");
@@ -888,15 +1009,37 @@ extern "C" moe_status moe_grouped_gemm_dx(const moe_bf16* dC, const moe_bf16* B,
   p.mt_bound = (int)((R + TM - 1) / TM + G);
   p.n_tiles = (int)((K + TN - 1) / TN);
   const int64_t tiles = (int64_t)p.mt_bound * p.n_tiles;   // upper bound; exact count on device
+  const moe_status st = attach_split(p, ws, ws_bytes, "moe_grouped_gemm_dx", stream);
+  if (st != MOE_SUCCESS) return st;
   if (dC2) return launch<KIND_DX, true, false>(p, tiles, stream, "grouped_gemm_dx(dual)");
   return launch<KIND_DX, false, false>(p, tiles, stream, "grouped_gemm_dx");
 }
+}  // namespace
+}  // namespace moe
 
-extern "C" moe_status moe_grouped_gemm_dx_swiglu_bwd(const moe_bf16* dC, const moe_bf16* B,
-                                                      const int32_t* offsets, int32_t G, int64_t R,
-                                                      int64_t K, int64_t N, const moe_bf16* h_gate,
-                                                      const moe_bf16* h_up, moe_bf16* dh_gate,
-                                                      moe_bf16* dh_up, hipStream_t stream) {
+extern "C" moe_status moe_grouped_gemm_dx(const moe_bf16* dC, const moe_bf16* B, const moe_bf16* dC2,
+                                          const moe_bf16* B2, const int32_t* offsets, int32_t G,
+                                          int64_t R, int64_t K, int64_t N, moe_bf16* dA,
+                                          hipStream_t stream) {
+  return grouped_gemm_dx_impl(dC, B, dC2, B2, offsets, G, R, K, N, dA, nullptr, 0, stream);
+}
+
+extern "C" size_t moe_grouped_gemm_split_workspace_bytes(void) { return SPLIT_BYTES; }
+
+extern "C" moe_status moe_grouped_gemm_dx_split(const moe_bf16* dC, const moe_bf16* B, const moe_bf16* dC2,
+                                                const moe_bf16* B2, const int32_t* offsets, int32_t G,
+                                                int64_t R, int64_t K, int64_t N, moe_bf16* dA, void* workspace,
+                                                size_t workspace_bytes, hipStream_t stream) {
+  if (!workspace) return fail(MOE_ERROR_WORKSPACE, "moe_grouped_gemm_dx_split: workspace is NULL");
+  return grouped_gemm_dx_impl(dC, B, dC2, B2, offsets, G, R, K, N, dA, workspace, workspace_bytes, stream);
+}
+
+namespace moe {
+namespace {
+moe_status grouped_gemm_dx_swiglu_bwd_impl(const moe_bf16* dC, const moe_bf16* B, const int32_t* offsets, int32_t G,
+                                           int64_t R, int64_t K, int64_t N, const moe_bf16* h_gate,
+                                           const moe_bf16* h_up, moe_bf16* dh_gate, moe_bf16* dh_up, void* ws,
+                                           size_t ws_bytes, hipStream_t stream) {
   const char* fn = "moe_grouped_gemm_dx_swiglu_bwd";
   if (G < 1 || G > 256) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: need 1 <= G <= 256", fn);
   if (R < 0 || K <= 0 || N <= 0) return fail(MOE_ERROR_INVALID_VALUE, "%s: bad size", fn);
@@ -917,7 +1060,31 @@ extern "C" moe_status moe_grouped_gemm_dx_swiglu_bwd(const moe_bf16* dC, const m
   p.mt_bound = (int)((R + TM - 1) / TM + G);
   p.n_tiles = (int)((K + TN - 1) / TN);
   const int64_t tiles = (int64_t)p.mt_bound * p.n_tiles;   // upper bound; exact count on device
+  const moe_status st = attach_split(p, ws, ws_bytes, fn, stream);
+  if (st != MOE_SUCCESS) return st;
   return launch<KIND_DX, false, true>(p, tiles, stream, "grouped_gemm_dx(swiglu_bwd)");
+}
+}  // namespace
+}  // namespace moe
+
+extern "C" moe_status moe_grouped_gemm_dx_swiglu_bwd(const moe_bf16* dC, const moe_bf16* B,
+                                                      const int32_t* offsets, int32_t G, int64_t R,
+                                                      int64_t K, int64_t N, const moe_bf16* h_gate,
+                                                      const moe_bf16* h_up, moe_bf16* dh_gate,
+                                                      moe_bf16* dh_up, hipStream_t stream) {
+  return grouped_gemm_dx_swiglu_bwd_impl(dC, B, offsets, G, R, K, N, h_gate, h_up, dh_gate, dh_up, nullptr, 0,
+                                         stream);
+}
+
+extern "C" moe_status moe_grouped_gemm_dx_swiglu_bwd_split(const moe_bf16* dC, const moe_bf16* B,
+                                                            const int32_t* offsets, int32_t G, int64_t R,
+                                                            int64_t K, int64_t N, const moe_bf16* h_gate,
+                                                            const moe_bf16* h_up, moe_bf16* dh_gate,
+                                                            moe_bf16* dh_up, void* workspace,
+                                                            size_t workspace_bytes, hipStream_t stream) {
+  if (!workspace) return fail(MOE_ERROR_WORKSPACE, "moe_grouped_gemm_dx_swiglu_bwd_split: workspace is NULL");
+  return grouped_gemm_dx_swiglu_bwd_impl(dC, B, offsets, G, R, K, N, h_gate, h_up, dh_gate, dh_up, workspace,
+                                         workspace_bytes, stream);
 }
 
 namespace moe {

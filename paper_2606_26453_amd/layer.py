@@ -46,8 +46,11 @@ class MoELayer(_Traced):
 
     def __init__(self, cfg, inputs: dict, normalize_topk: bool = True, fuse_swiglu_bwd: bool = True,
                  router: bool = False, aux_alpha: float = 0.0, dw_transposed: bool = False,
-                 concurrent: bool = False):
+                 concurrent: bool = False, split_tail: bool = True):
         self.cfg = cfg
+        # split_tail: the persistent dX products split their last partial round of tiles along the
+        # contraction (a workspace of fp32 partial tiles)
+        self.split_ws = moe.split_workspace(inputs["x"].device) if split_tail else None
         self.fuse = fuse_swiglu_bwd
         self.dw_t = dw_transposed
         # concurrent: independent products run on a second stream (default priority): the weight
@@ -181,7 +184,8 @@ class MoELayer(_Traced):
                 stream=side)
         if self.fuse:
             run("dx_down_swiglu_bwd", moe.moe_grouped_gemm_dx_swiglu_bwd, b["dy_perm"], i["w_down"],
-                b["offsets"], b["h_gate"], b["h_up"], b["dh_gate"], b["dh_up"], stream=stream)
+                b["offsets"], b["h_gate"], b["h_up"], b["dh_gate"], b["dh_up"], stream=stream,
+                workspace=self.split_ws)
         else:
             run("dx_down", moe.moe_grouped_gemm_dx, b["dy_perm"], i["w_down"], b["offsets"], dA=b["d_act"],
                 stream=stream)
@@ -189,7 +193,7 @@ class MoELayer(_Traced):
                 b["dh_up"], stream=stream)
         self._join(side, main)            # dW_gate/dW_up need dH
         run("dx_gate_up", moe.moe_grouped_gemm_dx, b["dh_gate"], i["w_gate"], b["offsets"], b["dh_up"],
-            i["w_up"], dA=b["dx_perm"], stream=stream)
+            i["w_up"], dA=b["dx_perm"], stream=stream, workspace=self.split_ws)
         if self.dw_t:
             run("transpose_x_perm", moe.moe_transpose_grouped, b["x_perm"], b["offsets"], dst=b["x_perm_t"],
                 stream=side)

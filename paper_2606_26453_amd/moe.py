@@ -44,6 +44,11 @@ _SIG = {
     "moe_grouped_gemm_dx": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P]),
     "moe_grouped_gemm_dw": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P]),
     "moe_grouped_gemm_dw_bf16": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P]),
+    "moe_grouped_gemm_split_workspace_bytes": (ctypes.c_size_t, []),
+    "moe_grouped_gemm_dx_split": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, ctypes.c_size_t,
+                                                 _P]),
+    "moe_grouped_gemm_dx_swiglu_bwd_split": (ctypes.c_int, [_P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P, _P, _P,
+                                                            ctypes.c_size_t, _P]),
     "moe_grouped_gemm_dw_t": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _I64, _P, _P, _I32, _P]),
     "moe_transposed_cols_bound": (ctypes.c_int64, [_I64, _I32]),
     "moe_transpose_grouped": (ctypes.c_int, [_P, _P, _I32, _I64, _I64, _P, _I64, _P]),
@@ -222,7 +227,12 @@ def moe_unpermute_combine_bwd(dy, topk_w, row_of_slot, k, y_perm=None, dy_perm=N
     return dy_perm, d_topk_w
 
 
-def moe_grouped_gemm_dx(dC, B, offsets, dC2=None, B2=None, dA=None, stream=None):
+def split_workspace(device):
+    """A workspace for the split-tail variants of the persistent dX products."""
+    return torch.empty(lib().moe_grouped_gemm_split_workspace_bytes(), dtype=torch.uint8, device=device)
+
+
+def moe_grouped_gemm_dx(dC, B, offsets, dC2=None, B2=None, dA=None, stream=None, workspace=None):
     R, N = dC.shape
     G, K, N2 = B.shape
     if N2 != N:
@@ -234,9 +244,14 @@ def moe_grouped_gemm_dx(dC, B, offsets, dC2=None, B2=None, dA=None, stream=None)
     _need(offsets, torch.int32, (G + 1,), "offsets")
     dA = torch.empty((R, K), dtype=torch.bfloat16, device=dC.device) if dA is None else dA
     _need(dA, torch.bfloat16, (R, K), "dA")
-    _check("moe_grouped_gemm_dx",
-           lib().moe_grouped_gemm_dx(_ptr(dC), _ptr(B), _ptr(dC2), _ptr(B2), _ptr(offsets), G, R, K, N,
-                                     _ptr(dA), _stream(stream)))
+    if workspace is None:
+        _check("moe_grouped_gemm_dx",
+               lib().moe_grouped_gemm_dx(_ptr(dC), _ptr(B), _ptr(dC2), _ptr(B2), _ptr(offsets), G, R, K, N,
+                                         _ptr(dA), _stream(stream)))
+    else:
+        _check("moe_grouped_gemm_dx_split",
+               lib().moe_grouped_gemm_dx_split(_ptr(dC), _ptr(B), _ptr(dC2), _ptr(B2), _ptr(offsets), G, R, K, N,
+                                               _ptr(dA), _ptr(workspace), workspace.numel(), _stream(stream)))
     return dA
 
 
@@ -279,7 +294,8 @@ def moe_grouped_gemm_dw_bf16(A, dC, offsets, dC2=None, dB=None, dB2=None, stream
     return dB, dB2
 
 
-def moe_grouped_gemm_dx_swiglu_bwd(dC, B, offsets, h_gate, h_up, dh_gate=None, dh_up=None, stream=None):
+def moe_grouped_gemm_dx_swiglu_bwd(dC, B, offsets, h_gate, h_up, dh_gate=None, dh_up=None, stream=None,
+                                   workspace=None):
     R, N = dC.shape
     G, K, N2 = B.shape
     if N2 != N:
@@ -293,9 +309,15 @@ def moe_grouped_gemm_dx_swiglu_bwd(dC, B, offsets, h_gate, h_up, dh_gate=None, d
     dh_up = torch.empty((R, K), dtype=torch.bfloat16, device=dC.device) if dh_up is None else dh_up
     _need(dh_gate, torch.bfloat16, (R, K), "dh_gate")
     _need(dh_up, torch.bfloat16, (R, K), "dh_up")
-    _check("moe_grouped_gemm_dx_swiglu_bwd",
-           lib().moe_grouped_gemm_dx_swiglu_bwd(_ptr(dC), _ptr(B), _ptr(offsets), G, R, K, N, _ptr(h_gate),
-                                                _ptr(h_up), _ptr(dh_gate), _ptr(dh_up), _stream(stream)))
+    if workspace is None:
+        _check("moe_grouped_gemm_dx_swiglu_bwd",
+               lib().moe_grouped_gemm_dx_swiglu_bwd(_ptr(dC), _ptr(B), _ptr(offsets), G, R, K, N, _ptr(h_gate),
+                                                    _ptr(h_up), _ptr(dh_gate), _ptr(dh_up), _stream(stream)))
+    else:
+        _check("moe_grouped_gemm_dx_swiglu_bwd_split",
+               lib().moe_grouped_gemm_dx_swiglu_bwd_split(_ptr(dC), _ptr(B), _ptr(offsets), G, R, K, N,
+                                                          _ptr(h_gate), _ptr(h_up), _ptr(dh_gate), _ptr(dh_up),
+                                                          _ptr(workspace), workspace.numel(), _stream(stream)))
     return dh_gate, dh_up
 
 

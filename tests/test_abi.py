@@ -85,6 +85,19 @@ def test_gemm_rejects():
     assert dxs(N=100) == 2 and dxs(hg=None) == 1 and dxs(hg=BAD) == 1 and dxs(R=0) == 0
 
 
+def test_split_rejects():
+    """The split-tail dX entries need a workspace of the queried size: missing or short -> 3."""
+    L = moe.lib()
+    need = L.moe_grouped_gemm_split_workspace_bytes()
+    assert need >= 256 * 256 * 256 * 4
+    dx = lambda ws=FAKE, n=need, K=128: L.moe_grouped_gemm_dx_split(
+        FAKE, FAKE, None, None, FAKE, 4, 100, K, 128, FAKE, ws, n, None)
+    assert dx(ws=None) == 3 and dx(n=need - 1) == 3 and dx(ws=BAD) == 3 and dx(K=65) == 2
+    dxs = lambda ws=FAKE, n=need: L.moe_grouped_gemm_dx_swiglu_bwd_split(
+        FAKE, FAKE, FAKE, 4, 100, 128, 128, FAKE, FAKE, FAKE, FAKE, ws, n, None)
+    assert dxs(ws=None) == 3 and dxs(n=16) == 3
+
+
 def test_dw_t_and_transpose_rejects():
     L = moe.lib()
     assert L.moe_transposed_cols_bound(100, 4) == 128 + 128

@@ -291,6 +291,49 @@ def test_grouped_gemm_dw_t_exact(K, N):
     assert torch.equal(d_rm.view(torch.int32), d_t.view(torch.int32))
 
 
+def test_grouped_gemm_dx_split_tail():
+    """The persistent dX kernels with a split workspace: a tile count just past a full round of
+    CUs (so the last round's tiles are split along the contraction) -- exact on small-integer
+    operands and bitwise equal to the unsplit kernels there, deterministic on Gaussian operands
+    and within tolerance of the oracle; the fused SwiGLU backward likewise."""
+    _say("gemm dx split tail")
+    slots = torch.cuda.get_device_properties(0).multi_processor_count // 8 * 8
+    rng = np.random.default_rng(9)
+    K, N = 512, 512                                   # 2 column tiles, 16 contraction steps (32 dual)
+    rows_tiles = slots // 2 + 3                       # slots + 6 tiles in all: a round and a bit
+    counts = [256] * (rows_tiles - 5) + [1, 255, 129, 0, 70]
+    G, R = len(counts), sum(counts)
+    assert G <= 256
+    off = torch.tensor(np.concatenate([[0], np.cumsum(counts)]), dtype=torch.int32).to(DEV)
+    g = torch.Generator().manual_seed(9)
+    ws = moe.split_workspace(DEV)
+    dC, dC2 = _int_tensor(g, (R, N)).to(DEV), _int_tensor(g, (R, N)).to(DEV)
+    B, B2 = _int_tensor(g, (G, K, N)).to(DEV), _int_tensor(g, (G, K, N)).to(DEV)
+    ref_s = moe.moe_grouped_gemm_dx(dC, B, off, dC2, B2)
+    got_s = moe.moe_grouped_gemm_dx(dC, B, off, dC2, B2, workspace=ws)
+    got_1 = moe.moe_grouped_gemm_dx(dC, B, off, workspace=ws)
+    torch.cuda.synchronize()
+    offn = off.cpu().numpy()
+    np.testing.assert_array_equal(f64(got_s), O.grouped_gemm_dx(f64(dC), f64(B), offn, f64(dC2), f64(B2)))
+    np.testing.assert_array_equal(f64(got_1), O.grouped_gemm_dx(f64(dC), f64(B), offn))
+    assert torch.equal(got_s.view(torch.int16), ref_s.view(torch.int16))
+    hg = (torch.randn((R, K), generator=g) * 2).to(torch.bfloat16).to(DEV)
+    hu = torch.randn((R, K), generator=g).to(torch.bfloat16).to(DEV)
+    a_g, a_u = moe.moe_grouped_gemm_dx_swiglu_bwd(dC, B, off, hg, hu)
+    b_g, b_u = moe.moe_grouped_gemm_dx_swiglu_bwd(dC, B, off, hg, hu, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(a_g.view(torch.int16), b_g.view(torch.int16))
+    assert torch.equal(a_u.view(torch.int16), b_u.view(torch.int16))
+    # Gaussian operands: deterministic, and oracle parity
+    dCg = torch.randn((R, N), generator=g).to(torch.bfloat16).to(DEV)
+    Bg = (torch.randn((G, K, N), generator=g) * 0.05).to(torch.bfloat16).to(DEV)
+    x1 = moe.moe_grouped_gemm_dx(dCg, Bg, off, workspace=ws)
+    x2 = moe.moe_grouped_gemm_dx(dCg, Bg, off, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(x1.view(torch.int16), x2.view(torch.int16))
+    check_float("dA split", f64(x1), O.grouped_gemm_dx(f64(dCg), f64(Bg), offn))
+
+
 def test_grouped_gemm_dw_worked_example():
     """The hand-evaluated dW1 example of Appendix H's definition, zero-padded to 64-multiples."""
     import json, os
@@ -330,10 +373,10 @@ def test_swiglu_fwd_bwd():
 # ---------------------------------------------------------------------------------------------
 # whole layer, small configs: every tensor vs the oracle
 # ---------------------------------------------------------------------------------------------
-def _layer_parity(cfg, seed=0, expert_bias=None, log=None, fuse=True, dw_t=False):
+def _layer_parity(cfg, seed=0, expert_bias=None, log=None, fuse=True, dw_t=False, split=True):
     inp = W.make_inputs(cfg, seed, "cpu", expert_bias=expert_bias)
     dinp = {k_: v.to(DEV) for k_, v in inp.items()}
-    lay = L.MoELayer(cfg, dinp, fuse_swiglu_bwd=fuse, dw_transposed=dw_t)
+    lay = L.MoELayer(cfg, dinp, fuse_swiglu_bwd=fuse, dw_transposed=dw_t, split_tail=split)
     for t in lay.buf.values():
         if t.dtype != torch.uint8:
             poison_(t)
@@ -374,6 +417,22 @@ def test_layer_config0_parity(fuse):
     log = {}
     _layer_parity(W.CONFIGS[0], log=log, fuse=fuse)
     _say({k_: f"{v:.2e}" for k_, v in log.items()})
+
+
+def test_layer_split_tail_parity():
+    """The layer with the split tail in both dX products, on a shape whose dX of gate/up has a
+    round and a bit of 256x256 tiles (d=2048: 8 column tiles x ~36 row tiles): oracle parity of
+    every output, and the forward and the weight gradients (not split) bitwise equal to the
+    unsplit layer's."""
+    cfg = W.custom("split_tail", T=4096, d=2048, f=512, E=8, k=2)
+    _say("layer split tail", cfg)
+    lay_s = _layer_parity(cfg, split=True)
+    inp = W.make_inputs(cfg, 0, "cpu")
+    lay = L.MoELayer(cfg, {k_: v.to(DEV) for k_, v in inp.items()}, split_tail=False)
+    lay.step()
+    torch.cuda.synchronize()
+    for key in ("y", "dw_gate", "dw_up", "dw_down", "dy_perm"):
+        assert torch.equal(lay.buf[key].view(torch.uint8), lay_s.buf[key].view(torch.uint8)), key
 
 
 @pytest.mark.parametrize("cfg_id", [0, 2, 3])
