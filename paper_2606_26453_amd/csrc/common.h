@@ -41,9 +41,15 @@ __device__ __forceinline__ u32x4 pack8(const float* f) {
   return v;
 }
 
-// silu(g) = g * sigmoid(g) = g / (1 + exp(-g)), fp32.
-__device__ __forceinline__ float silu_f32(float g) { return g / (1.0f + expf(-g)); }
-__device__ __forceinline__ float sigmoid_f32(float g) { return 1.0f / (1.0f + expf(-g)); }
+// sigmoid(g) = 1 / (1 + exp(-g)) and silu(g) = g * sigmoid(g) in fp32, from the hardware base-2
+// exponential and reciprocal (each within 1 ulp): exp(-g) = 2^(-g * log2(e)).  The results are
+// stored as bf16, whose rounding step is 2^16 times coarser than these errors.  Limits: g -> -inf
+// gives exp -> inf, sigmoid -> 0, silu -> -0; g -> +inf gives sigmoid -> 1, silu -> g.
+__device__ __forceinline__ float sigmoid_f32(float g) {
+  constexpr float LOG2E = 1.4426950408889634f;
+  return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-g * LOG2E));
+}
+__device__ __forceinline__ float silu_f32(float g) { return g * sigmoid_f32(g); }
 
 // SwiGLU backward for one element (the same arithmetic everywhere it is computed):
 // dh_up = d * g * s, dh_gate = d * u * s * (1 + g * (1 - s)), s = sigmoid(g).
