@@ -68,6 +68,8 @@ struct GemmParams {
   int* split_cnt;      // persistent kernels: split the last partial round's tiles (NULL: no split);
   float* split_part;   //   arrival counters (zero at launch) and fp32 partial tiles, one per unit
   int split_max;       //   at most this many contraction pieces per tail tile
+  int split_slots;     //   workgroups resident at once (one-workgroup-per-tile kernels)
+  int split_min_steps; //   contraction steps (of BK) a piece must have at least
 };
 
 typedef int i32x4 __attribute__((ext_vector_type(4)));
@@ -751,17 +753,25 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
   };
 
   // ---------------- tile loop -----------------------------------------------------------------
-  // A persistent kernel given a split workspace runs only the full rounds of tiles this way; the
-  // tiles of the last, partial round are split along the contraction (below).
+  // Given a split workspace, only the full rounds of tiles (a round: one tile per resident
+  // workgroup) run this way; the tiles of the last, partial round are split along the
+  // contraction (below).
   int normal_end = ntiles_all, tail_first = ntiles_all, S = 1;
-  if constexpr (PERSIST) {
+  {
     if (p.split_part != nullptr) {
-      const int slots = (int)gridDim.x;
+      const int slots = PERSIST ? (int)gridDim.x : p.split_slots;
       const int full = (ntiles_all / slots) * slots;
       const int tail = ntiles_all - full;
       if (tail > 0) {
+        // pieces of a tile: as many as the idle slots allow, at most split_max, and each at least
+        // split_min_steps long (short pieces cost more in partial-tile traffic than they save)
+        int64_t clen;
+        if constexpr (KIND == KIND_FWD) clen = p.K;
+        else clen = DUAL ? 2 * p.N : p.N;
+        const int csteps = (int)((clen + BK - 1) / BK);
         int sp = slots / tail;
         if (sp > p.split_max) sp = p.split_max;
+        if (sp > csteps / p.split_min_steps) sp = csteps / p.split_min_steps;
         if (sp > 1) {
           S = sp;
           normal_end = full;
@@ -815,15 +825,18 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
   }
 
   // ---------------- split tail ------------------------------------------------------------------
-  // Unit u (one per workgroup) computes piece q = u % S of tail tile u / S: contraction steps
-  // [q*n/S, (q+1)*n/S).  It stores its fp32 partial tile to the workspace and counts itself in; the
-  // last of the S pieces to arrive adds the S partials in piece order (a fixed order: the result
-  // does not depend on which piece arrives last) and runs the tile's epilogue.
-  if constexpr (PERSIST) {
+  // Unit u (one per workgroup: a persistent workgroup after its full rounds, else one of the
+  // workgroups past the full rounds' tiles, which the dispatcher starts as the last round's CUs
+  // free) computes piece q = u % S of tail tile u / S: contraction steps [q*n/S, (q+1)*n/S).  It
+  // stores its fp32 partial tile to the workspace and counts itself in; the last of the S pieces
+  // to arrive adds the S partials in piece order (a fixed order: the result does not depend on
+  // which piece arrives last) and runs the tile's epilogue.  Nothing waits for another workgroup.
+  {
     __shared__ int s_arrived;
     const int units = (ntiles_all - tail_first) * S;
-    if (S > 1 && (int)blockIdx.x < units) {
-      const int u = blockIdx.x, tl = u / S, q = u - tl * S;
+    const int u = PERSIST ? (int)blockIdx.x : (int)blockIdx.x - tail_first;
+    if (S > 1 && u >= 0 && u < units) {
+      const int tl = u / S, q = u - tl * S;
       __syncthreads();   // the ring and the staging area are free (the last normal tile is done)
       map_tile(tail_first + tl, g, mt, nt, row_lo, row_hi);
       setup(g, mt, nt, row_lo, row_hi);
@@ -906,10 +919,16 @@ template <int KIND> struct Cfg {
   static constexpr bool PERSIST = (KIND == KIND_DX);
 };
 
+// Split-tail workspace: 256 arrival counters, then one fp32 256x256 partial tile per unit (at most
+// one unit per resident workgroup, i.e. per CU, which attach_split bounds by 256).
+constexpr int SPLIT_UNITS = 256, SPLIT_MAX = 8, SPLIT_MIN_STEPS = 64;
+constexpr size_t SPLIT_CNT_BYTES = SPLIT_UNITS * sizeof(int);
+constexpr size_t SPLIT_BYTES = SPLIT_CNT_BYTES + (size_t)SPLIT_UNITS * 256 * TN * sizeof(float);
+
 template <int KIND, bool DUAL, bool ACT, bool OUT16 = false>
 moe_status launch(const GemmParams& p, int64_t tiles_bound, hipStream_t stream, const char* name) {
   if (tiles_bound == 0) return MOE_SUCCESS;
-  if (tiles_bound >= ((int64_t)1 << 31)) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: too many tiles", name);
+  if (tiles_bound >= ((int64_t)1 << 31) - SPLIT_UNITS) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: too many tiles", name);
   using C = Cfg<KIND>;
   // persistent grid: one workgroup per CU slot (a multiple of 8, one share per XCD), or one per
   // tile when there are fewer tiles; otherwise one workgroup per (bound on the) tile count
@@ -918,6 +937,8 @@ moe_status launch(const GemmParams& p, int64_t tiles_bound, hipStream_t stream, 
     unsigned slots = (unsigned)device_cu_count() * C::WPE;
     if (slots > 8) slots &= ~7u;
     if (grid > slots) grid = slots;
+  } else if (p.split_part != nullptr) {
+    grid += SPLIT_UNITS;   // the split units run past the full rounds' tiles (idle ones exit)
   }
   grouped_gemm_kernel<KIND, DUAL, ACT, C::TM, C::WM, C::WN, C::NS, C::PP, C::WPE, C::PERSIST, OUT16>
       <<<grid, 64 * C::WM * C::WN, 0, stream>>>(p);
@@ -926,11 +947,6 @@ moe_status launch(const GemmParams& p, int64_t tiles_bound, hipStream_t stream, 
 
 bool bad_ptr(const void* q) { return q != nullptr && !aligned16(q); }
 
-// Split-tail workspace: 256 arrival counters, then one fp32 256x256 partial tile per unit (at most
-// one unit per persistent workgroup, i.e. per CU slot, which device_cu_count bounds by 256 here).
-constexpr int SPLIT_UNITS = 256, SPLIT_MAX = 8;
-constexpr size_t SPLIT_CNT_BYTES = SPLIT_UNITS * sizeof(int);
-constexpr size_t SPLIT_BYTES = SPLIT_CNT_BYTES + (size_t)SPLIT_UNITS * 256 * TN * sizeof(float);
 
 __global__ void zero_i32_kernel(int* p, int n) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
@@ -942,10 +958,13 @@ moe_status attach_split(GemmParams& p, void* ws, size_t ws_bytes, const char* fn
   if (ws == nullptr) return MOE_SUCCESS;
   if (ws_bytes < SPLIT_BYTES || !aligned16(ws))
     return fail(MOE_ERROR_WORKSPACE, "%s: a 16-byte aligned workspace of %zu bytes is needed", fn, SPLIT_BYTES);
-  if (device_cu_count() > SPLIT_UNITS) return MOE_SUCCESS;   // more slots than partial tiles: no split
+  const int cus = device_cu_count();
+  if (cus > SPLIT_UNITS) return MOE_SUCCESS;   // more slots than partial tiles: no split
   p.split_cnt = static_cast<int*>(ws);
+  p.split_slots = cus;   // one workgroup per CU (the LDS ring admits no second)
   p.split_part = reinterpret_cast<float*>(static_cast<char*>(ws) + SPLIT_CNT_BYTES);
   p.split_max = SPLIT_MAX;
+  p.split_min_steps = SPLIT_MIN_STEPS;
   zero_i32_kernel<<<1, SPLIT_UNITS, 0, stream>>>(p.split_cnt, SPLIT_UNITS);
   return check_launch(fn);
 }
@@ -955,10 +974,11 @@ moe_status attach_split(GemmParams& p, void* ws, size_t ws_bytes, const char* fn
 
 using namespace moe;
 
-extern "C" moe_status moe_grouped_gemm_fwd(const moe_bf16* A, const moe_bf16* B, const moe_bf16* B2,
-                                           const int32_t* offsets, int32_t G, int64_t R, int64_t K,
-                                           int64_t N, moe_bf16* C, moe_bf16* C2, moe_bf16* act,
-                                           hipStream_t stream) {
+namespace moe {
+namespace {
+moe_status grouped_gemm_fwd_impl(const moe_bf16* A, const moe_bf16* B, const moe_bf16* B2, const int32_t* offsets,
+                                 int32_t G, int64_t R, int64_t K, int64_t N, moe_bf16* C, moe_bf16* C2,
+                                 moe_bf16* act, void* ws, size_t ws_bytes, hipStream_t stream) {
   if (G < 1 || G > 256) return fail(MOE_ERROR_NOT_SUPPORTED, "moe_grouped_gemm_fwd: need 1 <= G <= 256");
   if (R < 0 || K <= 0 || N <= 0) return fail(MOE_ERROR_INVALID_VALUE, "moe_grouped_gemm_fwd: bad size");
   if (K % 64 || N % 64) return fail(MOE_ERROR_NOT_SUPPORTED, "moe_grouped_gemm_fwd: K and N must be multiples of 64");
@@ -979,9 +999,28 @@ extern "C" moe_status moe_grouped_gemm_fwd(const moe_bf16* A, const moe_bf16* B,
   const int cols_per_tile = B2 ? TN / 2 : TN;
   p.n_tiles = (int)((N + cols_per_tile - 1) / cols_per_tile);
   const int64_t tiles = (int64_t)p.mt_bound * p.n_tiles;   // upper bound; exact count on device
+  const moe_status st = attach_split(p, ws, ws_bytes, "moe_grouped_gemm_fwd", stream);
+  if (st != MOE_SUCCESS) return st;
   if (B2 && act) return launch<KIND_FWD, true, true>(p, tiles, stream, "grouped_gemm_fwd(dual,swiglu)");
   if (B2) return launch<KIND_FWD, true, false>(p, tiles, stream, "grouped_gemm_fwd(dual)");
   return launch<KIND_FWD, false, false>(p, tiles, stream, "grouped_gemm_fwd");
+}
+}  // namespace
+}  // namespace moe
+
+extern "C" moe_status moe_grouped_gemm_fwd(const moe_bf16* A, const moe_bf16* B, const moe_bf16* B2,
+                                           const int32_t* offsets, int32_t G, int64_t R, int64_t K,
+                                           int64_t N, moe_bf16* C, moe_bf16* C2, moe_bf16* act,
+                                           hipStream_t stream) {
+  return grouped_gemm_fwd_impl(A, B, B2, offsets, G, R, K, N, C, C2, act, nullptr, 0, stream);
+}
+
+extern "C" moe_status moe_grouped_gemm_fwd_split(const moe_bf16* A, const moe_bf16* B, const moe_bf16* B2,
+                                                 const int32_t* offsets, int32_t G, int64_t R, int64_t K,
+                                                 int64_t N, moe_bf16* C, moe_bf16* C2, moe_bf16* act,
+                                                 void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!workspace) return fail(MOE_ERROR_WORKSPACE, "moe_grouped_gemm_fwd_split: workspace is NULL");
+  return grouped_gemm_fwd_impl(A, B, B2, offsets, G, R, K, N, C, C2, act, workspace, workspace_bytes, stream);
 }
 
 namespace moe {

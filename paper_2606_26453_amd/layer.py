@@ -48,8 +48,8 @@ class MoELayer(_Traced):
                  router: bool = False, aux_alpha: float = 0.0, dw_transposed: bool = False,
                  concurrent: bool = False, split_tail: bool = True):
         self.cfg = cfg
-        # split_tail: the persistent dX products split their last partial round of tiles along the
-        # contraction (a workspace of fp32 partial tiles)
+        # split_tail: the fwd and dX products on the main stream split their last partial round of
+        # tiles along the contraction (a workspace of fp32 partial tiles)
         self.split_ws = moe.split_workspace(inputs["x"].device) if split_tail else None
         self.fuse = fuse_swiglu_bwd
         self.dw_t = dw_transposed
@@ -138,9 +138,9 @@ class MoELayer(_Traced):
             run("router_aux_loss", moe.moe_router_aux_loss, logits, b["offsets"], k, self.aux_alpha,
                 loss=b["aux_loss"], workspace=b["aux_ws"], stream=stream)
         run("fwd_gate_up", moe.moe_grouped_gemm_fwd, b["x_perm"], i["w_gate"], b["offsets"], i["w_up"],
-            b["h_gate"], b["h_up"], b["act"], want_act=True, stream=stream)
+            b["h_gate"], b["h_up"], b["act"], want_act=True, stream=stream, workspace=self.split_ws)
         run("fwd_down", moe.moe_grouped_gemm_fwd, b["act"], i["w_down"], b["offsets"], C=b["y_perm"],
-            stream=stream)
+            stream=stream, workspace=self.split_ws)
         self._join(main, side)
         run("combine", moe.moe_unpermute_combine, b["y_perm"], b["topk_w"], b["row_of_slot"], k, add=add,
             y=b["y"], stream=stream)

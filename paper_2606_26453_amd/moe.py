@@ -37,6 +37,8 @@ _SIG = {
     "moe_route_permute": (ctypes.c_int, [_P, _P, _I64, _I64, _I32, _I32, _I32, _P, _P, _P, _P, _P,
                                          _P, _P, ctypes.c_size_t, _P]),
     "moe_grouped_gemm_fwd": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P, _P]),
+    "moe_grouped_gemm_fwd_split": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P, _P,
+                                                  ctypes.c_size_t, _P]),
     "moe_swiglu": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _P]),
     "moe_swiglu_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _I64, _I64, _P]),
     "moe_unpermute_combine": (ctypes.c_int, [_P, _P, _P, _P, _I64, _I64, _I32, _P, _P]),
@@ -148,7 +150,7 @@ def moe_route_permute(logits, x, k, normalize_topk=True, topk_idx=None, topk_w=N
 
 
 def moe_grouped_gemm_fwd(A, B, offsets, B2=None, C=None, C2=None, act=None, want_act=False,
-                         stream=None):
+                         stream=None, workspace=None):
     R, K = A.shape
     G, K2, N = B.shape
     if K2 != K:
@@ -165,9 +167,15 @@ def moe_grouped_gemm_fwd(A, B, offsets, B2=None, C=None, C2=None, act=None, want
         act = torch.empty((R, N), dtype=torch.bfloat16, device=dev)
     for t, n in ((C, "C"), (C2, "C2"), (act, "act")):
         _need(t, torch.bfloat16, (R, N), n)
-    st = lib().moe_grouped_gemm_fwd(_ptr(A), _ptr(B), _ptr(B2), _ptr(offsets), G, R, K, N, _ptr(C),
-                                    _ptr(C2), _ptr(act), _stream(stream))
-    _check("moe_grouped_gemm_fwd", st)
+    if workspace is None:
+        st = lib().moe_grouped_gemm_fwd(_ptr(A), _ptr(B), _ptr(B2), _ptr(offsets), G, R, K, N, _ptr(C),
+                                        _ptr(C2), _ptr(act), _stream(stream))
+        _check("moe_grouped_gemm_fwd", st)
+    else:
+        st = lib().moe_grouped_gemm_fwd_split(_ptr(A), _ptr(B), _ptr(B2), _ptr(offsets), G, R, K, N, _ptr(C),
+                                              _ptr(C2), _ptr(act), _ptr(workspace), workspace.numel(),
+                                              _stream(stream))
+        _check("moe_grouped_gemm_fwd_split", st)
     return C, C2, act
 
 

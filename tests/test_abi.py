@@ -96,6 +96,9 @@ def test_split_rejects():
     dxs = lambda ws=FAKE, n=need: L.moe_grouped_gemm_dx_swiglu_bwd_split(
         FAKE, FAKE, FAKE, 4, 100, 128, 128, FAKE, FAKE, FAKE, FAKE, ws, n, None)
     assert dxs(ws=None) == 3 and dxs(n=16) == 3
+    fwd = lambda ws=FAKE, n=need, N=128: L.moe_grouped_gemm_fwd_split(
+        FAKE, FAKE, None, FAKE, 4, 100, 128, N, FAKE, None, None, ws, n, None)
+    assert fwd(ws=None) == 3 and fwd(n=need // 2) == 3 and fwd(N=96) == 2
 
 
 def test_dw_t_and_transpose_rejects():
