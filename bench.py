@@ -73,6 +73,8 @@ def _args():
     ap.add_argument("--aux-alpha", type=float, default=0.01, help="load-balancing loss weight with --router")
     ap.add_argument("--dw-transposed", action="store_true",
                     help="weight gradients from contraction-major copies of their operands")
+    ap.add_argument("--gather-fused", action="store_true",
+                    help="gate/up product reads x through token_of_row; X_perm is gathered in the backward")
     ap.add_argument("--no-split-tail", action="store_true",
                     help="persistent dX products do not split their last partial round of tiles")
     ap.add_argument("--concurrent", action="store_true",
@@ -162,7 +164,8 @@ def main():
     else:
         inp = W.make_inputs(cfg, a.seed, dev)
         lay = L.MoELayer(cfg, inp, router=a.router, aux_alpha=a.aux_alpha if a.router else 0.0,
-                         dw_transposed=a.dw_transposed, concurrent=a.concurrent, split_tail=not a.no_split_tail)
+                         dw_transposed=a.dw_transposed, concurrent=a.concurrent, split_tail=not a.no_split_tail,
+                         gather_fused=a.gather_fused)
     torch.cuda.synchronize()
     t_gen = time.perf_counter() - t_gen
 

@@ -89,6 +89,17 @@ moe_status moe_route_permute(const float* logits, const moe_bf16* x, int64_t T, 
                              int32_t* token_of_row, moe_bf16* x_perm, void* workspace,
                              size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * A4 alone: x_perm[row_of_slot[t*k + j], :] = x[t, :] for t < T, j < k (a bit copy; the gather of
+ * moe_route_permute, for a caller that routed without it, e.g. when the forward product gathered
+ * its rows itself and only the weight gradient needs X_perm).  x [T,d], x_perm [T*k,d] bf16;
+ * row_of_slot [T*k] int32 as moe_route_permute returns it (a permutation of 0..T*k-1; not
+ * checked).  Errors: d not a positive multiple of 64 -> NOT_SUPPORTED; NULL or misaligned
+ * pointers -> INVALID_VALUE.  T = 0 is a no-op.
+ */
+moe_status moe_gather_rows(const moe_bf16* x, int64_t T, int64_t d, int32_t k, const int32_t* row_of_slot,
+                           moe_bf16* x_perm, hipStream_t stream);
+
 /* ------------------------------------------------------------------------------------------ */
 /* B, D: forward grouped GEMM (+ fused SwiGLU)                                                 */
 /* ------------------------------------------------------------------------------------------ */
@@ -201,6 +212,20 @@ size_t moe_grouped_gemm_split_workspace_bytes(void);
  * hardware dispatcher starts as the last full round's CUs free up.  The fused SwiGLU, when
  * requested, is computed from the summed tile exactly as in the unsplit kernel.
  */
+/*
+ * The gate/up product with the gather folded into its A operand (steps A4 + B): rows are read
+ * straight from X through a row list instead of from the packed, expert-ordered X_perm.  For rows r
+ * of group g: C[r, :] = X[row_src[r], :] . B[g] (and C2, act as in moe_grouped_gemm_fwd); with
+ * row_src = token_of_row of moe_route_permute this equals moe_grouped_gemm_fwd on X_perm bit for
+ * bit (same data, same arithmetic).  X [T,K] bf16 (T*K*2 < 2 GiB); row_src [R] int32, values in
+ * [0,T) (not checked on the host: a row index past the source reads zeros); everything else as
+ * moe_grouped_gemm_fwd.  workspace: NULL, or a split workspace as for moe_grouped_gemm_fwd_split.
+ */
+moe_status moe_grouped_gemm_fwd_gather(const moe_bf16* X, int64_t T, const int32_t* row_src, const moe_bf16* B,
+                                       const moe_bf16* B2, const int32_t* offsets, int32_t G, int64_t R,
+                                       int64_t K, int64_t N, moe_bf16* C, moe_bf16* C2, moe_bf16* act,
+                                       void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 moe_status moe_grouped_gemm_fwd_split(const moe_bf16* A, const moe_bf16* B, const moe_bf16* B2,
                                       const int32_t* offsets, int32_t G, int64_t R, int64_t K, int64_t N,
                                       moe_bf16* C, moe_bf16* C2, moe_bf16* act, void* workspace,

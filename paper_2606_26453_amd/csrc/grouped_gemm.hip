@@ -70,6 +70,8 @@ struct GemmParams {
   int split_max;       //   at most this many contraction pieces per tail tile
   int split_slots;     //   workgroups resident at once (one-workgroup-per-tile kernels)
   int split_min_steps; //   contraction steps (of BK) a piece must have at least
+  const int32_t* gather;   // FWD: row r of A is row gather[r] of a [gather_rows, K] source (NULL: A itself)
+  int64_t gather_rows;
 };
 
 typedef int i32x4 __attribute__((ext_vector_type(4)));
@@ -146,7 +148,7 @@ __device__ __forceinline__ void band_order(int id, int mtiles, int ntiles, int& 
 // workgroup loops over tiles (grid = CU slots) instead of computing one tile (grid = tiles).  OUT16:
 // dW results are rounded to bf16 (as the paper's kernel stores them) instead of stored as fp32.
 template <int KIND, bool DUAL, bool ACT, int TM, int WAVES_M, int WAVES_N, int NSTAGE, bool PINGPONG, int WPE,
-          bool PERSIST, bool OUT16>
+          bool PERSIST, bool OUT16, bool GATHER>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kernel(GemmParams p) {
   constexpr int NWAVE = WAVES_M * WAVES_N;
   constexpr int OPND_M = TM * BK * 2;         // bytes of the M-side tile of one stage
@@ -308,14 +310,28 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
     } else if constexpr (!M_T) {
       m_ld = (KIND == KIND_FWD) ? p.K : p.N;
       const int64_t rows_valid = row_hi - row_lo;   // > 0
-      m_src = reinterpret_cast<const char*>(p.a + row_lo * m_ld);
-      if constexpr (KIND == KIND_DX && DUAL) m_src2 = reinterpret_cast<const char*>(p.a2 + row_lo * m_ld);
+      if constexpr (GATHER) {
+        // gathered rows: each lane's row of the source, read through the row list (the rows of
+        // a ragged group's end clamp to its last row, as below)
+        m_src = reinterpret_cast<const char*>(p.a);
 #pragma unroll
-      for (int i = 0; i < DPW_M; ++i) {
-        int64_t r = 16 * (DPW_M * wave + i) + (lane >> 2);
-        if (r > rows_valid - 1) r = rows_valid - 1;
-        const int c = (lane & 3) ^ swz_d(lane >> 2);
-        m_voff[i] = (int)((r * m_ld + 8 * c) * 2);
+        for (int i = 0; i < DPW_M; ++i) {
+          int64_t r = 16 * (DPW_M * wave + i) + (lane >> 2);
+          if (r > rows_valid - 1) r = rows_valid - 1;
+          const int64_t src = p.gather[row_lo + r];
+          const int c = (lane & 3) ^ swz_d(lane >> 2);
+          m_voff[i] = (int)((src * m_ld + 8 * c) * 2);
+        }
+      } else {
+        m_src = reinterpret_cast<const char*>(p.a + row_lo * m_ld);
+        if constexpr (KIND == KIND_DX && DUAL) m_src2 = reinterpret_cast<const char*>(p.a2 + row_lo * m_ld);
+#pragma unroll
+        for (int i = 0; i < DPW_M; ++i) {
+          int64_t r = 16 * (DPW_M * wave + i) + (lane >> 2);
+          if (r > rows_valid - 1) r = rows_valid - 1;
+          const int c = (lane & 3) ^ swz_d(lane >> 2);
+          m_voff[i] = (int)((r * m_ld + 8 * c) * 2);
+        }
       }
     } else {
       m_ld = p.K;
@@ -404,6 +420,10 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
       int64_t cc = c0;
       if constexpr (KIND == KIND_DX && DUAL) {
         if (c0 >= p.N) { base = m_src2; cc = c0 - p.N; }
+      }
+      if constexpr (GATHER) {
+        // gathered rows: the window ends with the source, so a row index past it reads zeros
+        return make_rsrc(base + cc * 2, (p.gather_rows * m_ld - cc) * 2);
       }
       return make_rsrc(base + cc * 2, (int64_t)0x7fffffff);
     } else {
@@ -925,7 +945,7 @@ constexpr int SPLIT_UNITS = 256, SPLIT_MAX = 8, SPLIT_MIN_STEPS = 64;
 constexpr size_t SPLIT_CNT_BYTES = SPLIT_UNITS * sizeof(int);
 constexpr size_t SPLIT_BYTES = SPLIT_CNT_BYTES + (size_t)SPLIT_UNITS * 256 * TN * sizeof(float);
 
-template <int KIND, bool DUAL, bool ACT, bool OUT16 = false>
+template <int KIND, bool DUAL, bool ACT, bool OUT16 = false, bool GATHER = false>
 moe_status launch(const GemmParams& p, int64_t tiles_bound, hipStream_t stream, const char* name) {
   if (tiles_bound == 0) return MOE_SUCCESS;
   if (tiles_bound >= ((int64_t)1 << 31) - SPLIT_UNITS) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: too many tiles", name);
@@ -940,7 +960,8 @@ moe_status launch(const GemmParams& p, int64_t tiles_bound, hipStream_t stream, 
   } else if (p.split_part != nullptr) {
     grid += SPLIT_UNITS;   // the split units run past the full rounds' tiles (idle ones exit)
   }
-  grouped_gemm_kernel<KIND, DUAL, ACT, C::TM, C::WM, C::WN, C::NS, C::PP, C::WPE, C::PERSIST, OUT16>
+  static_assert(!GATHER || KIND == KIND_FWD, "gathered rows feed the forward product only");
+  grouped_gemm_kernel<KIND, DUAL, ACT, C::TM, C::WM, C::WN, C::NS, C::PP, C::WPE, C::PERSIST, OUT16, GATHER>
       <<<grid, 64 * C::WM * C::WN, 0, stream>>>(p);
   return check_launch(name);
 }
@@ -978,7 +999,8 @@ namespace moe {
 namespace {
 moe_status grouped_gemm_fwd_impl(const moe_bf16* A, const moe_bf16* B, const moe_bf16* B2, const int32_t* offsets,
                                  int32_t G, int64_t R, int64_t K, int64_t N, moe_bf16* C, moe_bf16* C2,
-                                 moe_bf16* act, void* ws, size_t ws_bytes, hipStream_t stream) {
+                                 moe_bf16* act, void* ws, size_t ws_bytes, hipStream_t stream,
+                                 const int32_t* gather = nullptr, int64_t gather_rows = 0) {
   if (G < 1 || G > 256) return fail(MOE_ERROR_NOT_SUPPORTED, "moe_grouped_gemm_fwd: need 1 <= G <= 256");
   if (R < 0 || K <= 0 || N <= 0) return fail(MOE_ERROR_INVALID_VALUE, "moe_grouped_gemm_fwd: bad size");
   if (K % 64 || N % 64) return fail(MOE_ERROR_NOT_SUPPORTED, "moe_grouped_gemm_fwd: K and N must be multiples of 64");
@@ -994,6 +1016,7 @@ moe_status grouped_gemm_fwd_impl(const moe_bf16* A, const moe_bf16* B, const moe
   GemmParams p{};
   p.a = A; p.b = B; p.b2 = B2; p.offsets = offsets; p.out = C; p.out2 = C2; p.act = act;
   p.G = G; p.R = R; p.K = K; p.N = N;
+  p.gather = gather; p.gather_rows = gather_rows;
   constexpr int TM = Cfg<KIND_FWD>::TM;
   p.mt_bound = (int)((R + TM - 1) / TM + G);
   const int cols_per_tile = B2 ? TN / 2 : TN;
@@ -1001,6 +1024,11 @@ moe_status grouped_gemm_fwd_impl(const moe_bf16* A, const moe_bf16* B, const moe
   const int64_t tiles = (int64_t)p.mt_bound * p.n_tiles;   // upper bound; exact count on device
   const moe_status st = attach_split(p, ws, ws_bytes, "moe_grouped_gemm_fwd", stream);
   if (st != MOE_SUCCESS) return st;
+  if (gather) {
+    if (B2 && act) return launch<KIND_FWD, true, true, false, true>(p, tiles, stream, "grouped_gemm_fwd(gather,dual,swiglu)");
+    if (B2) return launch<KIND_FWD, true, false, false, true>(p, tiles, stream, "grouped_gemm_fwd(gather,dual)");
+    return launch<KIND_FWD, false, false, false, true>(p, tiles, stream, "grouped_gemm_fwd(gather)");
+  }
   if (B2 && act) return launch<KIND_FWD, true, true>(p, tiles, stream, "grouped_gemm_fwd(dual,swiglu)");
   if (B2) return launch<KIND_FWD, true, false>(p, tiles, stream, "grouped_gemm_fwd(dual)");
   return launch<KIND_FWD, false, false>(p, tiles, stream, "grouped_gemm_fwd");
@@ -1013,6 +1041,20 @@ extern "C" moe_status moe_grouped_gemm_fwd(const moe_bf16* A, const moe_bf16* B,
                                            int64_t N, moe_bf16* C, moe_bf16* C2, moe_bf16* act,
                                            hipStream_t stream) {
   return grouped_gemm_fwd_impl(A, B, B2, offsets, G, R, K, N, C, C2, act, nullptr, 0, stream);
+}
+
+extern "C" moe_status moe_grouped_gemm_fwd_gather(const moe_bf16* X, int64_t T, const int32_t* row_src,
+                                                  const moe_bf16* B, const moe_bf16* B2, const int32_t* offsets,
+                                                  int32_t G, int64_t R, int64_t K, int64_t N, moe_bf16* C,
+                                                  moe_bf16* C2, moe_bf16* act, void* workspace,
+                                                  size_t workspace_bytes, hipStream_t stream) {
+  const char* fn = "moe_grouped_gemm_fwd_gather";
+  if (T < 0) return fail(MOE_ERROR_INVALID_VALUE, "%s: bad size", fn);
+  if (R > 0 && (!row_src || T == 0)) return fail(MOE_ERROR_INVALID_VALUE, "%s: row_src is NULL or T == 0", fn);
+  if (T * K * 2 >= ((int64_t)1 << 31))
+    return fail(MOE_ERROR_NOT_SUPPORTED, "%s: the source X must be < 2 GiB", fn);
+  return grouped_gemm_fwd_impl(X, B, B2, offsets, G, R, K, N, C, C2, act, workspace, workspace_bytes, stream,
+                               row_src, T);
 }
 
 extern "C" moe_status moe_grouped_gemm_fwd_split(const moe_bf16* A, const moe_bf16* B, const moe_bf16* B2,

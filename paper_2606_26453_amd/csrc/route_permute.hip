@@ -278,3 +278,17 @@ extern "C" moe_status moe_route_permute(const float* logits, const moe_bf16* x, 
   }
   return MOE_SUCCESS;
 }
+
+extern "C" moe_status moe_gather_rows(const moe_bf16* x, int64_t T, int64_t d, int32_t k,
+                                      const int32_t* row_of_slot, moe_bf16* x_perm, hipStream_t stream) {
+  const char* fn = "moe_gather_rows";
+  if (T < 0 || k < 1) return fail(MOE_ERROR_INVALID_VALUE, "%s: need T >= 0 and k >= 1", fn);
+  if (d <= 0 || d % 64 != 0) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: d must be a positive multiple of 64", fn);
+  if (T * (int64_t)k >= ((int64_t)1 << 31)) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: T*k >= 2^31", fn);
+  if (T == 0) return MOE_SUCCESS;
+  if (!x || !row_of_slot || !x_perm) return fail(MOE_ERROR_INVALID_VALUE, "%s: NULL pointer", fn);
+  if (!aligned16(x) || !aligned16(x_perm)) return fail(MOE_ERROR_INVALID_VALUE, "%s: x/x_perm not 16-byte aligned", fn);
+  gather_kernel<4><<<(unsigned)((T + 3) / 4), 256, 0, stream>>>(
+      reinterpret_cast<const u32x4*>(x), T, d / 8, k, row_of_slot, reinterpret_cast<u32x4*>(x_perm));
+  return check_launch("gather_kernel");
+}

@@ -46,8 +46,12 @@ class MoELayer(_Traced):
 
     def __init__(self, cfg, inputs: dict, normalize_topk: bool = True, fuse_swiglu_bwd: bool = True,
                  router: bool = False, aux_alpha: float = 0.0, dw_transposed: bool = False,
-                 concurrent: bool = False, split_tail: bool = True):
+                 concurrent: bool = False, split_tail: bool = True, gather_fused: bool = False):
         self.cfg = cfg
+        # gather_fused: the gate/up product reads its rows straight from x through token_of_row
+        # (moe_grouped_gemm_fwd_gather); X_perm is then gathered only in the backward, for dW_gate
+        # and dW_up (moe_gather_rows), so a forward alone never writes it
+        self.gather_fused = gather_fused
         # split_tail: the fwd and dX products on the main stream split their last partial round of
         # tiles along the contraction (a workspace of fp32 partial tiles)
         self.split_ws = moe.split_workspace(inputs["x"].device) if split_tail else None
@@ -131,14 +135,20 @@ class MoELayer(_Traced):
             logits = b["logits"]
             run("router_logits", moe.moe_router_logits, i["x"], i["wr"], i.get("router_bias"), logits=logits,
                 stream=stream)
-        run("route_permute", moe.moe_route_permute, logits, i["x"], k, self.normalize, b["topk_idx"],
-            b["topk_w"], b["offsets"], b["row_of_slot"], b["token_of_row"], b["x_perm"], b["workspace"],
-            stream=stream)
+        gf = self.gather_fused
+        run("route_permute", moe.moe_route_permute, logits, None if gf else i["x"], k, self.normalize,
+            b["topk_idx"], b["topk_w"], b["offsets"], b["row_of_slot"], b["token_of_row"],
+            None if gf else b["x_perm"], b["workspace"], stream=stream)
         if self.router and self.aux_alpha:
             run("router_aux_loss", moe.moe_router_aux_loss, logits, b["offsets"], k, self.aux_alpha,
                 loss=b["aux_loss"], workspace=b["aux_ws"], stream=stream)
-        run("fwd_gate_up", moe.moe_grouped_gemm_fwd, b["x_perm"], i["w_gate"], b["offsets"], i["w_up"],
-            b["h_gate"], b["h_up"], b["act"], want_act=True, stream=stream, workspace=self.split_ws)
+        if gf:
+            run("fwd_gate_up", moe.moe_grouped_gemm_fwd_gather, i["x"], b["token_of_row"], i["w_gate"],
+                b["offsets"], i["w_up"], b["h_gate"], b["h_up"], b["act"], want_act=True, stream=stream,
+                workspace=self.split_ws)
+        else:
+            run("fwd_gate_up", moe.moe_grouped_gemm_fwd, b["x_perm"], i["w_gate"], b["offsets"], i["w_up"],
+                b["h_gate"], b["h_up"], b["act"], want_act=True, stream=stream, workspace=self.split_ws)
         run("fwd_down", moe.moe_grouped_gemm_fwd, b["act"], i["w_down"], b["offsets"], C=b["y_perm"],
             stream=stream, workspace=self.split_ws)
         self._join(main, side)
@@ -151,6 +161,8 @@ class MoELayer(_Traced):
         main, side = self._streams(stream)
         stream = main
         self._join(side, main)
+        if self.gather_fused:             # X_perm for dW_gate/dW_up (the forward read x directly)
+            run("gather_x", moe.moe_gather_rows, i["x"], b["row_of_slot"], k, b["x_perm"], stream=side)
         dx_add = None
         if self.shared:                   # needs dY and the shared forward only
             wg, wu, wd = self.w_sh
@@ -231,7 +243,9 @@ class MoELayer(_Traced):
         T, d, f, k, E = c.T, c.d, c.f, c.k, c.E
         R = T * k
         w = {
-            "route_permute": ("bytes", T * E * 4 + T * k * 8 + R * 8 + T * d * 2 + R * d * 2),
+            "route_permute": ("bytes", T * E * 4 + T * k * 8 + R * 8
+                              + (0 if self.gather_fused else T * d * 2 + R * d * 2)),
+            "gather_x": ("bytes", T * d * 2 + R * d * 2 + R * 4),
             "fwd_gate_up": ("flops", 4 * R * d * f), "fwd_down": ("flops", 2 * R * f * d),
             "combine": ("bytes", R * d * 2 + T * d * 2 + T * k * 8 + (T * d * 2 if self.shared else 0)),
             "combine_bwd": ("bytes", T * d * 2 + 2 * R * d * 2 + T * k * 12),

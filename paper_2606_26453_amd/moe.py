@@ -39,6 +39,9 @@ _SIG = {
     "moe_grouped_gemm_fwd": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P, _P]),
     "moe_grouped_gemm_fwd_split": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P, _P,
                                                   ctypes.c_size_t, _P]),
+    "moe_grouped_gemm_fwd_gather": (ctypes.c_int, [_P, _I64, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P,
+                                                   _P, ctypes.c_size_t, _P]),
+    "moe_gather_rows": (ctypes.c_int, [_P, _I64, _I64, _I32, _P, _P, _P]),
     "moe_swiglu": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _P]),
     "moe_swiglu_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _I64, _I64, _P]),
     "moe_unpermute_combine": (ctypes.c_int, [_P, _P, _P, _P, _I64, _I64, _I32, _P, _P]),
@@ -177,6 +180,46 @@ def moe_grouped_gemm_fwd(A, B, offsets, B2=None, C=None, C2=None, act=None, want
                                               _stream(stream))
         _check("moe_grouped_gemm_fwd_split", st)
     return C, C2, act
+
+
+def moe_grouped_gemm_fwd_gather(X, row_src, B, offsets, B2=None, C=None, C2=None, act=None, want_act=False,
+                                stream=None, workspace=None):
+    """moe_grouped_gemm_fwd on the rows X[row_src[r]] (the gather folded into the product)."""
+    T, K = X.shape
+    (R,) = row_src.shape
+    G, K2, N = B.shape
+    if K2 != K:
+        raise ValueError("X and B disagree on K")
+    _need(X, torch.bfloat16, (T, K), "X")
+    _need(row_src, torch.int32, (R,), "row_src")
+    _need(B, torch.bfloat16, (G, K, N), "B")
+    _need(B2, torch.bfloat16, (G, K, N), "B2")
+    _need(offsets, torch.int32, (G + 1,), "offsets")
+    dev = X.device
+    C = torch.empty((R, N), dtype=torch.bfloat16, device=dev) if C is None else C
+    if B2 is not None and C2 is None:
+        C2 = torch.empty((R, N), dtype=torch.bfloat16, device=dev)
+    if want_act and act is None:
+        act = torch.empty((R, N), dtype=torch.bfloat16, device=dev)
+    for t, n in ((C, "C"), (C2, "C2"), (act, "act")):
+        _need(t, torch.bfloat16, (R, N), n)
+    st = lib().moe_grouped_gemm_fwd_gather(_ptr(X), T, _ptr(row_src), _ptr(B), _ptr(B2), _ptr(offsets), G, R, K, N,
+                                           _ptr(C), _ptr(C2), _ptr(act), _ptr(workspace),
+                                           0 if workspace is None else workspace.numel(), _stream(stream))
+    _check("moe_grouped_gemm_fwd_gather", st)
+    return C, C2, act
+
+
+def moe_gather_rows(x, row_of_slot, k, x_perm=None, stream=None):
+    """x_perm[row_of_slot[t*k + j]] = x[t] (the gather step alone)."""
+    T, d = x.shape
+    _need(x, torch.bfloat16, (T, d), "x")
+    _need(row_of_slot, torch.int32, (T * k,), "row_of_slot")
+    x_perm = torch.empty((T * k, d), dtype=torch.bfloat16, device=x.device) if x_perm is None else x_perm
+    _need(x_perm, torch.bfloat16, (T * k, d), "x_perm")
+    _check("moe_gather_rows", lib().moe_gather_rows(_ptr(x), T, d, k, _ptr(row_of_slot), _ptr(x_perm),
+                                                    _stream(stream)))
+    return x_perm
 
 
 def moe_swiglu(h_gate, h_up, act=None, stream=None):

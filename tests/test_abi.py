@@ -101,6 +101,17 @@ def test_split_rejects():
     assert fwd(ws=None) == 3 and fwd(n=need // 2) == 3 and fwd(N=96) == 2
 
 
+def test_gather_rejects():
+    L = moe.lib()
+    fg = lambda T=50, src=FAKE, K=128, ws=None, n=0: L.moe_grouped_gemm_fwd_gather(
+        FAKE, T, src, FAKE, None, FAKE, 4, 100, K, 128, FAKE, None, None, ws, n, None)
+    assert fg(src=None) == 1 and fg(T=0) == 1 and fg(T=-1) == 1 and fg(K=100) == 2
+    assert fg(T=1 << 20, K=1024) == 2                     # the source must be < 2 GiB
+    assert fg(ws=FAKE, n=16) == 3                         # a split workspace that is too small
+    gr = lambda T=10, d=128, k=2, x=FAKE: L.moe_gather_rows(x, T, d, k, FAKE, FAKE, None)
+    assert gr(d=100) == 2 and gr(k=0) == 1 and gr(x=None) == 1 and gr(x=BAD) == 1 and gr(T=0) == 0
+
+
 def test_dw_t_and_transpose_rejects():
     L = moe.lib()
     assert L.moe_transposed_cols_bound(100, 4) == 128 + 128

@@ -516,6 +516,63 @@ def test_layer_dw_transposed(cfg_id):
         assert torch.equal(lay.buf[key].view(torch.int32), lay_t.buf[key].view(torch.int32)), key
 
 
+@pytest.mark.parametrize("T,d,E,k,N", [(300, 256, 8, 2, 320), (1000, 512, 16, 4, 256), (64, 64, 4, 1, 64)])
+def test_grouped_gemm_fwd_gather(T, d, E, k, N):
+    """The gate/up product reading its rows through token_of_row equals the product on the
+    gathered X_perm bit for bit (single, dual, dual + SwiGLU; with and without a split
+    workspace), and equals the oracle exactly on small-integer operands; moe_gather_rows equals
+    the oracle's gather bit for bit."""
+    _say("gemm fwd gather", T, d, E, k, N)
+    g = torch.Generator().manual_seed(T + d)
+    logits = torch.randn((T, E), generator=g)
+    x = _int_tensor(g, (T, d)).to(DEV)
+    B, B2 = _int_tensor(g, (E, d, N)).to(DEV), _int_tensor(g, (E, d, N)).to(DEV)
+    r = moe.moe_route_permute(logits.to(DEV), x, k)
+    xg = poison_(torch.empty((T * k, d), dtype=torch.bfloat16, device=DEV))
+    moe.moe_gather_rows(x, r["row_of_slot"], k, xg)
+    torch.cuda.synchronize()
+    tor = i64(r["token_of_row"])
+    np.testing.assert_array_equal(f64(xg), f64(x)[tor])
+    assert torch.equal(xg.view(torch.int16), r["x_perm"].view(torch.int16))
+    off = r["offsets"]
+    ws = moe.split_workspace(DEV)
+    for w in (None, ws):
+        a1 = moe.moe_grouped_gemm_fwd(r["x_perm"], B, off)[0]
+        b1 = moe.moe_grouped_gemm_fwd_gather(x, r["token_of_row"], B, off, workspace=w)[0]
+        a3 = moe.moe_grouped_gemm_fwd(r["x_perm"], B, off, B2, want_act=True)
+        b3 = moe.moe_grouped_gemm_fwd_gather(x, r["token_of_row"], B, off, B2, want_act=True, workspace=w)
+        torch.cuda.synchronize()
+        assert torch.equal(a1.view(torch.int16), b1.view(torch.int16))
+        for u, v in zip(a3, b3):
+            assert torch.equal(u.view(torch.int16), v.view(torch.int16))
+    np.testing.assert_array_equal(f64(b1), O.grouped_gemm(f64(x)[tor], f64(B), i64(off)))
+
+
+@pytest.mark.parametrize("cfg_id", [0, 2])
+def test_layer_gather_fused_bitwise(cfg_id):
+    """The layer with the gather folded into the gate/up product gives bitwise the outputs of the
+    default layer (X_perm, gathered in the backward instead, included), over two steps."""
+    import dataclasses
+    cfg = W.CONFIGS[cfg_id]
+    if cfg_id:
+        cfg = dataclasses.replace(cfg, T=1024)
+    _say("layer gather fused", cfg)
+    inp = W.make_inputs(cfg, 0, "cpu")
+    dinp = {k_: v.to(DEV) for k_, v in inp.items()}
+    ref = L.MoELayer(cfg, dinp)
+    gat = L.MoELayer(cfg, dinp, gather_fused=True)
+    ref.step()
+    for _ in range(2):
+        for t in gat.buf.values():
+            poison_(t)
+        gat.step()
+    torch.cuda.synchronize()
+    for key, t in ref.buf.items():
+        if key in ("workspace", "d_act", "d_act_sh"):
+            continue
+        assert torch.equal(t.view(torch.uint8), gat.buf[key].view(torch.uint8)), key
+
+
 @pytest.mark.parametrize("cfg_id", [0, 2])
 def test_layer_concurrent_bitwise(cfg_id):
     """The two-stream schedule (weight gradients and the shared FFN beside the main chain) gives
