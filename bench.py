@@ -30,15 +30,15 @@ METRIC = "MoE layer fwd+bwd tokens/sec + grouped-GEMM TFLOP/s (% of bf16 MFMA pe
 
 # HBM bytes per launch of each grouped GEMM on the Mixtral-shaped layer, from rocprofv3 FETCH_SIZE /
 # WRITE_SIZE runs scaled by a plain copy of known size (profiles/grouped_gemm_hbm_traffic_*.md).
-# Valid only for the kernel code they were measured on (sha256 prefix of the source with comments
+# Valid only for the kernel code they were measured on (sha256 prefix of the sources with comments
 # and blank lines removed); otherwise reported null.
-TRAFFIC_SOURCE = ("paper_2606_26453_amd/csrc/grouped_gemm.hip", "0565df3d83ed8e93")
+TRAFFIC_SOURCE = (("paper_2606_26453_amd/csrc/grouped_gemm.hip", "paper_2606_26453_amd/csrc/common.h"), "87b1147df7d5f6e9")
 TRAFFIC_CONFIG = 1
 FETCH_SCALE, WRITE_SCALE = 2.0 * 1024, 1.0 * 1024
 TRAFFIC_KIB = {  # call: (FETCH_SIZE KiB, WRITE_SIZE KiB) per dispatch
-    "fwd_gate_up": (4609741, 1376256), "fwd_down": (2044464, 131072),
-    "dx_down_swiglu_bwd": (3036474, 917504), "dx_gate_up": (4296027, 131072),
-    "dw_down": (1545215, 1835017), "dw_gate_up": (2756682, 3671501),
+    "fwd_gate_up": (4372359, 1391488), "fwd_down": (2035947, 198664),
+    "dx_down_swiglu_bwd": (2930889, 917504), "dx_gate_up": (4339457, 196616),
+    "dw_down": (1507458, 1835014), "dw_gate_up": (2762929, 3672077),
 }
 
 
@@ -50,9 +50,8 @@ def code_hash(text):
 
 
 def measured_traffic(call, config):
-    path = os.path.join(ROOT, TRAFFIC_SOURCE[0])
     try:
-        sha = code_hash(open(path).read())
+        sha = code_hash("".join(open(os.path.join(ROOT, f)).read() for f in TRAFFIC_SOURCE[0]))
     except OSError:
         return None
     if sha != TRAFFIC_SOURCE[1] or config != TRAFFIC_CONFIG or call not in TRAFFIC_KIB:
@@ -247,7 +246,7 @@ def main():
         "input_gen_s": round(t_gen, 1),
     }
     if not a.no_cpu_baseline and not cfg.dw_only:
-        ts = a.cpu_sample_tokens or max(8, min(cfg.T, int(2e12 // (18 * cfg.k * cfg.d * cfg.f))))
+        ts = a.cpu_sample_tokens or max(8, min(cfg.T, int(6e12 // (18 * cfg.k * cfg.d * cfg.f))))
         out["cpu_baseline"] = cpu_baseline(cfg, inp, ts)
     print(json.dumps(out), flush=True)
 
