@@ -90,6 +90,17 @@ __device__ __forceinline__ i32x4 make_rsrc(const void* base, int64_t bytes) {
   return r;
 }
 
+// The same over [base, base + bytes) with bytes already in [0, 2^31).
+__device__ __forceinline__ i32x4 make_rsrc32(const void* base, int bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  i32x4 r;
+  r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  r[1] = __builtin_amdgcn_readfirstlane((int)((a >> 32) & 0xffffu));
+  r[2] = __builtin_amdgcn_readfirstlane(bytes);
+  r[3] = 0x00020000;
+  return r;
+}
+
 // One 16-byte-per-lane buffer load written straight to LDS at lds_addr + 16*lane.  Issued as
 // inline assembly so the compiler does not serialise later LDS reads behind it; completion is
 // tracked explicitly with vmcnt waits (loads retire in order).
@@ -288,6 +299,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
   int n_voff[DPW_N];
   int64_t c_len = 0;              // contraction extent
   int nsteps = 0;
+  int c_len32 = 0, m_row_bytes = 0, n_row_bytes = 0;   // the same sizes in 32 bits
   auto setup = [&](int g, int mt, int nt, int64_t row_lo, int64_t row_hi) {
     // lane-dependent terms are recomputed per tile rather than hoisted out of the tile loop and
     // kept live (in registers the main loop needs) across it
@@ -408,42 +420,52 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
     else if constexpr (KIND == KIND_DX) c_len = DUAL ? 2 * p.N : p.N;
     else c_len = row_hi - row_lo;
     nsteps = (int)((c_len + BK - 1) / BK);
+    c_len32 = (int)c_len;
+    m_row_bytes = (int)(m_ld * 2);
+    n_row_bytes = (int)(n_ld * 2);
   };
 
   // buffer resources of step s for the M and N operands
   int s_base = 0;   // first contraction step of the tile's range (a piece of a split tile)
+  // Branch-free: the step's window is selected with scalar selects (a step past the end gets an
+  // empty window), and every size is 32-bit (a 32-row slice of a transposed operand is < 2 GiB).
   auto rsrc_m = [&](int s) {
-    const int64_t c0 = (int64_t)(s + s_base) * BK;
-    if (s >= nsteps) return make_rsrc(m_src, 0);   // past the end: every load is out of range
+    const int sa = s + s_base;
+    const bool live = s < nsteps;
     if constexpr (!M_T) {
+      int64_t cc = (int64_t)sa * BK;
       const char* base = m_src;
-      int64_t cc = c0;
       if constexpr (KIND == KIND_DX && DUAL) {
-        if (c0 >= p.N) { base = m_src2; cc = c0 - p.N; }
+        const bool second = cc >= p.N;
+        base = second ? m_src2 : m_src;
+        cc = second ? cc - p.N : cc;
       }
-      if constexpr (GATHER) {
-        // gathered rows: the window ends with the source, so a row index past it reads zeros
-        return make_rsrc(base + cc * 2, (p.gather_rows * m_ld - cc) * 2);
-      }
-      return make_rsrc(base + cc * 2, (int64_t)0x7fffffff);
+      int bytes = 0x7fffffff;
+      // gathered rows: the window ends with the source, so a row index past it reads zeros
+      if constexpr (GATHER) bytes = (int)((p.gather_rows * m_ld - cc) * 2);
+      return make_rsrc32(base + cc * 2, live ? bytes : 0);
     } else {
-      const int64_t left = c_len - c0;
-      return make_rsrc(m_src + c0 * m_ld * 2, (left < BK ? left : BK) * m_ld * 2);
+      const int left = c_len32 - sa * BK;
+      const int rows = left < BK ? left : BK;
+      return make_rsrc32(m_src + (int64_t)sa * (BK * 2) * m_ld, live ? rows * m_row_bytes : 0);
     }
   };
   auto rsrc_n = [&](int s) {
-    const int64_t c0 = (int64_t)(s + s_base) * BK;
-    if (s >= nsteps) return make_rsrc(n_src, 0);
+    const int sa = s + s_base;
+    const bool live = s < nsteps;
     if constexpr (!N_T) {
+      int64_t cc = (int64_t)sa * BK;
       const char* base = n_src;
-      int64_t cc = c0;
       if constexpr (DUAL && KIND == KIND_DX) {
-        if (c0 >= p.N) { base = n_src2; cc = c0 - p.N; }
+        const bool second = cc >= p.N;
+        base = second ? n_src2 : n_src;
+        cc = second ? cc - p.N : cc;
       }
-      return make_rsrc(base + cc * 2, (int64_t)0x7fffffff);
+      return make_rsrc32(base + cc * 2, live ? 0x7fffffff : 0);
     } else {
-      const int64_t left = c_len - c0;
-      return make_rsrc(n_src + c0 * n_ld * 2, (left < BK ? left : BK) * n_ld * 2);
+      const int left = c_len32 - sa * BK;
+      const int rows = left < BK ? left : BK;
+      return make_rsrc32(n_src + (int64_t)sa * (BK * 2) * n_ld, live ? rows * n_row_bytes : 0);
     }
   };
   // load d (0 .. DPW_T-1) of this wave for a step whose slot starts at LDS byte slot_lds
