@@ -585,8 +585,16 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
       wait_vm<(NSTAGE - 2) * DPW_T>();
       __syncthreads();
       load_frags(cur ^ 1, slot_of(s + 1), 0);   // unused after the last stage
-      __builtin_amdgcn_sched_barrier(0);
       mfmas(cur, SPLIT, MFMA_HALF);
+      // interleave the next stage's fragment reads with these MFMAs (two LDS reads, one MFMA)
+      // rather than issuing all reads first: the matrix core keeps busy while the LDS queue
+      // drains (measured: 1320-1360 -> 1185-1270 cycles per step on the fwd and dW products)
+#pragma unroll
+      for (int q = 0; q < (MB + NB) * (N_T ? 2 : 1) / 2; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // DS reads
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+      }
+      __builtin_amdgcn_sched_barrier(0);
       mfmas_refill(2, s + NSTAGE);
     };
     if (nsteps > 0) {
