@@ -32,13 +32,13 @@ METRIC = "MoE layer fwd+bwd tokens/sec + grouped-GEMM TFLOP/s (% of bf16 MFMA pe
 # WRITE_SIZE runs scaled by a plain copy of known size (profiles/grouped_gemm_hbm_traffic_*.md).
 # Valid only for the kernel code they were measured on (sha256 prefix of the sources with comments
 # and blank lines removed); otherwise reported null.
-TRAFFIC_SOURCE = (("paper_2606_26453_amd/csrc/grouped_gemm.hip", "paper_2606_26453_amd/csrc/common.h"), "87b1147df7d5f6e9")
+TRAFFIC_SOURCE = (("paper_2606_26453_amd/csrc/grouped_gemm.hip", "paper_2606_26453_amd/csrc/common.h"), "2b28fd5fbc98c922")
 TRAFFIC_CONFIG = 1
 FETCH_SCALE, WRITE_SCALE = 2.0 * 1024, 1.0 * 1024
 TRAFFIC_KIB = {  # call: (FETCH_SIZE KiB, WRITE_SIZE KiB) per dispatch
-    "fwd_gate_up": (4372359, 1391488), "fwd_down": (2035947, 198664),
-    "dx_down_swiglu_bwd": (2930889, 917504), "dx_gate_up": (4339457, 196616),
-    "dw_down": (1507458, 1835014), "dw_gate_up": (2762929, 3672077),
+    "fwd_gate_up": (4627608, 1399104), "fwd_down": (2173060, 199688),
+    "dx_down_swiglu_bwd": (2899104, 917504), "dx_gate_up": (4373611, 196616),
+    "dw_down": (1507454, 1835100), "dw_gate_up": (2851561, 3671297),
 }
 
 
