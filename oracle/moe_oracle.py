@@ -18,7 +18,8 @@ the first FFN projection is dW1_e = X_e^T G_e, a contraction over that expert's 
 be zero).  `grouped_gemm_dw` is that definition.  The paper states no routing rule, row order,
 activation, combine, router or other backward formula; the readings used for those are the
 standard MoE layer (and, for the router's load-balancing loss, the Switch-style auxiliary loss) and
-are named at each function.
+are named at each function.  The FP8 functions at the end serve a variant the paper does not
+describe (OCP E4M3 operands with fp32 scales); their reading is stated there.
 
 Parity: every function here is pinned by the CPU test suite against closed forms, library
 routines, brute force or automatic differentiation; no function is "parity unpinned".
@@ -430,6 +431,88 @@ def dw_gate_up_cols(x_perm_e, dy_perm_e, w_gate_e, w_up_e, w_down_e, cols_f, rnd
     da = grouped_gemm_dx(dy_perm_e, np.asarray(w_down_e)[None, cols_f, :], off, rnd=rnd)
     dhg, dhu = swiglu_bwd(hg, hu, da, rnd)
     return grouped_gemm_dw(x_perm_e, dhg, off)[0], grouped_gemm_dw(x_perm_e, dhu, off)[0]
+
+
+# --------------------------------------------------------------------------------------------
+# FP8 variant of the forward products (a variant beyond the paper, which is silent on it; the
+# reading: the OCP 8-bit floating-point format E4M3, activations scaled per row and weights per
+# output channel by fp32 factors, products accumulated exactly and rounded once to bf16)
+# --------------------------------------------------------------------------------------------
+E4M3_MAX = 448.0
+
+
+def e4m3_decode(codes):
+    """E4M3 codes (uint8) -> float64, exactly.
+
+    Bit 7 is the sign, bits 6..3 the exponent field E (bias 7), bits 2..0 the mantissa M.  E = 0
+    encodes the subnormals M/8 * 2**-6; otherwise the value is (1 + M/8) * 2**(E - 7).  The code
+    with E = 15 and M = 7 (either sign) is NaN; the format has no infinities, so the largest finite
+    magnitude is 1.75 * 2**8 = 448.
+    """
+    c = np.asarray(codes, dtype=np.uint8).astype(np.int64)
+    e = (c >> 3) & 0xF
+    m = (c & 0x7).astype(np.float64)
+    mag = np.where(e == 0, m / 8.0 * 2.0 ** -6, (1.0 + m / 8.0) * np.ldexp(1.0, e - 7))
+    mag = np.where((e == 15) & (c & 0x7 == 7), np.nan, mag)
+    return np.where(c & 0x80, -mag, mag)
+
+
+def e4m3_encode(x):
+    """float -> E4M3 codes: round to the nearest representable magnitude, ties to the even
+    mantissa; magnitudes beyond 448 saturate to 448; NaN -> 0x7F; the sign bit is x's (so values
+    that round to zero keep their sign).
+
+    A magnitude a in [2**n, 2**(n+1)) with n >= -6 has representable neighbours 2**(n-3) apart; below
+    2**-6 (the subnormals) the spacing is 2**-9.  Rounding a / spacing to the nearest integer with
+    ties to even gives the neighbour with the even mantissa.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    a = np.minimum(np.abs(np.where(np.isnan(x), 0.0, x)), E4M3_MAX)
+    _, fe = np.frexp(a)                       # a = f * 2**fe, 0.5 <= f < 1
+    n = np.maximum(fe - 1, -6)                # binade exponent, clamped to the subnormal range
+    q = np.ldexp(np.rint(np.ldexp(a, 3 - n)), n - 3)   # the rounded magnitude
+    _, qe = np.frexp(q)
+    qn = qe - 1
+    normal = q >= 2.0 ** -6
+    mant = np.where(normal, np.rint(np.ldexp(q, 3 - np.where(normal, qn, 0))) - 8, np.rint(q * 2.0 ** 9))
+    code = np.where(normal, ((np.where(normal, qn, 0) + 7) << 3) + mant.astype(np.int64), mant.astype(np.int64))
+    code = code.astype(np.int64) | np.where(np.signbit(x), 0x80, 0)
+    code = np.where(np.isnan(x), 0x7F, code)
+    return code.astype(np.uint8)
+
+
+def quantize_rows_fp8(x):
+    """Per-row E4M3 quantization: with amax = max |x[r, :]| (fp32), scale[r] = amax / 448 and
+    codes[r, :] = e4m3_encode(x[r, :] * (448 / amax)), both quotients and the product taken in fp32
+    (the precision the device kernel decides the codes in), so that the row's largest magnitude
+    lands on 448; an all-zero row gets scale 1 and zero codes.  x ~= e4m3_decode(codes) * scale."""
+    x32 = np.asarray(x, dtype=np.float32)
+    amax = np.max(np.abs(x32), axis=-1)
+    big = amax > 0
+    scale = np.ones_like(amax)
+    np.divide(amax, np.float32(E4M3_MAX), out=scale, where=big)
+    inv = np.ones_like(amax)
+    np.divide(np.float32(E4M3_MAX), amax, out=inv, where=big)
+    y = (x32 * inv[..., None]).astype(np.float32)
+    return e4m3_encode(y.astype(np.float64)), scale.astype(np.float32)
+
+
+def grouped_gemm_fp8(a_codes, a_scale, wt_codes, w_scale, offsets, rnd=bf16_round):
+    """The forward grouped product on E4M3 operands: for rows r of group g,
+    C[r, n] = a_scale[r] * w_scale[g, n] * sum_k dec(A[r, k]) * dec(Wt[g, n, k]), rounded once to
+    bf16.  A [R, K] codes with per-row scales [R]; Wt [G, N, K] codes (the weight in the layout
+    [output channel, contraction]) with per-channel scales [G, N]."""
+    A = e4m3_decode(a_codes)
+    W = e4m3_decode(wt_codes)
+    sa = np.asarray(a_scale, dtype=np.float64)
+    sw = np.asarray(w_scale, dtype=np.float64)
+    G, N, _ = W.shape
+    C = np.zeros((A.shape[0], N))
+    for g in range(G):
+        lo, hi = int(offsets[g]), int(offsets[g + 1])
+        if hi > lo:
+            C[lo:hi] = (A[lo:hi] @ W[g].T) * sa[lo:hi, None] * sw[g][None, :]
+    return _r(rnd, C)
 
 
 def rel_fro(got, ref):

@@ -478,3 +478,96 @@ def test_router_bwd_autograd():
     dx0 = O.bf16_round(rng.normal(size=(T, d)))
     _, dxs = O.router_bwd(x, wr, g, dx=dx0)
     np.testing.assert_array_equal(dxs, O.bf16_round(dx0 + xt.grad.numpy()))
+
+
+# ---------------------------------------------------------------------------------------------
+# FP8 (E4M3) variant
+# ---------------------------------------------------------------------------------------------
+def test_e4m3_decode_spec_values_and_torch():
+    """Values fixed by the E4M3 format definition, and torch's float8_e4m3fn decoding of every
+    code (a library routine)."""
+    spec = {0x00: 0.0, 0x01: 2.0 ** -9, 0x07: 7 * 2.0 ** -9, 0x08: 2.0 ** -6, 0x38: 1.0, 0x3C: 1.5,
+            0x40: 2.0, 0x77: 240.0, 0x7E: 448.0, 0x80: -0.0, 0xB8: -1.0, 0xFE: -448.0}
+    v = O.e4m3_decode(np.arange(256, dtype=np.uint8))
+    for c, val in spec.items():
+        assert v[c] == val and np.signbit(v[c]) == np.signbit(val), hex(c)
+    assert np.isnan(v[0x7F]) and np.isnan(v[0xFF]) and np.isnan(v).sum() == 2
+    t = torch.arange(256, dtype=torch.int32).to(torch.uint8).view(torch.float8_e4m3fn).double().numpy()
+    np.testing.assert_array_equal(v, t)
+
+
+def _e4m3_nearest_brute(x):
+    """Nearest finite E4M3 code by exhaustive search, ties to the even code, saturating."""
+    codes = np.arange(256, dtype=np.uint8)
+    vals = O.e4m3_decode(codes)
+    ok = ~np.isnan(vals) & ((codes & 0x80) == 0)          # non-negative codes; sign applied after
+    cv, vv = codes[ok].astype(np.int64), vals[ok]
+    out = []
+    for xi in np.asarray(x, dtype=np.float64):
+        a = min(abs(xi), 448.0)
+        d = np.abs(vv - a)
+        best = cv[d == d.min()]
+        c = int(best[0]) if len(best) == 1 else int(best[best % 2 == 0][0])
+        out.append(c | (0x80 if np.signbit(xi) else 0))
+    return np.array(out, dtype=np.uint8)
+
+
+def test_e4m3_encode_brute_force_and_torch():
+    rng = np.random.default_rng(8)
+    vals = O.e4m3_decode(np.arange(0, 0x7F, dtype=np.uint8))            # 0 .. 448
+    mids = (vals[1:] + vals[:-1]) / 2                                    # exact ties
+    x = np.concatenate([rng.uniform(-470, 470, 3000), rng.normal(0, 0.01, 1000), mids, -mids,
+                        vals, [0.0, -0.0, 1e-12, -1e-12, 448.0, 463.9, 1e6, -1e6]])
+    got = O.e4m3_encode(x)
+    np.testing.assert_array_equal(got, _e4m3_nearest_brute(x))
+    inr = np.abs(x) < 464                                                # torch overflows to NaN beyond
+    t = torch.from_numpy(x[inr]).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    np.testing.assert_array_equal(got[inr], t)
+    assert O.e4m3_encode(np.array([np.nan]))[0] == 0x7F
+    assert O.e4m3_encode(np.array([1e9]))[0] == 0x7E and O.e4m3_encode(np.array([-1e9]))[0] == 0xFE
+
+
+def test_quantize_rows_fp8_properties():
+    rng = np.random.default_rng(9)
+    x = O.bf16_round(rng.normal(0, 1, (40, 96)) * rng.uniform(0.01, 100, (40, 1)))
+    x[3] = 0.0
+    codes, scale = O.quantize_rows_fp8(x)
+    assert codes.dtype == np.uint8 and scale.dtype == np.float32
+    dec = O.e4m3_decode(codes)
+    assert np.all(codes[3] == 0) and scale[3] == 1.0
+    nz = np.arange(40) != 3
+    # each row's largest magnitude lands on 448 (saturation absorbs the fp32 rounding of 448/amax)
+    np.testing.assert_array_equal(np.abs(dec[nz]).max(axis=1), 448.0)
+    # reconstruction within half an E4M3 spacing (relative 2**-4) plus the fp32 rounding of the
+    # scaled value, and the subnormal spacing near zero
+    rec = dec * scale[:, None].astype(np.float64)
+    tol = (np.abs(x) * (2.0 ** -4 + 2.0 ** -20) + 2.0 ** -10 * scale[:, None]) * 1.0001
+    assert np.all(np.abs(rec - x) <= tol)
+    # the scale is amax / 448 in fp32
+    amax = np.abs(x).max(axis=1).astype(np.float32)
+    np.testing.assert_array_equal(scale[nz], (amax / np.float32(448))[nz])
+
+
+def test_grouped_gemm_fp8_vs_library():
+    """Exact on small-integer codes (torch matmul of the decoded operands, then the scales), and
+    linear in each scale."""
+    rng = np.random.default_rng(10)
+    counts = [5, 0, 7, 1, 3]
+    G, R, K, N = len(counts), sum(counts), 32, 12
+    off = np.concatenate([[0], np.cumsum(counts)])
+    ints = np.arange(-4, 5, dtype=np.float64)
+    a = O.e4m3_encode(rng.choice(ints, (R, K)))
+    w = O.e4m3_encode(rng.choice(ints, (G, N, K)))
+    sa = np.float32(2.0) ** rng.integers(-3, 3, R).astype(np.float32)
+    sw = np.float32(2.0) ** rng.integers(-3, 3, (G, N)).astype(np.float32)
+    got = O.grouped_gemm_fp8(a, sa, w, sw, off, rnd=None)
+    A = torch.from_numpy(O.e4m3_decode(a))
+    W = torch.from_numpy(O.e4m3_decode(w))
+    for g in range(G):
+        lo, hi = off[g], off[g + 1]
+        ref = (A[lo:hi] @ W[g].T).numpy() * sa[lo:hi, None] * sw[g][None, :]
+        np.testing.assert_array_equal(got[lo:hi], ref)
+    sa2 = sa.copy()
+    sa2[2] *= 4
+    np.testing.assert_array_equal(O.grouped_gemm_fp8(a, sa2, w, sw, off, rnd=None)[2], 4 * got[2])
+    np.testing.assert_array_equal(O.grouped_gemm_fp8(a, sa, w, sw, off), O.bf16_round(got))

@@ -29,6 +29,10 @@ PINS = [
     P.test_route_topk_bwd_properties_and_fd,
     P.test_aux_loss_closed_form_and_autograd,
     P.test_router_bwd_autograd,
+    P.test_e4m3_decode_spec_values_and_torch,
+    P.test_e4m3_encode_brute_force_and_torch,
+    P.test_quantize_rows_fp8_properties,
+    P.test_grouped_gemm_fp8_vs_library,
 ]
 
 
@@ -141,7 +145,33 @@ def _router_bwd_misaligned(x, wr, dlogits, dx=None, rnd=O.bf16_round):     # tok
     return x.T @ np.roll(g, 1, axis=0), O._r(rnd, share)
 
 
+def _e4m3_ties_away(x):                                                   # ties away from zero
+    x = np.asarray(x, dtype=np.float64)
+    a = np.minimum(np.abs(x), 448.0)
+    _, fe = np.frexp(a)
+    n = np.maximum(fe - 1, -6)
+    q = np.ldexp(np.floor(np.ldexp(a, 3 - n) + 0.5), n - 3)
+    return O.__dict__["_orig_enc"](np.copysign(q, x))
+
+
+def _e4m3_decode_bias8(codes):                                            # exponent bias off by one
+    return O.__dict__["_orig_dec"](codes) * 0.5
+
+
+def _fp8_gemm_no_weight_scale(a_codes, a_scale, wt_codes, w_scale, offsets, rnd=O.bf16_round):
+    return O.__dict__["_orig_f8"](a_codes, a_scale, wt_codes, np.ones_like(w_scale), offsets, rnd)
+
+
+def _quant_inverted_scale(x):                                             # scale = 448 / amax
+    codes, scale = O.__dict__["_orig_q8"](x)
+    return codes, np.where(scale != 1, (np.float32(448.0) ** 2 / 448.0) / (scale * 448.0), scale).astype(np.float32)
+
+
 MUTANTS = {
+    "e4m3 ties away from zero": ("e4m3_encode", _e4m3_ties_away),
+    "e4m3 exponent bias 8": ("e4m3_decode", _e4m3_decode_bias8),
+    "fp8 gemm ignores the weight scale": ("grouped_gemm_fp8", _fp8_gemm_no_weight_scale),
+    "fp8 quantization stores the inverse scale": ("quantize_rows_fp8", _quant_inverted_scale),
     "router logits drop the bias": ("router_logits", _logits_no_bias),
     "route_topk_bwd drops the weighted mean": ("route_topk_bwd", _topk_bwd_no_mean),
     "route_topk_bwd uses the full softmax": ("route_topk_bwd", _topk_bwd_full_softmax),
@@ -169,6 +199,10 @@ def test_planted_mistake_is_caught(name, monkeypatch):
     monkeypatch.setitem(O.__dict__, "_orig_comb", O.combine)
     monkeypatch.setitem(O.__dict__, "_orig_tkb", O.route_topk_bwd)
     monkeypatch.setitem(O.__dict__, "_orig_aux", O.aux_loss)
+    monkeypatch.setitem(O.__dict__, "_orig_enc", O.e4m3_encode)
+    monkeypatch.setitem(O.__dict__, "_orig_dec", O.e4m3_decode)
+    monkeypatch.setitem(O.__dict__, "_orig_f8", O.grouped_gemm_fp8)
+    monkeypatch.setitem(O.__dict__, "_orig_q8", O.quantize_rows_fp8)
     monkeypatch.setattr(O, attr, fn)
     if attr == "bf16_round":
         # default arguments captured the original function; patch the module-level users too
