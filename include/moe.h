@@ -226,6 +226,39 @@ moe_status moe_grouped_gemm_fwd_gather(const moe_bf16* X, int64_t T, const int32
                                        int64_t K, int64_t N, moe_bf16* C, moe_bf16* C2, moe_bf16* act,
                                        void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* ------------------------------------------------------------------------------------------ */
+/* FP8 variant of the forward products (beyond the paper, which describes bf16 operands only):  */
+/* OCP E4M3 operands with fp32 scales, fp32 accumulation, bf16 output.                        */
+/* ------------------------------------------------------------------------------------------ */
+
+/*
+ * Per-row E4M3 quantization.  For each of the M rows of x [M,K] bf16: amax = max |x[r,:]|,
+ * scale[r] = amax / 448 and q[r,k] = the E4M3 code nearest to x[r,k] * (448 / amax) (ties to the
+ * even mantissa; magnitudes beyond 448 saturate), both quotients and the product single fp32
+ * operations; an all-zero row gets scale 1 and zero codes.  x ~= decode(q) * scale.  Used for
+ * activations (rows of A) and for weights stored as [output channel, contraction] (rows of Wt,
+ * i.e. one scale per output channel).  q [M,K] uint8 (8-byte aligned), scale [M] fp32.  Errors: K
+ * not a multiple of 16 -> NOT_SUPPORTED; NULL or misaligned pointers -> INVALID_VALUE.  M = 0 is a
+ * no-op.
+ */
+moe_status moe_quantize_fp8_rows(const moe_bf16* x, int64_t M, int64_t K, uint8_t* q, float* scale,
+                                 hipStream_t stream);
+
+/*
+ * The forward grouped product on E4M3 operands: for rows r of group g (offsets as in
+ * moe_grouped_gemm_fwd), C[r,n] = bf16(a_scale[r] * w_scale[g,n] * sum_k A[r,k] * Wt[g,n,k]) with
+ * A and Wt decoded from E4M3 and the sum accumulated in fp32 by the gfx950 8-bit matrix cores
+ * (v_mfma_scale_f32_32x32x64_f8f6f4, 64 contraction elements per instruction).  The weight is in
+ * the layout [G, N, K] (output channel, contraction): both operands are then read along the
+ * contraction, as in the data-gradient product.  A [R,K] uint8, a_scale [R] fp32, Wt [G,N,K]
+ * uint8, w_scale [G,N] fp32, C [R,N] bf16.  workspace: NULL, or a split workspace as for
+ * moe_grouped_gemm_fwd_split (same tail split).  Errors as moe_grouped_gemm_fwd; K and N multiples
+ * of 64; one group's weight < 2 GiB.
+ */
+moe_status moe_grouped_gemm_fwd_fp8(const uint8_t* A, const float* a_scale, const uint8_t* Wt, const float* w_scale,
+                                    const int32_t* offsets, int32_t G, int64_t R, int64_t K, int64_t N, moe_bf16* C,
+                                    void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 moe_status moe_grouped_gemm_fwd_split(const moe_bf16* A, const moe_bf16* B, const moe_bf16* B2,
                                       const int32_t* offsets, int32_t G, int64_t R, int64_t K, int64_t N,
                                       moe_bf16* C, moe_bf16* C2, moe_bf16* act, void* workspace,

@@ -72,9 +72,12 @@ struct GemmParams {
   int split_min_steps; //   contraction steps (of BK) a piece must have at least
   const int32_t* gather;   // FWD: row r of A is row gather[r] of a [gather_rows, K] source (NULL: A itself)
   int64_t gather_rows;
+  const float* a_scale;    // FP8 products: per-row scale of the row operand [R]
+  const float* w_scale;    //               per-output-column scale of the weight [G, K]
 };
 
 typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x8 __attribute__((ext_vector_type(8)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 
 // Raw buffer resource (four scalar dwords) over [base, base + bytes): reads at offsets >= bytes
@@ -158,9 +161,17 @@ __device__ __forceinline__ void band_order(int id, int mtiles, int ntiles, int& 
 // NSTAGE-deep LDS ring; WPE workgroups share a CU (2 when the ring is small enough).  PERSIST: the
 // workgroup loops over tiles (grid = CU slots) instead of computing one tile (grid = tiles).  OUT16:
 // dW results are rounded to bf16 (as the paper's kernel stores them) instead of stored as fp32.
+//
+// F8 (dX kind only): both operands are E4M3 bytes; a stage then holds 64 contraction elements in the
+// same 64-byte rows, and one v_mfma_scale_f32_32x32x64_f8f6f4 per block consumes the two 16-byte
+// fragments a bf16 stage feeds to two 32x32x16 MFMAs.  The epilogue applies the fp32 row and
+// column scales before rounding to bf16.
 template <int KIND, bool DUAL, bool ACT, int TM, int WAVES_M, int WAVES_N, int NSTAGE, bool PINGPONG, int WPE,
-          bool PERSIST, bool OUT16, bool GATHER>
+          bool PERSIST, bool OUT16, bool GATHER, bool F8>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kernel(GemmParams p) {
+  static_assert(!F8 || (KIND == KIND_DX && !DUAL && !ACT), "FP8 operands: the single dX-shaped product only");
+  constexpr int ES = F8 ? 1 : 2;              // bytes per operand element
+  constexpr int BKE = F8 ? 2 * BK : BK;       // contraction elements per stage (64-byte rows)
   constexpr int NWAVE = WAVES_M * WAVES_N;
   constexpr int OPND_M = TM * BK * 2;         // bytes of the M-side tile of one stage
   constexpr int OPND_N = TN * BK * 2;         // bytes of the N-side tile of one stage (16 KiB)
@@ -335,14 +346,14 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
           m_voff[i] = (int)((src * m_ld + 8 * c) * 2);
         }
       } else {
-        m_src = reinterpret_cast<const char*>(p.a + row_lo * m_ld);
-        if constexpr (KIND == KIND_DX && DUAL) m_src2 = reinterpret_cast<const char*>(p.a2 + row_lo * m_ld);
+        m_src = reinterpret_cast<const char*>(p.a) + row_lo * m_ld * ES;
+        if constexpr (KIND == KIND_DX && DUAL) m_src2 = reinterpret_cast<const char*>(p.a2) + row_lo * m_ld * ES;
 #pragma unroll
         for (int i = 0; i < DPW_M; ++i) {
           int64_t r = 16 * (DPW_M * wave + i) + (lane >> 2);
           if (r > rows_valid - 1) r = rows_valid - 1;
           const int c = (lane & 3) ^ swz_d(lane >> 2);
-          m_voff[i] = (int)((r * m_ld + 8 * c) * 2);
+          m_voff[i] = (int)(r * m_ld * ES + 16 * c);
         }
       }
     } else {
@@ -382,14 +393,14 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
     } else if constexpr (!N_T) {
       // DX: B[g][kk, c]; the tile's output columns kk = nt*TN + row, clamped
       n_ld = p.N;
-      n_src = reinterpret_cast<const char*>(p.b + (int64_t)g * p.K * p.N);
-      if constexpr (DUAL) n_src2 = reinterpret_cast<const char*>(p.b2 + (int64_t)g * p.K * p.N);
+      n_src = reinterpret_cast<const char*>(p.b) + (int64_t)g * p.K * p.N * ES;
+      if constexpr (DUAL) n_src2 = reinterpret_cast<const char*>(p.b2) + (int64_t)g * p.K * p.N * ES;
 #pragma unroll
       for (int i = 0; i < DPW_N; ++i) {
         int64_t kk = (int64_t)nt * TN + 16 * (DPW_N * wave + i) + (lane >> 2);
         if (kk > p.K - 1) kk = p.K - 1;
         const int c = (lane & 3) ^ swz_d(lane >> 2);
-        n_voff[i] = (int)((kk * p.N + 8 * c) * 2);
+        n_voff[i] = (int)(kk * p.N * ES + 16 * c);
       }
     } else {
       // this wave's column group: in dual mode groups 0,2 come from the first source and 1,3 from
@@ -419,7 +430,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
     if constexpr (KIND == KIND_FWD) c_len = p.K;
     else if constexpr (KIND == KIND_DX) c_len = DUAL ? 2 * p.N : p.N;
     else c_len = row_hi - row_lo;
-    nsteps = (int)((c_len + BK - 1) / BK);
+    nsteps = (int)((c_len + BKE - 1) / BKE);
     c_len32 = (int)c_len;
     m_row_bytes = (int)(m_ld * 2);
     n_row_bytes = (int)(n_ld * 2);
@@ -433,7 +444,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
     const int sa = s + s_base;
     const bool live = s < nsteps;
     if constexpr (!M_T) {
-      int64_t cc = (int64_t)sa * BK;
+      int64_t cc = (int64_t)sa * BKE;
       const char* base = m_src;
       if constexpr (KIND == KIND_DX && DUAL) {
         const bool second = cc >= p.N;
@@ -443,7 +454,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
       int bytes = 0x7fffffff;
       // gathered rows: the window ends with the source, so a row index past it reads zeros
       if constexpr (GATHER) bytes = (int)((p.gather_rows * m_ld - cc) * 2);
-      return make_rsrc32(base + cc * 2, live ? bytes : 0);
+      return make_rsrc32(base + cc * ES, live ? bytes : 0);
     } else {
       const int left = c_len32 - sa * BK;
       const int rows = left < BK ? left : BK;
@@ -454,14 +465,14 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
     const int sa = s + s_base;
     const bool live = s < nsteps;
     if constexpr (!N_T) {
-      int64_t cc = (int64_t)sa * BK;
+      int64_t cc = (int64_t)sa * BKE;
       const char* base = n_src;
       if constexpr (DUAL && KIND == KIND_DX) {
         const bool second = cc >= p.N;
         base = second ? n_src2 : n_src;
         cc = second ? cc - p.N : cc;
       }
-      return make_rsrc32(base + cc * 2, live ? 0x7fffffff : 0);
+      return make_rsrc32(base + cc * ES, live ? 0x7fffffff : 0);
     } else {
       const int left = c_len32 - sa * BK;
       const int rows = left < BK ? left : BK;
@@ -533,6 +544,21 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
     for (int m = m0; m < m1; ++m)
       acc[m / NB][m % NB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[set][m % NB], fb[set][m / NB],
                                                                    acc[m / NB][m % NB], 0, 0, 0);
+  };
+  // FP8: one 32x32x64 MFMA per block from the concatenated 16-byte fragments of sets 0 and 1
+  // (any assignment of the 64 contraction bytes to lanes works as long as both operands use the
+  // same one: each lane half holds bytes {0-15, 32-47} or {16-31, 48-63} of the stage's row)
+  auto mfmas_f8 = [&]() {
+#pragma unroll
+    for (int m = 0; m < MB * NB; ++m) {
+      const i32x4 a0 = __builtin_bit_cast(i32x4, fa[0][m % NB]), a1 = __builtin_bit_cast(i32x4, fa[1][m % NB]);
+      const i32x4 b0 = __builtin_bit_cast(i32x4, fb[0][m / NB]), b1 = __builtin_bit_cast(i32x4, fb[1][m / NB]);
+      const i32x8 a8 = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
+      const i32x8 b8 = __builtin_shufflevector(b0, b1, 0, 1, 2, 3, 4, 5, 6, 7);
+      // operand formats 0 (E4M3) for both; block scales 127 (2^0) leave the products unscaled
+      acc[m / NB][m % NB] =
+          __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, acc[m / NB][m % NB], 0, 0, 0, 127, 0, 127);
+    }
   };
   // the same, with the DPW_T refill loads of step `s` spread evenly between the MFMAs so the
   // vector-memory and LDS-write work of the refill overlaps the matrix cores
@@ -642,8 +668,12 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
       for (int s = 0; s < nsteps; ++s) {
         memory_phase(s);
         half_end();
-        mfmas(0, 0, MFMA_HALF);
-        mfmas(1, 0, MFMA_HALF);
+        if constexpr (F8) {
+          mfmas_f8();
+        } else {
+          mfmas(0, 0, MFMA_HALF);
+          mfmas(1, 0, MFMA_HALF);
+        }
         half_end();
       }
       if (grp == 0) half_end();
@@ -717,8 +747,21 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
           if constexpr (SPLIT) c = (j >= NB / 2 ? 16 : 0) + (wn * (WTN / 2) + 32 * (j % (NB / 2)) + 8 * q) / 8;
           else c = (wn * WTN + 32 * j + 8 * q) / 8;
           uint2 v;
-          v.x = pack_bf16(acc[i][j][4 * q], acc[i][j][4 * q + 1]);
-          v.y = pack_bf16(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+          if constexpr (F8) {
+            // fp32 row and column scales; rows past the group and columns past the output (not
+            // stored) read clamped scales
+            int64_t r = row_lo + wm * WTM + 32 * i + l32;
+            if (r > row_hi - 1) r = row_hi - 1;
+            int64_t n = (int64_t)nt * TN + wn * WTN + 32 * j + 8 * q + col_in;
+            if (n > p.K - 4) n = p.K - 4;
+            const float sr = p.a_scale[r];
+            const f32x4 sc = *reinterpret_cast<const f32x4*>(p.w_scale + (int64_t)g * p.K + n);
+            v.x = pack_bf16(acc[i][j][4 * q] * sr * sc[0], acc[i][j][4 * q + 1] * sr * sc[1]);
+            v.y = pack_bf16(acc[i][j][4 * q + 2] * sr * sc[2], acc[i][j][4 * q + 3] * sr * sc[3]);
+          } else {
+            v.x = pack_bf16(acc[i][j][4 * q], acc[i][j][4 * q + 1]);
+            v.y = pack_bf16(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+          }
           *reinterpret_cast<uint2*>(trow + 16 * (c ^ l32) + 8 * fh) = v;
         }
     }
@@ -818,7 +861,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
         int64_t clen;
         if constexpr (KIND == KIND_FWD) clen = p.K;
         else clen = DUAL ? 2 * p.N : p.N;
-        const int csteps = (int)((clen + BK - 1) / BK);
+        const int csteps = (int)((clen + BKE - 1) / BKE);
         int sp = slots / tail;
         if (sp > p.split_max) sp = p.split_max;
         if (sp > csteps / p.split_min_steps) sp = csteps / p.split_min_steps;
@@ -975,7 +1018,7 @@ constexpr int SPLIT_UNITS = 256, SPLIT_MAX = 8, SPLIT_MIN_STEPS = 64;
 constexpr size_t SPLIT_CNT_BYTES = SPLIT_UNITS * sizeof(int);
 constexpr size_t SPLIT_BYTES = SPLIT_CNT_BYTES + (size_t)SPLIT_UNITS * 256 * TN * sizeof(float);
 
-template <int KIND, bool DUAL, bool ACT, bool OUT16 = false, bool GATHER = false>
+template <int KIND, bool DUAL, bool ACT, bool OUT16 = false, bool GATHER = false, bool F8 = false>
 moe_status launch(const GemmParams& p, int64_t tiles_bound, hipStream_t stream, const char* name) {
   if (tiles_bound == 0) return MOE_SUCCESS;
   if (tiles_bound >= ((int64_t)1 << 31) - SPLIT_UNITS) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: too many tiles", name);
@@ -991,7 +1034,7 @@ moe_status launch(const GemmParams& p, int64_t tiles_bound, hipStream_t stream, 
     grid += SPLIT_UNITS;   // the split units run past the full rounds' tiles (idle ones exit)
   }
   static_assert(!GATHER || KIND == KIND_FWD, "gathered rows feed the forward product only");
-  grouped_gemm_kernel<KIND, DUAL, ACT, C::TM, C::WM, C::WN, C::NS, C::PP, C::WPE, C::PERSIST, OUT16, GATHER>
+  grouped_gemm_kernel<KIND, DUAL, ACT, C::TM, C::WM, C::WN, C::NS, C::PP, C::WPE, C::PERSIST, OUT16, GATHER, F8>
       <<<grid, 64 * C::WM * C::WN, 0, stream>>>(p);
   return check_launch(name);
 }
@@ -1136,6 +1179,36 @@ extern "C" moe_status moe_grouped_gemm_dx(const moe_bf16* dC, const moe_bf16* B,
 }
 
 extern "C" size_t moe_grouped_gemm_split_workspace_bytes(void) { return SPLIT_BYTES; }
+
+extern "C" moe_status moe_grouped_gemm_fwd_fp8(const uint8_t* A, const float* a_scale, const uint8_t* Wt,
+                                               const float* w_scale, const int32_t* offsets, int32_t G, int64_t R,
+                                               int64_t K, int64_t N, moe_bf16* C, void* workspace,
+                                               size_t workspace_bytes, hipStream_t stream) {
+  const char* fn = "moe_grouped_gemm_fwd_fp8";
+  if (G < 1 || G > 256) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: need 1 <= G <= 256", fn);
+  if (R < 0 || K <= 0 || N <= 0) return fail(MOE_ERROR_INVALID_VALUE, "%s: bad size", fn);
+  if (K % 64 || N % 64) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: K and N must be multiples of 64", fn);
+  if (R >= ((int64_t)1 << 31)) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: R >= 2^31", fn);
+  if (N * K >= ((int64_t)1 << 31)) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: one group's weight must be < 2 GiB", fn);
+  if (!offsets) return fail(MOE_ERROR_INVALID_VALUE, "%s: offsets is NULL", fn);
+  if (R == 0) return MOE_SUCCESS;
+  if (!A || !a_scale || !Wt || !w_scale || !C) return fail(MOE_ERROR_INVALID_VALUE, "%s: NULL pointer", fn);
+  if (bad_ptr(A) || bad_ptr(Wt) || bad_ptr(C) || bad_ptr(w_scale) || (reinterpret_cast<uintptr_t>(a_scale) & 3))
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: A, Wt, C, w_scale must be 16-byte aligned, a_scale 4-byte", fn);
+  // the dX-shaped product: rows of A (contraction K) against rows of Wt[g] (output columns N)
+  GemmParams p{};
+  p.a = reinterpret_cast<const uint16_t*>(A);
+  p.b = reinterpret_cast<const uint16_t*>(Wt);
+  p.offsets = offsets; p.out = C; p.a_scale = a_scale; p.w_scale = w_scale;
+  p.G = G; p.R = R; p.K = N; p.N = K;
+  constexpr int TM = Cfg<KIND_DX>::TM;
+  p.mt_bound = (int)((R + TM - 1) / TM + G);
+  p.n_tiles = (int)((N + TN - 1) / TN);
+  const int64_t tiles = (int64_t)p.mt_bound * p.n_tiles;
+  const moe_status st = attach_split(p, workspace, workspace_bytes, fn, stream);
+  if (st != MOE_SUCCESS) return st;
+  return launch<KIND_DX, false, false, false, false, true>(p, tiles, stream, "grouped_gemm_fwd_fp8");
+}
 
 extern "C" moe_status moe_grouped_gemm_dx_split(const moe_bf16* dC, const moe_bf16* B, const moe_bf16* dC2,
                                                 const moe_bf16* B2, const int32_t* offsets, int32_t G,

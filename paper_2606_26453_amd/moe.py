@@ -42,6 +42,9 @@ _SIG = {
     "moe_grouped_gemm_fwd_gather": (ctypes.c_int, [_P, _I64, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P,
                                                    _P, ctypes.c_size_t, _P]),
     "moe_gather_rows": (ctypes.c_int, [_P, _I64, _I64, _I32, _P, _P, _P]),
+    "moe_quantize_fp8_rows": (ctypes.c_int, [_P, _I64, _I64, _P, _P, _P]),
+    "moe_grouped_gemm_fwd_fp8": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P,
+                                                ctypes.c_size_t, _P]),
     "moe_swiglu": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _P]),
     "moe_swiglu_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _I64, _I64, _P]),
     "moe_unpermute_combine": (ctypes.c_int, [_P, _P, _P, _P, _I64, _I64, _I32, _P, _P]),
@@ -220,6 +223,40 @@ def moe_gather_rows(x, row_of_slot, k, x_perm=None, stream=None):
     _check("moe_gather_rows", lib().moe_gather_rows(_ptr(x), T, d, k, _ptr(row_of_slot), _ptr(x_perm),
                                                     _stream(stream)))
     return x_perm
+
+
+def moe_quantize_fp8_rows(x, q=None, scale=None, stream=None):
+    """Per-row E4M3 codes (uint8) and fp32 scales of the rows of x (any leading shape)."""
+    K = x.shape[-1]
+    M = x.numel() // K
+    if x.dtype != torch.bfloat16 or not x.is_contiguous():
+        raise ValueError("x must be a contiguous bf16 tensor")
+    q = torch.empty(x.shape, dtype=torch.uint8, device=x.device) if q is None else q
+    scale = torch.empty(x.shape[:-1], dtype=torch.float32, device=x.device) if scale is None else scale
+    _need(q, torch.uint8, tuple(x.shape), "q")
+    _need(scale, torch.float32, tuple(x.shape[:-1]), "scale")
+    _check("moe_quantize_fp8_rows", lib().moe_quantize_fp8_rows(_ptr(x), M, K, _ptr(q), _ptr(scale), _stream(stream)))
+    return q, scale
+
+
+def moe_grouped_gemm_fwd_fp8(A, a_scale, Wt, w_scale, offsets, C=None, stream=None, workspace=None):
+    """C = (A . Wt[g]^T) * a_scale * w_scale per group, bf16; A [R,K] and Wt [G,N,K] E4M3 codes."""
+    R, K = A.shape
+    G, N, K2 = Wt.shape
+    if K2 != K:
+        raise ValueError("A and Wt disagree on K")
+    _need(A, torch.uint8, (R, K), "A")
+    _need(a_scale, torch.float32, (R,), "a_scale")
+    _need(Wt, torch.uint8, (G, N, K), "Wt")
+    _need(w_scale, torch.float32, (G, N), "w_scale")
+    _need(offsets, torch.int32, (G + 1,), "offsets")
+    C = torch.empty((R, N), dtype=torch.bfloat16, device=A.device) if C is None else C
+    _need(C, torch.bfloat16, (R, N), "C")
+    st = lib().moe_grouped_gemm_fwd_fp8(_ptr(A), _ptr(a_scale), _ptr(Wt), _ptr(w_scale), _ptr(offsets), G, R, K, N,
+                                        _ptr(C), _ptr(workspace), 0 if workspace is None else workspace.numel(),
+                                        _stream(stream))
+    _check("moe_grouped_gemm_fwd_fp8", st)
+    return C
 
 
 def moe_swiglu(h_gate, h_up, act=None, stream=None):

@@ -101,6 +101,16 @@ def test_split_rejects():
     assert fwd(ws=None) == 3 and fwd(n=need // 2) == 3 and fwd(N=96) == 2
 
 
+def test_fp8_rejects():
+    L = moe.lib()
+    qz = lambda M=10, K=64, x=FAKE, q=FAKE: L.moe_quantize_fp8_rows(x, M, K, q, FAKE, None)
+    assert qz(K=24) == 2 and qz(x=None) == 1 and qz(x=BAD) == 1 and qz(q=FAKE + 4) == 1 and qz(M=0) == 0
+    f8 = lambda G=4, R=100, K=128, N=128, A=FAKE, sa=FAKE, ws=None, n=0: L.moe_grouped_gemm_fwd_fp8(
+        A, sa, FAKE, FAKE, FAKE, G, R, K, N, FAKE, ws, n, None)
+    assert f8(K=96) == 2 and f8(N=100) == 2 and f8(G=0) == 2 and f8(A=None) == 1 and f8(sa=None) == 1
+    assert f8(A=BAD) == 1 and f8(R=0) == 0 and f8(ws=FAKE, n=16) == 3
+
+
 def test_gather_rejects():
     L = moe.lib()
     fg = lambda T=50, src=FAKE, K=128, ws=None, n=0: L.moe_grouped_gemm_fwd_gather(
