@@ -26,6 +26,7 @@ if ROOT not in sys.path:
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 PEAK_FP32_VALU_TFLOPS = 157.3   # MI355X fp32 vector
+PEAK_FP8_TFLOPS = 5000.0    # MI355X dense fp8 MFMA
 METRIC = "MoE layer fwd+bwd tokens/sec + grouped-GEMM TFLOP/s (% of bf16 MFMA peak), 1 GPU"
 
 # HBM bytes per launch of each grouped GEMM on the Mixtral-shaped layer, from rocprofv3 FETCH_SIZE /
@@ -72,6 +73,9 @@ def _args():
     ap.add_argument("--aux-alpha", type=float, default=0.01, help="load-balancing loss weight with --router")
     ap.add_argument("--dw-transposed", action="store_true",
                     help="weight gradients from contraction-major copies of their operands")
+    ap.add_argument("--fp8-forward", action="store_true",
+                    help="the routed experts' forward products on E4M3 operands (a variant; the metric is bf16)")
+    ap.add_argument("--forward-only", action="store_true", help="time the forward alone (a variant)")
     ap.add_argument("--gather-fused", action="store_true",
                     help="gate/up product reads x through token_of_row; X_perm is gathered in the backward")
     ap.add_argument("--no-split-tail", action="store_true",
@@ -164,13 +168,14 @@ def main():
         inp = W.make_inputs(cfg, a.seed, dev)
         lay = L.MoELayer(cfg, inp, router=a.router, aux_alpha=a.aux_alpha if a.router else 0.0,
                          dw_transposed=a.dw_transposed, concurrent=a.concurrent, split_tail=not a.no_split_tail,
-                         gather_fused=a.gather_fused)
+                         gather_fused=a.gather_fused, fp8_forward=a.fp8_forward)
     torch.cuda.synchronize()
     t_gen = time.perf_counter() - t_gen
 
     stream = torch.cuda.current_stream()
+    step = lay.forward if (a.forward_only and not cfg.dw_only) else lay.step
     for _ in range(a.warmup):
-        lay.step()
+        step()
     torch.cuda.synchronize()
 
     lay.trace = None if a.no_trace else []
@@ -178,7 +183,7 @@ def main():
     torch.cuda.synchronize()
     start.record(stream)
     for _ in range(a.steps):
-        lay.step()
+        step()
     end.record(stream)
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(end)
@@ -200,6 +205,9 @@ def main():
             rec["frac_peak"] = round(amount / avg / 1e9 / PEAK_BF16_TFLOPS, 4)
             gemm_ms += avg
             gemm_flops += amount
+        elif kind == "flops8":
+            rec["tflops_fp8"] = round(amount / avg / 1e9, 1)
+            rec["frac_peak"] = round(amount / avg / 1e9 / PEAK_FP8_TFLOPS, 4)
         elif kind == "valu":
             rec["tflops_fp32"] = round(amount / avg / 1e9, 1)
             rec["frac_peak"] = round(amount / avg / 1e9 / PEAK_FP32_VALU_TFLOPS, 4)
@@ -213,11 +221,12 @@ def main():
         dom = max((n for n in per if work[n][0] != "valu"), key=lambda n: sum(per[n]))
         kind, amount = work[dom]
         avg = sum(per[dom]) / len(per[dom])
-        if kind == "flops":
+        if kind in ("flops", "flops8"):
             ach = amount / avg / 1e9
-            roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 1), "peak": PEAK_BF16_TFLOPS,
-                        "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
-                        "traffic": measured_traffic(dom, a.config),
+            peak = PEAK_BF16_TFLOPS if kind == "flops" else PEAK_FP8_TFLOPS
+            roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 1), "peak": peak,
+                        "unit": "TFLOP/s", "frac": round(ach / peak, 4),
+                        "traffic": measured_traffic(dom, a.config) if kind == "flops" else None,
                         "work_per_launch": amount, "avg_launch_ms": round(avg, 4)}
         else:
             ach = amount / avg / 1e6
@@ -232,20 +241,23 @@ def main():
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
         "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms_per_step, 4),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "fp8-e4m3 (forward expert products) + bf16" if a.fp8_forward else "bf16",
         "data": "synthetic (seeded N(0,1) activations, N(0,0.02) weights, router logits X.Wr)",
-        "config": {"workload": workload_name(a.config, cfg, a.router and not cfg.dw_only),
+        "config": {"workload": workload_name(a.config, cfg, a.router and not cfg.dw_only)
+                   + (" (forward only)" if a.forward_only and not cfg.dw_only else "")
+                   + (", expert forward products in FP8 E4M3" if a.fp8_forward else ""),
                    "T": cfg.T, "d": cfg.d, "f": cfg.f, "E": cfg.E, "k": cfg.k, "f_shared": cfg.f_shared,
                    "parallelism": "single GPU"},
         "gemm_tflops": round(gemm_flops / gemm_ms / 1e9, 1) if gemm_ms else None,
         "gemm_frac_peak": round(gemm_flops / gemm_ms / 1e9 / PEAK_BF16_TFLOPS, 4) if gemm_ms else None,
-        "gemm_tflops_step": round(cfg.gemm_flops() / (ms_per_step / 1e3) / 1e12, 1),
+        "gemm_tflops_step": round(cfg.gemm_flops() * (1 / 3 if a.forward_only else 1) / (ms_per_step / 1e3) / 1e12, 1),
         "calls": calls,
         "roofline": roofline,
         "groups": W.group_stats(counts),
         "input_gen_s": round(t_gen, 1),
     }
-    if not a.no_cpu_baseline and not cfg.dw_only:
+    if not a.no_cpu_baseline and not cfg.dw_only and not (a.fp8_forward or a.forward_only):
         ts = a.cpu_sample_tokens or max(8, min(cfg.T, int(6e12 // (18 * cfg.k * cfg.d * cfg.f))))
         out["cpu_baseline"] = cpu_baseline(cfg, inp, ts)
     print(json.dumps(out), flush=True)

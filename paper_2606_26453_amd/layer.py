@@ -46,8 +46,14 @@ class MoELayer(_Traced):
 
     def __init__(self, cfg, inputs: dict, normalize_topk: bool = True, fuse_swiglu_bwd: bool = True,
                  router: bool = False, aux_alpha: float = 0.0, dw_transposed: bool = False,
-                 concurrent: bool = False, split_tail: bool = True, gather_fused: bool = False):
+                 concurrent: bool = False, split_tail: bool = True, gather_fused: bool = False,
+                 fp8_forward: bool = False):
         self.cfg = cfg
+        # fp8_forward: the routed experts' forward products run on E4M3 operands (activations
+        # quantized per row each step, weights per output channel once, here): gate and up as two
+        # FP8 products, the SwiGLU as its own pass, the down product on the quantized SwiGLU
+        # output; everything else (shared FFN, backward) stays bf16
+        self.fp8 = fp8_forward
         # gather_fused: the gate/up product reads its rows straight from x through token_of_row
         # (moe_grouped_gemm_fwd_gather); X_perm is then gathered only in the backward, for dW_gate
         # and dW_up (moe_gather_rows), so a forward alone never writes it
@@ -92,6 +98,18 @@ class MoELayer(_Traced):
                 "router_ws": e(max(16, moe.lib().moe_router_bwd_workspace_bytes(T, d, E)), torch.uint8),
                 "aux_ws": e(max(16, moe.lib().moe_router_aux_loss_workspace_bytes(T, E)), torch.uint8),
             })
+        if fp8_forward:
+            if gather_fused:
+                raise ValueError("fp8_forward reads X_perm: it does not combine with gather_fused")
+            u8 = torch.uint8
+            b.update({"x_q": e((R, d), u8), "x_s": e(R, f32), "act_q": e((R, f), u8), "act_s": e(R, f32)})
+            # weights in the layout [expert, output channel, contraction], quantized per channel
+            # (a one-off preparation outside the step)
+            self.w8 = {}
+            for name, w in (("gate", inputs["w_gate"]), ("up", inputs["w_up"]), ("down", inputs["w_down"])):
+                wt = w.transpose(1, 2).contiguous()
+                self.w8[name] = moe.moe_quantize_fp8_rows(wt)
+                del wt
         self.shared = cfg.f_shared > 0
         if self.shared:
             fs = cfg.f_shared
@@ -142,15 +160,27 @@ class MoELayer(_Traced):
         if self.router and self.aux_alpha:
             run("router_aux_loss", moe.moe_router_aux_loss, logits, b["offsets"], k, self.aux_alpha,
                 loss=b["aux_loss"], workspace=b["aux_ws"], stream=stream)
-        if gf:
+        if self.fp8:
+            ws = self.split_ws
+            run("quantize_x", moe.moe_quantize_fp8_rows, b["x_perm"], b["x_q"], b["x_s"], stream=stream)
+            run("fwd_gate", moe.moe_grouped_gemm_fwd_fp8, b["x_q"], b["x_s"], *self.w8["gate"], b["offsets"],
+                C=b["h_gate"], stream=stream, workspace=ws)
+            run("fwd_up", moe.moe_grouped_gemm_fwd_fp8, b["x_q"], b["x_s"], *self.w8["up"], b["offsets"],
+                C=b["h_up"], stream=stream, workspace=ws)
+            run("swiglu", moe.moe_swiglu, b["h_gate"], b["h_up"], b["act"], stream=stream)
+            run("quantize_act", moe.moe_quantize_fp8_rows, b["act"], b["act_q"], b["act_s"], stream=stream)
+            run("fwd_down", moe.moe_grouped_gemm_fwd_fp8, b["act_q"], b["act_s"], *self.w8["down"], b["offsets"],
+                C=b["y_perm"], stream=stream, workspace=ws)
+        elif gf:
             run("fwd_gate_up", moe.moe_grouped_gemm_fwd_gather, i["x"], b["token_of_row"], i["w_gate"],
                 b["offsets"], i["w_up"], b["h_gate"], b["h_up"], b["act"], want_act=True, stream=stream,
                 workspace=self.split_ws)
         else:
             run("fwd_gate_up", moe.moe_grouped_gemm_fwd, b["x_perm"], i["w_gate"], b["offsets"], i["w_up"],
                 b["h_gate"], b["h_up"], b["act"], want_act=True, stream=stream, workspace=self.split_ws)
-        run("fwd_down", moe.moe_grouped_gemm_fwd, b["act"], i["w_down"], b["offsets"], C=b["y_perm"],
-            stream=stream, workspace=self.split_ws)
+        if not self.fp8:
+            run("fwd_down", moe.moe_grouped_gemm_fwd, b["act"], i["w_down"], b["offsets"], C=b["y_perm"],
+                stream=stream, workspace=self.split_ws)
         self._join(main, side)
         run("combine", moe.moe_unpermute_combine, b["y_perm"], b["topk_w"], b["row_of_slot"], k, add=add,
             y=b["y"], stream=stream)
@@ -246,7 +276,11 @@ class MoELayer(_Traced):
             "route_permute": ("bytes", T * E * 4 + T * k * 8 + R * 8
                               + (0 if self.gather_fused else T * d * 2 + R * d * 2)),
             "gather_x": ("bytes", T * d * 2 + R * d * 2 + R * 4),
-            "fwd_gate_up": ("flops", 4 * R * d * f), "fwd_down": ("flops", 2 * R * f * d),
+            # FP8 forward: E4M3 products (8-bit MFMA work), quantizers and the standalone SwiGLU
+            "fwd_gate": ("flops8", 2 * R * d * f), "fwd_up": ("flops8", 2 * R * d * f),
+            "quantize_x": ("bytes", R * d * 3 + R * 4), "quantize_act": ("bytes", R * f * 3 + R * 4),
+            "swiglu": ("bytes", 3 * R * f * 2),
+            "fwd_gate_up": ("flops", 4 * R * d * f), "fwd_down": ("flops8" if self.fp8 else "flops", 2 * R * f * d),
             "combine": ("bytes", R * d * 2 + T * d * 2 + T * k * 8 + (T * d * 2 if self.shared else 0)),
             "combine_bwd": ("bytes", T * d * 2 + 2 * R * d * 2 + T * k * 12),
             "dx_down": ("flops", 2 * R * d * f), "dw_down": ("flops", 2 * R * f * d),

@@ -119,3 +119,56 @@ def test_grouped_gemm_fp8_quantized_gaussian(K, N):
     err = O.rel_fro(f64(C), exact)
     _say(f"fp8 vs unquantized bf16 product: relative Frobenius {err:.3e}")
     assert err < 0.1
+
+
+@pytest.mark.parametrize("cfg_id", [0, 2])
+def test_layer_fp8_forward(cfg_id):
+    """The layer with its expert forward products in FP8, checked stage by stage on the GPU's own
+    intermediate tensors: the per-channel weight codes and the per-row activation codes bit for
+    bit, each FP8 product and the SwiGLU against the oracle on the same codes, Y against the
+    combine, and the (bf16) backward against the oracle's backward of those forward tensors; the
+    deviation of Y from the all-bf16 oracle forward is reported.  Config 2 at 1024 tokens."""
+    import dataclasses
+    from paper_2606_26453_amd import layer as L, workloads as W
+    cfg = W.CONFIGS[cfg_id]
+    if cfg_id:
+        cfg = dataclasses.replace(cfg, T=1024)
+    _say("layer fp8 forward", cfg)
+    inp = W.make_inputs(cfg, 0, "cpu")
+    lay = L.MoELayer(cfg, {k_: v.to(DEV) for k_, v in inp.items()}, fp8_forward=True)
+    lay.step()
+    torch.cuda.synchronize()
+    b = lay.buf
+    wg, wu, wd = (f64(inp[n]) for n in ("w_gate", "w_up", "w_down"))
+    for name, w in (("gate", wg), ("up", wu), ("down", wd)):
+        q, s = O.quantize_rows_fp8(np.transpose(w, (0, 2, 1)))
+        np.testing.assert_array_equal(_u8(lay.w8[name][0]), q)
+        np.testing.assert_array_equal(lay.w8[name][1].cpu().numpy(), s)
+    off = b["offsets"].cpu().numpy()
+    xq, xs = O.quantize_rows_fp8(f64(b["x_perm"]))
+    np.testing.assert_array_equal(_u8(b["x_q"]), xq)
+    np.testing.assert_array_equal(b["x_s"].cpu().numpy(), xs)
+    gq, gs = (t.cpu().numpy() for t in lay.w8["gate"])
+    uq, us = (t.cpu().numpy() for t in lay.w8["up"])
+    dq, ds = (t.cpu().numpy() for t in lay.w8["down"])
+    check_float("h_gate", f64(b["h_gate"]), O.grouped_gemm_fp8(xq, xs, gq, gs, off), 2e-3)
+    check_float("h_up", f64(b["h_up"]), O.grouped_gemm_fp8(xq, xs, uq, us, off), 2e-3)
+    check_float("act", f64(b["act"]), O.swiglu(f64(b["h_gate"]), f64(b["h_up"])), 2e-3)
+    aq, as_ = O.quantize_rows_fp8(f64(b["act"]))
+    np.testing.assert_array_equal(_u8(b["act_q"]), aq)
+    np.testing.assert_array_equal(b["act_s"].cpu().numpy(), as_)
+    check_float("y_perm", f64(b["y_perm"]), O.grouped_gemm_fp8(aq, as_, dq, ds, off), 2e-3)
+    x = f64(inp["x"])
+    shared = None
+    if cfg.f_shared:
+        shared = tuple(f64(inp[n]) for n in ("w_gate_sh", "w_up_sh", "w_down_sh"))
+    ref = O.layer_forward(x, inp["logits"].numpy(), wg, wu, wd, cfg.k, shared=shared)
+    fwd = dict(ref)
+    for key in ("h_gate", "h_up", "act", "y_perm"):
+        fwd[key] = f64(b[key])
+    y_sh = ref["shared"]["y"] if shared else None
+    check_float("y", f64(b["y"]), O.combine(fwd["y_perm"], ref["topk_w"], ref["row_of_slot"], cfg.k, add=y_sh))
+    bwd = O.layer_backward(fwd, x, f64(inp["dy"]), wg, wu, wd, shared=shared)
+    for key in ("dh_gate", "dh_up", "dx_perm", "dw_gate", "dw_up", "dw_down", "dx"):
+        check_float(key, f64(b[key]), bwd[key])
+    _say(f"fp8 forward Y vs the all-bf16 oracle: relative Frobenius {O.rel_fro(f64(b['y']), ref['y']):.3e}")
