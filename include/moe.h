@@ -259,6 +259,21 @@ moe_status moe_grouped_gemm_fwd_fp8(const uint8_t* A, const float* a_scale, cons
                                     const int32_t* offsets, int32_t G, int64_t R, int64_t K, int64_t N, moe_bf16* C,
                                     void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * The gate and up projections (steps B + C) on E4M3 operands in one product: Wt [G, 2F, K] holds
+ * both weights with their output channels interleaved by 128 (rows 256t .. 256t+127 are gate
+ * channels 128t .., the next 128 rows the up channels 128t ..; w_scale [G, 2F] in the same order),
+ * so each 256-column tile computes 128 gate and the matching 128 up columns.  h_gate, h_up [R, F]
+ * bf16 as moe_grouped_gemm_fwd_fp8 would compute them from the de-interleaved weights (bit for
+ * bit), and, if act is non-NULL, act = silu(h_gate) * h_up from the rounded values exactly as
+ * moe_swiglu computes it.  F a multiple of 128, K of 64; other arguments and errors as
+ * moe_grouped_gemm_fwd_fp8.
+ */
+moe_status moe_grouped_gemm_fwd_fp8_gate_up(const uint8_t* A, const float* a_scale, const uint8_t* Wt,
+                                            const float* w_scale, const int32_t* offsets, int32_t G, int64_t R,
+                                            int64_t K, int64_t F, moe_bf16* h_gate, moe_bf16* h_up, moe_bf16* act,
+                                            void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 moe_status moe_grouped_gemm_fwd_split(const moe_bf16* A, const moe_bf16* B, const moe_bf16* B2,
                                       const int32_t* offsets, int32_t G, int64_t R, int64_t K, int64_t N,
                                       moe_bf16* C, moe_bf16* C2, moe_bf16* act, void* workspace,

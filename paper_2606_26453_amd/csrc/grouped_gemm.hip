@@ -169,7 +169,9 @@ __device__ __forceinline__ void band_order(int id, int mtiles, int ntiles, int& 
 template <int KIND, bool DUAL, bool ACT, int TM, int WAVES_M, int WAVES_N, int NSTAGE, bool PINGPONG, int WPE,
           bool PERSIST, bool OUT16, bool GATHER, bool F8>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kernel(GemmParams p) {
-  static_assert(!F8 || (KIND == KIND_DX && !DUAL && !ACT), "FP8 operands: the single dX-shaped product only");
+  // F8 && DUAL: one weight whose output channels interleave gate and up by 128 (tile columns
+  // 0..127 gate, 128..255 up), stored as two outputs (+ SwiGLU with ACT) like the fwd dual product
+  static_assert(!F8 || (KIND == KIND_DX && (DUAL || !ACT)), "FP8 operands: the dX-shaped product");
   constexpr int ES = F8 ? 1 : 2;              // bytes per operand element
   constexpr int BKE = F8 ? 2 * BK : BK;       // contraction elements per stage (64-byte rows)
   constexpr int NWAVE = WAVES_M * WAVES_N;
@@ -347,7 +349,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
         }
       } else {
         m_src = reinterpret_cast<const char*>(p.a) + row_lo * m_ld * ES;
-        if constexpr (KIND == KIND_DX && DUAL) m_src2 = reinterpret_cast<const char*>(p.a2) + row_lo * m_ld * ES;
+        if constexpr (KIND == KIND_DX && DUAL && !F8) m_src2 = reinterpret_cast<const char*>(p.a2) + row_lo * m_ld * ES;
 #pragma unroll
         for (int i = 0; i < DPW_M; ++i) {
           int64_t r = 16 * (DPW_M * wave + i) + (lane >> 2);
@@ -428,7 +430,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
 
     // contraction extent
     if constexpr (KIND == KIND_FWD) c_len = p.K;
-    else if constexpr (KIND == KIND_DX) c_len = DUAL ? 2 * p.N : p.N;
+    else if constexpr (KIND == KIND_DX) c_len = (DUAL && !F8) ? 2 * p.N : p.N;
     else c_len = row_hi - row_lo;
     nsteps = (int)((c_len + BKE - 1) / BKE);
     c_len32 = (int)c_len;
@@ -446,7 +448,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
     if constexpr (!M_T) {
       int64_t cc = (int64_t)sa * BKE;
       const char* base = m_src;
-      if constexpr (KIND == KIND_DX && DUAL) {
+      if constexpr (KIND == KIND_DX && DUAL && !F8) {
         const bool second = cc >= p.N;
         base = second ? m_src2 : m_src;
         cc = second ? cc - p.N : cc;
@@ -467,7 +469,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
     if constexpr (!N_T) {
       int64_t cc = (int64_t)sa * BKE;
       const char* base = n_src;
-      if constexpr (DUAL && KIND == KIND_DX) {
+      if constexpr (DUAL && KIND == KIND_DX && !F8) {
         const bool second = cc >= p.N;
         base = second ? n_src2 : n_src;
         cc = second ? cc - p.N : cc;
@@ -726,7 +728,8 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
     static_assert(TM * TN * 2 <= NSTAGE * STAGE, "the bf16 tile fits in the ring");
     // the dual fwd and dW products have two outputs side by side in their tile; the dual dX
     // product sums both contractions into one output
-    constexpr bool SPLIT = (KIND != KIND_DX) && DUAL;
+    constexpr bool SPLIT = DUAL && (KIND != KIND_DX || F8);       // two outputs side by side in the tile
+    constexpr bool ACC_SPLIT = DUAL && (KIND != KIND_DX);         // ... within each wave's columns
     // output rows of the tile: fwd/dX the permuted rows row_lo .. row_hi-1; dW rows mt*TM .. of
     // dB[g] (at most K)
     int64_t obase = 0;
@@ -744,7 +747,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           int c;
-          if constexpr (SPLIT) c = (j >= NB / 2 ? 16 : 0) + (wn * (WTN / 2) + 32 * (j % (NB / 2)) + 8 * q) / 8;
+          if constexpr (ACC_SPLIT) c = (j >= NB / 2 ? 16 : 0) + (wn * (WTN / 2) + 32 * (j % (NB / 2)) + 8 * q) / 8;
           else c = (wn * WTN + 32 * j + 8 * q) / 8;
           uint2 v;
           if constexpr (F8) {
@@ -769,24 +772,25 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
     constexpr int NT = 64 * NWAVE;
     auto chunk = [&](int t, int c) { return *reinterpret_cast<const u32x4*>(lds + t * 512 + 16 * (c ^ (t & 31))); };
     if constexpr (SPLIT) {
-      // FWD gate/up (+ SwiGLU): thread -> gate chunk c and up chunk 16 + c of rows t, t + NT/16, ...
+      // FWD gate/up and FP8 interleaved gate/up (+ SwiGLU): thread -> gate chunk c and up chunk 16 + c of rows t, t + NT/16, ...
       const int c = tid & 15;
+      const int64_t Wo = F8 ? p.K / 2 : p.N;   // width of each output
       const int64_t n = (int64_t)nt * (TN / 2) + 8 * c;
-      if (n < p.N) {
+      if (n < Wo) {
         uint16_t* c1 = static_cast<uint16_t*>(p.out) + obase + n;
         uint16_t* c2 = static_cast<uint16_t*>(p.out2) + obase + n;
         for (int t = tid >> 4; t < TM; t += NT / 16) {
           const int64_t r = row_lo + t;
           if (r >= row_hi) break;
           const u32x4 vg = chunk(t, c), vu = chunk(t, 16 + c);
-          *reinterpret_cast<u32x4*>(c1 + r * p.N) = vg;
-          *reinterpret_cast<u32x4*>(c2 + r * p.N) = vu;
+          *reinterpret_cast<u32x4*>(c1 + r * Wo) = vg;
+          *reinterpret_cast<u32x4*>(c2 + r * Wo) = vu;
           if constexpr (ACT) {
             u32x4 va;
 #pragma unroll
             for (int e = 0; e < 4; ++e)
               va[e] = pack_bf16(silu_f32(bf16_lo(vg[e])) * bf16_lo(vu[e]), silu_f32(bf16_hi(vg[e])) * bf16_hi(vu[e]));
-            *reinterpret_cast<u32x4*>(p.act + r * p.N + n) = va;
+            *reinterpret_cast<u32x4*>(p.act + r * Wo + n) = va;
           }
         }
       }
@@ -860,7 +864,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
         // split_min_steps long (short pieces cost more in partial-tile traffic than they save)
         int64_t clen;
         if constexpr (KIND == KIND_FWD) clen = p.K;
-        else clen = DUAL ? 2 * p.N : p.N;
+        else clen = (DUAL && !F8) ? 2 * p.N : p.N;
         const int csteps = (int)((clen + BKE - 1) / BKE);
         int sp = slots / tail;
         if (sp > p.split_max) sp = p.split_max;
@@ -1179,6 +1183,38 @@ extern "C" moe_status moe_grouped_gemm_dx(const moe_bf16* dC, const moe_bf16* B,
 }
 
 extern "C" size_t moe_grouped_gemm_split_workspace_bytes(void) { return SPLIT_BYTES; }
+
+extern "C" moe_status moe_grouped_gemm_fwd_fp8_gate_up(const uint8_t* A, const float* a_scale, const uint8_t* Wt,
+                                                       const float* w_scale, const int32_t* offsets, int32_t G,
+                                                       int64_t R, int64_t K, int64_t F, moe_bf16* h_gate,
+                                                       moe_bf16* h_up, moe_bf16* act, void* workspace,
+                                                       size_t workspace_bytes, hipStream_t stream) {
+  const char* fn = "moe_grouped_gemm_fwd_fp8_gate_up";
+  if (G < 1 || G > 256) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: need 1 <= G <= 256", fn);
+  if (R < 0 || K <= 0 || F <= 0) return fail(MOE_ERROR_INVALID_VALUE, "%s: bad size", fn);
+  if (K % 64 || F % 128) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: K must be a multiple of 64, F of 128", fn);
+  if (R >= ((int64_t)1 << 31)) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: R >= 2^31", fn);
+  if (2 * F * K >= ((int64_t)1 << 31)) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: one group's weight must be < 2 GiB", fn);
+  if (!offsets) return fail(MOE_ERROR_INVALID_VALUE, "%s: offsets is NULL", fn);
+  if (R == 0) return MOE_SUCCESS;
+  if (!A || !a_scale || !Wt || !w_scale || !h_gate || !h_up) return fail(MOE_ERROR_INVALID_VALUE, "%s: NULL pointer", fn);
+  if (bad_ptr(A) || bad_ptr(Wt) || bad_ptr(h_gate) || bad_ptr(h_up) || bad_ptr(act) || bad_ptr(w_scale) ||
+      (reinterpret_cast<uintptr_t>(a_scale) & 3))
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: pointers must be 16-byte aligned (a_scale 4-byte)", fn);
+  GemmParams p{};
+  p.a = reinterpret_cast<const uint16_t*>(A);
+  p.b = reinterpret_cast<const uint16_t*>(Wt);
+  p.offsets = offsets; p.out = h_gate; p.out2 = h_up; p.act = act; p.a_scale = a_scale; p.w_scale = w_scale;
+  p.G = G; p.R = R; p.K = 2 * F; p.N = K;
+  constexpr int TM = Cfg<KIND_DX>::TM;
+  p.mt_bound = (int)((R + TM - 1) / TM + G);
+  p.n_tiles = (int)((2 * F + TN - 1) / TN);
+  const int64_t tiles = (int64_t)p.mt_bound * p.n_tiles;
+  const moe_status st = attach_split(p, workspace, workspace_bytes, fn, stream);
+  if (st != MOE_SUCCESS) return st;
+  if (act) return launch<KIND_DX, true, true, false, false, true>(p, tiles, stream, "grouped_gemm_fwd_fp8(gate_up,swiglu)");
+  return launch<KIND_DX, true, false, false, false, true>(p, tiles, stream, "grouped_gemm_fwd_fp8(gate_up)");
+}
 
 extern "C" moe_status moe_grouped_gemm_fwd_fp8(const uint8_t* A, const float* a_scale, const uint8_t* Wt,
                                                const float* w_scale, const int32_t* offsets, int32_t G, int64_t R,

@@ -50,9 +50,10 @@ class MoELayer(_Traced):
                  fp8_forward: bool = False):
         self.cfg = cfg
         # fp8_forward: the routed experts' forward products run on E4M3 operands (activations
-        # quantized per row each step, weights per output channel once, here): gate and up as two
-        # FP8 products, the SwiGLU as its own pass, the down product on the quantized SwiGLU
-        # output; everything else (shared FFN, backward) stays bf16
+        # quantized per row each step, weights per output channel once, here): gate and up in one
+        # product over their 128-channel-interleaved weights with the SwiGLU in its epilogue, then
+        # the down product on the quantized SwiGLU output; everything else (shared FFN, backward)
+        # stays bf16
         self.fp8 = fp8_forward
         # gather_fused: the gate/up product reads its rows straight from x through token_of_row
         # (moe_grouped_gemm_fwd_gather); X_perm is then gathered only in the backward, for dW_gate
@@ -106,10 +107,11 @@ class MoELayer(_Traced):
             # weights in the layout [expert, output channel, contraction], quantized per channel
             # (a one-off preparation outside the step)
             self.w8 = {}
-            for name, w in (("gate", inputs["w_gate"]), ("up", inputs["w_up"]), ("down", inputs["w_down"])):
-                wt = w.transpose(1, 2).contiguous()
-                self.w8[name] = moe.moe_quantize_fp8_rows(wt)
-                del wt
+            wg_t = inputs["w_gate"].transpose(1, 2).contiguous()
+            wu_t = inputs["w_up"].transpose(1, 2).contiguous()
+            self.w8["gate_up"] = moe.moe_quantize_fp8_rows(moe.interleave_gate_up(wg_t, wu_t))
+            del wg_t, wu_t
+            self.w8["down"] = moe.moe_quantize_fp8_rows(inputs["w_down"].transpose(1, 2).contiguous())
         self.shared = cfg.f_shared > 0
         if self.shared:
             fs = cfg.f_shared
@@ -163,11 +165,8 @@ class MoELayer(_Traced):
         if self.fp8:
             ws = self.split_ws
             run("quantize_x", moe.moe_quantize_fp8_rows, b["x_perm"], b["x_q"], b["x_s"], stream=stream)
-            run("fwd_gate", moe.moe_grouped_gemm_fwd_fp8, b["x_q"], b["x_s"], *self.w8["gate"], b["offsets"],
-                C=b["h_gate"], stream=stream, workspace=ws)
-            run("fwd_up", moe.moe_grouped_gemm_fwd_fp8, b["x_q"], b["x_s"], *self.w8["up"], b["offsets"],
-                C=b["h_up"], stream=stream, workspace=ws)
-            run("swiglu", moe.moe_swiglu, b["h_gate"], b["h_up"], b["act"], stream=stream)
+            run("fwd_gate_up", moe.moe_grouped_gemm_fwd_fp8_gate_up, b["x_q"], b["x_s"], *self.w8["gate_up"],
+                b["offsets"], b["h_gate"], b["h_up"], b["act"], stream=stream, workspace=ws)
             run("quantize_act", moe.moe_quantize_fp8_rows, b["act"], b["act_q"], b["act_s"], stream=stream)
             run("fwd_down", moe.moe_grouped_gemm_fwd_fp8, b["act_q"], b["act_s"], *self.w8["down"], b["offsets"],
                 C=b["y_perm"], stream=stream, workspace=ws)
@@ -277,10 +276,9 @@ class MoELayer(_Traced):
                               + (0 if self.gather_fused else T * d * 2 + R * d * 2)),
             "gather_x": ("bytes", T * d * 2 + R * d * 2 + R * 4),
             # FP8 forward: E4M3 products (8-bit MFMA work), quantizers and the standalone SwiGLU
-            "fwd_gate": ("flops8", 2 * R * d * f), "fwd_up": ("flops8", 2 * R * d * f),
             "quantize_x": ("bytes", R * d * 3 + R * 4), "quantize_act": ("bytes", R * f * 3 + R * 4),
-            "swiglu": ("bytes", 3 * R * f * 2),
-            "fwd_gate_up": ("flops", 4 * R * d * f), "fwd_down": ("flops8" if self.fp8 else "flops", 2 * R * f * d),
+            "fwd_gate_up": ("flops8" if self.fp8 else "flops", 4 * R * d * f),
+            "fwd_down": ("flops8" if self.fp8 else "flops", 2 * R * f * d),
             "combine": ("bytes", R * d * 2 + T * d * 2 + T * k * 8 + (T * d * 2 if self.shared else 0)),
             "combine_bwd": ("bytes", T * d * 2 + 2 * R * d * 2 + T * k * 12),
             "dx_down": ("flops", 2 * R * d * f), "dw_down": ("flops", 2 * R * f * d),

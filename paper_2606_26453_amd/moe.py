@@ -45,6 +45,8 @@ _SIG = {
     "moe_quantize_fp8_rows": (ctypes.c_int, [_P, _I64, _I64, _P, _P, _P]),
     "moe_grouped_gemm_fwd_fp8": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P,
                                                 ctypes.c_size_t, _P]),
+    "moe_grouped_gemm_fwd_fp8_gate_up": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P, _P,
+                                                        ctypes.c_size_t, _P]),
     "moe_swiglu": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _P]),
     "moe_swiglu_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _I64, _I64, _P]),
     "moe_unpermute_combine": (ctypes.c_int, [_P, _P, _P, _P, _I64, _I64, _I32, _P, _P]),
@@ -257,6 +259,45 @@ def moe_grouped_gemm_fwd_fp8(A, a_scale, Wt, w_scale, offsets, C=None, stream=No
                                         _stream(stream))
     _check("moe_grouped_gemm_fwd_fp8", st)
     return C
+
+
+def interleave_gate_up(w_gate_t, w_up_t):
+    """[G, F, K] gate and up weights (output channel, contraction) -> [G, 2F, K] with the channels
+    interleaved by 128 (rows 256t .. 256t+127: gate channels 128t ..; the next 128: up channels),
+    the layout moe_grouped_gemm_fwd_fp8_gate_up reads (a one-off weight preparation)."""
+    G, F, K = w_gate_t.shape
+    if F % 128:
+        raise ValueError("F must be a multiple of 128")
+    g = w_gate_t.reshape(G, F // 128, 128, K)
+    u = w_up_t.reshape(G, F // 128, 128, K)
+    return torch.cat([g, u], dim=2).reshape(G, 2 * F, K).contiguous()
+
+
+def moe_grouped_gemm_fwd_fp8_gate_up(A, a_scale, Wt_gu, w_scale_gu, offsets, h_gate=None, h_up=None, act=None,
+                                     want_act=True, stream=None, workspace=None):
+    """Gate and up projections from one E4M3 weight interleaved by 128 channels, + SwiGLU."""
+    R, K = A.shape
+    G, F2, K2 = Wt_gu.shape
+    if K2 != K or F2 % 256:
+        raise ValueError("bad shapes")
+    F = F2 // 2
+    _need(A, torch.uint8, (R, K), "A")
+    _need(a_scale, torch.float32, (R,), "a_scale")
+    _need(Wt_gu, torch.uint8, (G, F2, K), "Wt_gu")
+    _need(w_scale_gu, torch.float32, (G, F2), "w_scale_gu")
+    _need(offsets, torch.int32, (G + 1,), "offsets")
+    dev = A.device
+    h_gate = torch.empty((R, F), dtype=torch.bfloat16, device=dev) if h_gate is None else h_gate
+    h_up = torch.empty((R, F), dtype=torch.bfloat16, device=dev) if h_up is None else h_up
+    if want_act and act is None:
+        act = torch.empty((R, F), dtype=torch.bfloat16, device=dev)
+    for t, n in ((h_gate, "h_gate"), (h_up, "h_up"), (act, "act")):
+        _need(t, torch.bfloat16, (R, F), n)
+    st = lib().moe_grouped_gemm_fwd_fp8_gate_up(_ptr(A), _ptr(a_scale), _ptr(Wt_gu), _ptr(w_scale_gu), _ptr(offsets),
+                                                G, R, K, F, _ptr(h_gate), _ptr(h_up), _ptr(act), _ptr(workspace),
+                                                0 if workspace is None else workspace.numel(), _stream(stream))
+    _check("moe_grouped_gemm_fwd_fp8_gate_up", st)
+    return h_gate, h_up, act
 
 
 def moe_swiglu(h_gate, h_up, act=None, stream=None):

@@ -109,6 +109,9 @@ def test_fp8_rejects():
         A, sa, FAKE, FAKE, FAKE, G, R, K, N, FAKE, ws, n, None)
     assert f8(K=96) == 2 and f8(N=100) == 2 and f8(G=0) == 2 and f8(A=None) == 1 and f8(sa=None) == 1
     assert f8(A=BAD) == 1 and f8(R=0) == 0 and f8(ws=FAKE, n=16) == 3
+    gu = lambda F=128, K=128, act=FAKE, hg=FAKE: L.moe_grouped_gemm_fwd_fp8_gate_up(
+        FAKE, FAKE, FAKE, FAKE, FAKE, 4, 100, K, F, hg, FAKE, act, None, 0, None)
+    assert gu(F=64) == 2 and gu(K=96) == 2 and gu(hg=None) == 1 and gu(act=BAD) == 1
 
 
 def test_gather_rejects():

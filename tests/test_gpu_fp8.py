@@ -121,6 +121,33 @@ def test_grouped_gemm_fp8_quantized_gaussian(K, N):
     assert err < 0.1
 
 
+@pytest.mark.parametrize("K,F", [(64, 128), (512, 384), (2048, 1408)])
+def test_grouped_gemm_fp8_gate_up(K, F):
+    """The gate/up product over the 128-channel-interleaved weight equals the two separate FP8
+    products bit for bit (same codes, scales and accumulation order per output), and its SwiGLU
+    equals moe_swiglu on those outputs bit for bit; with and without the split tail."""
+    _say("gemm fp8 gate/up", K, F)
+    g = torch.Generator().manual_seed(K + F)
+    G, R = len(GROUPS), sum(GROUPS)
+    off = torch.tensor(np.concatenate([[0], np.cumsum(GROUPS)]), dtype=torch.int32, device=DEV)
+    x = torch.randn((R, K), generator=g).to(torch.bfloat16).to(DEV)
+    wg = (torch.randn((G, F, K), generator=g) * 0.05).to(torch.bfloat16).to(DEV)
+    wu = (torch.randn((G, F, K), generator=g) * 0.05).to(torch.bfloat16).to(DEV)
+    aq, sa = moe.moe_quantize_fp8_rows(x)
+    gq, gs = moe.moe_quantize_fp8_rows(wg)
+    uq, us = moe.moe_quantize_fp8_rows(wu)
+    iq, is_ = moe.moe_quantize_fp8_rows(moe.interleave_gate_up(wg, wu))
+    hg = moe.moe_grouped_gemm_fwd_fp8(aq, sa, gq, gs, off)
+    hu = moe.moe_grouped_gemm_fwd_fp8(aq, sa, uq, us, off)
+    act = moe.moe_swiglu(hg, hu)
+    for ws in (None, moe.split_workspace(DEV)):
+        h1, h2, a1 = moe.moe_grouped_gemm_fwd_fp8_gate_up(aq, sa, iq, is_, off, workspace=ws)
+        torch.cuda.synchronize()
+        assert torch.equal(h1.view(torch.int16), hg.view(torch.int16))
+        assert torch.equal(h2.view(torch.int16), hu.view(torch.int16))
+        assert torch.equal(a1.view(torch.int16), act.view(torch.int16))
+
+
 @pytest.mark.parametrize("cfg_id", [0, 2])
 def test_layer_fp8_forward(cfg_id):
     """The layer with its expert forward products in FP8, checked stage by stage on the GPU's own
@@ -140,17 +167,22 @@ def test_layer_fp8_forward(cfg_id):
     torch.cuda.synchronize()
     b = lay.buf
     wg, wu, wd = (f64(inp[n]) for n in ("w_gate", "w_up", "w_down"))
-    for name, w in (("gate", wg), ("up", wu), ("down", wd)):
-        q, s = O.quantize_rows_fp8(np.transpose(w, (0, 2, 1)))
-        np.testing.assert_array_equal(_u8(lay.w8[name][0]), q)
-        np.testing.assert_array_equal(lay.w8[name][1].cpu().numpy(), s)
+    gq, gs = O.quantize_rows_fp8(np.transpose(wg, (0, 2, 1)))
+    uq, us = O.quantize_rows_fp8(np.transpose(wu, (0, 2, 1)))
+    dq, ds = O.quantize_rows_fp8(np.transpose(wd, (0, 2, 1)))
+    # the gate/up weight interleaved by 128 channels: per-channel codes are those of each weight
+    E, F = gq.shape[0], gq.shape[1]
+    lq, ls = _u8(lay.w8["gate_up"][0]).reshape(E, F // 128, 2, 128, -1), lay.w8["gate_up"][1].cpu().numpy()
+    np.testing.assert_array_equal(lq[:, :, 0].reshape(E, F, -1), gq)
+    np.testing.assert_array_equal(lq[:, :, 1].reshape(E, F, -1), uq)
+    np.testing.assert_array_equal(ls.reshape(E, F // 128, 2, 128)[:, :, 0].reshape(E, F), gs)
+    np.testing.assert_array_equal(ls.reshape(E, F // 128, 2, 128)[:, :, 1].reshape(E, F), us)
+    np.testing.assert_array_equal(_u8(lay.w8["down"][0]), dq)
+    np.testing.assert_array_equal(lay.w8["down"][1].cpu().numpy(), ds)
     off = b["offsets"].cpu().numpy()
     xq, xs = O.quantize_rows_fp8(f64(b["x_perm"]))
     np.testing.assert_array_equal(_u8(b["x_q"]), xq)
     np.testing.assert_array_equal(b["x_s"].cpu().numpy(), xs)
-    gq, gs = (t.cpu().numpy() for t in lay.w8["gate"])
-    uq, us = (t.cpu().numpy() for t in lay.w8["up"])
-    dq, ds = (t.cpu().numpy() for t in lay.w8["down"])
     check_float("h_gate", f64(b["h_gate"]), O.grouped_gemm_fp8(xq, xs, gq, gs, off), 2e-3)
     check_float("h_up", f64(b["h_up"]), O.grouped_gemm_fp8(xq, xs, uq, us, off), 2e-3)
     check_float("act", f64(b["act"]), O.swiglu(f64(b["h_gate"]), f64(b["h_up"])), 2e-3)
