@@ -146,7 +146,7 @@ def workload_name(i, cfg, router=False):
 def main():
     a = _args()
     if a.gpus != 1:
-        print(f"bench.py measures one GPU only (--gpus {a.gpus} requested): this build has no "
+        print(f"bench.py measures one GPU only (--gpus {a.gpus} requested): the library has no "
               f"multi-GPU path; run with --gpus 1", file=sys.stderr)
         sys.exit(2)
     if a.copy_probe:
