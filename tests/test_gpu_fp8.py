@@ -204,3 +204,51 @@ def test_layer_fp8_forward(cfg_id):
     for key in ("dh_gate", "dh_up", "dx_perm", "dw_gate", "dw_up", "dw_down", "dx"):
         check_float(key, f64(b[key]), bwd[key])
     _say(f"fp8 forward Y vs the all-bf16 oracle: relative Frobenius {O.rel_fro(f64(b['y']), ref['y']):.3e}")
+
+
+def test_fp8_forward_fullsize_sampled():
+    """The FP8 forward products at the Mixtral-shaped layer's full size (R = 16384 routed rows over
+    8 experts, d = 4096, f = 14336), in the launch configuration the benchmark times (split tail
+    on): gate/up + SwiGLU over the interleaved weight and the down product, on quantized Gaussian
+    operands; 16 sampled rows of the first and of the last expert against the oracle on the same
+    codes and scales (the product for those rows alone, the expert's weight decoded once)."""
+    from paper_2606_26453_amd import workloads as W
+    cfg = W.CONFIGS[1]
+    R, d, f, E = cfg.T * cfg.k, cfg.d, cfg.f, cfg.E
+    _say("fp8 full size", R, d, f, E)
+    g = torch.Generator(device=DEV).manual_seed(11)
+    counts = [R // E] * E
+    off_np = np.concatenate([[0], np.cumsum(counts)])
+    off = torch.tensor(off_np, dtype=torch.int32, device=DEV)
+    x = torch.randn((R, d), generator=g, device=DEV).to(torch.bfloat16)
+    ws = moe.split_workspace(DEV)
+    wg = (torch.randn((E, f, d), generator=g, device=DEV) * 0.02).to(torch.bfloat16)
+    wu = (torch.randn((E, f, d), generator=g, device=DEV) * 0.02).to(torch.bfloat16)
+    iq, is_ = moe.moe_quantize_fp8_rows(moe.interleave_gate_up(wg, wu))
+    del wg, wu
+    wd = (torch.randn((E, d, f), generator=g, device=DEV) * 0.02).to(torch.bfloat16)
+    dq, ds = moe.moe_quantize_fp8_rows(wd)
+    del wd
+    xq, xs = moe.moe_quantize_fp8_rows(x)
+    hg, hu, act = moe.moe_grouped_gemm_fwd_fp8_gate_up(xq, xs, iq, is_, off, workspace=ws)
+    aq, as_ = moe.moe_quantize_fp8_rows(act)
+    y = moe.moe_grouped_gemm_fwd_fp8(aq, as_, dq, ds, off, workspace=ws)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(12)
+    for e in (0, E - 1):
+        rows = np.sort(rng.choice(np.arange(off_np[e], off_np[e + 1]), 16, replace=False))
+        ridx = torch.tensor(rows, device=DEV)
+        sub = np.array([0, 16])
+        il = _u8(iq[e]).reshape(f // 128, 2, 128, d)
+        ils = is_[e].cpu().numpy().reshape(f // 128, 2, 128)
+        gq, uq = il[:, 0].reshape(1, f, d), il[:, 1].reshape(1, f, d)
+        gs, us = ils[:, 0].reshape(1, f), ils[:, 1].reshape(1, f)
+        a_c, a_s = _u8(xq[ridx]), xs[ridx].cpu().numpy()
+        check_float(f"h_gate e{e}", f64(hg[ridx]), O.grouped_gemm_fp8(a_c, a_s, gq, gs, sub), 2e-3)
+        check_float(f"h_up e{e}", f64(hu[ridx]), O.grouped_gemm_fp8(a_c, a_s, uq, us, sub), 2e-3)
+        check_float(f"act e{e}", f64(act[ridx]), O.swiglu(f64(hg[ridx]), f64(hu[ridx])), 2e-3)
+        rq, rs = O.quantize_rows_fp8(f64(act[ridx]))
+        np.testing.assert_array_equal(_u8(aq[ridx]), rq)
+        np.testing.assert_array_equal(as_[ridx].cpu().numpy(), rs)
+        check_float(f"y e{e}", f64(y[ridx]), O.grouped_gemm_fp8(rq, rs, _u8(dq[e])[None], ds[e].cpu().numpy()[None], sub),
+                    2e-3)
