@@ -1000,11 +1000,12 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
 // Tile shape and schedule per product, chosen by measurement on the Mixtral-shaped layer: every
 // product uses 256x256 tiles with a 4-slot ring (128-row tiles, which would pad ragged groups
 // less, measured 10-20% slower: they need 1.5x the LDS and DMA traffic per MFMA).  dX (both
-// operands read 16 bytes per lane) runs 8 wavefronts in the ping-pong schedule; fwd and dW, whose
-// transposing LDS reads make a memory phase longer than a compute phase, run 4 wavefronts (one
-// per SIMD, 128x128 each) in the single-group schedule.  dX walks its tiles persistently (1-3%
-// faster than one workgroup per tile); fwd keeps one workgroup per tile (its tile loop would spill
-// registers in the epilogue: 3-5% slower), and so does dW, whose tiles differ in length with the
+// operands read 16 bytes per lane) runs 8 wavefronts in the ping-pong schedule (the single-group
+// schedule below measured 6-8% slower for it); fwd and dW, whose transposing LDS reads make a
+// memory phase longer than a compute phase, run 4 wavefronts (one per SIMD, 128x128 each) in the
+// single-group schedule.  dX walks its tiles persistently (1-3% faster than one workgroup per
+// tile); fwd keeps one workgroup per tile (a persistent fwd spills 24-56 registers), and so does
+// dW, whose tiles differ in length with the
 // group sizes: the hardware dispatcher then balances them dynamically, where a static walk of the
 // largest-first order measured 7% slower on the Zipf-skewed layer.
 template <int KIND> struct Cfg {
