@@ -33,13 +33,13 @@ METRIC = "MoE layer fwd+bwd tokens/sec + grouped-GEMM TFLOP/s (% of bf16 MFMA pe
 # WRITE_SIZE runs scaled by a plain copy of known size (profiles/grouped_gemm_hbm_traffic_*.md).
 # Valid only for the kernel code they were measured on (sha256 prefix of the sources with comments
 # and blank lines removed); otherwise reported null.
-TRAFFIC_SOURCE = (("paper_2606_26453_amd/csrc/grouped_gemm.hip", "paper_2606_26453_amd/csrc/common.h"), "2b28fd5fbc98c922")
+TRAFFIC_SOURCE = (("paper_2606_26453_amd/csrc/grouped_gemm.hip", "paper_2606_26453_amd/csrc/common.h"), "56940dafba1d0ddf")
 TRAFFIC_CONFIG = 1
 FETCH_SCALE, WRITE_SCALE = 2.0 * 1024, 1.0 * 1024
 TRAFFIC_KIB = {  # call: (FETCH_SIZE KiB, WRITE_SIZE KiB) per dispatch
-    "fwd_gate_up": (4627608, 1399104), "fwd_down": (2173060, 199688),
-    "dx_down_swiglu_bwd": (2899104, 917504), "dx_gate_up": (4373611, 196616),
-    "dw_down": (1507454, 1835100), "dw_gate_up": (2851561, 3671297),
+    "fwd_gate_up": (4847194, 1399104), "fwd_down": (2088128, 199688),
+    "dx_down_swiglu_bwd": (2996785, 917504), "dx_gate_up": (4377875, 196616),
+    "dw_down": (1507454, 1835008), "dw_gate_up": (2796774, 3672265),
 }
 
 
@@ -87,6 +87,9 @@ def _args():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tokens", type=int, default=0)
     ap.add_argument("--no-trace", action="store_true", help="no per-call events inside the timed region")
+    ap.add_argument("--gemm-probe", choices=["fwd", "dx", "dw"],
+                    help="run one gate/up-shaped grouped GEMM (uniform groups of the chosen config) 3 times and "
+                         "exit: the target of hardware-counter runs")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES bytes 3 times (counter calibration)")
     return ap.parse_args()
@@ -101,6 +104,32 @@ def copy_probe(nbytes):
         b.copy_(a)
     torch.cuda.synchronize()
     print(json.dumps({"copy_probe_bytes": nbytes, "copies": 3}), flush=True)
+
+
+def gemm_probe(kind, cfg):
+    """The gate/up-shaped grouped product of one kind on uniform groups (R/E rows each), three
+    launches: fwd H_g, H_u (+ SwiGLU) = X·W_{g,u}; dX = dH_g·W_gᵀ + dH_u·W_uᵀ; dW_{g,u} = Xᵀ·dH_{g,u}."""
+    import torch
+
+    from paper_2606_26453_amd import moe
+    dev = "cuda:0"
+    g = torch.Generator(device=dev).manual_seed(0)
+    R, d, f, E = cfg.T * cfg.k, cfg.d, cfg.f, cfg.E
+    off = torch.tensor([R * e // E for e in range(E + 1)], dtype=torch.int32, device=dev)
+    rn = lambda *sh: torch.randn(sh, generator=g, device=dev).to(torch.bfloat16)
+    if kind == "fwd":
+        A, B, B2 = rn(R, d), rn(E, d, f), rn(E, d, f)
+        fn = lambda: moe.moe_grouped_gemm_fwd(A, B, off, B2, want_act=True)
+    elif kind == "dx":
+        dC, dC2, B, B2 = rn(R, f), rn(R, f), rn(E, d, f), rn(E, d, f)
+        fn = lambda: moe.moe_grouped_gemm_dx(dC, B, off, dC2, B2)
+    else:
+        A, dC, dC2 = rn(R, d), rn(R, f), rn(R, f)
+        fn = lambda: moe.moe_grouped_gemm_dw(A, dC, off, dC2)
+    for _ in range(3):
+        fn()
+    torch.cuda.synchronize()
+    print(json.dumps({"gemm_probe": kind, "R": R, "d": d, "f": f, "E": E, "launches": 3}), flush=True)
 
 
 def cpu_baseline(cfg, inp, sample_tokens):
@@ -151,6 +180,10 @@ def main():
         sys.exit(2)
     if a.copy_probe:
         copy_probe(a.copy_probe)
+        return
+    if a.gemm_probe:
+        from paper_2606_26453_amd import workloads as W
+        gemm_probe(a.gemm_probe, W.CONFIGS[a.config])
         return
     import torch
 
