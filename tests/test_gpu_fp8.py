@@ -252,3 +252,29 @@ def test_fp8_forward_fullsize_sampled():
         np.testing.assert_array_equal(as_[ridx].cpu().numpy(), rs)
         check_float(f"y e{e}", f64(y[ridx]), O.grouped_gemm_fp8(rq, rs, _u8(dq[e])[None], ds[e].cpu().numpy()[None], sub),
                     2e-3)
+
+
+def test_grouped_gemm_fp8_256_groups_exact():
+    """The maximum group count (G = 256, empty groups included, more row tiles than CUs): the FP8
+    product and the FP8 gate/up product exact against the oracle on integer codes."""
+    _say("gemm fp8 256 groups")
+    rng = np.random.default_rng(2560)
+    counts = rng.integers(0, 400, 256)
+    counts[rng.choice(256, 20, replace=False)] = 0
+    G, R, K, N = 256, int(counts.sum()), 128, 256
+    off = torch.tensor(np.concatenate([[0], np.cumsum(counts)]), dtype=torch.int32)
+    g = torch.Generator().manual_seed(2560)
+    a, w, w2 = _int_codes(g, (R, K)), _int_codes(g, (G, N, K)), _int_codes(g, (G, N, K))
+    sa, sw, sw2 = _pow2(g, (R,)), _pow2(g, (G, N)), _pow2(g, (G, N))
+    ws = moe.split_workspace(DEV)
+    C = moe.moe_grouped_gemm_fwd_fp8(a.to(DEV), sa.to(DEV), w.to(DEV), sw.to(DEV), off.to(DEV), workspace=ws)
+    iq = moe.interleave_gate_up(w.to(DEV), w2.to(DEV))
+    iscale = moe.interleave_gate_up(sw.to(DEV)[..., None], sw2.to(DEV)[..., None])[..., 0]
+    hg, hu, act = moe.moe_grouped_gemm_fwd_fp8_gate_up(a.to(DEV), sa.to(DEV), iq, iscale.contiguous(), off.to(DEV),
+                                                        workspace=ws)
+    torch.cuda.synchronize()
+    ref = O.grouped_gemm_fp8(_u8(a), sa.numpy(), _u8(w), sw.numpy(), off.numpy())
+    np.testing.assert_array_equal(f64(C), ref)
+    np.testing.assert_array_equal(f64(hg), ref)
+    np.testing.assert_array_equal(f64(hu), O.grouped_gemm_fp8(_u8(a), sa.numpy(), _u8(w2), sw2.numpy(), off.numpy()))
+    check_float("act", f64(act), O.swiglu(f64(hg), f64(hu)), 1e-2)
