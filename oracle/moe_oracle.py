@@ -184,7 +184,10 @@ def grouped_gemm_dw(A, dC, offsets, G=None):
 # C, I: SwiGLU
 # --------------------------------------------------------------------------------------------
 def sigmoid(x):
-    return 1.0 / (1.0 + np.exp(-np.asarray(x, dtype=np.float64)))
+    """1 / (1 + exp(-x)), evaluated without overflow: for x < 0 as exp(x) / (1 + exp(x))."""
+    x = np.asarray(x, dtype=np.float64)
+    e = np.exp(-np.abs(x))
+    return np.where(x >= 0, 1.0 / (1.0 + e), e / (1.0 + e))
 
 
 def swiglu(h_gate, h_up, rnd=bf16_round):
