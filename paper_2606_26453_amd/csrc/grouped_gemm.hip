@@ -814,18 +814,36 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
       if (n < Wo) {
         uint16_t* c1 = static_cast<uint16_t*>(p.out) + obase + n;
         uint16_t* c2 = static_cast<uint16_t*>(p.out2) + obase + n;
-        for (int t = tid >> 4; t < TM; t += NT / 16) {
-          const int64_t r = row_lo + t;
-          if (r >= row_hi) break;
-          const u32x4 vg = chunk(t, c), vu = chunk(t, 16 + c);
-          *reinterpret_cast<u32x4*>(c1 + r * Wo) = vg;
-          *reinterpret_cast<u32x4*>(c2 + r * Wo) = vu;
-          if constexpr (ACT) {
-            u32x4 va;
+        // passes of NT/16 rows, UB passes' LDS reads issued ahead of their stores
+        constexpr int RPP = NT / 16, PASSES = TM / RPP, UB = 4;
+        static_assert(PASSES % UB == 0, "batches of passes");
 #pragma unroll
-            for (int e = 0; e < 4; ++e)
-              va[e] = pack_bf16(silu_f32(bf16_lo(vg[e])) * bf16_lo(vu[e]), silu_f32(bf16_hi(vg[e])) * bf16_hi(vu[e]));
-            *reinterpret_cast<u32x4*>(p.act + r * Wo + n) = va;
+        for (int b = 0; b < PASSES; b += UB) {
+          if (row_lo + b * RPP >= row_hi) break;   // uniform: no row of the batch is an output row
+          u32x4 vg[UB], vu[UB];
+#pragma unroll
+          for (int u = 0; u < UB; ++u) {
+            const int t = (tid >> 4) + (b + u) * RPP;
+            vg[u] = chunk(t, c);
+            vu[u] = chunk(t, 16 + c);
+          }
+#pragma unroll
+          for (int u = 0; u < UB; ++u) asm volatile("" : "+v"(vg[u]), "+v"(vu[u]));
+#pragma unroll
+          for (int u = 0; u < UB; ++u) {
+            const int64_t r = row_lo + (tid >> 4) + (b + u) * RPP;
+            if (r < row_hi) {
+              *reinterpret_cast<u32x4*>(c1 + r * Wo) = vg[u];
+              *reinterpret_cast<u32x4*>(c2 + r * Wo) = vu[u];
+              if constexpr (ACT) {
+                u32x4 va;
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                  va[e] = pack_bf16(silu_f32(bf16_lo(vg[u][e])) * bf16_lo(vu[u][e]),
+                                    silu_f32(bf16_hi(vg[u][e])) * bf16_hi(vu[u][e]));
+                *reinterpret_cast<u32x4*>(p.act + r * Wo + n) = va;
+              }
+            }
           }
         }
       }
@@ -873,10 +891,21 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
           }
         } else {
           uint16_t* dst = static_cast<uint16_t*>(p.out) + obase + n;
-          for (int t = tid >> 5; t < TM; t += NT / 32) {
-            const int64_t r = row_lo + t;
-            if (r >= row_hi) break;
-            *reinterpret_cast<u32x4*>(dst + r * W) = chunk(t, c);
+          constexpr int RPP = NT / 32, PASSES = TM / RPP, UB = 8;
+          static_assert(PASSES % UB == 0, "batches of passes");
+#pragma unroll
+          for (int b = 0; b < PASSES; b += UB) {
+            if (row_lo + b * RPP >= row_hi) break;   // uniform
+            u32x4 v[UB];
+#pragma unroll
+            for (int u = 0; u < UB; ++u) v[u] = chunk((tid >> 5) + (b + u) * RPP, c);
+#pragma unroll
+            for (int u = 0; u < UB; ++u) asm volatile("" : "+v"(v[u]));
+#pragma unroll
+            for (int u = 0; u < UB; ++u) {
+              const int64_t r = row_lo + (tid >> 5) + (b + u) * RPP;
+              if (r < row_hi) *reinterpret_cast<u32x4*>(dst + r * W) = v[u];
+            }
           }
         }
       }
