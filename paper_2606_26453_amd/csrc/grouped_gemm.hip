@@ -214,7 +214,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
     if (tid < 256) s_pp[tid + 1] = tid < p.G ? ((s_off[tid + 1] - s_off[tid] + 31) & ~31) : 0;
     if (tid == 0) s_pp[0] = 0;
     __syncthreads();
-    for (int off = 1; off < 256; off <<= 1) {
+    for (int off = 1; off < p.G; off <<= 1) {   // entries past G are zero
       const int add = (tid < 256 && tid >= off) ? s_pp[tid + 1 - off] : 0;
       __syncthreads();
       if (tid < 256) s_pp[tid + 1] += add;
@@ -242,13 +242,13 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
     if (tid < p.G) cnt = (p.offsets[tid + 1] - p.offsets[tid] + TM - 1) / TM;
     if (tid < 256) s_scan[tid] = cnt;
     __syncthreads();
-    for (int off = 1; off < 256; off <<= 1) {
+    for (int off = 1; off < p.G; off <<= 1) {   // entries past G are zero
       const int add = (tid < 256 && tid >= off) ? s_scan[tid - off] : 0;
       __syncthreads();
       if (tid < 256) s_scan[tid] += add;
       __syncthreads();
     }
-    mtotal = s_scan[255];
+    mtotal = s_scan[p.G - 1];
     ntiles_all = mtotal * p.n_tiles;
   }
   // dispatch index -> (group, row tile, column tile, row range).  FWD/DX: output rows of the
