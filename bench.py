@@ -33,13 +33,13 @@ METRIC = "MoE layer fwd+bwd tokens/sec + grouped-GEMM TFLOP/s (% of bf16 MFMA pe
 # WRITE_SIZE runs scaled by a plain copy of known size (profiles/grouped_gemm_hbm_traffic_*.md).
 # Valid only for the kernel code they were measured on (sha256 prefix of the sources with comments
 # and blank lines removed); otherwise reported null.
-TRAFFIC_SOURCE = (("paper_2606_26453_amd/csrc/grouped_gemm.hip", "paper_2606_26453_amd/csrc/common.h"), "56940dafba1d0ddf")
+TRAFFIC_SOURCE = (("paper_2606_26453_amd/csrc/grouped_gemm.hip", "paper_2606_26453_amd/csrc/common.h"), "592c451ea4b96faf")
 TRAFFIC_CONFIG = 1
 FETCH_SCALE, WRITE_SCALE = 2.0 * 1024, 1.0 * 1024
 TRAFFIC_KIB = {  # call: (FETCH_SIZE KiB, WRITE_SIZE KiB) per dispatch
-    "fwd_gate_up": (4847194, 1399104), "fwd_down": (2088128, 199688),
-    "dx_down_swiglu_bwd": (2996785, 917504), "dx_gate_up": (4377875, 196616),
-    "dw_down": (1507454, 1835008), "dw_gate_up": (2796774, 3672265),
+    "fwd_gate_up": (4745296, 1391488), "fwd_down": (2134541, 198664),
+    "dx_down_swiglu_bwd": (2918509, 917504), "dx_gate_up": (4410080, 196616),
+    "dw_down": (1507475, 1835008), "dw_gate_up": (2903954, 3670016),
 }
 
 
