@@ -313,7 +313,9 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
   int64_t c_len = 0;              // contraction extent
   int nsteps = 0;
   int c_len32 = 0, m_row_bytes = 0, n_row_bytes = 0;   // the same sizes in 32 bits
+  int tile_rows = TM;             // FWD/DX: output rows of the tile that are rows of its group
   auto setup = [&](int g, int mt, int nt, int64_t row_lo, int64_t row_hi) {
+    tile_rows = (int)(row_hi - row_lo < TM ? row_hi - row_lo : TM);
     // lane-dependent terms are recomputed per tile rather than hoisted out of the tile loop and
     // kept live (in registers the main loop needs) across it
     int lane = threadIdx.x & 63;
@@ -648,6 +650,13 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
     static_assert(NWAVE == 8 && WAVES_N == 2 && TM == 256, "ping-pong needs the 4x2 wave layout");
     const int grp = wave >> 2;
     static_assert(NSTAGE == 4, "ping-pong refill distance assumes a 4-slot ring");
+    // A tile with at most 128 rows (the last tile of a group) gives group 1 no output rows: it
+    // then skips its MFMAs (its fragment reads and share of the DMA stay, keeping the schedule and
+    // the registers as they are), so each SIMD's matrix core serves group 0 alone and the step
+    // costs about a compute phase plus a memory phase instead of two compute phases.  (The single-group schedule cannot gain this way: its
+    // four wavefronts sit on four SIMDs.)
+    static_assert(!PINGPONG || KIND == KIND_DX || KIND == KIND_DWT, "row-tile kinds");
+    const bool live = (grp == 0) || (KIND == KIND_DWT) || (tile_rows > 128);   // uniform
     auto memory_phase = [&](int s) {
       const int slot = slot_of(s);
       load_frags(0, slot, 0);
@@ -670,11 +679,13 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
       for (int s = 0; s < nsteps; ++s) {
         memory_phase(s);
         half_end();
-        if constexpr (F8) {
-          mfmas_f8();
-        } else {
-          mfmas(0, 0, MFMA_HALF);
-          mfmas(1, 0, MFMA_HALF);
+        if (live) {
+          if constexpr (F8) {
+            mfmas_f8();
+          } else {
+            mfmas(0, 0, MFMA_HALF);
+            mfmas(1, 0, MFMA_HALF);
+          }
         }
         half_end();
       }
