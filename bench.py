@@ -279,7 +279,11 @@ def main():
         "data": "synthetic (seeded N(0,1) activations, N(0,0.02) weights, router logits X.Wr)",
         "config": {"workload": workload_name(a.config, cfg, a.router and not cfg.dw_only)
                    + (" (forward only)" if a.forward_only and not cfg.dw_only else "")
-                   + (", expert forward products in FP8 E4M3" if a.fp8_forward else ""),
+                   + (", expert forward products in FP8 E4M3" if a.fp8_forward else "")
+                   + (", gather fused into the gate/up product" if a.gather_fused else "")
+                   + (", dW from contraction-major copies" if a.dw_transposed else "")
+                   + (", no split tail" if a.no_split_tail else "")
+                   + (", two streams" if a.concurrent else ""),
                    "T": cfg.T, "d": cfg.d, "f": cfg.f, "E": cfg.E, "k": cfg.k, "f_shared": cfg.f_shared,
                    "parallelism": "single GPU"},
         "gemm_tflops": round(gemm_flops / gemm_ms / 1e9, 1) if gemm_ms else None,
