@@ -45,8 +45,8 @@ __global__ __launch_bounds__(256) void swiglu_bwd_kernel(const u32x4* __restrict
   dhu[i] = b;
 }
 
-// y[t] = bf16(sum_j w[t,j] * y_perm[row_of_slot[t*k+j]] + add[t])
-template <int U>
+// y[t] = bf16(sum_j w[t,j] * y_perm[row_of_slot[t*k+j]] + add[t]).  KK > 0: k == KK.
+template <int U, int KK>
 __global__ __launch_bounds__(256) void combine_kernel(const u32x4* __restrict__ y_perm,
                                                       const float* __restrict__ w,
                                                       const int32_t* __restrict__ row_of_slot,
@@ -56,6 +56,51 @@ __global__ __launch_bounds__(256) void combine_kernel(const u32x4* __restrict__ 
   const int lane = threadIdx.x & 63;
   const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;
+  if constexpr (KK > 0) {
+    // k known at compile time: the chunks of all k source rows are loaded before any is summed
+    // (KK*U loads in flight per lane instead of U), summed in the same order as below
+    const u32x4* src[KK];
+    float wj[KK];
+#pragma unroll
+    for (int j = 0; j < KK; ++j) {
+      src[j] = y_perm + (int64_t)row_of_slot[t * KK + j] * chunks;
+      wj[j] = w ? w[t * KK + j] : 1.0f;
+    }
+    for (int64_t c0 = 0; c0 < chunks; c0 += 64 * U) {
+      u32x4 v[KK][U];
+#pragma unroll
+      for (int j = 0; j < KK; ++j)
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int64_t c = c0 + u * 64 + lane;
+          v[j][u] = c < chunks ? src[j][c] : u32x4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t c = c0 + u * 64 + lane;
+        float acc[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+#pragma unroll
+        for (int j = 0; j < KK; ++j) {
+          float f[8];
+          unpack8(v[j][u], f);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) acc[i] += wj[j] * f[i];
+        }
+        if (c < chunks) {
+          if (add) {
+            float f[8];
+            unpack8(add[t * chunks + c], f);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) acc[i] += f[i];
+          }
+          y[t * chunks + c] = pack8(acc);
+        }
+      }
+    }
+    return;
+  }
   for (int64_t c0 = 0; c0 < chunks; c0 += 64 * U) {
     float acc[U][8];
 #pragma unroll
@@ -98,7 +143,9 @@ __global__ __launch_bounds__(256) void combine_kernel(const u32x4* __restrict__ 
 
 // dy_perm[row] = bf16(w * dy[t]); d_w[t,j] = <dy[t], y_perm[row]>.  The token's choices are taken
 // eight at a time; for each group the dY row is read once per chunk and the partial dot products
-// stay in registers until one wavefront reduction per choice at the end.
+// stay in registers until one wavefront reduction per choice at the end.  KK > 0: k == KK, and U
+// chunks of dY and of every Y_perm row are loaded per lane before any is used (the same sums).
+template <int U, int KK>
 __global__ __launch_bounds__(256) void combine_bwd_kernel(const u32x4* __restrict__ dy,
                                                           const float* __restrict__ w,
                                                           const int32_t* __restrict__ row_of_slot,
@@ -111,6 +158,60 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(const u32x4* __restric
   const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;
   const u32x4* src = dy + t * chunks;
+  if constexpr (KK > 0) {
+    static_assert(KK <= J, "one group of choices");
+    int64_t row[KK];
+    float wj[KK], dot[KK];
+#pragma unroll
+    for (int j = 0; j < KK; ++j) {
+      row[j] = row_of_slot[t * KK + j];
+      wj[j] = w[t * KK + j];
+      dot[j] = 0.f;
+    }
+    for (int64_t c0 = lane; c0 < chunks; c0 += 64 * U) {
+      u32x4 dv[U], yv[KK][U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t c = c0 + 64 * u;
+        dv[u] = c < chunks ? src[c] : u32x4{0u, 0u, 0u, 0u};
+        if (y_perm) {
+#pragma unroll
+          for (int j = 0; j < KK; ++j) yv[j][u] = c < chunks ? y_perm[row[j] * chunks + c] : u32x4{0u, 0u, 0u, 0u};
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t c = c0 + 64 * u;
+        if (c < chunks) {
+          float f[8];
+          unpack8(dv[u], f);
+#pragma unroll
+          for (int j = 0; j < KK; ++j) {
+            float o[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) o[i] = wj[j] * f[i];
+            dy_perm[row[j] * chunks + c] = pack8(o);
+            if (y_perm) {
+              float yf[8];
+              unpack8(yv[j][u], yf);
+#pragma unroll
+              for (int i = 0; i < 8; ++i) dot[j] += f[i] * yf[i];
+            }
+          }
+        }
+      }
+    }
+    if (y_perm && d_w) {
+#pragma unroll
+      for (int j = 0; j < KK; ++j) {
+        float v = dot[j];
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+        if (lane == 0) d_w[t * KK + j] = v;
+      }
+    }
+    return;
+  }
   for (int j0 = 0; j0 < k; j0 += J) {
     const int nj = k - j0 < J ? k - j0 : J;
     int64_t row[J];
@@ -214,9 +315,19 @@ extern "C" moe_status moe_unpermute_combine(const moe_bf16* y_perm, const float*
   if (!aligned16(y_perm) || !aligned16(y) || (add && !aligned16(add)))
     return fail(MOE_ERROR_INVALID_VALUE, "moe_unpermute_combine: pointers must be 16-byte aligned");
   const int64_t chunks = d / 8;
-  combine_kernel<4><<<(unsigned)((T + 3) / 4), 256, 0, stream>>>(
-      reinterpret_cast<const u32x4*>(y_perm), topk_w, row_of_slot,
-      reinterpret_cast<const u32x4*>(add), T, chunks, k, reinterpret_cast<u32x4*>(y));
+  const unsigned grid = (unsigned)((T + 3) / 4);
+  const u32x4* yp = reinterpret_cast<const u32x4*>(y_perm);
+  const u32x4* ad = reinterpret_cast<const u32x4*>(add);
+  u32x4* yo = reinterpret_cast<u32x4*>(y);
+  // about eight 16-byte loads in flight per lane for the common k
+  switch (k) {
+    case 1: combine_kernel<8, 1><<<grid, 256, 0, stream>>>(yp, topk_w, row_of_slot, ad, T, chunks, k, yo); break;
+    case 2: combine_kernel<4, 2><<<grid, 256, 0, stream>>>(yp, topk_w, row_of_slot, ad, T, chunks, k, yo); break;
+    case 4: combine_kernel<2, 4><<<grid, 256, 0, stream>>>(yp, topk_w, row_of_slot, ad, T, chunks, k, yo); break;
+    case 6: combine_kernel<1, 6><<<grid, 256, 0, stream>>>(yp, topk_w, row_of_slot, ad, T, chunks, k, yo); break;
+    case 8: combine_kernel<1, 8><<<grid, 256, 0, stream>>>(yp, topk_w, row_of_slot, ad, T, chunks, k, yo); break;
+    default: combine_kernel<4, 0><<<grid, 256, 0, stream>>>(yp, topk_w, row_of_slot, ad, T, chunks, k, yo); break;
+  }
   return check_launch("combine_kernel");
 }
 
@@ -233,9 +344,17 @@ extern "C" moe_status moe_unpermute_combine_bwd(const moe_bf16* dy, const float*
   if (!aligned16(dy) || !aligned16(dy_perm) || (y_perm && !aligned16(y_perm)))
     return fail(MOE_ERROR_INVALID_VALUE, "moe_unpermute_combine_bwd: pointers must be 16-byte aligned");
   const int64_t chunks = d / 8;
-  combine_bwd_kernel<<<(unsigned)((T + 3) / 4), 256, 0, stream>>>(
-      reinterpret_cast<const u32x4*>(dy), topk_w, row_of_slot,
-      reinterpret_cast<const u32x4*>(y_perm), T, chunks, k, reinterpret_cast<u32x4*>(dy_perm),
-      d_topk_w);
+  const unsigned grid = (unsigned)((T + 3) / 4);
+  const u32x4* dyp = reinterpret_cast<const u32x4*>(dy);
+  const u32x4* yp = reinterpret_cast<const u32x4*>(y_perm);
+  u32x4* dpo = reinterpret_cast<u32x4*>(dy_perm);
+  switch (k) {
+    case 1: combine_bwd_kernel<4, 1><<<grid, 256, 0, stream>>>(dyp, topk_w, row_of_slot, yp, T, chunks, k, dpo, d_topk_w); break;
+    case 2: combine_bwd_kernel<4, 2><<<grid, 256, 0, stream>>>(dyp, topk_w, row_of_slot, yp, T, chunks, k, dpo, d_topk_w); break;
+    case 4: combine_bwd_kernel<2, 4><<<grid, 256, 0, stream>>>(dyp, topk_w, row_of_slot, yp, T, chunks, k, dpo, d_topk_w); break;
+    case 6: combine_bwd_kernel<1, 6><<<grid, 256, 0, stream>>>(dyp, topk_w, row_of_slot, yp, T, chunks, k, dpo, d_topk_w); break;
+    case 8: combine_bwd_kernel<1, 8><<<grid, 256, 0, stream>>>(dyp, topk_w, row_of_slot, yp, T, chunks, k, dpo, d_topk_w); break;
+    default: combine_bwd_kernel<1, 0><<<grid, 256, 0, stream>>>(dyp, topk_w, row_of_slot, yp, T, chunks, k, dpo, d_topk_w); break;
+  }
   return check_launch("combine_bwd_kernel");
 }

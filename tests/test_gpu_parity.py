@@ -132,6 +132,43 @@ def test_grouped_gemm_dx_exact(K, N):
     np.testing.assert_array_equal(f64(dA1), O.grouped_gemm_dx(f64(dC), f64(B), off.numpy()))
 
 
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5, 6, 8, 9])
+@pytest.mark.parametrize("d", [64, 576])
+def test_combine_exact(k, d):
+    """The weighted and unweighted combine (with and without the added token rows) and its
+    backward, for every k the library specialises (1, 2, 4, 6, 8) and others (the general path),
+    on small integers with power-of-two weights, where every fp32 sum is exact: bit-equal to the
+    oracle.  d = 576 gives each lane several 16-byte chunks (72 per row)."""
+    _say("combine exact", k, d)
+    g = torch.Generator().manual_seed(1000 * k + d)
+    T = 37
+    R = T * k
+    row_of_slot = torch.randperm(R, generator=g).to(torch.int32)
+    w = (2.0 ** torch.randint(-2, 2, (T, k), generator=g)).to(torch.float32)
+    y_perm = _int_tensor(g, (R, d), -8, 8)
+    add = _int_tensor(g, (T, d), -8, 8)
+    dy = _int_tensor(g, (T, d), -8, 8)
+    dv = lambda t: t.to(DEV)
+    rs = i64(row_of_slot)
+    for wt, ad in ((w, None), (None, None), (w, add), (None, add)):
+        y = poison_(torch.empty((T, d), dtype=torch.bfloat16, device=DEV))
+        moe.moe_unpermute_combine(dv(y_perm), None if wt is None else dv(wt), dv(row_of_slot), k,
+                                  add=None if ad is None else dv(ad), y=y)
+        torch.cuda.synchronize()
+        ref = O.combine(f64(y_perm), None if wt is None else f64(wt), rs, k, add=None if ad is None else f64(ad))
+        np.testing.assert_array_equal(f64(y), ref)
+    for yp in (y_perm, None):
+        dy_perm = poison_(torch.empty((R, d), dtype=torch.bfloat16, device=DEV))
+        d_w = poison_(torch.empty((T, k), dtype=torch.float32, device=DEV)) if yp is not None else None
+        moe.moe_unpermute_combine_bwd(dv(dy), dv(w), dv(row_of_slot), k, y_perm=None if yp is None else dv(yp),
+                                      dy_perm=dy_perm, d_topk_w=d_w)
+        torch.cuda.synchronize()
+        ref_p, ref_w = O.combine_bwd(f64(dy), f64(w), rs, None if yp is None else f64(yp), k)
+        np.testing.assert_array_equal(f64(dy_perm), ref_p)
+        if yp is not None:
+            np.testing.assert_array_equal(f64(d_w), ref_w)
+
+
 @pytest.mark.parametrize("K,N", [(192, 320), (256, 256), (576, 64)])
 def test_grouped_gemm_dw_exact(K, N):
     _say("gemm_dw exact", K, N)
