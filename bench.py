@@ -80,6 +80,8 @@ def _args():
                     help="gate/up product reads x through token_of_row; X_perm is gathered in the backward")
     ap.add_argument("--no-split-tail", action="store_true",
                     help="persistent dX products do not split their last partial round of tiles")
+    ap.add_argument("--dw-one-per-tile", action="store_true",
+                    help="variant: the dW products launch one workgroup per tile (no persistent grid)")
     ap.add_argument("--concurrent", action="store_true",
                     help="weight gradients and the shared FFN on a second stream beside the main chain "
                          "(per-call times then include the sharing of the CUs)")
@@ -196,12 +198,13 @@ def main():
     t_gen = time.perf_counter()
     if cfg.dw_only:
         inp = W.make_dw_inputs(cfg, a.seed, dev)
-        lay = L.DWOnly(cfg, inp)
+        lay = L.DWOnly(cfg, inp, persistent=not a.dw_one_per_tile)
     else:
         inp = W.make_inputs(cfg, a.seed, dev)
         lay = L.MoELayer(cfg, inp, router=a.router, aux_alpha=a.aux_alpha if a.router else 0.0,
                          dw_transposed=a.dw_transposed, concurrent=a.concurrent, split_tail=not a.no_split_tail,
-                         gather_fused=a.gather_fused, fp8_forward=a.fp8_forward)
+                         gather_fused=a.gather_fused, fp8_forward=a.fp8_forward,
+                         dw_persistent=not a.dw_one_per_tile)
     torch.cuda.synchronize()
     t_gen = time.perf_counter() - t_gen
 
@@ -283,6 +286,7 @@ def main():
                    + (", gather fused into the gate/up product" if a.gather_fused else "")
                    + (", dW from contraction-major copies" if a.dw_transposed else "")
                    + (", no split tail" if a.no_split_tail else "")
+                   + (", dW one workgroup per tile" if a.dw_one_per_tile else "")
                    + (", two streams" if a.concurrent else ""),
                    "T": cfg.T, "d": cfg.d, "f": cfg.f, "E": cfg.E, "k": cfg.k, "f_shared": cfg.f_shared,
                    "parallelism": "single GPU"},

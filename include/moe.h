@@ -317,6 +317,27 @@ moe_status moe_grouped_gemm_dw_bf16(const moe_bf16* A, const moe_bf16* dC, const
                                     int64_t N, moe_bf16* dB, moe_bf16* dB2, hipStream_t stream);
 
 /*
+ * The same two weight gradients (fp32, bf16) from a persistent grid, one workgroup per CU, whose
+ * workgroups take their next tile from one of eight claim counters (one per XCD) while the
+ * current tile's contraction runs, instead of one workgroup per tile: the tiles of a ragged dW
+ * differ in length with their group's size (section 5.4, the ragged K_e), and the per-tile start
+ * and store costs then overlap.  Results are bit-identical to moe_grouped_gemm_dw /
+ * moe_grouped_gemm_dw_bf16 (the same per-element reduction order).
+ * counters: at least 8 int32 of device memory, 4-byte aligned, caller-owned; the call zeroes them
+ * on `stream` and its kernel updates them.  Calls that may run at the same time need distinct
+ * counters.  NULL or misaligned counters: MOE_ERROR_INVALID_VALUE.  Everything else as
+ * moe_grouped_gemm_dw.
+ */
+moe_status moe_grouped_gemm_dw_persistent(const moe_bf16* A, const moe_bf16* dC, const moe_bf16* dC2,
+                                          const int32_t* offsets, int32_t G, int64_t R, int64_t K,
+                                          int64_t N, float* dB, float* dB2, int32_t* counters,
+                                          hipStream_t stream);
+moe_status moe_grouped_gemm_dw_bf16_persistent(const moe_bf16* A, const moe_bf16* dC, const moe_bf16* dC2,
+                                               const int32_t* offsets, int32_t G, int64_t R, int64_t K,
+                                               int64_t N, moe_bf16* dB, moe_bf16* dB2, int32_t* counters,
+                                               hipStream_t stream);
+
+/*
  * The weight gradient of moe_grouped_gemm_dw from contraction-major copies of its operands
  * (the layout moe_transpose_grouped writes): At [K, ld] and dCt, dC2t [N, ld] bf16, in which
  * group g's rows occupy columns pstart[g] .. pstart[g] + K_g - 1, pstart[g] = sum over h < g of

@@ -18,9 +18,12 @@ LIB_PATH = os.path.join(PKG, LIB_NAME)
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
-# packed fp32 VALU ops are disabled for all device code
+# packed fp32 VALU ops are disabled for all device code.  The atomic optimizer is off: every
+# atomic here is issued by one lane, and its wave-level expansion uses the result at once, which
+# would wait for a dW tile claim (and every load in flight) where the claim is issued.
 FLAGS = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-I" + INCLUDE, "-I" + CSRC,
-         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-Wno-unused-command-line-argument"]
+         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-Wno-unused-command-line-argument",
+         "-mllvm", "-amdgpu-atomic-optimizer-strategy=None"]
 
 
 def _compile(src: str) -> str:

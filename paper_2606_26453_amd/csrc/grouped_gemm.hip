@@ -74,6 +74,7 @@ struct GemmParams {
   int64_t gather_rows;
   const float* a_scale;    // FP8 products: per-row scale of the row operand [R]
   const float* w_scale;    //               per-output-column scale of the weight [G, K]
+  int* tile_queue;         // DW, persistent: 8 tile-claim counters, one per XCD (zero at launch)
 };
 
 typedef int i32x4 __attribute__((ext_vector_type(4)));
@@ -653,8 +654,8 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
     // A tile with at most 128 rows (the last tile of a group) gives group 1 no output rows: it
     // then skips its MFMAs (its fragment reads and share of the DMA stay, keeping the schedule and
     // the registers as they are), so each SIMD's matrix core serves group 0 alone and the step
-    // costs about a compute phase plus a memory phase instead of two compute phases.  (The single-group schedule cannot gain this way: its
-    // four wavefronts sit on four SIMDs.)
+    // costs about a compute phase plus a memory phase instead of two compute phases.  (The
+    // single-group schedule cannot gain this way: its four wavefronts sit on four SIMDs.)
     static_assert(!PINGPONG || KIND == KIND_DX || KIND == KIND_DWT, "row-tile kinds");
     const bool live = (grp == 0) || (KIND == KIND_DWT) || (tile_rows > 128);   // uniform
     auto memory_phase = [&](int s) {
@@ -965,12 +966,33 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
       epilogue(g, mt, nt, row_lo, row_hi);
       return;
     }
+    // dW: tiles differ in length with their group's size, so instead of walking a fixed list the
+    // workgroup claims its next tile from its XCD's queue (dispatch indices x, x + 8, ... in claim
+    // order after the grid's own first round), issuing the claim as this tile's main loop starts
+    // so that its round trip is hidden.  dX walks b, b + gridDim.x, ...
+    __shared__ int s_next;
     for (;;) {
+      int claim = 0;
+      if constexpr (IS_DW) {
+        if (tid == 0)
+          claim = __hip_atomic_fetch_add(p.tile_queue + (blockIdx.x & 7), 1, __ATOMIC_RELAXED,
+                                         __HIP_MEMORY_SCOPE_AGENT);
+      }
       main_loop();
-      const int next = it + (int)gridDim.x;
-      const bool more = next < normal_end;   // uniform
+      if constexpr (IS_DW) {
+        // the claim's result is first needed here (kept opaque until now, so that nothing derived
+        // from it, and hence no wait for it, is placed before the main loop)
+        asm volatile("" : "+v"(claim));
+        if (tid == 0) {
+          const int x = blockIdx.x & 7;
+          s_next = 8 * (claim + (((int)gridDim.x - x + 7) >> 3)) + x;
+        }
+      }
+      int next = it + (int)gridDim.x;
       int g2 = 0, mt2 = 0, nt2 = 0, lo2 = 0, hi2 = 0;
-      epilogue(g, mt, nt, row_lo, row_hi);   // stages the tile through the ring
+      epilogue(g, mt, nt, row_lo, row_hi);   // stages the tile through the ring (barriers first)
+      if constexpr (IS_DW) next = __builtin_amdgcn_readfirstlane(s_next);
+      const bool more = next < normal_end;   // uniform
       if (more) {
         __syncthreads();   // every staged chunk has been read
         map_tile(next, g2, mt2, nt2, lo2, hi2);
@@ -1086,15 +1108,19 @@ constexpr int SPLIT_UNITS = 256, SPLIT_MAX = 8, SPLIT_MIN_STEPS = 64;
 constexpr size_t SPLIT_CNT_BYTES = SPLIT_UNITS * sizeof(int);
 constexpr size_t SPLIT_BYTES = SPLIT_CNT_BYTES + (size_t)SPLIT_UNITS * 256 * TN * sizeof(float);
 
-template <int KIND, bool DUAL, bool ACT, bool OUT16 = false, bool GATHER = false, bool F8 = false>
+// QUEUE (dW): a persistent grid whose workgroups claim tiles from p.tile_queue.
+template <int KIND, bool DUAL, bool ACT, bool OUT16 = false, bool GATHER = false, bool F8 = false,
+          bool QUEUE = false>
 moe_status launch(const GemmParams& p, int64_t tiles_bound, hipStream_t stream, const char* name) {
   if (tiles_bound == 0) return MOE_SUCCESS;
   if (tiles_bound >= ((int64_t)1 << 31) - SPLIT_UNITS) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: too many tiles", name);
+  static_assert(!QUEUE || KIND == KIND_DW, "tile queues: the dW product");
   using C = Cfg<KIND>;
+  constexpr bool PERSIST = C::PERSIST || QUEUE;
   // persistent grid: one workgroup per CU slot (a multiple of 8, one share per XCD), or one per
   // tile when there are fewer tiles; otherwise one workgroup per (bound on the) tile count
   unsigned grid = (unsigned)tiles_bound;
-  if constexpr (C::PERSIST) {
+  if constexpr (PERSIST) {
     unsigned slots = (unsigned)device_cu_count() * C::WPE;
     if (slots > 8) slots &= ~7u;
     if (grid > slots) grid = slots;
@@ -1102,7 +1128,7 @@ moe_status launch(const GemmParams& p, int64_t tiles_bound, hipStream_t stream, 
     grid += SPLIT_UNITS;   // the split units run past the full rounds' tiles (idle ones exit)
   }
   static_assert(!GATHER || KIND == KIND_FWD, "gathered rows feed the forward product only");
-  grouped_gemm_kernel<KIND, DUAL, ACT, C::TM, C::WM, C::WN, C::NS, C::PP, C::WPE, C::PERSIST, OUT16, GATHER, F8>
+  grouped_gemm_kernel<KIND, DUAL, ACT, C::TM, C::WM, C::WN, C::NS, C::PP, C::WPE, PERSIST, OUT16, GATHER, F8>
       <<<grid, 64 * C::WM * C::WN, 0, stream>>>(p);
   return check_launch(name);
 }
@@ -1375,7 +1401,10 @@ namespace moe {
 namespace {
 moe_status grouped_gemm_dw_impl(const char* fn, bool out16, const moe_bf16* A, const moe_bf16* dC,
                                 const moe_bf16* dC2, const int32_t* offsets, int32_t G, int64_t R,
-                                int64_t K, int64_t N, void* dB, void* dB2, hipStream_t stream) {
+                                int64_t K, int64_t N, void* dB, void* dB2, int32_t* counters,
+                                bool persistent, hipStream_t stream) {
+  if (persistent && (counters == nullptr || (reinterpret_cast<uintptr_t>(counters) & 3u)))
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: counters must be 8 int32 of device memory", fn);
   if (G < 1 || G > 256) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: need 1 <= G <= 256", fn);
   if (R < 0 || K <= 0 || N <= 0) return fail(MOE_ERROR_INVALID_VALUE, "%s: bad size", fn);
   if (K % 64 || N % 64) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: K and N must be multiples of 64", fn);
@@ -1393,6 +1422,16 @@ moe_status grouped_gemm_dw_impl(const char* fn, bool out16, const moe_bf16* A, c
   const int cols_per_tile = dC2 ? TN / 2 : TN;
   p.n_tiles = (int)((N + cols_per_tile - 1) / cols_per_tile);
   const int64_t tiles = (int64_t)G * p.m_tiles * p.n_tiles;
+  if (persistent && tiles > 0) {
+    p.tile_queue = counters;
+    zero_i32_kernel<<<1, 64, 0, stream>>>(counters, 8);
+    if (out16) {
+      if (dC2) return launch<KIND_DW, true, false, true, false, false, true>(p, tiles, stream, "grouped_gemm_dw_bf16(dual, persistent)");
+      return launch<KIND_DW, false, false, true, false, false, true>(p, tiles, stream, "grouped_gemm_dw_bf16(persistent)");
+    }
+    if (dC2) return launch<KIND_DW, true, false, false, false, false, true>(p, tiles, stream, "grouped_gemm_dw(dual, persistent)");
+    return launch<KIND_DW, false, false, false, false, false, true>(p, tiles, stream, "grouped_gemm_dw(persistent)");
+  }
   if (out16) {
     if (dC2) return launch<KIND_DW, true, false, true>(p, tiles, stream, "grouped_gemm_dw_bf16(dual)");
     return launch<KIND_DW, false, false, true>(p, tiles, stream, "grouped_gemm_dw_bf16");
@@ -1441,12 +1480,29 @@ extern "C" moe_status moe_grouped_gemm_dw_t(const moe_bf16* At, const moe_bf16* 
 extern "C" moe_status moe_grouped_gemm_dw(const moe_bf16* A, const moe_bf16* dC, const moe_bf16* dC2,
                                           const int32_t* offsets, int32_t G, int64_t R, int64_t K,
                                           int64_t N, float* dB, float* dB2, hipStream_t stream) {
-  return grouped_gemm_dw_impl("moe_grouped_gemm_dw", false, A, dC, dC2, offsets, G, R, K, N, dB, dB2, stream);
+  return grouped_gemm_dw_impl("moe_grouped_gemm_dw", false, A, dC, dC2, offsets, G, R, K, N, dB, dB2, nullptr,
+                              false, stream);
+}
+
+extern "C" moe_status moe_grouped_gemm_dw_persistent(const moe_bf16* A, const moe_bf16* dC, const moe_bf16* dC2,
+                                                     const int32_t* offsets, int32_t G, int64_t R, int64_t K,
+                                                     int64_t N, float* dB, float* dB2, int32_t* counters,
+                                                     hipStream_t stream) {
+  return grouped_gemm_dw_impl("moe_grouped_gemm_dw_persistent", false, A, dC, dC2, offsets, G, R, K, N, dB, dB2,
+                              counters, true, stream);
 }
 
 extern "C" moe_status moe_grouped_gemm_dw_bf16(const moe_bf16* A, const moe_bf16* dC, const moe_bf16* dC2,
                                                const int32_t* offsets, int32_t G, int64_t R, int64_t K,
                                                int64_t N, moe_bf16* dB, moe_bf16* dB2, hipStream_t stream) {
-  return grouped_gemm_dw_impl("moe_grouped_gemm_dw_bf16", true, A, dC, dC2, offsets, G, R, K, N, dB, dB2,
-                              stream);
+  return grouped_gemm_dw_impl("moe_grouped_gemm_dw_bf16", true, A, dC, dC2, offsets, G, R, K, N, dB, dB2, nullptr,
+                              false, stream);
+}
+
+extern "C" moe_status moe_grouped_gemm_dw_bf16_persistent(const moe_bf16* A, const moe_bf16* dC,
+                                                          const moe_bf16* dC2, const int32_t* offsets, int32_t G,
+                                                          int64_t R, int64_t K, int64_t N, moe_bf16* dB,
+                                                          moe_bf16* dB2, int32_t* counters, hipStream_t stream) {
+  return grouped_gemm_dw_impl("moe_grouped_gemm_dw_bf16_persistent", true, A, dC, dC2, offsets, G, R, K, N, dB,
+                              dB2, counters, true, stream);
 }

@@ -47,7 +47,7 @@ class MoELayer(_Traced):
     def __init__(self, cfg, inputs: dict, normalize_topk: bool = True, fuse_swiglu_bwd: bool = True,
                  router: bool = False, aux_alpha: float = 0.0, dw_transposed: bool = False,
                  concurrent: bool = False, split_tail: bool = True, gather_fused: bool = False,
-                 fp8_forward: bool = False):
+                 fp8_forward: bool = False, dw_persistent: bool = True):
         self.cfg = cfg
         # fp8_forward: the routed experts' forward products run on E4M3 operands (activations
         # quantized per row each step, weights per output channel once, here): gate and up in one
@@ -64,6 +64,9 @@ class MoELayer(_Traced):
         self.split_ws = moe.split_workspace(inputs["x"].device) if split_tail else None
         self.fuse = fuse_swiglu_bwd
         self.dw_t = dw_transposed
+        # dw_persistent: the dW products run as persistent grids that claim their tiles through
+        # these counters (every dW call is on one stream, so one set serves them all)
+        self.dw_cnt = moe.dw_counters(inputs["x"].device) if dw_persistent else None
         # concurrent: independent products run on a second stream (default priority): the weight
         # gradients beside the data gradients, the shared FFN beside the routed experts, so each
         # kernel's last partial round of tiles fills with the other's tiles
@@ -202,14 +205,14 @@ class MoELayer(_Traced):
                 run("dx_down_sh", moe.moe_grouped_gemm_dx, i["dy"], wd, self.offsets_sh, dA=b["d_act_sh"],
                     stream=side)
             run("dw_down_sh", moe.moe_grouped_gemm_dw, b["act_sh"], i["dy"], self.offsets_sh,
-                dB=b["dw_down_sh"], stream=side)
+                dB=b["dw_down_sh"], stream=side, counters=self.dw_cnt)
             if not self.fuse:
                 run("swiglu_bwd_sh", moe.moe_swiglu_bwd, b["h_gate_sh"], b["h_up_sh"], b["d_act_sh"],
                     b["dh_gate_sh"], b["dh_up_sh"], stream=side)
             run("dx_gate_up_sh", moe.moe_grouped_gemm_dx, b["dh_gate_sh"], wg, self.offsets_sh, b["dh_up_sh"],
                 wu, dA=b["dx_sh"], stream=side)
             run("dw_gate_up_sh", moe.moe_grouped_gemm_dw, i["x"], b["dh_gate_sh"], self.offsets_sh,
-                b["dh_up_sh"], dB=b["dw_gate_sh"], dB2=b["dw_up_sh"], stream=side)
+                b["dh_up_sh"], dB=b["dw_gate_sh"], dB2=b["dw_up_sh"], stream=side, counters=self.dw_cnt)
             dx_add = b["dx_sh"]
         run("combine_bwd", moe.moe_unpermute_combine_bwd, i["dy"], b["topk_w"], b["row_of_slot"], k,
             y_perm=b["y_perm"], dy_perm=b["dy_perm"], d_topk_w=b["d_topk_w"], stream=stream)
@@ -222,7 +225,7 @@ class MoELayer(_Traced):
                 dB=b["dw_down"], stream=side)
         else:
             run("dw_down", moe.moe_grouped_gemm_dw, b["act"], b["dy_perm"], b["offsets"], dB=b["dw_down"],
-                stream=side)
+                stream=side, counters=self.dw_cnt)
         if self.fuse:
             run("dx_down_swiglu_bwd", moe.moe_grouped_gemm_dx_swiglu_bwd, b["dy_perm"], i["w_down"],
                 b["offsets"], b["h_gate"], b["h_up"], b["dh_gate"], b["dh_up"], stream=stream,
@@ -243,7 +246,7 @@ class MoELayer(_Traced):
                 b["dh_up_t"], dB=b["dw_gate"], dB2=b["dw_up"], stream=side)
         else:
             run("dw_gate_up", moe.moe_grouped_gemm_dw, b["x_perm"], b["dh_gate"], b["offsets"], b["dh_up"],
-                dB=b["dw_gate"], dB2=b["dw_up"], stream=side)
+                dB=b["dw_gate"], dB2=b["dw_up"], stream=side, counters=self.dw_cnt)
         self._join(main, side)            # the shared dX, and every weight gradient, are complete
         run("unpermute_dx", moe.moe_unpermute_combine, b["dx_perm"], None, b["row_of_slot"], k, add=dx_add,
             y=b["dx"], stream=stream)
@@ -307,10 +310,11 @@ class DWOnly(_Traced):
     """The weight-gradient-only workload: dW_gate and dW_up in one pass, then dW_down (unless
     cfg.dw1_only: the paper's dW1 alone); fp32 results, or bf16 when cfg.dw_bf16."""
 
-    def __init__(self, cfg, inputs: dict):
+    def __init__(self, cfg, inputs: dict, persistent: bool = True):
         self.cfg = cfg
         self.inp = inputs
         dev = inputs["x_perm"].device
+        self.cnt = moe.dw_counters(dev) if persistent else None
         E, d, f = cfg.E, cfg.d, cfg.f
         dt = torch.bfloat16 if cfg.dw_bf16 else torch.float32
         self.buf = {
@@ -324,9 +328,10 @@ class DWOnly(_Traced):
         i, b = self.inp, self.buf
         dw = moe.moe_grouped_gemm_dw_bf16 if self.cfg.dw_bf16 else moe.moe_grouped_gemm_dw
         self._run("dw_gate_up", dw, i["x_perm"], i["dh_gate"], i["offsets"], i["dh_up"],
-                  dB=b["dw_gate"], dB2=b["dw_up"], stream=stream)
+                  dB=b["dw_gate"], dB2=b["dw_up"], stream=stream, counters=self.cnt)
         if not self.cfg.dw1_only:
-            self._run("dw_down", dw, i["act"], i["dy_perm"], i["offsets"], dB=b["dw_down"], stream=stream)
+            self._run("dw_down", dw, i["act"], i["dy_perm"], i["offsets"], dB=b["dw_down"], stream=stream,
+                      counters=self.cnt)
 
     def work(self):
         c = self.cfg

@@ -54,6 +54,8 @@ _SIG = {
     "moe_grouped_gemm_dx": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P]),
     "moe_grouped_gemm_dw": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P]),
     "moe_grouped_gemm_dw_bf16": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P]),
+    "moe_grouped_gemm_dw_persistent": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P, _P]),
+    "moe_grouped_gemm_dw_bf16_persistent": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P, _P]),
     "moe_grouped_gemm_split_workspace_bytes": (ctypes.c_size_t, []),
     "moe_grouped_gemm_dx_split": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, ctypes.c_size_t,
                                                  _P]),
@@ -384,7 +386,14 @@ def moe_grouped_gemm_dx(dC, B, offsets, dC2=None, B2=None, dA=None, stream=None,
     return dA
 
 
-def moe_grouped_gemm_dw(A, dC, offsets, dC2=None, dB=None, dB2=None, stream=None):
+def dw_counters(device):
+    """Claim counters for the persistent dW entry points (8 int32; each call zeroes them)."""
+    return torch.zeros(8, dtype=torch.int32, device=device)
+
+
+def moe_grouped_gemm_dw(A, dC, offsets, dC2=None, dB=None, dB2=None, stream=None, counters=None):
+    """dB[g] = A_g^T dC_g (and dB2 from dC2) in fp32.  counters (from dw_counters): run the
+    persistent entry point, which hands out tiles through them (bit-identical results)."""
     R, K = A.shape
     N = dC.shape[1]
     G = offsets.numel() - 1
@@ -397,14 +406,20 @@ def moe_grouped_gemm_dw(A, dC, offsets, dC2=None, dB=None, dB2=None, stream=None
         dB2 = torch.empty((G, K, N), dtype=torch.float32, device=A.device)
     _need(dB, torch.float32, (G, K, N), "dB")
     _need(dB2, torch.float32, (G, K, N), "dB2")
+    if counters is not None:
+        _need(counters, torch.int32, (8,), "counters")
+        _check("moe_grouped_gemm_dw_persistent",
+               lib().moe_grouped_gemm_dw_persistent(_ptr(A), _ptr(dC), _ptr(dC2), _ptr(offsets), G, R, K, N,
+                                                    _ptr(dB), _ptr(dB2), _ptr(counters), _stream(stream)))
+        return dB, dB2
     _check("moe_grouped_gemm_dw",
            lib().moe_grouped_gemm_dw(_ptr(A), _ptr(dC), _ptr(dC2), _ptr(offsets), G, R, K, N, _ptr(dB),
                                      _ptr(dB2), _stream(stream)))
     return dB, dB2
 
 
-def moe_grouped_gemm_dw_bf16(A, dC, offsets, dC2=None, dB=None, dB2=None, stream=None):
-    """moe_grouped_gemm_dw with bf16 results (one rounding of the fp32 sum)."""
+def moe_grouped_gemm_dw_bf16(A, dC, offsets, dC2=None, dB=None, dB2=None, stream=None, counters=None):
+    """moe_grouped_gemm_dw with bf16 results (one rounding of the fp32 sum); counters as there."""
     R, K = A.shape
     N = dC.shape[1]
     G = offsets.numel() - 1
@@ -417,6 +432,12 @@ def moe_grouped_gemm_dw_bf16(A, dC, offsets, dC2=None, dB=None, dB2=None, stream
         dB2 = torch.empty((G, K, N), dtype=torch.bfloat16, device=A.device)
     _need(dB, torch.bfloat16, (G, K, N), "dB")
     _need(dB2, torch.bfloat16, (G, K, N), "dB2")
+    if counters is not None:
+        _need(counters, torch.int32, (8,), "counters")
+        _check("moe_grouped_gemm_dw_bf16_persistent",
+               lib().moe_grouped_gemm_dw_bf16_persistent(_ptr(A), _ptr(dC), _ptr(dC2), _ptr(offsets), G, R, K,
+                                                         N, _ptr(dB), _ptr(dB2), _ptr(counters), _stream(stream)))
+        return dB, dB2
     _check("moe_grouped_gemm_dw_bf16",
            lib().moe_grouped_gemm_dw_bf16(_ptr(A), _ptr(dC), _ptr(dC2), _ptr(offsets), G, R, K, N, _ptr(dB),
                                           _ptr(dB2), _stream(stream)))

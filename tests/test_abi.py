@@ -80,6 +80,12 @@ def test_gemm_rejects():
         FAKE, FAKE, dC2, FAKE, G, R, K, N, dB, dB2, None)
     assert dw16(G=257) == 2 and dw16(K=2880 + 32) == 2 and dw16(dC2=FAKE) == 1 and dw16(dB=None) == 1
     assert dw16(dB=BAD) == 1 and dw16(R=-1) == 1
+    dwp = lambda G=4, R=100, K=128, N=128, cnt=FAKE, dB=FAKE: L.moe_grouped_gemm_dw_persistent(
+        FAKE, FAKE, None, FAKE, G, R, K, N, dB, None, cnt, None)
+    assert dwp(cnt=None) == 1 and dwp(cnt=BAD) == 1 and dwp(N=32) == 2 and dwp(dB=None) == 1
+    dwp16 = lambda G=4, R=100, K=128, N=128, cnt=FAKE: L.moe_grouped_gemm_dw_bf16_persistent(
+        FAKE, FAKE, None, FAKE, G, R, K, N, FAKE, None, cnt, None)
+    assert dwp16(cnt=None) == 1 and dwp16(cnt=BAD) == 1 and dwp16(G=0) == 2
     dxs = lambda G=4, R=100, K=128, N=128, hg=FAKE: L.moe_grouped_gemm_dx_swiglu_bwd(
         FAKE, FAKE, FAKE, G, R, K, N, hg, FAKE, FAKE, FAKE, None)
     assert dxs(N=100) == 2 and dxs(hg=None) == 1 and dxs(hg=BAD) == 1 and dxs(R=0) == 0

@@ -240,6 +240,41 @@ def test_grouped_gemm_256_groups_exact():
         assert torch.count_nonzero(dB[int(e)]) == 0 and torch.count_nonzero(dBt[int(e)]) == 0
 
 
+@pytest.mark.parametrize("K,N,counts", [
+    (192, 320, GROUPS),
+    (1024, 2048, [700, 0, 3000, 1, 255, 257, 4096, 64, 1900, 0, 33, 2500]),   # several tiles per CU
+    (256, 128, [0] * 200 + [37] * 40 + [600] * 16),                           # G = 256, mostly empty
+])
+def test_grouped_gemm_dw_persistent_bitwise(K, N, counts):
+    """The persistent dW entry points (tiles handed out through per-XCD claim counters) against
+    the one-workgroup-per-tile ones: bit-identical fp32 and bf16 results, single and dual, empty
+    groups included, and twice in a row on the same counters (each call resets them)."""
+    _say("gemm dw persistent", K, N, len(counts))
+    g = torch.Generator(device=DEV).manual_seed(K + N + len(counts))
+    G, R = len(counts), sum(counts)
+    off = torch.tensor(np.concatenate([[0], np.cumsum(counts)]), dtype=torch.int32, device=DEV)
+    A = (torch.randn((R, K), generator=g, device=DEV)).to(torch.bfloat16)
+    dC = (torch.randn((R, N), generator=g, device=DEV)).to(torch.bfloat16)
+    dC2 = (torch.randn((R, N), generator=g, device=DEV)).to(torch.bfloat16)
+    cnt = moe.dw_counters(DEV)
+    ref1, ref2 = moe.moe_grouped_gemm_dw(A, dC, off, dC2)
+    ref_s, _ = moe.moe_grouped_gemm_dw(A, dC, off)
+    ref16, ref16b = moe.moe_grouped_gemm_dw_bf16(A, dC, off, dC2)
+    for _ in range(2):
+        got1, got2 = moe.moe_grouped_gemm_dw(A, dC, off, dC2, dB=poison_(torch.empty_like(ref1)),
+                                             dB2=poison_(torch.empty_like(ref2)), counters=cnt)
+        got_s, _ = moe.moe_grouped_gemm_dw(A, dC, off, dB=poison_(torch.empty_like(ref_s)), counters=cnt)
+        got16, got16b = moe.moe_grouped_gemm_dw_bf16(A, dC, off, dC2, dB=poison_(torch.empty_like(ref16)),
+                                                     dB2=poison_(torch.empty_like(ref16b)), counters=cnt)
+        torch.cuda.synchronize()
+        for name, a, b in (("dB", got1, ref1), ("dB2", got2, ref2), ("dB single", got_s, ref_s),
+                           ("dB bf16", got16, ref16), ("dB2 bf16", got16b, ref16b)):
+            assert torch.equal(a, b), f"{name}: persistent and one-per-tile results differ"
+    empty = [i for i, c in enumerate(counts) if c == 0]
+    if empty:
+        assert torch.count_nonzero(got1[empty]) == 0 and torch.count_nonzero(got16[empty]) == 0
+
+
 @pytest.mark.parametrize("K,N", [(320, 192), (256, 256)])
 def test_grouped_gemm_dw_bf16_exact(K, N):
     """bf16-output dW: the fp32 sum of small integers is exact, so every output equals the
