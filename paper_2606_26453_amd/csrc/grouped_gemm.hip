@@ -1089,10 +1089,12 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
 // schedule below measured 6-8% slower for it); fwd and dW, whose transposing LDS reads make a
 // memory phase longer than a compute phase, run 4 wavefronts (one per SIMD, 128x128 each) in the
 // single-group schedule.  dX walks its tiles persistently (1-3% faster than one workgroup per
-// tile); fwd keeps one workgroup per tile (a persistent fwd spills 24-56 registers), and so does
-// dW, whose tiles differ in length with the
-// group sizes: the hardware dispatcher then balances them dynamically, where a static walk of the
-// largest-first order measured 7% slower on the Zipf-skewed layer.
+// tile); fwd keeps one workgroup per tile (a persistent fwd, walking or claiming its tiles,
+// measured 1% and more slower: it spills registers around its epilogue).  dW, whose tiles differ
+// in length with the group sizes, runs one workgroup per tile, which the hardware dispatcher
+// balances (a static walk of the largest-first order measured 7% slower on the Zipf-skewed
+// layer), or, given claim counters, as a persistent grid whose workgroups claim their tiles
+// (launch<..., QUEUE>): 2-13% faster than one per tile.
 template <int KIND> struct Cfg {
   static constexpr bool PP = (KIND == KIND_DX || KIND == KIND_DWT);   // both operands read directly
   static constexpr int TM = 256;
