@@ -1,0 +1,44 @@
+"""bench.py's host-side contract, on the CPU: the one-GPU refusal, the traffic table's validity
+check, and the workload names (no GPU, no library call)."""
+import os
+import subprocess
+import sys
+
+import bench
+from paper_2606_26453_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, "bench.py", "--gpus", "2"], cwd=ROOT, capture_output=True, text=True,
+                       timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_code_hash_ignores_comments_and_blank_lines():
+    a = "int x = 1;  // one\n\n  return x;\n"
+    b = "int x = 1;\n  return x;   // two\n"
+    assert bench.code_hash(a) == bench.code_hash(b)
+    assert bench.code_hash(a) != bench.code_hash(a.replace("1", "2"))
+
+
+def test_traffic_is_reported_only_for_the_measured_code(monkeypatch):
+    call = next(iter(bench.TRAFFIC_KIB))
+    f, w = bench.TRAFFIC_KIB[call]
+    src = "".join(open(os.path.join(ROOT, p)).read() for p in bench.TRAFFIC_SOURCE[0])
+    monkeypatch.setattr(bench, "TRAFFIC_SOURCE", (bench.TRAFFIC_SOURCE[0], bench.code_hash(src)))
+    assert bench.measured_traffic(call, bench.TRAFFIC_CONFIG) == int(f * bench.FETCH_SCALE + w * bench.WRITE_SCALE)
+    assert bench.measured_traffic(call, bench.TRAFFIC_CONFIG + 1) is None   # another workload
+    assert bench.measured_traffic("no_such_call", bench.TRAFFIC_CONFIG) is None
+    monkeypatch.setattr(bench, "TRAFFIC_SOURCE", (bench.TRAFFIC_SOURCE[0], "0" * 16))
+    assert bench.measured_traffic(call, bench.TRAFFIC_CONFIG) is None        # the kernels changed since
+
+
+def test_workload_names():
+    assert bench.workload_name(1, W.CONFIGS[1]) == "config 1: mixtral MoE FFN layer fwd+bwd"
+    assert bench.workload_name(1, W.CONFIGS[1], router=True).endswith("incl. router")
+    n5 = bench.workload_name(5, W.CONFIGS[5])
+    assert "dW1" in n5 and "bf16 output" in n5 and "alpha=0.24" in n5
+    assert "fp32 output" in bench.workload_name(4, W.CONFIGS[4])
