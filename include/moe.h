@@ -245,6 +245,22 @@ moe_status moe_quantize_fp8_rows(const moe_bf16* x, int64_t M, int64_t K, uint8_
                                  hipStream_t stream);
 
 /*
+ * The same quantization for a weight kept as [expert, contraction, output channel], in one pass
+ * per column block: W [G,K,N] bf16 -> Q [G,N',K] uint8 and scale [G,N'] fp32, where row (g, n) of
+ * Q holds the codes of column n of W[g] (an output channel over its K contraction elements).
+ * W2 == NULL: N' = N, Q[g] = the codes moe_quantize_fp8_rows gives for W[g]^T.  W2 != NULL (same
+ * shape): N' = 2N and the rows interleave W's and W2's channels by 128 (rows 256b .. 256b+127:
+ * W's channels 128b ..; the next 128: W2's), the weight layout moe_grouped_gemm_fwd_fp8_gate_up
+ * reads.  Code for code equal to transposing (and interleaving) and then calling
+ * moe_quantize_fp8_rows; this is the per-step weight preparation of an FP8 training step (the
+ * weights change at every optimizer step).  Q 16-byte, W/W2 16-byte, scale 4-byte aligned.
+ * Errors: K % 16 != 0, or N % 64 != 0 (N % 128 with W2) -> NOT_SUPPORTED; NULL or misaligned
+ * pointers -> INVALID_VALUE.  G = 0 is a no-op.
+ */
+moe_status moe_quantize_fp8_weight(const moe_bf16* w, const moe_bf16* w2, int64_t G, int64_t K, int64_t N,
+                                   uint8_t* q, float* scale, hipStream_t stream);
+
+/*
  * The forward grouped product on E4M3 operands: for rows r of group g (offsets as in
  * moe_grouped_gemm_fwd), C[r,n] = bf16(a_scale[r] * w_scale[g,n] * sum_k A[r,k] * Wt[g,n,k]) with
  * A and Wt decoded from E4M3 and the sum accumulated in fp32 by the gfx950 8-bit matrix cores

@@ -62,10 +62,159 @@ __global__ __launch_bounds__(256) void quantize_fp8_rows_kernel(const u32x4* __r
   }
 }
 
+// The same quantization applied to the columns of a weight W [G, K, N] (column n of expert g: one
+// output channel, its K elements the contraction), written transposed: row (g, n) of Q [G, N', K]
+// holds column n's codes and scale [G, N'] its scale.  With a second weight W2 of the same shape
+// the output interleaves the two by IL = 128 channels: output row 2*IL*b + i (i < IL) is W's
+// channel IL*b + i and row 2*IL*b + IL + i is W2's.  Code for code and scale for scale this is
+// quantize_fp8_rows_kernel on the transposed (and interleaved) weight: the same amax, quotients
+// and products.  Three passes, each spread over (64-column block, expert, matrix, K block)
+// workgroups so that long contractions still fill the chip: the column amax (partial maxima of K
+// blocks combined with an integer atomic max on the fp32 bits, which orders non-negative floats
+// like their values; kept in `scale`), the codes, then scale = amax / 448.  Thread t of a
+// workgroup handles 8-column chunk t % 8 of row (quad) t / 8, so that a wavefront's 16-byte loads
+// cover 8 whole 128-byte row segments.
+constexpr int QC_IL = 128;   // gate/up interleave (channels)
+constexpr int QC_CW = 64;    // columns per workgroup
+constexpr int QC_KA = 2048;  // rows per workgroup, amax pass
+constexpr int QC_KQ = 1024;  // rows per workgroup, code pass (8 blocks of 128)
+
+__device__ __forceinline__ int64_t qc_out_row(int64_t n, bool dual, bool second) {
+  if (!dual) return n;
+  return (n / QC_IL) * 2 * QC_IL + (second ? QC_IL : 0) + n % QC_IL;
+}
+
+__global__ __launch_bounds__(256) void fill_f32_kernel(float* p, int64_t n, float v) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+// pass 1: blockIdx.z = matrix * kblocks + kb
+__global__ __launch_bounds__(256) void amax_cols_kernel(const uint16_t* __restrict__ w, const uint16_t* __restrict__ w2,
+                                                        int64_t K, int64_t N, int64_t n_out, int kblocks,
+                                                        float* __restrict__ amax) {
+  __shared__ float s_part[32][QC_CW];
+  const int t = threadIdx.x, c = t & 7, rq = t >> 3;
+  const bool second = (int)blockIdx.z >= kblocks;
+  const int64_t kb = blockIdx.z - (second ? kblocks : 0);
+  const int64_t g = blockIdx.y, n0 = (int64_t)blockIdx.x * QC_CW;
+  const uint16_t* src = (second ? w2 : w) + g * K * N + n0 + 8 * c;
+  const int64_t k_end = (kb + 1) * QC_KA < K ? (kb + 1) * QC_KA : K;
+  float m[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) m[i] = 0.0f;
+#pragma unroll 4
+  for (int64_t k = kb * QC_KA + rq; k < k_end; k += 32) {
+    const u32x4 v = *reinterpret_cast<const u32x4*>(src + k * N);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      m[2 * e] = fmaxf(m[2 * e], fabsf(bf16_lo(v[e])));
+      m[2 * e + 1] = fmaxf(m[2 * e + 1], fabsf(bf16_hi(v[e])));
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) s_part[rq][8 * c + i] = m[i];
+  __syncthreads();
+  if (t < QC_CW) {
+    float a = 0.0f;
+    for (int r = 0; r < 32; ++r) a = fmaxf(a, s_part[r][t]);
+    // fmaxf drops NaNs as the row quantizer's reduction does, so a >= 0 here
+    atomicMax(reinterpret_cast<unsigned*>(amax) + g * n_out + qc_out_row(n0 + t, w2 != nullptr, second),
+              __float_as_uint(a));
+  }
+}
+
+// pass 2: the codes of K block kb (QC_KQ rows) of 64 columns, written transposed 128 rows at a time
+__global__ __launch_bounds__(256) void quantize_cols_kernel(const uint16_t* __restrict__ w,
+                                                            const uint16_t* __restrict__ w2, int64_t K, int64_t N,
+                                                            int64_t n_out, int kblocks, const float* __restrict__ amax,
+                                                            uint8_t* __restrict__ q) {
+  constexpr int TS = 132;   // LDS row stride (bytes) of the transposed 64-column x 128-row block
+  __shared__ __attribute__((aligned(16))) uint8_t s_t[QC_CW * TS];
+  const int t = threadIdx.x, c = t & 7, rq = t >> 3;
+  const bool second = (int)blockIdx.z >= kblocks;
+  const int64_t kb = blockIdx.z - (second ? kblocks : 0);
+  const int64_t g = blockIdx.y, n0 = (int64_t)blockIdx.x * QC_CW;
+  const bool dual = w2 != nullptr;
+  const uint16_t* src = (second ? w2 : w) + g * K * N + n0 + 8 * c;
+  float inv[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const float a = amax[g * n_out + qc_out_row(n0 + 8 * c + i, dual, second)];
+    inv[i] = a > 0.0f ? __fdiv_rn(448.0f, a) : 1.0f;
+  }
+  const int64_t k_beg = kb * QC_KQ, k_end = (kb + 1) * QC_KQ < K ? (kb + 1) * QC_KQ : K;
+  for (int64_t k0 = k_beg; k0 < k_end; k0 += 128) {
+    uint32_t packed[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) packed[i] = 0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int64_t k = k0 + 4 * rq + u;
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (k < k_end) v = *reinterpret_cast<const u32x4*>(src + k * N);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        packed[2 * e] |= e4m3_code(__fmul_rn(bf16_lo(v[e]), inv[2 * e])) << (8 * u);
+        packed[2 * e + 1] |= e4m3_code(__fmul_rn(bf16_hi(v[e]), inv[2 * e + 1])) << (8 * u);
+      }
+    }
+    __syncthreads();   // the previous block's codes have been written out
+#pragma unroll
+    for (int i = 0; i < 8; ++i) *reinterpret_cast<uint32_t*>(s_t + (8 * c + i) * TS + 4 * rq) = packed[i];
+    __syncthreads();
+    // write out: thread -> column j = t / 4, 32 bytes at k0 + 32 * (t % 4)
+    const int j = t >> 2, seg = t & 3;
+    const int64_t kk = k0 + 32 * seg;
+    uint32_t o[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[i] = *reinterpret_cast<const uint32_t*>(s_t + j * TS + 32 * seg + 4 * i);
+    uint8_t* dst = q + (g * n_out + qc_out_row(n0 + j, dual, second)) * K + kk;
+    if (kk < k_end) *reinterpret_cast<u32x4*>(dst) = u32x4{o[0], o[1], o[2], o[3]};
+    if (kk + 16 < k_end) *reinterpret_cast<u32x4*>(dst + 16) = u32x4{o[4], o[5], o[6], o[7]};
+  }
+}
+
+// pass 3: amax -> scale
+__global__ __launch_bounds__(256) void scale_from_amax_kernel(float* __restrict__ s, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) {
+    const float a = s[i];
+    s[i] = a > 0.0f ? __fdiv_rn(a, 448.0f) : 1.0f;
+  }
+}
+
 }  // namespace
 }  // namespace moe
 
 using namespace moe;
+
+extern "C" moe_status moe_quantize_fp8_weight(const moe_bf16* w, const moe_bf16* w2, int64_t G, int64_t K,
+                                              int64_t N, uint8_t* q, float* scale, hipStream_t stream) {
+  const char* fn = "moe_quantize_fp8_weight";
+  if (G < 0 || K <= 0 || N <= 0) return fail(MOE_ERROR_INVALID_VALUE, "%s: bad size", fn);
+  const int nmul = w2 ? QC_IL : QC_CW;
+  if (K % 16 || N % nmul)
+    return fail(MOE_ERROR_NOT_SUPPORTED, "%s: K must be a multiple of 16 and N of %d", fn, nmul);
+  const int64_t nmat = w2 ? 2 : 1;
+  const int64_t ka = (K + QC_KA - 1) / QC_KA, kq = (K + QC_KQ - 1) / QC_KQ;
+  if (G > 65535 || N / QC_CW > 0x7fffffff || nmat * kq > 65535)
+    return fail(MOE_ERROR_NOT_SUPPORTED, "%s: too many experts, columns or rows", fn);
+  if (G == 0) return MOE_SUCCESS;
+  if (!w || !q || !scale) return fail(MOE_ERROR_INVALID_VALUE, "%s: NULL pointer", fn);
+  if (!aligned16(w) || (w2 && !aligned16(w2)) || !aligned16(q) || (reinterpret_cast<uintptr_t>(scale) & 3))
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: w, w2 and q must be 16-byte, scale 4-byte aligned", fn);
+  const int64_t n_out = nmat * N, ns = G * n_out;
+  const uint16_t* a = w;
+  const uint16_t* b = w2;
+  fill_f32_kernel<<<(unsigned)((ns + 255) / 256), 256, 0, stream>>>(scale, ns, 0.0f);
+  amax_cols_kernel<<<dim3((unsigned)(N / QC_CW), (unsigned)G, (unsigned)(nmat * ka)), 256, 0, stream>>>(
+      a, b, K, N, n_out, (int)ka, scale);
+  quantize_cols_kernel<<<dim3((unsigned)(N / QC_CW), (unsigned)G, (unsigned)(nmat * kq)), 256, 0, stream>>>(
+      a, b, K, N, n_out, (int)kq, scale, q);
+  scale_from_amax_kernel<<<(unsigned)((ns + 255) / 256), 256, 0, stream>>>(scale, ns);
+  return check_launch("quantize_cols_kernel");
+}
 
 extern "C" moe_status moe_quantize_fp8_rows(const moe_bf16* x, int64_t M, int64_t K, uint8_t* q, float* scale,
                                             hipStream_t stream) {

@@ -47,7 +47,7 @@ class MoELayer(_Traced):
     def __init__(self, cfg, inputs: dict, normalize_topk: bool = True, fuse_swiglu_bwd: bool = True,
                  router: bool = False, aux_alpha: float = 0.0, dw_transposed: bool = False,
                  concurrent: bool = False, split_tail: bool = True, gather_fused: bool = False,
-                 fp8_forward: bool = False, dw_persistent: bool = True):
+                 fp8_forward: bool = False, dw_persistent: bool = True, fp8_requantize: bool = True):
         self.cfg = cfg
         # fp8_forward: the routed experts' forward products run on E4M3 operands (activations
         # quantized per row each step, weights per output channel once, here): gate and up in one
@@ -108,13 +108,15 @@ class MoELayer(_Traced):
             u8 = torch.uint8
             b.update({"x_q": e((R, d), u8), "x_s": e(R, f32), "act_q": e((R, f), u8), "act_s": e(R, f32)})
             # weights in the layout [expert, output channel, contraction], quantized per channel
-            # (a one-off preparation outside the step)
-            self.w8 = {}
-            wg_t = inputs["w_gate"].transpose(1, 2).contiguous()
-            wu_t = inputs["w_up"].transpose(1, 2).contiguous()
-            self.w8["gate_up"] = moe.moe_quantize_fp8_rows(moe.interleave_gate_up(wg_t, wu_t))
-            del wg_t, wu_t
-            self.w8["down"] = moe.moe_quantize_fp8_rows(inputs["w_down"].transpose(1, 2).contiguous())
+            # (moe_quantize_fp8_weight: transposed, gate/up interleaved by 128, one pass each).  A
+            # training step re-quantizes them every forward, since the optimizer changes them;
+            # fp8_requantize=False keeps this preparation's codes (weights held fixed)
+            self.w8 = {
+                "gate_up": (e((E, 2 * f, d), u8), e((E, 2 * f), f32)),
+                "down": (e((E, d, f), u8), e((E, d), f32)),
+            }
+            self.fp8_requantize = fp8_requantize
+            self._quantize_weights()
         self.shared = cfg.f_shared > 0
         if self.shared:
             fs = cfg.f_shared
@@ -126,6 +128,12 @@ class MoELayer(_Traced):
             })
             self.w_sh = (inputs["w_gate_sh"].unsqueeze(0), inputs["w_up_sh"].unsqueeze(0),
                          inputs["w_down_sh"].unsqueeze(0))
+
+    def _quantize_weights(self, stream=None):
+        """E4M3 codes and per-channel scales of the expert weights, in the FP8 products' layout."""
+        i, w8 = self.inp, self.w8
+        moe.moe_quantize_fp8_weight(i["w_gate"], i["w_up"], *w8["gate_up"], stream=stream)
+        moe.moe_quantize_fp8_weight(i["w_down"], None, *w8["down"], stream=stream)
 
     # ------------------------------------------------------------------------------------------
     def _streams(self, stream):
@@ -167,6 +175,8 @@ class MoELayer(_Traced):
                 loss=b["aux_loss"], workspace=b["aux_ws"], stream=stream)
         if self.fp8:
             ws = self.split_ws
+            if self.fp8_requantize:
+                run("quantize_w", self._quantize_weights, stream=stream)
             run("quantize_x", moe.moe_quantize_fp8_rows, b["x_perm"], b["x_q"], b["x_s"], stream=stream)
             run("fwd_gate_up", moe.moe_grouped_gemm_fwd_fp8_gate_up, b["x_q"], b["x_s"], *self.w8["gate_up"],
                 b["offsets"], b["h_gate"], b["h_up"], b["act"], stream=stream, workspace=ws)
@@ -280,6 +290,7 @@ class MoELayer(_Traced):
             "gather_x": ("bytes", T * d * 2 + R * d * 2 + R * 4),
             # FP8 forward: E4M3 products (8-bit MFMA work), quantizers and the standalone SwiGLU
             "quantize_x": ("bytes", R * d * 3 + R * 4), "quantize_act": ("bytes", R * f * 3 + R * 4),
+            "quantize_w": ("bytes", 3 * E * d * f * 3 + 3 * E * (d + f) * 4),   # read bf16, write codes
             "fwd_gate_up": ("flops8" if self.fp8 else "flops", 4 * R * d * f),
             "fwd_down": ("flops8" if self.fp8 else "flops", 2 * R * f * d),
             "combine": ("bytes", R * d * 2 + T * d * 2 + T * k * 8 + (T * d * 2 if self.shared else 0)),

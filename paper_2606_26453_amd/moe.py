@@ -43,6 +43,7 @@ _SIG = {
                                                    _P, ctypes.c_size_t, _P]),
     "moe_gather_rows": (ctypes.c_int, [_P, _I64, _I64, _I32, _P, _P, _P]),
     "moe_quantize_fp8_rows": (ctypes.c_int, [_P, _I64, _I64, _P, _P, _P]),
+    "moe_quantize_fp8_weight": (ctypes.c_int, [_P, _P, _I64, _I64, _I64, _P, _P, _P]),
     "moe_grouped_gemm_fwd_fp8": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P,
                                                 ctypes.c_size_t, _P]),
     "moe_grouped_gemm_fwd_fp8_gate_up": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P, _P,
@@ -240,6 +241,24 @@ def moe_quantize_fp8_rows(x, q=None, scale=None, stream=None):
     _need(q, torch.uint8, tuple(x.shape), "q")
     _need(scale, torch.float32, tuple(x.shape[:-1]), "scale")
     _check("moe_quantize_fp8_rows", lib().moe_quantize_fp8_rows(_ptr(x), M, K, _ptr(q), _ptr(scale), _stream(stream)))
+    return q, scale
+
+
+def moe_quantize_fp8_weight(w, w2=None, q=None, scale=None, stream=None):
+    """E4M3 codes and per-channel scales of a weight [G, K, N] (contraction K, channels N), written
+    as [G, N, K] (or, with w2, [G, 2N, K] with the two weights' channels interleaved by 128)."""
+    G, K, N = w.shape
+    _need(w, torch.bfloat16, (G, K, N), "w")
+    _need(w2, torch.bfloat16, (G, K, N), "w2")
+    if not w.is_contiguous() or (w2 is not None and not w2.is_contiguous()):
+        raise ValueError("w and w2 must be contiguous")
+    n_out = 2 * N if w2 is not None else N
+    q = torch.empty((G, n_out, K), dtype=torch.uint8, device=w.device) if q is None else q
+    scale = torch.empty((G, n_out), dtype=torch.float32, device=w.device) if scale is None else scale
+    _need(q, torch.uint8, (G, n_out, K), "q")
+    _need(scale, torch.float32, (G, n_out), "scale")
+    _check("moe_quantize_fp8_weight",
+           lib().moe_quantize_fp8_weight(_ptr(w), _ptr(w2), G, K, N, _ptr(q), _ptr(scale), _stream(stream)))
     return q, scale
 
 

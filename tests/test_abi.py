@@ -118,6 +118,9 @@ def test_fp8_rejects():
     gu = lambda F=128, K=128, act=FAKE, hg=FAKE: L.moe_grouped_gemm_fwd_fp8_gate_up(
         FAKE, FAKE, FAKE, FAKE, FAKE, 4, 100, K, F, hg, FAKE, act, None, 0, None)
     assert gu(F=64) == 2 and gu(K=96) == 2 and gu(hg=None) == 1 and gu(act=BAD) == 1
+    qw = lambda G=2, K=64, N=128, w=FAKE, w2=None, q=FAKE: L.moe_quantize_fp8_weight(w, w2, G, K, N, q, FAKE, None)
+    assert qw(K=24) == 2 and qw(N=96) == 2 and qw(N=192, w2=FAKE) == 2 and qw(G=-1) == 1
+    assert qw(w=None) == 1 and qw(w=BAD) == 1 and qw(q=FAKE + 8) == 1 and qw(w2=BAD) == 1 and qw(G=0) == 0
 
 
 def test_gather_rejects():

@@ -43,6 +43,36 @@ def test_quantize_fp8_rows(M, K):
     np.testing.assert_array_equal(s.cpu().numpy(), rs)
 
 
+@pytest.mark.parametrize("G,K,N,dual", [(2, 64, 64, False), (3, 208, 128, True), (2, 4096, 256, True),
+                                         (1, 2880, 2880, False), (2, 512, 1408, True)])
+def test_quantize_fp8_weight(G, K, N, dual):
+    """The one-pass weight quantizer (transpose, optional 128-channel gate/up interleave, per-channel
+    E4M3): codes and scales bit for bit against the oracle's row quantizer on the transposed
+    (interleaved) weight and against moe_quantize_fp8_rows on the GPU; zero and half-zero columns
+    included, K = 208 leaves a partial 128-row block."""
+    _say("quantize fp8 weight", G, K, N, dual)
+    gen = torch.Generator().manual_seed(G * 7 + K + N)
+    mk = lambda: (torch.randn((G, K, N), generator=gen) * torch.exp(torch.randn((G, 1, N), generator=gen) * 3)
+                  ).to(torch.bfloat16)
+    w = mk()
+    w[:, :, 5] = 0
+    w[0, : K // 2, 7] = 0
+    w2 = mk() if dual else None
+    q, sc = moe.moe_quantize_fp8_weight(w.to(DEV), None if w2 is None else w2.to(DEV),
+                                        q=poison_(torch.empty((G, 2 * N if dual else N, K), dtype=torch.uint8, device=DEV)),
+                                        scale=poison_(torch.empty((G, 2 * N if dual else N), dtype=torch.float32, device=DEV)))
+    torch.cuda.synchronize()
+    wt = w.transpose(1, 2).contiguous()
+    if dual:
+        wt = moe.interleave_gate_up(wt, w2.transpose(1, 2).contiguous())
+    rq, rs = O.quantize_rows_fp8(f64(wt.reshape(-1, K)))
+    np.testing.assert_array_equal(_u8(q).reshape(-1, K), rq)
+    np.testing.assert_array_equal(sc.cpu().numpy().reshape(-1), rs)
+    q2, s2 = moe.moe_quantize_fp8_rows(wt.to(DEV))
+    torch.cuda.synchronize()
+    assert torch.equal(q2, q) and torch.equal(s2, sc)
+
+
 def _int_codes(g, shape, lim=4):
     vals = torch.randint(-lim, lim + 1, shape, generator=g).double().numpy()
     return torch.from_numpy(O.e4m3_encode(vals))
