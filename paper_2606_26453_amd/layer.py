@@ -248,6 +248,12 @@ class MoELayer(_Traced):
         self._join(side, main)            # dW_gate/dW_up need dH
         run("dx_gate_up", moe.moe_grouped_gemm_dx, b["dh_gate"], i["w_gate"], b["offsets"], b["dh_up"],
             i["w_up"], dA=b["dx_perm"], stream=stream, workspace=self.split_ws)
+        # one stream: the unpermute-sum reads dX_perm right after it was written, while it still sits
+        # in the last-level cache (dW gate/up's 3.8 GB of fp32 results would evict it first)
+        early = side is main
+        if early:
+            run("unpermute_dx", moe.moe_unpermute_combine, b["dx_perm"], None, b["row_of_slot"], k, add=dx_add,
+                y=b["dx"], stream=stream)
         if self.dw_t:
             run("transpose_x_perm", moe.moe_transpose_grouped, b["x_perm"], b["offsets"], dst=b["x_perm_t"],
                 stream=side)
@@ -258,8 +264,9 @@ class MoELayer(_Traced):
             run("dw_gate_up", moe.moe_grouped_gemm_dw, b["x_perm"], b["dh_gate"], b["offsets"], b["dh_up"],
                 dB=b["dw_gate"], dB2=b["dw_up"], stream=side, counters=self.dw_cnt)
         self._join(main, side)            # the shared dX, and every weight gradient, are complete
-        run("unpermute_dx", moe.moe_unpermute_combine, b["dx_perm"], None, b["row_of_slot"], k, add=dx_add,
-            y=b["dx"], stream=stream)
+        if not early:
+            run("unpermute_dx", moe.moe_unpermute_combine, b["dx_perm"], None, b["row_of_slot"], k, add=dx_add,
+                y=b["dx"], stream=stream)
         if self.router:
             run("router_bwd", moe.moe_router_bwd, i["x"], i["wr"], b["logits"], b["topk_idx"], b["topk_w"],
                 b["d_topk_w"], b["offsets"], self.normalize, self.aux_alpha, dx=b["dx"], workspace=b["router_ws"],
