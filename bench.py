@@ -37,9 +37,9 @@ TRAFFIC_SOURCE = (("paper_2606_26453_amd/csrc/grouped_gemm.hip", "paper_2606_264
 TRAFFIC_CONFIG = 1
 FETCH_SCALE, WRITE_SCALE = 2.0 * 1024, 1.0 * 1024
 TRAFFIC_KIB = {  # call: (FETCH_SIZE KiB, WRITE_SIZE KiB) per dispatch
-    "fwd_gate_up": (4714771, 1391488), "fwd_down": (2152533, 198664),
-    "dx_down_swiglu_bwd": (3048647, 917504), "dx_gate_up": (4363844, 196616),
-    "dw_down": (1507506, 1835232), "dw_gate_up": (2768965, 3670464),
+    "fwd_gate_up": (4734134, 1391488), "fwd_down": (2184855, 198664),
+    "dx_down_swiglu_bwd": (3087924, 917504), "dx_gate_up": (4360931, 196616),
+    "dw_down": (1507504, 1835232), "dw_gate_up": (2779845, 3670464),
 }
 
 
