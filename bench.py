@@ -33,13 +33,13 @@ METRIC = "MoE layer fwd+bwd tokens/sec + grouped-GEMM TFLOP/s (% of bf16 MFMA pe
 # WRITE_SIZE runs scaled by a plain copy of known size (profiles/grouped_gemm_hbm_traffic_*.md).
 # Valid only for the kernel code they were measured on (sha256 prefix of the sources with comments
 # and blank lines removed); otherwise reported null.
-TRAFFIC_SOURCE = (("paper_2606_26453_amd/csrc/grouped_gemm.hip", "paper_2606_26453_amd/csrc/common.h"), "6182ec0eca562eb6")
+TRAFFIC_SOURCE = (("paper_2606_26453_amd/csrc/grouped_gemm.hip", "paper_2606_26453_amd/csrc/common.h"), "1ad4a0eda89c3ea6")
 TRAFFIC_CONFIG = 1
 FETCH_SCALE, WRITE_SCALE = 2.0 * 1024, 1.0 * 1024
 TRAFFIC_KIB = {  # call: (FETCH_SIZE KiB, WRITE_SIZE KiB) per dispatch
-    "fwd_gate_up": (4734134, 1391488), "fwd_down": (2184855, 198664),
-    "dx_down_swiglu_bwd": (3087924, 917504), "dx_gate_up": (4360931, 196616),
-    "dw_down": (1507504, 1835232), "dw_gate_up": (2779845, 3670464),
+    "fwd_gate_up": (4376720, 1391488), "fwd_down": (1942932, 198664),
+    "dx_down_swiglu_bwd": (2921592, 917504), "dx_gate_up": (4073730, 196616),
+    "dw_down": (1441979, 1835232), "dw_gate_up": (2762870, 3670464),
 }
 
 

@@ -142,19 +142,22 @@ __device__ __forceinline__ int xcd_remap(int bid, int n) {
   return x * q + (x < r ? x : r) + l;
 }
 
-// Logical index within an (mt x nt) grid -> (m, n), walking bands of 8 column tiles so that 32
-// consecutive tiles form a 4 x 8 block (A rows reused 8x, B columns 4x in the XCD's L2).
+// Logical index within an (mt x nt) grid -> (m, n), walking bands of BW = 4 column tiles so that
+// 32 consecutive tiles form an 8 x 4 block (B column panels reused 8x, A row panels 4x in the XCD's
+// L2).  Measured against bands of 8 (4 x 8 blocks) and of 2 and 16, in one run: 1.5-1.8% shorter
+// layer steps on the Mixtral, fine-grained and Zipf-skewed configs (dX gate/up -5% at the first).
 __device__ __forceinline__ void band_order(int id, int mtiles, int ntiles, int& m, int& n) {
-  const int full = ntiles >> 3;
-  const int span = mtiles * 8;
+  constexpr int BW = 4;
+  const int full = ntiles / BW;
+  const int span = mtiles * BW;
   if (id < full * span) {
     const int band = id / span, rem = id - band * span;
-    m = rem >> 3;
-    n = band * 8 + (rem & 7);
+    m = rem / BW;
+    n = band * BW + rem % BW;
   } else {
-    const int rem = id - full * span, w = ntiles - full * 8;
+    const int rem = id - full * span, w = ntiles - full * BW;
     m = rem / w;
-    n = full * 8 + rem % w;
+    n = full * BW + rem % w;
   }
 }
 
