@@ -144,7 +144,7 @@ __device__ __forceinline__ int xcd_remap(int bid, int n) {
 
 // Logical index within an (mt x nt) grid -> (m, n), walking bands of BW = 4 column tiles so that
 // 32 consecutive tiles form an 8 x 4 block (B column panels reused 8x, A row panels 4x in the XCD's
-// L2).  Measured against bands of 8 (4 x 8 blocks) and of 2 and 16, in one run: 1.5-1.8% shorter
+// L2).  Measured against bands of 8 (4 x 8 blocks) and of 2, 3, 5 and 16: 1.1-1.8% shorter
 // layer steps on the Mixtral, fine-grained and Zipf-skewed configs (dX gate/up -5% at the first).
 __device__ __forceinline__ void band_order(int id, int mtiles, int ntiles, int& m, int& n) {
   constexpr int BW = 4;
