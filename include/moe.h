@@ -253,7 +253,9 @@ moe_status moe_quantize_fp8_rows(const moe_bf16* x, int64_t M, int64_t K, uint8_
  * W's channels 128b ..; the next 128: W2's), the weight layout moe_grouped_gemm_fwd_fp8_gate_up
  * reads.  Code for code equal to transposing (and interleaving) and then calling
  * moe_quantize_fp8_rows; this is the per-step weight preparation of an FP8 training step (the
- * weights change at every optimizer step).  Q 16-byte, W/W2 16-byte, scale 4-byte aligned.
+ * weights change at every optimizer step).  Four kernels on `stream`; `scale` holds the column
+ * maxima between them (final values once the last has run).  Q 16-byte, W/W2 16-byte, scale
+ * 4-byte aligned.
  * Errors: K % 16 != 0, or N % 64 != 0 (N % 128 with W2) -> NOT_SUPPORTED; NULL or misaligned
  * pointers -> INVALID_VALUE.  G = 0 is a no-op.
  */
