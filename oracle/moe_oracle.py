@@ -22,7 +22,10 @@ are named at each function.  The FP8 functions at the end serve a variant the pa
 describe (OCP E4M3 operands with fp32 scales); their reading is stated there.
 
 Parity: every function here is pinned by the CPU test suite against closed forms, library
-routines, brute force or automatic differentiation; no function is "parity unpinned".
+routines, brute force, hand-worked values or automatic differentiation, and the suite plants
+plausible mistakes in each to show that a pin catches them.  That includes `rel_fro`, the
+comparison metric every floating-point parity check uses (pinned on hand-computed ratios and its
+zero-reference conventions).  No function is "parity unpinned".
 """
 from __future__ import annotations
 

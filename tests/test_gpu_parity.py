@@ -458,6 +458,121 @@ def test_grouped_gemm_dx_split_tail():
     check_float("dA split (sampled rows)", f64(x1[ridx]), O.grouped_gemm_dx(f64(dCg[ridx]), f64(Bg), sub))
 
 
+# Host replica of the fwd/dX products' dispatch order (blocks round-robin over the 8 XCDs, each XCD
+# walking a contiguous logical range in bands of 4 column tiles): used only to check the premise of
+# the ragged split-tail tests, i.e. that the last partial round really holds ragged tiles.
+def _xcd_remap(bid, n):
+    q, r, x, l = n >> 3, n & 7, bid & 7, bid >> 3
+    return x * q + (x if x < r else r) + l
+
+
+def _band_order(i, mt, nt, bw=4):
+    full, span = nt // bw, mt * bw
+    if i < full * span:
+        band, rem = divmod(i, span)
+        return rem // bw, band * bw + rem % bw
+    rem, w = i - full * span, nt - full * bw
+    return rem // w, full * bw + rem % w
+
+
+def _tail_tile_rows(counts, n_tiles, slots, tm=256):
+    """Rows of each tile that the last partial round of `slots` workgroups computes."""
+    pre = np.cumsum([(c + tm - 1) // tm for c in counts])
+    mtotal = int(pre[-1])
+    nall = mtotal * n_tiles
+    out = []
+    for it in range((nall // slots) * slots, nall):
+        m, _ = _band_order(_xcd_remap(it, nall), mtotal, n_tiles)
+        g = int(np.sum(pre <= m))
+        mt = m - (int(pre[g - 1]) if g else 0)
+        out.append(min(tm, counts[g] - mt * tm))
+    return out
+
+
+# groups of 0 to 255 rows, one row tile each (empty groups between them): every tile is ragged,
+# the ones of the split round included
+_RAGGED = [1, 63, 0, 129, 255, 70, 0, 193, 2, 64, 0, 200, 31, 250, 128, 97]
+
+
+def _ragged_counts(n_row_tiles, rot=0):
+    pat = _RAGGED[rot:] + _RAGGED[:rot]
+    c, i = [], 0
+    while sum(1 for x in c if x > 0) < n_row_tiles:
+        c.append(pat[i % len(pat)])
+        i += 1
+    return c
+
+
+def _cu_slots():
+    return torch.cuda.get_device_properties(0).multi_processor_count
+
+
+def test_grouped_gemm_fwd_split_tail_ragged():
+    """Split tail over ragged groups: 66 one-tile groups of 1..255 rows with empty groups between
+    them (264 tiles, dual 528), so the last partial round splits tiles of 1, 2, 128, 129, 193, 200,
+    250 and 255 rows (dual: 1, 2, 250, 255) along K = 8192.  Small-integer operands: bitwise equal
+    to the unsplit product and exactly equal to the oracle on every row."""
+    _say("gemm fwd split tail, ragged groups")
+    counts = _ragged_counts(66)
+    slots = _cu_slots()
+    G, R, K, N = len(counts), sum(counts), 8192, 1024
+    for nt in (N // 256, N // 128):
+        tail = _tail_tile_rows(counts, nt, slots)
+        assert 0 < len(tail) <= slots // 2 and sum(1 for r in tail if r < 256) >= 3, tail
+    off = torch.tensor(np.concatenate([[0], np.cumsum(counts)]), dtype=torch.int32, device=DEV)
+    g = torch.Generator(device=DEV).manual_seed(21)
+    ws = moe.split_workspace(DEV)
+    A, B, B2 = _int_dev(g, (R, K)), _int_dev(g, (G, K, N)), _int_dev(g, (G, K, N))
+    c1 = moe.moe_grouped_gemm_fwd(A, B, off)[0]
+    s1 = moe.moe_grouped_gemm_fwd(A, B, off, workspace=ws)[0]
+    c2 = moe.moe_grouped_gemm_fwd(A, B, off, B2, want_act=True)
+    s2 = moe.moe_grouped_gemm_fwd(A, B, off, B2, want_act=True, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(c1.view(torch.int16), s1.view(torch.int16))
+    for u, v in zip(c2, s2):
+        assert torch.equal(u.view(torch.int16), v.view(torch.int16))
+    offn = np.concatenate([[0], np.cumsum(counts)])
+    Af = f64(A)
+    np.testing.assert_array_equal(f64(s1), O.grouped_gemm(Af, f64(B), offn))
+    np.testing.assert_array_equal(f64(s2[0]), O.grouped_gemm(Af, f64(B), offn))
+    np.testing.assert_array_equal(f64(s2[1]), O.grouped_gemm(Af, f64(B2), offn))
+
+
+def test_grouped_gemm_dx_split_tail_ragged():
+    """The persistent dX products' split tail over ragged groups: 131 one-tile groups of 1..255
+    rows with empty groups between them (262 tiles), so the split round holds tiles of 1, 2, 31,
+    97, 129 and 255 rows.  Small-integer operands: the plain and dual products bitwise equal to the
+    unsplit kernels and exactly equal to the oracle on every row; the fused SwiGLU backward bitwise
+    equal to the unsplit kernel's."""
+    _say("gemm dx split tail, ragged groups")
+    counts = _ragged_counts(131, rot=12)
+    slots = _cu_slots() & ~7
+    G, R, K, N = len(counts), sum(counts), 512, 4096
+    tail = _tail_tile_rows(counts, K // 256, slots)
+    assert 0 < len(tail) <= slots // 2 and sum(1 for r in tail if r < 256) >= 3, tail
+    off = torch.tensor(np.concatenate([[0], np.cumsum(counts)]), dtype=torch.int32, device=DEV)
+    g = torch.Generator(device=DEV).manual_seed(22)
+    ws = moe.split_workspace(DEV)
+    dC, dC2 = _int_dev(g, (R, N)), _int_dev(g, (R, N))
+    B, B2 = _int_dev(g, (G, K, N)), _int_dev(g, (G, K, N))
+    ref_s = moe.moe_grouped_gemm_dx(dC, B, off, dC2, B2)
+    got_s = moe.moe_grouped_gemm_dx(dC, B, off, dC2, B2, workspace=ws)
+    ref_1 = moe.moe_grouped_gemm_dx(dC, B, off)
+    got_1 = moe.moe_grouped_gemm_dx(dC, B, off, workspace=ws)
+    hg = (torch.randn((R, K), generator=g, device=DEV) * 2).to(torch.bfloat16)
+    hu = torch.randn((R, K), generator=g, device=DEV).to(torch.bfloat16)
+    a_g, a_u = moe.moe_grouped_gemm_dx_swiglu_bwd(dC, B, off, hg, hu)
+    b_g, b_u = moe.moe_grouped_gemm_dx_swiglu_bwd(dC, B, off, hg, hu, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(got_s.view(torch.int16), ref_s.view(torch.int16))
+    assert torch.equal(got_1.view(torch.int16), ref_1.view(torch.int16))
+    assert torch.equal(a_g.view(torch.int16), b_g.view(torch.int16))
+    assert torch.equal(a_u.view(torch.int16), b_u.view(torch.int16))
+    offn = np.concatenate([[0], np.cumsum(counts)])
+    np.testing.assert_array_equal(f64(got_s), O.grouped_gemm_dx(f64(dC), f64(B), offn, f64(dC2), f64(B2)))
+    np.testing.assert_array_equal(f64(got_1), O.grouped_gemm_dx(f64(dC), f64(B), offn))
+
+
 def test_grouped_gemm_dw_worked_example():
     """The hand-evaluated dW1 example of Appendix H's definition, zero-padded to 64-multiples."""
     import json, os

@@ -571,3 +571,42 @@ def test_grouped_gemm_fp8_vs_library():
     sa2[2] *= 4
     np.testing.assert_array_equal(O.grouped_gemm_fp8(a, sa2, w, sw, off, rnd=None)[2], 4 * got[2])
     np.testing.assert_array_equal(O.grouped_gemm_fp8(a, sa, w, sw, off), O.bf16_round(got))
+
+
+# ---------------------------------------------------------------------------------------------
+# the comparison metric every floating-point parity check goes through
+# ---------------------------------------------------------------------------------------------
+def test_rel_fro_hand_values():
+    """rel_fro(got, ref) = ||got - ref||_F / ||ref||_F over the whole tensor, values worked by hand."""
+    # ref = [[3, 0], [0, 4]] has norm 5; the difference [[1, 2], [2, 0]] has norm 3: exactly 3/5.
+    # (A squared ratio gives 0.36, dividing by ||got|| = sqrt(40) gives 0.4743, no square root
+    # gives 9/25 as well, a max-abs ratio gives 2/4.)
+    ref = np.array([[3.0, 0.0], [0.0, 4.0]])
+    got = np.array([[4.0, 2.0], [2.0, 4.0]])
+    assert O.rel_fro(got, ref) == 0.6
+    # not symmetric: with the roles swapped the denominator is sqrt(40)
+    assert abs(O.rel_fro(ref, got) - 3.0 / math.sqrt(40.0)) < 1e-15
+    # one Frobenius norm over the tensor, not a mean of per-row ratios: ref rows of norm 1 and 100,
+    # an error of 1 in the first row only -> 1 / sqrt(10001) (a per-row mean would give 0.5)
+    ref = np.array([[1.0, 0.0], [0.0, 100.0]])
+    got = np.array([[2.0, 0.0], [0.0, 100.0]])
+    assert abs(O.rel_fro(got, ref) - 1.0 / math.sqrt(10001.0)) < 1e-15
+    # a 3-4-5 error on a 12-5-13 reference, in three dimensions: 5/13
+    ref = np.array([12.0, 5.0, 0.0]).reshape(1, 3, 1)
+    got = np.array([15.0, 9.0, 0.0]).reshape(1, 3, 1)
+    assert abs(O.rel_fro(got, ref) - 5.0 / 13.0) < 1e-15
+    # scale invariance, and exactness on equal inputs
+    assert abs(O.rel_fro(7.0 * got, 7.0 * ref) - 5.0 / 13.0) < 1e-15
+    assert O.rel_fro(ref, ref) == 0.0
+    # the zero-reference conventions: 0/0 -> 0 (an exactly zero output matches), x/0 -> inf
+    z = np.zeros((3, 2))
+    assert O.rel_fro(z, z) == 0.0
+    assert O.rel_fro(np.full((3, 2), 1e-30), z) == float("inf")
+    # float64 norms: values whose squares overflow float32 still give the exact ratio
+    ref = np.array([3e30, 4e30])
+    got = np.array([3e30, 4e30 + 5e29])
+    assert abs(O.rel_fro(got, ref) - 0.1) < 1e-15
+    # inputs of any dtype are compared in float64 (bf16-valued float32 arrays here)
+    ref32 = np.array([[3.0, 0.0], [0.0, 4.0]], dtype=np.float32)
+    got32 = np.array([[4.0, 2.0], [2.0, 4.0]], dtype=np.float32)
+    assert O.rel_fro(got32, ref32) == 0.6

@@ -33,6 +33,7 @@ PINS = [
     P.test_e4m3_encode_brute_force_and_torch,
     P.test_quantize_rows_fp8_properties,
     P.test_grouped_gemm_fp8_vs_library,
+    P.test_rel_fro_hand_values,
 ]
 
 
@@ -167,7 +168,37 @@ def _quant_inverted_scale(x):                                             # scal
     return codes, np.where(scale != 1, (np.float32(448.0) ** 2 / 448.0) / (scale * 448.0), scale).astype(np.float32)
 
 
+def _rel_fro_squared(got, ref):                                           # squared ratio
+    r = O.__dict__["_orig_rf"](got, ref)
+    return r * r
+
+
+def _rel_fro_got_norm(got, ref):                                          # ||got|| denominator
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    den = np.linalg.norm(got.ravel())
+    num = np.linalg.norm((got - ref).ravel())
+    return 0.0 if num == 0.0 else (float("inf") if den == 0.0 else float(num / den))
+
+
+def _rel_fro_row_mean(got, ref):                                          # mean of per-row ratios
+    got = np.atleast_2d(np.asarray(got, dtype=np.float64))
+    ref = np.atleast_2d(np.asarray(ref, dtype=np.float64))
+    g2 = got.reshape(got.shape[0], -1)
+    r2 = ref.reshape(ref.shape[0], -1)
+    vals = [O.__dict__["_orig_rf"](a, b) for a, b in zip(g2, r2)]
+    return float(np.mean(vals))
+
+
+def _rel_fro_zero(got, ref):                                              # always passes
+    return 0.0
+
+
 MUTANTS = {
+    "rel_fro squared": ("rel_fro", _rel_fro_squared),
+    "rel_fro divides by the norm of got": ("rel_fro", _rel_fro_got_norm),
+    "rel_fro averages per-row ratios": ("rel_fro", _rel_fro_row_mean),
+    "rel_fro returns zero": ("rel_fro", _rel_fro_zero),
     "e4m3 ties away from zero": ("e4m3_encode", _e4m3_ties_away),
     "e4m3 exponent bias 8": ("e4m3_decode", _e4m3_decode_bias8),
     "fp8 gemm ignores the weight scale": ("grouped_gemm_fp8", _fp8_gemm_no_weight_scale),
@@ -203,6 +234,7 @@ def test_planted_mistake_is_caught(name, monkeypatch):
     monkeypatch.setitem(O.__dict__, "_orig_dec", O.e4m3_decode)
     monkeypatch.setitem(O.__dict__, "_orig_f8", O.grouped_gemm_fp8)
     monkeypatch.setitem(O.__dict__, "_orig_q8", O.quantize_rows_fp8)
+    monkeypatch.setitem(O.__dict__, "_orig_rf", O.rel_fro)
     monkeypatch.setattr(O, attr, fn)
     if attr == "bf16_round":
         # default arguments captured the original function; patch the module-level users too
