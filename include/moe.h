@@ -79,8 +79,8 @@ size_t moe_route_permute_workspace_bytes(int64_t T, int32_t E, int32_t k);
  *   - x_perm[r, :] = x[token_of_row[r], :] (bit copy) when x and x_perm are non-NULL.
  * logits [T,E] fp32; x [T,d] bf16 or NULL; topk_idx [T,k] int32; topk_w [T,k] fp32;
  * offsets [E+1] int32; row_of_slot [T*k] int32; token_of_row [T*k] int32; x_perm [T*k,d] bf16 or
- * NULL.  workspace: device scratch of at least moe_route_permute_workspace_bytes(T, E, k) bytes,
- * contents on entry ignored.  Results are deterministic and bit-exact (no order-dependent
+ * NULL.  workspace: 16-byte aligned device scratch of at least
+ * moe_route_permute_workspace_bytes(T, E, k) bytes, contents on entry ignored.  Results are deterministic and bit-exact (no order-dependent
  * atomics).  NaN logits are not supported.
  */
 moe_status moe_route_permute(const float* logits, const moe_bf16* x, int64_t T, int64_t d,
