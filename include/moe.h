@@ -90,6 +90,23 @@ moe_status moe_route_permute(const float* logits, const moe_bf16* x, int64_t T, 
                              size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * For callers that cannot allocate (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid device allocation): moe_route_permute without a workspace.  Same arguments, results
+ * and errors as moe_route_permute, bit for bit; the per-range histogram lives in a device array of
+ * the library (moe_route_permute_noalloc_max_scratch_bytes() bytes per device, held until the
+ * process ends) instead of a caller workspace.  Sizes whose histogram would not fit
+ * (moe_route_permute_workspace_bytes(T, E, k) above that maximum) return MOE_ERROR_NOT_SUPPORTED
+ * before any launch.  Calls no allocator.  Every call on a device shares that device's array, so
+ * calls that may overlap on one device (concurrent streams, threads) race and must be serialized
+ * by the caller; each call overwrites whatever the previous one left there.
+ */
+size_t moe_route_permute_noalloc_max_scratch_bytes(void);
+moe_status moe_route_permute_noalloc(const float* logits, const moe_bf16* x, int64_t T, int64_t d,
+                                     int32_t E, int32_t k, int32_t normalize_topk, int32_t* topk_idx,
+                                     float* topk_w, int32_t* offsets, int32_t* row_of_slot,
+                                     int32_t* token_of_row, moe_bf16* x_perm, hipStream_t stream);
+
+/*
  * A4 alone: x_perm[row_of_slot[t*k + j], :] = x[t, :] for t < T, j < k (a bit copy; the gather of
  * moe_route_permute, for a caller that routed without it, e.g. when the forward product gathered
  * its rows itself and only the weight gradient needs X_perm).  x [T,d], x_perm [T*k,d] bf16;

@@ -6,6 +6,8 @@
 // slots taken in slot order, counts and offsets from integer sums in a fixed order.
 #include "common.h"
 
+#include <mutex>
+
 namespace moe {
 namespace {
 
@@ -321,8 +323,8 @@ size_t route_workspace_bytes(int64_t T, int E, int k) {
   return (size_t)E * p.nranges * sizeof(int32_t);
 }
 
-// Body of moe_route_permute; hist is the caller's scratch of at least route_workspace_bytes(T, E, k)
-// bytes (contents on entry ignored).
+// Shared body of moe_route_permute and its allocation-free variant; hist is the caller's scratch
+// of at least route_workspace_bytes(T, E, k) bytes (contents on entry ignored).
 moe_status route_permute_impl(const char* fn, const float* logits, const moe_bf16* x, int64_t T, int64_t d,
                               int32_t E, int32_t k, int32_t normalize_topk, int32_t* topk_idx, float* topk_w,
                               int32_t* offsets, int32_t* row_of_slot, int32_t* token_of_row, moe_bf16* x_perm,
@@ -421,6 +423,64 @@ extern "C" moe_status moe_route_permute(const float* logits, const moe_bf16* x, 
     return fail(MOE_ERROR_WORKSPACE, "%s: a 16-byte aligned workspace of %zu bytes is needed", fn, need);
   return route_permute_impl(fn, logits, x, T, d, E, k, normalize_topk, topk_idx, topk_w, offsets, row_of_slot,
                             token_of_row, x_perm, static_cast<int32_t*>(workspace), stream);
+}
+
+// ---- allocation-free variant -----------------------------------------------------------------
+// Scratch for moe_route_permute_noalloc: the per-range histogram lives in this file-scope device
+// array instead of a caller workspace.  In host code `route_scratch` names a host-side stand-in,
+// not device memory: its device address is looked up once per device (hipGetSymbolAddress, with
+// that device current) and only that address is passed to kernels.  Every device holds its own
+// copy until the process ends; calls on one device share it (overlapping calls race).
+constexpr size_t kNoAllocScratchBytes = 256 * 1024;
+static __device__ __align__(256) int32_t route_scratch[kNoAllocScratchBytes / sizeof(int32_t)];
+
+namespace moe {
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's address of route_scratch, looked up on the first call on that device.
+moe_status route_scratch_ptr(const char* fn, int32_t** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+    return fail(MOE_ERROR_HIP, "%s: no current device (or device index >= %d)", fn, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(route_scratch));
+    if (e != hipSuccess || ptr == nullptr)
+      return fail(MOE_ERROR_HIP, "%s: hipGetSymbolAddress(route_scratch) failed: %s", fn, hipGetErrorString(e));
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = static_cast<int32_t*>(g_scratch_ptr[dev]);
+  return MOE_SUCCESS;
+}
+}  // namespace
+}  // namespace moe
+
+extern "C" size_t moe_route_permute_noalloc_max_scratch_bytes(void) { return kNoAllocScratchBytes; }
+
+extern "C" moe_status moe_route_permute_noalloc(const float* logits, const moe_bf16* x, int64_t T, int64_t d,
+                                                int32_t E, int32_t k, int32_t normalize_topk, int32_t* topk_idx,
+                                                float* topk_w, int32_t* offsets, int32_t* row_of_slot,
+                                                int32_t* token_of_row, moe_bf16* x_perm, hipStream_t stream) {
+  const char* fn = "moe_route_permute_noalloc";
+  moe_status st = route_check(fn, logits, x, T, d, E, k, normalize_topk, topk_idx, topk_w, offsets, row_of_slot,
+                              token_of_row, x_perm);
+  if (st != MOE_SUCCESS) return st;
+  if (T == 0) {
+    fill_i32_kernel<<<1, 256, 0, stream>>>(offsets, E + 1, 0);
+    return check_launch("moe_route_permute_noalloc(T=0)");
+  }
+  const size_t need = route_workspace_bytes(T, E, k);
+  if (need > kNoAllocScratchBytes)
+    return fail(MOE_ERROR_NOT_SUPPORTED, "%s: these sizes need %zu bytes of scratch, more than the %zu it holds "
+                "(use moe_route_permute with a workspace)", fn, need, kNoAllocScratchBytes);
+  int32_t* hist = nullptr;
+  if ((st = route_scratch_ptr(fn, &hist)) != MOE_SUCCESS) return st;
+  return route_permute_impl(fn, logits, x, T, d, E, k, normalize_topk, topk_idx, topk_w, offsets, row_of_slot,
+                            token_of_row, x_perm, hist, stream);
 }
 
 extern "C" moe_status moe_gather_rows(const moe_bf16* x, int64_t T, int64_t d, int32_t k,

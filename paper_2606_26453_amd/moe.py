@@ -42,6 +42,8 @@ _SIG = {
     "moe_grouped_gemm_fwd_gather": (ctypes.c_int, [_P, _I64, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P,
                                                    _P, ctypes.c_size_t, _P]),
     "moe_gather_rows": (ctypes.c_int, [_P, _I64, _I64, _I32, _P, _P, _P]),
+    "moe_route_permute_noalloc_max_scratch_bytes": (ctypes.c_size_t, []),
+    "moe_route_permute_noalloc": (ctypes.c_int, [_P, _P, _I64, _I64, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P, _P]),
     "moe_quantize_fp8_rows": (ctypes.c_int, [_P, _I64, _I64, _P, _P, _P]),
     "moe_quantize_fp8_weight": (ctypes.c_int, [_P, _P, _I64, _I64, _I64, _P, _P, _P]),
     "moe_grouped_gemm_fwd_fp8": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P,
@@ -156,6 +158,38 @@ def moe_route_permute(logits, x, k, normalize_topk=True, topk_idx=None, topk_w=N
                                  _ptr(token_of_row), _ptr(x_perm), _ptr(workspace),
                                  workspace.numel() * workspace.element_size(), _stream(stream))
     _check("moe_route_permute", st)
+    return {"topk_idx": topk_idx, "topk_w": topk_w, "offsets": offsets, "row_of_slot": row_of_slot,
+            "token_of_row": token_of_row, "x_perm": x_perm}
+
+
+def moe_route_permute_noalloc(logits, x, k, normalize_topk=True, topk_idx=None, topk_w=None, offsets=None,
+                              row_of_slot=None, token_of_row=None, x_perm=None, stream=None):
+    """moe_route_permute without a workspace: the library's own device scratch holds the
+    per-range histogram (calls on one device must not overlap)."""
+    T, E = logits.shape
+    dev = logits.device
+    _need(logits, torch.float32, (T, E), "logits")
+    d = x.shape[1] if x is not None else 0
+    if x is not None:
+        _need(x, torch.bfloat16, (T, d), "x")
+    R = T * k
+    topk_idx = torch.empty((T, k), dtype=torch.int32, device=dev) if topk_idx is None else topk_idx
+    topk_w = torch.empty((T, k), dtype=torch.float32, device=dev) if topk_w is None else topk_w
+    offsets = torch.empty(E + 1, dtype=torch.int32, device=dev) if offsets is None else offsets
+    row_of_slot = torch.empty(R, dtype=torch.int32, device=dev) if row_of_slot is None else row_of_slot
+    token_of_row = torch.empty(R, dtype=torch.int32, device=dev) if token_of_row is None else token_of_row
+    if x is not None and x_perm is None:
+        x_perm = torch.empty((R, d), dtype=torch.bfloat16, device=dev)
+    _need(topk_idx, torch.int32, (T, k), "topk_idx")
+    _need(topk_w, torch.float32, (T, k), "topk_w")
+    _need(offsets, torch.int32, (E + 1,), "offsets")
+    _need(row_of_slot, torch.int32, (R,), "row_of_slot")
+    _need(token_of_row, torch.int32, (R,), "token_of_row")
+    _need(x_perm, torch.bfloat16, (R, d), "x_perm")
+    st = lib().moe_route_permute_noalloc(_ptr(logits), _ptr(x), T, d, E, k, int(bool(normalize_topk)),
+                                         _ptr(topk_idx), _ptr(topk_w), _ptr(offsets), _ptr(row_of_slot),
+                                         _ptr(token_of_row), _ptr(x_perm), _stream(stream))
+    _check("moe_route_permute_noalloc", st)
     return {"topk_idx": topk_idx, "topk_w": topk_w, "offsets": offsets, "row_of_slot": row_of_slot,
             "token_of_row": token_of_row, "x_perm": x_perm}
 
