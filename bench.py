@@ -1,6 +1,7 @@
 """Benchmark of the MoE expert-FFN training layer (forward + backward) on one MI355X.
 
-python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1] [--no-cpu-baseline]
+python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1] [--no-cpu-baseline] [--flush]
+python bench.py --all-configs      (an opt-in summary line over configurations 0-5)
 
 --config 0..4 are the layer configurations (1, the Mixtral-shaped layer, is the default and the
 headline); --config 5 times the paper's own kernel alone, the gate/up weight gradient dW1 at its
@@ -10,6 +11,12 @@ A step is one forward and one backward pass of the whole layer (routing, permuta
 gate/up grouped GEMM with fused SwiGLU, down grouped GEMM, combine, and the backward dX/dW grouped
 GEMMs, SwiGLU backward, combine backward and dX unpermute) over one batch of synthetic tokens
 whose inputs already sit in HBM.  Prints one JSON line.
+
+Besides the whole-region figure (`value`, `ms_per_step`), the line carries the per-step
+distribution (median, p10, p90 of the same timed steps, from one event pair per step), the shader
+clock sampled while the timed steps run (amdsmi, every XCD) and the fraction of peak at that clock,
+and, with --flush, the same steps timed one at a time after a 1 GiB read that replaces the
+Infinity Cache contents (a read, so the next step does not pay to write dirty lines back).
 """
 from __future__ import annotations
 
@@ -27,6 +34,8 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 PEAK_FP32_VALU_TFLOPS = 157.3   # MI355X fp32 vector
 PEAK_FP8_TFLOPS = 5000.0    # MI355X dense fp8 MFMA
+PEAK_CLOCK_MHZ = 2400.0     # the clock the peaks are quoted at
+VALU_RIDGE = PEAK_FP32_VALU_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)   # FLOP per byte where fp32 VALU meets HBM
 METRIC = "MoE layer fwd+bwd tokens/sec + grouped-GEMM TFLOP/s (% of bf16 MFMA peak), 1 GPU"
 
 # HBM bytes per launch of each grouped GEMM on the Mixtral-shaped layer, from rocprofv3 FETCH_SIZE /
@@ -94,7 +103,109 @@ def _args():
                          "exit: the target of hardware-counter runs")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES bytes 3 times (counter calibration)")
+    ap.add_argument("--flush", action="store_true",
+                    help="also time each step alone after a 1 GiB read that replaces the Infinity Cache contents")
+    ap.add_argument("--no-clock", action="store_true", help="do not sample the shader clock")
+    ap.add_argument("--all-configs", action="store_true",
+                    help="print one summary line over configurations 0-5 (a few steps each) instead of the headline")
     return ap.parse_args()
+
+
+class ClockSampler:
+    """Samples the current graphics clock of every XCD (amdsmi) from a host thread while the GPU
+    works; reads nothing on the GPU, so it does not disturb the kernels.  The driver refreshes this
+    table only every ~0.1 s, so the sampler runs over a window of extra steps of its own (after the
+    timed ones) and drops the first `delay_s` (values from before the GPU got busy)."""
+
+    def __init__(self, period_s=0.004, delay_s=0.8):
+        self.delay = delay_s
+        import threading
+        self.period = period_s
+        self.samples = []
+        self.error = None
+        self._stop = threading.Event()
+        self._thread = None
+        try:
+            import amdsmi
+            amdsmi.amdsmi_init()
+            self._smi = amdsmi
+            self._h = amdsmi.amdsmi_get_processor_handles()[0]
+            self._read()   # fail early if the metric is not readable
+        except Exception as e:   # no amdsmi, no permission, no device
+            self._smi = None
+            self.error = f"{type(e).__name__}: {e}"
+
+    def _read(self):
+        m = self._smi.amdsmi_get_gpu_metrics_info(self._h)
+        vals = m.get("current_gfxclks")
+        if isinstance(vals, (list, tuple)):
+            vals = [v for v in vals if isinstance(v, (int, float)) and 0 < v < 10000]
+        else:
+            vals = []
+        if not vals:
+            v = m.get("current_gfxclk")
+            vals = [v] if isinstance(v, (int, float)) and 0 < v < 10000 else []
+        return vals
+
+    def _run(self):
+        import time as _t
+        if self._stop.wait(self.delay):
+            return
+        while not self._stop.is_set():
+            try:
+                self.samples.extend(self._read())
+            except Exception as e:
+                self.error = f"{type(e).__name__}: {e}"
+                return
+            _t.sleep(self.period)
+
+    def start(self):
+        import threading
+        if self._smi is None:
+            return
+        self._thread = threading.Thread(target=self._run, daemon=True)
+        self._thread.start()
+
+    def stop(self):
+        if self._thread is not None:
+            self._stop.set()
+            self._thread.join()
+        if self._smi is not None:
+            try:
+                self._smi.amdsmi_shut_down()
+            except Exception:
+                pass
+
+    def summary(self):
+        if not self.samples:
+            return {"gfx_mhz_median": None, "samples": 0, "source": "amdsmi current_gfxclks",
+                    "error": self.error or "no samples"}
+        v = sorted(self.samples)
+        q = lambda f: v[min(len(v) - 1, int(f * (len(v) - 1) + 0.5))]
+        return {"gfx_mhz_median": q(0.5), "gfx_mhz_p10": q(0.1), "gfx_mhz_p90": q(0.9), "samples": len(v),
+                "source": "amdsmi gpu_metrics current_gfxclks (every XCD), sampled every 4 ms over ~1.2 s of "
+                          "extra steps run after the timed ones (the first 0.8 s dropped)"}
+
+
+def valu_record(flops, nbytes, avg_ms):
+    """An fp32 vector-ALU call with its HBM bytes, scored against whichever roof its arithmetic
+    intensity reaches first: below the ridge (157.3 TFLOP/s over 8 TB/s, 19.7 FLOP/B) it is HBM-bound."""
+    rec = {"tflops_fp32": round(flops / avg_ms / 1e9, 1), "gbs": round(nbytes / avg_ms / 1e6, 1),
+           "intensity_flop_per_byte": round(flops / nbytes, 2)}
+    if flops / nbytes < VALU_RIDGE:
+        rec["bound"] = "hbm"
+        rec["frac_peak"] = round(nbytes / avg_ms / 1e6 / PEAK_HBM_GBS, 4)
+    else:
+        rec["bound"] = "valu"
+        rec["frac_peak"] = round(flops / avg_ms / 1e9 / PEAK_FP32_VALU_TFLOPS, 4)
+    return rec
+
+
+def _stats(ts):
+    v = sorted(ts)
+    q = lambda f: v[min(len(v) - 1, int(f * (len(v) - 1) + 0.5))]
+    return {"median": round(q(0.5), 4), "p10": round(q(0.1), 4), "p90": round(q(0.9), 4),
+            "min": round(v[0], 4), "max": round(v[-1], 4)}
 
 
 def copy_probe(nbytes):
@@ -174,6 +285,54 @@ def workload_name(i, cfg, router=False):
     return f"config {i}: {cfg.name} {what}, " + ", ".join(extra)
 
 
+def all_configs(a):
+    """One summary line over configurations 0-5: each layer (or dW-only workload) timed for a few
+    steps after a warm-up, with its grouped-GEMM TFLOP/s from per-call events.  Not the headline."""
+    import torch
+
+    from paper_2606_26453_amd import layer as L
+    from paper_2606_26453_amd import workloads as W
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    rows = []
+    steps = max(3, min(a.steps, 10))
+    for i in sorted(W.CONFIGS):
+        cfg = W.CONFIGS[i]
+        if cfg.dw_only:
+            inp = W.make_dw_inputs(cfg, a.seed, dev)
+            lay = L.DWOnly(cfg, inp)
+        else:
+            inp = W.make_inputs(cfg, a.seed, dev)
+            lay = L.MoELayer(cfg, inp)
+        for _ in range(2):
+            lay.step()
+        torch.cuda.synchronize()
+        lay.trace = []
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            lay.step()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        work = lay.work()
+        gms = gfl = 0.0
+        for name, x0, x1 in lay.trace:
+            if work[name][0] == "flops":
+                gms += x0.elapsed_time(x1) / steps
+                gfl += work[name][1]
+        gfl /= steps
+        rows.append({"config": i, "workload": workload_name(i, cfg), "ms_per_step": round(ms, 4),
+                     "tokens_per_s": round(cfg.T / (ms / 1e3), 1),
+                     "gemm_tflops": round(gfl / gms / 1e9, 1) if gms else None,
+                     "gemm_frac_peak": round(gfl / gms / 1e9 / PEAK_BF16_TFLOPS, 4) if gms else None,
+                     "gemm_tflops_step": round(cfg.gemm_flops() / (ms / 1e3) / 1e12, 1)})
+        del lay, inp
+        torch.cuda.empty_cache()
+    print(json.dumps({"summary": "all configurations, 1 GPU, bf16, synthetic inputs", "steps": steps,
+                      "configs": rows}), flush=True)
+
+
 def main():
     a = _args()
     if a.gpus != 1:
@@ -186,6 +345,9 @@ def main():
     if a.gemm_probe:
         from paper_2606_26453_amd import workloads as W
         gemm_probe(a.gemm_probe, W.CONFIGS[a.config])
+        return
+    if a.all_configs:
+        all_configs(a)
         return
     import torch
 
@@ -216,18 +378,33 @@ def main():
 
     lay.trace = None if a.no_trace else []
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    step_ev = [torch.cuda.Event(enable_timing=True) for _ in range(a.steps + 1)]
     torch.cuda.synchronize()
     start.record(stream)
-    for _ in range(a.steps):
+    step_ev[0].record(stream)
+    for i in range(a.steps):
         step()
+        step_ev[i + 1].record(stream)
     end.record(stream)
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(end)
     ms_per_step = total_ms / a.steps
+    step_ms = [step_ev[i].elapsed_time(step_ev[i + 1]) for i in range(a.steps)]
+    trace = lay.trace
+    lay.trace = None
+
+    # the shader clock under this workload: ~2 s of further steps, sampled from the host
+    clock = None if a.no_clock else ClockSampler()
+    if clock:
+        clock.start()
+        for _ in range(max(10, int(2000 / max(ms_per_step, 0.01)))):
+            step()
+        torch.cuda.synchronize()
+        clock.stop()
 
     # per-call averages over the timed region
     per = {}
-    for name, e0, e1 in (lay.trace or []):
+    for name, e0, e1 in (trace or []):
         per.setdefault(name, []).append(e0.elapsed_time(e1))
     work = lay.work()
     calls = {}
@@ -245,8 +422,7 @@ def main():
             rec["tflops_fp8"] = round(amount / avg / 1e9, 1)
             rec["frac_peak"] = round(amount / avg / 1e9 / PEAK_FP8_TFLOPS, 4)
         elif kind == "valu":
-            rec["tflops_fp32"] = round(amount / avg / 1e9, 1)
-            rec["frac_peak"] = round(amount / avg / 1e9 / PEAK_FP32_VALU_TFLOPS, 4)
+            rec.update(valu_record(*amount, avg))
         else:
             rec["gbs"] = round(amount / avg / 1e6, 1)
             rec["frac_peak"] = round(amount / avg / 1e6 / PEAK_HBM_GBS, 4)
@@ -269,6 +445,31 @@ def main():
             roofline = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
                         "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None,
                         "work_per_launch": amount, "avg_launch_ms": round(avg, 4)}
+
+    clock_info = clock.summary() if clock else None
+    mhz = clock_info.get("gfx_mhz_median") if clock_info else None
+    if roofline is not None:
+        roofline["sustained_clock_mhz"] = mhz
+        roofline["frac_at_sustained_clock"] = (round(roofline["frac"] * PEAK_CLOCK_MHZ / mhz, 4) if mhz else None)
+        roofline["clock_source"] = (clock_info or {}).get("source")
+
+    flushed = None
+    if a.flush:
+        # each step alone, after a 1 GiB read (4x the 256 MB Infinity Cache), timed by its own events
+        lay.trace = None
+        junk = torch.empty(1 << 28, dtype=torch.float32, device=dev).fill_(1.0)
+        sink = torch.empty(1, dtype=torch.float32, device=dev)
+        ts = []
+        for _ in range(a.steps):
+            torch.sum(junk, dim=0, keepdim=True, out=sink)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            step()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        flushed = _stats(ts)
+        del junk
 
     tokens = cfg.T
     value = tokens * a.steps / (total_ms / 1e3)
@@ -293,6 +494,9 @@ def main():
         "gemm_tflops": round(gemm_flops / gemm_ms / 1e9, 1) if gemm_ms else None,
         "gemm_frac_peak": round(gemm_flops / gemm_ms / 1e9 / PEAK_BF16_TFLOPS, 4) if gemm_ms else None,
         "gemm_tflops_step": round(cfg.gemm_flops() * (1 / 3 if a.forward_only else 1) / (ms_per_step / 1e3) / 1e12, 1),
+        "step_ms": _stats(step_ms),
+        "flushed_step_ms": flushed,
+        "clock": clock_info,
         "calls": calls,
         "roofline": roofline,
         "groups": W.group_stats(counts),

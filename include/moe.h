@@ -223,13 +223,6 @@ moe_status moe_grouped_gemm_dx_swiglu_bwd(const moe_bf16* dC, const moe_bf16* B,
 size_t moe_grouped_gemm_split_workspace_bytes(void);
 
 /*
- * moe_grouped_gemm_fwd with the same split of the last, partial round of tiles (same arguments,
- * definitions and errors as moe_grouped_gemm_fwd, plus the workspace described above).  The
- * forward kernel runs one workgroup per tile; the split pieces run as extra workgroups that the
- * hardware dispatcher starts as the last full round's CUs free up.  The fused SwiGLU, when
- * requested, is computed from the summed tile exactly as in the unsplit kernel.
- */
-/*
  * The gate/up product with the gather folded into its A operand (steps A4 + B): rows are read
  * straight from X through a row list instead of from the packed, expert-ordered X_perm.  For rows r
  * of group g: C[r, :] = X[row_src[r], :] . B[g] (and C2, act as in moe_grouped_gemm_fwd); with
@@ -309,10 +302,22 @@ moe_status moe_grouped_gemm_fwd_fp8_gate_up(const uint8_t* A, const float* a_sca
                                             int64_t K, int64_t F, moe_bf16* h_gate, moe_bf16* h_up, moe_bf16* act,
                                             void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * moe_grouped_gemm_fwd with the same split of the last, partial round of tiles (same arguments,
+ * definitions and errors as moe_grouped_gemm_fwd, plus a split workspace as described at
+ * moe_grouped_gemm_split_workspace_bytes).  The
+ * forward kernel runs one workgroup per tile; the split pieces run as extra workgroups that the
+ * hardware dispatcher starts as the last full round's CUs free up.  The fused SwiGLU, when
+ * requested, is computed from the summed tile exactly as in the unsplit kernel.
+ */
 moe_status moe_grouped_gemm_fwd_split(const moe_bf16* A, const moe_bf16* B, const moe_bf16* B2,
                                       const int32_t* offsets, int32_t G, int64_t R, int64_t K, int64_t N,
                                       moe_bf16* C, moe_bf16* C2, moe_bf16* act, void* workspace,
                                       size_t workspace_bytes, hipStream_t stream);
+/*
+ * moe_grouped_gemm_dx and moe_grouped_gemm_dx_swiglu_bwd with the split workspace described at
+ * moe_grouped_gemm_split_workspace_bytes (same arguments, definitions and errors otherwise).
+ */
 moe_status moe_grouped_gemm_dx_split(const moe_bf16* dC, const moe_bf16* B, const moe_bf16* dC2,
                                      const moe_bf16* B2, const int32_t* offsets, int32_t G, int64_t R,
                                      int64_t K, int64_t N, moe_bf16* dA, void* workspace,

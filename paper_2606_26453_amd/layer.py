@@ -307,8 +307,11 @@ class MoELayer(_Traced):
             "swiglu_bwd": ("bytes", 5 * R * f * 2),
             "dx_gate_up": ("flops", 4 * R * d * f), "dw_gate_up": ("flops", 4 * R * d * f),
             "unpermute_dx": ("bytes", R * d * 2 + T * d * 2 + R * 4 + (T * d * 2 if self.shared else 0)),
-            # router: fp32 vector-ALU work (multiply-adds x2) of the two contractions with Wr
-            "router_logits": ("valu", 2 * T * d * E), "router_bwd": ("valu", 4 * T * d * E),
+            # router: fp32 vector-ALU work (multiply-adds x2) of the contractions with Wr, with the
+            # HBM bytes each call must move (x bf16 read; logits / dlogits fp32; the backward also
+            # reads and rewrites dX); at these E the intensity sits below the fp32 VALU / HBM ridge
+            "router_logits": ("valu", (2 * T * d * E, T * d * 2 + d * E * 4 + T * E * 4)),
+            "router_bwd": ("valu", (4 * T * d * E, T * d * 2 + 2 * T * d * 2 + 2 * T * E * 4 + T * k * 12)),
             "router_aux_loss": ("bytes", T * E * 4),
             # contraction-major copies for the dW products (read + write)
             "transpose_act": ("bytes", 2 * R * f * 2), "transpose_dy_perm": ("bytes", 2 * R * d * 2),

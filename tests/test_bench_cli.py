@@ -42,3 +42,21 @@ def test_workload_names():
     n5 = bench.workload_name(5, W.CONFIGS[5])
     assert "dW1" in n5 and "bf16 output" in n5 and "alpha=0.24" in n5
     assert "fp32 output" in bench.workload_name(4, W.CONFIGS[4])
+
+
+def test_step_statistics():
+    st = bench._stats([5.0, 1.0, 3.0, 2.0, 4.0, 6.0, 7.0, 8.0, 9.0, 10.0, 11.0])
+    assert st["median"] == 6.0 and st["p10"] == 2.0 and st["p90"] == 10.0
+    assert st["min"] == 1.0 and st["max"] == 11.0
+
+
+def test_vector_alu_calls_are_scored_against_their_roof():
+    # the router's logits at the Mixtral shape: 2*T*d*E FLOP over ~2*T*d bytes -> E FLOP/B = 8,
+    # below the 19.7 FLOP/B ridge: HBM-bound, scored against 8 TB/s
+    T, d, E = 8192, 4096, 8
+    r = bench.valu_record(2 * T * d * E, T * d * 2 + d * E * 4 + T * E * 4, 0.05)
+    assert r["bound"] == "hbm" and abs(r["frac_peak"] - r["gbs"] / 8000.0) < 1e-3
+    assert abs(bench.VALU_RIDGE - 19.6625) < 1e-3
+    # 64 FLOP/B: above the ridge, scored against the fp32 vector peak
+    r = bench.valu_record(64e9, 1e9, 1.0)
+    assert r["bound"] == "valu" and abs(r["frac_peak"] - 64.0 / 157.3) < 1e-3
