@@ -44,12 +44,14 @@ def test_quantize_fp8_rows(M, K):
 
 
 @pytest.mark.parametrize("G,K,N,dual", [(2, 64, 64, False), (3, 208, 128, True), (2, 4096, 256, True),
-                                         (1, 2880, 2880, False), (2, 512, 1408, True)])
+                                         (1, 2880, 2880, False), (2, 512, 1408, True), (1, 14336, 128, False),
+                                         (2, 4112, 256, True)])
 def test_quantize_fp8_weight(G, K, N, dual):
     """The one-pass weight quantizer (transpose, optional 128-channel gate/up interleave, per-channel
     E4M3): codes and scales bit for bit against the oracle's row quantizer on the transposed
     (interleaved) weight and against moe_quantize_fp8_rows on the GPU; zero and half-zero columns
-    included, K = 208 leaves a partial 128-row block."""
+    included; K = 208 leaves a partial block of rows, K = 14336 and 4112 span several 4096-row chunks
+    (the last one partial)."""
     _say("quantize fp8 weight", G, K, N, dual)
     gen = torch.Generator().manual_seed(G * 7 + K + N)
     mk = lambda: (torch.randn((G, K, N), generator=gen) * torch.exp(torch.randn((G, 1, N), generator=gen) * 3)
