@@ -38,17 +38,24 @@ PEAK_CLOCK_MHZ = 2400.0     # the clock the peaks are quoted at
 VALU_RIDGE = PEAK_FP32_VALU_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)   # FLOP per byte where fp32 VALU meets HBM
 METRIC = "MoE layer fwd+bwd tokens/sec + grouped-GEMM TFLOP/s (% of bf16 MFMA peak), 1 GPU"
 
-# HBM bytes per launch of each grouped GEMM on the Mixtral-shaped layer, from rocprofv3 FETCH_SIZE /
-# WRITE_SIZE runs scaled by a plain copy of known size (profiles/grouped_gemm_hbm_traffic_*.md).
+# HBM bytes per launch of each layer call on the Mixtral-shaped layer, from rocprofv3 FETCH_SIZE /
+# WRITE_SIZE runs scaled by a plain copy of known size (profiles/moe_layer_hbm_traffic_*.md).
 # Valid only for the kernel code they were measured on (sha256 prefix of the sources with comments
 # and blank lines removed); otherwise reported null.
-TRAFFIC_SOURCE = (("paper_2606_26453_amd/csrc/grouped_gemm.hip", "paper_2606_26453_amd/csrc/common.h"), "1ad4a0eda89c3ea6")
+TRAFFIC_SOURCES = {
+    "gemm": (("paper_2606_26453_amd/csrc/grouped_gemm.hip", "paper_2606_26453_amd/csrc/common.h"), "b8220e71ad852f69"),
+    "route": (("paper_2606_26453_amd/csrc/route_permute.hip", "paper_2606_26453_amd/csrc/common.h"), "9d885379b7ef9324"),
+    "combine": (("paper_2606_26453_amd/csrc/elementwise.hip", "paper_2606_26453_amd/csrc/common.h"), "9a05da4cb2ca26d3"),
+}
 TRAFFIC_CONFIG = 1
 FETCH_SCALE, WRITE_SCALE = 2.0 * 1024, 1.0 * 1024
-TRAFFIC_KIB = {  # call: (FETCH_SIZE KiB, WRITE_SIZE KiB) per dispatch
-    "fwd_gate_up": (4376720, 1391488), "fwd_down": (1942932, 198664),
-    "dx_down_swiglu_bwd": (2921592, 917504), "dx_gate_up": (4073730, 196616),
-    "dw_down": (1441979, 1835232), "dw_gate_up": (2762870, 3670464),
+TRAFFIC_KIB = {  # call: (source group, FETCH_SIZE KiB, WRITE_SIZE KiB) per dispatch (routing: both launches)
+    "route_permute": ("route", 33110, 131518),
+    "fwd_gate_up": ("gemm", 5525043, 1399104), "fwd_down": ("gemm", 1958329, 199688),
+    "combine": ("combine", 65813, 65536), "combine_bwd": ("combine", 98597, 131141),
+    "dw_down": ("gemm", 1441973, 1835232), "dx_down_swiglu_bwd": ("gemm", 3857606, 917504),
+    "dx_gate_up": ("gemm", 4045202, 196616), "unpermute_dx": ("combine", 65684, 65536),
+    "dw_gate_up": ("gemm", 2771254, 3670464),
 }
 
 
@@ -59,14 +66,20 @@ def code_hash(text):
     return hashlib.sha256("\n".join(ln for ln in lines if ln.strip()).encode()).hexdigest()[:16]
 
 
+def source_hash(files):
+    return code_hash("".join(open(os.path.join(ROOT, f)).read() for f in files))
+
+
 def measured_traffic(call, config):
+    if config != TRAFFIC_CONFIG or call not in TRAFFIC_KIB:
+        return None
+    group, f, w = TRAFFIC_KIB[call]
+    files, sha = TRAFFIC_SOURCES[group]
     try:
-        sha = code_hash("".join(open(os.path.join(ROOT, f)).read() for f in TRAFFIC_SOURCE[0]))
+        if source_hash(files) != sha:
+            return None
     except OSError:
         return None
-    if sha != TRAFFIC_SOURCE[1] or config != TRAFFIC_CONFIG or call not in TRAFFIC_KIB:
-        return None
-    f, w = TRAFFIC_KIB[call]
     return int(f * FETCH_SCALE + w * WRITE_SCALE)
 
 
@@ -426,6 +439,9 @@ def main():
         else:
             rec["gbs"] = round(amount / avg / 1e6, 1)
             rec["frac_peak"] = round(amount / avg / 1e6 / PEAK_HBM_GBS, 4)
+        hbm = measured_traffic(name, a.config)
+        if hbm is not None:   # counter bytes over the algorithmic bytes or operand+output bytes
+            rec["hbm_bytes_measured"] = hbm
         calls[name] = rec
 
     roofline = None
@@ -443,7 +459,8 @@ def main():
         else:
             ach = amount / avg / 1e6
             roofline = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
-                        "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None,
+                        "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4),
+                        "traffic": measured_traffic(dom, a.config),
                         "work_per_launch": amount, "avg_launch_ms": round(avg, 4)}
 
     clock_info = clock.summary() if clock else None

@@ -25,15 +25,39 @@ def test_code_hash_ignores_comments_and_blank_lines():
 
 
 def test_traffic_is_reported_only_for_the_measured_code(monkeypatch):
-    call = next(iter(bench.TRAFFIC_KIB))
-    f, w = bench.TRAFFIC_KIB[call]
-    src = "".join(open(os.path.join(ROOT, p)).read() for p in bench.TRAFFIC_SOURCE[0])
-    monkeypatch.setattr(bench, "TRAFFIC_SOURCE", (bench.TRAFFIC_SOURCE[0], bench.code_hash(src)))
-    assert bench.measured_traffic(call, bench.TRAFFIC_CONFIG) == int(f * bench.FETCH_SCALE + w * bench.WRITE_SCALE)
-    assert bench.measured_traffic(call, bench.TRAFFIC_CONFIG + 1) is None   # another workload
+    for call, (group, f, w) in bench.TRAFFIC_KIB.items():
+        files = bench.TRAFFIC_SOURCES[group][0]
+        src = {g: (fs, bench.source_hash(fs)) for g, (fs, _) in bench.TRAFFIC_SOURCES.items()}
+        monkeypatch.setattr(bench, "TRAFFIC_SOURCES", src)
+        assert bench.measured_traffic(call, bench.TRAFFIC_CONFIG) == int(f * bench.FETCH_SCALE + w * bench.WRITE_SCALE)
+        assert bench.measured_traffic(call, bench.TRAFFIC_CONFIG + 1) is None   # another workload
+        monkeypatch.setattr(bench, "TRAFFIC_SOURCES", dict(src, **{group: (files, "0" * 16)}))
+        assert bench.measured_traffic(call, bench.TRAFFIC_CONFIG) is None        # the kernels changed since
     assert bench.measured_traffic("no_such_call", bench.TRAFFIC_CONFIG) is None
-    monkeypatch.setattr(bench, "TRAFFIC_SOURCE", (bench.TRAFFIC_SOURCE[0], "0" * 16))
-    assert bench.measured_traffic(call, bench.TRAFFIC_CONFIG) is None        # the kernels changed since
+
+
+def test_measured_traffic_covers_every_layer_call():
+    # every call of the default layer step has counter bytes, and none moves fewer bytes than it
+    # must (the unique bytes of the HBM-bound calls; the MFMA calls' operands and outputs)
+    from paper_2606_26453_amd.layer import MoELayer
+    lay = object.__new__(MoELayer)
+    lay.cfg, lay.fp8, lay.gather_fused, lay.shared = W.CONFIGS[bench.TRAFFIC_CONFIG], False, False, False
+    work = lay.work()
+    c = lay.cfg
+    R = c.T * c.k
+    operands = {"fwd_gate_up": R * c.d * 2 + 2 * c.E * c.d * c.f * 2 + 3 * R * c.f * 2,
+                "fwd_down": R * c.f * 2 + c.E * c.f * c.d * 2 + R * c.d * 2,
+                "dw_down": R * c.f * 2 + R * c.d * 2 + c.E * c.f * c.d * 4,
+                "dx_down_swiglu_bwd": R * c.d * 2 + c.E * c.f * c.d * 2 + 4 * R * c.f * 2,
+                "dx_gate_up": 2 * R * c.f * 2 + 2 * c.E * c.d * c.f * 2 + R * c.d * 2,
+                "dw_gate_up": R * c.d * 2 + 2 * R * c.f * 2 + 2 * c.E * c.d * c.f * 4}
+    step_calls = {"route_permute", "fwd_gate_up", "fwd_down", "combine", "combine_bwd", "dw_down",
+                  "dx_down_swiglu_bwd", "dx_gate_up", "unpermute_dx", "dw_gate_up"}
+    assert set(bench.TRAFFIC_KIB) == step_calls
+    for call, (_, f, w) in bench.TRAFFIC_KIB.items():
+        hbm = f * bench.FETCH_SCALE + w * bench.WRITE_SCALE
+        need = work[call][1] if work[call][0] == "bytes" else operands[call]
+        assert hbm >= 0.999 * need, call
 
 
 def test_workload_names():
