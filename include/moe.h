@@ -414,9 +414,11 @@ moe_status moe_transpose_grouped(const moe_bf16* src, const int32_t* offsets, in
  * logits[t, e] = sum_i x[t, i] * wr[i, e] (+ bias[e]) in fp32: the router ahead of the top-k
  * selection (section 5.4 names top-k routing; the router itself is not described: one linear
  * map, the usual MoE router).  x [T,d] bf16 (16-byte aligned); wr [d,E] fp32; bias [E] fp32 or
- * NULL; logits [T,E] fp32.  1 <= E <= 256, d a multiple of 64.  The sum runs over eight slices
- * of the hidden dimension added in a fixed order: deterministic, but not bitwise equal to a CPU
- * fp32 dot product, so decisions at near-tied logits may differ from one computed elsewhere.
+ * NULL; logits [T,E] fp32.  1 <= E <= 256, d a multiple of 64.  The sum runs in a fixed order
+ * (d <= 4096: products over groups of 8 consecutive columns, the groups added pairwise within a
+ * 512-column slice and the slices in order; larger d: eight slices of the hidden dimension added
+ * in order): deterministic, but not bitwise equal to a CPU fp32 dot product, so decisions at
+ * near-tied logits may differ from one computed elsewhere.
  */
 moe_status moe_router_logits(const moe_bf16* x, const float* wr, const float* bias, int64_t T,
                              int64_t d, int32_t E, float* logits, hipStream_t stream);
@@ -448,6 +450,23 @@ moe_status moe_router_bwd(const moe_bf16* x, const float* wr, const float* logit
                           int32_t normalize_topk, float aux_alpha, void* workspace,
                           size_t workspace_bytes, float* dlogits, float* dwr, moe_bf16* dx,
                           hipStream_t stream);
+
+/*
+ * The unpermute-sum of dX fused with the router's share of the token gradient:
+ *   dx[t, i] = bf16( bf16(sum_j dx_perm[row_of_slot[t*k + j], i] + add[t, i])
+ *                    + sum_e dlogits[t, e] * wr[i, e] )
+ * i.e. exactly moe_unpermute_combine (topk_w = NULL) followed by moe_router_bwd's update of dx,
+ * bitwise, in one pass over dX instead of two (the router's share of dX, section 5.4's top-k
+ * routing read as a linear router; the experts' sum as in moe_unpermute_combine).  dx_perm [T*k,d]
+ * bf16; row_of_slot [T*k] int32; add [T,d] bf16 or NULL (the shared experts' dX); dlogits [T,E]
+ * and wr [d,E] fp32; dx [T,d] bf16 output (must not overlap dx_perm).  dx_perm, add and dx 16-byte
+ * aligned.  Supports 1 <= E <= 16 and d <= 4096 (a multiple of 64); other sizes return
+ * MOE_ERROR_NOT_SUPPORTED (call the two functions instead).  No workspace.
+ */
+moe_status moe_unpermute_router_dx(const moe_bf16* dx_perm, const int32_t* row_of_slot,
+                                   const moe_bf16* add, const float* dlogits, const float* wr,
+                                   int64_t T, int64_t d, int32_t k, int32_t E, moe_bf16* dx,
+                                   hipStream_t stream);
 
 /* Bytes of device workspace moe_router_aux_loss needs. */
 size_t moe_router_aux_loss_workspace_bytes(int64_t T, int32_t E);

@@ -73,6 +73,10 @@ class MoELayer(_Traced):
         self.concurrent = concurrent
         self.side = torch.cuda.Stream(device=inputs["x"].device) if concurrent else None
         self.router = router
+        # with the router at E <= 16, d <= 4096 its backward (dlogits, dWr) runs as soon as d_topk_w
+        # exists, and its share of dX joins the experts' unpermute-sum in one pass over dX
+        # (moe_unpermute_router_dx, bitwise the two-pass result)
+        self.router_fused_dx = router and cfg.E <= 16 and cfg.d <= 4096
         self.aux_alpha = float(aux_alpha)
         self.inp = inputs
         self.normalize = normalize_topk
@@ -226,6 +230,10 @@ class MoELayer(_Traced):
             dx_add = b["dx_sh"]
         run("combine_bwd", moe.moe_unpermute_combine_bwd, i["dy"], b["topk_w"], b["row_of_slot"], k,
             y_perm=b["y_perm"], dy_perm=b["dy_perm"], d_topk_w=b["d_topk_w"], stream=stream)
+        if self.router_fused_dx:
+            run("router_bwd", moe.moe_router_bwd, i["x"], i["wr"], b["logits"], b["topk_idx"], b["topk_w"],
+                b["d_topk_w"], b["offsets"], self.normalize, self.aux_alpha, dx=None, workspace=b["router_ws"],
+                dlogits=b["dlogits"], dwr=b["dwr"], stream=stream)
         self._join(side, main)            # dW_down needs dY_perm
         if self.dw_t:
             run("transpose_act", moe.moe_transpose_grouped, b["act"], b["offsets"], dst=b["act_t"], stream=side)
@@ -252,8 +260,7 @@ class MoELayer(_Traced):
         # in the last-level cache (dW gate/up's 3.8 GB of fp32 results would evict it first)
         early = side is main
         if early:
-            run("unpermute_dx", moe.moe_unpermute_combine, b["dx_perm"], None, b["row_of_slot"], k, add=dx_add,
-                y=b["dx"], stream=stream)
+            self._unpermute_dx(dx_add, stream)
         if self.dw_t:
             run("transpose_x_perm", moe.moe_transpose_grouped, b["x_perm"], b["offsets"], dst=b["x_perm_t"],
                 stream=side)
@@ -265,13 +272,21 @@ class MoELayer(_Traced):
                 dB=b["dw_gate"], dB2=b["dw_up"], stream=side, counters=self.dw_cnt)
         self._join(main, side)            # the shared dX, and every weight gradient, are complete
         if not early:
-            run("unpermute_dx", moe.moe_unpermute_combine, b["dx_perm"], None, b["row_of_slot"], k, add=dx_add,
-                y=b["dx"], stream=stream)
-        if self.router:
+            self._unpermute_dx(dx_add, stream)
+        if self.router and not self.router_fused_dx:
             run("router_bwd", moe.moe_router_bwd, i["x"], i["wr"], b["logits"], b["topk_idx"], b["topk_w"],
                 b["d_topk_w"], b["offsets"], self.normalize, self.aux_alpha, dx=b["dx"], workspace=b["router_ws"],
                 dlogits=b["dlogits"], dwr=b["dwr"], stream=stream)
         return b["dx"]
+
+    def _unpermute_dx(self, dx_add, stream):
+        b, i, k = self.buf, self.inp, self.cfg.k
+        if self.router_fused_dx:
+            self._run("unpermute_dx_router", moe.moe_unpermute_router_dx, b["dx_perm"], b["row_of_slot"], k,
+                      b["dlogits"], i["wr"], add=dx_add, dx=b["dx"], stream=stream)
+        else:
+            self._run("unpermute_dx", moe.moe_unpermute_combine, b["dx_perm"], None, b["row_of_slot"], k,
+                      add=dx_add, y=b["dx"], stream=stream)
 
     @property
     def R(self):
@@ -311,7 +326,12 @@ class MoELayer(_Traced):
             # HBM bytes each call must move (x bf16 read; logits / dlogits fp32; the backward also
             # reads and rewrites dX); at these E the intensity sits below the fp32 VALU / HBM ridge
             "router_logits": ("valu", (2 * T * d * E, T * d * 2 + d * E * 4 + T * E * 4)),
-            "router_bwd": ("valu", (4 * T * d * E, T * d * 2 + 2 * T * d * 2 + 2 * T * E * 4 + T * k * 12)),
+            "router_bwd": (("valu", (2 * T * d * E, T * d * 2 + 2 * T * E * 4 + T * k * 12 + d * E * 4))
+                           if self.router_fused_dx else
+                           ("valu", (4 * T * d * E, T * d * 2 + 2 * T * d * 2 + 2 * T * E * 4 + T * k * 12))),
+            # the unpermute-sum with the router's share of dX (read dlogits and Wr as well)
+            "unpermute_dx_router": ("bytes", R * d * 2 + T * d * 2 + R * 4 + T * E * 4 + d * E * 4
+                                    + (T * d * 2 if self.shared else 0)),
             "router_aux_loss": ("bytes", T * E * 4),
             # contraction-major copies for the dW products (read + write)
             "transpose_act": ("bytes", 2 * R * f * 2), "transpose_dy_perm": ("bytes", 2 * R * d * 2),

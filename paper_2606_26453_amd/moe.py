@@ -71,6 +71,7 @@ _SIG = {
     "moe_router_bwd_workspace_bytes": (ctypes.c_size_t, [_I64, _I64, _I32]),
     "moe_router_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I32, _I32, _I32, ctypes.c_float,
                                       _P, ctypes.c_size_t, _P, _P, _P, _P]),
+    "moe_unpermute_router_dx": (ctypes.c_int, [_P, _P, _P, _P, _P, _I64, _I64, _I32, _I32, _P, _P]),
     "moe_router_aux_loss_workspace_bytes": (ctypes.c_size_t, [_I64, _I32]),
     "moe_router_aux_loss": (ctypes.c_int, [_P, _P, _I64, _I32, _I32, ctypes.c_float, _P, ctypes.c_size_t, _P, _P]),
     "moe_grouped_gemm_dx_swiglu_bwd": (ctypes.c_int, [_P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P, _P, _P]),
@@ -391,6 +392,23 @@ def moe_unpermute_combine(y_perm, topk_w, row_of_slot, k, add=None, y=None, stre
            lib().moe_unpermute_combine(_ptr(y_perm), _ptr(topk_w), _ptr(row_of_slot), _ptr(add), T, d, k,
                                        _ptr(y), _stream(stream)))
     return y
+
+
+def moe_unpermute_router_dx(dx_perm, row_of_slot, k, dlogits, wr, add=None, dx=None, stream=None):
+    R, d = dx_perm.shape
+    T = R // k
+    E = wr.shape[1]
+    _need(dx_perm, torch.bfloat16, (T * k, d), "dx_perm")
+    _need(row_of_slot, torch.int32, (R,), "row_of_slot")
+    _need(add, torch.bfloat16, (T, d), "add")
+    _need(dlogits, torch.float32, (T, E), "dlogits")
+    _need(wr, torch.float32, (d, E), "wr")
+    dx = torch.empty((T, d), dtype=torch.bfloat16, device=dx_perm.device) if dx is None else dx
+    _need(dx, torch.bfloat16, (T, d), "dx")
+    _check("moe_unpermute_router_dx",
+           lib().moe_unpermute_router_dx(_ptr(dx_perm), _ptr(row_of_slot), _ptr(add), _ptr(dlogits), _ptr(wr),
+                                         T, d, k, E, _ptr(dx), _stream(stream)))
+    return dx
 
 
 def moe_unpermute_combine_bwd(dy, topk_w, row_of_slot, k, y_perm=None, dy_perm=None, d_topk_w=None,

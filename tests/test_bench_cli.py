@@ -42,6 +42,7 @@ def test_measured_traffic_covers_every_layer_call():
     from paper_2606_26453_amd.layer import MoELayer
     lay = object.__new__(MoELayer)
     lay.cfg, lay.fp8, lay.gather_fused, lay.shared = W.CONFIGS[bench.TRAFFIC_CONFIG], False, False, False
+    lay.router_fused_dx = False
     work = lay.work()
     c = lay.cfg
     R = c.T * c.k

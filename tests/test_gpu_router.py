@@ -30,7 +30,8 @@ def _inputs(T, d, E, seed, bias=True):
 
 # logits: fp32 sums of d products against the exact sum; bound |err| <= 2^-22 * d * sum|x_i wr_i|
 @pytest.mark.parametrize("T,d,E", [(1, 64, 1), (130, 256, 4), (1000, 512, 8), (333, 128, 16), (257, 192, 40),
-                                   (200, 1024, 64), (64, 64, 256)])
+                                   (200, 1024, 64), (64, 64, 256), (2000, 4096, 8), (37, 2880, 9),
+                                   (100, 4160, 8)])
 def test_router_logits(T, d, E):
     _say("router logits", T, d, E)
     x, wr, b = _inputs(T, d, E, T + d + E)
@@ -72,7 +73,8 @@ def test_routing_decision_near_ties():
 
 
 @pytest.mark.parametrize("normalize,alpha", [(True, 0.0), (True, 0.01), (False, 0.0), (False, 0.02)])
-@pytest.mark.parametrize("T,d,E,k", [(300, 256, 8, 2), (257, 128, 64, 6), (64, 192, 40, 3)])
+@pytest.mark.parametrize("T,d,E,k", [(300, 256, 8, 2), (257, 128, 64, 6), (64, 192, 40, 3), (513, 320, 16, 4),
+                                     (700, 4160, 8, 2)])
 def test_router_bwd(T, d, E, k, normalize, alpha):
     _say("router bwd", T, d, E, k, normalize, alpha)
     x, wr, b = _inputs(T, d, E, 7 * T + E)
@@ -103,8 +105,9 @@ def test_router_bwd(T, d, E, k, normalize, alpha):
     assert (np.abs(f64(dx) - ref_dx) <= ulp * 1.01).all()
 
 
-def test_router_aux_loss():
-    T, E, k, alpha = 1000, 32, 4, 0.01
+@pytest.mark.parametrize("T,E,k", [(1000, 32, 4), (1000, 8, 2), (4099, 13, 3), (1, 4, 1)])
+def test_router_aux_loss(T, E, k):
+    alpha = 0.01
     g = torch.Generator().manual_seed(5)
     logits = (torch.randn((T, E), generator=g) * 2).to(DEV)
     r = moe.moe_route_permute(logits, None, k)
@@ -117,6 +120,43 @@ def test_router_aux_loss():
     lz = moe.moe_router_aux_loss(z, r["offsets"], k, alpha)
     torch.cuda.synchronize()
     assert abs(lz.item() - alpha) <= 1e-6
+
+
+@pytest.mark.parametrize("T,d,E,k,with_add", [(1, 64, 1, 1, False), (37, 192, 5, 2, True), (300, 256, 8, 2, False),
+                                               (129, 2048, 13, 3, True), (64, 4096, 16, 4, False),
+                                               (50, 512, 8, 6, True), (40, 128, 16, 8, False),
+                                               (1000, 4096, 8, 2, True)])
+def test_unpermute_router_dx(T, d, E, k, with_add):
+    """The unpermute-sum of dX fused with the router's share: bitwise equal to moe_unpermute_combine
+    followed by moe_router_bwd's in-place update of dx (same dlogits), and within one bf16 step of
+    the oracle's composition of the two (each rounded to bf16)."""
+    _say("unpermute + router dx", T, d, E, k, with_add)
+    x, wr, _ = _inputs(T, d, E, 3 * T + d + E, bias=False)
+    xd, wrd = x.to(DEV), wr.to(DEV)
+    logits = moe.moe_router_logits(xd, wrd)
+    r = moe.moe_route_permute(logits, None, k)
+    g = torch.Generator().manual_seed(T + k)
+    d_w = torch.randn((T, k), generator=g).to(DEV)
+    dx_perm = torch.randn((T * k, d), generator=g).to(torch.bfloat16)
+    add = torch.randn((T, d), generator=g).to(torch.bfloat16) if with_add else None
+    addd = add.to(DEV) if with_add else None
+    two = moe.moe_unpermute_combine(dx_perm.to(DEV), None, r["row_of_slot"], k, add=addd)
+    dl, _ = moe.moe_router_bwd(xd, wrd, logits, r["topk_idx"], r["topk_w"], d_w, r["offsets"], dx=two)
+    fused = poison_(torch.empty((T, d), dtype=torch.bfloat16, device=DEV))
+    moe.moe_unpermute_router_dx(dx_perm.to(DEV), r["row_of_slot"], k, dl, wrd, add=addd, dx=fused)
+    torch.cuda.synchronize()
+    assert torch.equal(fused.view(torch.int16), two.view(torch.int16))
+    base = O.combine(f64(dx_perm), None, i64(r["row_of_slot"]), k, add=None if add is None else f64(add))
+    _, ref = O.router_bwd(f64(x), f64(wr), f64(dl), dx=base)
+    ulp = np.maximum(np.abs(ref), 2.0 ** -126) * 2.0 ** -7
+    assert (np.abs(f64(fused) - ref) <= ulp * 1.01).all()
+
+
+def test_unpermute_router_dx_refuses_unsupported_sizes():
+    z = torch.zeros((4, 64), dtype=torch.bfloat16, device=DEV)
+    ros = torch.arange(4, dtype=torch.int32, device=DEV)
+    with pytest.raises(RuntimeError, match="E <= 16"):
+        moe.moe_unpermute_router_dx(z, ros, 1, torch.zeros((4, 17), device=DEV), torch.zeros((64, 17), device=DEV))
 
 
 @pytest.mark.parametrize("cfg_id", [0, 2])
