@@ -97,6 +97,10 @@ def _args():
                     help="weight gradients from contraction-major copies of their operands")
     ap.add_argument("--fp8-forward", action="store_true",
                     help="the routed experts' forward products on E4M3 operands (a variant; the metric is bf16)")
+    ap.add_argument("--fp8-backward", action="store_true",
+                    help="the routed experts' data-gradient products on E4M3 operands (a variant; the metric is bf16)")
+    ap.add_argument("--fp8-fixed-weights", action="store_true",
+                    help="with --fp8-forward/--fp8-backward: quantize the weights once (held fixed), not every step")
     ap.add_argument("--forward-only", action="store_true", help="time the forward alone (a variant)")
     ap.add_argument("--gather-fused", action="store_true",
                     help="gate/up product reads x through token_of_row; X_perm is gathered in the backward")
@@ -198,6 +202,12 @@ class ClockSampler:
         return {"gfx_mhz_median": q(0.5), "gfx_mhz_p10": q(0.1), "gfx_mhz_p90": q(0.9), "samples": len(v),
                 "source": "amdsmi gpu_metrics current_gfxclks (every XCD), sampled every 4 ms over ~1.2 s of "
                           "extra steps run after the timed ones (the first 0.8 s dropped)"}
+
+
+def fp8_dtype(a):
+    """The arithmetic types of the run: bf16, or which expert products run on E4M3 operands."""
+    parts = [n for n, on in (("forward", a.fp8_forward), ("data-gradient", a.fp8_backward)) if on]
+    return f"fp8-e4m3 ({' and '.join(parts)} expert products) + bf16" if parts else "bf16"
 
 
 def valu_record(flops, nbytes, avg_ms):
@@ -379,6 +389,7 @@ def main():
         lay = L.MoELayer(cfg, inp, router=a.router, aux_alpha=a.aux_alpha if a.router else 0.0,
                          dw_transposed=a.dw_transposed, concurrent=a.concurrent, split_tail=not a.no_split_tail,
                          gather_fused=a.gather_fused, fp8_forward=a.fp8_forward,
+                         fp8_backward=a.fp8_backward, fp8_requantize=not a.fp8_fixed_weights,
                          dw_persistent=not a.dw_one_per_tile)
     torch.cuda.synchronize()
     t_gen = time.perf_counter() - t_gen
@@ -496,11 +507,13 @@ def main():
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
         "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "fp8-e4m3 (forward expert products) + bf16" if a.fp8_forward else "bf16",
+        "dtype": fp8_dtype(a),
         "data": "synthetic (seeded N(0,1) activations, N(0,0.02) weights, router logits X.Wr)",
         "config": {"workload": workload_name(a.config, cfg, a.router and not cfg.dw_only)
                    + (" (forward only)" if a.forward_only and not cfg.dw_only else "")
                    + (", expert forward products in FP8 E4M3" if a.fp8_forward else "")
+                   + (", expert data-gradient products in FP8 E4M3" if a.fp8_backward else "")
+                   + (", FP8 weights quantized once (held fixed)" if a.fp8_fixed_weights else "")
                    + (", gather fused into the gate/up product" if a.gather_fused else "")
                    + (", dW from contraction-major copies" if a.dw_transposed else "")
                    + (", no split tail" if a.no_split_tail else "")
@@ -519,7 +532,7 @@ def main():
         "groups": W.group_stats(counts),
         "input_gen_s": round(t_gen, 1),
     }
-    if not a.no_cpu_baseline and not cfg.dw_only and not (a.fp8_forward or a.forward_only):
+    if not a.no_cpu_baseline and not cfg.dw_only and not (a.fp8_forward or a.fp8_backward or a.forward_only):
         ts = a.cpu_sample_tokens or max(8, min(cfg.T, int(6e12 // (18 * cfg.k * cfg.d * cfg.f))))
         out["cpu_baseline"] = cpu_baseline(cfg, inp, ts)
     print(json.dumps(out), flush=True)

@@ -255,6 +255,19 @@ moe_status moe_quantize_fp8_rows(const moe_bf16* x, int64_t M, int64_t K, uint8_
                                  hipStream_t stream);
 
 /*
+ * The same quantization of the rows of two matrices joined along the contraction: row r is
+ * [x[r, :] | x2[r, :]] (x, x2 [M,K] bf16), with one amax and one scale over both halves, and
+ * q [M, 2K] holds x's codes in columns 0..K-1 and x2's in K..2K-1, code for code what
+ * moe_quantize_fp8_rows gives for the concatenated [M, 2K] matrix.  The operand of a product whose
+ * contraction runs over two matrices: the data gradient of the gate and up projections (section
+ * 5.4's backward), dX = dH_gate . W_gate^T + dH_up . W_up^T, as one FP8 product over [dH_gate |
+ * dH_up] (rows of M = R routed rows) and [W_gate | W_up] (rows of M = G*K_out output channels).
+ * Alignment and errors as moe_quantize_fp8_rows; x2 NULL -> INVALID_VALUE.
+ */
+moe_status moe_quantize_fp8_rows2(const moe_bf16* x, const moe_bf16* x2, int64_t M, int64_t K, uint8_t* q,
+                                  float* scale, hipStream_t stream);
+
+/*
  * The same quantization for a weight kept as [expert, contraction, output channel], in one pass
  * per column block: W [G,K,N] bf16 -> Q [G,N',K] uint8 and scale [G,N'] fp32, where row (g, n) of
  * Q holds the codes of column n of W[g] (an output channel over its K contraction elements).
@@ -286,6 +299,21 @@ moe_status moe_quantize_fp8_weight(const moe_bf16* w, const moe_bf16* w2, int64_
 moe_status moe_grouped_gemm_fwd_fp8(const uint8_t* A, const float* a_scale, const uint8_t* Wt, const float* w_scale,
                                     const int32_t* offsets, int32_t G, int64_t R, int64_t K, int64_t N, moe_bf16* C,
                                     void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Steps G + I on E4M3 operands (section 5.4's backward of the down projection and of the SwiGLU):
+ * dA[r,n] = bf16(a_scale[r] * w_scale[g,n] * sum_k A[r,k] * Wt[g,n,k]) as moe_grouped_gemm_fwd_fp8
+ * computes it (A = the quantized dY_perm [R,K], Wt = the down weight as [G, N, K]: output channel n
+ * of the expert's ffn dimension, contraction over the hidden dimension, the layout it is stored in,
+ * quantized per row by moe_quantize_fp8_rows), followed in the epilogue by the SwiGLU backward of
+ * moe_grouped_gemm_dx_swiglu_bwd on that bf16 dA: dh_gate, dh_up [R,N] bf16 from h_gate, h_up [R,N].
+ * workspace: NULL or a split workspace.  Errors as moe_grouped_gemm_fwd_fp8.
+ */
+moe_status moe_grouped_gemm_dx_swiglu_bwd_fp8(const uint8_t* A, const float* a_scale, const uint8_t* Wt,
+                                              const float* w_scale, const int32_t* offsets, int32_t G, int64_t R,
+                                              int64_t K, int64_t N, const moe_bf16* h_gate, const moe_bf16* h_up,
+                                              moe_bf16* dh_gate, moe_bf16* dh_up, void* workspace,
+                                              size_t workspace_bytes, hipStream_t stream);
 
 /*
  * The gate and up projections (steps B + C) on E4M3 operands in one product: Wt [G, 2F, K] holds

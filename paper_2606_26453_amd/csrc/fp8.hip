@@ -29,17 +29,23 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
-// One workgroup (256 threads) per row; each thread handles 8 elements (16 bytes) at a time.
-__global__ __launch_bounds__(256) void quantize_fp8_rows_kernel(const u32x4* __restrict__ x, int64_t K8,
+// One workgroup (256 threads) per row; each thread handles 8 elements (16 bytes) at a time.  With
+// a second source x2 the row is the concatenation [x[r, :] | x2[r, :]] (one amax and one scale
+// over both, x's codes first): the operand of a product whose contraction runs over two matrices.
+__global__ __launch_bounds__(256) void quantize_fp8_rows_kernel(const u32x4* __restrict__ x,
+                                                                const u32x4* __restrict__ x2, int64_t K8,
                                                                 uint2* __restrict__ q, float* __restrict__ scale) {
   __shared__ float s_max[4];
   const int64_t r = blockIdx.x;
-  const u32x4* row = x + r * K8;
+  const int nsrc = x2 ? 2 : 1;
   float m = 0.0f;
-  for (int64_t c = threadIdx.x; c < K8; c += 256) {
-    const u32x4 v = row[c];
+  for (int h = 0; h < nsrc; ++h) {
+    const u32x4* row = (h ? x2 : x) + r * K8;
+    for (int64_t c = threadIdx.x; c < K8; c += 256) {
+      const u32x4 v = row[c];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) m = fmaxf(m, fmaxf(fabsf(bf16_lo(v[e])), fabsf(bf16_hi(v[e]))));
+      for (int e = 0; e < 4; ++e) m = fmaxf(m, fmaxf(fabsf(bf16_lo(v[e])), fabsf(bf16_hi(v[e]))));
+    }
   }
   m = wave_max(m);
   if ((threadIdx.x & 63) == 0) s_max[threadIdx.x >> 6] = m;
@@ -48,17 +54,20 @@ __global__ __launch_bounds__(256) void quantize_fp8_rows_kernel(const u32x4* __r
   const bool nz = amax > 0.0f;
   const float inv = nz ? __fdiv_rn(448.0f, amax) : 1.0f;
   if (threadIdx.x == 0) scale[r] = nz ? __fdiv_rn(amax, 448.0f) : 1.0f;
-  uint2* qrow = q + r * K8;
-  for (int64_t c = threadIdx.x; c < K8; c += 256) {
-    const u32x4 v = row[c];
-    uint32_t w[2];
+  for (int h = 0; h < nsrc; ++h) {
+    const u32x4* row = (h ? x2 : x) + r * K8;
+    uint2* qrow = q + r * (nsrc * K8) + h * K8;
+    for (int64_t c = threadIdx.x; c < K8; c += 256) {
+      const u32x4 v = row[c];
+      uint32_t w[2];
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      w[h] = e4m3_code(__fmul_rn(bf16_lo(v[2 * h]), inv)) | (e4m3_code(__fmul_rn(bf16_hi(v[2 * h]), inv)) << 8) |
-             (e4m3_code(__fmul_rn(bf16_lo(v[2 * h + 1]), inv)) << 16) |
-             (e4m3_code(__fmul_rn(bf16_hi(v[2 * h + 1]), inv)) << 24);
+      for (int hh = 0; hh < 2; ++hh) {
+        w[hh] = e4m3_code(__fmul_rn(bf16_lo(v[2 * hh]), inv)) | (e4m3_code(__fmul_rn(bf16_hi(v[2 * hh]), inv)) << 8) |
+                (e4m3_code(__fmul_rn(bf16_lo(v[2 * hh + 1]), inv)) << 16) |
+                (e4m3_code(__fmul_rn(bf16_hi(v[2 * hh + 1]), inv)) << 24);
+      }
+      qrow[c] = make_uint2(w[0], w[1]);
     }
-    qrow[c] = make_uint2(w[0], w[1]);
   }
 }
 
@@ -216,17 +225,33 @@ extern "C" moe_status moe_quantize_fp8_weight(const moe_bf16* w, const moe_bf16*
   return check_launch("quantize_cols_kernel");
 }
 
-extern "C" moe_status moe_quantize_fp8_rows(const moe_bf16* x, int64_t M, int64_t K, uint8_t* q, float* scale,
-                                            hipStream_t stream) {
-  const char* fn = "moe_quantize_fp8_rows";
+namespace moe {
+namespace {
+moe_status quantize_rows_impl(const char* fn, const moe_bf16* x, const moe_bf16* x2, int64_t M, int64_t K,
+                              uint8_t* q, float* scale, hipStream_t stream) {
   if (M < 0 || K <= 0) return fail(MOE_ERROR_INVALID_VALUE, "%s: bad size", fn);
   if (K % 16) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: K must be a multiple of 16", fn);
   if (M >= ((int64_t)1 << 31)) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: M >= 2^31", fn);
   if (M == 0) return MOE_SUCCESS;
   if (!x || !q || !scale) return fail(MOE_ERROR_INVALID_VALUE, "%s: NULL pointer", fn);
-  if (!aligned16(x) || (reinterpret_cast<uintptr_t>(q) & 7) || (reinterpret_cast<uintptr_t>(scale) & 3))
-    return fail(MOE_ERROR_INVALID_VALUE, "%s: x must be 16-byte, q 8-byte, scale 4-byte aligned", fn);
-  quantize_fp8_rows_kernel<<<(unsigned)M, 256, 0, stream>>>(reinterpret_cast<const u32x4*>(x), K / 8,
+  if (!aligned16(x) || (x2 && !aligned16(x2)) || (reinterpret_cast<uintptr_t>(q) & 7) ||
+      (reinterpret_cast<uintptr_t>(scale) & 3))
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: x (and x2) must be 16-byte, q 8-byte, scale 4-byte aligned", fn);
+  quantize_fp8_rows_kernel<<<(unsigned)M, 256, 0, stream>>>(reinterpret_cast<const u32x4*>(x),
+                                                             reinterpret_cast<const u32x4*>(x2), K / 8,
                                                              reinterpret_cast<uint2*>(q), scale);
   return check_launch("quantize_fp8_rows_kernel");
+}
+}  // namespace
+}  // namespace moe
+
+extern "C" moe_status moe_quantize_fp8_rows(const moe_bf16* x, int64_t M, int64_t K, uint8_t* q, float* scale,
+                                            hipStream_t stream) {
+  return quantize_rows_impl("moe_quantize_fp8_rows", x, nullptr, M, K, q, scale, stream);
+}
+
+extern "C" moe_status moe_quantize_fp8_rows2(const moe_bf16* x, const moe_bf16* x2, int64_t M, int64_t K,
+                                             uint8_t* q, float* scale, hipStream_t stream) {
+  if (!x2) return fail(MOE_ERROR_INVALID_VALUE, "moe_quantize_fp8_rows2: x2 is NULL");
+  return quantize_rows_impl("moe_quantize_fp8_rows2", x, x2, M, K, q, scale, stream);
 }

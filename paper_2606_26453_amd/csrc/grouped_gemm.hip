@@ -174,8 +174,10 @@ template <int KIND, bool DUAL, bool ACT, int TM, int WAVES_M, int WAVES_N, int N
           bool PERSIST, bool OUT16, bool GATHER, bool F8>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kernel(GemmParams p) {
   // F8 && DUAL: one weight whose output channels interleave gate and up by 128 (tile columns
-  // 0..127 gate, 128..255 up), stored as two outputs (+ SwiGLU with ACT) like the fwd dual product
-  static_assert(!F8 || (KIND == KIND_DX && (DUAL || !ACT)), "FP8 operands: the dX-shaped product");
+  // 0..127 gate, 128..255 up), stored as two outputs (+ SwiGLU with ACT) like the fwd dual product.
+  // F8 && ACT && !DUAL: the dX-down product with the SwiGLU backward in its epilogue, applied to
+  // the scaled, bf16-rounded dA exactly as in the bf16 product.
+  static_assert(!F8 || KIND == KIND_DX, "FP8 operands: the dX-shaped product");
   constexpr int ES = F8 ? 1 : 2;              // bytes per operand element
   constexpr int BKE = F8 ? 2 * BK : BK;       // contraction elements per stage (64-byte rows)
   constexpr int NWAVE = WAVES_M * WAVES_N;
@@ -1357,6 +1359,40 @@ extern "C" moe_status moe_grouped_gemm_fwd_fp8(const uint8_t* A, const float* a_
   const moe_status st = attach_split(p, workspace, workspace_bytes, fn, stream);
   if (st != MOE_SUCCESS) return st;
   return launch<KIND_DX, false, false, false, false, true>(p, tiles, stream, "grouped_gemm_fwd_fp8");
+}
+
+extern "C" moe_status moe_grouped_gemm_dx_swiglu_bwd_fp8(const uint8_t* A, const float* a_scale, const uint8_t* Wt,
+                                                          const float* w_scale, const int32_t* offsets, int32_t G,
+                                                          int64_t R, int64_t K, int64_t N, const moe_bf16* h_gate,
+                                                          const moe_bf16* h_up, moe_bf16* dh_gate, moe_bf16* dh_up,
+                                                          void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  const char* fn = "moe_grouped_gemm_dx_swiglu_bwd_fp8";
+  if (G < 1 || G > 256) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: need 1 <= G <= 256", fn);
+  if (R < 0 || K <= 0 || N <= 0) return fail(MOE_ERROR_INVALID_VALUE, "%s: bad size", fn);
+  if (K % 64 || N % 64) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: K and N must be multiples of 64", fn);
+  if (R >= ((int64_t)1 << 31)) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: R >= 2^31", fn);
+  if (N * K >= ((int64_t)1 << 31)) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: one group's weight must be < 2 GiB", fn);
+  if (!offsets) return fail(MOE_ERROR_INVALID_VALUE, "%s: offsets is NULL", fn);
+  if (R == 0) return MOE_SUCCESS;
+  if (!A || !a_scale || !Wt || !w_scale || !h_gate || !h_up || !dh_gate || !dh_up)
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: NULL pointer", fn);
+  if (bad_ptr(A) || bad_ptr(Wt) || bad_ptr(w_scale) || bad_ptr(h_gate) || bad_ptr(h_up) || bad_ptr(dh_gate) ||
+      bad_ptr(dh_up) || (reinterpret_cast<uintptr_t>(a_scale) & 3))
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: pointers must be 16-byte aligned (a_scale 4-byte)", fn);
+  // the dX-shaped product (rows of A against rows of Wt[g]) with the SwiGLU-backward epilogue
+  GemmParams p{};
+  p.a = reinterpret_cast<const uint16_t*>(A);
+  p.b = reinterpret_cast<const uint16_t*>(Wt);
+  p.offsets = offsets; p.out = dh_gate; p.out2 = dh_up; p.hg = h_gate; p.hu = h_up;
+  p.a_scale = a_scale; p.w_scale = w_scale;
+  p.G = G; p.R = R; p.K = N; p.N = K;
+  constexpr int TM = Cfg<KIND_DX>::TM;
+  p.mt_bound = (int)((R + TM - 1) / TM + G);
+  p.n_tiles = (int)((N + TN - 1) / TN);
+  const int64_t tiles = (int64_t)p.mt_bound * p.n_tiles;
+  const moe_status st = attach_split(p, workspace, workspace_bytes, fn, stream);
+  if (st != MOE_SUCCESS) return st;
+  return launch<KIND_DX, false, true, false, false, true>(p, tiles, stream, "grouped_gemm_dx_swiglu_bwd_fp8");
 }
 
 extern "C" moe_status moe_grouped_gemm_dx_split(const moe_bf16* dC, const moe_bf16* B, const moe_bf16* dC2,

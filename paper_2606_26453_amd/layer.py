@@ -47,7 +47,8 @@ class MoELayer(_Traced):
     def __init__(self, cfg, inputs: dict, normalize_topk: bool = True, fuse_swiglu_bwd: bool = True,
                  router: bool = False, aux_alpha: float = 0.0, dw_transposed: bool = False,
                  concurrent: bool = False, split_tail: bool = True, gather_fused: bool = False,
-                 fp8_forward: bool = False, dw_persistent: bool = True, fp8_requantize: bool = True):
+                 fp8_forward: bool = False, dw_persistent: bool = True, fp8_requantize: bool = True,
+                 fp8_backward: bool = False):
         self.cfg = cfg
         # fp8_forward: the routed experts' forward products run on E4M3 operands (activations
         # quantized per row each step, weights per output channel once, here): gate and up in one
@@ -55,6 +56,13 @@ class MoELayer(_Traced):
         # the down product on the quantized SwiGLU output; everything else (shared FFN, backward)
         # stays bf16
         self.fp8 = fp8_forward
+        # fp8_backward: the routed experts' two data-gradient products run on E4M3 operands: dY_perm
+        # per row against the down weight per output channel (its stored [f, d] rows), with the
+        # SwiGLU backward in the epilogue; then [dH_gate | dH_up] per row against [W_gate | W_up]
+        # per output channel (rows of the stored [d, f] weights joined along f), one product over
+        # the 2f-long contraction.  The weight gradients stay bf16 (their contraction runs over the
+        # tokens, which a per-row or per-channel scale cannot factor out)
+        self.fp8_bwd = fp8_backward
         # gather_fused: the gate/up product reads its rows straight from x through token_of_row
         # (moe_grouped_gemm_fwd_gather); X_perm is then gathered only in the backward, for dW_gate
         # and dW_up (moe_gather_rows), so a forward alone never writes it
@@ -119,8 +127,18 @@ class MoELayer(_Traced):
                 "gate_up": (e((E, 2 * f, d), u8), e((E, 2 * f), f32)),
                 "down": (e((E, d, f), u8), e((E, d), f32)),
             }
-            self.fp8_requantize = fp8_requantize
             self._quantize_weights()
+        self.fp8_requantize = fp8_requantize
+        if fp8_backward:
+            if not fuse_swiglu_bwd:
+                raise ValueError("fp8_backward fuses the SwiGLU backward into the dX-down product")
+            u8 = torch.uint8
+            b.update({"dy_q": e((R, d), u8), "dy_s": e(R, f32), "dh_q": e((R, 2 * f), u8), "dh_s": e(R, f32)})
+            self.w8b = {
+                "down": (e((E, f, d), u8), e((E, f), f32)),
+                "gate_up": (e((E, d, 2 * f), u8), e((E, d), f32)),
+            }
+            self._quantize_weights_bwd()
         self.shared = cfg.f_shared > 0
         if self.shared:
             fs = cfg.f_shared
@@ -138,6 +156,14 @@ class MoELayer(_Traced):
         i, w8 = self.inp, self.w8
         moe.moe_quantize_fp8_weight(i["w_gate"], i["w_up"], *w8["gate_up"], stream=stream)
         moe.moe_quantize_fp8_weight(i["w_down"], None, *w8["down"], stream=stream)
+
+    def _quantize_weights_bwd(self, stream=None):
+        """E4M3 codes and per-row scales of the expert weights in their stored layouts, the
+        operands of the FP8 data-gradient products: W_down [E, f, d] per output channel of dA,
+        [W_gate | W_up] [E, d, 2f] per output channel of dX."""
+        i, w8 = self.inp, self.w8b
+        moe.moe_quantize_fp8_rows(i["w_down"], *w8["down"], stream=stream)
+        moe.moe_quantize_fp8_rows2(i["w_gate"], i["w_up"], *w8["gate_up"], stream=stream)
 
     # ------------------------------------------------------------------------------------------
     def _streams(self, stream):
@@ -244,7 +270,14 @@ class MoELayer(_Traced):
         else:
             run("dw_down", moe.moe_grouped_gemm_dw, b["act"], b["dy_perm"], b["offsets"], dB=b["dw_down"],
                 stream=side, counters=self.dw_cnt)
-        if self.fuse:
+        if self.fp8_bwd:
+            if self.fp8_requantize:
+                run("quantize_w_bwd", self._quantize_weights_bwd, stream=stream)
+            run("quantize_dy", moe.moe_quantize_fp8_rows, b["dy_perm"], b["dy_q"], b["dy_s"], stream=stream)
+            run("dx_down_swiglu_bwd", moe.moe_grouped_gemm_dx_swiglu_bwd_fp8, b["dy_q"], b["dy_s"],
+                *self.w8b["down"], b["offsets"], b["h_gate"], b["h_up"], b["dh_gate"], b["dh_up"], stream=stream,
+                workspace=self.split_ws)
+        elif self.fuse:
             run("dx_down_swiglu_bwd", moe.moe_grouped_gemm_dx_swiglu_bwd, b["dy_perm"], i["w_down"],
                 b["offsets"], b["h_gate"], b["h_up"], b["dh_gate"], b["dh_up"], stream=stream,
                 workspace=self.split_ws)
@@ -254,8 +287,14 @@ class MoELayer(_Traced):
             run("swiglu_bwd", moe.moe_swiglu_bwd, b["h_gate"], b["h_up"], b["d_act"], b["dh_gate"],
                 b["dh_up"], stream=stream)
         self._join(side, main)            # dW_gate/dW_up need dH
-        run("dx_gate_up", moe.moe_grouped_gemm_dx, b["dh_gate"], i["w_gate"], b["offsets"], b["dh_up"],
-            i["w_up"], dA=b["dx_perm"], stream=stream, workspace=self.split_ws)
+        if self.fp8_bwd:
+            run("quantize_dh", moe.moe_quantize_fp8_rows2, b["dh_gate"], b["dh_up"], b["dh_q"], b["dh_s"],
+                stream=stream)
+            run("dx_gate_up", moe.moe_grouped_gemm_fwd_fp8, b["dh_q"], b["dh_s"], *self.w8b["gate_up"], b["offsets"],
+                C=b["dx_perm"], stream=stream, workspace=self.split_ws)
+        else:
+            run("dx_gate_up", moe.moe_grouped_gemm_dx, b["dh_gate"], i["w_gate"], b["offsets"], b["dh_up"],
+                i["w_up"], dA=b["dx_perm"], stream=stream, workspace=self.split_ws)
         # one stream: the unpermute-sum reads dX_perm right after it was written, while it still sits
         # in the last-level cache (dW gate/up's 3.8 GB of fp32 results would evict it first)
         early = side is main
@@ -318,9 +357,13 @@ class MoELayer(_Traced):
             "combine": ("bytes", R * d * 2 + T * d * 2 + T * k * 8 + (T * d * 2 if self.shared else 0)),
             "combine_bwd": ("bytes", T * d * 2 + 2 * R * d * 2 + T * k * 12),
             "dx_down": ("flops", 2 * R * d * f), "dw_down": ("flops", 2 * R * f * d),
-            "dx_down_swiglu_bwd": ("flops", 2 * R * d * f),
+            "dx_down_swiglu_bwd": ("flops8" if self.fp8_bwd else "flops", 2 * R * d * f),
+            # FP8 backward: dY_perm and [dH_gate | dH_up] per row, the weights in their stored layouts
+            "quantize_dy": ("bytes", R * d * 3 + R * 4), "quantize_dh": ("bytes", 2 * R * f * 3 + R * 4),
+            "quantize_w_bwd": ("bytes", 3 * E * d * f * 3 + E * (d + f) * 4),
             "swiglu_bwd": ("bytes", 5 * R * f * 2),
-            "dx_gate_up": ("flops", 4 * R * d * f), "dw_gate_up": ("flops", 4 * R * d * f),
+            "dx_gate_up": ("flops8" if self.fp8_bwd else "flops", 4 * R * d * f),
+            "dw_gate_up": ("flops", 4 * R * d * f),
             "unpermute_dx": ("bytes", R * d * 2 + T * d * 2 + R * 4 + (T * d * 2 if self.shared else 0)),
             # router: fp32 vector-ALU work (multiply-adds x2) of the contractions with Wr, with the
             # HBM bytes each call must move (x bf16 read; logits / dlogits fp32; the backward also

@@ -45,6 +45,9 @@ _SIG = {
     "moe_route_permute_noalloc_max_scratch_bytes": (ctypes.c_size_t, []),
     "moe_route_permute_noalloc": (ctypes.c_int, [_P, _P, _I64, _I64, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P, _P]),
     "moe_quantize_fp8_rows": (ctypes.c_int, [_P, _I64, _I64, _P, _P, _P]),
+    "moe_quantize_fp8_rows2": (ctypes.c_int, [_P, _P, _I64, _I64, _P, _P, _P]),
+    "moe_grouped_gemm_dx_swiglu_bwd_fp8": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P,
+                                                          _P, _P, ctypes.c_size_t, _P]),
     "moe_quantize_fp8_weight": (ctypes.c_int, [_P, _P, _I64, _I64, _I64, _P, _P, _P]),
     "moe_grouped_gemm_fwd_fp8": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P,
                                                 ctypes.c_size_t, _P]),
@@ -279,6 +282,26 @@ def moe_quantize_fp8_rows(x, q=None, scale=None, stream=None):
     return q, scale
 
 
+def moe_quantize_fp8_rows2(x, x2, q=None, scale=None, stream=None):
+    """E4M3 codes [.., 2K] and fp32 scales of the rows [x | x2] (x and x2 of one shape [.., K]), one
+    scale per joined row."""
+    K = x.shape[-1]
+    M = x.numel() // K
+    for t, n in ((x, "x"), (x2, "x2")):
+        if t.dtype != torch.bfloat16 or not t.is_contiguous():
+            raise ValueError(f"{n} must be a contiguous bf16 tensor")
+    if tuple(x2.shape) != tuple(x.shape):
+        raise ValueError("x and x2 must have one shape")
+    qshape = tuple(x.shape[:-1]) + (2 * K,)
+    q = torch.empty(qshape, dtype=torch.uint8, device=x.device) if q is None else q
+    scale = torch.empty(x.shape[:-1], dtype=torch.float32, device=x.device) if scale is None else scale
+    _need(q, torch.uint8, qshape, "q")
+    _need(scale, torch.float32, tuple(x.shape[:-1]), "scale")
+    _check("moe_quantize_fp8_rows2",
+           lib().moe_quantize_fp8_rows2(_ptr(x), _ptr(x2), M, K, _ptr(q), _ptr(scale), _stream(stream)))
+    return q, scale
+
+
 def moe_quantize_fp8_weight(w, w2=None, q=None, scale=None, stream=None):
     """E4M3 codes and per-channel scales of a weight [G, K, N] (contraction K, channels N), written
     as [G, N, K] (or, with w2, [G, 2N, K] with the two weights' channels interleaved by 128)."""
@@ -315,6 +338,33 @@ def moe_grouped_gemm_fwd_fp8(A, a_scale, Wt, w_scale, offsets, C=None, stream=No
                                         _stream(stream))
     _check("moe_grouped_gemm_fwd_fp8", st)
     return C
+
+
+def moe_grouped_gemm_dx_swiglu_bwd_fp8(A, a_scale, Wt, w_scale, offsets, h_gate, h_up, dh_gate=None, dh_up=None,
+                                       stream=None, workspace=None):
+    """dA = (A . Wt[g]^T) * a_scale * w_scale (bf16) and its SwiGLU backward: (dh_gate, dh_up) from
+    h_gate, h_up [R, N]; A [R, K] and Wt [G, N, K] E4M3 codes."""
+    R, K = A.shape
+    G, N, K2 = Wt.shape
+    if K2 != K:
+        raise ValueError("A and Wt disagree on K")
+    _need(A, torch.uint8, (R, K), "A")
+    _need(a_scale, torch.float32, (R,), "a_scale")
+    _need(Wt, torch.uint8, (G, N, K), "Wt")
+    _need(w_scale, torch.float32, (G, N), "w_scale")
+    _need(offsets, torch.int32, (G + 1,), "offsets")
+    _need(h_gate, torch.bfloat16, (R, N), "h_gate")
+    _need(h_up, torch.bfloat16, (R, N), "h_up")
+    dh_gate = torch.empty((R, N), dtype=torch.bfloat16, device=A.device) if dh_gate is None else dh_gate
+    dh_up = torch.empty((R, N), dtype=torch.bfloat16, device=A.device) if dh_up is None else dh_up
+    _need(dh_gate, torch.bfloat16, (R, N), "dh_gate")
+    _need(dh_up, torch.bfloat16, (R, N), "dh_up")
+    st = lib().moe_grouped_gemm_dx_swiglu_bwd_fp8(_ptr(A), _ptr(a_scale), _ptr(Wt), _ptr(w_scale), _ptr(offsets), G,
+                                                  R, K, N, _ptr(h_gate), _ptr(h_up), _ptr(dh_gate), _ptr(dh_up),
+                                                  _ptr(workspace), 0 if workspace is None else workspace.numel(),
+                                                  _stream(stream))
+    _check("moe_grouped_gemm_dx_swiglu_bwd_fp8", st)
+    return dh_gate, dh_up
 
 
 def interleave_gate_up(w_gate_t, w_up_t):

@@ -310,3 +310,151 @@ def test_grouped_gemm_fp8_256_groups_exact():
     np.testing.assert_array_equal(f64(hg), ref)
     np.testing.assert_array_equal(f64(hu), O.grouped_gemm_fp8(_u8(a), sa.numpy(), _u8(w2), sw2.numpy(), off.numpy()))
     check_float("act", f64(act), O.swiglu(f64(hg), f64(hu)), 1e-2)
+
+
+# ------------------------------------------------------------------------------------------------
+# The backward's data-gradient products on E4M3 operands
+# ------------------------------------------------------------------------------------------------
+def _dequant(codes, scale):
+    """bf16 tensor of decode(codes) * scale (exact for small-integer codes and power-of-two scales)."""
+    return torch.from_numpy(O.e4m3_decode(_u8(codes)) * scale.double().numpy()[..., None]).to(torch.bfloat16)
+
+
+@pytest.mark.parametrize("M,K", [(1, 16), (7, 64), (300, 4112), (33, 14336)])
+def test_quantize_fp8_rows2(M, K):
+    """Joint per-row quantization of [x | x2]: codes and scales bit for bit against the oracle's row
+    quantizer on the concatenated rows and against moe_quantize_fp8_rows on the concatenation;
+    rows whose maximum sits in either half, an all-zero row and rows with one all-zero half."""
+    _say("quantize fp8 rows2", M, K)
+    g = torch.Generator().manual_seed(3 * M + K)
+    mk = lambda: (torch.randn((M, K), generator=g) * torch.exp(torch.randn((M, 1), generator=g) * 3)).to(torch.bfloat16)
+    x, x2 = mk(), mk()
+    if M > 3:
+        x[1] = 0
+        x2[1] = 0
+        x[2] = 0
+        x2[3] = 0
+    q = poison_(torch.empty((M, 2 * K), dtype=torch.uint8, device=DEV))
+    s = poison_(torch.empty(M, dtype=torch.float32, device=DEV))
+    moe.moe_quantize_fp8_rows2(x.to(DEV), x2.to(DEV), q, s)
+    torch.cuda.synchronize()
+    cat = torch.cat([x, x2], dim=1)
+    rq, rs = O.quantize_rows_fp8(f64(cat))
+    np.testing.assert_array_equal(_u8(q), rq)
+    np.testing.assert_array_equal(s.cpu().numpy(), rs)
+    q1, s1 = moe.moe_quantize_fp8_rows(cat.contiguous().to(DEV))
+    torch.cuda.synchronize()
+    assert torch.equal(q1, q) and torch.equal(s1, s)
+
+
+@pytest.mark.parametrize("K,N", [(64, 128), (256, 320), (512, 576)])
+def test_dx_swiglu_bwd_fp8_exact(K, N):
+    """The FP8 dX-down product with the SwiGLU backward in its epilogue, on small-integer codes with
+    power-of-two scales (every sum exact in fp32): bitwise equal to the bf16 product with the same
+    epilogue (moe_grouped_gemm_dx_swiglu_bwd) on the decoded operands, with and without the split
+    tail, over ragged and empty groups; and against the oracle's SwiGLU backward of the oracle's
+    FP8 product."""
+    _say("dx swiglu bwd fp8 exact", K, N)
+    g = torch.Generator().manual_seed(K + 7 * N)
+    G, R = len(GROUPS), sum(GROUPS)
+    off = torch.tensor(np.concatenate([[0], np.cumsum(GROUPS)]), dtype=torch.int32)
+    a, w = _int_codes(g, (R, K)), _int_codes(g, (G, N, K))
+    sa, sw = _pow2(g, (R,)), _pow2(g, (G, N))
+    hg = torch.randn((R, N), generator=g).to(torch.bfloat16)
+    hu = torch.randn((R, N), generator=g).to(torch.bfloat16)
+    D = lambda t: t.to(DEV)
+    rg, ru = moe.moe_grouped_gemm_dx_swiglu_bwd(D(_dequant(a, sa)), D(_dequant(w, sw)), D(off), D(hg), D(hu))
+    ws = moe.split_workspace(DEV)
+    da = O.grouped_gemm_fp8(_u8(a), sa.numpy(), _u8(w), sw.numpy(), off.numpy())
+    og, ou = O.swiglu_bwd(f64(hg), f64(hu), da)
+    for wsp in (None, ws):
+        dg = poison_(torch.empty((R, N), dtype=torch.bfloat16, device=DEV))
+        du = poison_(torch.empty((R, N), dtype=torch.bfloat16, device=DEV))
+        moe.moe_grouped_gemm_dx_swiglu_bwd_fp8(D(a), D(sa), D(w), D(sw), D(off), D(hg), D(hu), dg, du, workspace=wsp)
+        torch.cuda.synchronize()
+        assert torch.equal(dg.view(torch.int16), rg.view(torch.int16))
+        assert torch.equal(du.view(torch.int16), ru.view(torch.int16))
+        check_float("dh_gate", f64(dg), og, 2e-3)
+        check_float("dh_up", f64(du), ou, 2e-3)
+
+
+@pytest.mark.parametrize("F,N", [(64, 64), (192, 320), (704, 256)])
+def test_dx_gate_up_fp8_joint_exact(F, N):
+    """The gate/up data gradient as one FP8 product over the joined contraction [dH_g | dH_u] x
+    [W_g | W_u] (moe_grouped_gemm_fwd_fp8 with K = 2F): on small-integer codes with one power-of-two
+    scale per joined row and per output channel, bitwise equal to the bf16 dual product
+    moe_grouped_gemm_dx on the decoded halves (with and without the split tail) and exact against
+    the oracle's FP8 product."""
+    _say("dx gate/up fp8 joint", F, N)
+    g = torch.Generator().manual_seed(F + 3 * N)
+    G, R = len(GROUPS), sum(GROUPS)
+    off = torch.tensor(np.concatenate([[0], np.cumsum(GROUPS)]), dtype=torch.int32)
+    a, w = _int_codes(g, (R, 2 * F)), _int_codes(g, (G, N, 2 * F))
+    sa, sw = _pow2(g, (R,)), _pow2(g, (G, N))
+    ad, wd = _dequant(a, sa), _dequant(w, sw)
+    D = lambda t: t.contiguous().to(DEV)
+    ref = moe.moe_grouped_gemm_dx(D(ad[:, :F]), D(wd[:, :, :F]), D(off), D(ad[:, F:]), D(wd[:, :, F:]))
+    ws = moe.split_workspace(DEV)
+    oref = O.grouped_gemm_fp8(_u8(a), sa.numpy(), _u8(w), sw.numpy(), off.numpy())
+    for wsp in (None, ws):
+        C = poison_(torch.empty((R, N), dtype=torch.bfloat16, device=DEV))
+        moe.moe_grouped_gemm_fwd_fp8(D(a), D(sa), D(w), D(sw), D(off), C=C, workspace=wsp)
+        torch.cuda.synchronize()
+        assert torch.equal(C.view(torch.int16), ref.view(torch.int16))
+        np.testing.assert_array_equal(f64(C), oref)
+
+
+@pytest.mark.parametrize("cfg_id", [0, 2])
+def test_layer_fp8_backward(cfg_id):
+    """The layer with its expert data-gradient products in FP8 (forward in bf16), stage by stage on
+    the GPU's own intermediate tensors: the weight codes (down per stored row, [W_gate | W_up] per
+    joined row) and the dY_perm and [dH_gate | dH_up] codes bit for bit, dH against the oracle's
+    SwiGLU backward of its FP8 product on the same codes, dX_perm against the oracle's FP8 product,
+    dX against the unpermute-sum and the bf16 weight gradients against the oracle on the GPU's dY_perm
+    and dH.  Two steps, so the second re-quantizes the weights.  Config 2 at 1024 tokens."""
+    import dataclasses
+    from paper_2606_26453_amd import layer as L, workloads as W
+    cfg = W.CONFIGS[cfg_id]
+    if cfg_id:
+        cfg = dataclasses.replace(cfg, T=1024)
+    _say("layer fp8 backward", cfg)
+    inp = W.make_inputs(cfg, 0, "cpu")
+    lay = L.MoELayer(cfg, {k_: v.to(DEV) for k_, v in inp.items()}, fp8_backward=True)
+    lay.step()
+    lay.step()
+    torch.cuda.synchronize()
+    b = lay.buf
+    wg, wu, wd = (f64(inp[n]) for n in ("w_gate", "w_up", "w_down"))
+    dq, ds = O.quantize_rows_fp8(wd)
+    np.testing.assert_array_equal(_u8(lay.w8b["down"][0]), dq)
+    np.testing.assert_array_equal(lay.w8b["down"][1].cpu().numpy(), ds)
+    gq, gs = O.quantize_rows_fp8(np.concatenate([wg, wu], axis=2))
+    np.testing.assert_array_equal(_u8(lay.w8b["gate_up"][0]), gq)
+    np.testing.assert_array_equal(lay.w8b["gate_up"][1].cpu().numpy(), gs)
+    off = b["offsets"].cpu().numpy()
+    yq, ys = O.quantize_rows_fp8(f64(b["dy_perm"]))
+    np.testing.assert_array_equal(_u8(b["dy_q"]), yq)
+    np.testing.assert_array_equal(b["dy_s"].cpu().numpy(), ys)
+    og, ou = O.swiglu_bwd(f64(b["h_gate"]), f64(b["h_up"]), O.grouped_gemm_fp8(yq, ys, dq, ds, off))
+    check_float("dh_gate", f64(b["dh_gate"]), og, 4e-3)
+    check_float("dh_up", f64(b["dh_up"]), ou, 4e-3)
+    hq, hs = O.quantize_rows_fp8(np.concatenate([f64(b["dh_gate"]), f64(b["dh_up"])], axis=1))
+    np.testing.assert_array_equal(_u8(b["dh_q"]), hq)
+    np.testing.assert_array_equal(b["dh_s"].cpu().numpy(), hs)
+    check_float("dx_perm", f64(b["dx_perm"]), O.grouped_gemm_fp8(hq, hs, gq, gs, off), 2e-3)
+    ros = b["row_of_slot"].cpu().numpy()
+    add = None
+    if cfg.f_shared:
+        add = f64(b["dx_sh"])
+    check_float("dx", f64(b["dx"]), O.combine(f64(b["dx_perm"]), None, ros, cfg.k, add=add), 2e-3)
+    check_float("dw_down", f64(b["dw_down"]), O.grouped_gemm_dw(f64(b["act"]), f64(b["dy_perm"]), off), 1e-4)
+    check_float("dw_gate", f64(b["dw_gate"]), O.grouped_gemm_dw(f64(b["x_perm"]), f64(b["dh_gate"]), off), 1e-4)
+    check_float("dw_up", f64(b["dw_up"]), O.grouped_gemm_dw(f64(b["x_perm"]), f64(b["dh_up"]), off), 1e-4)
+    # how far the FP8 data gradient moves dX from the all-bf16 layer's
+    x = f64(inp["x"])
+    shared = None
+    if cfg.f_shared:
+        shared = tuple(f64(inp[n]) for n in ("w_gate_sh", "w_up_sh", "w_down_sh"))
+    fwd = O.layer_forward(x, inp["logits"].numpy(), wg, wu, wd, cfg.k, shared=shared)
+    bwd = O.layer_backward(fwd, x, f64(inp["dy"]), wg, wu, wd, shared=shared)
+    _say(f"fp8 data gradient dX vs the all-bf16 oracle: relative Frobenius {O.rel_fro(f64(b['dx']), bwd['dx']):.3e}")
