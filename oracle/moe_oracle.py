@@ -18,8 +18,9 @@ the first FFN projection is dW1_e = X_e^T G_e, a contraction over that expert's 
 be zero).  `grouped_gemm_dw` is that definition.  The paper states no routing rule, row order,
 activation, combine, router or other backward formula; the readings used for those are the
 standard MoE layer (and, for the router's load-balancing loss, the Switch-style auxiliary loss) and
-are named at each function.  The FP8 functions at the end serve a variant the paper does not
-describe (OCP E4M3 operands with fp32 scales); their reading is stated there.
+are named at each function.  The FP8 and MX functions at the end serve variants the paper does not
+describe (OCP E4M3 operands with fp32 scales, or with a power-of-two scale per 32 elements); their
+reading is stated there.
 
 Parity: every function here is pinned by the CPU test suite against closed forms, library
 routines, brute force, hand-worked values or automatic differentiation, and the suite plants
@@ -518,6 +519,66 @@ def grouped_gemm_fp8(a_codes, a_scale, wt_codes, w_scale, offsets, rnd=bf16_roun
         lo, hi = int(offsets[g]), int(offsets[g + 1])
         if hi > lo:
             C[lo:hi] = (A[lo:hi] @ W[g].T) * sa[lo:hi, None] * sw[g][None, :]
+    return _r(rnd, C)
+
+
+# --------------------------------------------------------------------------------------------
+# MX (microscaling) variant of the FP8 products, also beyond the paper.  The reading: the OCP
+# microscaling formats' block structure, E4M3 elements sharing one power-of-two scale (an E8M0
+# byte, value 2**(byte - 127)) per 32 consecutive contraction elements of a row; the shared
+# exponent is the smallest one that keeps every element of the block within E4M3's range (no
+# element saturates), and an all-zero block gets the smallest scale, byte 0.
+# --------------------------------------------------------------------------------------------
+MX_BLOCK = 32
+
+
+def mx_block_exponent(amax):
+    """The smallest integer e with amax <= 448 * 2**e, raised to -127 where it is below (the
+    smallest E8M0 value; every all-zero block gets it).  amax >= 0, finite."""
+    amax = np.asarray(amax, dtype=np.float64)
+    pos = amax > 0
+    e = np.where(pos, np.ceil(np.log2(np.where(pos, amax, 1.0) / E4M3_MAX)), -127.0).astype(np.int64)
+    # the logarithm may be off by one ulp next to a power of two: settle e on the definition
+    e = np.where(pos & (amax > np.ldexp(E4M3_MAX, e)), e + 1, e)
+    e = np.where(pos & (amax <= np.ldexp(E4M3_MAX, e - 1)), e - 1, e)
+    return np.maximum(e, -127)
+
+
+def quantize_rows_mx(x):
+    """MX quantization along the last axis (its length a multiple of 32): for each block of 32
+    consecutive elements, e = mx_block_exponent(max |block|), scale byte e + 127 and codes
+    e4m3_encode(x * 2**-e) (an exact scaling, so the codes round x itself to the E4M3 grid times
+    2**e).  Returns codes (x's shape, uint8) and scale bytes (x's shape with the last axis / 32,
+    uint8); x ~= e4m3_decode(codes) * 2**(bytes - 127) per block."""
+    x = np.asarray(x, dtype=np.float64)
+    C = x.shape[-1]
+    assert C % MX_BLOCK == 0
+    blocks = x.reshape(x.shape[:-1] + (C // MX_BLOCK, MX_BLOCK))
+    e = mx_block_exponent(np.max(np.abs(blocks), axis=-1))
+    codes = e4m3_encode(np.ldexp(blocks, -e[..., None]))
+    return codes.reshape(x.shape), (e + 127).astype(np.uint8)
+
+
+def mx_decode(codes, scale_bytes):
+    """MX operand -> float64: e4m3_decode(codes) times 2**(byte - 127) of each element's block."""
+    v = e4m3_decode(codes)
+    s = np.asarray(scale_bytes, dtype=np.int64) - 127
+    return np.ldexp(v, np.repeat(s, MX_BLOCK, axis=-1))
+
+
+def grouped_gemm_mx(a_codes, a_scale, wt_codes, w_scale, offsets, rnd=bf16_round):
+    """The grouped product on MX operands: for rows r of group g,
+    C[r, n] = sum_k mx(A)[r, k] * mx(Wt[g])[n, k], accumulated exactly and rounded once to bf16.
+    A [R, K] codes with scale bytes [R, K/32]; Wt [G, N, K] codes (the weight in the layout
+    [output channel, contraction]) with scale bytes [G, N, K/32]."""
+    A = mx_decode(a_codes, a_scale)
+    W = mx_decode(wt_codes, w_scale)
+    G, N, _ = W.shape
+    C = np.zeros((A.shape[0], N))
+    for g in range(G):
+        lo, hi = int(offsets[g]), int(offsets[g + 1])
+        if hi > lo:
+            C[lo:hi] = A[lo:hi] @ W[g].T
     return _r(rnd, C)
 
 

@@ -574,6 +574,122 @@ def test_grouped_gemm_fp8_vs_library():
 
 
 # ---------------------------------------------------------------------------------------------
+# MX variant: E4M3 elements with a power-of-two scale per 32 elements
+# ---------------------------------------------------------------------------------------------
+def test_mx_block_exponent_hand_values():
+    """The smallest e with amax <= 448 * 2**e, worked by hand; -127 at the bottom."""
+    cases = {
+        448.0: 0,            # exactly the largest E4M3 magnitude
+        450.0: 1,            # the next bf16 above 448 no longer fits at e = 0
+        224.0: -1,           # 448 / 2 fits at e = -1 (and 224 > 448 * 2**-2 = 112)
+        225.0: 0,
+        1.0: -8,             # 448 * 2**-8 = 1.75 >= 1 > 0.875 = 448 * 2**-9
+        1.75: -8,            # equal to 448 * 2**-8
+        1.7578125: -7,       # the next bf16 above 1.75
+        256.0: 0,            # a power of two: 256 <= 448 (a floor(log2) - 8 rule gives 0 too)
+        300.0: 0,
+        500.0: 1,            # floor(log2(500)) - 8 = 0 would saturate: 500 > 448
+        0.0: -127,           # an all-zero block
+        2.0 ** -140: -127,   # e would be -148: raised to the smallest scale
+        448.0 * 2.0 ** -127: -127,
+        448.0 * 2.0 ** -126: -126,
+    }
+    for amax, e in cases.items():
+        assert int(O.mx_block_exponent(np.array([amax]))[0]) == e, amax
+    for k in (-100, -20, -1, 3, 60, 110):
+        assert int(O.mx_block_exponent(np.array([448.0 * 2.0 ** k]))[0]) == k
+        assert int(O.mx_block_exponent(np.array([450.0 * 2.0 ** k]))[0]) == k + 1
+
+
+def test_quantize_rows_mx_worked_example():
+    """One row of three blocks, every code and scale byte worked by hand.
+    Block 0: amax 100 -> e = -2 (100 <= 448/4 = 112, 100 > 56), byte 125; scaled values x * 4:
+      100 -> 400, halfway between 384 and 416: ties to the even mantissa, 384 = 1.5 * 2**8 ->
+      exponent field 15, mantissa 4: 0x7C;  1 -> 4 = 2**2: field 9, mantissa 0: 0x48;
+      -3.5 -> -14 = -1.75 * 2**3: field 10, mantissa 6, sign: 0xD6;  2**-9 -> 2**-7, a subnormal,
+      4 * 2**-9: 0x04;  the rest 0.
+    Block 1: all zero -> byte 0 and zero codes.
+    Block 2: amax 0.4375 = 448 * 2**-10 -> byte 117; 0.4375 -> 448: 0x7E; -0.25 -> -256 =
+      -2**8: field 15, mantissa 0, sign: 0xF8."""
+    x = np.zeros((1, 96))
+    x[0, 0], x[0, 1], x[0, 2], x[0, 3] = 100.0, 1.0, -3.5, 2.0 ** -9
+    x[0, 64], x[0, 70] = 0.4375, -0.25
+    codes, sb = O.quantize_rows_mx(x)
+    assert codes.dtype == np.uint8 and sb.dtype == np.uint8 and sb.shape == (1, 3)
+    assert sb.tolist() == [[125, 0, 117]]
+    want = np.zeros(96, dtype=np.uint8)
+    want[0], want[1], want[2], want[3], want[64], want[70] = 0x7C, 0x48, 0xD6, 0x04, 0x7E, 0xF8
+    np.testing.assert_array_equal(codes[0], want)
+    # decoded: 384 * 2**-2 = 96 for the tie, the others exact
+    dec = O.mx_decode(codes, sb)[0]
+    assert dec[0] == 96.0 and dec[1] == 1.0 and dec[2] == -3.5 and dec[3] == 2.0 ** -9
+    assert dec[64] == 0.4375 and dec[70] == -0.25 and not np.any(dec[32:64])
+
+
+def test_quantize_rows_mx_properties():
+    """On rows whose blocks span many magnitudes (and all-zero and tiny blocks): the scaled block
+    never exceeds 448 and a smaller exponent would (unless at -127); each code is the nearest E4M3
+    value to x * 2**-e by exhaustive search; blocks are quantized independently."""
+    rng = np.random.default_rng(11)
+    R, C = 6, 256
+    mag = 2.0 ** rng.integers(-30, 30, (R, C // 32))
+    x = O.bf16_round(rng.normal(0, 1, (R, C)) * np.repeat(mag, 32, axis=1))
+    x[1, 32:64] = 0.0
+    x[2, 0:32] = O.bf16_round(rng.normal(0, 1, 32) * 2.0 ** -131)        # bf16 subnormals
+    codes, sb = O.quantize_rows_mx(x)
+    e = sb.astype(np.int64) - 127
+    blocks = x.reshape(R, C // 32, 32)
+    amax = np.abs(blocks).max(axis=2)
+    assert sb[1, 1] == 0 and not np.any(codes[1, 32:64])
+    assert np.all(amax <= np.ldexp(448.0, e))
+    assert np.all((e == -127) | (amax > np.ldexp(448.0, e - 1)))
+    scaled = np.ldexp(blocks, -e[..., None]).reshape(-1)
+    np.testing.assert_array_equal(codes.reshape(-1), _e4m3_nearest_brute(scaled))
+    # block independence: changing block 3 of row 0 changes nothing else
+    x2 = x.copy()
+    x2[0, 96:128] *= 1024.0
+    c2, s2 = O.quantize_rows_mx(x2)
+    assert s2[0, 3] == sb[0, 3] + 10
+    keep = np.ones(C, dtype=bool)
+    keep[96:128] = False
+    np.testing.assert_array_equal(c2[0, keep], codes[0, keep])
+    np.testing.assert_array_equal(np.delete(s2, 3, axis=1), np.delete(sb, 3, axis=1))
+
+
+def test_grouped_gemm_mx_vs_library():
+    """Exact on small-integer codes with random block scales: torch matmuls of one 32-column block
+    at a time, each scaled by its two scale columns, summed over the blocks; one scale byte one
+    higher doubles exactly its block's share."""
+    rng = np.random.default_rng(12)
+    counts = [5, 0, 7, 1, 3]
+    G, R, K, N = len(counts), sum(counts), 96, 12
+    off = np.concatenate([[0], np.cumsum(counts)])
+    ints = np.arange(-4, 5, dtype=np.float64)
+    a = O.e4m3_encode(rng.choice(ints, (R, K)))
+    w = O.e4m3_encode(rng.choice(ints, (G, N, K)))
+    sa = rng.integers(120, 134, (R, K // 32)).astype(np.uint8)
+    sw = rng.integers(120, 134, (G, N, K // 32)).astype(np.uint8)
+    got = O.grouped_gemm_mx(a, sa, w, sw, off, rnd=None)
+    A = torch.from_numpy(O.e4m3_decode(a))
+    W = torch.from_numpy(O.e4m3_decode(w))
+    SA = torch.from_numpy(2.0 ** (sa.astype(np.float64) - 127))
+    SW = torch.from_numpy(2.0 ** (sw.astype(np.float64) - 127))
+    for g in range(G):
+        lo, hi = off[g], off[g + 1]
+        ref = torch.zeros(hi - lo, N, dtype=torch.float64)
+        for b in range(K // 32):
+            cols = slice(32 * b, 32 * b + 32)
+            ref += (A[lo:hi, cols] @ W[g][:, cols].T) * SA[lo:hi, b][:, None] * SW[g][:, b][None, :]
+        np.testing.assert_array_equal(got[lo:hi], ref.numpy())
+    sa2 = sa.copy()
+    sa2[2, 1] += 1
+    share = (A[2, 32:64] @ W[0][:, 32:64].T).numpy() * 2.0 ** (sa[2, 1] - 127.0) * \
+        (2.0 ** (sw[0][:, 1].astype(np.float64) - 127))
+    np.testing.assert_array_equal(O.grouped_gemm_mx(a, sa2, w, sw, off, rnd=None)[2], got[2] + share)
+    np.testing.assert_array_equal(O.grouped_gemm_mx(a, sa, w, sw, off), O.bf16_round(got))
+
+
+# ---------------------------------------------------------------------------------------------
 # the comparison metric every floating-point parity check goes through
 # ---------------------------------------------------------------------------------------------
 def test_rel_fro_hand_values():

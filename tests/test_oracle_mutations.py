@@ -33,6 +33,10 @@ PINS = [
     P.test_e4m3_encode_brute_force_and_torch,
     P.test_quantize_rows_fp8_properties,
     P.test_grouped_gemm_fp8_vs_library,
+    P.test_mx_block_exponent_hand_values,
+    P.test_quantize_rows_mx_worked_example,
+    P.test_quantize_rows_mx_properties,
+    P.test_grouped_gemm_mx_vs_library,
     P.test_rel_fro_hand_values,
 ]
 
@@ -168,6 +172,39 @@ def _quant_inverted_scale(x):                                             # scal
     return codes, np.where(scale != 1, (np.float32(448.0) ** 2 / 448.0) / (scale * 448.0), scale).astype(np.float32)
 
 
+def _mx_exponent_floor_rule(amax):                                      # e = floor(log2 amax) - 8
+    amax = np.asarray(amax, dtype=np.float64)
+    pos = amax > 0
+    _, fe = np.frexp(np.where(pos, amax, 1.0))
+    return np.where(pos, np.maximum(fe - 1 - 8, -127), -127).astype(np.int64)
+
+
+def _mx_exponent_no_clamp(amax):                                          # no floor at -127
+    amax = np.asarray(amax, dtype=np.float64)
+    pos = amax > 0
+    e = np.ceil(np.log2(np.where(pos, amax, 1.0) / 448.0)).astype(np.int64)
+    return np.where(pos, e, -127)
+
+
+def _quant_mx_blocks_of_16(x):                                             # 16-element blocks
+    x = np.asarray(x, dtype=np.float64)
+    blocks = x.reshape(x.shape[:-1] + (x.shape[-1] // 16, 16))
+    e = O.mx_block_exponent(np.max(np.abs(blocks), axis=-1))
+    codes = O.e4m3_encode(np.ldexp(blocks, -e[..., None]))
+    return codes.reshape(x.shape), (e[..., ::2] + 127).astype(np.uint8)
+
+
+def _mx_decode_tiled_scales(codes, scale_bytes):                           # scales tiled, not repeated
+    v = O.e4m3_decode(codes)
+    s = np.asarray(scale_bytes, dtype=np.int64) - 127
+    return np.ldexp(v, np.tile(s, (1,) * (s.ndim - 1) + (32,)))
+
+
+def _mx_gemm_scale_negated(a_codes, a_scale, wt_codes, w_scale, offsets, rnd=O.bf16_round):   # 2**(127 - byte)
+    return O.__dict__["_orig_mxg"](a_codes, (254 - np.asarray(a_scale, dtype=np.int64)).astype(np.uint8),
+                                   wt_codes, w_scale, offsets, rnd)
+
+
 def _rel_fro_squared(got, ref):                                           # squared ratio
     r = O.__dict__["_orig_rf"](got, ref)
     return r * r
@@ -203,6 +240,11 @@ MUTANTS = {
     "e4m3 exponent bias 8": ("e4m3_decode", _e4m3_decode_bias8),
     "fp8 gemm ignores the weight scale": ("grouped_gemm_fp8", _fp8_gemm_no_weight_scale),
     "fp8 quantization stores the inverse scale": ("quantize_rows_fp8", _quant_inverted_scale),
+    "mx exponent by floor(log2 amax) - 8": ("mx_block_exponent", _mx_exponent_floor_rule),
+    "mx exponent not raised to -127": ("mx_block_exponent", _mx_exponent_no_clamp),
+    "mx blocks of 16": ("quantize_rows_mx", _quant_mx_blocks_of_16),
+    "mx decode tiles the scales": ("mx_decode", _mx_decode_tiled_scales),
+    "mx gemm negated activation scale": ("grouped_gemm_mx", _mx_gemm_scale_negated),
     "router logits drop the bias": ("router_logits", _logits_no_bias),
     "route_topk_bwd drops the weighted mean": ("route_topk_bwd", _topk_bwd_no_mean),
     "route_topk_bwd uses the full softmax": ("route_topk_bwd", _topk_bwd_full_softmax),
@@ -235,6 +277,7 @@ def test_planted_mistake_is_caught(name, monkeypatch):
     monkeypatch.setitem(O.__dict__, "_orig_f8", O.grouped_gemm_fp8)
     monkeypatch.setitem(O.__dict__, "_orig_q8", O.quantize_rows_fp8)
     monkeypatch.setitem(O.__dict__, "_orig_rf", O.rel_fro)
+    monkeypatch.setitem(O.__dict__, "_orig_mxg", O.grouped_gemm_mx)
     monkeypatch.setattr(O, attr, fn)
     if attr == "bf16_round":
         # default arguments captured the original function; patch the module-level users too
