@@ -70,8 +70,10 @@ def source_hash(files):
     return code_hash("".join(open(os.path.join(ROOT, f)).read() for f in files))
 
 
-def measured_traffic(call, config):
-    if config != TRAFFIC_CONFIG or call not in TRAFFIC_KIB:
+def measured_traffic(call, config, variant=False):
+    """Counter bytes of `call` from the table above, for the default kernels only (a variant flag
+    swaps in other kernels under the same call names)."""
+    if variant or config != TRAFFIC_CONFIG or call not in TRAFFIC_KIB:
         return None
     group, f, w = TRAFFIC_KIB[call]
     files, sha = TRAFFIC_SOURCES[group]
@@ -99,6 +101,9 @@ def _args():
                     help="the routed experts' forward products on E4M3 operands (a variant; the metric is bf16)")
     ap.add_argument("--fp8-backward", action="store_true",
                     help="the routed experts' data-gradient products on E4M3 operands (a variant; the metric is bf16)")
+    ap.add_argument("--mx", action="store_true",
+                    help="with --fp8-forward/--fp8-backward: MX block scales (a power of two per 32 contraction "
+                         "elements) instead of fp32 per-row/per-channel scales")
     ap.add_argument("--fp8-fixed-weights", action="store_true",
                     help="with --fp8-forward/--fp8-backward: quantize the weights once (held fixed), not every step")
     ap.add_argument("--forward-only", action="store_true", help="time the forward alone (a variant)")
@@ -207,7 +212,8 @@ class ClockSampler:
 def fp8_dtype(a):
     """The arithmetic types of the run: bf16, or which expert products run on E4M3 operands."""
     parts = [n for n, on in (("forward", a.fp8_forward), ("data-gradient", a.fp8_backward)) if on]
-    return f"fp8-e4m3 ({' and '.join(parts)} expert products) + bf16" if parts else "bf16"
+    kind = "mxfp8-e4m3" if getattr(a, "mx", False) else "fp8-e4m3"
+    return f"{kind} ({' and '.join(parts)} expert products) + bf16" if parts else "bf16"
 
 
 def valu_record(flops, nbytes, avg_ms):
@@ -389,7 +395,7 @@ def main():
         lay = L.MoELayer(cfg, inp, router=a.router, aux_alpha=a.aux_alpha if a.router else 0.0,
                          dw_transposed=a.dw_transposed, concurrent=a.concurrent, split_tail=not a.no_split_tail,
                          gather_fused=a.gather_fused, fp8_forward=a.fp8_forward,
-                         fp8_backward=a.fp8_backward, fp8_requantize=not a.fp8_fixed_weights,
+                         fp8_backward=a.fp8_backward, fp8_requantize=not a.fp8_fixed_weights, mx=a.mx,
                          dw_persistent=not a.dw_one_per_tile)
     torch.cuda.synchronize()
     t_gen = time.perf_counter() - t_gen
@@ -433,6 +439,8 @@ def main():
     work = lay.work()
     calls = {}
     gemm_ms = gemm_flops = 0.0
+    variant = (a.fp8_forward or a.fp8_backward or a.gather_fused or a.dw_transposed or a.no_split_tail
+               or a.dw_one_per_tile or a.concurrent)
     for name, ts in per.items():
         avg = sum(ts) / len(ts)
         kind, amount = work[name]
@@ -450,7 +458,7 @@ def main():
         else:
             rec["gbs"] = round(amount / avg / 1e6, 1)
             rec["frac_peak"] = round(amount / avg / 1e6 / PEAK_HBM_GBS, 4)
-        hbm = measured_traffic(name, a.config)
+        hbm = measured_traffic(name, a.config, variant)
         if hbm is not None:   # counter bytes over the algorithmic bytes or operand+output bytes
             rec["hbm_bytes_measured"] = hbm
         calls[name] = rec
@@ -465,13 +473,13 @@ def main():
             peak = PEAK_BF16_TFLOPS if kind == "flops" else PEAK_FP8_TFLOPS
             roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 1), "peak": peak,
                         "unit": "TFLOP/s", "frac": round(ach / peak, 4),
-                        "traffic": measured_traffic(dom, a.config) if kind == "flops" else None,
+                        "traffic": measured_traffic(dom, a.config, variant) if kind == "flops" else None,
                         "work_per_launch": amount, "avg_launch_ms": round(avg, 4)}
         else:
             ach = amount / avg / 1e6
             roofline = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
                         "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4),
-                        "traffic": measured_traffic(dom, a.config),
+                        "traffic": measured_traffic(dom, a.config, variant),
                         "work_per_launch": amount, "avg_launch_ms": round(avg, 4)}
 
     clock_info = clock.summary() if clock else None
@@ -513,6 +521,7 @@ def main():
                    + (" (forward only)" if a.forward_only and not cfg.dw_only else "")
                    + (", expert forward products in FP8 E4M3" if a.fp8_forward else "")
                    + (", expert data-gradient products in FP8 E4M3" if a.fp8_backward else "")
+                   + (", MX block scales (E8M0 per 32 contraction elements)" if a.mx else "")
                    + (", FP8 weights quantized once (held fixed)" if a.fp8_fixed_weights else "")
                    + (", gather fused into the gate/up product" if a.gather_fused else "")
                    + (", dW from contraction-major copies" if a.dw_transposed else "")

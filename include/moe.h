@@ -330,6 +330,96 @@ moe_status moe_grouped_gemm_fwd_fp8_gate_up(const uint8_t* A, const float* a_sca
                                             int64_t K, int64_t F, moe_bf16* h_gate, moe_bf16* h_up, moe_bf16* act,
                                             void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* ------------------------------------------------------------------------------------------ */
+/* MX variant (also beyond the paper): E4M3 operands with one power-of-two scale per 32        */
+/* consecutive contraction elements of every row (OCP microscaling block structure), applied  */
+/* by the gfx950 matrix cores inside the product; fp32 accumulation, bf16 output.             */
+/* ------------------------------------------------------------------------------------------ */
+
+/*
+ * The MX scale layout, for a matrix of `rows` rows of C elements (C a multiple of 32): the E8M0
+ * scale of block b (elements 32b .. 32b+31) of row r is byte ((b / 4) * rows + r) * 4 + b % 4,
+ * i.e. the array is [ceil(C/128)][rows][4]: each row's four scales of a 128-element group form one
+ * 4-byte word, and the words of all rows for one group lie side by side, so that the product's
+ * scale loads for 64 consecutive rows read 256 contiguous bytes.  When C/32 is not a multiple of
+ * 4, the bytes of the missing blocks of the last group are padding that nothing reads or writes.
+ * Returns the array's size in bytes, ceil(C/128) * rows * 4 (0 if rows or C <= 0).
+ */
+int64_t moe_mx_scale_bytes(int64_t rows, int64_t C);
+
+/*
+ * MX quantization of rows: for each block of 32 consecutive elements of a row of x [M, K] bf16, or
+ * of the concatenation [x[r, :] | x2[r, :]] when x2 [M, K] is given (the operand of the gate/up
+ * data gradient, section 5.4's backward, whose contraction runs over both matrices), amax = max
+ * |block|, e = the smallest integer with amax <= 448 * 2^e, raised to -127 if below (an all-zero
+ * block gets -127); scale byte e + 127 (E8M0) and codes = the E4M3 values nearest to x * 2^-e
+ * (ties to the even mantissa; nothing saturates).  x ~= decode(q) * 2^(byte - 127).
+ * q [M, C] uint8 (C = K, or 2K with x2; 8-byte aligned), scale: the MX scale layout of M rows of C
+ * (moe_mx_scale_bytes(M, C) bytes).
+ * Inputs are finite.  Errors: K % 32 != 0 -> NOT_SUPPORTED; NULL or misaligned pointers ->
+ * INVALID_VALUE.  M = 0 is a no-op.
+ */
+moe_status moe_quantize_mx_rows(const moe_bf16* x, const moe_bf16* x2, int64_t M, int64_t K, uint8_t* q,
+                                uint8_t* scale, hipStream_t stream);
+
+/*
+ * MX quantization of a weight W [G, K, N] bf16 (kept as [expert, contraction of the forward
+ * product, output channel]) in both orientations from one read, each code for code what
+ * moe_quantize_mx_rows gives for the corresponding matrix:
+ *   qt/st: the forward operand [G, N', K], row (g, n) = column n of W[g] over K (blocks along K);
+ *     with W2 (same shape) N' = 2N and the rows interleave W's and W2's channels by 128 as in
+ *     moe_quantize_fp8_weight (the layout moe_grouped_gemm_fwd_mx_gate_up reads); st in the MX
+ *     scale layout of G * N' rows of K.
+ *   qr/sr: the data-gradient operand [G, K, N''], row (g, k) = W[g][k, :] (N'' = N), or
+ *     [W[g][k, :] | W2[g][k, :]] (N'' = 2N), blocks along the row; sr in the MX scale layout of
+ *     G * K rows of N''.
+ * Either pair may be NULL (not both).  One kernel on `stream`.  qt 16-byte, qr 8-byte, W/W2
+ * 16-byte aligned.  Errors: K % 32 != 0, or N % 64 != 0 (N % 128 with W2) -> NOT_SUPPORTED; a
+ * missing half of a pair, NULL or misaligned pointers -> INVALID_VALUE.  G = 0 is a no-op.
+ */
+moe_status moe_quantize_mx_weight(const moe_bf16* w, const moe_bf16* w2, int64_t G, int64_t K, int64_t N,
+                                  uint8_t* qt, uint8_t* st, uint8_t* qr, uint8_t* sr, hipStream_t stream);
+
+/*
+ * The grouped product on MX operands: for rows r of group g (offsets as in moe_grouped_gemm_fwd),
+ * C[r, n] = bf16(sum_k A[r,k] 2^(sa(r, k/32) - 127) * Wt[g,n,k] 2^(sw(g*N + n, k/32) - 127)),
+ * the E4M3 products scaled and accumulated in fp32 by v_mfma_scale_f32_32x32x64_f8f6f4 (each
+ * lane supplies its row's scale byte of one of the instruction's two 32-element blocks).  A [R, K]
+ * uint8 with a_scale in the MX scale layout of R rows of K; Wt [G, N, K] uint8 with w_scale in the
+ * MX scale layout of G * N rows of K (as moe_quantize_mx_rows / moe_quantize_mx_weight write
+ * them); C [R, N] bf16.  workspace: NULL or a split workspace.  Errors as moe_grouped_gemm_fwd_fp8,
+ * with both scale pointers 4-byte aligned.
+ */
+moe_status moe_grouped_gemm_fwd_mx(const uint8_t* A, const uint8_t* a_scale, const uint8_t* Wt,
+                                   const uint8_t* w_scale, const int32_t* offsets, int32_t G, int64_t R, int64_t K,
+                                   int64_t N, moe_bf16* C, void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream);
+
+/*
+ * Steps B + C on MX operands: moe_grouped_gemm_fwd_fp8_gate_up with MX scales (Wt [G, 2F, K] and
+ * w_scale for its G * 2F rows, interleaved by 128 as moe_quantize_mx_weight writes them with W2).
+ * h_gate, h_up bit for bit what moe_grouped_gemm_fwd_mx gives for the de-interleaved weights;
+ * act = silu(h_gate) * h_up as moe_swiglu computes it, if non-NULL.  Errors as
+ * moe_grouped_gemm_fwd_mx; F a multiple of 128.
+ */
+moe_status moe_grouped_gemm_fwd_mx_gate_up(const uint8_t* A, const uint8_t* a_scale, const uint8_t* Wt,
+                                           const uint8_t* w_scale, const int32_t* offsets, int32_t G, int64_t R,
+                                           int64_t K, int64_t F, moe_bf16* h_gate, moe_bf16* h_up, moe_bf16* act,
+                                           void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Steps G + I on MX operands (section 5.4's backward of the down projection and of the SwiGLU):
+ * dA as moe_grouped_gemm_fwd_mx computes it from A = the MX dY_perm [R, K] and Wt = the down
+ * weight's rows [G, N, K] (moe_quantize_mx_weight's qr of W_down), followed in the epilogue by the
+ * SwiGLU backward of moe_grouped_gemm_dx_swiglu_bwd: dh_gate, dh_up [R, N] bf16 from h_gate, h_up.
+ * Errors as moe_grouped_gemm_fwd_mx.
+ */
+moe_status moe_grouped_gemm_dx_swiglu_bwd_mx(const uint8_t* A, const uint8_t* a_scale, const uint8_t* Wt,
+                                             const uint8_t* w_scale, const int32_t* offsets, int32_t G, int64_t R,
+                                             int64_t K, int64_t N, const moe_bf16* h_gate, const moe_bf16* h_up,
+                                             moe_bf16* dh_gate, moe_bf16* dh_up, void* workspace,
+                                             size_t workspace_bytes, hipStream_t stream);
+
 /*
  * moe_grouped_gemm_fwd with the same split of the last, partial round of tiles (same arguments,
  * definitions and errors as moe_grouped_gemm_fwd, plus a split workspace as described at

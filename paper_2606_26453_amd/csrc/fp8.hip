@@ -255,3 +255,172 @@ extern "C" moe_status moe_quantize_fp8_rows2(const moe_bf16* x, const moe_bf16* 
   if (!x2) return fail(MOE_ERROR_INVALID_VALUE, "moe_quantize_fp8_rows2: x2 is NULL");
   return quantize_rows_impl("moe_quantize_fp8_rows2", x, x2, M, K, q, scale, stream);
 }
+
+// ---------------------------------------------------------------------------------------------
+// MX quantization: E4M3 codes with one power-of-two scale per 32 consecutive elements of a row,
+// stored as an E8M0 byte (value 2^(byte - 127)).  The block's exponent is the smallest e with
+// amax <= 448 * 2^e (no element saturates), at least -127 (all-zero blocks get byte 0); the codes
+// round x * 2^-e, an exact scaling, to the nearest E4M3 value (ties to the even mantissa).
+// ---------------------------------------------------------------------------------------------
+namespace moe {
+namespace {
+
+// amax = (1 + m / 2^23) * 2^(E - 127) for a biased exponent E >= 1, and 448 * 2^e = 1.75 * 2^(e + 8):
+// e = E - 135 when the significand is at most 1.75 (m <= 0x600000), else E - 134.  A zero or
+// subnormal amax (E = 0) gives at most -134, raised to -127.  The byte is e + 127.
+__device__ __forceinline__ uint32_t mx_scale_byte(float amax) {
+  const uint32_t b = __float_as_uint(amax);   // amax >= 0
+  const int byte = (int)(b >> 23) - 8 + ((b & 0x7FFFFFu) > 0x600000u ? 1 : 0);
+  return byte < 0 ? 0u : (uint32_t)byte;
+}
+
+// 2^-e for byte = e + 127: the biased exponent 127 - e = 254 - byte, 7 .. 254 for the bytes that
+// finite bf16 inputs produce (0 .. 247)
+__device__ __forceinline__ float mx_inv_scale(uint32_t byte) { return __uint_as_float((254u - byte) << 23); }
+
+__device__ __forceinline__ uint32_t e4m3_pack4(float a, float b, float c, float d, float inv) {
+  return e4m3_code(a * inv) | (e4m3_code(b * inv) << 8) | (e4m3_code(c * inv) << 16) | (e4m3_code(d * inv) << 24);
+}
+
+// Scale byte of block b of row r in the MX scale layout of a matrix with `rows` rows: the four
+// scales of a row's 128-element group form one 4-byte word, and the words of all rows for one group
+// lie side by side (what the product's scale loads read, 256 contiguous bytes per wavefront).
+__device__ __forceinline__ int64_t mx_scale_at(int64_t r, int64_t b, int64_t rows) {
+  return ((b >> 2) * rows + r) * 4 + (b & 3);
+}
+
+// Rows: workgroup (row r, chunk block cb) covers 8-element chunks cb*256 .. cb*256+255 of row r of
+// the [M, C] matrix (C = K, or 2K for the concatenation [x | x2]); four neighbouring lanes hold a
+// 32-element block and combine their maxima by lane exchange.
+__global__ __launch_bounds__(256) void quantize_mx_rows_kernel(const u32x4* __restrict__ x, const u32x4* __restrict__ x2,
+                                                               int64_t K8, int cpr, int64_t M, uint2* __restrict__ q,
+                                                               uint8_t* __restrict__ s) {
+  const int64_t C8 = x2 ? 2 * K8 : K8;
+  const int64_t r = blockIdx.x / cpr;
+  const int64_t c8 = (int64_t)(blockIdx.x - r * cpr) * 256 + threadIdx.x;
+  const bool live = c8 < C8;   // whole blocks: C8 is a multiple of 4
+  u32x4 v = {0u, 0u, 0u, 0u};
+  if (live) v = (c8 < K8) ? x[r * K8 + c8] : x2[r * K8 + c8 - K8];
+  float m = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) m = fmaxf(m, fmaxf(fabsf(bf16_lo(v[e])), fabsf(bf16_hi(v[e]))));
+  m = fmaxf(m, __shfl_xor(m, 1));
+  m = fmaxf(m, __shfl_xor(m, 2));
+  const uint32_t byte = mx_scale_byte(m);
+  const float inv = mx_inv_scale(byte);
+  if (live) {
+    q[r * C8 + c8] = make_uint2(e4m3_pack4(bf16_lo(v[0]), bf16_hi(v[0]), bf16_lo(v[1]), bf16_hi(v[1]), inv),
+                                e4m3_pack4(bf16_lo(v[2]), bf16_hi(v[2]), bf16_lo(v[3]), bf16_hi(v[3]), inv));
+    if ((c8 & 3) == 0) s[mx_scale_at(r, c8 >> 2, M)] = (uint8_t)byte;
+  }
+}
+
+// Weights, both orientations from one read.  Workgroup (column block n0 = 64*bx, row block
+// k0 = 128*by, matrix/expert bz) stages the 128 x 64 tile of W[g] (or W2[g]) in LDS:
+//   rows (qr, sr): row (g, k) of the [G, K, nmat*N] matrix [W[g] | W2[g]], blocks of 32 columns;
+//     thread t: column chunk t%8 of rows k0 + t/8 + 32u (u < 4), lanes t^1, t^2 share its block;
+//   columns (qt, st): row (g, n') of [G, N', K] = column n of W[g] (or W2[g], interleaved by 128
+//     as in the fp32-scale weight layout), blocks of 32 rows; thread t: column t%64, rows
+//     k0 + 32*(t/64) .. +31, 32 contiguous bytes of row n' (a workgroup writes 128 per row).
+// Scales in the MX scale layout of each output (rows G*K for qr, G*N' for qt).
+__global__ __launch_bounds__(256) void quantize_mx_weight_kernel(const uint16_t* __restrict__ w,
+                                                                 const uint16_t* __restrict__ w2, int64_t G, int64_t K,
+                                                                 int64_t N, uint8_t* __restrict__ qt,
+                                                                 uint8_t* __restrict__ st, uint8_t* __restrict__ qr,
+                                                                 uint8_t* __restrict__ sr) {
+  __shared__ __attribute__((aligned(16))) uint16_t s_w[128 * 64];
+  const int t = threadIdx.x;
+  const int nmat = w2 ? 2 : 1;
+  const int64_t g = blockIdx.z / nmat;
+  const bool second = (int)(blockIdx.z - g * nmat) == 1;
+  const int64_t n0 = (int64_t)blockIdx.x * 64, k0 = (int64_t)blockIdx.y * 128;
+  const uint16_t* src = (second ? w2 : w) + g * K * N + n0;
+  const int c8 = t & 7, rq = t >> 3;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int kl = rq + 32 * u;
+    const int64_t k = k0 + kl;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (k < K) v = *reinterpret_cast<const u32x4*>(src + k * N + 8 * c8);
+    *reinterpret_cast<u32x4*>(s_w + kl * 64 + 8 * c8) = v;
+    if (qr != nullptr) {
+      float m = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) m = fmaxf(m, fmaxf(fabsf(bf16_lo(v[e])), fabsf(bf16_hi(v[e]))));
+      m = fmaxf(m, __shfl_xor(m, 1));
+      m = fmaxf(m, __shfl_xor(m, 2));
+      const uint32_t byte = mx_scale_byte(m);
+      const float inv = mx_inv_scale(byte);
+      if (k < K) {
+        const int64_t row = g * K + k, col = (second ? N : 0) + n0 + 8 * c8;
+        *reinterpret_cast<uint2*>(qr + row * (nmat * N) + col) =
+            make_uint2(e4m3_pack4(bf16_lo(v[0]), bf16_hi(v[0]), bf16_lo(v[1]), bf16_hi(v[1]), inv),
+                       e4m3_pack4(bf16_lo(v[2]), bf16_hi(v[2]), bf16_lo(v[3]), bf16_hi(v[3]), inv));
+        if ((c8 & 3) == 0) sr[mx_scale_at(row, col >> 5, G * K)] = (uint8_t)byte;
+      }
+    }
+  }
+  if (qt == nullptr) return;   // uniform
+  __syncthreads();
+  const int n = t & 63, kb = t >> 6;
+  if (k0 + 32 * kb >= K) return;   // K is a multiple of 32: the block is whole or absent
+  float v[32];
+  float m = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 32; ++i) {
+    v[i] = __uint_as_float((uint32_t)s_w[(32 * kb + i) * 64 + n] << 16);
+    m = fmaxf(m, fabsf(v[i]));
+  }
+  const uint32_t byte = mx_scale_byte(m);
+  const float inv = mx_inv_scale(byte);
+  uint32_t o[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) o[i] = e4m3_pack4(v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3], inv);
+  const int64_t row = g * (nmat * N) + qc_out_row(n0 + n, w2 != nullptr, second);
+  uint8_t* dst = qt + row * K + k0 + 32 * kb;
+  *reinterpret_cast<u32x4*>(dst) = u32x4{o[0], o[1], o[2], o[3]};
+  *reinterpret_cast<u32x4*>(dst + 16) = u32x4{o[4], o[5], o[6], o[7]};
+  st[mx_scale_at(row, (k0 >> 5) + kb, G * nmat * N)] = (uint8_t)byte;
+}
+
+}  // namespace
+}  // namespace moe
+
+extern "C" moe_status moe_quantize_mx_rows(const moe_bf16* x, const moe_bf16* x2, int64_t M, int64_t K, uint8_t* q,
+                                           uint8_t* scale, hipStream_t stream) {
+  const char* fn = "moe_quantize_mx_rows";
+  if (M < 0 || K <= 0) return fail(MOE_ERROR_INVALID_VALUE, "%s: bad size", fn);
+  if (K % 32) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: K must be a multiple of 32", fn);
+  const int64_t C8 = (x2 ? 2 : 1) * K / 8;
+  const int64_t cpr = (C8 + 255) / 256;
+  if (M * cpr >= ((int64_t)1 << 31)) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: too many rows", fn);
+  if (M == 0) return MOE_SUCCESS;
+  if (!x || !q || !scale) return fail(MOE_ERROR_INVALID_VALUE, "%s: NULL pointer", fn);
+  if (!aligned16(x) || (x2 && !aligned16(x2)) || (reinterpret_cast<uintptr_t>(q) & 7))
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: x (and x2) must be 16-byte, q 8-byte aligned", fn);
+  quantize_mx_rows_kernel<<<(unsigned)(M * cpr), 256, 0, stream>>>(
+      reinterpret_cast<const u32x4*>(x), reinterpret_cast<const u32x4*>(x2), K / 8, (int)cpr, M,
+      reinterpret_cast<uint2*>(q), scale);
+  return check_launch("quantize_mx_rows_kernel");
+}
+
+extern "C" moe_status moe_quantize_mx_weight(const moe_bf16* w, const moe_bf16* w2, int64_t G, int64_t K, int64_t N,
+                                             uint8_t* qt, uint8_t* st, uint8_t* qr, uint8_t* sr, hipStream_t stream) {
+  const char* fn = "moe_quantize_mx_weight";
+  if (G < 0 || K <= 0 || N <= 0) return fail(MOE_ERROR_INVALID_VALUE, "%s: bad size", fn);
+  const int nmul = w2 ? QC_IL : 64;
+  if (K % 32 || N % nmul)
+    return fail(MOE_ERROR_NOT_SUPPORTED, "%s: K must be a multiple of 32 and N of %d", fn, nmul);
+  const int64_t nmat = w2 ? 2 : 1;
+  if (G * nmat > 65535 || (K + 127) / 128 > 65535 || N / 64 > 0x7fffffff)
+    return fail(MOE_ERROR_NOT_SUPPORTED, "%s: too many experts, rows or columns", fn);
+  if ((qt == nullptr) != (st == nullptr) || (qr == nullptr) != (sr == nullptr) || (!qt && !qr))
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: give qt with st and/or qr with sr", fn);
+  if (G == 0) return MOE_SUCCESS;
+  if (!w) return fail(MOE_ERROR_INVALID_VALUE, "%s: NULL pointer", fn);
+  if (!aligned16(w) || (w2 && !aligned16(w2)) || (qt && !aligned16(qt)) || (reinterpret_cast<uintptr_t>(qr) & 7))
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: w, w2 and qt must be 16-byte, qr 8-byte aligned", fn);
+  quantize_mx_weight_kernel<<<dim3((unsigned)(N / 64), (unsigned)((K + 127) / 128), (unsigned)(G * nmat)), 256, 0,
+                              stream>>>(w, w2, G, K, N, qt, st, qr, sr);
+  return check_launch("quantize_mx_weight_kernel");
+}

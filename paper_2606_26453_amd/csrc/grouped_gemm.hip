@@ -74,6 +74,9 @@ struct GemmParams {
   int64_t gather_rows;
   const float* a_scale;    // FP8 products: per-row scale of the row operand [R]
   const float* w_scale;    //               per-output-column scale of the weight [G, K]
+  const uint8_t* a_mx;     // MX products: E8M0 block scales of the row operand [C/128][R][4]
+  const uint8_t* w_mx;     //              ... of the weight's rows [C/128][G*K][4]
+  int64_t mx_a_step, mx_w_step;   //       bytes from one 128-element group of scales to the next
   int* tile_queue;         // DW, persistent: 8 tile-claim counters, one per XCD (zero at launch)
 };
 
@@ -110,6 +113,14 @@ __device__ __forceinline__ i32x4 make_rsrc32(const void* base, int bytes) {
 // tracked explicitly with vmcnt waits (loads retire in order).
 __device__ __forceinline__ void dma16(i32x4 rsrc, int voff, int lds_addr) {
   asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+               :
+               : "v"(voff), "s"(rsrc), "s"(lds_addr)
+               : "memory", "m0");
+}
+
+// The same with 4 bytes per lane (lds_addr + 4*lane).
+__device__ __forceinline__ void dma4(i32x4 rsrc, int voff, int lds_addr) {
+  asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dword %0, %1, 0 offen lds"
                :
                : "v"(voff), "s"(rsrc), "s"(lds_addr)
                : "memory", "m0");
@@ -169,15 +180,23 @@ __device__ __forceinline__ void band_order(int id, int mtiles, int ntiles, int& 
 // F8 (dX kind only): both operands are E4M3 bytes; a stage then holds 64 contraction elements in the
 // same 64-byte rows, and one v_mfma_scale_f32_32x32x64_f8f6f4 per block consumes the two 16-byte
 // fragments a bf16 stage feeds to two 32x32x16 MFMAs.  The epilogue applies the fp32 row and
-// column scales before rounding to bf16.
+// column scales before rounding to bf16.  MX (with F8): the scales are instead powers of two, one
+// per 32 contraction elements of every row of either operand, stored with each row's four scales
+// of a 128-element group in one 4-byte word and the words of consecutive rows side by side; each
+// stage carries its two blocks' scale bytes (one 4-byte LDS DMA load per wavefront, 256 contiguous
+// bytes: waves 0-3 the words of the 256 tile rows, waves 4-7 those of the 256 weight rows, each
+// word serving two stages), and the matrix core applies them inside the product (the epilogue only
+// rounds).
 template <int KIND, bool DUAL, bool ACT, int TM, int WAVES_M, int WAVES_N, int NSTAGE, bool PINGPONG, int WPE,
-          bool PERSIST, bool OUT16, bool GATHER, bool F8>
+          bool PERSIST, bool OUT16, bool GATHER, bool F8, bool MX>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kernel(GemmParams p) {
   // F8 && DUAL: one weight whose output channels interleave gate and up by 128 (tile columns
   // 0..127 gate, 128..255 up), stored as two outputs (+ SwiGLU with ACT) like the fwd dual product.
   // F8 && ACT && !DUAL: the dX-down product with the SwiGLU backward in its epilogue, applied to
   // the scaled, bf16-rounded dA exactly as in the bf16 product.
   static_assert(!F8 || KIND == KIND_DX, "FP8 operands: the dX-shaped product");
+  static_assert(!MX || (F8 && PINGPONG && WAVES_M * WAVES_N == 8 && TM == 256),
+                "MX scales: the FP8 product's 8-wavefront ping-pong schedule");
   constexpr int ES = F8 ? 1 : 2;              // bytes per operand element
   constexpr int BKE = F8 ? 2 * BK : BK;       // contraction elements per stage (64-byte rows)
   constexpr int NWAVE = WAVES_M * WAVES_N;
@@ -187,6 +206,8 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
   constexpr int DPW_M = TM / 16 / NWAVE;      // 1 KiB DMA loads per wave per stage, M side
   constexpr int DPW_N = TN / 16 / NWAVE;      // ... N side
   constexpr int DPW_T = DPW_M + DPW_N;
+  constexpr int OPS = DPW_T + (MX ? 1 : 0);   // DMA loads per wave per stage (MX: + the scales)
+  constexpr bool FSCALE = F8 && !MX;          // fp32 row/column scales applied in the epilogue
   static_assert(DPW_M * NWAVE * 16 == TM && DPW_N * NWAVE * 16 == TN, "DMA split");
   constexpr int WTM = TM / WAVES_M;           // per-wave tile rows
   constexpr int WTN = TN / WAVES_N;           // per-wave tile columns
@@ -198,6 +219,10 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
                                                                 // contraction, outputs are dB[g]
 
   __shared__ __attribute__((aligned(16))) char lds[NSTAGE * STAGE];
+  // MX: per stage, the scale words of the 256 tile rows (bytes 0..1023) and of the 256 weight rows
+  // (1024..2047); word of row r: 4*r, byte 2*(step & 1) + half is the scale of that half
+  constexpr int SC_STAGE = 2048;
+  __shared__ __attribute__((aligned(16))) char lds_sc[MX ? NSTAGE * SC_STAGE : 16];
   __shared__ int s_scan[256];
 
   const int tid = threadIdx.x;
@@ -338,6 +363,9 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
   int nsteps = 0;
   int c_len32 = 0, m_row_bytes = 0, n_row_bytes = 0;   // the same sizes in 32 bits
   int tile_rows = TM;             // FWD/DX: output rows of the tile that are rows of its group
+  const char* sc_src = nullptr;   // MX: this wave's scale words (tile rows or weight rows), group 0
+  int sc_voff = 0;
+  int64_t sc_step = 0;            //     bytes between consecutive 128-element groups
   auto setup = [&](int g, int mt, int nt, int64_t row_lo, int64_t row_hi) {
     tile_rows = (int)(row_hi - row_lo < TM ? row_hi - row_lo : TM);
     // lane-dependent terms are recomputed per tile rather than hoisted out of the tile loop and
@@ -454,6 +482,24 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
       }
     }
 
+    if constexpr (MX) {
+      // waves 0-3: tile rows 64*wave + lane (clamped to the group, like the row loads); waves 4-7:
+      // weight rows (output columns) nt*TN + 64*(wave-4) + lane, clamped to the last
+      const int r = 64 * (wave & 3) + lane;
+      if (wave < 4) {
+        int64_t rr = r;
+        if (rr > row_hi - row_lo - 1) rr = row_hi - row_lo - 1;
+        sc_src = reinterpret_cast<const char*>(p.a_mx) + row_lo * 4;
+        sc_voff = (int)(rr * 4);
+        sc_step = p.mx_a_step;
+      } else {
+        int64_t kk = (int64_t)nt * TN + r;
+        if (kk > p.K - 1) kk = p.K - 1;
+        sc_src = reinterpret_cast<const char*>(p.w_mx) + (int64_t)g * p.K * 4;
+        sc_voff = (int)(kk * 4);
+        sc_step = p.mx_w_step;
+      }
+    }
     // contraction extent
     if constexpr (KIND == KIND_FWD) c_len = p.K;
     else if constexpr (KIND == KIND_DX) c_len = (DUAL && !F8) ? 2 * p.N : p.N;
@@ -513,11 +559,20 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
     else dma16(rn, n_voff[d - DPW_M], slot_lds + OPND_M + (DPW_N * wave + d - DPW_M) * 1024);
   };
   auto slot_of = [&](int s) { return s % NSTAGE; };
+  // MX: this wave's scale load of step s: the 4-byte word holding the scales of steps s & ~1 and
+  // s | 1 (a step past the end reads zeros, like the operands)
+  const int lds_sc0 = (int)(size_t)(const __attribute__((address_space(3))) char*)lds_sc;
+  auto dma_sc = [&](int s) {
+    const int sa = s + s_base;
+    const i32x4 rs = make_rsrc32(sc_src + (int64_t)(sa >> 1) * sc_step, s < nsteps ? 0x7fffffff : 0);
+    dma4(rs, sc_voff, lds_sc0 + slot_of(s) * SC_STAGE + wave * 256);
+  };
   auto issue = [&](int s) {
     const int slot_lds = lds0 + slot_of(s) * STAGE;
     const i32x4 rm = rsrc_m(s), rn = rsrc_n(s);
 #pragma unroll
     for (int d = 0; d < DPW_T; ++d) dma_one(d, rm, rn, slot_lds);
+    if constexpr (MX) dma_sc(s);
   };
 
   // ---------------- fragment reads ---------------------------------------------------------------
@@ -573,9 +628,22 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
       acc[m / NB][m % NB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[set][m % NB], fb[set][m / NB],
                                                                    acc[m / NB][m % NB], 0, 0, 0);
   };
-  // FP8: one 32x32x64 MFMA per block from the concatenated 16-byte fragments of sets 0 and 1
-  // (any assignment of the 64 contraction bytes to lanes works as long as both operands use the
-  // same one: each lane half holds bytes {0-15, 32-47} or {16-31, 48-63} of the stage's row)
+  // FP8: one 32x32x64 MFMA per block from the concatenated 16-byte fragments of sets 0 and 1: lane
+  // half h holds bytes 16h..16h+15 and 32+16h..32+16h+15 of the stage's row, which the instruction
+  // takes as its contraction elements in the same order (its first 16 bytes of either half are
+  // elements 0..31, the second 16 elements 32..63).  So its two scale blocks are the contraction's
+  // own 32-element blocks 2*step and 2*step + 1, and lane half h supplies block h's scale of its row.
+  int sc_m[MB], sc_n[NB];   // MX: this lane's scale bytes for the current stage
+  auto read_scales = [&](int s) {
+    if constexpr (MX) {
+      const char* b = lds_sc + slot_of(s) * SC_STAGE + 2 * ((s + s_base) & 1) + fh;
+#pragma unroll
+      for (int i = 0; i < MB; ++i) sc_m[i] = *reinterpret_cast<const uint8_t*>(b + 4 * (wm * WTM + 32 * i + l32));
+#pragma unroll
+      for (int j = 0; j < NB; ++j)
+        sc_n[j] = *reinterpret_cast<const uint8_t*>(b + 1024 + 4 * (wn * WTN + 32 * j + l32));
+    }
+  };
   auto mfmas_f8 = [&]() {
 #pragma unroll
     for (int m = 0; m < MB * NB; ++m) {
@@ -583,9 +651,14 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
       const i32x4 b0 = __builtin_bit_cast(i32x4, fb[0][m / NB]), b1 = __builtin_bit_cast(i32x4, fb[1][m / NB]);
       const i32x8 a8 = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
       const i32x8 b8 = __builtin_shufflevector(b0, b1, 0, 1, 2, 3, 4, 5, 6, 7);
-      // operand formats 0 (E4M3) for both; block scales 127 (2^0) leave the products unscaled
-      acc[m / NB][m % NB] =
-          __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, acc[m / NB][m % NB], 0, 0, 0, 127, 0, 127);
+      // operand formats 0 (E4M3) for both; without MX the block scales are 127 (2^0), leaving the
+      // products unscaled
+      if constexpr (MX)
+        acc[m / NB][m % NB] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+            a8, b8, acc[m / NB][m % NB], 0, 0, 0, sc_n[m % NB], 0, sc_m[m / NB]);
+      else
+        acc[m / NB][m % NB] =
+            __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, acc[m / NB][m % NB], 0, 0, 0, 127, 0, 127);
     }
   };
   // the same, with the DPW_T refill loads of step `s` spread evenly between the MFMAs so the
@@ -685,19 +758,21 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
       const int slot = slot_of(s);
       load_frags(0, slot, 0);
       load_frags(1, slot, 1);
+      read_scales(s);
       const int slot_lds = lds0 + slot_of(s + 3) * STAGE;
       const i32x4 rm = rsrc_m(s + 3), rn = rsrc_n(s + 3);
 #pragma unroll
       for (int d = 0; d < DPW_T; ++d) dma_one(d, rm, rn, slot_lds);
+      if constexpr (MX) dma_sc(s + 3);
     };
     auto half_end = [&]() {
       __builtin_amdgcn_sched_barrier(0);
-      wait_vm<(NSTAGE - 2) * DPW_T>();
+      wait_vm<(NSTAGE - 2) * OPS>();
       __syncthreads();
       __builtin_amdgcn_sched_barrier(0);
     };
     if (nsteps > 0) {
-      wait_vm<(NSTAGE - 2) * DPW_T>();
+      wait_vm<(NSTAGE - 2) * OPS>();
       __syncthreads();
       if (grp == 1) half_end();
       for (int s = 0; s < nsteps; ++s) {
@@ -820,7 +895,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
           if constexpr (ACC_SPLIT) c = (j >= NB / 2 ? 16 : 0) + (wn * (WTN / 2) + 32 * (j % (NB / 2)) + 8 * q) / 8;
           else c = (wn * WTN + 32 * j + 8 * q) / 8;
           uint2 v;
-          if constexpr (F8) {
+          if constexpr (FSCALE) {
             // fp32 row and column scales; rows past the group and columns past the output (not
             // stored) read clamped scales
             int64_t r = row_lo + wm * WTM + 32 * i + l32;
@@ -1135,7 +1210,7 @@ constexpr size_t SPLIT_BYTES = SPLIT_CNT_BYTES + (size_t)SPLIT_UNITS * 256 * TN 
 
 // QUEUE (dW): a persistent grid whose workgroups claim tiles from p.tile_queue.
 template <int KIND, bool DUAL, bool ACT, bool OUT16 = false, bool GATHER = false, bool F8 = false,
-          bool QUEUE = false>
+          bool QUEUE = false, bool MX = false>
 moe_status launch(const GemmParams& p, int64_t tiles_bound, hipStream_t stream, const char* name) {
   if (tiles_bound == 0) return MOE_SUCCESS;
   if (tiles_bound >= ((int64_t)1 << 31) - SPLIT_UNITS) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: too many tiles", name);
@@ -1153,7 +1228,7 @@ moe_status launch(const GemmParams& p, int64_t tiles_bound, hipStream_t stream, 
     grid += SPLIT_UNITS;   // the split units run past the full rounds' tiles (idle ones exit)
   }
   static_assert(!GATHER || KIND == KIND_FWD, "gathered rows feed the forward product only");
-  grouped_gemm_kernel<KIND, DUAL, ACT, C::TM, C::WM, C::WN, C::NS, C::PP, C::WPE, PERSIST, OUT16, GATHER, F8>
+  grouped_gemm_kernel<KIND, DUAL, ACT, C::TM, C::WM, C::WN, C::NS, C::PP, C::WPE, PERSIST, OUT16, GATHER, F8, MX>
       <<<grid, 64 * C::WM * C::WN, 0, stream>>>(p);
   return check_launch(name);
 }
@@ -1299,66 +1374,86 @@ extern "C" moe_status moe_grouped_gemm_dx(const moe_bf16* dC, const moe_bf16* B,
 
 extern "C" size_t moe_grouped_gemm_split_workspace_bytes(void) { return SPLIT_BYTES; }
 
+namespace moe {
+namespace {
+// The E4M3 products, all dX-shaped (rows of A against rows of Wt[g], both read along the
+// contraction Kc; Nout output columns): plain, the interleaved gate/up pair (+ SwiGLU), and the
+// dX-down product with the SwiGLU backward in its epilogue.  Scales: fp32 per row / per output
+// channel, or (mx) E8M0 bytes per 32 contraction elements of every row of either operand.
+enum F8Op { F8_PLAIN, F8_GATE_UP, F8_SWIGLU_BWD };
+
+template <bool MX>
+moe_status f8_product(const char* fn, F8Op op, const uint8_t* A, const void* a_scale, const uint8_t* Wt,
+                      const void* w_scale, const int32_t* offsets, int32_t G, int64_t R, int64_t Kc, int64_t Nout,
+                      moe_bf16* out, moe_bf16* out2, moe_bf16* act, const moe_bf16* hg, const moe_bf16* hu,
+                      void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (G < 1 || G > 256) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: need 1 <= G <= 256", fn);
+  if (R < 0 || Kc <= 0 || Nout <= 0) return fail(MOE_ERROR_INVALID_VALUE, "%s: bad size", fn);
+  if (op == F8_GATE_UP) {
+    if (Kc % 64 || Nout % 256) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: K must be a multiple of 64, F of 128", fn);
+  } else if (Kc % 64 || Nout % 64) {
+    return fail(MOE_ERROR_NOT_SUPPORTED, "%s: K and N must be multiples of 64", fn);
+  }
+  if (R >= ((int64_t)1 << 31)) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: R >= 2^31", fn);
+  if (Nout * Kc >= ((int64_t)1 << 31)) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: one group's weight must be < 2 GiB", fn);
+  if (!offsets) return fail(MOE_ERROR_INVALID_VALUE, "%s: offsets is NULL", fn);
+  if (R == 0) return MOE_SUCCESS;
+  if (!A || !a_scale || !Wt || !w_scale || !out) return fail(MOE_ERROR_INVALID_VALUE, "%s: NULL pointer", fn);
+  if ((op == F8_GATE_UP && !out2) || (op == F8_SWIGLU_BWD && (!out2 || !hg || !hu)))
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: NULL pointer", fn);
+  if (bad_ptr(A) || bad_ptr(Wt) || bad_ptr(out) || bad_ptr(out2) || bad_ptr(act) || bad_ptr(hg) || bad_ptr(hu))
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: operand and output pointers must be 16-byte aligned", fn);
+  if ((reinterpret_cast<uintptr_t>(a_scale) & 3) || (MX ? (reinterpret_cast<uintptr_t>(w_scale) & 3) : bad_ptr(w_scale)))
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: a_scale must be 4-byte, w_scale %s aligned", fn, MX ? "4-byte" : "16-byte");
+  GemmParams p{};
+  p.a = reinterpret_cast<const uint16_t*>(A);
+  p.b = reinterpret_cast<const uint16_t*>(Wt);
+  p.offsets = offsets; p.out = out; p.out2 = out2; p.act = act; p.hg = hg; p.hu = hu;
+  if constexpr (MX) {
+    p.a_mx = static_cast<const uint8_t*>(a_scale);
+    p.w_mx = static_cast<const uint8_t*>(w_scale);
+    p.mx_a_step = R * 4;
+    p.mx_w_step = (int64_t)G * Nout * 4;
+  } else {
+    p.a_scale = static_cast<const float*>(a_scale);
+    p.w_scale = static_cast<const float*>(w_scale);
+  }
+  p.G = G; p.R = R; p.K = Nout; p.N = Kc;
+  constexpr int TM = Cfg<KIND_DX>::TM;
+  p.mt_bound = (int)((R + TM - 1) / TM + G);
+  p.n_tiles = (int)((Nout + TN - 1) / TN);
+  const int64_t tiles = (int64_t)p.mt_bound * p.n_tiles;
+  const moe_status st = attach_split(p, workspace, workspace_bytes, fn, stream);
+  if (st != MOE_SUCCESS) return st;
+  if (op == F8_GATE_UP) {
+    if (act) return launch<KIND_DX, true, true, false, false, true, false, MX>(p, tiles, stream, fn);
+    return launch<KIND_DX, true, false, false, false, true, false, MX>(p, tiles, stream, fn);
+  }
+  if (op == F8_SWIGLU_BWD) return launch<KIND_DX, false, true, false, false, true, false, MX>(p, tiles, stream, fn);
+  return launch<KIND_DX, false, false, false, false, true, false, MX>(p, tiles, stream, fn);
+}
+}  // namespace
+}  // namespace moe
+
+extern "C" int64_t moe_mx_scale_bytes(int64_t rows, int64_t C) {
+  return rows <= 0 || C <= 0 ? 0 : (C + 127) / 128 * rows * 4;
+}
+
 extern "C" moe_status moe_grouped_gemm_fwd_fp8_gate_up(const uint8_t* A, const float* a_scale, const uint8_t* Wt,
                                                        const float* w_scale, const int32_t* offsets, int32_t G,
                                                        int64_t R, int64_t K, int64_t F, moe_bf16* h_gate,
                                                        moe_bf16* h_up, moe_bf16* act, void* workspace,
                                                        size_t workspace_bytes, hipStream_t stream) {
-  const char* fn = "moe_grouped_gemm_fwd_fp8_gate_up";
-  if (G < 1 || G > 256) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: need 1 <= G <= 256", fn);
-  if (R < 0 || K <= 0 || F <= 0) return fail(MOE_ERROR_INVALID_VALUE, "%s: bad size", fn);
-  if (K % 64 || F % 128) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: K must be a multiple of 64, F of 128", fn);
-  if (R >= ((int64_t)1 << 31)) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: R >= 2^31", fn);
-  if (2 * F * K >= ((int64_t)1 << 31)) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: one group's weight must be < 2 GiB", fn);
-  if (!offsets) return fail(MOE_ERROR_INVALID_VALUE, "%s: offsets is NULL", fn);
-  if (R == 0) return MOE_SUCCESS;
-  if (!A || !a_scale || !Wt || !w_scale || !h_gate || !h_up) return fail(MOE_ERROR_INVALID_VALUE, "%s: NULL pointer", fn);
-  if (bad_ptr(A) || bad_ptr(Wt) || bad_ptr(h_gate) || bad_ptr(h_up) || bad_ptr(act) || bad_ptr(w_scale) ||
-      (reinterpret_cast<uintptr_t>(a_scale) & 3))
-    return fail(MOE_ERROR_INVALID_VALUE, "%s: pointers must be 16-byte aligned (a_scale 4-byte)", fn);
-  GemmParams p{};
-  p.a = reinterpret_cast<const uint16_t*>(A);
-  p.b = reinterpret_cast<const uint16_t*>(Wt);
-  p.offsets = offsets; p.out = h_gate; p.out2 = h_up; p.act = act; p.a_scale = a_scale; p.w_scale = w_scale;
-  p.G = G; p.R = R; p.K = 2 * F; p.N = K;
-  constexpr int TM = Cfg<KIND_DX>::TM;
-  p.mt_bound = (int)((R + TM - 1) / TM + G);
-  p.n_tiles = (int)((2 * F + TN - 1) / TN);
-  const int64_t tiles = (int64_t)p.mt_bound * p.n_tiles;
-  const moe_status st = attach_split(p, workspace, workspace_bytes, fn, stream);
-  if (st != MOE_SUCCESS) return st;
-  if (act) return launch<KIND_DX, true, true, false, false, true>(p, tiles, stream, "grouped_gemm_fwd_fp8(gate_up,swiglu)");
-  return launch<KIND_DX, true, false, false, false, true>(p, tiles, stream, "grouped_gemm_fwd_fp8(gate_up)");
+  return f8_product<false>("moe_grouped_gemm_fwd_fp8_gate_up", F8_GATE_UP, A, a_scale, Wt, w_scale, offsets, G, R, K,
+                           2 * F, h_gate, h_up, act, nullptr, nullptr, workspace, workspace_bytes, stream);
 }
 
 extern "C" moe_status moe_grouped_gemm_fwd_fp8(const uint8_t* A, const float* a_scale, const uint8_t* Wt,
                                                const float* w_scale, const int32_t* offsets, int32_t G, int64_t R,
                                                int64_t K, int64_t N, moe_bf16* C, void* workspace,
                                                size_t workspace_bytes, hipStream_t stream) {
-  const char* fn = "moe_grouped_gemm_fwd_fp8";
-  if (G < 1 || G > 256) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: need 1 <= G <= 256", fn);
-  if (R < 0 || K <= 0 || N <= 0) return fail(MOE_ERROR_INVALID_VALUE, "%s: bad size", fn);
-  if (K % 64 || N % 64) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: K and N must be multiples of 64", fn);
-  if (R >= ((int64_t)1 << 31)) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: R >= 2^31", fn);
-  if (N * K >= ((int64_t)1 << 31)) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: one group's weight must be < 2 GiB", fn);
-  if (!offsets) return fail(MOE_ERROR_INVALID_VALUE, "%s: offsets is NULL", fn);
-  if (R == 0) return MOE_SUCCESS;
-  if (!A || !a_scale || !Wt || !w_scale || !C) return fail(MOE_ERROR_INVALID_VALUE, "%s: NULL pointer", fn);
-  if (bad_ptr(A) || bad_ptr(Wt) || bad_ptr(C) || bad_ptr(w_scale) || (reinterpret_cast<uintptr_t>(a_scale) & 3))
-    return fail(MOE_ERROR_INVALID_VALUE, "%s: A, Wt, C, w_scale must be 16-byte aligned, a_scale 4-byte", fn);
-  // the dX-shaped product: rows of A (contraction K) against rows of Wt[g] (output columns N)
-  GemmParams p{};
-  p.a = reinterpret_cast<const uint16_t*>(A);
-  p.b = reinterpret_cast<const uint16_t*>(Wt);
-  p.offsets = offsets; p.out = C; p.a_scale = a_scale; p.w_scale = w_scale;
-  p.G = G; p.R = R; p.K = N; p.N = K;
-  constexpr int TM = Cfg<KIND_DX>::TM;
-  p.mt_bound = (int)((R + TM - 1) / TM + G);
-  p.n_tiles = (int)((N + TN - 1) / TN);
-  const int64_t tiles = (int64_t)p.mt_bound * p.n_tiles;
-  const moe_status st = attach_split(p, workspace, workspace_bytes, fn, stream);
-  if (st != MOE_SUCCESS) return st;
-  return launch<KIND_DX, false, false, false, false, true>(p, tiles, stream, "grouped_gemm_fwd_fp8");
+  return f8_product<false>("moe_grouped_gemm_fwd_fp8", F8_PLAIN, A, a_scale, Wt, w_scale, offsets, G, R, K, N, C,
+                           nullptr, nullptr, nullptr, nullptr, workspace, workspace_bytes, stream);
 }
 
 extern "C" moe_status moe_grouped_gemm_dx_swiglu_bwd_fp8(const uint8_t* A, const float* a_scale, const uint8_t* Wt,
@@ -1366,33 +1461,34 @@ extern "C" moe_status moe_grouped_gemm_dx_swiglu_bwd_fp8(const uint8_t* A, const
                                                           int64_t R, int64_t K, int64_t N, const moe_bf16* h_gate,
                                                           const moe_bf16* h_up, moe_bf16* dh_gate, moe_bf16* dh_up,
                                                           void* workspace, size_t workspace_bytes, hipStream_t stream) {
-  const char* fn = "moe_grouped_gemm_dx_swiglu_bwd_fp8";
-  if (G < 1 || G > 256) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: need 1 <= G <= 256", fn);
-  if (R < 0 || K <= 0 || N <= 0) return fail(MOE_ERROR_INVALID_VALUE, "%s: bad size", fn);
-  if (K % 64 || N % 64) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: K and N must be multiples of 64", fn);
-  if (R >= ((int64_t)1 << 31)) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: R >= 2^31", fn);
-  if (N * K >= ((int64_t)1 << 31)) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: one group's weight must be < 2 GiB", fn);
-  if (!offsets) return fail(MOE_ERROR_INVALID_VALUE, "%s: offsets is NULL", fn);
-  if (R == 0) return MOE_SUCCESS;
-  if (!A || !a_scale || !Wt || !w_scale || !h_gate || !h_up || !dh_gate || !dh_up)
-    return fail(MOE_ERROR_INVALID_VALUE, "%s: NULL pointer", fn);
-  if (bad_ptr(A) || bad_ptr(Wt) || bad_ptr(w_scale) || bad_ptr(h_gate) || bad_ptr(h_up) || bad_ptr(dh_gate) ||
-      bad_ptr(dh_up) || (reinterpret_cast<uintptr_t>(a_scale) & 3))
-    return fail(MOE_ERROR_INVALID_VALUE, "%s: pointers must be 16-byte aligned (a_scale 4-byte)", fn);
-  // the dX-shaped product (rows of A against rows of Wt[g]) with the SwiGLU-backward epilogue
-  GemmParams p{};
-  p.a = reinterpret_cast<const uint16_t*>(A);
-  p.b = reinterpret_cast<const uint16_t*>(Wt);
-  p.offsets = offsets; p.out = dh_gate; p.out2 = dh_up; p.hg = h_gate; p.hu = h_up;
-  p.a_scale = a_scale; p.w_scale = w_scale;
-  p.G = G; p.R = R; p.K = N; p.N = K;
-  constexpr int TM = Cfg<KIND_DX>::TM;
-  p.mt_bound = (int)((R + TM - 1) / TM + G);
-  p.n_tiles = (int)((N + TN - 1) / TN);
-  const int64_t tiles = (int64_t)p.mt_bound * p.n_tiles;
-  const moe_status st = attach_split(p, workspace, workspace_bytes, fn, stream);
-  if (st != MOE_SUCCESS) return st;
-  return launch<KIND_DX, false, true, false, false, true>(p, tiles, stream, "grouped_gemm_dx_swiglu_bwd_fp8");
+  return f8_product<false>("moe_grouped_gemm_dx_swiglu_bwd_fp8", F8_SWIGLU_BWD, A, a_scale, Wt, w_scale, offsets, G,
+                           R, K, N, dh_gate, dh_up, nullptr, h_gate, h_up, workspace, workspace_bytes, stream);
+}
+
+extern "C" moe_status moe_grouped_gemm_fwd_mx_gate_up(const uint8_t* A, const uint8_t* a_scale, const uint8_t* Wt,
+                                                     const uint8_t* w_scale, const int32_t* offsets, int32_t G,
+                                                     int64_t R, int64_t K, int64_t F, moe_bf16* h_gate, moe_bf16* h_up,
+                                                     moe_bf16* act, void* workspace, size_t workspace_bytes,
+                                                     hipStream_t stream) {
+  return f8_product<true>("moe_grouped_gemm_fwd_mx_gate_up", F8_GATE_UP, A, a_scale, Wt, w_scale, offsets, G, R, K,
+                          2 * F, h_gate, h_up, act, nullptr, nullptr, workspace, workspace_bytes, stream);
+}
+
+extern "C" moe_status moe_grouped_gemm_fwd_mx(const uint8_t* A, const uint8_t* a_scale, const uint8_t* Wt,
+                                             const uint8_t* w_scale, const int32_t* offsets, int32_t G, int64_t R,
+                                             int64_t K, int64_t N, moe_bf16* C, void* workspace,
+                                             size_t workspace_bytes, hipStream_t stream) {
+  return f8_product<true>("moe_grouped_gemm_fwd_mx", F8_PLAIN, A, a_scale, Wt, w_scale, offsets, G, R, K, N, C,
+                          nullptr, nullptr, nullptr, nullptr, workspace, workspace_bytes, stream);
+}
+
+extern "C" moe_status moe_grouped_gemm_dx_swiglu_bwd_mx(const uint8_t* A, const uint8_t* a_scale, const uint8_t* Wt,
+                                                        const uint8_t* w_scale, const int32_t* offsets, int32_t G,
+                                                        int64_t R, int64_t K, int64_t N, const moe_bf16* h_gate,
+                                                        const moe_bf16* h_up, moe_bf16* dh_gate, moe_bf16* dh_up,
+                                                        void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return f8_product<true>("moe_grouped_gemm_dx_swiglu_bwd_mx", F8_SWIGLU_BWD, A, a_scale, Wt, w_scale, offsets, G, R,
+                          K, N, dh_gate, dh_up, nullptr, h_gate, h_up, workspace, workspace_bytes, stream);
 }
 
 extern "C" moe_status moe_grouped_gemm_dx_split(const moe_bf16* dC, const moe_bf16* B, const moe_bf16* dC2,

@@ -48,7 +48,7 @@ class MoELayer(_Traced):
                  router: bool = False, aux_alpha: float = 0.0, dw_transposed: bool = False,
                  concurrent: bool = False, split_tail: bool = True, gather_fused: bool = False,
                  fp8_forward: bool = False, dw_persistent: bool = True, fp8_requantize: bool = True,
-                 fp8_backward: bool = False):
+                 fp8_backward: bool = False, mx: bool = False):
         self.cfg = cfg
         # fp8_forward: the routed experts' forward products run on E4M3 operands (activations
         # quantized per row each step, weights per output channel once, here): gate and up in one
@@ -63,6 +63,13 @@ class MoELayer(_Traced):
         # the 2f-long contraction.  The weight gradients stay bf16 (their contraction runs over the
         # tokens, which a per-row or per-channel scale cannot factor out)
         self.fp8_bwd = fp8_backward
+        # mx: those E4M3 products take MX block scales instead (a power of two per 32 contraction
+        # elements of every row of either operand, applied by the matrix cores): activations are
+        # quantized per 32-element block of their rows, and each weight is read once per step for
+        # both the forward and the data-gradient orientation (moe_quantize_mx_weight)
+        if mx and not (fp8_forward or fp8_backward):
+            raise ValueError("mx selects the block scales of the FP8 products: enable fp8_forward and/or fp8_backward")
+        self.mx = mx
         # gather_fused: the gate/up product reads its rows straight from x through token_of_row
         # (moe_grouped_gemm_fwd_gather); X_perm is then gathered only in the backward, for dW_gate
         # and dW_up (moe_gather_rows), so a forward alone never writes it
@@ -114,9 +121,31 @@ class MoELayer(_Traced):
                 "router_ws": e(max(16, moe.lib().moe_router_bwd_workspace_bytes(T, d, E)), torch.uint8),
                 "aux_ws": e(max(16, moe.lib().moe_router_aux_loss_workspace_bytes(T, E)), torch.uint8),
             })
-        if fp8_forward:
-            if gather_fused:
-                raise ValueError("fp8_forward reads X_perm: it does not combine with gather_fused")
+        P = moe.mx_groups
+        if fp8_forward and gather_fused:
+            raise ValueError("fp8_forward reads X_perm: it does not combine with gather_fused")
+        if fp8_backward and not fuse_swiglu_bwd:
+            raise ValueError("fp8_backward fuses the SwiGLU backward into the dX-down product")
+        if mx:
+            u8 = torch.uint8
+            if fp8_forward:
+                b.update({"x_q": e((R, d), u8), "x_s": e((P(d), R, 4), u8), "act_q": e((R, f), u8),
+                          "act_s": e((P(f), R, 4), u8)})
+            if fp8_backward:
+                b.update({"dy_q": e((R, d), u8), "dy_s": e((P(d), R, 4), u8), "dh_q": e((R, 2 * f), u8),
+                          "dh_s": e((P(2 * f), R, 4), u8)})
+            # codes and block scales of the expert weights: "_t" the forward operands [expert, output
+            # channel, contraction] (gate/up interleaved by 128 channels), "_r" the data-gradient
+            # operands in the stored layouts (W_down's rows; rows of [W_gate | W_up])
+            self.wmx = {}
+            if fp8_forward:
+                self.wmx["gate_up_t"] = (e((E, 2 * f, d), u8), e((P(d), E, 2 * f, 4), u8))
+                self.wmx["down_t"] = (e((E, d, f), u8), e((P(f), E, d, 4), u8))
+            if fp8_backward:
+                self.wmx["gate_up_r"] = (e((E, d, 2 * f), u8), e((P(2 * f), E, d, 4), u8))
+                self.wmx["down_r"] = (e((E, f, d), u8), e((P(d), E, f, 4), u8))
+            self._quantize_weights_mx()
+        elif fp8_forward:
             u8 = torch.uint8
             b.update({"x_q": e((R, d), u8), "x_s": e(R, f32), "act_q": e((R, f), u8), "act_s": e(R, f32)})
             # weights in the layout [expert, output channel, contraction], quantized per channel
@@ -129,9 +158,7 @@ class MoELayer(_Traced):
             }
             self._quantize_weights()
         self.fp8_requantize = fp8_requantize
-        if fp8_backward:
-            if not fuse_swiglu_bwd:
-                raise ValueError("fp8_backward fuses the SwiGLU backward into the dX-down product")
+        if fp8_backward and not mx:
             u8 = torch.uint8
             b.update({"dy_q": e((R, d), u8), "dy_s": e(R, f32), "dh_q": e((R, 2 * f), u8), "dh_s": e(R, f32)})
             self.w8b = {
@@ -156,6 +183,17 @@ class MoELayer(_Traced):
         i, w8 = self.inp, self.w8
         moe.moe_quantize_fp8_weight(i["w_gate"], i["w_up"], *w8["gate_up"], stream=stream)
         moe.moe_quantize_fp8_weight(i["w_down"], None, *w8["down"], stream=stream)
+
+    def _quantize_weights_mx(self, stream=None):
+        """MX codes and block scales of the expert weights, every orientation the enabled products
+        read, from one pass over each weight."""
+        i, w = self.inp, self.wmx
+        for src, src2, t, r in ((i["w_gate"], i["w_up"], "gate_up_t", "gate_up_r"),
+                                (i["w_down"], None, "down_t", "down_r")):
+            qt, st = w.get(t, (None, None))
+            qr, sr = w.get(r, (None, None))
+            moe.moe_quantize_mx_weight(src, src2, want_t=qt is not None, want_r=qr is not None, qt=qt, st=st,
+                                       qr=qr, sr=sr, stream=stream)
 
     def _quantize_weights_bwd(self, stream=None):
         """E4M3 codes and per-row scales of the expert weights in their stored layouts, the
@@ -203,7 +241,17 @@ class MoELayer(_Traced):
         if self.router and self.aux_alpha:
             run("router_aux_loss", moe.moe_router_aux_loss, logits, b["offsets"], k, self.aux_alpha,
                 loss=b["aux_loss"], workspace=b["aux_ws"], stream=stream)
-        if self.fp8:
+        if self.fp8 and self.mx:
+            ws = self.split_ws
+            if self.fp8_requantize:
+                run("quantize_w", self._quantize_weights_mx, stream=stream)
+            run("quantize_x", moe.moe_quantize_mx_rows, b["x_perm"], None, b["x_q"], b["x_s"], stream=stream)
+            run("fwd_gate_up", moe.moe_grouped_gemm_fwd_mx_gate_up, b["x_q"], b["x_s"], *self.wmx["gate_up_t"],
+                b["offsets"], b["h_gate"], b["h_up"], b["act"], stream=stream, workspace=ws)
+            run("quantize_act", moe.moe_quantize_mx_rows, b["act"], None, b["act_q"], b["act_s"], stream=stream)
+            run("fwd_down", moe.moe_grouped_gemm_fwd_mx, b["act_q"], b["act_s"], *self.wmx["down_t"], b["offsets"],
+                C=b["y_perm"], stream=stream, workspace=ws)
+        elif self.fp8:
             ws = self.split_ws
             if self.fp8_requantize:
                 run("quantize_w", self._quantize_weights, stream=stream)
@@ -270,7 +318,14 @@ class MoELayer(_Traced):
         else:
             run("dw_down", moe.moe_grouped_gemm_dw, b["act"], b["dy_perm"], b["offsets"], dB=b["dw_down"],
                 stream=side, counters=self.dw_cnt)
-        if self.fp8_bwd:
+        if self.fp8_bwd and self.mx:
+            if self.fp8_requantize and not self.fp8:   # else the forward's pass wrote both orientations
+                run("quantize_w_bwd", self._quantize_weights_mx, stream=stream)
+            run("quantize_dy", moe.moe_quantize_mx_rows, b["dy_perm"], None, b["dy_q"], b["dy_s"], stream=stream)
+            run("dx_down_swiglu_bwd", moe.moe_grouped_gemm_dx_swiglu_bwd_mx, b["dy_q"], b["dy_s"],
+                *self.wmx["down_r"], b["offsets"], b["h_gate"], b["h_up"], b["dh_gate"], b["dh_up"], stream=stream,
+                workspace=self.split_ws)
+        elif self.fp8_bwd:
             if self.fp8_requantize:
                 run("quantize_w_bwd", self._quantize_weights_bwd, stream=stream)
             run("quantize_dy", moe.moe_quantize_fp8_rows, b["dy_perm"], b["dy_q"], b["dy_s"], stream=stream)
@@ -287,7 +342,12 @@ class MoELayer(_Traced):
             run("swiglu_bwd", moe.moe_swiglu_bwd, b["h_gate"], b["h_up"], b["d_act"], b["dh_gate"],
                 b["dh_up"], stream=stream)
         self._join(side, main)            # dW_gate/dW_up need dH
-        if self.fp8_bwd:
+        if self.fp8_bwd and self.mx:
+            run("quantize_dh", moe.moe_quantize_mx_rows, b["dh_gate"], b["dh_up"], b["dh_q"], b["dh_s"],
+                stream=stream)
+            run("dx_gate_up", moe.moe_grouped_gemm_fwd_mx, b["dh_q"], b["dh_s"], *self.wmx["gate_up_r"],
+                b["offsets"], C=b["dx_perm"], stream=stream, workspace=self.split_ws)
+        elif self.fp8_bwd:
             run("quantize_dh", moe.moe_quantize_fp8_rows2, b["dh_gate"], b["dh_up"], b["dh_q"], b["dh_s"],
                 stream=stream)
             run("dx_gate_up", moe.moe_grouped_gemm_fwd_fp8, b["dh_q"], b["dh_s"], *self.w8b["gate_up"], b["offsets"],
@@ -345,13 +405,18 @@ class MoELayer(_Traced):
         c = self.cfg
         T, d, f, k, E = c.T, c.d, c.f, c.k, c.E
         R = T * k
+        # per-row scale bytes: one fp32, or (MX) one byte per 32 elements
+        sc = (lambda n: n // 32) if self.mx else (lambda n: 4)
+        n_or = (1 if self.fp8 else 0) + (1 if self.fp8_bwd else 0)   # weight orientations written
         w = {
             "route_permute": ("bytes", T * E * 4 + T * k * 8 + R * 8
                               + (0 if self.gather_fused else T * d * 2 + R * d * 2)),
             "gather_x": ("bytes", T * d * 2 + R * d * 2 + R * 4),
             # FP8 forward: E4M3 products (8-bit MFMA work), quantizers and the standalone SwiGLU
-            "quantize_x": ("bytes", R * d * 3 + R * 4), "quantize_act": ("bytes", R * f * 3 + R * 4),
-            "quantize_w": ("bytes", 3 * E * d * f * 3 + 3 * E * (d + f) * 4),   # read bf16, write codes
+            "quantize_x": ("bytes", R * d * 3 + R * sc(d)), "quantize_act": ("bytes", R * f * 3 + R * sc(f)),
+            # read bf16, write codes (MX: both orientations a step needs, from one read)
+            "quantize_w": ("bytes", (3 * E * d * f * (2 + n_or) + n_or * 3 * E * d * f // 32) if self.mx
+                           else (3 * E * d * f * 3 + 3 * E * (d + f) * 4)),
             "fwd_gate_up": ("flops8" if self.fp8 else "flops", 4 * R * d * f),
             "fwd_down": ("flops8" if self.fp8 else "flops", 2 * R * f * d),
             "combine": ("bytes", R * d * 2 + T * d * 2 + T * k * 8 + (T * d * 2 if self.shared else 0)),
@@ -359,8 +424,9 @@ class MoELayer(_Traced):
             "dx_down": ("flops", 2 * R * d * f), "dw_down": ("flops", 2 * R * f * d),
             "dx_down_swiglu_bwd": ("flops8" if self.fp8_bwd else "flops", 2 * R * d * f),
             # FP8 backward: dY_perm and [dH_gate | dH_up] per row, the weights in their stored layouts
-            "quantize_dy": ("bytes", R * d * 3 + R * 4), "quantize_dh": ("bytes", 2 * R * f * 3 + R * 4),
-            "quantize_w_bwd": ("bytes", 3 * E * d * f * 3 + E * (d + f) * 4),
+            "quantize_dy": ("bytes", R * d * 3 + R * sc(d)), "quantize_dh": ("bytes", 2 * R * f * 3 + R * sc(2 * f)),
+            "quantize_w_bwd": ("bytes", (3 * E * d * f * 3 + 3 * E * d * f // 32) if self.mx
+                               else (3 * E * d * f * 3 + E * (d + f) * 4)),
             "swiglu_bwd": ("bytes", 5 * R * f * 2),
             "dx_gate_up": ("flops8" if self.fp8_bwd else "flops", 4 * R * d * f),
             "dw_gate_up": ("flops", 4 * R * d * f),

@@ -53,6 +53,15 @@ _SIG = {
                                                 ctypes.c_size_t, _P]),
     "moe_grouped_gemm_fwd_fp8_gate_up": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P, _P,
                                                         ctypes.c_size_t, _P]),
+    "moe_mx_scale_bytes": (_I64, [_I64, _I64]),
+    "moe_quantize_mx_rows": (ctypes.c_int, [_P, _P, _I64, _I64, _P, _P, _P]),
+    "moe_quantize_mx_weight": (ctypes.c_int, [_P, _P, _I64, _I64, _I64, _P, _P, _P, _P, _P]),
+    "moe_grouped_gemm_fwd_mx": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P,
+                                               ctypes.c_size_t, _P]),
+    "moe_grouped_gemm_fwd_mx_gate_up": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P, _P,
+                                                       ctypes.c_size_t, _P]),
+    "moe_grouped_gemm_dx_swiglu_bwd_mx": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P,
+                                                         _P, _P, ctypes.c_size_t, _P]),
     "moe_swiglu": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _P]),
     "moe_swiglu_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _I64, _I64, _P]),
     "moe_unpermute_combine": (ctypes.c_int, [_P, _P, _P, _P, _I64, _I64, _I32, _P, _P]),
@@ -404,6 +413,150 @@ def moe_grouped_gemm_fwd_fp8_gate_up(A, a_scale, Wt_gu, w_scale_gu, offsets, h_g
                                                 0 if workspace is None else workspace.numel(), _stream(stream))
     _check("moe_grouped_gemm_fwd_fp8_gate_up", st)
     return h_gate, h_up, act
+
+
+def mx_groups(C):
+    """128-element scale groups of a row of C elements (the leading extent of an MX scale array)."""
+    return (C + 127) // 128
+
+
+def mx_scales_by_row(s, C):
+    """An MX scale array [groups, *rows, 4] (the library's layout) as [*rows, C/32]: block b of a row
+    in column b (a view-and-copy for inspection and tests; the kernels read the first form)."""
+    t = s.movedim(0, -2)
+    return t.reshape(t.shape[:-2] + (t.shape[-2] * 4,))[..., : C // 32].contiguous()
+
+
+def mx_scales_from_rows(sb, C, pad=0):
+    """[*rows, C/32] scale bytes -> the library's MX scale array [groups, *rows, 4] (padding bytes
+    set to `pad`)."""
+    P = mx_groups(C)
+    out = torch.full(sb.shape[:-1] + (4 * P,), pad, dtype=torch.uint8, device=sb.device)
+    out[..., : C // 32] = sb
+    return out.reshape(sb.shape[:-1] + (P, 4)).movedim(-2, 0).contiguous()
+
+
+def moe_quantize_mx_rows(x, x2=None, q=None, scale=None, stream=None):
+    """MX codes [.., C] and E8M0 block scales (the MX scale layout, [ceil(C/128), .., 4]) of the rows
+    of x, or of the joined rows [x | x2] (C = 2K) when x2 is given."""
+    K = x.shape[-1]
+    M = x.numel() // K
+    for t, n in ((x, "x"), (x2, "x2")):
+        if t is not None and (t.dtype != torch.bfloat16 or not t.is_contiguous()):
+            raise ValueError(f"{n} must be a contiguous bf16 tensor")
+    if x2 is not None and tuple(x2.shape) != tuple(x.shape):
+        raise ValueError("x and x2 must have one shape")
+    C = 2 * K if x2 is not None else K
+    qshape = tuple(x.shape[:-1]) + (C,)
+    sshape = (mx_groups(C),) + tuple(x.shape[:-1]) + (4,)
+    q = torch.empty(qshape, dtype=torch.uint8, device=x.device) if q is None else q
+    scale = torch.empty(sshape, dtype=torch.uint8, device=x.device) if scale is None else scale
+    _need(q, torch.uint8, qshape, "q")
+    _need(scale, torch.uint8, sshape, "scale")
+    _check("moe_quantize_mx_rows",
+           lib().moe_quantize_mx_rows(_ptr(x), _ptr(x2), M, K, _ptr(q), _ptr(scale), _stream(stream)))
+    return q, scale
+
+
+def moe_quantize_mx_weight(w, w2=None, want_t=True, want_r=True, qt=None, st=None, qr=None, sr=None,
+                           stream=None):
+    """MX codes and block scales of a weight [G, K, N] in both orientations from one read:
+    (qt [G, N', K], st [ceil(K/128), G, N', 4]) the forward operand (N' = 2N with w2, channels
+    interleaved by 128) and (qr [G, K, N''], sr [ceil(N''/128), G, K, 4]) the data-gradient operand
+    (N'' = 2N with w2: rows [W | W2]).  Returns (qt, st, qr, sr), None for an orientation not asked
+    for."""
+    G, K, N = w.shape
+    _need(w, torch.bfloat16, (G, K, N), "w")
+    _need(w2, torch.bfloat16, (G, K, N), "w2")
+    if not w.is_contiguous() or (w2 is not None and not w2.is_contiguous()):
+        raise ValueError("w and w2 must be contiguous")
+    n2 = 2 * N if w2 is not None else N
+    dev = w.device
+    if want_t:
+        qt = torch.empty((G, n2, K), dtype=torch.uint8, device=dev) if qt is None else qt
+        st = torch.empty((mx_groups(K), G, n2, 4), dtype=torch.uint8, device=dev) if st is None else st
+        _need(qt, torch.uint8, (G, n2, K), "qt")
+        _need(st, torch.uint8, (mx_groups(K), G, n2, 4), "st")
+    else:
+        qt = st = None
+    if want_r:
+        qr = torch.empty((G, K, n2), dtype=torch.uint8, device=dev) if qr is None else qr
+        sr = torch.empty((mx_groups(n2), G, K, 4), dtype=torch.uint8, device=dev) if sr is None else sr
+        _need(qr, torch.uint8, (G, K, n2), "qr")
+        _need(sr, torch.uint8, (mx_groups(n2), G, K, 4), "sr")
+    else:
+        qr = sr = None
+    _check("moe_quantize_mx_weight",
+           lib().moe_quantize_mx_weight(_ptr(w), _ptr(w2), G, K, N, _ptr(qt), _ptr(st), _ptr(qr), _ptr(sr),
+                                        _stream(stream)))
+    return qt, st, qr, sr
+
+
+def _need_mx(A, a_scale, Wt, w_scale, offsets):
+    R, K = A.shape
+    G, N, K2 = Wt.shape
+    if K2 != K:
+        raise ValueError("A and Wt disagree on K")
+    P = mx_groups(K)
+    _need(A, torch.uint8, (R, K), "A")
+    _need(a_scale, torch.uint8, (P, R, 4), "a_scale")
+    _need(Wt, torch.uint8, (G, N, K), "Wt")
+    _need(w_scale, torch.uint8, (P, G, N, 4), "w_scale")
+    _need(offsets, torch.int32, (G + 1,), "offsets")
+    return R, K, G, N
+
+
+def moe_grouped_gemm_fwd_mx(A, a_scale, Wt, w_scale, offsets, C=None, stream=None, workspace=None):
+    """C = A . Wt[g]^T per group on MX operands (E4M3 codes with E8M0 scales per 32 of K, in the MX
+    scale layout: a_scale [ceil(K/128), R, 4], w_scale [ceil(K/128), G, N, 4]), bf16."""
+    R, K, G, N = _need_mx(A, a_scale, Wt, w_scale, offsets)
+    C = torch.empty((R, N), dtype=torch.bfloat16, device=A.device) if C is None else C
+    _need(C, torch.bfloat16, (R, N), "C")
+    st = lib().moe_grouped_gemm_fwd_mx(_ptr(A), _ptr(a_scale), _ptr(Wt), _ptr(w_scale), _ptr(offsets), G, R, K, N,
+                                       _ptr(C), _ptr(workspace), 0 if workspace is None else workspace.numel(),
+                                       _stream(stream))
+    _check("moe_grouped_gemm_fwd_mx", st)
+    return C
+
+
+def moe_grouped_gemm_fwd_mx_gate_up(A, a_scale, Wt_gu, w_scale_gu, offsets, h_gate=None, h_up=None, act=None,
+                                    want_act=True, stream=None, workspace=None):
+    """Gate and up projections on MX operands from one weight interleaved by 128 channels, + SwiGLU."""
+    R, K, G, F2 = _need_mx(A, a_scale, Wt_gu, w_scale_gu, offsets)
+    if F2 % 256:
+        raise ValueError("bad shapes")
+    F = F2 // 2
+    dev = A.device
+    h_gate = torch.empty((R, F), dtype=torch.bfloat16, device=dev) if h_gate is None else h_gate
+    h_up = torch.empty((R, F), dtype=torch.bfloat16, device=dev) if h_up is None else h_up
+    if want_act and act is None:
+        act = torch.empty((R, F), dtype=torch.bfloat16, device=dev)
+    for t, n in ((h_gate, "h_gate"), (h_up, "h_up"), (act, "act")):
+        _need(t, torch.bfloat16, (R, F), n)
+    st = lib().moe_grouped_gemm_fwd_mx_gate_up(_ptr(A), _ptr(a_scale), _ptr(Wt_gu), _ptr(w_scale_gu), _ptr(offsets),
+                                               G, R, K, F, _ptr(h_gate), _ptr(h_up), _ptr(act), _ptr(workspace),
+                                               0 if workspace is None else workspace.numel(), _stream(stream))
+    _check("moe_grouped_gemm_fwd_mx_gate_up", st)
+    return h_gate, h_up, act
+
+
+def moe_grouped_gemm_dx_swiglu_bwd_mx(A, a_scale, Wt, w_scale, offsets, h_gate, h_up, dh_gate=None, dh_up=None,
+                                      stream=None, workspace=None):
+    """dA = A . Wt[g]^T on MX operands (bf16) and its SwiGLU backward: (dh_gate, dh_up) from
+    h_gate, h_up [R, N]."""
+    R, K, G, N = _need_mx(A, a_scale, Wt, w_scale, offsets)
+    _need(h_gate, torch.bfloat16, (R, N), "h_gate")
+    _need(h_up, torch.bfloat16, (R, N), "h_up")
+    dh_gate = torch.empty((R, N), dtype=torch.bfloat16, device=A.device) if dh_gate is None else dh_gate
+    dh_up = torch.empty((R, N), dtype=torch.bfloat16, device=A.device) if dh_up is None else dh_up
+    _need(dh_gate, torch.bfloat16, (R, N), "dh_gate")
+    _need(dh_up, torch.bfloat16, (R, N), "dh_up")
+    st = lib().moe_grouped_gemm_dx_swiglu_bwd_mx(_ptr(A), _ptr(a_scale), _ptr(Wt), _ptr(w_scale), _ptr(offsets), G,
+                                                 R, K, N, _ptr(h_gate), _ptr(h_up), _ptr(dh_gate), _ptr(dh_up),
+                                                 _ptr(workspace), 0 if workspace is None else workspace.numel(),
+                                                 _stream(stream))
+    _check("moe_grouped_gemm_dx_swiglu_bwd_mx", st)
+    return dh_gate, dh_up
 
 
 def moe_swiglu(h_gate, h_up, act=None, stream=None):

@@ -33,6 +33,8 @@ def test_traffic_is_reported_only_for_the_measured_code(monkeypatch):
         assert bench.measured_traffic(call, bench.TRAFFIC_CONFIG + 1) is None   # another workload
         monkeypatch.setattr(bench, "TRAFFIC_SOURCES", dict(src, **{group: (files, "0" * 16)}))
         assert bench.measured_traffic(call, bench.TRAFFIC_CONFIG) is None        # the kernels changed since
+        monkeypatch.setattr(bench, "TRAFFIC_SOURCES", src)
+        assert bench.measured_traffic(call, bench.TRAFFIC_CONFIG, variant=True) is None   # other kernels
     assert bench.measured_traffic("no_such_call", bench.TRAFFIC_CONFIG) is None
 
 
@@ -43,7 +45,7 @@ def test_measured_traffic_covers_every_layer_call():
     lay = object.__new__(MoELayer)
     lay.cfg, lay.fp8, lay.gather_fused, lay.shared = W.CONFIGS[bench.TRAFFIC_CONFIG], False, False, False
     lay.router_fused_dx = False
-    lay.fp8_bwd = False
+    lay.fp8_bwd = lay.mx = False
     work = lay.work()
     c = lay.cfg
     R = c.T * c.k
