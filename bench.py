@@ -107,6 +107,8 @@ def _args():
     ap.add_argument("--fp8-fixed-weights", action="store_true",
                     help="with --fp8-forward/--fp8-backward: quantize the weights once (held fixed), not every step")
     ap.add_argument("--forward-only", action="store_true", help="time the forward alone (a variant)")
+    ap.add_argument("--combine-fused", action="store_true",
+                    help="the weighted combine in the down product's epilogue (a variant)")
     ap.add_argument("--gather-fused", action="store_true",
                     help="gate/up product reads x through token_of_row; X_perm is gathered in the backward")
     ap.add_argument("--no-split-tail", action="store_true",
@@ -396,6 +398,7 @@ def main():
                          dw_transposed=a.dw_transposed, concurrent=a.concurrent, split_tail=not a.no_split_tail,
                          gather_fused=a.gather_fused, fp8_forward=a.fp8_forward,
                          fp8_backward=a.fp8_backward, fp8_requantize=not a.fp8_fixed_weights, mx=a.mx,
+                         combine_fused=a.combine_fused,
                          dw_persistent=not a.dw_one_per_tile)
     torch.cuda.synchronize()
     t_gen = time.perf_counter() - t_gen
@@ -440,7 +443,7 @@ def main():
     calls = {}
     gemm_ms = gemm_flops = 0.0
     variant = (a.fp8_forward or a.fp8_backward or a.gather_fused or a.dw_transposed or a.no_split_tail
-               or a.dw_one_per_tile or a.concurrent)
+               or a.dw_one_per_tile or a.concurrent or a.combine_fused)
     for name, ts in per.items():
         avg = sum(ts) / len(ts)
         kind, amount = work[name]
@@ -524,6 +527,7 @@ def main():
                    + (", MX block scales (E8M0 per 32 contraction elements)" if a.mx else "")
                    + (", FP8 weights quantized once (held fixed)" if a.fp8_fixed_weights else "")
                    + (", gather fused into the gate/up product" if a.gather_fused else "")
+                   + (", combine fused into the down product" if a.combine_fused else "")
                    + (", dW from contraction-major copies" if a.dw_transposed else "")
                    + (", no split tail" if a.no_split_tail else "")
                    + (", dW one workgroup per tile" if a.dw_one_per_tile else "")

@@ -169,6 +169,31 @@ moe_status moe_unpermute_combine(const moe_bf16* y_perm, const float* topk_w,
                                  int64_t d, int32_t k, moe_bf16* y, hipStream_t stream);
 
 /*
+ * Steps D + E in one call: the down product of moe_grouped_gemm_fwd (single B, no SwiGLU) with
+ * the weighted combine of moe_unpermute_combine fused into its epilogue.  y_perm [R, N] =
+ * bf16(A . B[g]) is stored as by moe_grouped_gemm_fwd (the backward's d_topk_w reads it), and
+ * y [T, N] = bf16(sum_j topk_w[t,j] * y_perm[row_of_slot[t*k+j], :] + add[t, :]) bit for bit as
+ * moe_unpermute_combine computes it: each tile stores its rows of y_perm (written through to
+ * memory, agent-coherent), then counts one arrival per row for the (token, 256-column tile)
+ * pair; the tile that brings a pair's count to k computes those 256 columns of the token's Y row
+ * from the k stored rows, in slot order (a tile stores all its rows before it counts any, so the
+ * count reaches k only once every row is in memory).  R == T * k; topk_w [T, k] fp32,
+ * row_of_slot [T*k] and token_of_row [R] int32 as moe_route_permute returns them; add [T, N]
+ * bf16 or NULL.  count_workspace: moe_grouped_gemm_fwd_combine_workspace_bytes(T, N) bytes,
+ * 4-byte aligned (zeroed here, on `stream`); split_workspace: NULL or a split workspace as for
+ * moe_grouped_gemm_fwd_split.  Errors as moe_grouped_gemm_fwd; R != T*k -> INVALID_VALUE; a short
+ * count workspace -> WORKSPACE; R * N * 2 >= 2^31 -> NOT_SUPPORTED.  Not the layer's default:
+ * the coherent stores cost more than the separate combine saves (measured).
+ */
+size_t moe_grouped_gemm_fwd_combine_workspace_bytes(int64_t T, int64_t N);
+moe_status moe_grouped_gemm_fwd_combine(const moe_bf16* A, const moe_bf16* B, const int32_t* offsets, int32_t G,
+                                        int64_t R, int64_t K, int64_t N, const float* topk_w,
+                                        const int32_t* row_of_slot, const int32_t* token_of_row, int64_t T,
+                                        int32_t k, const moe_bf16* add, moe_bf16* y_perm, moe_bf16* y,
+                                        void* count_workspace, size_t count_workspace_bytes, void* split_workspace,
+                                        size_t split_workspace_bytes, hipStream_t stream);
+
+/*
  * Backward of the weighted combine (the routing weight is applied while permuting dY):
  *   dy_perm[row_of_slot[t*k+j], :] = bf16(w[t,j] * dy[t, :])
  *   d_topk_w[t, j] = sum_c dy[t,c] * y_perm[row_of_slot[t*k+j], c]   (fp32; skipped if y_perm or

@@ -23,6 +23,8 @@
 // two sources at the same output columns; each wave's 128 N-columns are 64 from each source, so the
 // accumulators for the same (row, column) of both products sit in the same lane, which is what
 // the fused SwiGLU epilogue needs.  DX dual mode appends the second pair to the contraction.
+#include <type_traits>
+
 #include "common.h"
 
 namespace moe {
@@ -78,6 +80,14 @@ struct GemmParams {
   const uint8_t* w_mx;     //              ... of the weight's rows [C/128][G*K][4]
   int64_t mx_a_step, mx_w_step;   //       bytes from one 128-element group of scales to the next
   int* tile_queue;         // DW, persistent: 8 tile-claim counters, one per XCD (zero at launch)
+  int* comb_cnt;           // FWD single output, fused combine: arrival counters [T, n_tiles] (zero
+                           //   at launch); NULL: no combine
+  const float* comb_w;     //   routing weights [T, k]
+  const int32_t* comb_ros; //   row_of_slot [T * k]
+  const int32_t* comb_tor; //   token_of_row [R]
+  const uint16_t* comb_add;//   added to every Y row (shared FFN output) [T, N], or NULL
+  uint16_t* comb_y;        //   Y [T, N]
+  int comb_k;
 };
 
 typedef int i32x4 __attribute__((ext_vector_type(4)));
@@ -125,6 +135,10 @@ __device__ __forceinline__ void dma4(i32x4 rsrc, int voff, int lds_addr) {
                : "v"(voff), "s"(rsrc), "s"(lds_addr)
                : "memory", "m0");
 }
+
+// Cache-policy bit of buffer accesses: agent-scope coherent (sc1), i.e. written through to / read
+// past the per-XCD L2s, which are not coherent with each other.
+constexpr int CP_SC1 = 16;
 
 template <int N>
 __device__ __forceinline__ void wait_vm() {
@@ -208,6 +222,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
   constexpr int DPW_T = DPW_M + DPW_N;
   constexpr int OPS = DPW_T + (MX ? 1 : 0);   // DMA loads per wave per stage (MX: + the scales)
   constexpr bool FSCALE = F8 && !MX;          // fp32 row/column scales applied in the epilogue
+  constexpr bool FUSE_COMBINE = KIND == KIND_FWD && !DUAL && !ACT && !GATHER;   // may fuse the combine
   static_assert(DPW_M * NWAVE * 16 == TM && DPW_N * NWAVE * 16 == TN, "DMA split");
   constexpr int WTM = TM / WAVES_M;           // per-wave tile rows
   constexpr int WTN = TN / WAVES_N;           // per-wave tile columns
@@ -1003,18 +1018,85 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
           uint16_t* dst = static_cast<uint16_t*>(p.out) + obase + n;
           constexpr int RPP = NT / 32, PASSES = TM / RPP, UB = 8;
           static_assert(PASSES % UB == 0, "batches of passes");
+          // fused combine: the rows are stored agent-coherent (sc1: through to memory), since the
+          // tile that completes a token's combine may run on another XCD
+          auto store_rows = [&](auto coherent) {
+            const __amdgpu_buffer_rsrc_t ys = __builtin_amdgcn_make_buffer_rsrc(dst + row_lo * W, 0, TM * (int)W * 2,
+                                                                                0x00020000);
 #pragma unroll
-          for (int b = 0; b < PASSES; b += UB) {
-            if (row_lo + b * RPP >= row_hi) break;   // uniform
-            u32x4 v[UB];
+            for (int b = 0; b < PASSES; b += UB) {
+              if (row_lo + b * RPP >= row_hi) break;   // uniform
+              u32x4 v[UB];
 #pragma unroll
-            for (int u = 0; u < UB; ++u) v[u] = chunk((tid >> 5) + (b + u) * RPP, c);
+              for (int u = 0; u < UB; ++u) v[u] = chunk((tid >> 5) + (b + u) * RPP, c);
 #pragma unroll
-            for (int u = 0; u < UB; ++u) asm volatile("" : "+v"(v[u]));
+              for (int u = 0; u < UB; ++u) asm volatile("" : "+v"(v[u]));
 #pragma unroll
-            for (int u = 0; u < UB; ++u) {
-              const int64_t r = row_lo + (tid >> 5) + (b + u) * RPP;
-              if (r < row_hi) *reinterpret_cast<u32x4*>(dst + r * W) = v[u];
+              for (int u = 0; u < UB; ++u) {
+                const int t = (tid >> 5) + (b + u) * RPP;
+                const int64_t r = row_lo + t;
+                if (r < row_hi) {
+                  if constexpr (decltype(coherent)::value)
+                    __builtin_amdgcn_raw_buffer_store_b128(v[u], ys, (int)(t * W * 2), 0, CP_SC1);
+                  else
+                    *reinterpret_cast<u32x4*>(dst + r * W) = v[u];
+                }
+              }
+            }
+          };
+          if (FUSE_COMBINE && p.comb_cnt != nullptr) store_rows(std::true_type{});
+          else store_rows(std::false_type{});
+        }
+      }
+      if constexpr (FUSE_COMBINE) {
+        if (p.comb_cnt != nullptr) {   // uniform
+          // The weighted combine (section 5.4's step E) fused: once this tile's Y_perm rows have
+          // all been stored, each of its rows counts one arrival for its (token, column tile); the
+          // tile whose arrival brings a pair's count to k sums that token's k rows of these 256
+          // columns in slot order (read agent-coherent), adds the shared output and stores Y --
+          // the arithmetic of moe_unpermute_combine, so Y is bitwise the two-call result.  No
+          // tile waits for another.
+          __shared__ int s_last[TM];
+          __shared__ int s_nlast;
+          wait_vm<0>();
+          if (tid == 0) s_nlast = 0;
+          __syncthreads();
+          for (int t = tid; t < TM; t += NT) {
+            const int64_t r = row_lo + t;
+            if (r < row_hi) {
+              const int tok = p.comb_tor[r];
+              const int old = __hip_atomic_fetch_add(p.comb_cnt + (int64_t)tok * p.n_tiles + nt, 1,
+                                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              if (old == p.comb_k - 1) s_last[atomicAdd(&s_nlast, 1)] = tok;
+            }
+          }
+          __syncthreads();
+          const int nl = s_nlast;
+          if (n < W) {
+            const __amdgpu_buffer_rsrc_t yp =
+                __builtin_amdgcn_make_buffer_rsrc(static_cast<uint16_t*>(p.out), 0, (int)(p.R * W * 2), 0x00020000);
+            for (int i = tid >> 5; i < nl; i += NT / 32) {
+              const int64_t tok = s_last[i];
+              float acc[8];
+#pragma unroll
+              for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+              for (int j = 0; j < p.comb_k; ++j) {
+                const int64_t rj = p.comb_ros[tok * p.comb_k + j];
+                const float wj = p.comb_w[tok * p.comb_k + j];
+                const u32x4 v = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                              yp, (int)((rj * W + n) * 2), 0, CP_SC1));
+                float f[8];
+                unpack8(v, f);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) acc[e] += wj * f[e];
+              }
+              if (p.comb_add) {
+                float f[8];
+                unpack8(*reinterpret_cast<const u32x4*>(p.comb_add + tok * W + n), f);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) acc[e] += f[e];
+              }
+              *reinterpret_cast<u32x4*>(p.comb_y + tok * W + n) = pack8(acc);
             }
           }
         }
@@ -1136,7 +1218,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
       // before the piece is counted, and the reads start after the count was seen.  A device-scope
       // fence would do the same by writing back and invalidating the whole L2 of the XCD, which
       // measured 3-4% slower on the whole product.
-      constexpr int SC1 = 16;   // cache-policy bit: agent-scope coherent
+      constexpr int SC1 = CP_SC1;
       auto off_of = [&](int i, int j, int q4) { return (((i * NB + j) * 4 + q4) * SLOT + tid * 4) * 4; };
       {
         const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(part_of(u), 0, TM * TN * 4, 0x00020000);
@@ -1264,10 +1346,23 @@ using namespace moe;
 
 namespace moe {
 namespace {
+// The combine fused into the single-output forward product (moe_grouped_gemm_fwd_combine).
+struct FusedCombine {
+  int* cnt;
+  const float* w;
+  const int32_t* row_of_slot;
+  const int32_t* token_of_row;
+  const moe_bf16* add;
+  moe_bf16* y;
+  int64_t T;
+  int k;
+};
+
 moe_status grouped_gemm_fwd_impl(const moe_bf16* A, const moe_bf16* B, const moe_bf16* B2, const int32_t* offsets,
                                  int32_t G, int64_t R, int64_t K, int64_t N, moe_bf16* C, moe_bf16* C2,
                                  moe_bf16* act, void* ws, size_t ws_bytes, hipStream_t stream,
-                                 const int32_t* gather = nullptr, int64_t gather_rows = 0) {
+                                 const int32_t* gather = nullptr, int64_t gather_rows = 0,
+                                 const FusedCombine* fc = nullptr) {
   if (G < 1 || G > 256) return fail(MOE_ERROR_NOT_SUPPORTED, "moe_grouped_gemm_fwd: need 1 <= G <= 256");
   if (R < 0 || K <= 0 || N <= 0) return fail(MOE_ERROR_INVALID_VALUE, "moe_grouped_gemm_fwd: bad size");
   if (K % 64 || N % 64) return fail(MOE_ERROR_NOT_SUPPORTED, "moe_grouped_gemm_fwd: K and N must be multiples of 64");
@@ -1291,6 +1386,15 @@ moe_status grouped_gemm_fwd_impl(const moe_bf16* A, const moe_bf16* B, const moe
   const int64_t tiles = (int64_t)p.mt_bound * p.n_tiles;   // upper bound; exact count on device
   const moe_status st = attach_split(p, ws, ws_bytes, "moe_grouped_gemm_fwd", stream);
   if (st != MOE_SUCCESS) return st;
+  if (fc) {
+    p.comb_cnt = fc->cnt; p.comb_w = fc->w; p.comb_ros = fc->row_of_slot; p.comb_tor = fc->token_of_row;
+    p.comb_add = fc->add; p.comb_y = fc->y; p.comb_k = fc->k;
+    const int64_t ncnt = fc->T * p.n_tiles;
+    zero_i32_kernel<<<(unsigned)((ncnt + 255) / 256), 256, 0, stream>>>(fc->cnt, (int)ncnt);
+    const moe_status zs = check_launch("moe_grouped_gemm_fwd_combine");
+    if (zs != MOE_SUCCESS) return zs;
+    return launch<KIND_FWD, false, false>(p, tiles, stream, "grouped_gemm_fwd(combine)");
+  }
   if (gather) {
     if (B2 && act) return launch<KIND_FWD, true, true, false, true>(p, tiles, stream, "grouped_gemm_fwd(gather,dual,swiglu)");
     if (B2) return launch<KIND_FWD, true, false, false, true>(p, tiles, stream, "grouped_gemm_fwd(gather,dual)");
@@ -1308,6 +1412,35 @@ extern "C" moe_status moe_grouped_gemm_fwd(const moe_bf16* A, const moe_bf16* B,
                                            int64_t N, moe_bf16* C, moe_bf16* C2, moe_bf16* act,
                                            hipStream_t stream) {
   return grouped_gemm_fwd_impl(A, B, B2, offsets, G, R, K, N, C, C2, act, nullptr, 0, stream);
+}
+
+extern "C" size_t moe_grouped_gemm_fwd_combine_workspace_bytes(int64_t T, int64_t N) {
+  return T <= 0 || N <= 0 ? 0 : (size_t)T * (size_t)((N + TN - 1) / TN) * sizeof(int);
+}
+
+extern "C" moe_status moe_grouped_gemm_fwd_combine(const moe_bf16* A, const moe_bf16* B, const int32_t* offsets,
+                                                   int32_t G, int64_t R, int64_t K, int64_t N, const float* topk_w,
+                                                   const int32_t* row_of_slot, const int32_t* token_of_row,
+                                                   int64_t T, int32_t k, const moe_bf16* add, moe_bf16* y_perm,
+                                                   moe_bf16* y, void* count_workspace, size_t count_workspace_bytes,
+                                                   void* split_workspace, size_t split_workspace_bytes,
+                                                   hipStream_t stream) {
+  const char* fn = "moe_grouped_gemm_fwd_combine";
+  if (T < 0 || k < 1 || R != T * (int64_t)k)
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: need k >= 1 and R == T * k", fn);
+  if (R * N * 2 >= ((int64_t)1 << 31) || T * ((N + TN - 1) / TN) >= ((int64_t)1 << 31))
+    return fail(MOE_ERROR_NOT_SUPPORTED, "%s: Y_perm must be < 2 GiB", fn);
+  if (R == 0) return MOE_SUCCESS;
+  if (!topk_w || !row_of_slot || !token_of_row || !y || !count_workspace)
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: NULL pointer", fn);
+  if (bad_ptr(add) || bad_ptr(y) || (reinterpret_cast<uintptr_t>(count_workspace) & 3))
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: add and y must be 16-byte, the counters 4-byte aligned", fn);
+  if (count_workspace_bytes < moe_grouped_gemm_fwd_combine_workspace_bytes(T, N))
+    return fail(MOE_ERROR_WORKSPACE, "%s: the counters need %zu bytes", fn,
+                moe_grouped_gemm_fwd_combine_workspace_bytes(T, N));
+  const FusedCombine fc{static_cast<int*>(count_workspace), topk_w, row_of_slot, token_of_row, add, y, T, k};
+  return grouped_gemm_fwd_impl(A, B, nullptr, offsets, G, R, K, N, y_perm, nullptr, nullptr, split_workspace,
+                               split_workspace_bytes, stream, nullptr, 0, &fc);
 }
 
 extern "C" moe_status moe_grouped_gemm_fwd_gather(const moe_bf16* X, int64_t T, const int32_t* row_src,

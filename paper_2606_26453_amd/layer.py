@@ -48,7 +48,7 @@ class MoELayer(_Traced):
                  router: bool = False, aux_alpha: float = 0.0, dw_transposed: bool = False,
                  concurrent: bool = False, split_tail: bool = True, gather_fused: bool = False,
                  fp8_forward: bool = False, dw_persistent: bool = True, fp8_requantize: bool = True,
-                 fp8_backward: bool = False, mx: bool = False):
+                 fp8_backward: bool = False, mx: bool = False, combine_fused: bool = False):
         self.cfg = cfg
         # fp8_forward: the routed experts' forward products run on E4M3 operands (activations
         # quantized per row each step, weights per output channel once, here): gate and up in one
@@ -70,6 +70,12 @@ class MoELayer(_Traced):
         if mx and not (fp8_forward or fp8_backward):
             raise ValueError("mx selects the block scales of the FP8 products: enable fp8_forward and/or fp8_backward")
         self.mx = mx
+        # combine_fused: the weighted combine runs in the down product's epilogue
+        # (moe_grouped_gemm_fwd_combine: the tile that stores a token's last row of a column tile
+        # sums its k rows); bitwise the separate call's Y, measured slower (its coherent stores)
+        if combine_fused and fp8_forward:
+            raise ValueError("combine_fused is a form of the bf16 down product")
+        self.combine_fused = combine_fused
         # gather_fused: the gate/up product reads its rows straight from x through token_of_row
         # (moe_grouped_gemm_fwd_gather); X_perm is then gathered only in the backward, for dW_gate
         # and dW_up (moe_gather_rows), so a forward alone never writes it
@@ -166,6 +172,7 @@ class MoELayer(_Traced):
                 "gate_up": (e((E, d, 2 * f), u8), e((E, d), f32)),
             }
             self._quantize_weights_bwd()
+        self.comb_cnt = moe.combine_counters(T, d, dev) if combine_fused else None
         self.shared = cfg.f_shared > 0
         if self.shared:
             fs = cfg.f_shared
@@ -268,6 +275,12 @@ class MoELayer(_Traced):
         else:
             run("fwd_gate_up", moe.moe_grouped_gemm_fwd, b["x_perm"], i["w_gate"], b["offsets"], i["w_up"],
                 b["h_gate"], b["h_up"], b["act"], want_act=True, stream=stream, workspace=self.split_ws)
+        if self.combine_fused:
+            self._join(main, side)        # the shared output is added in the down product
+            run("fwd_down_combine", moe.moe_grouped_gemm_fwd_combine, b["act"], i["w_down"], b["offsets"],
+                b["topk_w"], b["row_of_slot"], b["token_of_row"], add=add, y_perm=b["y_perm"], y=b["y"],
+                counters=self.comb_cnt, workspace=self.split_ws, stream=stream)
+            return b["y"]
         if not self.fp8:
             run("fwd_down", moe.moe_grouped_gemm_fwd, b["act"], i["w_down"], b["offsets"], C=b["y_perm"],
                 stream=stream, workspace=self.split_ws)
@@ -419,6 +432,7 @@ class MoELayer(_Traced):
                            else (3 * E * d * f * 3 + 3 * E * (d + f) * 4)),
             "fwd_gate_up": ("flops8" if self.fp8 else "flops", 4 * R * d * f),
             "fwd_down": ("flops8" if self.fp8 else "flops", 2 * R * f * d),
+            "fwd_down_combine": ("flops", 2 * R * f * d),
             "combine": ("bytes", R * d * 2 + T * d * 2 + T * k * 8 + (T * d * 2 if self.shared else 0)),
             "combine_bwd": ("bytes", T * d * 2 + 2 * R * d * 2 + T * k * 12),
             "dx_down": ("flops", 2 * R * d * f), "dw_down": ("flops", 2 * R * f * d),

@@ -39,6 +39,9 @@ _SIG = {
     "moe_grouped_gemm_fwd": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P, _P]),
     "moe_grouped_gemm_fwd_split": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P, _P,
                                                   ctypes.c_size_t, _P]),
+    "moe_grouped_gemm_fwd_combine_workspace_bytes": (ctypes.c_size_t, [_I64, _I64]),
+    "moe_grouped_gemm_fwd_combine": (ctypes.c_int, [_P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P, _I64, _I32, _P,
+                                                    _P, _P, _P, ctypes.c_size_t, _P, ctypes.c_size_t, _P]),
     "moe_grouped_gemm_fwd_gather": (ctypes.c_int, [_P, _I64, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P,
                                                    _P, ctypes.c_size_t, _P]),
     "moe_gather_rows": (ctypes.c_int, [_P, _I64, _I64, _I32, _P, _P, _P]),
@@ -557,6 +560,41 @@ def moe_grouped_gemm_dx_swiglu_bwd_mx(A, a_scale, Wt, w_scale, offsets, h_gate, 
                                                  _stream(stream))
     _check("moe_grouped_gemm_dx_swiglu_bwd_mx", st)
     return dh_gate, dh_up
+
+
+def combine_counters(T, N, device):
+    """Arrival counters for moe_grouped_gemm_fwd_combine (allocated once, zeroed by each call)."""
+    n = int(lib().moe_grouped_gemm_fwd_combine_workspace_bytes(T, N))
+    return torch.empty(max(16, n), dtype=torch.uint8, device=device)
+
+
+def moe_grouped_gemm_fwd_combine(A, B, offsets, topk_w, row_of_slot, token_of_row, add=None, y_perm=None, y=None,
+                                 counters=None, workspace=None, stream=None):
+    """Down product with the weighted combine fused: (y_perm [R, N], y [T, N]) bit for bit as
+    moe_grouped_gemm_fwd followed by moe_unpermute_combine."""
+    R, K = A.shape
+    G, K2, N = B.shape
+    T, k = topk_w.shape
+    if K2 != K or R != T * k:
+        raise ValueError("bad shapes")
+    _need(A, torch.bfloat16, (R, K), "A")
+    _need(B, torch.bfloat16, (G, K, N), "B")
+    _need(offsets, torch.int32, (G + 1,), "offsets")
+    _need(topk_w, torch.float32, (T, k), "topk_w")
+    _need(row_of_slot, torch.int32, (R,), "row_of_slot")
+    _need(token_of_row, torch.int32, (R,), "token_of_row")
+    _need(add, torch.bfloat16, (T, N), "add")
+    y_perm = torch.empty((R, N), dtype=torch.bfloat16, device=A.device) if y_perm is None else y_perm
+    y = torch.empty((T, N), dtype=torch.bfloat16, device=A.device) if y is None else y
+    _need(y_perm, torch.bfloat16, (R, N), "y_perm")
+    _need(y, torch.bfloat16, (T, N), "y")
+    counters = combine_counters(T, N, A.device) if counters is None else counters
+    st = lib().moe_grouped_gemm_fwd_combine(_ptr(A), _ptr(B), _ptr(offsets), G, R, K, N, _ptr(topk_w),
+                                            _ptr(row_of_slot), _ptr(token_of_row), T, k, _ptr(add), _ptr(y_perm),
+                                            _ptr(y), _ptr(counters), counters.numel(), _ptr(workspace),
+                                            0 if workspace is None else workspace.numel(), _stream(stream))
+    _check("moe_grouped_gemm_fwd_combine", st)
+    return y_perm, y
 
 
 def moe_swiglu(h_gate, h_up, act=None, stream=None):

@@ -760,6 +760,76 @@ def test_layer_gather_fused_bitwise(cfg_id):
         assert torch.equal(t.view(torch.uint8), gat.buf[key].view(torch.uint8)), key
 
 
+def _routing(g, T, E, k):
+    """Seeded top-k choices over distinct experts and the stable expert-ordered packing they imply
+    (built here with torch sorting: offsets, row_of_slot, token_of_row)."""
+    idx = torch.stack([torch.randperm(E, generator=g)[:k] for _ in range(T)])
+    flat = idx.reshape(-1)
+    order = torch.sort(flat, stable=True).indices
+    row_of_slot = torch.empty(T * k, dtype=torch.int64)
+    row_of_slot[order] = torch.arange(T * k)
+    off = torch.zeros(E + 1, dtype=torch.int64)
+    off[1:] = torch.cumsum(torch.bincount(flat, minlength=E), 0)
+    return off.to(torch.int32), row_of_slot.to(torch.int32), (order // k).to(torch.int32)
+
+
+@pytest.mark.parametrize("k,N,shared,split", [(2, 320, False, False), (2, 512, True, True), (1, 256, False, True),
+                                              (4, 192, True, False), (6, 128, False, True), (8, 64, True, True)])
+def test_grouped_gemm_fwd_combine_exact(k, N, shared, split):
+    """The down product with the weighted combine fused into its epilogue, on small integers with
+    power-of-two routing weights (every sum exact): Y_perm and Y exact against the oracle's product
+    and combine, for every k the combine specialises and a general one, with and without the shared
+    output, with and without the split tail, several column tiles (N = 320: a partial one); called
+    twice (the arrival counters are re-zeroed by each call)."""
+    _say("fwd combine exact", k, N, shared, split)
+    g = torch.Generator().manual_seed(77 * k + N)
+    T, E, K = 300, 8, 192
+    R = T * k
+    off, ros, tor = _routing(g, T, E, k)
+    a = _int_tensor(g, (R, K))
+    b = _int_tensor(g, (E, K, N))
+    w = (2.0 ** torch.randint(-2, 2, (T, k), generator=g)).to(torch.float32)
+    add = _int_tensor(g, (T, N), -8, 8) if shared else None
+    ref_perm = O.grouped_gemm(f64(a), f64(b), i64(off))
+    ref_y = O.combine(ref_perm, f64(w), i64(ros), k, add=None if add is None else f64(add))
+    dv = lambda t: None if t is None else t.to(DEV)
+    ws = moe.split_workspace(DEV) if split else None
+    cnt = moe.combine_counters(T, N, DEV)
+    for _ in range(2):
+        yp = poison_(torch.empty((R, N), dtype=torch.bfloat16, device=DEV))
+        y = poison_(torch.empty((T, N), dtype=torch.bfloat16, device=DEV))
+        moe.moe_grouped_gemm_fwd_combine(dv(a), dv(b), dv(off), dv(w), dv(ros), dv(tor), add=dv(add), y_perm=yp,
+                                         y=y, counters=cnt, workspace=ws)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(f64(yp), ref_perm)
+        np.testing.assert_array_equal(f64(y), ref_y)
+
+
+@pytest.mark.parametrize("cfg_id", [0, 2])
+def test_layer_combine_fused_bitwise(cfg_id):
+    """The layer with the combine fused into the down product gives bitwise the outputs of the
+    default layer (Y, Y_perm and everything the backward derives from them), over two steps."""
+    import dataclasses
+    cfg = W.CONFIGS[cfg_id]
+    if cfg_id:
+        cfg = dataclasses.replace(cfg, T=1024)
+    _say("layer combine fused", cfg)
+    inp = W.make_inputs(cfg, 0, "cpu")
+    dinp = {k_: v.to(DEV) for k_, v in inp.items()}
+    ref = L.MoELayer(cfg, dinp)
+    fus = L.MoELayer(cfg, dinp, combine_fused=True)
+    ref.step()
+    for _ in range(2):
+        for t in fus.buf.values():
+            poison_(t)
+        fus.step()
+    torch.cuda.synchronize()
+    for key, t in ref.buf.items():
+        if key in ("workspace", "d_act", "d_act_sh"):
+            continue
+        assert torch.equal(t.view(torch.uint8), fus.buf[key].view(torch.uint8)), key
+
+
 @pytest.mark.parametrize("cfg_id", [0, 2])
 def test_layer_concurrent_bitwise(cfg_id):
     """The two-stream schedule (weight gradients and the shared FFN beside the main chain) gives
