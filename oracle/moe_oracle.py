@@ -582,6 +582,41 @@ def grouped_gemm_mx(a_codes, a_scale, wt_codes, w_scale, offsets, rnd=bf16_round
     return _r(rnd, C)
 
 
+def pack_groups_t(x, offsets, align=128):
+    """The contraction-major form of a routed buffer for the weight gradient on MX operands: x
+    [R, C] rows grouped by offsets -> [C, L], group g's rows as columns p[g] .. p[g] + K_g - 1 with
+    p[g] = sum over h < g of K_h rounded up to a multiple of `align`, zeros elsewhere (so that no
+    32-element block of a row spans two groups).  Returns the packed matrix and p [G+1]."""
+    x = np.asarray(x, dtype=np.float64)
+    off = np.asarray(offsets, dtype=np.int64)
+    cnt = off[1:] - off[:-1]
+    p = np.zeros(len(cnt) + 1, dtype=np.int64)
+    p[1:] = np.cumsum((cnt + align - 1) // align * align)
+    out = np.zeros((x.shape[1], int(p[-1])))
+    for g in range(len(cnt)):
+        out[:, p[g]:p[g] + cnt[g]] = x[off[g]:off[g + 1]].T
+    return out, p
+
+
+def grouped_gemm_dw_mx(at_codes, at_scale, ct_codes, ct_scale, offsets, align=128):
+    """The ragged weight gradient on MX operands (Appendix H's dW_e = X_e^T G_e with both operands
+    quantized along the token axis): At [K, L] and Ct [N, L] codes in the layout of pack_groups_t
+    with scale bytes [K, L/32] and [N, L/32]; dW[g] = sum over the group's K_g token columns of
+    mx(At)[:, t] mx(Ct)[:, t]^T, float64 (fp32 storage is not modelled: the result stays exact)."""
+    A = mx_decode(at_codes, at_scale)
+    C = mx_decode(ct_codes, ct_scale)
+    off = np.asarray(offsets, dtype=np.int64)
+    cnt = off[1:] - off[:-1]
+    G = len(cnt)
+    p = np.zeros(G + 1, dtype=np.int64)
+    p[1:] = np.cumsum((cnt + align - 1) // align * align)
+    out = np.zeros((G, A.shape[0], C.shape[0]))
+    for g in range(G):
+        cols = slice(int(p[g]), int(p[g] + cnt[g]))
+        out[g] = A[:, cols] @ C[:, cols].T
+    return out
+
+
 def rel_fro(got, ref):
     """||got - ref||_F / ||ref||_F in float64 (0 if both are zero, inf if only ref is zero)."""
     got = np.asarray(got, dtype=np.float64)

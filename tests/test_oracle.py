@@ -689,6 +689,57 @@ def test_grouped_gemm_mx_vs_library():
     np.testing.assert_array_equal(O.grouped_gemm_mx(a, sa, w, sw, off), O.bf16_round(got))
 
 
+def test_pack_groups_t_brute_force():
+    """Every element placed by hand-style loops: group g's i-th row becomes column p[g] + i, the
+    starts are the 128-rounded prefix of the counts (empty groups take no columns), the rest zero."""
+    rng = np.random.default_rng(13)
+    counts = [5, 0, 130, 128, 1]
+    off = np.concatenate([[0], np.cumsum(counts)])
+    x = rng.normal(0, 1, (sum(counts), 7))
+    got, p = O.pack_groups_t(x, off)
+    assert p.tolist() == [0, 128, 128, 384, 512, 640]
+    want = np.zeros((7, 640))
+    for g in range(len(counts)):
+        for i in range(counts[g]):
+            for c in range(7):
+                want[c, p[g] + i] = x[off[g] + i, c]
+    np.testing.assert_array_equal(got, want)
+    got32, p32 = O.pack_groups_t(x, off, align=32)
+    assert p32.tolist() == [0, 32, 32, 192, 320, 352] and got32.shape == (7, 352)
+
+
+def test_grouped_gemm_dw_mx_vs_library():
+    """The MX weight gradient on integer codes with random block scales: exact against torch's
+    matmul of each group's un-padded token columns, one 32-token block at a time with the block's
+    scales; padding columns (zero codes) add nothing; an empty group's gradient is zero."""
+    rng = np.random.default_rng(14)
+    counts = [40, 0, 150, 7]
+    off = np.concatenate([[0], np.cumsum(counts)])
+    K, N = 6, 5
+    L = 128 + 0 + 256 + 128
+    ints = np.arange(-4, 5, dtype=np.float64)
+    at = np.zeros((K, L))
+    ct = np.zeros((N, L))
+    _, p = O.pack_groups_t(np.zeros((sum(counts), 1)), off)
+    for g in range(len(counts)):
+        at[:, p[g]:p[g] + counts[g]] = rng.choice(ints, (K, counts[g]))
+        ct[:, p[g]:p[g] + counts[g]] = rng.choice(ints, (N, counts[g]))
+    ac, cc = O.e4m3_encode(at), O.e4m3_encode(ct)
+    sa = rng.integers(122, 132, (K, L // 32)).astype(np.uint8)
+    sc = rng.integers(122, 132, (N, L // 32)).astype(np.uint8)
+    got = O.grouped_gemm_dw_mx(ac, sa, cc, sc, off)
+    A, C = torch.from_numpy(at), torch.from_numpy(ct)
+    SA = torch.from_numpy(2.0 ** (sa.astype(np.float64) - 127))
+    SC = torch.from_numpy(2.0 ** (sc.astype(np.float64) - 127))
+    for g in range(len(counts)):
+        ref = torch.zeros(K, N, dtype=torch.float64)
+        for b in range(int(p[g]) // 32, int(p[g + 1]) // 32):
+            cols = slice(32 * b, 32 * b + 32)
+            ref += (A[:, cols] * SA[:, b:b + 1]) @ (C[:, cols] * SC[:, b:b + 1]).T
+        np.testing.assert_array_equal(got[g], ref.numpy())
+    assert not np.any(got[1])
+
+
 # ---------------------------------------------------------------------------------------------
 # the comparison metric every floating-point parity check goes through
 # ---------------------------------------------------------------------------------------------

@@ -37,6 +37,8 @@ PINS = [
     P.test_quantize_rows_mx_worked_example,
     P.test_quantize_rows_mx_properties,
     P.test_grouped_gemm_mx_vs_library,
+    P.test_pack_groups_t_brute_force,
+    P.test_grouped_gemm_dw_mx_vs_library,
     P.test_rel_fro_hand_values,
 ]
 
@@ -205,6 +207,23 @@ def _mx_gemm_scale_negated(a_codes, a_scale, wt_codes, w_scale, offsets, rnd=O.b
                                    wt_codes, w_scale, offsets, rnd)
 
 
+def _pack_groups_t_align32(x, offsets, align=128):                        # padding to 32, not 128
+    return O.__dict__["_orig_pgt"](x, offsets, 32)
+
+
+def _pack_groups_t_drop_last(x, offsets, align=128):                      # each group's last row lost
+    out, p = O.__dict__["_orig_pgt"](x, offsets, align)
+    off = np.asarray(offsets)
+    for g in range(len(off) - 1):
+        if off[g + 1] > off[g]:
+            out[:, p[g] + off[g + 1] - off[g] - 1] = 0.0
+    return out, p
+
+
+def _dw_mx_next_group_scales(at_codes, at_scale, ct_codes, ct_scale, offsets, align=128):   # scales shifted a block
+    return O.__dict__["_orig_dwmx"](at_codes, np.roll(at_scale, 1, axis=1), ct_codes, ct_scale, offsets, align)
+
+
 def _rel_fro_squared(got, ref):                                           # squared ratio
     r = O.__dict__["_orig_rf"](got, ref)
     return r * r
@@ -245,6 +264,9 @@ MUTANTS = {
     "mx blocks of 16": ("quantize_rows_mx", _quant_mx_blocks_of_16),
     "mx decode tiles the scales": ("mx_decode", _mx_decode_tiled_scales),
     "mx gemm negated activation scale": ("grouped_gemm_mx", _mx_gemm_scale_negated),
+    "pack_groups_t pads to 32": ("pack_groups_t", _pack_groups_t_align32),
+    "pack_groups_t drops each group's last row": ("pack_groups_t", _pack_groups_t_drop_last),
+    "mx dW ignores the scales of a shifted block": ("grouped_gemm_dw_mx", _dw_mx_next_group_scales),
     "router logits drop the bias": ("router_logits", _logits_no_bias),
     "route_topk_bwd drops the weighted mean": ("route_topk_bwd", _topk_bwd_no_mean),
     "route_topk_bwd uses the full softmax": ("route_topk_bwd", _topk_bwd_full_softmax),
@@ -278,6 +300,8 @@ def test_planted_mistake_is_caught(name, monkeypatch):
     monkeypatch.setitem(O.__dict__, "_orig_q8", O.quantize_rows_fp8)
     monkeypatch.setitem(O.__dict__, "_orig_rf", O.rel_fro)
     monkeypatch.setitem(O.__dict__, "_orig_mxg", O.grouped_gemm_mx)
+    monkeypatch.setitem(O.__dict__, "_orig_pgt", O.pack_groups_t)
+    monkeypatch.setitem(O.__dict__, "_orig_dwmx", O.grouped_gemm_dw_mx)
     monkeypatch.setattr(O, attr, fn)
     if attr == "bf16_round":
         # default arguments captured the original function; patch the module-level users too
