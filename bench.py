@@ -104,6 +104,8 @@ def _args():
     ap.add_argument("--mx", action="store_true",
                     help="with --fp8-forward/--fp8-backward: MX block scales (a power of two per 32 contraction "
                          "elements) instead of fp32 per-row/per-channel scales")
+    ap.add_argument("--fp8-dw", action="store_true",
+                    help="with --mx: the weight gradients on MX operands quantized along the tokens (a variant)")
     ap.add_argument("--fp8-fixed-weights", action="store_true",
                     help="with --fp8-forward/--fp8-backward: quantize the weights once (held fixed), not every step")
     ap.add_argument("--forward-only", action="store_true", help="time the forward alone (a variant)")
@@ -213,7 +215,8 @@ class ClockSampler:
 
 def fp8_dtype(a):
     """The arithmetic types of the run: bf16, or which expert products run on E4M3 operands."""
-    parts = [n for n, on in (("forward", a.fp8_forward), ("data-gradient", a.fp8_backward)) if on]
+    parts = [n for n, on in (("forward", a.fp8_forward), ("data-gradient", a.fp8_backward),
+                              ("weight-gradient", getattr(a, "fp8_dw", False))) if on]
     kind = "mxfp8-e4m3" if getattr(a, "mx", False) else "fp8-e4m3"
     return f"{kind} ({' and '.join(parts)} expert products) + bf16" if parts else "bf16"
 
@@ -398,7 +401,7 @@ def main():
                          dw_transposed=a.dw_transposed, concurrent=a.concurrent, split_tail=not a.no_split_tail,
                          gather_fused=a.gather_fused, fp8_forward=a.fp8_forward,
                          fp8_backward=a.fp8_backward, fp8_requantize=not a.fp8_fixed_weights, mx=a.mx,
-                         combine_fused=a.combine_fused,
+                         combine_fused=a.combine_fused, fp8_dw=a.fp8_dw,
                          dw_persistent=not a.dw_one_per_tile)
     torch.cuda.synchronize()
     t_gen = time.perf_counter() - t_gen
@@ -443,7 +446,7 @@ def main():
     calls = {}
     gemm_ms = gemm_flops = 0.0
     variant = (a.fp8_forward or a.fp8_backward or a.gather_fused or a.dw_transposed or a.no_split_tail
-               or a.dw_one_per_tile or a.concurrent or a.combine_fused)
+               or a.dw_one_per_tile or a.concurrent or a.combine_fused or a.fp8_dw)
     for name, ts in per.items():
         avg = sum(ts) / len(ts)
         kind, amount = work[name]
@@ -525,6 +528,7 @@ def main():
                    + (", expert forward products in FP8 E4M3" if a.fp8_forward else "")
                    + (", expert data-gradient products in FP8 E4M3" if a.fp8_backward else "")
                    + (", MX block scales (E8M0 per 32 contraction elements)" if a.mx else "")
+                   + (", expert weight-gradient products in MX FP8" if a.fp8_dw else "")
                    + (", FP8 weights quantized once (held fixed)" if a.fp8_fixed_weights else "")
                    + (", gather fused into the gate/up product" if a.gather_fused else "")
                    + (", combine fused into the down product" if a.combine_fused else "")

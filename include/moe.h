@@ -446,6 +446,40 @@ moe_status moe_grouped_gemm_dx_swiglu_bwd_mx(const uint8_t* A, const uint8_t* a_
                                              size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * Columns needed by the token-major MX operands of the weight gradient for R routed rows in G
+ * groups: the counts rounded up to 128 and summed, bounded by R + 127 G, rounded up to 128.
+ */
+int64_t moe_mx_tokens_cols_bound(int64_t R, int32_t G);
+
+/*
+ * MX quantization of a routed buffer along its token axis, for the weight gradient (Appendix H's
+ * dW_e = X_e^T G_e, whose contraction runs over the K_e rows of expert e): x [R, C] bf16, rows
+ * grouped by offsets -> qt [C, ld] uint8, where group g's rows are columns p[g] .. p[g] + K_g - 1,
+ * p[g] = sum over h < g of K_h rounded up to a multiple of 128, and the columns up to p[g+1] hold
+ * zero codes; each 32-column block of a row of qt (a block never spans two groups) is quantized as
+ * moe_quantize_mx_rows does; st: the MX scale layout of C rows of ld.  Columns from p[G] on are
+ * not written.  C a multiple of 64; ld a multiple of 128, >= moe_mx_tokens_cols_bound(R, G);
+ * x and qt 16-byte aligned.  Errors: bad sizes -> INVALID_VALUE / NOT_SUPPORTED (G outside
+ * 1..256); NULL or misaligned pointers -> INVALID_VALUE.  R = 0 is a no-op.
+ */
+moe_status moe_quantize_mx_tokens_t(const moe_bf16* x, const int32_t* offsets, int32_t G, int64_t R, int64_t C,
+                                    uint8_t* qt, uint8_t* st, int64_t ld, hipStream_t stream);
+
+/*
+ * The weight gradient on MX operands (Appendix H's dW1_e = X_e^T G_e; also dW_down): At [K, ld] and
+ * dCt (dC2t) [N, ld] as moe_quantize_mx_tokens_t writes them (with their scales), dB[g] [K, N]
+ * (dB2[g] from dC2t, the dual gate/up form reading each At tile once) = sum over the group's
+ * tokens of mx(At)[:, t] mx(dCt)[:, t]^T, E4M3 products scaled and accumulated in fp32 by the
+ * matrix cores, stored fp32 (out_bf16 = 0) or rounded once to bf16.  Empty groups give zeros.
+ * K, N multiples of 64; ld as for moe_quantize_mx_tokens_t; max(K, N) * ld < 2^31.  Errors as
+ * moe_grouped_gemm_dw_t; scale pointers 4-byte aligned; dC2t, c2_scale and dB2 all set or all NULL.
+ */
+moe_status moe_grouped_gemm_dw_mx(const uint8_t* At, const uint8_t* a_scale, const uint8_t* dCt,
+                                  const uint8_t* c_scale, const uint8_t* dC2t, const uint8_t* c2_scale,
+                                  const int32_t* offsets, int32_t G, int64_t R, int64_t K, int64_t N, int64_t ld,
+                                  void* dB, void* dB2, int32_t out_bf16, hipStream_t stream);
+
+/*
  * moe_grouped_gemm_fwd with the same split of the last, partial round of tiles (same arguments,
  * definitions and errors as moe_grouped_gemm_fwd, plus a split workspace as described at
  * moe_grouped_gemm_split_workspace_bytes).  The

@@ -315,6 +315,23 @@ __global__ __launch_bounds__(256) void quantize_mx_rows_kernel(const u32x4* __re
   }
 }
 
+// From a 128 x 64 bf16 tile staged row-major in LDS: the MX codes of column n over rows
+// 32*kb .. 32*kb + 31 (one block), packed 4 to a word in o[8]; returns the block's scale byte.
+__device__ __forceinline__ uint32_t mx_tile_col_block(const uint16_t* s_w, int n, int kb, uint32_t o[8]) {
+  float v[32];
+  float m = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 32; ++i) {
+    v[i] = __uint_as_float((uint32_t)s_w[(32 * kb + i) * 64 + n] << 16);
+    m = fmaxf(m, fabsf(v[i]));
+  }
+  const uint32_t byte = mx_scale_byte(m);
+  const float inv = mx_inv_scale(byte);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) o[i] = e4m3_pack4(v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3], inv);
+  return byte;
+}
+
 // Weights, both orientations from one read.  Workgroup (column block n0 = 64*bx, row block
 // k0 = 128*by, matrix/expert bz) stages the 128 x 64 tile of W[g] (or W2[g]) in LDS:
 //   rows (qr, sr): row (g, k) of the [G, K, nmat*N] matrix [W[g] | W2[g]], blocks of 32 columns;
@@ -364,18 +381,8 @@ __global__ __launch_bounds__(256) void quantize_mx_weight_kernel(const uint16_t*
   __syncthreads();
   const int n = t & 63, kb = t >> 6;
   if (k0 + 32 * kb >= K) return;   // K is a multiple of 32: the block is whole or absent
-  float v[32];
-  float m = 0.0f;
-#pragma unroll
-  for (int i = 0; i < 32; ++i) {
-    v[i] = __uint_as_float((uint32_t)s_w[(32 * kb + i) * 64 + n] << 16);
-    m = fmaxf(m, fabsf(v[i]));
-  }
-  const uint32_t byte = mx_scale_byte(m);
-  const float inv = mx_inv_scale(byte);
   uint32_t o[8];
-#pragma unroll
-  for (int i = 0; i < 8; ++i) o[i] = e4m3_pack4(v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3], inv);
+  const uint32_t byte = mx_tile_col_block(s_w, n, kb, o);
   const int64_t row = g * (nmat * N) + qc_out_row(n0 + n, w2 != nullptr, second);
   uint8_t* dst = qt + row * K + k0 + 32 * kb;
   *reinterpret_cast<u32x4*>(dst) = u32x4{o[0], o[1], o[2], o[3]};
@@ -383,8 +390,81 @@ __global__ __launch_bounds__(256) void quantize_mx_weight_kernel(const uint16_t*
   st[mx_scale_at(row, (k0 >> 5) + kb, G * nmat * N)] = (uint8_t)byte;
 }
 
+// Token-major operands of the weight gradient: x [R, C] bf16, rows grouped by offsets -> qt [C, ld]
+// codes with group g's K_g rows as columns p[g] .. p[g] + K_g - 1, p the prefix of the counts
+// rounded up to 128 (no 32-element block spans two groups, and each group starts a 128-element
+// scale word), zero codes in each group's padding; scales in the MX layout of C rows of ld.
+// Workgroup (64-column block n0 = 64*bx of x, 128-column block j0 = 128*by of qt) stages the 128
+// source rows that land in columns j0 .. j0+127 (zeros past the group's end) and quantizes them
+// column by column as the weight kernel's transposed half does; blocks past p[G] are left alone.
+__global__ __launch_bounds__(256) void quantize_mx_tokens_t_kernel(const uint16_t* __restrict__ x,
+                                                                   const int32_t* __restrict__ offsets, int G,
+                                                                   int64_t C, int64_t ld, uint8_t* __restrict__ qt,
+                                                                   uint8_t* __restrict__ st) {
+  __shared__ int s_o[257];
+  __shared__ int s_p[257];
+  __shared__ __attribute__((aligned(16))) uint16_t s_w[128 * 64];
+  const int t = threadIdx.x;
+  for (int i = t; i <= G; i += 256) s_o[i] = offsets[i];
+  __syncthreads();
+  s_p[t + 1] = t < G ? ((s_o[t + 1] - s_o[t] + 127) & ~127) : 0;
+  if (t == 0) s_p[0] = 0;
+  __syncthreads();
+  for (int off = 1; off < G; off <<= 1) {   // inclusive scan of the rounded counts
+    const int add = t >= off ? s_p[t + 1 - off] : 0;
+    __syncthreads();
+    s_p[t + 1] += add;
+    __syncthreads();
+  }
+  const int64_t j0 = (int64_t)blockIdx.y * 128;
+  if (j0 >= s_p[G]) return;   // uniform
+  const int g = __syncthreads_count(t < G && s_p[t + 1] <= j0);   // the group holding j0 .. j0+127
+  const int64_t src0 = s_o[g] + (j0 - s_p[g]), src_end = s_o[g + 1];
+  const int64_t n0 = (int64_t)blockIdx.x * 64;
+  const int c8 = t & 7, rq = t >> 3;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int kl = rq + 32 * u;
+    const int64_t r = src0 + kl;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (r < src_end) v = *reinterpret_cast<const u32x4*>(x + r * C + n0 + 8 * c8);
+    *reinterpret_cast<u32x4*>(s_w + kl * 64 + 8 * c8) = v;
+  }
+  __syncthreads();
+  const int n = t & 63, kb = t >> 6;
+  uint32_t o[8];
+  const uint32_t byte = mx_tile_col_block(s_w, n, kb, o);
+  uint8_t* dst = qt + (n0 + n) * ld + j0 + 32 * kb;
+  *reinterpret_cast<u32x4*>(dst) = u32x4{o[0], o[1], o[2], o[3]};
+  *reinterpret_cast<u32x4*>(dst + 16) = u32x4{o[4], o[5], o[6], o[7]};
+  st[mx_scale_at(n0 + n, (j0 >> 5) + kb, C)] = (uint8_t)byte;
+}
+
 }  // namespace
 }  // namespace moe
+
+extern "C" int64_t moe_mx_tokens_cols_bound(int64_t R, int32_t G) {
+  return R < 0 || G < 1 ? 0 : (R + 127 * (int64_t)G + 127) / 128 * 128;
+}
+
+extern "C" moe_status moe_quantize_mx_tokens_t(const moe_bf16* x, const int32_t* offsets, int32_t G, int64_t R,
+                                               int64_t C, uint8_t* qt, uint8_t* st, int64_t ld, hipStream_t stream) {
+  const char* fn = "moe_quantize_mx_tokens_t";
+  if (G < 1 || G > 256) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: need 1 <= G <= 256", fn);
+  if (R < 0 || C <= 0) return fail(MOE_ERROR_INVALID_VALUE, "%s: bad size", fn);
+  if (C % 64) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: C must be a multiple of 64", fn);
+  if (ld % 128 || ld < moe_mx_tokens_cols_bound(R, G))
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: ld must be a multiple of 128 and >= %lld", fn,
+                (long long)moe_mx_tokens_cols_bound(R, G));
+  if (ld / 128 > 65535 || C / 64 > 0x7fffffff) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: too many columns", fn);
+  if (!offsets || !qt || !st || (R > 0 && !x)) return fail(MOE_ERROR_INVALID_VALUE, "%s: NULL pointer", fn);
+  if ((x && !aligned16(x)) || !aligned16(qt))
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: x and qt must be 16-byte aligned", fn);
+  if (R == 0) return MOE_SUCCESS;
+  quantize_mx_tokens_t_kernel<<<dim3((unsigned)(C / 64), (unsigned)(ld / 128)), 256, 0, stream>>>(
+      x, offsets, G, C, ld, qt, st);
+  return check_launch("quantize_mx_tokens_t_kernel");
+}
 
 extern "C" moe_status moe_quantize_mx_rows(const moe_bf16* x, const moe_bf16* x2, int64_t M, int64_t K, uint8_t* q,
                                            uint8_t* scale, hipStream_t stream) {

@@ -77,7 +77,8 @@ struct GemmParams {
   const float* a_scale;    // FP8 products: per-row scale of the row operand [R]
   const float* w_scale;    //               per-output-column scale of the weight [G, K]
   const uint8_t* a_mx;     // MX products: E8M0 block scales of the row operand [C/128][R][4]
-  const uint8_t* w_mx;     //              ... of the weight's rows [C/128][G*K][4]
+  const uint8_t* w_mx;     //              ... of the weight's rows [C/128][G*K][4] (DWT: of dC^T's rows)
+  const uint8_t* w_mx2;    //              DWT dual: of dC2^T's rows
   int64_t mx_a_step, mx_w_step;   //       bytes from one 128-element group of scales to the next
   int* tile_queue;         // DW, persistent: 8 tile-claim counters, one per XCD (zero at launch)
   int* comb_cnt;           // FWD single output, fused combine: arrival counters [T, n_tiles] (zero
@@ -208,7 +209,8 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
   // 0..127 gate, 128..255 up), stored as two outputs (+ SwiGLU with ACT) like the fwd dual product.
   // F8 && ACT && !DUAL: the dX-down product with the SwiGLU backward in its epilogue, applied to
   // the scaled, bf16-rounded dA exactly as in the bf16 product.
-  static_assert(!F8 || KIND == KIND_DX, "FP8 operands: the dX-shaped product");
+  static_assert(!F8 || KIND == KIND_DX || (KIND == KIND_DWT && MX),
+                "FP8 operands: the dX-shaped products (and, with MX scales along the tokens, dW)");
   static_assert(!MX || (F8 && PINGPONG && WAVES_M * WAVES_N == 8 && TM == 256),
                 "MX scales: the FP8 product's 8-wavefront ping-pong schedule");
   constexpr int ES = F8 ? 1 : 2;              // bytes per operand element
@@ -257,7 +259,9 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
   int ntiles_all, mtotal = 0;
   if constexpr (KIND == KIND_DWT) {
     __syncthreads();
-    if (tid < 256) s_pp[tid + 1] = tid < p.G ? ((s_off[tid + 1] - s_off[tid] + 31) & ~31) : 0;
+    // segments padded to 32 rows (128 with MX scales: each segment then starts a scale word)
+    constexpr int PADM = MX ? 127 : 31;
+    if (tid < 256) s_pp[tid + 1] = tid < p.G ? ((s_off[tid + 1] - s_off[tid] + PADM) & ~PADM) : 0;
     if (tid == 0) s_pp[0] = 0;
     __syncthreads();
     for (int off = 1; off < p.G; off <<= 1) {   // entries past G are zero
@@ -393,13 +397,13 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
       // padded segment starting at column row_lo
       m_ld = p.ld_t;
       const int64_t rows_valid = p.K - (int64_t)mt * TM;   // > 0
-      m_src = reinterpret_cast<const char*>(p.a + (int64_t)mt * TM * m_ld + row_lo);
+      m_src = reinterpret_cast<const char*>(p.a) + ((int64_t)mt * TM * m_ld + row_lo) * ES;
 #pragma unroll
       for (int i = 0; i < DPW_M; ++i) {
         int64_t r = 16 * (DPW_M * wave + i) + (lane >> 2);
         if (r > rows_valid - 1) r = rows_valid - 1;
         const int c = (lane & 3) ^ swz_d(lane >> 2);
-        m_voff[i] = (int)((r * m_ld + 8 * c) * 2);
+        m_voff[i] = (int)(r * m_ld * ES + 16 * c);
       }
     } else if constexpr (!M_T) {
       m_ld = (KIND == KIND_FWD) ? p.K : p.N;
@@ -452,14 +456,14 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
       if constexpr (DUAL) {
         if ((r0w & 127) >= 64) src = p.b2;
       }
-      n_src = reinterpret_cast<const char*>(src + row_lo);
+      n_src = reinterpret_cast<const char*>(src) + row_lo * ES;
 #pragma unroll
       for (int i = 0; i < DPW_N; ++i) {
         const int r = 16 * (DPW_N * wave + i) + (lane >> 2);
         int64_t col = DUAL ? (int64_t)nt * (TN / 2) + 64 * (r >> 7) + (r & 63) : (int64_t)nt * TN + r;
         if (col > p.N - 1) col = p.N - 1;
         const int c = (lane & 3) ^ swz_d(lane >> 2);
-        n_voff[i] = (int)((col * n_ld + 8 * c) * 2);
+        n_voff[i] = (int)(col * n_ld * ES + 16 * c);
       }
     } else if constexpr (!N_T) {
       // DX: B[g][kk, c]; the tile's output columns kk = nt*TN + row, clamped
@@ -497,7 +501,34 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
       }
     }
 
-    if constexpr (MX) {
+    if constexpr (MX && KIND == KIND_DWT) {
+      // dW: the contraction is the group's padded token segment, starting at column row_lo (a
+      // multiple of 128: scale word row_lo / 128).  waves 0-3: rows mt*TM + 64*wave + lane of A^T;
+      // waves 4-7: the rows of dC^T (dual: dC^T or dC2^T, one source per wave) that tile rows
+      // 64*(wave-4) + lane map to, as for the operand loads; all clamped to the last row
+      const int r = 64 * (wave & 3) + lane;
+      const int64_t grp0 = row_lo >> 7;
+      if (wave < 4) {
+        int64_t rr = (int64_t)mt * TM + r;
+        if (rr > p.K - 1) rr = p.K - 1;
+        sc_src = reinterpret_cast<const char*>(p.a_mx) + grp0 * p.mx_a_step;
+        sc_voff = (int)(rr * 4);
+        sc_step = p.mx_a_step;
+      } else {
+        const uint8_t* base = p.w_mx;
+        int64_t col;
+        if constexpr (DUAL) {
+          col = (int64_t)nt * (TN / 2) + 64 * (r >> 7) + (r & 63);
+          if ((r & 127) >= 64) base = p.w_mx2;
+        } else {
+          col = (int64_t)nt * TN + r;
+        }
+        if (col > p.N - 1) col = p.N - 1;
+        sc_src = reinterpret_cast<const char*>(base) + grp0 * p.mx_w_step;
+        sc_voff = (int)(col * 4);
+        sc_step = p.mx_w_step;
+      }
+    } else if constexpr (MX) {
       // waves 0-3: tile rows 64*wave + lane (clamped to the group, like the row loads); waves 4-7:
       // weight rows (output columns) nt*TN + 64*(wave-4) + lane, clamped to the last
       const int r = 64 * (wave & 3) + lane;
@@ -934,7 +965,9 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
     if constexpr (SPLIT) {
       // FWD gate/up and FP8 interleaved gate/up (+ SwiGLU): thread -> gate chunk c and up chunk 16 + c of rows t, t + NT/16, ...
       const int c = tid & 15;
-      const int64_t Wo = F8 ? p.K / 2 : p.N;   // width of each output
+      // width of each output (the FP8 interleaved gate/up product is dX-shaped: its 2F output
+      // columns are p.K)
+      const int64_t Wo = (F8 && KIND == KIND_DX) ? p.K / 2 : p.N;
       const int64_t n = (int64_t)nt * (TN / 2) + 8 * c;
       if (n < Wo) {
         uint16_t* c1 = static_cast<uint16_t*>(p.out) + obase + n;
@@ -1763,6 +1796,49 @@ extern "C" moe_status moe_grouped_gemm_dw_t(const moe_bf16* At, const moe_bf16* 
   }
   if (dC2t) return launch<KIND_DWT, true, false>(p, tiles, stream, "grouped_gemm_dw_t(dual)");
   return launch<KIND_DWT, false, false>(p, tiles, stream, "grouped_gemm_dw_t");
+}
+
+extern "C" moe_status moe_grouped_gemm_dw_mx(const uint8_t* At, const uint8_t* a_scale, const uint8_t* dCt,
+                                             const uint8_t* c_scale, const uint8_t* dC2t, const uint8_t* c2_scale,
+                                             const int32_t* offsets, int32_t G, int64_t R, int64_t K, int64_t N,
+                                             int64_t ld, void* dB, void* dB2, int32_t out_bf16, hipStream_t stream) {
+  const char* fn = "moe_grouped_gemm_dw_mx";
+  if (G < 1 || G > 256) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: need 1 <= G <= 256", fn);
+  if (R < 0 || K <= 0 || N <= 0) return fail(MOE_ERROR_INVALID_VALUE, "%s: bad size", fn);
+  if (K % 64 || N % 64) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: K and N must be multiples of 64", fn);
+  if (R >= ((int64_t)1 << 31)) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: R >= 2^31", fn);
+  const int64_t bound = moe_mx_tokens_cols_bound(R, G);
+  if (ld < bound || ld % 128)
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: ld must be a multiple of 128 and >= %lld", fn, (long long)bound);
+  if ((K > N ? K : N) * ld >= ((int64_t)1 << 31))
+    return fail(MOE_ERROR_NOT_SUPPORTED, "%s: operands of 2 GiB or more", fn);
+  if (!offsets) return fail(MOE_ERROR_INVALID_VALUE, "%s: offsets is NULL", fn);
+  if ((dC2t == nullptr) != (dB2 == nullptr) || (dC2t == nullptr) != (c2_scale == nullptr))
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: dC2t, c2_scale and dB2 must all be set or all NULL", fn);
+  if (!dB || !At || !dCt || !a_scale || !c_scale) return fail(MOE_ERROR_INVALID_VALUE, "%s: NULL pointer", fn);
+  if (bad_ptr(At) || bad_ptr(dCt) || bad_ptr(dC2t) || bad_ptr(dB) || bad_ptr(dB2) ||
+      ((reinterpret_cast<uintptr_t>(a_scale) | reinterpret_cast<uintptr_t>(c_scale) |
+        reinterpret_cast<uintptr_t>(c2_scale)) & 3))
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: operands and outputs must be 16-byte, scales 4-byte aligned", fn);
+  GemmParams p{};
+  p.a = reinterpret_cast<const uint16_t*>(At);
+  p.b = reinterpret_cast<const uint16_t*>(dCt);
+  p.b2 = reinterpret_cast<const uint16_t*>(dC2t);
+  p.a_mx = a_scale; p.w_mx = c_scale; p.w_mx2 = c2_scale;
+  p.mx_a_step = K * 4;
+  p.mx_w_step = N * 4;
+  p.offsets = offsets; p.out = dB; p.out2 = dB2;
+  p.G = G; p.R = R; p.K = K; p.N = N; p.ld_t = ld;
+  p.m_tiles = (int)((K + Cfg<KIND_DWT>::TM - 1) / Cfg<KIND_DWT>::TM);
+  const int cols_per_tile = dC2t ? TN / 2 : TN;
+  p.n_tiles = (int)((N + cols_per_tile - 1) / cols_per_tile);
+  const int64_t tiles = (int64_t)G * p.m_tiles * p.n_tiles;
+  if (out_bf16) {
+    if (dC2t) return launch<KIND_DWT, true, false, true, false, true, false, true>(p, tiles, stream, fn);
+    return launch<KIND_DWT, false, false, true, false, true, false, true>(p, tiles, stream, fn);
+  }
+  if (dC2t) return launch<KIND_DWT, true, false, false, false, true, false, true>(p, tiles, stream, fn);
+  return launch<KIND_DWT, false, false, false, false, true, false, true>(p, tiles, stream, fn);
 }
 
 extern "C" moe_status moe_grouped_gemm_dw(const moe_bf16* A, const moe_bf16* dC, const moe_bf16* dC2,

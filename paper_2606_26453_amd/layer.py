@@ -48,7 +48,8 @@ class MoELayer(_Traced):
                  router: bool = False, aux_alpha: float = 0.0, dw_transposed: bool = False,
                  concurrent: bool = False, split_tail: bool = True, gather_fused: bool = False,
                  fp8_forward: bool = False, dw_persistent: bool = True, fp8_requantize: bool = True,
-                 fp8_backward: bool = False, mx: bool = False, combine_fused: bool = False):
+                 fp8_backward: bool = False, mx: bool = False, combine_fused: bool = False,
+                 fp8_dw: bool = False):
         self.cfg = cfg
         # fp8_forward: the routed experts' forward products run on E4M3 operands (activations
         # quantized per row each step, weights per output channel once, here): gate and up in one
@@ -70,6 +71,13 @@ class MoELayer(_Traced):
         if mx and not (fp8_forward or fp8_backward):
             raise ValueError("mx selects the block scales of the FP8 products: enable fp8_forward and/or fp8_backward")
         self.mx = mx
+        # fp8_dw: the weight gradients on MX operands quantized along the tokens (the contraction
+        # of dW): X_perm, the SwiGLU output, dY_perm, dH_gate and dH_up are quantized into
+        # token-major codes (each expert's rows from a 128-aligned column, so that no 32-token
+        # block spans two experts) that moe_grouped_gemm_dw_mx reads
+        if fp8_dw and not mx:
+            raise ValueError("fp8_dw takes MX block scales (mx=True)")
+        self.fp8_dw = fp8_dw
         # combine_fused: the weighted combine runs in the down product's epilogue
         # (moe_grouped_gemm_fwd_combine: the tile that stores a token's last row of a column tile
         # sums its k rows); bitwise the separate call's Y, measured slower (its coherent stores)
@@ -173,6 +181,12 @@ class MoELayer(_Traced):
             }
             self._quantize_weights_bwd()
         self.comb_cnt = moe.combine_counters(T, d, dev) if combine_fused else None
+        if fp8_dw:
+            u8 = torch.uint8
+            ldt = moe.mx_tokens_cols(R, E)
+            for name, rows in (("x", d), ("act", f), ("dy", d), ("dhg", f), ("dhu", f)):
+                b[name + "_qt"] = e((rows, ldt), u8)
+                b[name + "_st"] = e((ldt // 128, rows, 4), u8)
         self.shared = cfg.f_shared > 0
         if self.shared:
             fs = cfg.f_shared
@@ -322,7 +336,14 @@ class MoELayer(_Traced):
                 b["d_topk_w"], b["offsets"], self.normalize, self.aux_alpha, dx=None, workspace=b["router_ws"],
                 dlogits=b["dlogits"], dwr=b["dwr"], stream=stream)
         self._join(side, main)            # dW_down needs dY_perm
-        if self.dw_t:
+        if self.fp8_dw:
+            run("quantize_t_act", moe.moe_quantize_mx_tokens_t, b["act"], b["offsets"], b["act_qt"], b["act_st"],
+                stream=side)
+            run("quantize_t_dy", moe.moe_quantize_mx_tokens_t, b["dy_perm"], b["offsets"], b["dy_qt"], b["dy_st"],
+                stream=side)
+            run("dw_down", moe.moe_grouped_gemm_dw_mx, b["act_qt"], b["act_st"], b["dy_qt"], b["dy_st"],
+                b["offsets"], self.R, dB=b["dw_down"], stream=side)
+        elif self.dw_t:
             run("transpose_act", moe.moe_transpose_grouped, b["act"], b["offsets"], dst=b["act_t"], stream=side)
             run("transpose_dy_perm", moe.moe_transpose_grouped, b["dy_perm"], b["offsets"], dst=b["dy_perm_t"],
                 stream=side)
@@ -373,7 +394,13 @@ class MoELayer(_Traced):
         early = side is main
         if early:
             self._unpermute_dx(dx_add, stream)
-        if self.dw_t:
+        if self.fp8_dw:
+            run("quantize_t_x", moe.moe_quantize_mx_tokens_t, b["x_perm"], b["offsets"], b["x_qt"], b["x_st"],
+                stream=side)
+            run("quantize_t_dh", self._quantize_t_dh, stream=side)
+            run("dw_gate_up", moe.moe_grouped_gemm_dw_mx, b["x_qt"], b["x_st"], b["dhg_qt"], b["dhg_st"],
+                b["offsets"], self.R, b["dhu_qt"], b["dhu_st"], dB=b["dw_gate"], dB2=b["dw_up"], stream=side)
+        elif self.dw_t:
             run("transpose_x_perm", moe.moe_transpose_grouped, b["x_perm"], b["offsets"], dst=b["x_perm_t"],
                 stream=side)
             run("transpose_dh", self._transpose_dh, stream=side)
@@ -403,6 +430,11 @@ class MoELayer(_Traced):
     @property
     def R(self):
         return self.cfg.T * self.cfg.k
+
+    def _quantize_t_dh(self, stream=None):
+        b = self.buf
+        moe.moe_quantize_mx_tokens_t(b["dh_gate"], b["offsets"], b["dhg_qt"], b["dhg_st"], stream=stream)
+        moe.moe_quantize_mx_tokens_t(b["dh_up"], b["offsets"], b["dhu_qt"], b["dhu_st"], stream=stream)
 
     def _transpose_dh(self, stream=None):
         b = self.buf
@@ -435,7 +467,7 @@ class MoELayer(_Traced):
             "fwd_down_combine": ("flops", 2 * R * f * d),
             "combine": ("bytes", R * d * 2 + T * d * 2 + T * k * 8 + (T * d * 2 if self.shared else 0)),
             "combine_bwd": ("bytes", T * d * 2 + 2 * R * d * 2 + T * k * 12),
-            "dx_down": ("flops", 2 * R * d * f), "dw_down": ("flops", 2 * R * f * d),
+            "dx_down": ("flops", 2 * R * d * f), "dw_down": ("flops8" if self.fp8_dw else "flops", 2 * R * f * d),
             "dx_down_swiglu_bwd": ("flops8" if self.fp8_bwd else "flops", 2 * R * d * f),
             # FP8 backward: dY_perm and [dH_gate | dH_up] per row, the weights in their stored layouts
             "quantize_dy": ("bytes", R * d * 3 + R * sc(d)), "quantize_dh": ("bytes", 2 * R * f * 3 + R * sc(2 * f)),
@@ -443,7 +475,10 @@ class MoELayer(_Traced):
                                else (3 * E * d * f * 3 + E * (d + f) * 4)),
             "swiglu_bwd": ("bytes", 5 * R * f * 2),
             "dx_gate_up": ("flops8" if self.fp8_bwd else "flops", 4 * R * d * f),
-            "dw_gate_up": ("flops", 4 * R * d * f),
+            "dw_gate_up": ("flops8" if self.fp8_dw else "flops", 4 * R * d * f),
+            # MX weight gradient: token-major codes of its operands (read bf16, write codes + scales)
+            "quantize_t_x": ("bytes", R * d * 3 + R * d // 32), "quantize_t_act": ("bytes", R * f * 3 + R * f // 32),
+            "quantize_t_dy": ("bytes", R * d * 3 + R * d // 32), "quantize_t_dh": ("bytes", 2 * (R * f * 3 + R * f // 32)),
             "unpermute_dx": ("bytes", R * d * 2 + T * d * 2 + R * 4 + (T * d * 2 if self.shared else 0)),
             # router: fp32 vector-ALU work (multiply-adds x2) of the contractions with Wr, with the
             # HBM bytes each call must move (x bf16 read; logits / dlogits fp32; the backward also

@@ -57,6 +57,10 @@ _SIG = {
     "moe_grouped_gemm_fwd_fp8_gate_up": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P, _P,
                                                         ctypes.c_size_t, _P]),
     "moe_mx_scale_bytes": (_I64, [_I64, _I64]),
+    "moe_mx_tokens_cols_bound": (_I64, [_I64, _I32]),
+    "moe_quantize_mx_tokens_t": (ctypes.c_int, [_P, _P, _I32, _I64, _I64, _P, _P, _I64, _P]),
+    "moe_grouped_gemm_dw_mx": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _I64, _P, _P,
+                                              _I32, _P]),
     "moe_quantize_mx_rows": (ctypes.c_int, [_P, _P, _I64, _I64, _P, _P, _P]),
     "moe_quantize_mx_weight": (ctypes.c_int, [_P, _P, _I64, _I64, _I64, _P, _P, _P, _P, _P]),
     "moe_grouped_gemm_fwd_mx": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P,
@@ -595,6 +599,54 @@ def moe_grouped_gemm_fwd_combine(A, B, offsets, topk_w, row_of_slot, token_of_ro
                                             0 if workspace is None else workspace.numel(), _stream(stream))
     _check("moe_grouped_gemm_fwd_combine", st)
     return y_perm, y
+
+
+def mx_tokens_cols(R, G):
+    """Row length of the token-major MX operands of R routed rows in G groups (a multiple of 128)."""
+    return int(lib().moe_mx_tokens_cols_bound(R, G))
+
+
+def moe_quantize_mx_tokens_t(x, offsets, qt=None, st=None, stream=None):
+    """MX codes qt [C, ld] and scales st [ld/128, C, 4] of the routed buffer x [R, C] along its
+    token axis: expert g's rows as columns from a 128-aligned start, zero codes in the padding."""
+    R, C = x.shape
+    G = offsets.numel() - 1
+    _need(x, torch.bfloat16, (R, C), "x")
+    _need(offsets, torch.int32, (G + 1,), "offsets")
+    ld = mx_tokens_cols(R, G)
+    qt = torch.empty((C, ld), dtype=torch.uint8, device=x.device) if qt is None else qt
+    st = torch.empty((ld // 128, C, 4), dtype=torch.uint8, device=x.device) if st is None else st
+    _need(qt, torch.uint8, (C, ld), "qt")
+    _need(st, torch.uint8, (ld // 128, C, 4), "st")
+    _check("moe_quantize_mx_tokens_t", lib().moe_quantize_mx_tokens_t(_ptr(x), _ptr(offsets), G, R, C, _ptr(qt),
+                                                                      _ptr(st), ld, _stream(stream)))
+    return qt, st
+
+
+def moe_grouped_gemm_dw_mx(At, a_scale, dCt, c_scale, offsets, R, dC2t=None, c2_scale=None, dB=None, dB2=None,
+                           out_bf16=False, stream=None):
+    """The weight gradient on token-major MX operands (moe_quantize_mx_tokens_t): dB [G, K, N]
+    (dB2 from dC2t), fp32 or bf16."""
+    K, ld = At.shape
+    N = dCt.shape[0]
+    G = offsets.numel() - 1
+    _need(At, torch.uint8, (K, ld), "At")
+    _need(a_scale, torch.uint8, (ld // 128, K, 4), "a_scale")
+    _need(dCt, torch.uint8, (N, ld), "dCt")
+    _need(c_scale, torch.uint8, (ld // 128, N, 4), "c_scale")
+    _need(dC2t, torch.uint8, (N, ld), "dC2t")
+    _need(c2_scale, torch.uint8, (ld // 128, N, 4), "c2_scale")
+    dt = torch.bfloat16 if out_bf16 else torch.float32
+    dB = torch.empty((G, K, N), dtype=dt, device=At.device) if dB is None else dB
+    _need(dB, dt, (G, K, N), "dB")
+    if dC2t is not None:
+        dB2 = torch.empty((G, K, N), dtype=dt, device=At.device) if dB2 is None else dB2
+        _need(dB2, dt, (G, K, N), "dB2")
+    _check("moe_grouped_gemm_dw_mx",
+           lib().moe_grouped_gemm_dw_mx(_ptr(At), _ptr(a_scale), _ptr(dCt), _ptr(c_scale), _ptr(dC2t), _ptr(c2_scale),
+                                        _ptr(offsets), G, R, K, N, ld, _ptr(dB), _ptr(dB2) if dC2t is not None else None,
+                                        int(out_bf16), _stream(stream)))
+    return (dB, dB2) if dC2t is not None else dB
 
 
 def moe_swiglu(h_gate, h_up, act=None, stream=None):

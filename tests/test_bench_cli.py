@@ -45,7 +45,7 @@ def test_measured_traffic_covers_every_layer_call():
     lay = object.__new__(MoELayer)
     lay.cfg, lay.fp8, lay.gather_fused, lay.shared = W.CONFIGS[bench.TRAFFIC_CONFIG], False, False, False
     lay.router_fused_dx = False
-    lay.fp8_bwd = lay.mx = False
+    lay.fp8_bwd = lay.mx = lay.fp8_dw = False
     work = lay.work()
     c = lay.cfg
     R = c.T * c.k

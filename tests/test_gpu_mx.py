@@ -312,9 +312,78 @@ def test_grouped_gemm_mx_256_groups_exact():
 
 
 # ------------------------------------------------------------------------------------------------
+# The weight gradient on MX operands quantized along the tokens
+# ------------------------------------------------------------------------------------------------
+@pytest.mark.parametrize("counts,C", [([5, 0, 130, 128, 1, 300], 64), ([129, 127, 0, 0, 256], 320),
+                                      ([1], 128), ([700, 3, 41], 192)])
+def test_quantize_mx_tokens_t(counts, C):
+    """Token-major codes and scales bit for bit against the oracle's packing (each expert's rows as
+    columns from a 128-aligned start, zeros in the padding) quantized row by row; empty groups,
+    groups of 1, 127, 128, 129 rows; blocks of very different magnitudes."""
+    _say("quantize mx tokens", counts, C)
+    g = torch.Generator().manual_seed(sum(counts) + C)
+    R = sum(counts)
+    off = torch.tensor(np.concatenate([[0], np.cumsum(counts)]), dtype=torch.int32)
+    mag = 2.0 ** torch.randint(-20, 21, (R, 1), generator=g).double() * 2.0 ** torch.randint(-20, 21, (1, C),
+                                                                                             generator=g).double()
+    x = (torch.randn((R, C), generator=g, dtype=torch.float64) * mag).to(torch.bfloat16)
+    x[::7] = 0                                         # zero rows, so some blocks are all zero
+    G = len(counts)
+    ld = moe.mx_tokens_cols(R, G)
+    qt = poison_(torch.empty((C, ld), dtype=torch.uint8, device=DEV))
+    st = poison_(torch.empty((ld // 128, C, 4), dtype=torch.uint8, device=DEV))
+    moe.moe_quantize_mx_tokens_t(x.to(DEV), off.to(DEV), qt, st)
+    torch.cuda.synchronize()
+    packed, p = O.pack_groups_t(f64(x), off.numpy())
+    L = int(p[-1])
+    rq, rs = O.quantize_rows_mx(packed)
+    np.testing.assert_array_equal(_u8(qt)[:, :L], rq)
+    np.testing.assert_array_equal(_blocks(st, ld)[:, : L // 32], rs)
+
+
+def _tokens_operand(g, rows, counts, lo=125, hi=129):
+    """Integer codes |c| <= 4 in the token-major layout (zeros in each group's padding) and random
+    scale bytes: (codes [rows, ld], scales in the library's layout, scale bytes [rows, ld/32])."""
+    G, R = len(counts), sum(counts)
+    ld = moe.mx_tokens_cols(R, G)
+    _, p = O.pack_groups_t(np.zeros((R, 1)), np.concatenate([[0], np.cumsum(counts)]))
+    codes = torch.zeros((rows, ld), dtype=torch.uint8)
+    for i in range(G):
+        codes[:, p[i]:p[i] + counts[i]] = _int_codes(g, (rows, counts[i]))
+    sb = _scale_rows(g, (rows,), ld, lo, hi)
+    return codes, moe.mx_scales_from_rows(sb, ld), sb
+
+
+@pytest.mark.parametrize("K,N,dual,out16", [(64, 64, False, False), (320, 192, True, False),
+                                             (256, 512, False, True), (192, 320, True, True)])
+def test_grouped_gemm_dw_mx_exact(K, N, dual, out16):
+    """Integer codes with block scales 2^-2 .. 2^2 along the tokens: every partial sum is exact in
+    fp32, so dW (fp32) equals the oracle's ragged MX weight gradient exactly (bf16 output: its
+    rounding); empty groups give exact zeros; the dual form reads one At for two outputs."""
+    _say("dw mx exact", K, N, dual, out16)
+    g = torch.Generator().manual_seed(K * 7 + N + dual)
+    counts = [5, 0, 130, 128, 1, 300, 0, 61]
+    G, R = len(counts), sum(counts)
+    off = torch.tensor(np.concatenate([[0], np.cumsum(counts)]), dtype=torch.int32)
+    a, sa, sab = _tokens_operand(g, K, counts)
+    c, sc, scb = _tokens_operand(g, N, counts)
+    c2, sc2, sc2b = _tokens_operand(g, N, counts) if dual else (None, None, None)
+    rnd = O.bf16_round if out16 else (lambda v: v)
+    ref = rnd(O.grouped_gemm_dw_mx(_u8(a), _u8(sab), _u8(c), _u8(scb), off.numpy()))
+    D = lambda t: None if t is None else t.to(DEV)
+    out = moe.moe_grouped_gemm_dw_mx(D(a), D(sa), D(c), D(sc), D(off), R, D(c2), D(sc2), out_bf16=out16)
+    torch.cuda.synchronize()
+    dB = out[0] if dual else out
+    np.testing.assert_array_equal(f64(dB), ref)
+    if dual:
+        np.testing.assert_array_equal(f64(out[1]), rnd(O.grouped_gemm_dw_mx(_u8(a), _u8(sab), _u8(c2), _u8(sc2b),
+                                                                             off.numpy())))
+
+
+# ------------------------------------------------------------------------------------------------
 # The layer with its expert data products on MX operands, against an end-to-end oracle run
 # ------------------------------------------------------------------------------------------------
-def _oracle_layer_mx(inp, cfg):
+def _oracle_layer_mx(inp, cfg, mx_dw=False):
     """The layer's forward and backward with the four expert data products on MX operands (X_perm,
     the SwiGLU output, dY_perm and [dH_gate | dH_up] quantized per 32-element block of their rows,
     the weights per block of the matching contraction) and everything else as the bf16 oracle."""
@@ -355,35 +424,42 @@ def _oracle_layer_mx(inp, cfg):
     if shared is not None:
         dx_sh = O.dense_ffn_backward(fwd["shared"], x, dy, *shared)["dx"]
     dx = O.combine(dx_perm, None, ros, k, add=dx_sh)
+    if mx_dw:   # operands quantized along the tokens (the packed, 128-aligned token-major form)
+        qt = lambda v: q(O.pack_groups_t(v, off)[0])
+        dws = {"dw_down": O.grouped_gemm_dw_mx(*qt(act), *qt(dy_perm), off),
+               "dw_gate": O.grouped_gemm_dw_mx(*qt(xp), *qt(dhg), off),
+               "dw_up": O.grouped_gemm_dw_mx(*qt(xp), *qt(dhu), off)}
+    else:
+        dws = {"dw_down": O.grouped_gemm_dw(act, dy_perm, off), "dw_gate": O.grouped_gemm_dw(xp, dhg, off),
+               "dw_up": O.grouped_gemm_dw(xp, dhu, off)}
     return {"y": y, "y_perm": y_perm, "h_gate": hg, "h_up": hu, "act": act, "dy_perm": dy_perm,
-            "dh_gate": dhg, "dh_up": dhu, "dx_perm": dx_perm, "dx": dx,
-            "dw_down": O.grouped_gemm_dw(act, dy_perm, off), "dw_gate": O.grouped_gemm_dw(xp, dhg, off),
-            "dw_up": O.grouped_gemm_dw(xp, dhu, off),
+            "dh_gate": dhg, "dh_up": dhu, "dx_perm": dx_perm, "dx": dx, **dws,
             "w": {"gate_up_t": (gq, gs, uq, us), "down_t": (dq, ds), "down_r": (wdq, wds),
                   "gate_up_r": (wjq, wjs)}}
 
 
-@pytest.mark.parametrize("cfg_id", [0, 2])
-def test_layer_mx(cfg_id):
+@pytest.mark.parametrize("cfg_id,mx_dw", [(0, False), (2, False), (0, True), (2, True)])
+def test_layer_mx(cfg_id, mx_dw):
     """The layer with MX forward and data-gradient products (fp8_forward, fp8_backward, mx), two
     steps (the second re-quantizes the weights, both orientations from one read per weight): the
     weight codes and scale bytes bit for bit, and every output and gradient against the end-to-end
     oracle run, which quantizes its own bf16 intermediates (a code may differ where the two sides'
-    bf16 intermediates differ in the last bit; the tolerances cover that).  Config 2 at 1024
-    tokens."""
+    bf16 intermediates differ in the last bit; the tolerances cover that).  With mx_dw the weight
+    gradients run on operands quantized along the tokens as well.  Config 2 at 1024 tokens."""
     import dataclasses
     from paper_2606_26453_amd import layer as L, workloads as W
     cfg = W.CONFIGS[cfg_id]
     if cfg_id:
         cfg = dataclasses.replace(cfg, T=1024)
-    _say("layer mx", cfg)
+    _say("layer mx", cfg, mx_dw)
     inp = W.make_inputs(cfg, 0, "cpu")
-    lay = L.MoELayer(cfg, {k_: v.to(DEV) for k_, v in inp.items()}, fp8_forward=True, fp8_backward=True, mx=True)
+    lay = L.MoELayer(cfg, {k_: v.to(DEV) for k_, v in inp.items()}, fp8_forward=True, fp8_backward=True, mx=True,
+                     fp8_dw=mx_dw)
     lay.step()
     lay.step()
     torch.cuda.synchronize()
     b = lay.buf
-    ref = _oracle_layer_mx(inp, cfg)
+    ref = _oracle_layer_mx(inp, cfg, mx_dw)
     d, f, E = cfg.d, cfg.f, cfg.E
     gq, gs, uq, us = ref["w"]["gate_up_t"]
     lq = _u8(lay.wmx["gate_up_t"][0]).reshape(E, f // 128, 2, 128, d)
@@ -470,3 +546,44 @@ def test_mx_fullsize_sampled():
         og, ou = O.swiglu_bwd(pick(hg0, cfi), pick(hu0, cfi), O.grouped_gemm_mx(yr, yrs, rqe, rse, sub))
         check_float(f"dh_gate e{e}", pick(dhg, cfi), og, 4e-3)
         check_float(f"dh_up e{e}", pick(dhu, cfi), ou, 4e-3)
+
+
+def test_mx_dw_fullsize_sampled():
+    """The MX weight gradients at the Mixtral-shaped layer's full size (R = 16384 routed rows over 8
+    experts, d = 4096, f = 14336) on seeded Gaussian operands: the four token-major quantizations and
+    the dual gate/up and single down products as the layer runs them; 16 sampled rows x 64 sampled
+    columns of each output for the first and the last expert against the oracle's MX weight
+    gradient of its own token-major codes of the sampled columns."""
+    from paper_2606_26453_amd import workloads as W
+    cfg = W.CONFIGS[1]
+    R, d, f, E = cfg.T * cfg.k, cfg.d, cfg.f, cfg.E
+    _say("mx dW full size", R, d, f, E)
+    g = torch.Generator(device=DEV).manual_seed(15)
+    counts = [R // E - 37, R // E + 37] * (E // 2)
+    off_np = np.concatenate([[0], np.cumsum(counts)])
+    off = torch.tensor(off_np, dtype=torch.int32, device=DEV)
+    rnd = lambda shape, s_=1.0: (torch.randn(shape, generator=g, device=DEV) * s_).to(torch.bfloat16)
+    x, act, dy, dhg, dhu = rnd((R, d)), rnd((R, f)), rnd((R, d), 1e-3), rnd((R, f), 1e-3), rnd((R, f), 1e-3)
+    xq, xs = moe.moe_quantize_mx_tokens_t(x, off)
+    aq, as_ = moe.moe_quantize_mx_tokens_t(act, off)
+    yq, ys = moe.moe_quantize_mx_tokens_t(dy, off)
+    gq, gs = moe.moe_quantize_mx_tokens_t(dhg, off)
+    uq, us = moe.moe_quantize_mx_tokens_t(dhu, off)
+    dw_g, dw_u = moe.moe_grouped_gemm_dw_mx(xq, xs, gq, gs, off, R, uq, us)
+    del xq, gq, uq
+    dw_d = moe.moe_grouped_gemm_dw_mx(aq, as_, yq, ys, off, R)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(16)
+    q = O.quantize_rows_mx
+    qt = lambda t, cols: q(O.pack_groups_t(f64(t[:, torch.tensor(cols, device=DEV)]), off_np)[0])
+    for e in (0, E - 1):
+        rd = np.sort(rng.choice(d, 16, replace=False))
+        cf = np.sort(rng.choice(f, 64, replace=False))
+        rf = np.sort(rng.choice(f, 16, replace=False))
+        cd = np.sort(rng.choice(d, 64, replace=False))
+        pick = lambda t, r, c: f64(t[e][torch.tensor(r, device=DEV)][:, torch.tensor(c, device=DEV)])
+        xr = qt(x, rd)
+        check_float(f"dw_gate e{e}", pick(dw_g, rd, cf), O.grouped_gemm_dw_mx(*xr, *qt(dhg, cf), off_np)[e], 2e-3)
+        check_float(f"dw_up e{e}", pick(dw_u, rd, cf), O.grouped_gemm_dw_mx(*xr, *qt(dhu, cf), off_np)[e], 2e-3)
+        check_float(f"dw_down e{e}", pick(dw_d, rf, cd), O.grouped_gemm_dw_mx(*qt(act, rf), *qt(dy, cd), off_np)[e],
+                    2e-3)
