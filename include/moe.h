@@ -471,13 +471,16 @@ moe_status moe_quantize_mx_tokens_t(const moe_bf16* x, const int32_t* offsets, i
  * (dB2[g] from dC2t, the dual gate/up form reading each At tile once) = sum over the group's
  * tokens of mx(At)[:, t] mx(dCt)[:, t]^T, E4M3 products scaled and accumulated in fp32 by the
  * matrix cores, stored fp32 (out_bf16 = 0) or rounded once to bf16.  Empty groups give zeros.
- * K, N multiples of 64; ld as for moe_quantize_mx_tokens_t; max(K, N) * ld < 2^31.  Errors as
- * moe_grouped_gemm_dw_t; scale pointers 4-byte aligned; dC2t, c2_scale and dB2 all set or all NULL.
+ * K, N multiples of 64; ld as for moe_quantize_mx_tokens_t; max(K, N) * ld < 2^31.  counters: NULL
+ * (one workgroup per tile) or 8 int32 of device memory for a persistent grid that claims its tiles,
+ * as moe_grouped_gemm_dw_persistent (zeroed here, on `stream`; calls sharing them must be ordered).
+ * Errors as moe_grouped_gemm_dw_t; scale pointers 4-byte aligned; dC2t, c2_scale and dB2 all set or
+ * all NULL.
  */
 moe_status moe_grouped_gemm_dw_mx(const uint8_t* At, const uint8_t* a_scale, const uint8_t* dCt,
                                   const uint8_t* c_scale, const uint8_t* dC2t, const uint8_t* c2_scale,
                                   const int32_t* offsets, int32_t G, int64_t R, int64_t K, int64_t N, int64_t ld,
-                                  void* dB, void* dB2, int32_t out_bf16, hipStream_t stream);
+                                  void* dB, void* dB2, int32_t out_bf16, int32_t* counters, hipStream_t stream);
 
 /*
  * moe_grouped_gemm_fwd with the same split of the last, partial round of tiles (same arguments,

@@ -1329,7 +1329,7 @@ template <int KIND, bool DUAL, bool ACT, bool OUT16 = false, bool GATHER = false
 moe_status launch(const GemmParams& p, int64_t tiles_bound, hipStream_t stream, const char* name) {
   if (tiles_bound == 0) return MOE_SUCCESS;
   if (tiles_bound >= ((int64_t)1 << 31) - SPLIT_UNITS) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: too many tiles", name);
-  static_assert(!QUEUE || KIND == KIND_DW, "tile queues: the dW product");
+  static_assert(!QUEUE || KIND == KIND_DW || KIND == KIND_DWT, "tile queues: the dW products");
   using C = Cfg<KIND>;
   constexpr bool PERSIST = C::PERSIST || QUEUE;
   // persistent grid: one workgroup per CU slot (a multiple of 8, one share per XCD), or one per
@@ -1801,8 +1801,11 @@ extern "C" moe_status moe_grouped_gemm_dw_t(const moe_bf16* At, const moe_bf16* 
 extern "C" moe_status moe_grouped_gemm_dw_mx(const uint8_t* At, const uint8_t* a_scale, const uint8_t* dCt,
                                              const uint8_t* c_scale, const uint8_t* dC2t, const uint8_t* c2_scale,
                                              const int32_t* offsets, int32_t G, int64_t R, int64_t K, int64_t N,
-                                             int64_t ld, void* dB, void* dB2, int32_t out_bf16, hipStream_t stream) {
+                                             int64_t ld, void* dB, void* dB2, int32_t out_bf16, int32_t* counters,
+                                             hipStream_t stream) {
   const char* fn = "moe_grouped_gemm_dw_mx";
+  if (reinterpret_cast<uintptr_t>(counters) & 3u)
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: counters must be 8 int32 of device memory", fn);
   if (G < 1 || G > 256) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: need 1 <= G <= 256", fn);
   if (R < 0 || K <= 0 || N <= 0) return fail(MOE_ERROR_INVALID_VALUE, "%s: bad size", fn);
   if (K % 64 || N % 64) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: K and N must be multiples of 64", fn);
@@ -1833,6 +1836,16 @@ extern "C" moe_status moe_grouped_gemm_dw_mx(const uint8_t* At, const uint8_t* a
   const int cols_per_tile = dC2t ? TN / 2 : TN;
   p.n_tiles = (int)((N + cols_per_tile - 1) / cols_per_tile);
   const int64_t tiles = (int64_t)G * p.m_tiles * p.n_tiles;
+  if (counters != nullptr && tiles > 0) {   // persistent grid claiming its tiles, as the bf16 dW
+    p.tile_queue = counters;
+    zero_i32_kernel<<<1, 64, 0, stream>>>(counters, 8);
+    if (out_bf16) {
+      if (dC2t) return launch<KIND_DWT, true, false, true, false, true, true, true>(p, tiles, stream, fn);
+      return launch<KIND_DWT, false, false, true, false, true, true, true>(p, tiles, stream, fn);
+    }
+    if (dC2t) return launch<KIND_DWT, true, false, false, false, true, true, true>(p, tiles, stream, fn);
+    return launch<KIND_DWT, false, false, false, false, true, true, true>(p, tiles, stream, fn);
+  }
   if (out_bf16) {
     if (dC2t) return launch<KIND_DWT, true, false, true, false, true, false, true>(p, tiles, stream, fn);
     return launch<KIND_DWT, false, false, true, false, true, false, true>(p, tiles, stream, fn);

@@ -342,7 +342,7 @@ class MoELayer(_Traced):
             run("quantize_t_dy", moe.moe_quantize_mx_tokens_t, b["dy_perm"], b["offsets"], b["dy_qt"], b["dy_st"],
                 stream=side)
             run("dw_down", moe.moe_grouped_gemm_dw_mx, b["act_qt"], b["act_st"], b["dy_qt"], b["dy_st"],
-                b["offsets"], self.R, dB=b["dw_down"], stream=side)
+                b["offsets"], self.R, dB=b["dw_down"], counters=self.dw_cnt, stream=side)
         elif self.dw_t:
             run("transpose_act", moe.moe_transpose_grouped, b["act"], b["offsets"], dst=b["act_t"], stream=side)
             run("transpose_dy_perm", moe.moe_transpose_grouped, b["dy_perm"], b["offsets"], dst=b["dy_perm_t"],
@@ -399,7 +399,8 @@ class MoELayer(_Traced):
                 stream=side)
             run("quantize_t_dh", self._quantize_t_dh, stream=side)
             run("dw_gate_up", moe.moe_grouped_gemm_dw_mx, b["x_qt"], b["x_st"], b["dhg_qt"], b["dhg_st"],
-                b["offsets"], self.R, b["dhu_qt"], b["dhu_st"], dB=b["dw_gate"], dB2=b["dw_up"], stream=side)
+                b["offsets"], self.R, b["dhu_qt"], b["dhu_st"], dB=b["dw_gate"], dB2=b["dw_up"],
+                counters=self.dw_cnt, stream=side)
         elif self.dw_t:
             run("transpose_x_perm", moe.moe_transpose_grouped, b["x_perm"], b["offsets"], dst=b["x_perm_t"],
                 stream=side)

@@ -60,7 +60,7 @@ _SIG = {
     "moe_mx_tokens_cols_bound": (_I64, [_I64, _I32]),
     "moe_quantize_mx_tokens_t": (ctypes.c_int, [_P, _P, _I32, _I64, _I64, _P, _P, _I64, _P]),
     "moe_grouped_gemm_dw_mx": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _I64, _P, _P,
-                                              _I32, _P]),
+                                              _I32, _P, _P]),
     "moe_quantize_mx_rows": (ctypes.c_int, [_P, _P, _I64, _I64, _P, _P, _P]),
     "moe_quantize_mx_weight": (ctypes.c_int, [_P, _P, _I64, _I64, _I64, _P, _P, _P, _P, _P]),
     "moe_grouped_gemm_fwd_mx": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P,
@@ -624,9 +624,9 @@ def moe_quantize_mx_tokens_t(x, offsets, qt=None, st=None, stream=None):
 
 
 def moe_grouped_gemm_dw_mx(At, a_scale, dCt, c_scale, offsets, R, dC2t=None, c2_scale=None, dB=None, dB2=None,
-                           out_bf16=False, stream=None):
+                           out_bf16=False, counters=None, stream=None):
     """The weight gradient on token-major MX operands (moe_quantize_mx_tokens_t): dB [G, K, N]
-    (dB2 from dC2t), fp32 or bf16."""
+    (dB2 from dC2t), fp32 or bf16; with counters (dw_counters), a persistent grid claiming tiles."""
     K, ld = At.shape
     N = dCt.shape[0]
     G = offsets.numel() - 1
@@ -645,7 +645,7 @@ def moe_grouped_gemm_dw_mx(At, a_scale, dCt, c_scale, offsets, R, dC2t=None, c2_
     _check("moe_grouped_gemm_dw_mx",
            lib().moe_grouped_gemm_dw_mx(_ptr(At), _ptr(a_scale), _ptr(dCt), _ptr(c_scale), _ptr(dC2t), _ptr(c2_scale),
                                         _ptr(offsets), G, R, K, N, ld, _ptr(dB), _ptr(dB2) if dC2t is not None else None,
-                                        int(out_bf16), _stream(stream)))
+                                        int(out_bf16), _ptr(counters), _stream(stream)))
     return (dB, dB2) if dC2t is not None else dB
 
 

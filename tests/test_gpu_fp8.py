@@ -458,3 +458,71 @@ def test_layer_fp8_backward(cfg_id):
     fwd = O.layer_forward(x, inp["logits"].numpy(), wg, wu, wd, cfg.k, shared=shared)
     bwd = O.layer_backward(fwd, x, f64(inp["dy"]), wg, wu, wd, shared=shared)
     _say(f"fp8 data gradient dX vs the all-bf16 oracle: relative Frobenius {O.rel_fro(f64(b['dx']), bwd['dx']):.3e}")
+
+
+def _oracle_layer_fp8(inp, cfg):
+    """The layer's forward and backward with the four expert data products on E4M3 operands with
+    fp32 scales (X_perm, the SwiGLU output, dY_perm and [dH_gate | dH_up] per row; the forward
+    weights per output channel, the data-gradient weights per row of their stored layouts), every
+    quantization applied by the oracle to its own bf16 intermediates; the rest as the bf16 oracle."""
+    x = f64(inp["x"])
+    wg, wu, wd = (f64(inp[n]) for n in ("w_gate", "w_up", "w_down"))
+    shared = None
+    if cfg.f_shared:
+        shared = tuple(f64(inp[n]) for n in ("w_gate_sh", "w_up_sh", "w_down_sh"))
+    k = cfg.k
+    q = O.quantize_rows_fp8
+    idx, tw = O.route_topk(inp["logits"].numpy(), k)
+    off, ros, tor = O.permute(idx, cfg.E)
+    xp = O.gather(x, tor)
+    xq, xs = q(xp)
+    gq, gs = q(np.transpose(wg, (0, 2, 1)))
+    uq, us = q(np.transpose(wu, (0, 2, 1)))
+    dq, ds = q(np.transpose(wd, (0, 2, 1)))
+    hg = O.grouped_gemm_fp8(xq, xs, gq, gs, off)
+    hu = O.grouped_gemm_fp8(xq, xs, uq, us, off)
+    act = O.swiglu(hg, hu)
+    aq, as_ = q(act)
+    y_perm = O.grouped_gemm_fp8(aq, as_, dq, ds, off)
+    y_sh = dx_sh = None
+    dy = f64(inp["dy"])
+    if shared is not None:
+        sf = O.dense_ffn_forward(x, *shared)
+        y_sh = sf["y"]
+        dx_sh = O.dense_ffn_backward(sf, x, dy, *shared)["dx"]
+    y = O.combine(y_perm, tw, ros, k, add=y_sh)
+    dy_perm, _ = O.combine_bwd(dy, tw, ros, y_perm, k)
+    yq, ys = q(dy_perm)
+    rq, rs = q(wd)
+    dhg, dhu = O.swiglu_bwd(hg, hu, O.grouped_gemm_fp8(yq, ys, rq, rs, off))
+    hq, hs = q(np.concatenate([dhg, dhu], axis=1))
+    jq, js = q(np.concatenate([wg, wu], axis=2))
+    dx_perm = O.grouped_gemm_fp8(hq, hs, jq, js, off)
+    dx = O.combine(dx_perm, None, ros, k, add=dx_sh)
+    return {"y": y, "y_perm": y_perm, "h_gate": hg, "h_up": hu, "act": act, "dy_perm": dy_perm,
+            "dh_gate": dhg, "dh_up": dhu, "dx_perm": dx_perm, "dx": dx,
+            "dw_down": O.grouped_gemm_dw(act, dy_perm, off), "dw_gate": O.grouped_gemm_dw(xp, dhg, off),
+            "dw_up": O.grouped_gemm_dw(xp, dhu, off)}
+
+
+@pytest.mark.parametrize("cfg_id", [0, 2])
+def test_layer_fp8_end_to_end(cfg_id):
+    """The layer with FP8 (fp32-scale) forward and data-gradient products, two steps, against an
+    end-to-end oracle run that quantizes its own bf16 intermediates (no GPU tensor enters the
+    oracle): every output and gradient within 1e-2 (a code may differ where the two sides' bf16
+    intermediates differ in the last bit).  Config 2 at 1024 tokens."""
+    import dataclasses
+    from paper_2606_26453_amd import layer as L, workloads as W
+    cfg = W.CONFIGS[cfg_id]
+    if cfg_id:
+        cfg = dataclasses.replace(cfg, T=1024)
+    _say("layer fp8 end to end", cfg)
+    inp = W.make_inputs(cfg, 0, "cpu")
+    lay = L.MoELayer(cfg, {k_: v.to(DEV) for k_, v in inp.items()}, fp8_forward=True, fp8_backward=True)
+    lay.step()
+    lay.step()
+    torch.cuda.synchronize()
+    ref = _oracle_layer_fp8(inp, cfg)
+    for key in ("h_gate", "h_up", "act", "y_perm", "y", "dy_perm", "dh_gate", "dh_up", "dx_perm", "dx",
+                "dw_down", "dw_gate", "dw_up"):
+        check_float(key, f64(lay.buf[key]), ref[key], 1e-2)

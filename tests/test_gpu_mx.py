@@ -371,13 +371,15 @@ def test_grouped_gemm_dw_mx_exact(K, N, dual, out16):
     rnd = O.bf16_round if out16 else (lambda v: v)
     ref = rnd(O.grouped_gemm_dw_mx(_u8(a), _u8(sab), _u8(c), _u8(scb), off.numpy()))
     D = lambda t: None if t is None else t.to(DEV)
-    out = moe.moe_grouped_gemm_dw_mx(D(a), D(sa), D(c), D(sc), D(off), R, D(c2), D(sc2), out_bf16=out16)
-    torch.cuda.synchronize()
-    dB = out[0] if dual else out
-    np.testing.assert_array_equal(f64(dB), ref)
-    if dual:
-        np.testing.assert_array_equal(f64(out[1]), rnd(O.grouped_gemm_dw_mx(_u8(a), _u8(sab), _u8(c2), _u8(sc2b),
-                                                                             off.numpy())))
+    ref2 = rnd(O.grouped_gemm_dw_mx(_u8(a), _u8(sab), _u8(c2), _u8(sc2b), off.numpy())) if dual else None
+    for cnt in (None, moe.dw_counters(DEV)):   # one workgroup per tile; persistent with tile claims
+        out = moe.moe_grouped_gemm_dw_mx(D(a), D(sa), D(c), D(sc), D(off), R, D(c2), D(sc2), out_bf16=out16,
+                                         counters=cnt)
+        torch.cuda.synchronize()
+        dB = out[0] if dual else out
+        np.testing.assert_array_equal(f64(dB), ref)
+        if dual:
+            np.testing.assert_array_equal(f64(out[1]), ref2)
 
 
 # ------------------------------------------------------------------------------------------------
