@@ -466,6 +466,19 @@ moe_status moe_quantize_mx_tokens_t(const moe_bf16* x, const int32_t* offsets, i
                                     uint8_t* qt, uint8_t* st, int64_t ld, hipStream_t stream);
 
 /*
+ * Both MX orientations of a routed buffer from one read: qt/st as moe_quantize_mx_tokens_t (may be
+ * NULL) and the row-wise codes of moe_quantize_mx_rows written into a row buffer of ldr columns at
+ * column col0: qr[r, col0 + c] for c < C, scales sr in the MX scale layout of R rows of ldr (blocks
+ * col0/32 ..).  Two calls with col0 = 0 and col0 = C fill the joined rows [x | x2] of the gate/up
+ * data gradient.  col0 a multiple of 64, ldr of 32, col0 + C <= ldr; qr 8-byte aligned; qt/st and
+ * qr/sr each given together, at least one pair.  Other arguments and errors as
+ * moe_quantize_mx_tokens_t.
+ */
+moe_status moe_quantize_mx_tokens(const moe_bf16* x, const int32_t* offsets, int32_t G, int64_t R, int64_t C,
+                                  uint8_t* qt, uint8_t* st, int64_t ld, uint8_t* qr, uint8_t* sr, int64_t ldr,
+                                  int64_t col0, hipStream_t stream);
+
+/*
  * The weight gradient on MX operands (Appendix H's dW1_e = X_e^T G_e; also dW_down): At [K, ld] and
  * dCt (dC2t) [N, ld] as moe_quantize_mx_tokens_t writes them (with their scales), dB[g] [K, N]
  * (dB2[g] from dC2t, the dual gate/up form reading each At tile once) = sum over the group's

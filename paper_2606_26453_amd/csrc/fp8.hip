@@ -397,10 +397,15 @@ __global__ __launch_bounds__(256) void quantize_mx_weight_kernel(const uint16_t*
 // Workgroup (64-column block n0 = 64*bx of x, 128-column block j0 = 128*by of qt) stages the 128
 // source rows that land in columns j0 .. j0+127 (zeros past the group's end) and quantizes them
 // column by column as the weight kernel's transposed half does; blocks past p[G] are left alone.
+// With qr, the same read also gives the row-wise codes (every source row lies in exactly one such
+// tile): row r's blocks of 32 columns go to qr[r, col0 + c] (rows of ldr bytes, e.g. one half of
+// the joined rows [dH_gate | dH_up]) with scales in the MX layout of R rows of ldr.
 __global__ __launch_bounds__(256) void quantize_mx_tokens_t_kernel(const uint16_t* __restrict__ x,
                                                                    const int32_t* __restrict__ offsets, int G,
-                                                                   int64_t C, int64_t ld, uint8_t* __restrict__ qt,
-                                                                   uint8_t* __restrict__ st) {
+                                                                   int64_t R, int64_t C, int64_t ld,
+                                                                   uint8_t* __restrict__ qt, uint8_t* __restrict__ st,
+                                                                   uint8_t* __restrict__ qr, uint8_t* __restrict__ sr,
+                                                                   int64_t ldr, int64_t col0) {
   __shared__ int s_o[257];
   __shared__ int s_p[257];
   __shared__ __attribute__((aligned(16))) uint16_t s_w[128 * 64];
@@ -429,7 +434,24 @@ __global__ __launch_bounds__(256) void quantize_mx_tokens_t_kernel(const uint16_
     u32x4 v = {0u, 0u, 0u, 0u};
     if (r < src_end) v = *reinterpret_cast<const u32x4*>(x + r * C + n0 + 8 * c8);
     *reinterpret_cast<u32x4*>(s_w + kl * 64 + 8 * c8) = v;
+    if (qr != nullptr) {   // uniform; lanes t^1, t^2 share the block (same row)
+      float m = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) m = fmaxf(m, fmaxf(fabsf(bf16_lo(v[e])), fabsf(bf16_hi(v[e]))));
+      m = fmaxf(m, __shfl_xor(m, 1));
+      m = fmaxf(m, __shfl_xor(m, 2));
+      const uint32_t byte = mx_scale_byte(m);
+      const float inv = mx_inv_scale(byte);
+      if (r < src_end) {
+        const int64_t col = col0 + n0 + 8 * c8;
+        *reinterpret_cast<uint2*>(qr + r * ldr + col) =
+            make_uint2(e4m3_pack4(bf16_lo(v[0]), bf16_hi(v[0]), bf16_lo(v[1]), bf16_hi(v[1]), inv),
+                       e4m3_pack4(bf16_lo(v[2]), bf16_hi(v[2]), bf16_lo(v[3]), bf16_hi(v[3]), inv));
+        if ((c8 & 3) == 0) sr[mx_scale_at(r, col >> 5, R)] = (uint8_t)byte;
+      }
+    }
   }
+  if (qt == nullptr) return;   // uniform
   __syncthreads();
   const int n = t & 63, kb = t >> 6;
   uint32_t o[8];
@@ -447,9 +469,11 @@ extern "C" int64_t moe_mx_tokens_cols_bound(int64_t R, int32_t G) {
   return R < 0 || G < 1 ? 0 : (R + 127 * (int64_t)G + 127) / 128 * 128;
 }
 
-extern "C" moe_status moe_quantize_mx_tokens_t(const moe_bf16* x, const int32_t* offsets, int32_t G, int64_t R,
-                                               int64_t C, uint8_t* qt, uint8_t* st, int64_t ld, hipStream_t stream) {
-  const char* fn = "moe_quantize_mx_tokens_t";
+namespace moe {
+namespace {
+moe_status quantize_mx_tokens_impl(const char* fn, const moe_bf16* x, const int32_t* offsets, int32_t G, int64_t R,
+                                   int64_t C, uint8_t* qt, uint8_t* st, int64_t ld, uint8_t* qr, uint8_t* sr,
+                                   int64_t ldr, int64_t col0, hipStream_t stream) {
   if (G < 1 || G > 256) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: need 1 <= G <= 256", fn);
   if (R < 0 || C <= 0) return fail(MOE_ERROR_INVALID_VALUE, "%s: bad size", fn);
   if (C % 64) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: C must be a multiple of 64", fn);
@@ -457,13 +481,33 @@ extern "C" moe_status moe_quantize_mx_tokens_t(const moe_bf16* x, const int32_t*
     return fail(MOE_ERROR_INVALID_VALUE, "%s: ld must be a multiple of 128 and >= %lld", fn,
                 (long long)moe_mx_tokens_cols_bound(R, G));
   if (ld / 128 > 65535 || C / 64 > 0x7fffffff) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: too many columns", fn);
-  if (!offsets || !qt || !st || (R > 0 && !x)) return fail(MOE_ERROR_INVALID_VALUE, "%s: NULL pointer", fn);
-  if ((x && !aligned16(x)) || !aligned16(qt))
-    return fail(MOE_ERROR_INVALID_VALUE, "%s: x and qt must be 16-byte aligned", fn);
+  if ((qt == nullptr) != (st == nullptr) || (qr == nullptr) != (sr == nullptr) || (!qt && !qr))
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: give qt with st and/or qr with sr", fn);
+  if (qr && (col0 < 0 || col0 % 64 || ldr % 32 || col0 + C > ldr))
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: need col0 a multiple of 64, ldr of 32, col0 + C <= ldr", fn);
+  if (!offsets || (R > 0 && !x)) return fail(MOE_ERROR_INVALID_VALUE, "%s: NULL pointer", fn);
+  if ((x && !aligned16(x)) || (qt && !aligned16(qt)) || (reinterpret_cast<uintptr_t>(qr) & 7))
+    return fail(MOE_ERROR_INVALID_VALUE, "%s: x and qt must be 16-byte, qr 8-byte aligned", fn);
   if (R == 0) return MOE_SUCCESS;
   quantize_mx_tokens_t_kernel<<<dim3((unsigned)(C / 64), (unsigned)(ld / 128)), 256, 0, stream>>>(
-      x, offsets, G, C, ld, qt, st);
+      x, offsets, G, R, C, ld, qt, st, qr, sr, ldr, col0);
   return check_launch("quantize_mx_tokens_t_kernel");
+}
+}  // namespace
+}  // namespace moe
+
+extern "C" moe_status moe_quantize_mx_tokens_t(const moe_bf16* x, const int32_t* offsets, int32_t G, int64_t R,
+                                               int64_t C, uint8_t* qt, uint8_t* st, int64_t ld, hipStream_t stream) {
+  if (!qt || !st) return fail(MOE_ERROR_INVALID_VALUE, "moe_quantize_mx_tokens_t: NULL pointer");
+  return quantize_mx_tokens_impl("moe_quantize_mx_tokens_t", x, offsets, G, R, C, qt, st, ld, nullptr, nullptr, 0,
+                                 0, stream);
+}
+
+extern "C" moe_status moe_quantize_mx_tokens(const moe_bf16* x, const int32_t* offsets, int32_t G, int64_t R,
+                                             int64_t C, uint8_t* qt, uint8_t* st, int64_t ld, uint8_t* qr,
+                                             uint8_t* sr, int64_t ldr, int64_t col0, hipStream_t stream) {
+  return quantize_mx_tokens_impl("moe_quantize_mx_tokens", x, offsets, G, R, C, qt, st, ld, qr, sr, ldr, col0,
+                                 stream);
 }
 
 extern "C" moe_status moe_quantize_mx_rows(const moe_bf16* x, const moe_bf16* x2, int64_t M, int64_t K, uint8_t* q,

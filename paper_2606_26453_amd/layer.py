@@ -77,6 +77,8 @@ class MoELayer(_Traced):
         # block spans two experts) that moe_grouped_gemm_dw_mx reads
         if fp8_dw and not mx:
             raise ValueError("fp8_dw takes MX block scales (mx=True)")
+        if fp8_dw and concurrent:
+            raise ValueError("fp8_dw shares its quantizations with the data products: one stream")
         self.fp8_dw = fp8_dw
         # combine_fused: the weighted combine runs in the down product's epilogue
         # (moe_grouped_gemm_fwd_combine: the tile that stores a token's last row of a column tile
@@ -266,10 +268,16 @@ class MoELayer(_Traced):
             ws = self.split_ws
             if self.fp8_requantize:
                 run("quantize_w", self._quantize_weights_mx, stream=stream)
-            run("quantize_x", moe.moe_quantize_mx_rows, b["x_perm"], None, b["x_q"], b["x_s"], stream=stream)
+            if self.fp8_dw:   # X_perm's row codes and, from the same read, its token-major codes for dW
+                run("quantize_x", self._quantize_mx_both, "x_perm", "x", "x_q", "x_s", stream=stream)
+            else:
+                run("quantize_x", moe.moe_quantize_mx_rows, b["x_perm"], None, b["x_q"], b["x_s"], stream=stream)
             run("fwd_gate_up", moe.moe_grouped_gemm_fwd_mx_gate_up, b["x_q"], b["x_s"], *self.wmx["gate_up_t"],
                 b["offsets"], b["h_gate"], b["h_up"], b["act"], stream=stream, workspace=ws)
-            run("quantize_act", moe.moe_quantize_mx_rows, b["act"], None, b["act_q"], b["act_s"], stream=stream)
+            if self.fp8_dw:
+                run("quantize_act", self._quantize_mx_both, "act", "act", "act_q", "act_s", stream=stream)
+            else:
+                run("quantize_act", moe.moe_quantize_mx_rows, b["act"], None, b["act_q"], b["act_s"], stream=stream)
             run("fwd_down", moe.moe_grouped_gemm_fwd_mx, b["act_q"], b["act_s"], *self.wmx["down_t"], b["offsets"],
                 C=b["y_perm"], stream=stream, workspace=ws)
         elif self.fp8:
@@ -335,12 +343,15 @@ class MoELayer(_Traced):
             run("router_bwd", moe.moe_router_bwd, i["x"], i["wr"], b["logits"], b["topk_idx"], b["topk_w"],
                 b["d_topk_w"], b["offsets"], self.normalize, self.aux_alpha, dx=None, workspace=b["router_ws"],
                 dlogits=b["dlogits"], dwr=b["dwr"], stream=stream)
+        if self.fp8_dw:                   # dY_perm's token-major codes (and its row codes for dX down)
+            if self.fp8_bwd:
+                run("quantize_dy", self._quantize_mx_both, "dy_perm", "dy", "dy_q", "dy_s", stream=stream)
+            else:
+                run("quantize_t_dy", self._quantize_mx_both, "dy_perm", "dy", None, None, stream=stream)
         self._join(side, main)            # dW_down needs dY_perm
         if self.fp8_dw:
-            run("quantize_t_act", moe.moe_quantize_mx_tokens_t, b["act"], b["offsets"], b["act_qt"], b["act_st"],
-                stream=side)
-            run("quantize_t_dy", moe.moe_quantize_mx_tokens_t, b["dy_perm"], b["offsets"], b["dy_qt"], b["dy_st"],
-                stream=side)
+            if not self.fp8:              # else the forward's quantization wrote them
+                run("quantize_t_act", self._quantize_mx_both, "act", "act", None, None, stream=side)
             run("dw_down", moe.moe_grouped_gemm_dw_mx, b["act_qt"], b["act_st"], b["dy_qt"], b["dy_st"],
                 b["offsets"], self.R, dB=b["dw_down"], counters=self.dw_cnt, stream=side)
         elif self.dw_t:
@@ -355,7 +366,8 @@ class MoELayer(_Traced):
         if self.fp8_bwd and self.mx:
             if self.fp8_requantize and not self.fp8:   # else the forward's pass wrote both orientations
                 run("quantize_w_bwd", self._quantize_weights_mx, stream=stream)
-            run("quantize_dy", moe.moe_quantize_mx_rows, b["dy_perm"], None, b["dy_q"], b["dy_s"], stream=stream)
+            if not self.fp8_dw:
+                run("quantize_dy", moe.moe_quantize_mx_rows, b["dy_perm"], None, b["dy_q"], b["dy_s"], stream=stream)
             run("dx_down_swiglu_bwd", moe.moe_grouped_gemm_dx_swiglu_bwd_mx, b["dy_q"], b["dy_s"],
                 *self.wmx["down_r"], b["offsets"], b["h_gate"], b["h_up"], b["dh_gate"], b["dh_up"], stream=stream,
                 workspace=self.split_ws)
@@ -377,8 +389,11 @@ class MoELayer(_Traced):
                 b["dh_up"], stream=stream)
         self._join(side, main)            # dW_gate/dW_up need dH
         if self.fp8_bwd and self.mx:
-            run("quantize_dh", moe.moe_quantize_mx_rows, b["dh_gate"], b["dh_up"], b["dh_q"], b["dh_s"],
-                stream=stream)
+            if self.fp8_dw:               # the joined rows' codes and both token-major codes, one read
+                run("quantize_dh", self._quantize_mx_dh, True, stream=stream)
+            else:
+                run("quantize_dh", moe.moe_quantize_mx_rows, b["dh_gate"], b["dh_up"], b["dh_q"], b["dh_s"],
+                    stream=stream)
             run("dx_gate_up", moe.moe_grouped_gemm_fwd_mx, b["dh_q"], b["dh_s"], *self.wmx["gate_up_r"],
                 b["offsets"], C=b["dx_perm"], stream=stream, workspace=self.split_ws)
         elif self.fp8_bwd:
@@ -395,9 +410,10 @@ class MoELayer(_Traced):
         if early:
             self._unpermute_dx(dx_add, stream)
         if self.fp8_dw:
-            run("quantize_t_x", moe.moe_quantize_mx_tokens_t, b["x_perm"], b["offsets"], b["x_qt"], b["x_st"],
-                stream=side)
-            run("quantize_t_dh", self._quantize_t_dh, stream=side)
+            if not self.fp8:
+                run("quantize_t_x", self._quantize_mx_both, "x_perm", "x", None, None, stream=side)
+            if not self.fp8_bwd:
+                run("quantize_t_dh", self._quantize_mx_dh, False, stream=side)
             run("dw_gate_up", moe.moe_grouped_gemm_dw_mx, b["x_qt"], b["x_st"], b["dhg_qt"], b["dhg_st"],
                 b["offsets"], self.R, b["dhu_qt"], b["dhu_st"], dB=b["dw_gate"], dB2=b["dw_up"],
                 counters=self.dw_cnt, stream=side)
@@ -432,10 +448,22 @@ class MoELayer(_Traced):
     def R(self):
         return self.cfg.T * self.cfg.k
 
-    def _quantize_t_dh(self, stream=None):
+    def _quantize_mx_both(self, src, tok, q, s, stream=None):
+        """Token-major MX codes of buffer `src` (into `tok`_qt/_st) and, when q is given, its row codes
+        (into q/s), from one read."""
         b = self.buf
-        moe.moe_quantize_mx_tokens_t(b["dh_gate"], b["offsets"], b["dhg_qt"], b["dhg_st"], stream=stream)
-        moe.moe_quantize_mx_tokens_t(b["dh_up"], b["offsets"], b["dhu_qt"], b["dhu_st"], stream=stream)
+        moe.moe_quantize_mx_tokens(b[src], b["offsets"], b[tok + "_qt"], b[tok + "_st"],
+                                   qr=None if q is None else b[q], sr=None if s is None else b[s],
+                                   want_r=q is not None, stream=stream)
+
+    def _quantize_mx_dh(self, rows, stream=None):
+        """Token-major MX codes of dH_gate and dH_up and, with rows, the codes of the joined rows
+        [dH_gate | dH_up] (each half written by the call that reads it)."""
+        b, f = self.buf, self.cfg.f
+        for src, tok, col0 in (("dh_gate", "dhg", 0), ("dh_up", "dhu", f)):
+            moe.moe_quantize_mx_tokens(b[src], b["offsets"], b[tok + "_qt"], b[tok + "_st"],
+                                       qr=b["dh_q"] if rows else None, sr=b["dh_s"] if rows else None,
+                                       col0=col0, want_r=rows, stream=stream)
 
     def _transpose_dh(self, stream=None):
         b = self.buf
@@ -459,7 +487,8 @@ class MoELayer(_Traced):
                               + (0 if self.gather_fused else T * d * 2 + R * d * 2)),
             "gather_x": ("bytes", T * d * 2 + R * d * 2 + R * 4),
             # FP8 forward: E4M3 products (8-bit MFMA work), quantizers and the standalone SwiGLU
-            "quantize_x": ("bytes", R * d * 3 + R * sc(d)), "quantize_act": ("bytes", R * f * 3 + R * sc(f)),
+            "quantize_x": ("bytes", R * d * (4 if self.fp8_dw else 3) + R * sc(d) * (2 if self.fp8_dw else 1)),
+            "quantize_act": ("bytes", R * f * (4 if self.fp8_dw else 3) + R * sc(f) * (2 if self.fp8_dw else 1)),
             # read bf16, write codes (MX: both orientations a step needs, from one read)
             "quantize_w": ("bytes", (3 * E * d * f * (2 + n_or) + n_or * 3 * E * d * f // 32) if self.mx
                            else (3 * E * d * f * 3 + 3 * E * (d + f) * 4)),
@@ -471,7 +500,8 @@ class MoELayer(_Traced):
             "dx_down": ("flops", 2 * R * d * f), "dw_down": ("flops8" if self.fp8_dw else "flops", 2 * R * f * d),
             "dx_down_swiglu_bwd": ("flops8" if self.fp8_bwd else "flops", 2 * R * d * f),
             # FP8 backward: dY_perm and [dH_gate | dH_up] per row, the weights in their stored layouts
-            "quantize_dy": ("bytes", R * d * 3 + R * sc(d)), "quantize_dh": ("bytes", 2 * R * f * 3 + R * sc(2 * f)),
+            "quantize_dy": ("bytes", R * d * (4 if self.fp8_dw else 3) + R * sc(d) * (2 if self.fp8_dw else 1)),
+            "quantize_dh": ("bytes", 2 * R * f * (4 if self.fp8_dw else 3) + R * sc(2 * f) * (2 if self.fp8_dw else 1)),
             "quantize_w_bwd": ("bytes", (3 * E * d * f * 3 + 3 * E * d * f // 32) if self.mx
                                else (3 * E * d * f * 3 + E * (d + f) * 4)),
             "swiglu_bwd": ("bytes", 5 * R * f * 2),

@@ -59,6 +59,7 @@ _SIG = {
     "moe_mx_scale_bytes": (_I64, [_I64, _I64]),
     "moe_mx_tokens_cols_bound": (_I64, [_I64, _I32]),
     "moe_quantize_mx_tokens_t": (ctypes.c_int, [_P, _P, _I32, _I64, _I64, _P, _P, _I64, _P]),
+    "moe_quantize_mx_tokens": (ctypes.c_int, [_P, _P, _I32, _I64, _I64, _P, _P, _I64, _P, _P, _I64, _I64, _P]),
     "moe_grouped_gemm_dw_mx": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _I64, _P, _P,
                                               _I32, _P, _P]),
     "moe_quantize_mx_rows": (ctypes.c_int, [_P, _P, _I64, _I64, _P, _P, _P]),
@@ -621,6 +622,38 @@ def moe_quantize_mx_tokens_t(x, offsets, qt=None, st=None, stream=None):
     _check("moe_quantize_mx_tokens_t", lib().moe_quantize_mx_tokens_t(_ptr(x), _ptr(offsets), G, R, C, _ptr(qt),
                                                                       _ptr(st), ld, _stream(stream)))
     return qt, st
+
+
+def moe_quantize_mx_tokens(x, offsets, qt=None, st=None, qr=None, sr=None, ldr=None, col0=0, want_t=True,
+                           want_r=True, stream=None):
+    """Both MX orientations of the routed buffer x [R, C] from one read: token-major (qt [C, ld],
+    st [ld/128, C, 4]) and row-wise codes written at column col0 of rows of ldr bytes (qr [R, ldr],
+    sr [ceil(ldr/128), R, 4]; ldr defaults to C).  Returns (qt, st, qr, sr), None where not asked."""
+    R, C = x.shape
+    G = offsets.numel() - 1
+    _need(x, torch.bfloat16, (R, C), "x")
+    _need(offsets, torch.int32, (G + 1,), "offsets")
+    ld = mx_tokens_cols(R, G)
+    dev = x.device
+    if want_t:
+        qt = torch.empty((C, ld), dtype=torch.uint8, device=dev) if qt is None else qt
+        st = torch.empty((ld // 128, C, 4), dtype=torch.uint8, device=dev) if st is None else st
+        _need(qt, torch.uint8, (C, ld), "qt")
+        _need(st, torch.uint8, (ld // 128, C, 4), "st")
+    else:
+        qt = st = None
+    if want_r:
+        ldr = (qr.shape[1] if qr is not None else C) if ldr is None else ldr
+        qr = torch.empty((R, ldr), dtype=torch.uint8, device=dev) if qr is None else qr
+        sr = torch.empty((mx_groups(ldr), R, 4), dtype=torch.uint8, device=dev) if sr is None else sr
+        _need(qr, torch.uint8, (R, ldr), "qr")
+        _need(sr, torch.uint8, (mx_groups(ldr), R, 4), "sr")
+    else:
+        qr = sr = None
+        ldr = 0
+    _check("moe_quantize_mx_tokens", lib().moe_quantize_mx_tokens(_ptr(x), _ptr(offsets), G, R, C, _ptr(qt), _ptr(st),
+                                                                  ld, _ptr(qr), _ptr(sr), ldr, col0, _stream(stream)))
+    return qt, st, qr, sr
 
 
 def moe_grouped_gemm_dw_mx(At, a_scale, dCt, c_scale, offsets, R, dC2t=None, c2_scale=None, dB=None, dB2=None,

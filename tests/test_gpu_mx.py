@@ -341,6 +341,38 @@ def test_quantize_mx_tokens_t(counts, C):
     np.testing.assert_array_equal(_blocks(st, ld)[:, : L // 32], rs)
 
 
+@pytest.mark.parametrize("counts,C", [([5, 0, 130, 128, 1, 300], 64), ([700, 3, 41], 192)])
+def test_quantize_mx_tokens_both(counts, C):
+    """moe_quantize_mx_tokens: from one read, the token-major codes (equal to
+    moe_quantize_mx_tokens_t's) and the row codes bit for bit against the oracle's row quantizer;
+    two calls at col0 = 0 and C fill the joined rows [x | x2] as the oracle quantizes them."""
+    _say("quantize mx tokens both", counts, C)
+    g = torch.Generator().manual_seed(3 * sum(counts) + C)
+    R, G = sum(counts), len(counts)
+    off = torch.tensor(np.concatenate([[0], np.cumsum(counts)]), dtype=torch.int32, device=DEV)
+    mk = lambda: (torch.randn((R, C), generator=g, dtype=torch.float64)
+                  * 2.0 ** torch.randint(-20, 21, (R, C // 32), generator=g).double().repeat_interleave(32, dim=1)
+                  ).to(torch.bfloat16)
+    x, x2 = mk(), mk()
+    qt0, st0 = moe.moe_quantize_mx_tokens_t(x.to(DEV), off)
+    qt, st, qr, sr = moe.moe_quantize_mx_tokens(x.to(DEV), off)
+    torch.cuda.synchronize()
+    L = int(O.pack_groups_t(np.zeros((R, 1)), off.cpu().numpy())[1][-1])
+    assert torch.equal(qt[:, :L], qt0[:, :L])
+    assert np.array_equal(_blocks(st, qt.shape[1])[:, : L // 32], _blocks(st0, qt.shape[1])[:, : L // 32])
+    rq, rs = O.quantize_rows_mx(f64(x))
+    np.testing.assert_array_equal(_u8(qr), rq)
+    np.testing.assert_array_equal(_blocks(sr, C), rs)
+    jq = poison_(torch.empty((R, 2 * C), dtype=torch.uint8, device=DEV))
+    js = poison_(torch.empty((moe.mx_groups(2 * C), R, 4), dtype=torch.uint8, device=DEV))
+    moe.moe_quantize_mx_tokens(x.to(DEV), off, qr=jq, sr=js, col0=0, want_t=False)
+    moe.moe_quantize_mx_tokens(x2.to(DEV), off, qr=jq, sr=js, col0=C, want_t=False)
+    torch.cuda.synchronize()
+    rq, rs = O.quantize_rows_mx(np.concatenate([f64(x), f64(x2)], axis=1))
+    np.testing.assert_array_equal(_u8(jq), rq)
+    np.testing.assert_array_equal(_blocks(js, 2 * C), rs)
+
+
 def _tokens_operand(g, rows, counts, lo=125, hi=129):
     """Integer codes |c| <= 4 in the token-major layout (zeros in each group's padding) and random
     scale bytes: (codes [rows, ld], scales in the library's layout, scale bytes [rows, ld/32])."""
