@@ -417,10 +417,12 @@ def test_grouped_gemm_dw_mx_exact(K, N, dual, out16):
 # ------------------------------------------------------------------------------------------------
 # The layer with its expert data products on MX operands, against an end-to-end oracle run
 # ------------------------------------------------------------------------------------------------
-def _oracle_layer_mx(inp, cfg, mx_dw=False):
-    """The layer's forward and backward with the four expert data products on MX operands (X_perm,
-    the SwiGLU output, dY_perm and [dH_gate | dH_up] quantized per 32-element block of their rows,
-    the weights per block of the matching contraction) and everything else as the bf16 oracle."""
+def _oracle_layer_mx(inp, cfg, mx_dw=False, mx_fwd=True, mx_bwd=True):
+    """The layer's forward and backward with the expert data products on MX operands (mx_fwd: the
+    forward's, X_perm and the SwiGLU output quantized per 32-element block of their rows; mx_bwd:
+    the data gradient's, dY_perm and [dH_gate | dH_up]; the weights per block of the matching
+    contraction), with mx_dw the weight gradients on operands quantized along the tokens, and
+    everything else as the bf16 oracle."""
     x = f64(inp["x"])
     wg, wu, wd = (f64(inp[n]) for n in ("w_gate", "w_up", "w_down"))
     shared = None
@@ -435,11 +437,14 @@ def _oracle_layer_mx(inp, cfg, mx_dw=False):
     gq, gs = q(np.transpose(wg, (0, 2, 1)))
     uq, us = q(np.transpose(wu, (0, 2, 1)))
     dq, ds = q(np.transpose(wd, (0, 2, 1)))
-    hg = O.grouped_gemm_mx(xq, xs, gq, gs, off)
-    hu = O.grouped_gemm_mx(xq, xs, uq, us, off)
+    if mx_fwd:
+        hg = O.grouped_gemm_mx(xq, xs, gq, gs, off)
+        hu = O.grouped_gemm_mx(xq, xs, uq, us, off)
+    else:
+        hg, hu = O.grouped_gemm(xp, wg, off), O.grouped_gemm(xp, wu, off)
     act = O.swiglu(hg, hu)
     aq, as_ = q(act)
-    y_perm = O.grouped_gemm_mx(aq, as_, dq, ds, off)
+    y_perm = O.grouped_gemm_mx(aq, as_, dq, ds, off) if mx_fwd else O.grouped_gemm(act, wd, off)
     fwd = {"offsets": off, "row_of_slot": ros, "topk_w": tw, "y_perm": y_perm}
     y_sh = None
     if shared is not None:
@@ -450,10 +455,12 @@ def _oracle_layer_mx(inp, cfg, mx_dw=False):
     dy_perm, _ = O.combine_bwd(dy, tw, ros, y_perm, k)
     yq, ys = q(dy_perm)
     wdq, wds = q(wd)                                           # rows of W_down [E, f, d]
-    dhg, dhu = O.swiglu_bwd(hg, hu, O.grouped_gemm_mx(yq, ys, wdq, wds, off))
+    da = O.grouped_gemm_mx(yq, ys, wdq, wds, off) if mx_bwd else O.grouped_gemm_dx(dy_perm, wd, off)
+    dhg, dhu = O.swiglu_bwd(hg, hu, da)
     hq, hs = q(np.concatenate([dhg, dhu], axis=1))
     wjq, wjs = q(np.concatenate([wg, wu], axis=2))             # rows [W_gate | W_up] [E, d, 2f]
-    dx_perm = O.grouped_gemm_mx(hq, hs, wjq, wjs, off)
+    dx_perm = (O.grouped_gemm_mx(hq, hs, wjq, wjs, off) if mx_bwd
+               else O.grouped_gemm_dx(dhg, wg, off, dhu, wu))
     dx_sh = None
     if shared is not None:
         dx_sh = O.dense_ffn_backward(fwd["shared"], x, dy, *shared)["dx"]
@@ -472,42 +479,49 @@ def _oracle_layer_mx(inp, cfg, mx_dw=False):
                   "gate_up_r": (wjq, wjs)}}
 
 
-@pytest.mark.parametrize("cfg_id,mx_dw", [(0, False), (2, False), (0, True), (2, True)])
-def test_layer_mx(cfg_id, mx_dw):
+@pytest.mark.parametrize("cfg_id,mx_dw,fwd,bwd", [(0, False, True, True), (2, False, True, True),
+                                                  (0, True, True, True), (2, True, True, True),
+                                                  (0, True, False, True), (0, True, True, False)])
+def test_layer_mx(cfg_id, mx_dw, fwd, bwd):
     """The layer with MX forward and data-gradient products (fp8_forward, fp8_backward, mx), two
     steps (the second re-quantizes the weights, both orientations from one read per weight): the
     weight codes and scale bytes bit for bit, and every output and gradient against the end-to-end
     oracle run, which quantizes its own bf16 intermediates (a code may differ where the two sides'
     bf16 intermediates differ in the last bit; the tolerances cover that).  With mx_dw the weight
-    gradients run on operands quantized along the tokens as well.  Config 2 at 1024 tokens."""
+    gradients run on operands quantized along the tokens as well; with only one of the forward and
+    data-gradient products in MX, the other stays bf16 and the token-major codes of the tensors it
+    does not quantize come from the token-only quantization.  Config 2 at 1024 tokens."""
     import dataclasses
     from paper_2606_26453_amd import layer as L, workloads as W
     cfg = W.CONFIGS[cfg_id]
     if cfg_id:
         cfg = dataclasses.replace(cfg, T=1024)
-    _say("layer mx", cfg, mx_dw)
+    _say("layer mx", cfg, mx_dw, fwd, bwd)
     inp = W.make_inputs(cfg, 0, "cpu")
-    lay = L.MoELayer(cfg, {k_: v.to(DEV) for k_, v in inp.items()}, fp8_forward=True, fp8_backward=True, mx=True,
+    lay = L.MoELayer(cfg, {k_: v.to(DEV) for k_, v in inp.items()}, fp8_forward=fwd, fp8_backward=bwd, mx=True,
                      fp8_dw=mx_dw)
     lay.step()
     lay.step()
     torch.cuda.synchronize()
     b = lay.buf
-    ref = _oracle_layer_mx(inp, cfg, mx_dw)
+    ref = _oracle_layer_mx(inp, cfg, mx_dw, fwd, bwd)
     d, f, E = cfg.d, cfg.f, cfg.E
-    gq, gs, uq, us = ref["w"]["gate_up_t"]
-    lq = _u8(lay.wmx["gate_up_t"][0]).reshape(E, f // 128, 2, 128, d)
-    ls = _blocks(lay.wmx["gate_up_t"][1], d).reshape(E, f // 128, 2, 128, d // 32)
-    np.testing.assert_array_equal(lq[:, :, 0].reshape(E, f, d), gq)
-    np.testing.assert_array_equal(lq[:, :, 1].reshape(E, f, d), uq)
-    np.testing.assert_array_equal(ls[:, :, 0].reshape(E, f, d // 32), gs)
-    np.testing.assert_array_equal(ls[:, :, 1].reshape(E, f, d // 32), us)
-    np.testing.assert_array_equal(_u8(lay.wmx["down_t"][0]), ref["w"]["down_t"][0])
-    np.testing.assert_array_equal(_blocks(lay.wmx["down_t"][1], f), ref["w"]["down_t"][1])
-    np.testing.assert_array_equal(_u8(lay.wmx["down_r"][0]), ref["w"]["down_r"][0])
-    np.testing.assert_array_equal(_blocks(lay.wmx["down_r"][1], d), ref["w"]["down_r"][1])
-    np.testing.assert_array_equal(_u8(lay.wmx["gate_up_r"][0]), ref["w"]["gate_up_r"][0])
-    np.testing.assert_array_equal(_blocks(lay.wmx["gate_up_r"][1], 2 * f), ref["w"]["gate_up_r"][1])
+    assert set(lay.wmx) == ({"gate_up_t", "down_t"} if fwd else set()) | ({"gate_up_r", "down_r"} if bwd else set())
+    if fwd:
+        gq, gs, uq, us = ref["w"]["gate_up_t"]
+        lq = _u8(lay.wmx["gate_up_t"][0]).reshape(E, f // 128, 2, 128, d)
+        ls = _blocks(lay.wmx["gate_up_t"][1], d).reshape(E, f // 128, 2, 128, d // 32)
+        np.testing.assert_array_equal(lq[:, :, 0].reshape(E, f, d), gq)
+        np.testing.assert_array_equal(lq[:, :, 1].reshape(E, f, d), uq)
+        np.testing.assert_array_equal(ls[:, :, 0].reshape(E, f, d // 32), gs)
+        np.testing.assert_array_equal(ls[:, :, 1].reshape(E, f, d // 32), us)
+        np.testing.assert_array_equal(_u8(lay.wmx["down_t"][0]), ref["w"]["down_t"][0])
+        np.testing.assert_array_equal(_blocks(lay.wmx["down_t"][1], f), ref["w"]["down_t"][1])
+    if bwd:
+        np.testing.assert_array_equal(_u8(lay.wmx["down_r"][0]), ref["w"]["down_r"][0])
+        np.testing.assert_array_equal(_blocks(lay.wmx["down_r"][1], d), ref["w"]["down_r"][1])
+        np.testing.assert_array_equal(_u8(lay.wmx["gate_up_r"][0]), ref["w"]["gate_up_r"][0])
+        np.testing.assert_array_equal(_blocks(lay.wmx["gate_up_r"][1], 2 * f), ref["w"]["gate_up_r"][1])
     for key in ("h_gate", "h_up", "act", "y_perm", "y", "dy_perm", "dh_gate", "dh_up", "dx_perm", "dx"):
         check_float(key, f64(b[key]), ref[key], 1e-2)
     for key in ("dw_down", "dw_gate", "dw_up"):
