@@ -123,6 +123,56 @@ def test_fp8_rejects():
     assert qw(w=None) == 1 and qw(w=BAD) == 1 and qw(q=FAKE + 8) == 1 and qw(w2=BAD) == 1 and qw(G=0) == 0
 
 
+def test_mx_rejects():
+    L = moe.lib()
+    assert L.moe_mx_scale_bytes(10, 64) == 40 and L.moe_mx_scale_bytes(10, 2880) == 23 * 40
+    assert L.moe_mx_scale_bytes(0, 64) == 0 and L.moe_mx_scale_bytes(10, 0) == 0
+    assert L.moe_mx_tokens_cols_bound(100, 4) == 640 and L.moe_mx_tokens_cols_bound(0, 1) == 128
+    qr = lambda M=10, K=64, x=FAKE, x2=None, q=FAKE: L.moe_quantize_mx_rows(x, x2, M, K, q, FAKE, None)
+    assert qr(K=48) == 2 and qr(x=None) == 1 and qr(x=BAD) == 1 and qr(x2=BAD) == 1 and qr(q=FAKE + 4) == 1
+    assert qr(M=-1) == 1 and qr(M=0) == 0
+    qw = lambda G=2, K=64, N=128, w=FAKE, w2=None, qt=FAKE, st=FAKE, q_r=FAKE, sr=FAKE: L.moe_quantize_mx_weight(
+        w, w2, G, K, N, qt, st, q_r, sr, None)
+    assert qw(K=48) == 2 and qw(N=96) == 2 and qw(N=192, w2=FAKE) == 2
+    assert qw(st=None) == 1 and qw(sr=None) == 1 and qw(qt=None, st=None, q_r=None, sr=None) == 1
+    assert qw(w=None) == 1 and qw(w=BAD) == 1 and qw(qt=FAKE + 8) == 1 and qw(q_r=FAKE + 4) == 1 and qw(G=0) == 0
+    mx = lambda G=4, R=100, K=128, N=128, A=FAKE, sa=FAKE, sw=FAKE, ws=None, n=0: L.moe_grouped_gemm_fwd_mx(
+        A, sa, FAKE, sw, FAKE, G, R, K, N, FAKE, ws, n, None)
+    assert mx(K=96) == 2 and mx(N=100) == 2 and mx(G=0) == 2 and mx(A=None) == 1 and mx(sa=None) == 1
+    assert mx(sa=FAKE + 2) == 1 and mx(sw=FAKE + 2) == 1 and mx(A=BAD) == 1 and mx(R=0) == 0
+    assert mx(ws=FAKE, n=16) == 3
+    gu = lambda F=128, hg=FAKE: L.moe_grouped_gemm_fwd_mx_gate_up(FAKE, FAKE, FAKE, FAKE, FAKE, 4, 100, 128, F, hg,
+                                                                  FAKE, None, None, 0, None)
+    assert gu(F=64) == 2 and gu(hg=None) == 1
+    sb = lambda hg=FAKE, hu=FAKE: L.moe_grouped_gemm_dx_swiglu_bwd_mx(FAKE, FAKE, FAKE, FAKE, FAKE, 4, 100, 128,
+                                                                      128, hg, hu, FAKE, FAKE, None, 0, None)
+    assert sb(hg=None) == 1 and sb(hu=BAD) == 1
+    ld = 640
+    tt = lambda G=4, C=128, ld=ld, x=FAKE, qt=FAKE: L.moe_quantize_mx_tokens_t(x, FAKE, G, 100, C, qt, FAKE, ld, None)
+    assert tt(G=0) == 2 and tt(C=96) == 2 and tt(ld=700) == 1 and tt(ld=512) == 1 and tt(qt=None) == 1
+    assert tt(x=BAD) == 1 and tt(qt=FAKE + 8) == 1
+    tb = lambda col0=0, ldr=128, qt=FAKE, st=FAKE, q_r=FAKE, sr=FAKE: L.moe_quantize_mx_tokens(
+        FAKE, FAKE, 4, 100, 128, qt, st, ld, q_r, sr, ldr, col0, None)
+    assert tb(col0=32, ldr=256) == 1 and tb(col0=64, ldr=128) == 1 and tb(ldr=112) == 1
+    assert tb(qt=None, st=None, q_r=None, sr=None) == 1 and tb(sr=None) == 1 and tb(q_r=FAKE + 4) == 1
+    dw = lambda K=128, ld=ld, c2=None, s2=None, dB2=None, cnt=None, sa=FAKE: L.moe_grouped_gemm_dw_mx(
+        FAKE, sa, FAKE, FAKE, c2, s2, FAKE, 4, 100, K, 128, ld, FAKE, dB2, 0, cnt, None)
+    assert dw(ld=512) == 1 and dw(ld=700) == 1 and dw(K=100) == 2 and dw(c2=FAKE, dB2=FAKE) == 1
+    assert dw(cnt=FAKE + 2) == 1 and dw(sa=FAKE + 2) == 1 and dw(K=1 << 22) == 2   # operand of 2 GiB or more
+
+
+def test_fwd_combine_rejects():
+    L = moe.lib()
+    need = L.moe_grouped_gemm_fwd_combine_workspace_bytes(50, 512)
+    assert need == 50 * 2 * 4 and L.moe_grouped_gemm_fwd_combine_workspace_bytes(0, 512) == 0
+    fc = lambda R=100, T=50, k=2, N=512, cnt=FAKE, n=need, y=FAKE, add=None: L.moe_grouped_gemm_fwd_combine(
+        FAKE, FAKE, FAKE, 4, R, 128, N, FAKE, FAKE, FAKE, T, k, add, FAKE, y, cnt, n, None, 0, None)
+    assert fc(R=99) == 1 and fc(k=0) == 1 and fc(T=-1) == 1 and fc(cnt=None) == 1 and fc(y=None) == 1
+    assert fc(y=BAD) == 1 and fc(add=BAD) == 1 and fc(cnt=FAKE + 2) == 1 and fc(n=need - 4) == 3
+    assert fc(R=1 << 20, T=1 << 19, N=4096) == 2          # Y_perm of 2 GiB or more
+    assert fc(R=0, T=0) == 0
+
+
 def test_gather_rejects():
     L = moe.lib()
     fg = lambda T=50, src=FAKE, K=128, ws=None, n=0: L.moe_grouped_gemm_fwd_gather(
