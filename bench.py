@@ -109,6 +109,8 @@ def _args():
     ap.add_argument("--fp8-fixed-weights", action="store_true",
                     help="with --fp8-forward/--fp8-backward: quantize the weights once (held fixed), not every step")
     ap.add_argument("--forward-only", action="store_true", help="time the forward alone (a variant)")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture the step into a HIP graph once and time its replays (no per-call events)")
     ap.add_argument("--combine-fused", action="store_true",
                     help="the weighted combine in the down product's epilogue (a variant)")
     ap.add_argument("--gather-fused", action="store_true",
@@ -411,8 +413,12 @@ def main():
     for _ in range(a.warmup):
         step()
     torch.cuda.synchronize()
+    if a.graph:   # from here on every step is one replay of the captured sequence
+        lay.capture(step)
+        torch.cuda.synchronize()
+        step = lay.replay
 
-    lay.trace = None if a.no_trace else []
+    lay.trace = None if (a.no_trace or a.graph) else []
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     step_ev = [torch.cuda.Event(enable_timing=True) for _ in range(a.steps + 1)]
     torch.cuda.synchronize()
@@ -532,6 +538,7 @@ def main():
                    + (", FP8 weights quantized once (held fixed)" if a.fp8_fixed_weights else "")
                    + (", gather fused into the gate/up product" if a.gather_fused else "")
                    + (", combine fused into the down product" if a.combine_fused else "")
+                   + (", HIP graph replay" if a.graph else "")
                    + (", dW from contraction-major copies" if a.dw_transposed else "")
                    + (", no split tail" if a.no_split_tail else "")
                    + (", dW one workgroup per tile" if a.dw_one_per_tile else "")

@@ -38,6 +38,35 @@ class _Traced:
         self.trace.append((name, e0, e1))
         return out
 
+    graph = None
+
+    def capture(self, fn=None):
+        """Record one call of `fn` (default: step) into a HIP graph (torch.cuda.CUDAGraph) and keep
+        it; replay() then re-issues the whole sequence with one launch.  Every library call of a step
+        can be captured: it only enqueues kernels on the current stream (counters and workspaces are
+        cleared by kernels, never by a memset), synchronizes nothing and allocates nothing, and the
+        layer's buffers are allocated once, so each replay rewrites them exactly as an eager call
+        does.  One warm-up call runs on a side stream first, as torch's capture recipe asks."""
+        if getattr(self, "concurrent", False):
+            raise ValueError("capture the one-stream schedule (concurrent=False)")
+        if self.trace is not None:
+            raise ValueError("capture without per-call tracing")
+        fn = self.step if fn is None else fn
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            fn()
+        torch.cuda.current_stream().wait_stream(side)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            fn()
+        self.graph = g
+        return g
+
+    def replay(self):
+        """Re-issue the captured sequence on the current stream."""
+        self.graph.replay()
+
 
 class MoELayer(_Traced):
     """fuse_swiglu_bwd: the down projection's dX GEMM computes the SwiGLU backward in its epilogue
