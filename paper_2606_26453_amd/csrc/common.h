@@ -26,6 +26,16 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, v);
 }
 
+// A 16-byte load of data read once and not again soon (a routed row on its way through a copy or
+// a combine, a weight on its way to its codes): non-temporal, i.e. streamed past the caches
+// instead of displacing what they hold.  Measured on the layer's copies and combines: 5-17%
+// shorter than plain loads.  Stores stay plain (non-temporal stores measured slower).
+__device__ __forceinline__ u32x4 ld_stream(const u32x4* p) { return __builtin_nontemporal_load(p); }
+template <bool NT> __device__ __forceinline__ u32x4 ld_maybe_stream(const u32x4* p) {
+  if constexpr (NT) return __builtin_nontemporal_load(p);
+  else return *p;
+}
+
 // 8 bf16 in a 16-byte vector <-> 8 floats.
 __device__ __forceinline__ void unpack8(const u32x4& v, float* f) {
 #pragma unroll

@@ -45,8 +45,9 @@ __global__ __launch_bounds__(256) void swiglu_bwd_kernel(const u32x4* __restrict
   dhu[i] = b;
 }
 
-// y[t] = bf16(sum_j w[t,j] * y_perm[row_of_slot[t*k+j]] + add[t]).  KK > 0: k == KK.
-template <int U, int KK>
+// y[t] = bf16(sum_j w[t,j] * y_perm[row_of_slot[t*k+j]] + add[t]).  KK > 0: k == KK.  NT: the
+// permuted rows (and add) are read with streaming loads.
+template <int U, int KK, bool NT>
 __global__ __launch_bounds__(256) void combine_kernel(const u32x4* __restrict__ y_perm,
                                                       const float* __restrict__ w,
                                                       const int32_t* __restrict__ row_of_slot,
@@ -73,7 +74,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const u32x4* __restrict__ 
 #pragma unroll
         for (int u = 0; u < U; ++u) {
           const int64_t c = c0 + u * 64 + lane;
-          v[j][u] = c < chunks ? src[j][c] : u32x4{0u, 0u, 0u, 0u};
+          v[j][u] = c < chunks ? ld_maybe_stream<NT>(src[j] + c) : u32x4{0u, 0u, 0u, 0u};
         }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
@@ -91,7 +92,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const u32x4* __restrict__ 
         if (c < chunks) {
           if (add) {
             float f[8];
-            unpack8(add[t * chunks + c], f);
+            unpack8(ld_maybe_stream<NT>(add + t * chunks + c), f);
 #pragma unroll
             for (int i = 0; i < 8; ++i) acc[i] += f[i];
           }
@@ -115,7 +116,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const u32x4* __restrict__ 
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int64_t c = c0 + u * 64 + lane;
-        if (c < chunks) v[u] = src[c];
+        if (c < chunks) v[u] = ld_maybe_stream<NT>(src + c);
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
@@ -131,7 +132,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const u32x4* __restrict__ 
       if (c < chunks) {
         if (add) {
           float f[8];
-          unpack8(add[t * chunks + c], f);
+          unpack8(ld_maybe_stream<NT>(add + t * chunks + c), f);
 #pragma unroll
           for (int i = 0; i < 8; ++i) acc[u][i] += f[i];
         }
@@ -173,10 +174,10 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(const u32x4* __restric
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int64_t c = c0 + 64 * u;
-        dv[u] = c < chunks ? src[c] : u32x4{0u, 0u, 0u, 0u};
+        dv[u] = c < chunks ? ld_stream(src + c) : u32x4{0u, 0u, 0u, 0u};
         if (y_perm) {
 #pragma unroll
-          for (int j = 0; j < KK; ++j) yv[j][u] = c < chunks ? y_perm[row[j] * chunks + c] : u32x4{0u, 0u, 0u, 0u};
+          for (int j = 0; j < KK; ++j) yv[j][u] = c < chunks ? ld_stream(y_perm + row[j] * chunks + c) : u32x4{0u, 0u, 0u, 0u};
         }
       }
 #pragma unroll
@@ -224,7 +225,7 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(const u32x4* __restric
     }
     for (int64_t c = lane; c < chunks; c += 64) {
       float f[8];
-      unpack8(src[c], f);
+      unpack8(ld_stream(src + c), f);
 #pragma unroll
       for (int j = 0; j < J; ++j) {
         if (j < nj) {
@@ -234,7 +235,7 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(const u32x4* __restric
           dy_perm[row[j] * chunks + c] = pack8(o);
           if (y_perm) {
             float yf[8];
-            unpack8(y_perm[row[j] * chunks + c], yf);
+            unpack8(ld_stream(y_perm + row[j] * chunks + c), yf);
 #pragma unroll
             for (int i = 0; i < 8; ++i) dot[j] += f[i] * yf[i];
           }
@@ -302,6 +303,20 @@ extern "C" moe_status moe_swiglu_bwd(const moe_bf16* h_gate, const moe_bf16* h_u
   return check_launch("swiglu_bwd_kernel");
 }
 
+// about eight 16-byte loads in flight per lane for the common k
+template <bool NT>
+static void launch_combine(unsigned grid, hipStream_t stream, const u32x4* yp, const float* w, const int32_t* rows,
+                    const u32x4* ad, int64_t T, int64_t chunks, int k, u32x4* yo) {
+  switch (k) {
+    case 1: combine_kernel<8, 1, NT><<<grid, 256, 0, stream>>>(yp, w, rows, ad, T, chunks, k, yo); break;
+    case 2: combine_kernel<4, 2, NT><<<grid, 256, 0, stream>>>(yp, w, rows, ad, T, chunks, k, yo); break;
+    case 4: combine_kernel<2, 4, NT><<<grid, 256, 0, stream>>>(yp, w, rows, ad, T, chunks, k, yo); break;
+    case 6: combine_kernel<1, 6, NT><<<grid, 256, 0, stream>>>(yp, w, rows, ad, T, chunks, k, yo); break;
+    case 8: combine_kernel<1, 8, NT><<<grid, 256, 0, stream>>>(yp, w, rows, ad, T, chunks, k, yo); break;
+    default: combine_kernel<4, 0, NT><<<grid, 256, 0, stream>>>(yp, w, rows, ad, T, chunks, k, yo); break;
+  }
+}
+
 extern "C" moe_status moe_unpermute_combine(const moe_bf16* y_perm, const float* topk_w,
                                             const int32_t* row_of_slot, const moe_bf16* add,
                                             int64_t T, int64_t d, int32_t k, moe_bf16* y,
@@ -319,15 +334,17 @@ extern "C" moe_status moe_unpermute_combine(const moe_bf16* y_perm, const float*
   const u32x4* yp = reinterpret_cast<const u32x4*>(y_perm);
   const u32x4* ad = reinterpret_cast<const u32x4*>(add);
   u32x4* yo = reinterpret_cast<u32x4*>(y);
-  // about eight 16-byte loads in flight per lane for the common k
-  switch (k) {
-    case 1: combine_kernel<8, 1><<<grid, 256, 0, stream>>>(yp, topk_w, row_of_slot, ad, T, chunks, k, yo); break;
-    case 2: combine_kernel<4, 2><<<grid, 256, 0, stream>>>(yp, topk_w, row_of_slot, ad, T, chunks, k, yo); break;
-    case 4: combine_kernel<2, 4><<<grid, 256, 0, stream>>>(yp, topk_w, row_of_slot, ad, T, chunks, k, yo); break;
-    case 6: combine_kernel<1, 6><<<grid, 256, 0, stream>>>(yp, topk_w, row_of_slot, ad, T, chunks, k, yo); break;
-    case 8: combine_kernel<1, 8><<<grid, 256, 0, stream>>>(yp, topk_w, row_of_slot, ad, T, chunks, k, yo); break;
-    default: combine_kernel<4, 0><<<grid, 256, 0, stream>>>(yp, topk_w, row_of_slot, ad, T, chunks, k, yo); break;
-  }
+  // Without weights this is the unpermute-sum of dX: its input was just written and is read once,
+  // so it streams.  The weighted forward combine streams Y_perm only when Y_perm is too large to
+  // stay in the 256 MiB Infinity Cache until the backward reads it again (taken as over half of
+  // it); a smaller one is read with plain loads, which leave it there (measured on the
+  // Mixtral-shaped layer, Y_perm 128 MiB: streaming made the combine 2 us shorter and its
+  // backward 8 us longer; on the fine-grained layer, Y_perm 384 MiB, the combine 111 -> 94 us).
+  constexpr int64_t kCacheHalf = (int64_t)128 << 20;
+  if (topk_w && T * k * d * 2 <= kCacheHalf)
+    launch_combine<false>(grid, stream, yp, topk_w, row_of_slot, ad, T, chunks, k, yo);
+  else
+    launch_combine<true>(grid, stream, yp, topk_w, row_of_slot, ad, T, chunks, k, yo);
   return check_launch("combine_kernel");
 }
 

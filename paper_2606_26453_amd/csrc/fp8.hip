@@ -114,7 +114,7 @@ __global__ __launch_bounds__(256) void amax_cols_kernel(const uint16_t* __restri
   for (int i = 0; i < 8; ++i) m[i] = 0.0f;
 #pragma unroll 4
   for (int64_t k = kb * QC_KA + rq; k < k_end; k += 32) {
-    const u32x4 v = *reinterpret_cast<const u32x4*>(src + k * N);
+    const u32x4 v = ld_stream(reinterpret_cast<const u32x4*>(src + k * N));
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       m[2 * e] = fmaxf(m[2 * e], fabsf(bf16_lo(v[e])));
@@ -161,7 +161,7 @@ __global__ __launch_bounds__(256) void quantize_cols_kernel(const uint16_t* __re
     for (int u = 0; u < 4; ++u) {
       const int64_t k = k0 + 4 * rq + u;
       u32x4 v = {0u, 0u, 0u, 0u};
-      if (k < k_end) v = *reinterpret_cast<const u32x4*>(src + k * N);
+      if (k < k_end) v = ld_stream(reinterpret_cast<const u32x4*>(src + k * N));
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         packed[2 * e] |= e4m3_code(__fmul_rn(bf16_lo(v[e]), inv[2 * e])) << (8 * u);

@@ -254,7 +254,7 @@ __global__ __launch_bounds__(kRowsThreads) void route_rows_kernel(const int32_t*
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int64_t c = c0 + u * 64 + lane;
-        if (c < chunks) v[u] = src[c];
+        if (c < chunks) v[u] = ld_stream(src + c);
       }
       for (int j = 0; j < k; ++j) {
         u32x4* dst = x_perm + (int64_t)rows[i * k + j] * chunks;
@@ -283,7 +283,7 @@ __global__ __launch_bounds__(256) void gather_kernel(const u32x4* __restrict__ x
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int64_t c = c0 + u * 64 + lane;
-      if (c < chunks) v[u] = src[c];
+      if (c < chunks) v[u] = ld_stream(src + c);
     }
     for (int j = 0; j < k; ++j) {
       u32x4* dst = x_perm + (int64_t)row_of_slot[t * k + j] * chunks;

@@ -897,10 +897,10 @@ __global__ __launch_bounds__(64 * NW) void router_dx_rows_kernel(
 #pragma unroll
         for (int j = 0; j < KR; ++j) {   // the slot index is the same in every lane: a scalar load
           const int64_t r = row_of_slot[__builtin_amdgcn_readfirstlane((int)(tt * k + j))];
-          b.r[u][j] = *reinterpret_cast<const u32x4*>(src + r * d + col);
+          b.r[u][j] = ld_stream(reinterpret_cast<const u32x4*>(src + r * d + col));
         }
       }
-      if constexpr (A) b.a[u] = *reinterpret_cast<const u32x4*>(add + tt * d + col);
+      if constexpr (A) b.a[u] = ld_stream(reinterpret_cast<const u32x4*>(add + tt * d + col));
     }
   };
   auto dl_ok = [&](int64_t tb) {
@@ -942,7 +942,7 @@ __global__ __launch_bounds__(64 * NW) void router_dx_rows_kernel(
           for (int j = 1; j < k; ++j) {
             const int64_t r = row_of_slot[t * k + j];
             float f[8];
-            unpack8(*reinterpret_cast<const u32x4*>(src + r * d + col), f);
+            unpack8(ld_stream(reinterpret_cast<const u32x4*>(src + r * d + col)), f);
 #pragma unroll
             for (int i = 0; i < 8; ++i) acc[i] += f[i];
           }
