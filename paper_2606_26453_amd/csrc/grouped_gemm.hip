@@ -234,6 +234,12 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
   constexpr bool N_T = (KIND == KIND_FWD || KIND == KIND_DW);   // N side stored contraction-major
   constexpr bool IS_DW = (KIND == KIND_DW || KIND == KIND_DWT); // weight gradient: groups own the
                                                                 // contraction, outputs are dB[g]
+  // persistent fp32 dW (single-group schedule): the next tile's first stages are issued before
+  // this tile's epilogue, which then stages its results through the other half of the ring
+  // (measured: dW gate/up 1.1% shorter on the Mixtral-shaped and long-batch layers, dW down 0.6%
+  // longer; with bf16 results the extra live state made the epilogue spill, and the paper's dW1
+  // shape ran 10% longer, so bf16 results keep the whole ring)
+  constexpr bool EARLY = PERSIST && KIND == KIND_DW && !OUT16;
 
   __shared__ __attribute__((aligned(16))) char lds[NSTAGE * STAGE];
   // MX: per stage, the scale words of the 256 tile rows (bytes 0..1023) and of the 256 weight rows
@@ -847,25 +853,32 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
   if constexpr (PERSIST) asm volatile("" : "+v"(tid));
   const int lane = tid & 63, l32 = lane & 31, fh = lane >> 5;
   const int col_in = 4 * fh;
+  // EARLY: the tile is staged through the ring's upper half (slots 2 and 3) one row half at a
+  // time, while the next tile's first two stages load into slots 0 and 1
+  constexpr int RH = EARLY ? 2 : 1, TMP = TM / RH;
+  char* const stg = lds + (EARLY ? 2 * STAGE : 0);
   if constexpr (IS_DW && !OUT16) {
     // fp32 results leave through LDS too, in two passes of 256 rows x 128 columns (128 KiB, the
-    // ring): pass h holds column blocks 2h and 2h+1 of every wavefront (dual: pass 0 the gate
+    // ring; EARLY: each pass once per 128-row half, 64 KiB in the ring's upper half): pass h holds
+    // column blocks 2h and 2h+1 of every wavefront (dual: pass 0 the gate
     // output's 128 columns of the tile, pass 1 the up output's).  Tile row t, 16-byte chunk c (4
     // columns) sits at t*512 + 16*(c ^ (t & 31)), conflict-free for both the accumulator-ordered
     // writes and the row-ordered reads.  Read back, every store instruction covers 4 rows x 256
     // contiguous bytes instead of the accumulator layout's 32 rows x 32 bytes, which a CU drains
     // 2-3x faster (256 KiB per tile).
-    static_assert(NB == 4 && TM * 512 <= NSTAGE * STAGE, "two passes of 128 columns through the ring");
-    constexpr int PER_WAVE = 2 * (TM / 4) / NWAVE;   // store instructions per wave and pass
+    static_assert(NB == 4 && TMP * 512 <= (EARLY ? 2 : NSTAGE) * STAGE, "passes of 128 columns through the ring");
+    constexpr int PER_WAVE = 2 * (TMP / 4) / NWAVE;   // store instructions per wave and pass
     constexpr int BATCH = 8;
     static_assert(PER_WAVE % BATCH == 0, "batches of LDS reads");
     const int64_t obase = (int64_t)g * p.K * p.N;
+    for (int rh = 0; rh < RH; ++rh)
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      __syncthreads();   // pass 0: every wave is done with the ring; pass 1: pass 0's reads are done
+      __syncthreads();   // first pass: every wave is done with the ring; then: the last pass's reads are done
+      if (!EARLY || wm == rh) {   // uniform per wavefront
 #pragma unroll
       for (int i = 0; i < MB; ++i) {
-        char* trow = lds + (wm * WTM + 32 * i + l32) * 512;   // (t & 31) == l32
+        char* trow = stg + (wm * WTM - rh * TMP + 32 * i + l32) * 512;   // (t & 31) == l32
 #pragma unroll
         for (int jj = 0; jj < 2; ++jj)
 #pragma unroll
@@ -875,6 +888,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
             const f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
             *reinterpret_cast<f32x4*>(trow + 16 * (c ^ l32)) = v;
           }
+      }
       }
       __syncthreads();
       // instruction s of wave w: tile rows 4*(w + NWAVE*(s/2)) + lane/16, chunks 16*(s%2) + lane%16.
@@ -886,8 +900,8 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
       const int64_t nseg0 = DUAL ? (int64_t)nt * (TN / 2) : (int64_t)nt * TN + 64 * h;
       constexpr int SEG1 = DUAL ? 64 : 128;
       const bool seg_in[2] = {nseg0 < p.N, nseg0 + SEG1 < p.N};
-      const int rows_left = (int)(p.K - (int64_t)mt * TM);   // > 0
-      float* base = out + ((int64_t)mt * TM + 4 * wave) * p.N + nseg0 + ((lane >> 4) * p.N + 4 * (lane & 15));
+      const int rows_left = (int)(p.K - (int64_t)mt * TM - rh * TMP);   // > 0 for the first row half
+      float* base = out + ((int64_t)mt * TM + rh * TMP + 4 * wave) * p.N + nseg0 + ((lane >> 4) * p.N + 4 * (lane & 15));
 #pragma unroll
       for (int b = 0; b < PER_WAVE; b += BATCH) {
         f32x4 v[BATCH];
@@ -896,7 +910,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
           const int s = b + e;
           const int t = 4 * (wave + NWAVE * (s >> 1)) + (lane >> 4);
           const int c = 16 * (s & 1) + (lane & 15);
-          v[e] = *reinterpret_cast<const f32x4*>(lds + t * 512 + 16 * (c ^ (t & 31)));
+          v[e] = *reinterpret_cast<const f32x4*>(stg + t * 512 + 16 * (c ^ (t & 31)));
         }
         // the whole batch of LDS reads is issued before the first store waits for its data
 #pragma unroll
@@ -916,7 +930,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
     // moves whole chunks, so a wavefront's global accesses cover two (dual: four) contiguous row
     // segments instead of 16 bytes in each of 32 rows.  Dual mode keeps the gate columns of a row in
     // chunks 0..15 and the up columns in chunks 16..31.
-    static_assert(TM * TN * 2 <= NSTAGE * STAGE, "the bf16 tile fits in the ring");
+    static_assert(TMP * TN * 2 <= (EARLY ? 2 : NSTAGE) * STAGE, "a row half (EARLY) or the bf16 tile fits");
     // the dual fwd and dW products have two outputs side by side in their tile; the dual dX
     // product sums both contractions into one output
     constexpr bool SPLIT = DUAL && (KIND != KIND_DX || F8);       // two outputs side by side in the tile
@@ -929,10 +943,13 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
       row_lo = (int64_t)mt * TM;
       row_hi = p.K;
     }
-    __syncthreads();   // every wave is done with the ring
+    for (int rh = 0; rh < RH; ++rh) {
+    __syncthreads();   // every wave is done with the ring (EARLY, second row half: with the first's reads)
+    const int64_t row_lo_p = row_lo + rh * TMP;   // first row of this pass
+    if (!EARLY || wm == rh) {   // uniform per wavefront
 #pragma unroll
     for (int i = 0; i < MB; ++i) {
-      char* trow = lds + (wm * WTM + 32 * i + l32) * 512;   // (t & 31) == l32
+      char* trow = stg + (wm * WTM - rh * TMP + 32 * i + l32) * 512;   // (t & 31) == l32
 #pragma unroll
       for (int j = 0; j < NB; ++j)
 #pragma unroll
@@ -959,9 +976,10 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
           *reinterpret_cast<uint2*>(trow + 16 * (c ^ l32) + 8 * fh) = v;
         }
     }
+    }
     __syncthreads();
     constexpr int NT = 64 * NWAVE;
-    auto chunk = [&](int t, int c) { return *reinterpret_cast<const u32x4*>(lds + t * 512 + 16 * (c ^ (t & 31))); };
+    auto chunk = [&](int t, int c) { return *reinterpret_cast<const u32x4*>(stg + t * 512 + 16 * (c ^ (t & 31))); };
     if constexpr (SPLIT) {
       // FWD gate/up and FP8 interleaved gate/up (+ SwiGLU): thread -> gate chunk c and up chunk 16 + c of rows t, t + NT/16, ...
       const int c = tid & 15;
@@ -973,11 +991,11 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
         uint16_t* c1 = static_cast<uint16_t*>(p.out) + obase + n;
         uint16_t* c2 = static_cast<uint16_t*>(p.out2) + obase + n;
         // passes of NT/16 rows, UB passes' LDS reads issued ahead of their stores
-        constexpr int RPP = NT / 16, PASSES = TM / RPP, UB = 4;
+        constexpr int RPP = NT / 16, PASSES = TMP / RPP, UB = 4;
         static_assert(PASSES % UB == 0, "batches of passes");
 #pragma unroll
         for (int b = 0; b < PASSES; b += UB) {
-          if (row_lo + b * RPP >= row_hi) break;   // uniform: no row of the batch is an output row
+          if (row_lo_p + b * RPP >= row_hi) break;   // uniform: no row of the batch is an output row
           u32x4 vg[UB], vu[UB];
 #pragma unroll
           for (int u = 0; u < UB; ++u) {
@@ -989,7 +1007,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
           for (int u = 0; u < UB; ++u) asm volatile("" : "+v"(vg[u]), "+v"(vu[u]));
 #pragma unroll
           for (int u = 0; u < UB; ++u) {
-            const int64_t r = row_lo + (tid >> 4) + (b + u) * RPP;
+            const int64_t r = row_lo_p + (tid >> 4) + (b + u) * RPP;
             if (r < row_hi) {
               if constexpr (IS_DW) {   // bf16 weight gradients: not read again in the step
                 __builtin_nontemporal_store(vg[u], reinterpret_cast<u32x4*>(c1 + r * Wo));
@@ -1020,15 +1038,15 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
           // SwiGLU backward on the bf16-rounded dA (what moe_swiglu_bwd would read back); the
           // H_gate/H_up chunks of U rows are loaded ahead of their use (rows clamped in range), as
           // streaming loads: H is read this once in the step (1.7% shorter than plain loads)
-          constexpr int RPP = NT / 32, U = (TM / RPP) < 4 ? (TM / RPP) : 4;
+          constexpr int RPP = NT / 32, U = (TMP / RPP) < 4 ? (TMP / RPP) : 4;
           uint16_t* og = static_cast<uint16_t*>(p.out) + n;
           uint16_t* ou = static_cast<uint16_t*>(p.out2) + n;
-          for (int t0 = tid >> 5; t0 < TM; t0 += U * RPP) {
-            if (row_lo + t0 >= row_hi) break;
+          for (int t0 = tid >> 5; t0 < TMP; t0 += U * RPP) {
+            if (row_lo_p + t0 >= row_hi) break;
             u32x4 gv[U], uv[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-              int64_t r = row_lo + t0 + u * RPP;
+              int64_t r = row_lo_p + t0 + u * RPP;
               if (r > row_hi - 1) r = row_hi - 1;
               gv[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p.hg + r * W + n));
               uv[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p.hu + r * W + n));
@@ -1036,7 +1054,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
 #pragma unroll
             for (int u = 0; u < U; ++u) {
               const int t = t0 + u * RPP;
-              const int64_t r = row_lo + t;
+              const int64_t r = row_lo_p + t;
               if (r < row_hi) {
                 const u32x4 dv = chunk(t, c);
                 u32x4 vg, vu;
@@ -1055,16 +1073,16 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
           }
         } else {
           uint16_t* dst = static_cast<uint16_t*>(p.out) + obase + n;
-          constexpr int RPP = NT / 32, PASSES = TM / RPP, UB = 8;
+          constexpr int RPP = NT / 32, PASSES = TMP / RPP, UB = 8;
           static_assert(PASSES % UB == 0, "batches of passes");
           // fused combine: the rows are stored agent-coherent (sc1: through to memory), since the
           // tile that completes a token's combine may run on another XCD
           auto store_rows = [&](auto coherent) {
-            const __amdgpu_buffer_rsrc_t ys = __builtin_amdgcn_make_buffer_rsrc(dst + row_lo * W, 0, TM * (int)W * 2,
+            const __amdgpu_buffer_rsrc_t ys = __builtin_amdgcn_make_buffer_rsrc(dst + row_lo_p * W, 0, TMP * (int)W * 2,
                                                                                 0x00020000);
 #pragma unroll
             for (int b = 0; b < PASSES; b += UB) {
-              if (row_lo + b * RPP >= row_hi) break;   // uniform
+              if (row_lo_p + b * RPP >= row_hi) break;   // uniform
               u32x4 v[UB];
 #pragma unroll
               for (int u = 0; u < UB; ++u) v[u] = chunk((tid >> 5) + (b + u) * RPP, c);
@@ -1073,7 +1091,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
 #pragma unroll
               for (int u = 0; u < UB; ++u) {
                 const int t = (tid >> 5) + (b + u) * RPP;
-                const int64_t r = row_lo + t;
+                const int64_t r = row_lo_p + t;
                 if (r < row_hi) {
                   if constexpr (decltype(coherent)::value)
                     __builtin_amdgcn_raw_buffer_store_b128(v[u], ys, (int)(t * W * 2), 0, CP_SC1);
@@ -1143,6 +1161,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
         }
       }
     }
+    }   // row halves
   }
   };
 
@@ -1211,16 +1230,42 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
       }
       int next = it + (int)gridDim.x;
       int g2 = 0, mt2 = 0, nt2 = 0, lo2 = 0, hi2 = 0;
-      epilogue(g, mt, nt, row_lo, row_hi);   // stages the tile through the ring (barriers first)
-      if constexpr (IS_DW) next = __builtin_amdgcn_readfirstlane(s_next);
-      const bool more = next < normal_end;   // uniform
-      if (more) {
+      if constexpr (EARLY) {
+        // The next tile's first two stages load into slots 0 and 1 while this tile's epilogue
+        // stages its results through slots 2 and 3; its stages 2 and 3 follow the epilogue.  The
+        // epilogue's stores then sit between stages 1 and 2 in the in-order vector-memory count,
+        // so the main loop's count-based waits still cover every stage they wait for.
+        static_assert(NSTAGE == 4 && PREFILL == 4 && WTM == TM / 2, "two slots each way, one row half per wave row");
+        __syncthreads();   // s_next is visible, and every wave is done with this tile's stages
+        next = __builtin_amdgcn_readfirstlane(s_next);
+        const bool more = next < normal_end;   // uniform
+        if (more) {
+          map_tile(next, g2, mt2, nt2, lo2, hi2);
+          setup(g2, mt2, nt2, lo2, hi2);
+          if (nsteps > 0) {
+            issue(0);
+            issue(1);
+          }
+        }
+        epilogue(g, mt, nt, row_lo, row_hi);
+        if (!more) break;
         __syncthreads();   // every staged chunk has been read
-        map_tile(next, g2, mt2, nt2, lo2, hi2);
-        setup(g2, mt2, nt2, lo2, hi2);
-        prefill();
+        if (nsteps > 0) {
+          issue(2);
+          issue(3);
+        }
+      } else {
+        epilogue(g, mt, nt, row_lo, row_hi);   // stages the tile through the ring (barriers first)
+        if constexpr (IS_DW) next = __builtin_amdgcn_readfirstlane(s_next);
+        const bool more = next < normal_end;   // uniform
+        if (more) {
+          __syncthreads();   // every staged chunk has been read
+          map_tile(next, g2, mt2, nt2, lo2, hi2);
+          setup(g2, mt2, nt2, lo2, hi2);
+          prefill();
+        }
+        if (!more) break;
       }
-      if (!more) break;
       it = next;
       g = g2; mt = mt2; nt = nt2; row_lo = lo2; row_hi = hi2;
       zero_acc();
