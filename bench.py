@@ -43,19 +43,19 @@ METRIC = "MoE layer fwd+bwd tokens/sec + grouped-GEMM TFLOP/s (% of bf16 MFMA pe
 # Valid only for the kernel code they were measured on (sha256 prefix of the sources with comments
 # and blank lines removed); otherwise reported null.
 TRAFFIC_SOURCES = {
-    "gemm": (("paper_2606_26453_amd/csrc/grouped_gemm.hip", "paper_2606_26453_amd/csrc/common.h"), "0fdcd75537d9632d"),
-    "route": (("paper_2606_26453_amd/csrc/route_permute.hip", "paper_2606_26453_amd/csrc/common.h"), "9d885379b7ef9324"),
-    "combine": (("paper_2606_26453_amd/csrc/elementwise.hip", "paper_2606_26453_amd/csrc/common.h"), "9a05da4cb2ca26d3"),
+    "gemm": (("paper_2606_26453_amd/csrc/grouped_gemm.hip", "paper_2606_26453_amd/csrc/common.h"), "73dd335ad465117d"),
+    "route": (("paper_2606_26453_amd/csrc/route_permute.hip", "paper_2606_26453_amd/csrc/common.h"), "72087f561c2c164f"),
+    "combine": (("paper_2606_26453_amd/csrc/elementwise.hip", "paper_2606_26453_amd/csrc/common.h"), "5fb5e5e15e3e53f4"),
 }
 TRAFFIC_CONFIG = 1
 FETCH_SCALE, WRITE_SCALE = 2.0 * 1024, 1.0 * 1024
 TRAFFIC_KIB = {  # call: (source group, FETCH_SIZE KiB, WRITE_SIZE KiB) per dispatch (routing: both launches)
     "route_permute": ("route", 33112, 131518),
-    "fwd_gate_up": ("gemm", 5566702, 1399104), "fwd_down": ("gemm", 1954453, 199688),
-    "combine": ("combine", 65813, 65536), "combine_bwd": ("combine", 98597, 131141),
-    "dw_down": ("gemm", 1441966, 1835232), "dx_down_swiglu_bwd": ("gemm", 3795221, 917504),
-    "dx_gate_up": ("gemm", 4082748, 196616), "unpermute_dx": ("combine", 65685, 65536),
-    "dw_gate_up": ("gemm", 2762796, 3670464),
+    "fwd_gate_up": ("gemm", 5571924, 1399104), "fwd_down": ("gemm", 1959399, 199688),
+    "combine": ("combine", 65813, 65536), "combine_bwd": ("combine", 98585, 131137),
+    "dw_down": ("gemm", 1442040, 1835232), "dx_down_swiglu_bwd": ("gemm", 3867640, 917504),
+    "dx_gate_up": ("gemm", 4033380, 196616), "unpermute_dx": ("combine", 65692, 65536),
+    "dw_gate_up": ("gemm", 2774456, 3670464),
 }
 
 
