@@ -1,26 +1,21 @@
 // Per-row quantization of bf16 rows to OCP E4M3 with an fp32 scale per row (the operand format of
 // the FP8 grouped product): amax = max |x[r, :]|, scale[r] = amax / 448, and each element becomes
-// the E4M3 code nearest to x * (448 / amax), ties to the even mantissa, magnitudes beyond 448
-// saturating; an all-zero row gets scale 1 and zero codes.  The quotients and the product are
-// single fp32 operations (IEEE round to nearest), so the codes are a function of the inputs alone.
+// the E4M3 code nearest to x * (448 / amax), ties to the even mantissa (the scaled magnitudes
+// exceed 448 by at most a rounding of the product, which rounds back to 448); an all-zero row gets
+// scale 1 and zero codes.  The quotients and the product are single fp32 operations (IEEE round to
+// nearest), so the codes are a function of the inputs alone.
 #include "common.h"
 
 namespace moe {
 namespace {
 
-// E4M3 code of an fp32 value: sign from the input, magnitude clamped to 448, then rounded to 3
-// mantissa bits (normal range, 2^-6 and up) or to a multiple of 2^-9 (subnormals).
-__device__ __forceinline__ uint32_t e4m3_code(float y) {
-  const uint32_t sign = (__float_as_uint(y) >> 24) & 0x80u;
-  if (y != y) return 0x7Fu;
-  const float a = fminf(fabsf(y), 448.0f);
-  if (a < 0.015625f) {                                   // below 2^-6: multiples of 2^-9, 0 .. 8
-    return sign | (uint32_t)__builtin_rintf(a * 512.0f); // 8 is the code of 2^-6 itself
-  }
-  const uint32_t b = __float_as_uint(a);
-  const uint32_t r = (b + 0x7FFFFu + ((b >> 20) & 1u)) & ~0xFFFFFu;   // ties to even at bit 20
-  const uint32_t e = (r >> 23) - 127u + 7u;             // biased E4M3 exponent, 1 .. 15
-  return sign | (e << 3) | ((r >> 20) & 7u);
+// E4M3 (OCP e4m3fn) codes of four fp32 values, packed low byte first, by gfx950's conversion
+// instruction (v_cvt_pk_fp8_f32, two values each): round to nearest, ties to the even mantissa, 3
+// mantissa bits in the normal range (2^-6 and up) and multiples of 2^-9 below it.  Every input here
+// has |y| <= 448 up to one rounding of its scaling product (which rounds back to 448).
+__device__ __forceinline__ uint32_t e4m3_pack4(float a, float b, float c, float d) {
+  const int lo = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
+  return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(c, d, lo, true);
 }
 
 __device__ __forceinline__ float wave_max(float v) {
@@ -62,9 +57,8 @@ __global__ __launch_bounds__(256) void quantize_fp8_rows_kernel(const u32x4* __r
       uint32_t w[2];
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
-        w[hh] = e4m3_code(__fmul_rn(bf16_lo(v[2 * hh]), inv)) | (e4m3_code(__fmul_rn(bf16_hi(v[2 * hh]), inv)) << 8) |
-                (e4m3_code(__fmul_rn(bf16_lo(v[2 * hh + 1]), inv)) << 16) |
-                (e4m3_code(__fmul_rn(bf16_hi(v[2 * hh + 1]), inv)) << 24);
+        w[hh] = e4m3_pack4(__fmul_rn(bf16_lo(v[2 * hh]), inv), __fmul_rn(bf16_hi(v[2 * hh]), inv),
+                           __fmul_rn(bf16_lo(v[2 * hh + 1]), inv), __fmul_rn(bf16_hi(v[2 * hh + 1]), inv));
       }
       qrow[c] = make_uint2(w[0], w[1]);
     }
@@ -155,18 +149,21 @@ __global__ __launch_bounds__(256) void quantize_cols_kernel(const uint16_t* __re
   const int64_t k_beg = kb * QC_KQ, k_end = (kb + 1) * QC_KQ < K ? (kb + 1) * QC_KQ : K;
   for (int64_t k0 = k_beg; k0 < k_end; k0 += 128) {
     uint32_t packed[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) packed[i] = 0;
+    u32x4 v[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int64_t k = k0 + 4 * rq + u;
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (k < k_end) v = ld_stream(reinterpret_cast<const u32x4*>(src + k * N));
+      v[u] = u32x4{0u, 0u, 0u, 0u};
+      if (k < k_end) v[u] = ld_stream(reinterpret_cast<const u32x4*>(src + k * N));
+    }
+    // column 2e (2e+1) of the chunk: its four rows' codes, row u in byte u
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        packed[2 * e] |= e4m3_code(__fmul_rn(bf16_lo(v[e]), inv[2 * e])) << (8 * u);
-        packed[2 * e + 1] |= e4m3_code(__fmul_rn(bf16_hi(v[e]), inv[2 * e + 1])) << (8 * u);
-      }
+    for (int e = 0; e < 4; ++e) {
+      packed[2 * e] = e4m3_pack4(__fmul_rn(bf16_lo(v[0][e]), inv[2 * e]), __fmul_rn(bf16_lo(v[1][e]), inv[2 * e]),
+                                 __fmul_rn(bf16_lo(v[2][e]), inv[2 * e]), __fmul_rn(bf16_lo(v[3][e]), inv[2 * e]));
+      packed[2 * e + 1] =
+          e4m3_pack4(__fmul_rn(bf16_hi(v[0][e]), inv[2 * e + 1]), __fmul_rn(bf16_hi(v[1][e]), inv[2 * e + 1]),
+                     __fmul_rn(bf16_hi(v[2][e]), inv[2 * e + 1]), __fmul_rn(bf16_hi(v[3][e]), inv[2 * e + 1]));
     }
     __syncthreads();   // the previous block's codes have been written out
 #pragma unroll
@@ -278,8 +275,9 @@ __device__ __forceinline__ uint32_t mx_scale_byte(float amax) {
 // finite bf16 inputs produce (0 .. 247)
 __device__ __forceinline__ float mx_inv_scale(uint32_t byte) { return __uint_as_float((254u - byte) << 23); }
 
+// the codes of a, b, c, d times an MX block's inverse scale (a power of two: the products are exact)
 __device__ __forceinline__ uint32_t e4m3_pack4(float a, float b, float c, float d, float inv) {
-  return e4m3_code(a * inv) | (e4m3_code(b * inv) << 8) | (e4m3_code(c * inv) << 16) | (e4m3_code(d * inv) << 24);
+  return e4m3_pack4(a * inv, b * inv, c * inv, d * inv);
 }
 
 // Scale byte of block b of row r in the MX scale layout of a matrix with `rows` rows: the four
