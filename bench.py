@@ -129,6 +129,9 @@ def _args():
     ap.add_argument("--gemm-probe", choices=["fwd", "dx", "dw"],
                     help="run one gate/up-shaped grouped GEMM (uniform groups of the chosen config) 3 times and "
                          "exit: the target of hardware-counter runs")
+    ap.add_argument("--vendor-loop", action="store_true",
+                    help="context only: the paper's dW1 shape (config 5) and the Mixtral-shaped gate/up forward "
+                         "through the library and through a per-expert hipBLASLt (torch.matmul) loop; one JSON line")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES bytes 3 times (counter calibration)")
     ap.add_argument("--flush", action="store_true",
@@ -281,6 +284,86 @@ def gemm_probe(kind, cfg):
     print(json.dumps({"gemm_probe": kind, "R": R, "d": d, "f": f, "E": E, "launches": 3}), flush=True)
 
 
+def vendor_loop():
+    """Context for the grouped kernels: the same products as a loop of per-expert vendor GEMMs
+    (hipBLASLt through torch.matmul on contiguous operands; the transposed X_e of the weight gradient
+    is copied out before timing).  Medians of 10 timed calls after 3 warm-up calls; each pair's
+    results are compared (relative Frobenius distance)."""
+    import torch
+
+    from paper_2606_26453_amd import moe
+    from paper_2606_26453_amd import workloads as W
+    dev = "cuda:0"
+
+    def med_ms(fn, reps=10, warm=3):
+        for _ in range(warm):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ts = []
+        for _ in range(reps):
+            a.record()
+            fn()
+            b.record()
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b))
+        return sorted(ts)[reps // 2]
+
+    rel = lambda x, y: float((x.float() - y.float()).norm() / y.float().norm())
+    out = {"metric": "vendor-loop context (not the benchmark metric)"}
+    # the paper's dW1 shape: dW_{g,u}[e] = X_e^T dH_{g,u,e}, bf16 results
+    cfg = W.CONFIGS[5]
+    inp = W.make_dw_inputs(cfg, 0, dev)
+    off, x, dg, du = inp["offsets"], inp["x_perm"], inp["dh_gate"], inp["dh_up"]
+    o = off.cpu().tolist()
+    E, d, f = cfg.E, cfg.d, cfg.f
+    cnt = moe.dw_counters(dev)
+    lg, lu = (torch.empty((E, d, f), dtype=torch.bfloat16, device=dev) for _ in range(2))
+    lib_ms = med_ms(lambda: moe.moe_grouped_gemm_dw_bf16(x, dg, off, du, dB=lg, dB2=lu, counters=cnt))
+    xt = [x[o[e]:o[e + 1]].t().contiguous() for e in range(E)]
+    vg, vu = torch.empty_like(lg), torch.empty_like(lu)
+
+    def loop_dw():
+        for e in range(E):
+            if o[e + 1] == o[e]:
+                vg[e].zero_()
+                vu[e].zero_()
+            else:
+                torch.matmul(xt[e], dg[o[e]:o[e + 1]], out=vg[e])
+                torch.matmul(xt[e], du[o[e]:o[e + 1]], out=vu[e])
+    loop_ms = med_ms(loop_dw)
+    fl = 4.0 * x.shape[0] * d * f
+    out["dw1_paper_shape"] = {"library_ms": round(lib_ms, 4), "vendor_loop_ms": round(loop_ms, 4),
+                              "library_tflops": round(fl / lib_ms / 1e9, 1), "vendor_tflops": round(fl / loop_ms / 1e9, 1),
+                              "rel_fro": max(rel(lg, vg), rel(lu, vu))}
+    del inp, x, dg, du, lg, lu, xt, vg, vu
+    torch.cuda.empty_cache()
+    # the Mixtral-shaped gate/up forward on uniform groups (the library also computes the SwiGLU)
+    cfg = W.CONFIGS[1]
+    R, d, f, E = cfg.T * cfg.k, cfg.d, cfg.f, cfg.E
+    g = torch.Generator(device=dev).manual_seed(0)
+    o = [R * e // E for e in range(E + 1)]
+    off = torch.tensor(o, dtype=torch.int32, device=dev)
+    x = torch.randn((R, d), generator=g, device=dev).to(torch.bfloat16)
+    wg, wu = ((torch.randn((E, d, f), generator=g, device=dev) * 0.02).to(torch.bfloat16) for _ in range(2))
+    hg, hu, act = (torch.empty((R, f), dtype=torch.bfloat16, device=dev) for _ in range(3))
+    ws = moe.split_workspace(dev)
+    lib_ms = med_ms(lambda: moe.moe_grouped_gemm_fwd(x, wg, off, wu, C=hg, C2=hu, act=act, workspace=ws))
+    vg, vu = torch.empty_like(hg), torch.empty_like(hu)
+
+    def loop_fwd():
+        for e in range(E):
+            torch.matmul(x[o[e]:o[e + 1]], wg[e], out=vg[o[e]:o[e + 1]])
+            torch.matmul(x[o[e]:o[e + 1]], wu[e], out=vu[o[e]:o[e + 1]])
+    loop_ms = med_ms(loop_fwd)
+    fl = 4.0 * R * d * f
+    out["mixtral_gate_up_forward"] = {"library_ms (with SwiGLU)": round(lib_ms, 4), "vendor_loop_ms": round(loop_ms, 4),
+                                      "library_tflops": round(fl / lib_ms / 1e9, 1),
+                                      "vendor_tflops": round(fl / loop_ms / 1e9, 1),
+                                      "rel_fro": max(rel(hg, vg), rel(hu, vu))}
+    print(json.dumps(out), flush=True)
+
+
 def cpu_baseline(cfg, inp, sample_tokens):
     """The CPU oracle (float64 numpy, as it stands) on a bounded sample of the same workload: the
     full layer forward+backward over the first `sample_tokens` tokens with all experts."""
@@ -381,6 +464,9 @@ def main():
     if a.gemm_probe:
         from paper_2606_26453_amd import workloads as W
         gemm_probe(a.gemm_probe, W.CONFIGS[a.config])
+        return
+    if a.vendor_loop:
+        vendor_loop()
         return
     if a.all_configs:
         all_configs(a)
