@@ -69,6 +69,42 @@ def test_quantize_mx_rows(M, K, joined):
     np.testing.assert_array_equal(_blocks(s, C), rs)
 
 
+def _every_bf16_in_range():
+    """Every finite bf16 value with |x| <= 448 (both zeros, subnormals, every exact tie between two
+    E4M3 values), 31 to a 32-element block whose last element is 448: each block's scale is then 2^0
+    (and each row's amax is 448), so every value's code is E4M3's rounding of the value itself."""
+    v = torch.arange(65536, dtype=torch.int32).to(torch.int16).view(torch.bfloat16)
+    v = v[torch.isfinite(v) & (v.float().abs() <= 448.0)]
+    n = (v.numel() + 31 * 64 - 1) // (31 * 64) * (31 * 64)
+    v = torch.cat([v, torch.zeros(n - v.numel(), dtype=torch.bfloat16)]).reshape(-1, 31)
+    x = torch.cat([v, torch.full((v.shape[0], 1), 448.0, dtype=torch.bfloat16)], dim=1)
+    return x.reshape(-1, 32 * 64)
+
+
+def test_quantize_every_bf16_value():
+    """The quantizers' E4M3 rounding (the hardware conversion) over every bf16 input in range, code
+    for code against the oracle: MX rows (block scale 2^0) and fp32-scale rows (scale 1)."""
+    x = _every_bf16_in_range()
+    M, K = x.shape
+    _say("quantize every bf16 value", M, K)
+    q = poison_(torch.empty((M, K), dtype=torch.uint8, device=DEV))
+    s = poison_(torch.empty((moe.mx_groups(K), M, 4), dtype=torch.uint8, device=DEV))
+    moe.moe_quantize_mx_rows(x.to(DEV), None, q, s)
+    q8 = poison_(torch.empty((M, K), dtype=torch.uint8, device=DEV))
+    s8 = poison_(torch.empty(M, dtype=torch.float32, device=DEV))
+    moe.moe_quantize_fp8_rows(x.to(DEV), q8, s8)
+    torch.cuda.synchronize()
+    rq, rs = O.quantize_rows_mx(f64(x))
+    assert (rs == 127).all()
+    np.testing.assert_array_equal(_u8(q), rq)
+    np.testing.assert_array_equal(_blocks(s, K), rs)
+    rq8, rs8 = O.quantize_rows_fp8(f64(x))
+    assert (rs8 == 1.0).all()
+    np.testing.assert_array_equal(_u8(q8), rq8)
+    np.testing.assert_array_equal(s8.cpu().numpy(), rs8)
+    np.testing.assert_array_equal(rq8, rq)   # the two formats agree when both scales are 1
+
+
 @pytest.mark.parametrize("G,K,N,dual", [(2, 64, 64, False), (3, 224, 128, True), (2, 4096, 256, True),
                                          (1, 2880, 2880, False), (2, 512, 1408, True), (1, 14336, 128, False)])
 def test_quantize_mx_weight(G, K, N, dual):
