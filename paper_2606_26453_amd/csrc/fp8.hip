@@ -313,14 +313,20 @@ __global__ __launch_bounds__(256) void quantize_mx_rows_kernel(const u32x4* __re
   }
 }
 
-// From a 128 x 64 bf16 tile staged row-major in LDS: the MX codes of column n over rows
-// 32*kb .. 32*kb + 31 (one block), packed 4 to a word in o[8]; returns the block's scale byte.
+// A 128 x 64 bf16 tile staged row-major in LDS with its 16-byte chunks (8 columns) permuted per
+// 32-row block: element (k, n) sits at k*64 + (n ^ 16*(k/32)), so that the lanes of a wavefront
+// reading 16 columns in each of the four blocks (below) cover four disjoint 32-byte spans of a
+// row, i.e. distinct banks.
+__device__ __forceinline__ int mx_tile_at(int k, int n) { return k * 64 + (n ^ ((k >> 5) << 4)); }
+
+// From that tile: the MX codes of column n over rows 32*kb .. 32*kb + 31 (one block), packed 4 to
+// a word in o[8]; returns the block's scale byte.
 __device__ __forceinline__ uint32_t mx_tile_col_block(const uint16_t* s_w, int n, int kb, uint32_t o[8]) {
   float v[32];
   float m = 0.0f;
 #pragma unroll
   for (int i = 0; i < 32; ++i) {
-    v[i] = __uint_as_float((uint32_t)s_w[(32 * kb + i) * 64 + n] << 16);
+    v[i] = __uint_as_float((uint32_t)s_w[mx_tile_at(32 * kb + i, n)] << 16);
     m = fmaxf(m, fabsf(v[i]));
   }
   const uint32_t byte = mx_scale_byte(m);
@@ -357,7 +363,7 @@ __global__ __launch_bounds__(256) void quantize_mx_weight_kernel(const uint16_t*
     const int64_t k = k0 + kl;
     u32x4 v = {0u, 0u, 0u, 0u};
     if (k < K) v = *reinterpret_cast<const u32x4*>(src + k * N + 8 * c8);
-    *reinterpret_cast<u32x4*>(s_w + kl * 64 + 8 * c8) = v;
+    *reinterpret_cast<u32x4*>(s_w + mx_tile_at(kl, 8 * c8)) = v;
     if (qr != nullptr) {
       float m = 0.0f;
 #pragma unroll
@@ -377,7 +383,9 @@ __global__ __launch_bounds__(256) void quantize_mx_weight_kernel(const uint16_t*
   }
   if (qt == nullptr) return;   // uniform
   __syncthreads();
-  const int n = t & 63, kb = t >> 6;
+  // thread -> column n = t/4, block kb = t%4: the four lanes of a column hold its 128 contiguous
+  // bytes of the output row, so a wavefront's stores touch 16 rows instead of 64
+  const int n = t >> 2, kb = t & 3;
   if (k0 + 32 * kb >= K) return;   // K is a multiple of 32: the block is whole or absent
   uint32_t o[8];
   const uint32_t byte = mx_tile_col_block(s_w, n, kb, o);
@@ -431,7 +439,7 @@ __global__ __launch_bounds__(256) void quantize_mx_tokens_t_kernel(const uint16_
     const int64_t r = src0 + kl;
     u32x4 v = {0u, 0u, 0u, 0u};
     if (r < src_end) v = *reinterpret_cast<const u32x4*>(x + r * C + n0 + 8 * c8);
-    *reinterpret_cast<u32x4*>(s_w + kl * 64 + 8 * c8) = v;
+    *reinterpret_cast<u32x4*>(s_w + mx_tile_at(kl, 8 * c8)) = v;
     if (qr != nullptr) {   // uniform; lanes t^1, t^2 share the block (same row)
       float m = 0.0f;
 #pragma unroll
@@ -451,7 +459,7 @@ __global__ __launch_bounds__(256) void quantize_mx_tokens_t_kernel(const uint16_
   }
   if (qt == nullptr) return;   // uniform
   __syncthreads();
-  const int n = t & 63, kb = t >> 6;
+  const int n = t >> 2, kb = t & 3;   // as in the weight kernel
   uint32_t o[8];
   const uint32_t byte = mx_tile_col_block(s_w, n, kb, o);
   uint8_t* dst = qt + (n0 + n) * ld + j0 + 32 * kb;
