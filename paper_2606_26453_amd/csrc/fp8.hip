@@ -313,20 +313,22 @@ __global__ __launch_bounds__(256) void quantize_mx_rows_kernel(const u32x4* __re
   }
 }
 
-// A 128 x 64 bf16 tile staged row-major in LDS with its 16-byte chunks (8 columns) permuted per
-// 32-row block: element (k, n) sits at k*64 + (n ^ 16*(k/32)), so that the lanes of a wavefront
+// A 128 x CW bf16 tile staged row-major in LDS with its 16-byte chunks (8 columns) permuted per
+// 32-row block: element (k, n) sits at k*CW + (n ^ 16*(k/32)), so that the lanes of a wavefront
 // reading 16 columns in each of the four blocks (below) cover four disjoint 32-byte spans of a
 // row, i.e. distinct banks.
-__device__ __forceinline__ int mx_tile_at(int k, int n) { return k * 64 + (n ^ ((k >> 5) << 4)); }
+template <int CW = 64>
+__device__ __forceinline__ int mx_tile_at(int k, int n) { return k * CW + (n ^ ((k >> 5) << 4)); }
 
 // From that tile: the MX codes of column n over rows 32*kb .. 32*kb + 31 (one block), packed 4 to
 // a word in o[8]; returns the block's scale byte.
+template <int CW = 64>
 __device__ __forceinline__ uint32_t mx_tile_col_block(const uint16_t* s_w, int n, int kb, uint32_t o[8]) {
   float v[32];
   float m = 0.0f;
 #pragma unroll
   for (int i = 0; i < 32; ++i) {
-    v[i] = __uint_as_float((uint32_t)s_w[mx_tile_at(32 * kb + i, n)] << 16);
+    v[i] = __uint_as_float((uint32_t)s_w[mx_tile_at<CW>(32 * kb + i, n)] << 16);
     m = fmaxf(m, fabsf(v[i]));
   }
   const uint32_t byte = mx_scale_byte(m);
@@ -336,34 +338,39 @@ __device__ __forceinline__ uint32_t mx_tile_col_block(const uint16_t* s_w, int n
   return byte;
 }
 
-// Weights, both orientations from one read.  Workgroup (column block n0 = 64*bx, row block
-// k0 = 128*by, matrix/expert bz) stages the 128 x 64 tile of W[g] (or W2[g]) in LDS:
+// Weights, both orientations from one read.  Workgroup (column block n0 = CW*bx, row block
+// k0 = 128*by, matrix/expert bz) stages the 128 x CW tile of W[g] (or W2[g]) in LDS (CW = 128
+// when N allows: each output row segment is then a whole 128-byte line, written by one workgroup):
 //   rows (qr, sr): row (g, k) of the [G, K, nmat*N] matrix [W[g] | W2[g]], blocks of 32 columns;
-//     thread t: column chunk t%8 of rows k0 + t/8 + 32u (u < 4), lanes t^1, t^2 share its block;
+//     thread t: column chunk t%(CW/8) of rows k0 + t/(CW/8) + (256/(CW/8))*u, lanes t^1, t^2
+//     share its block;
 //   columns (qt, st): row (g, n') of [G, N', K] = column n of W[g] (or W2[g], interleaved by 128
-//     as in the fp32-scale weight layout), blocks of 32 rows; thread t: column t%64, rows
-//     k0 + 32*(t/64) .. +31, 32 contiguous bytes of row n' (a workgroup writes 128 per row).
+//     as in the fp32-scale weight layout), blocks of 32 rows; thread t: columns t/4 + 64j, rows
+//     k0 + 32*(t%4) .. +31, 32 contiguous bytes of row n' (the four lanes of a column write its
+//     128 bytes of the row).
 // Scales in the MX scale layout of each output (rows G*K for qr, G*N' for qt).
+template <int CW>
 __global__ __launch_bounds__(256) void quantize_mx_weight_kernel(const uint16_t* __restrict__ w,
                                                                  const uint16_t* __restrict__ w2, int64_t G, int64_t K,
                                                                  int64_t N, uint8_t* __restrict__ qt,
                                                                  uint8_t* __restrict__ st, uint8_t* __restrict__ qr,
                                                                  uint8_t* __restrict__ sr) {
-  __shared__ __attribute__((aligned(16))) uint16_t s_w[128 * 64];
+  constexpr int CPR = CW / 8, RP = 256 / CPR;   // chunks per tile row, rows per pass
+  __shared__ __attribute__((aligned(16))) uint16_t s_w[128 * CW];
   const int t = threadIdx.x;
   const int nmat = w2 ? 2 : 1;
   const int64_t g = blockIdx.z / nmat;
   const bool second = (int)(blockIdx.z - g * nmat) == 1;
-  const int64_t n0 = (int64_t)blockIdx.x * 64, k0 = (int64_t)blockIdx.y * 128;
+  const int64_t n0 = (int64_t)blockIdx.x * CW, k0 = (int64_t)blockIdx.y * 128;
   const uint16_t* src = (second ? w2 : w) + g * K * N + n0;
-  const int c8 = t & 7, rq = t >> 3;
+  const int c8 = t % CPR, rq = t / CPR;
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int kl = rq + 32 * u;
+  for (int u = 0; u < 128 / RP; ++u) {
+    const int kl = rq + RP * u;
     const int64_t k = k0 + kl;
     u32x4 v = {0u, 0u, 0u, 0u};
     if (k < K) v = *reinterpret_cast<const u32x4*>(src + k * N + 8 * c8);
-    *reinterpret_cast<u32x4*>(s_w + mx_tile_at(kl, 8 * c8)) = v;
+    *reinterpret_cast<u32x4*>(s_w + mx_tile_at<CW>(kl, 8 * c8)) = v;
     if (qr != nullptr) {
       float m = 0.0f;
 #pragma unroll
@@ -383,17 +390,21 @@ __global__ __launch_bounds__(256) void quantize_mx_weight_kernel(const uint16_t*
   }
   if (qt == nullptr) return;   // uniform
   __syncthreads();
-  // thread -> column n = t/4, block kb = t%4: the four lanes of a column hold its 128 contiguous
-  // bytes of the output row, so a wavefront's stores touch 16 rows instead of 64
-  const int n = t >> 2, kb = t & 3;
+  // thread -> columns n = t/4 + 64j, block kb = t%4: the four lanes of a column hold its 128
+  // contiguous bytes of the output row, so a wavefront's stores touch 16 rows instead of 64
+  const int kb = t & 3;
   if (k0 + 32 * kb >= K) return;   // K is a multiple of 32: the block is whole or absent
-  uint32_t o[8];
-  const uint32_t byte = mx_tile_col_block(s_w, n, kb, o);
-  const int64_t row = g * (nmat * N) + qc_out_row(n0 + n, w2 != nullptr, second);
-  uint8_t* dst = qt + row * K + k0 + 32 * kb;
-  *reinterpret_cast<u32x4*>(dst) = u32x4{o[0], o[1], o[2], o[3]};
-  *reinterpret_cast<u32x4*>(dst + 16) = u32x4{o[4], o[5], o[6], o[7]};
-  st[mx_scale_at(row, (k0 >> 5) + kb, G * nmat * N)] = (uint8_t)byte;
+#pragma unroll
+  for (int j = 0; j < CW / 64; ++j) {
+    const int n = (t >> 2) + 64 * j;
+    uint32_t o[8];
+    const uint32_t byte = mx_tile_col_block<CW>(s_w, n, kb, o);
+    const int64_t row = g * (nmat * N) + qc_out_row(n0 + n, w2 != nullptr, second);
+    uint8_t* dst = qt + row * K + k0 + 32 * kb;
+    *reinterpret_cast<u32x4*>(dst) = u32x4{o[0], o[1], o[2], o[3]};
+    *reinterpret_cast<u32x4*>(dst + 16) = u32x4{o[4], o[5], o[6], o[7]};
+    st[mx_scale_at(row, (k0 >> 5) + kb, G * nmat * N)] = (uint8_t)byte;
+  }
 }
 
 // Token-major operands of the weight gradient: x [R, C] bf16, rows grouped by offsets -> qt [C, ld]
@@ -550,7 +561,11 @@ extern "C" moe_status moe_quantize_mx_weight(const moe_bf16* w, const moe_bf16* 
   if (!w) return fail(MOE_ERROR_INVALID_VALUE, "%s: NULL pointer", fn);
   if (!aligned16(w) || (w2 && !aligned16(w2)) || (qt && !aligned16(qt)) || (reinterpret_cast<uintptr_t>(qr) & 7))
     return fail(MOE_ERROR_INVALID_VALUE, "%s: w, w2 and qt must be 16-byte, qr 8-byte aligned", fn);
-  quantize_mx_weight_kernel<<<dim3((unsigned)(N / 64), (unsigned)((K + 127) / 128), (unsigned)(G * nmat)), 256, 0,
-                              stream>>>(w, w2, G, K, N, qt, st, qr, sr);
+  if (N % 128 == 0)
+    quantize_mx_weight_kernel<128><<<dim3((unsigned)(N / 128), (unsigned)((K + 127) / 128), (unsigned)(G * nmat)),
+                                     256, 0, stream>>>(w, w2, G, K, N, qt, st, qr, sr);
+  else
+    quantize_mx_weight_kernel<64><<<dim3((unsigned)(N / 64), (unsigned)((K + 127) / 128), (unsigned)(G * nmat)),
+                                    256, 0, stream>>>(w, w2, G, K, N, qt, st, qr, sr);
   return check_launch("quantize_mx_weight_kernel");
 }
