@@ -411,21 +411,24 @@ __global__ __launch_bounds__(256) void quantize_mx_weight_kernel(const uint16_t*
 // codes with group g's K_g rows as columns p[g] .. p[g] + K_g - 1, p the prefix of the counts
 // rounded up to 128 (no 32-element block spans two groups, and each group starts a 128-element
 // scale word), zero codes in each group's padding; scales in the MX layout of C rows of ld.
-// Workgroup (64-column block n0 = 64*bx of x, 128-column block j0 = 128*by of qt) stages the 128
-// source rows that land in columns j0 .. j0+127 (zeros past the group's end) and quantizes them
+// Workgroup (CW-column block n0 = CW*bx of x, CW = 128 when the widths allow, else 64; 128-column
+// block j0 = 128*by of qt) stages the 128 source rows that land in columns j0 .. j0+127 (zeros past
+// the group's end) and quantizes them
 // column by column as the weight kernel's transposed half does; blocks past p[G] are left alone.
 // With qr, the same read also gives the row-wise codes (every source row lies in exactly one such
 // tile): row r's blocks of 32 columns go to qr[r, col0 + c] (rows of ldr bytes, e.g. one half of
 // the joined rows [dH_gate | dH_up]) with scales in the MX layout of R rows of ldr.
+template <int CW>
 __global__ __launch_bounds__(256) void quantize_mx_tokens_t_kernel(const uint16_t* __restrict__ x,
                                                                    const int32_t* __restrict__ offsets, int G,
                                                                    int64_t R, int64_t C, int64_t ld,
                                                                    uint8_t* __restrict__ qt, uint8_t* __restrict__ st,
                                                                    uint8_t* __restrict__ qr, uint8_t* __restrict__ sr,
                                                                    int64_t ldr, int64_t col0) {
+  constexpr int CPR = CW / 8, RP = 256 / CPR;   // chunks per tile row, rows per pass
   __shared__ int s_o[257];
   __shared__ int s_p[257];
-  __shared__ __attribute__((aligned(16))) uint16_t s_w[128 * 64];
+  __shared__ __attribute__((aligned(16))) uint16_t s_w[128 * CW];
   const int t = threadIdx.x;
   for (int i = t; i <= G; i += 256) s_o[i] = offsets[i];
   __syncthreads();
@@ -442,15 +445,15 @@ __global__ __launch_bounds__(256) void quantize_mx_tokens_t_kernel(const uint16_
   if (j0 >= s_p[G]) return;   // uniform
   const int g = __syncthreads_count(t < G && s_p[t + 1] <= j0);   // the group holding j0 .. j0+127
   const int64_t src0 = s_o[g] + (j0 - s_p[g]), src_end = s_o[g + 1];
-  const int64_t n0 = (int64_t)blockIdx.x * 64;
-  const int c8 = t & 7, rq = t >> 3;
+  const int64_t n0 = (int64_t)blockIdx.x * CW;
+  const int c8 = t % CPR, rq = t / CPR;
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int kl = rq + 32 * u;
+  for (int u = 0; u < 128 / RP; ++u) {
+    const int kl = rq + RP * u;
     const int64_t r = src0 + kl;
     u32x4 v = {0u, 0u, 0u, 0u};
     if (r < src_end) v = *reinterpret_cast<const u32x4*>(x + r * C + n0 + 8 * c8);
-    *reinterpret_cast<u32x4*>(s_w + mx_tile_at(kl, 8 * c8)) = v;
+    *reinterpret_cast<u32x4*>(s_w + mx_tile_at<CW>(kl, 8 * c8)) = v;
     if (qr != nullptr) {   // uniform; lanes t^1, t^2 share the block (same row)
       float m = 0.0f;
 #pragma unroll
@@ -470,13 +473,17 @@ __global__ __launch_bounds__(256) void quantize_mx_tokens_t_kernel(const uint16_
   }
   if (qt == nullptr) return;   // uniform
   __syncthreads();
-  const int n = t >> 2, kb = t & 3;   // as in the weight kernel
-  uint32_t o[8];
-  const uint32_t byte = mx_tile_col_block(s_w, n, kb, o);
-  uint8_t* dst = qt + (n0 + n) * ld + j0 + 32 * kb;
-  *reinterpret_cast<u32x4*>(dst) = u32x4{o[0], o[1], o[2], o[3]};
-  *reinterpret_cast<u32x4*>(dst + 16) = u32x4{o[4], o[5], o[6], o[7]};
-  st[mx_scale_at(n0 + n, (j0 >> 5) + kb, C)] = (uint8_t)byte;
+  const int kb = t & 3;   // columns t/4 + 64j, as in the weight kernel
+#pragma unroll
+  for (int j = 0; j < CW / 64; ++j) {
+    const int n = (t >> 2) + 64 * j;
+    uint32_t o[8];
+    const uint32_t byte = mx_tile_col_block<CW>(s_w, n, kb, o);
+    uint8_t* dst = qt + (n0 + n) * ld + j0 + 32 * kb;
+    *reinterpret_cast<u32x4*>(dst) = u32x4{o[0], o[1], o[2], o[3]};
+    *reinterpret_cast<u32x4*>(dst + 16) = u32x4{o[4], o[5], o[6], o[7]};
+    st[mx_scale_at(n0 + n, (j0 >> 5) + kb, C)] = (uint8_t)byte;
+  }
 }
 
 }  // namespace
@@ -506,8 +513,13 @@ moe_status quantize_mx_tokens_impl(const char* fn, const moe_bf16* x, const int3
   if ((x && !aligned16(x)) || (qt && !aligned16(qt)) || (reinterpret_cast<uintptr_t>(qr) & 7))
     return fail(MOE_ERROR_INVALID_VALUE, "%s: x and qt must be 16-byte, qr 8-byte aligned", fn);
   if (R == 0) return MOE_SUCCESS;
-  quantize_mx_tokens_t_kernel<<<dim3((unsigned)(C / 64), (unsigned)(ld / 128)), 256, 0, stream>>>(
-      x, offsets, G, R, C, ld, qt, st, qr, sr, ldr, col0);
+  // 128-column tiles when the width allows (each row-code segment a whole 128-byte line)
+  if (C % 128 == 0 && col0 % 128 == 0)
+    quantize_mx_tokens_t_kernel<128><<<dim3((unsigned)(C / 128), (unsigned)(ld / 128)), 256, 0, stream>>>(
+        x, offsets, G, R, C, ld, qt, st, qr, sr, ldr, col0);
+  else
+    quantize_mx_tokens_t_kernel<64><<<dim3((unsigned)(C / 64), (unsigned)(ld / 128)), 256, 0, stream>>>(
+        x, offsets, G, R, C, ld, qt, st, qr, sr, ldr, col0);
   return check_launch("quantize_mx_tokens_t_kernel");
 }
 }  // namespace

@@ -351,7 +351,7 @@ def test_grouped_gemm_mx_256_groups_exact():
 # The weight gradient on MX operands quantized along the tokens
 # ------------------------------------------------------------------------------------------------
 @pytest.mark.parametrize("counts,C", [([5, 0, 130, 128, 1, 300], 64), ([129, 127, 0, 0, 256], 320),
-                                      ([1], 128), ([700, 3, 41], 192)])
+                                      ([1], 128), ([700, 3, 41], 192), ([129, 1, 300, 0], 384)])
 def test_quantize_mx_tokens_t(counts, C):
     """Token-major codes and scales bit for bit against the oracle's packing (each expert's rows as
     columns from a 128-aligned start, zeros in the padding) quantized row by row; empty groups,
@@ -377,7 +377,8 @@ def test_quantize_mx_tokens_t(counts, C):
     np.testing.assert_array_equal(_blocks(st, ld)[:, : L // 32], rs)
 
 
-@pytest.mark.parametrize("counts,C", [([5, 0, 130, 128, 1, 300], 64), ([700, 3, 41], 192)])
+@pytest.mark.parametrize("counts,C", [([5, 0, 130, 128, 1, 300], 64), ([700, 3, 41], 192),
+                                      ([129, 1, 300, 0], 256)])   # 128-column tiles (C, col0 % 128 == 0)
 def test_quantize_mx_tokens_both(counts, C):
     """moe_quantize_mx_tokens: from one read, the token-major codes (equal to
     moe_quantize_mx_tokens_t's) and the row codes bit for bit against the oracle's row quantizer;
