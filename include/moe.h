@@ -571,6 +571,28 @@ moe_status moe_grouped_gemm_dw_bf16_persistent(const moe_bf16* A, const moe_bf16
                                                hipStream_t stream);
 
 /*
+ * moe_grouped_gemm_dw_persistent with a split workspace (dB = A^T dC over one group's rows, fp32;
+ * the weight gradient of section 5.4 and Appendix H):
+ * with a single group (G == 1, e.g. the shared experts' weight gradient over all T tokens) every
+ * tile has the same contraction, and when the tiles do not fill the last round of CU slots (fewer
+ * tiles than CUs included) those tiles are split along the contraction into up to 8 pieces of at
+ * least 64 steps, each piece's fp32 partial tile goes to the workspace, and the last piece to
+ * arrive sums the pieces in piece order (a fixed order: the result does not depend on which
+ * piece finishes last) and stores the tile, as the split forms of the forward and dX products
+ * do.  Split tiles sum their contraction in a different association than the unsplit kernel
+ * (each piece separately, then the pieces), so results can differ from it by rounding.  With
+ * G > 1 the workspace is not used and the call equals moe_grouped_gemm_dw_persistent.
+ * workspace: moe_grouped_gemm_split_workspace_bytes() bytes, 16-byte aligned, caller-owned; its
+ * counters are zeroed on `stream` by the call; calls sharing it must be ordered.  A smaller or
+ * misaligned workspace: MOE_ERROR_WORKSPACE; NULL: no split.  Everything else as
+ * moe_grouped_gemm_dw_persistent.
+ */
+moe_status moe_grouped_gemm_dw_split(const moe_bf16* A, const moe_bf16* dC, const moe_bf16* dC2,
+                                     const int32_t* offsets, int32_t G, int64_t R, int64_t K, int64_t N,
+                                     float* dB, float* dB2, int32_t* counters, void* workspace,
+                                     size_t workspace_bytes, hipStream_t stream);
+
+/*
  * The weight gradient of moe_grouped_gemm_dw from contraction-major copies of its operands
  * (the layout moe_transpose_grouped writes): At [K, ld] and dCt, dC2t [N, ld] bf16, in which
  * group g's rows occupy columns pstart[g] .. pstart[g] + K_g - 1, pstart[g] = sum over h < g of

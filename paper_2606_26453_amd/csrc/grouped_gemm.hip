@@ -1180,6 +1180,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, WPE) void grouped_gemm_kern
         // split_min_steps long (short pieces cost more in partial-tile traffic than they save)
         int64_t clen;
         if constexpr (KIND == KIND_FWD) clen = p.K;
+        else if constexpr (IS_DW) clen = (KIND == KIND_DW && p.G == 1) ? s_off[1] - s_off[0] : 0;   // one group
         else clen = (DUAL && !F8) ? 2 * p.N : p.N;
         const int csteps = (int)((clen + BKE - 1) / BKE);
         int sp = slots / tail;
@@ -1391,7 +1392,14 @@ moe_status launch(const GemmParams& p, int64_t tiles_bound, hipStream_t stream, 
   if constexpr (PERSIST) {
     unsigned slots = (unsigned)device_cu_count() * C::WPE;
     if (slots > 8) slots &= ~7u;
-    if (grid > slots) grid = slots;
+    if (grid > slots) {
+      grid = slots;
+    } else if (p.split_part != nullptr) {
+      // fewer tiles than slots: every slot runs when the contraction is long enough for the tiles
+      // to be split into pieces (single-group dW: the group's rows; dX: N or 2N)
+      const int64_t clen = (KIND == KIND_DW) ? (p.G == 1 ? p.R : 0) : ((DUAL && !F8) ? 2 * p.N : p.N);
+      if (clen / (F8 ? 2 * BK : BK) >= 2 * SPLIT_MIN_STEPS) grid = slots;
+    }
   } else if (p.split_part != nullptr) {
     grid += SPLIT_UNITS;   // the split units run past the full rounds' tiles (idle ones exit)
   }
@@ -1776,7 +1784,7 @@ namespace {
 moe_status grouped_gemm_dw_impl(const char* fn, bool out16, const moe_bf16* A, const moe_bf16* dC,
                                 const moe_bf16* dC2, const int32_t* offsets, int32_t G, int64_t R,
                                 int64_t K, int64_t N, void* dB, void* dB2, int32_t* counters,
-                                bool persistent, hipStream_t stream) {
+                                bool persistent, hipStream_t stream, void* ws = nullptr, size_t ws_bytes = 0) {
   if (persistent && (counters == nullptr || (reinterpret_cast<uintptr_t>(counters) & 3u)))
     return fail(MOE_ERROR_INVALID_VALUE, "%s: counters must be 8 int32 of device memory", fn);
   if (G < 1 || G > 256) return fail(MOE_ERROR_NOT_SUPPORTED, "%s: need 1 <= G <= 256", fn);
@@ -1796,9 +1804,15 @@ moe_status grouped_gemm_dw_impl(const char* fn, bool out16, const moe_bf16* A, c
   const int cols_per_tile = dC2 ? TN / 2 : TN;
   p.n_tiles = (int)((N + cols_per_tile - 1) / cols_per_tile);
   const int64_t tiles = (int64_t)G * p.m_tiles * p.n_tiles;
+  if (ws != nullptr && (ws_bytes < SPLIT_BYTES || !aligned16(ws)))   // before any launch
+    return fail(MOE_ERROR_WORKSPACE, "%s: a 16-byte aligned workspace of %zu bytes is needed", fn, SPLIT_BYTES);
   if (persistent && tiles > 0) {
     p.tile_queue = counters;
     zero_i32_kernel<<<1, 64, 0, stream>>>(counters, 8);
+    if (G == 1) {   // one group: the last round's tiles may be split along the contraction
+      const moe_status st = attach_split(p, ws, ws_bytes, fn, stream);
+      if (st != MOE_SUCCESS) return st;
+    }
     if (out16) {
       if (dC2) return launch<KIND_DW, true, false, true, false, false, true>(p, tiles, stream, "grouped_gemm_dw_bf16(dual, persistent)");
       return launch<KIND_DW, false, false, true, false, false, true>(p, tiles, stream, "grouped_gemm_dw_bf16(persistent)");
@@ -1920,6 +1934,14 @@ extern "C" moe_status moe_grouped_gemm_dw_persistent(const moe_bf16* A, const mo
                                                      hipStream_t stream) {
   return grouped_gemm_dw_impl("moe_grouped_gemm_dw_persistent", false, A, dC, dC2, offsets, G, R, K, N, dB, dB2,
                               counters, true, stream);
+}
+
+extern "C" moe_status moe_grouped_gemm_dw_split(const moe_bf16* A, const moe_bf16* dC, const moe_bf16* dC2,
+                                                const int32_t* offsets, int32_t G, int64_t R, int64_t K, int64_t N,
+                                                float* dB, float* dB2, int32_t* counters, void* workspace,
+                                                size_t workspace_bytes, hipStream_t stream) {
+  return grouped_gemm_dw_impl("moe_grouped_gemm_dw_split", false, A, dC, dC2, offsets, G, R, K, N, dB, dB2,
+                              counters, true, stream, workspace, workspace_bytes);
 }
 
 extern "C" moe_status moe_grouped_gemm_dw_bf16(const moe_bf16* A, const moe_bf16* dC, const moe_bf16* dC2,

@@ -132,6 +132,9 @@ class MoELayer(_Traced):
         # kernel's last partial round of tiles fills with the other's tiles
         self.concurrent = concurrent
         self.side = torch.cuda.Stream(device=inputs["x"].device) if concurrent else None
+        # the shared experts' products (G = 1) take a split workspace too; on the side stream, one
+        # of their own (calls that may overlap need separate workspaces)
+        self.split_ws_side = moe.split_workspace(inputs["x"].device) if (split_tail and concurrent) else None
         self.router = router
         # with the router at E <= 16, d <= 4096 its backward (dlogits, dWr) runs as soon as d_topk_w
         # exists, and its share of dX joins the experts' unpermute-sum in one pass over dX
@@ -276,10 +279,11 @@ class MoELayer(_Traced):
         add = None
         if self.shared:                   # the shared FFN needs only x: beside the routed experts
             wg, wu, wd = self.w_sh
+            sws = self.split_ws if side is main else self.split_ws_side
             run("fwd_gate_up_sh", moe.moe_grouped_gemm_fwd, i["x"], wg, self.offsets_sh, wu, b["h_gate_sh"],
-                b["h_up_sh"], b["act_sh"], want_act=True, stream=side)
+                b["h_up_sh"], b["act_sh"], want_act=True, stream=side, workspace=sws)
             run("fwd_down_sh", moe.moe_grouped_gemm_fwd, b["act_sh"], wd, self.offsets_sh, C=b["y_sh"],
-                stream=side)
+                stream=side, workspace=sws)
             add = b["y_sh"]
         logits = i["logits"]
         if self.router:
@@ -350,21 +354,24 @@ class MoELayer(_Traced):
         dx_add = None
         if self.shared:                   # needs dY and the shared forward only
             wg, wu, wd = self.w_sh
+            sws = self.split_ws if side is main else self.split_ws_side
+            dws = sws if self.dw_cnt is not None else None  # the dW split needs the persistent form
             if self.fuse:
                 run("dx_down_swiglu_bwd_sh", moe.moe_grouped_gemm_dx_swiglu_bwd, i["dy"], wd, self.offsets_sh,
-                    b["h_gate_sh"], b["h_up_sh"], b["dh_gate_sh"], b["dh_up_sh"], stream=side)
+                    b["h_gate_sh"], b["h_up_sh"], b["dh_gate_sh"], b["dh_up_sh"], stream=side, workspace=sws)
             else:
                 run("dx_down_sh", moe.moe_grouped_gemm_dx, i["dy"], wd, self.offsets_sh, dA=b["d_act_sh"],
-                    stream=side)
+                    stream=side, workspace=sws)
             run("dw_down_sh", moe.moe_grouped_gemm_dw, b["act_sh"], i["dy"], self.offsets_sh,
-                dB=b["dw_down_sh"], stream=side, counters=self.dw_cnt)
+                dB=b["dw_down_sh"], stream=side, counters=self.dw_cnt, workspace=dws)
             if not self.fuse:
                 run("swiglu_bwd_sh", moe.moe_swiglu_bwd, b["h_gate_sh"], b["h_up_sh"], b["d_act_sh"],
                     b["dh_gate_sh"], b["dh_up_sh"], stream=side)
             run("dx_gate_up_sh", moe.moe_grouped_gemm_dx, b["dh_gate_sh"], wg, self.offsets_sh, b["dh_up_sh"],
-                wu, dA=b["dx_sh"], stream=side)
+                wu, dA=b["dx_sh"], stream=side, workspace=sws)
             run("dw_gate_up_sh", moe.moe_grouped_gemm_dw, i["x"], b["dh_gate_sh"], self.offsets_sh,
-                b["dh_up_sh"], dB=b["dw_gate_sh"], dB2=b["dw_up_sh"], stream=side, counters=self.dw_cnt)
+                b["dh_up_sh"], dB=b["dw_gate_sh"], dB2=b["dw_up_sh"], stream=side, counters=self.dw_cnt,
+                workspace=dws)
             dx_add = b["dx_sh"]
         run("combine_bwd", moe.moe_unpermute_combine_bwd, i["dy"], b["topk_w"], b["row_of_slot"], k,
             y_perm=b["y_perm"], dy_perm=b["dy_perm"], d_topk_w=b["d_topk_w"], stream=stream)

@@ -79,6 +79,8 @@ _SIG = {
     "moe_grouped_gemm_dw_bf16": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P]),
     "moe_grouped_gemm_dw_persistent": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P, _P]),
     "moe_grouped_gemm_dw_bf16_persistent": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P, _P]),
+    "moe_grouped_gemm_dw_split": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, _P, _P,
+                                                 ctypes.c_size_t, _P]),
     "moe_grouped_gemm_split_workspace_bytes": (ctypes.c_size_t, []),
     "moe_grouped_gemm_dx_split": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _I64, _I64, _I64, _P, _P, ctypes.c_size_t,
                                                  _P]),
@@ -756,7 +758,8 @@ def moe_unpermute_combine_bwd(dy, topk_w, row_of_slot, k, y_perm=None, dy_perm=N
 
 
 def split_workspace(device):
-    """A workspace for the split-tail variants of the persistent dX products."""
+    """A workspace for the split-tail variants of the fwd and persistent dX products and of the
+    single-group persistent dW."""
     return torch.empty(lib().moe_grouped_gemm_split_workspace_bytes(), dtype=torch.uint8, device=device)
 
 
@@ -788,9 +791,11 @@ def dw_counters(device):
     return torch.zeros(8, dtype=torch.int32, device=device)
 
 
-def moe_grouped_gemm_dw(A, dC, offsets, dC2=None, dB=None, dB2=None, stream=None, counters=None):
+def moe_grouped_gemm_dw(A, dC, offsets, dC2=None, dB=None, dB2=None, stream=None, counters=None, workspace=None):
     """dB[g] = A_g^T dC_g (and dB2 from dC2) in fp32.  counters (from dw_counters): run the
-    persistent entry point, which hands out tiles through them (bit-identical results)."""
+    persistent entry point, which hands out tiles through them (bit-identical results); with a
+    split workspace as well (split_workspace), moe_grouped_gemm_dw_split, which splits a single
+    group's last-round tiles along the contraction."""
     R, K = A.shape
     N = dC.shape[1]
     G = offsets.numel() - 1
@@ -803,8 +808,16 @@ def moe_grouped_gemm_dw(A, dC, offsets, dC2=None, dB=None, dB2=None, stream=None
         dB2 = torch.empty((G, K, N), dtype=torch.float32, device=A.device)
     _need(dB, torch.float32, (G, K, N), "dB")
     _need(dB2, torch.float32, (G, K, N), "dB2")
+    if workspace is not None and counters is None:
+        raise ValueError("moe_grouped_gemm_dw: a split workspace needs counters (the persistent form)")
     if counters is not None:
         _need(counters, torch.int32, (8,), "counters")
+        if workspace is not None:
+            _check("moe_grouped_gemm_dw_split",
+                   lib().moe_grouped_gemm_dw_split(_ptr(A), _ptr(dC), _ptr(dC2), _ptr(offsets), G, R, K, N,
+                                                   _ptr(dB), _ptr(dB2), _ptr(counters), _ptr(workspace),
+                                                   workspace.numel(), _stream(stream)))
+            return dB, dB2
         _check("moe_grouped_gemm_dw_persistent",
                lib().moe_grouped_gemm_dw_persistent(_ptr(A), _ptr(dC), _ptr(dC2), _ptr(offsets), G, R, K, N,
                                                     _ptr(dB), _ptr(dB2), _ptr(counters), _stream(stream)))

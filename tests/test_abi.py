@@ -105,6 +105,11 @@ def test_split_rejects():
     fwd = lambda ws=FAKE, n=need, N=128: L.moe_grouped_gemm_fwd_split(
         FAKE, FAKE, None, FAKE, 4, 100, 128, N, FAKE, None, None, ws, n, None)
     assert fwd(ws=None) == 3 and fwd(n=need // 2) == 3 and fwd(N=96) == 2
+    # the split dW: counters first, then a given workspace must be whole and aligned (NULL: no split)
+    dws = lambda cnt=FAKE, ws=FAKE, n=need, K=128: L.moe_grouped_gemm_dw_split(
+        FAKE, FAKE, None, FAKE, 1, 100, K, 128, FAKE, None, cnt, ws, n, None)
+    assert dws(cnt=None) == 1 and dws(cnt=BAD) == 1 and dws(n=need - 1) == 3 and dws(ws=BAD) == 3
+    assert dws(K=65) == 2
 
 
 def test_fp8_rejects():

@@ -190,6 +190,41 @@ def test_grouped_gemm_dw_exact(K, N):
     assert torch.count_nonzero(dB[5]) == 0 and torch.count_nonzero(dB[10]) == 0   # empty groups
 
 
+@pytest.mark.parametrize("K,N,R,dual", [(512, 256, 8192, False),      # 2 tiles: every tile split (4 pieces)
+                                         (512, 256, 8192, True),
+                                         (4352, 4096, 16384, False),    # 272 tiles: a round plus 16 split 8 ways
+                                         (256, 256, 4000, True)])       # contraction too short to split
+def test_grouped_gemm_dw_split_exact(K, N, R, dual):
+    """moe_grouped_gemm_dw_split on one group (the shared experts' weight gradient): tiles of the
+    last round split along the contraction, partial tiles summed in piece order; exact against
+    the oracle on small-integer operands (every partial and total sum exact in fp32), twice in a
+    row on the same counters and workspace; with several groups the workspace is unused and the
+    result is bitwise moe_grouped_gemm_dw_persistent's."""
+    _say("gemm dw split", K, N, R, dual)
+    g = torch.Generator().manual_seed(K + N + R + dual)
+    off = torch.tensor([0, R], dtype=torch.int32)
+    A = _int_tensor(g, (R, K), -1, 1).to(DEV)
+    dC = _int_tensor(g, (R, N), -1, 1).to(DEV)
+    dC2 = _int_tensor(g, (R, N), -1, 1).to(DEV) if dual else None
+    cnt, ws = moe.dw_counters(DEV), moe.split_workspace(DEV)
+    ref = O.grouped_gemm_dw(f64(A), f64(dC), off.numpy())
+    ref2 = O.grouped_gemm_dw(f64(A), f64(dC2), off.numpy()) if dual else None
+    for _ in range(2):
+        dB = poison_(torch.empty((1, K, N), dtype=torch.float32, device=DEV))
+        dB2 = poison_(torch.empty((1, K, N), dtype=torch.float32, device=DEV)) if dual else None
+        moe.moe_grouped_gemm_dw(A, dC, off.to(DEV), dC2, dB=dB, dB2=dB2, counters=cnt, workspace=ws)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(f64(dB), ref)
+        if dual:
+            np.testing.assert_array_equal(f64(dB2), ref2)
+    # several groups: no split, bitwise the persistent kernel
+    off3 = torch.tensor([0, R // 3, R // 3, R], dtype=torch.int32, device=DEV)
+    a, _ = moe.moe_grouped_gemm_dw(A, dC, off3, counters=cnt, workspace=ws)
+    b, _ = moe.moe_grouped_gemm_dw(A, dC, off3, counters=cnt)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
 def test_grouped_gemm_256_groups_exact():
     """The maximum group count (G = 256, empty groups included) with more row tiles than CUs, so
     the persistent dX kernel walks several tiles per workgroup: every product exact on
