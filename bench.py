@@ -43,7 +43,7 @@ METRIC = "MoE layer fwd+bwd tokens/sec + grouped-GEMM TFLOP/s (% of bf16 MFMA pe
 # Valid only for the kernel code they were measured on (sha256 prefix of the sources with comments
 # and blank lines removed); otherwise reported null.
 TRAFFIC_SOURCES = {
-    "gemm": (("paper_2606_26453_amd/csrc/grouped_gemm.hip", "paper_2606_26453_amd/csrc/common.h"), "73dd335ad465117d"),
+    "gemm": (("paper_2606_26453_amd/csrc/grouped_gemm.hip", "paper_2606_26453_amd/csrc/common.h"), "3da9d8a52732f4f6"),
     "route": (("paper_2606_26453_amd/csrc/route_permute.hip", "paper_2606_26453_amd/csrc/common.h"), "72087f561c2c164f"),
     "combine": (("paper_2606_26453_amd/csrc/elementwise.hip", "paper_2606_26453_amd/csrc/common.h"), "5fb5e5e15e3e53f4"),
 }
@@ -51,11 +51,11 @@ TRAFFIC_CONFIG = 1
 FETCH_SCALE, WRITE_SCALE = 2.0 * 1024, 1.0 * 1024
 TRAFFIC_KIB = {  # call: (source group, FETCH_SIZE KiB, WRITE_SIZE KiB) per dispatch (routing: both launches)
     "route_permute": ("route", 33112, 131518),
-    "fwd_gate_up": ("gemm", 5571924, 1399104), "fwd_down": ("gemm", 1959399, 199688),
+    "fwd_gate_up": ("gemm", 5344905, 1399104), "fwd_down": ("gemm", 1968892, 199688),
     "combine": ("combine", 65813, 65536), "combine_bwd": ("combine", 98585, 131137),
-    "dw_down": ("gemm", 1442040, 1835232), "dx_down_swiglu_bwd": ("gemm", 3867640, 917504),
-    "dx_gate_up": ("gemm", 4033380, 196616), "unpermute_dx": ("combine", 65692, 65536),
-    "dw_gate_up": ("gemm", 2774456, 3670464),
+    "dw_down": ("gemm", 1442369, 1835232), "dx_down_swiglu_bwd": ("gemm", 3827159, 917504),
+    "dx_gate_up": ("gemm", 4034670, 196616), "unpermute_dx": ("combine", 65692, 65536),
+    "dw_gate_up": ("gemm", 2773784, 3670464),
 }
 
 
