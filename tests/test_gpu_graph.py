@@ -39,11 +39,13 @@ def _written(lay, k):
     (0, {"fp8_forward": True, "fp8_backward": True, "mx": True, "fp8_dw": True}),
     (2, {"combine_fused": True}),
     (5, {}),
-], ids=["cfg0", "cfg2", "cfg0-router", "cfg0-mx", "cfg2-combine-fused", "cfg5-dw1"])
+    (2, {"full": True}),
+], ids=["cfg0", "cfg2", "cfg0-router", "cfg0-mx", "cfg2-combine-fused", "cfg5-dw1", "cfg2-full"])
 def test_graph_replay_bitwise(cfg_id, opts):
     import dataclasses
+    opts = dict(opts)
     cfg = W.CONFIGS[cfg_id]
-    if cfg_id == 2:
+    if cfg_id == 2 and not opts.pop("full", False):   # full size: the shared experts' dW is split
         cfg = dataclasses.replace(cfg, T=1024)
     _say("graph replay", cfg_id, opts)
     if cfg.dw_only:

@@ -217,6 +217,12 @@ def test_grouped_gemm_dw_split_exact(K, N, R, dual):
         np.testing.assert_array_equal(f64(dB), ref)
         if dual:
             np.testing.assert_array_equal(f64(dB2), ref2)
+    # an empty group: exact zeros (nothing to split)
+    z = poison_(torch.empty((1, K, N), dtype=torch.float32, device=DEV))
+    moe.moe_grouped_gemm_dw(A[:0], dC[:0], torch.zeros(2, dtype=torch.int32, device=DEV), dB=z, counters=cnt,
+                            workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(z) == 0
     # several groups: no split, bitwise the persistent kernel
     off3 = torch.tensor([0, R // 3, R // 3, R], dtype=torch.int32, device=DEV)
     a, _ = moe.moe_grouped_gemm_dw(A, dC, off3, counters=cnt, workspace=ws)
