@@ -169,6 +169,37 @@ def test_combine_exact(k, d):
             np.testing.assert_array_equal(f64(d_w), ref_w)
 
 
+def test_combine_exact_large():
+    """The weighted combine over a Y_perm larger than half the Infinity Cache (the streaming-load
+    branch; 8192 tokens x top-4 x d = 4096: 256 MiB), with the added rows, and its backward: exact
+    against the oracle on small integers with power-of-two weights, on 256 sampled tokens (the
+    oracle reads only their slots' rows)."""
+    T, k, d = 8192, 4, 4096
+    _say("combine exact large", T, k, d)
+    g = torch.Generator().manual_seed(4096)
+    R = T * k
+    row_of_slot = torch.randperm(R, generator=g).to(torch.int32)
+    w = (2.0 ** torch.randint(-2, 2, (T, k), generator=g)).to(torch.float32)
+    y_perm = _int_tensor(g, (R, d), -8, 8)
+    add = _int_tensor(g, (T, d), -8, 8)
+    dy = _int_tensor(g, (T, d), -8, 8)
+    y = poison_(torch.empty((T, d), dtype=torch.bfloat16, device=DEV))
+    moe.moe_unpermute_combine(y_perm.to(DEV), w.to(DEV), row_of_slot.to(DEV), k, add=add.to(DEV), y=y)
+    dy_perm = poison_(torch.empty((R, d), dtype=torch.bfloat16, device=DEV))
+    d_w = poison_(torch.empty((T, k), dtype=torch.float32, device=DEV))
+    moe.moe_unpermute_combine_bwd(dy.to(DEV), w.to(DEV), row_of_slot.to(DEV), k, y_perm=y_perm.to(DEV),
+                                  dy_perm=dy_perm, d_topk_w=d_w)
+    torch.cuda.synchronize()
+    sub = torch.randperm(T, generator=g)[:256].sort().values
+    rows = i64(row_of_slot).reshape(T, k)[sub.numpy()]           # [256, k] rows of Y_perm
+    yp_sub = f64(y_perm[torch.as_tensor(rows.reshape(-1))])        # those rows, slot by slot
+    local = np.arange(rows.size)
+    np.testing.assert_array_equal(f64(y[sub]), O.combine(yp_sub, f64(w[sub]), local, k, add=f64(add[sub])))
+    ref_p, ref_w = O.combine_bwd(f64(dy[sub]), f64(w[sub]), local, yp_sub, k)
+    np.testing.assert_array_equal(f64(dy_perm[torch.as_tensor(rows.reshape(-1)).to(DEV)]), ref_p)
+    np.testing.assert_array_equal(f64(d_w[sub.to(DEV)]), ref_w)
+
+
 @pytest.mark.parametrize("K,N", [(192, 320), (256, 256), (576, 64)])
 def test_grouped_gemm_dw_exact(K, N):
     _say("gemm_dw exact", K, N)
